@@ -1,0 +1,191 @@
+"""CPU oracle for tril(A A^T), the off-diagonal block A_i A_j^T and the mirror.
+
+TEST INFRASTRUCTURE ONLY: the tests, ``__graft_entry__.smoke()`` and the
+benchmark's CPU-baseline leg use it to check and time the GPU library.  The
+library never imports, links or calls anything here, and this package imports
+nothing from the library.
+
+The arithmetic lives in ``spsyrk_oracle.cpp`` (single-threaded Gustavson with
+an ordered-map accumulator, written from the definition C = A A^T of Sec. II-A,
+the lower-triangle restriction of Sec. III-A and the symmetric completion
+C = C_L + C_L^T - D of Eq. (spmv)).  This module only marshals numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spsyrk_oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+SEMIRINGS = {"f64": 0, "f32": 1, "count": 2, "jaccard": 3}
+_OUT_DTYPE = {0: np.float64, 1: np.float32, 2: np.int32, 3: np.float32}
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with g++ (host only)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _declare(lib):
+    i64, i32p, i64p, vp = ctypes.c_int64, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p
+    lib.oracle_syrk.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64p, i32p, vp,
+                                i64, i64, i64p, i32p, vp, i64p, i64, ctypes.POINTER(vp)]
+    lib.oracle_syrk.restype = ctypes.c_int
+    lib.oracle_mirror.argtypes = [i64, i64p, i32p, vp, ctypes.c_int, ctypes.POINTER(vp)]
+    lib.oracle_mirror.restype = ctypes.c_int
+    lib.oracle_check_canonical.argtypes = [i64, i64, i64p, i32p]
+    lib.oracle_check_canonical.restype = ctypes.c_int
+    lib.oracle_result_nrows.argtypes = [vp]
+    lib.oracle_result_nrows.restype = i64
+    lib.oracle_result_nnz.argtypes = [vp]
+    lib.oracle_result_nnz.restype = i64
+    lib.oracle_result_copy.argtypes = [vp, i64p, i32p, vp, ctypes.c_int, ctypes.c_int,
+                                       ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_uint32)]
+    lib.oracle_result_copy.restype = None
+    lib.oracle_result_free.argtypes = [vp]
+    lib.oracle_result_free.restype = None
+    return lib
+
+
+def _load(path: Optional[str] = None):
+    """The oracle library; ``path`` loads another build of the same source
+    (the tests plant mistakes in copies of it to check that the pins fail)."""
+    global _lib
+    if path is not None:
+        return _declare(ctypes.CDLL(path))
+    with _lock:
+        if _lib is None:
+            build()
+            _lib = _declare(ctypes.CDLL(_LIB))
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+@dataclass
+class Result:
+    nrows: int
+    ncols: int
+    row_ptr: np.ndarray
+    col_idx: np.ndarray
+    values: np.ndarray
+    sum_abs: Optional[np.ndarray] = None   # sum of |a_ik a_jk| per entry (fp tolerance scale)
+    count: Optional[np.ndarray] = None     # number of shared columns per entry
+
+    @property
+    def nnz(self) -> int:
+        return int(self.row_ptr[-1])
+
+
+def _p(a, t):
+    return a.ctypes.data_as(ctypes.POINTER(t)) if a is not None else None
+
+
+def _csr_args(A, semiring):
+    rp = np.ascontiguousarray(A.row_ptr, dtype=np.int64)
+    ci = np.ascontiguousarray(A.col_idx, dtype=np.int32)
+    if semiring == 0:
+        v = np.ascontiguousarray(A.values, dtype=np.float64)
+    elif semiring == 1:
+        v = np.ascontiguousarray(A.values, dtype=np.float32)
+    else:
+        v = None
+    return rp, ci, v
+
+
+def _take(lib, h, sr, nrows, ncols, with_aux=True) -> Result:
+    try:
+        nnz = lib.oracle_result_nnz(h)
+        rp = np.empty(nrows + 1, dtype=np.int64)
+        ci = np.empty(nnz, dtype=np.int32)
+        val = np.empty(nnz, dtype=_OUT_DTYPE[sr])
+        sa = np.empty(nnz, dtype=np.float64) if with_aux else None
+        cnt = np.empty(nnz, dtype=np.uint32) if with_aux else None
+        lib.oracle_result_copy(h, _p(rp, ctypes.c_int64), _p(ci, ctypes.c_int32),
+                               val.ctypes.data_as(ctypes.c_void_p), sr, 0,
+                               _p(sa, ctypes.c_double), _p(cnt, ctypes.c_uint32))
+    finally:
+        lib.oracle_result_free(h)
+    return Result(nrows, ncols, rp, ci, val, sa, cnt)
+
+
+def _run(mode, A, B, semiring, rows, lib=None):
+    lib = lib or _load()
+    sr = SEMIRINGS[semiring] if isinstance(semiring, str) else int(semiring)
+    rp, ci, v = _csr_args(A, sr)
+    if B is not None:
+        rpb, cib, vb = _csr_args(B, sr)
+        mb, nb = B.nrows, B.ncols
+    else:
+        rpb = cib = vb = None
+        mb = nb = 0
+    sel = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+    h = ctypes.c_void_p()
+    rc = lib.oracle_syrk(mode, sr, A.nrows, A.ncols, _p(rp, ctypes.c_int64), _p(ci, ctypes.c_int32),
+                         v.ctypes.data_as(ctypes.c_void_p) if v is not None else None,
+                         mb, nb, _p(rpb, ctypes.c_int64), _p(cib, ctypes.c_int32),
+                         vb.ctypes.data_as(ctypes.c_void_p) if vb is not None else None,
+                         _p(sel, ctypes.c_int64), 0 if sel is None else len(sel), ctypes.byref(h))
+    if rc != 0:
+        raise OracleError({1: "input not canonical", 2: "shape mismatch", 3: "out of memory"}.get(rc, str(rc)))
+    nrows = A.nrows if sel is None else len(sel)
+    return _take(lib, h, sr, nrows, A.nrows if B is None else B.nrows)
+
+
+def lower(A, semiring, rows=None, lib=None) -> Result:
+    """C_L = tril(A A^T) (diagonal included); ``rows`` restricts to a row subset."""
+    return _run(0, A, None, semiring, rows, lib)
+
+
+def offdiag(Ai, Aj, semiring, rows=None, lib=None) -> Result:
+    """Rectangular C = A_i A_j^T with no triangle prune."""
+    return _run(1, Ai, Aj, semiring, rows, lib)
+
+
+def mirror(m: int, row_ptr, col_idx, values, lib=None) -> Result:
+    """Full symmetric CSR from the stored lower part (values copied bit for bit)."""
+    lib = lib or _load()
+    rp = np.ascontiguousarray(row_ptr, dtype=np.int64)
+    ci = np.ascontiguousarray(col_idx, dtype=np.int32)
+    val = np.ascontiguousarray(values)
+    nb = val.dtype.itemsize
+    if nb not in (4, 8):
+        raise ValueError("values must be 4- or 8-byte")
+    h = ctypes.c_void_p()
+    rc = lib.oracle_mirror(m, _p(rp, ctypes.c_int64), _p(ci, ctypes.c_int32),
+                           val.ctypes.data_as(ctypes.c_void_p), nb, ctypes.byref(h))
+    if rc != 0:
+        raise OracleError("input not lower-triangular canonical CSR" if rc == 1 else str(rc))
+    try:
+        nnz = lib.oracle_result_nnz(h)
+        out_rp = np.empty(m + 1, dtype=np.int64)
+        out_ci = np.empty(nnz, dtype=np.int32)
+        out_v = np.empty(nnz, dtype=val.dtype)
+        lib.oracle_result_copy(h, _p(out_rp, ctypes.c_int64), _p(out_ci, ctypes.c_int32),
+                               out_v.ctypes.data_as(ctypes.c_void_p), 4, nb, None, None)
+    finally:
+        lib.oracle_result_free(h)
+    return Result(m, m, out_rp, out_ci, out_v)
+
+
+def is_canonical(A) -> bool:
+    lib = _load()
+    rp = np.ascontiguousarray(A.row_ptr, dtype=np.int64)
+    ci = np.ascontiguousarray(A.col_idx, dtype=np.int32)
+    return lib.oracle_check_canonical(A.nrows, A.ncols, _p(rp, ctypes.c_int64), _p(ci, ctypes.c_int32)) == 0
