@@ -1,0 +1,180 @@
+/*
+ * spsyrk.h -- local sparse SYRK on one AMD Instinct MI355X (gfx950).
+ *
+ * C-ABI of libspsyrk.so.  Every entry point computes on the GPU with
+ * hand-written HIP kernels; nothing falls back to the host.
+ *
+ * The operation (paper Sec. II-A): for a sparse A in R^{m x n}, C = A A^T is
+ * the m x m Gram matrix of the rows of A; it is symmetric, so one triangle
+ * holds all of its information.  Sec. III-A computes only the lower triangle
+ * of a diagonal block (C_ii = sum_s SYRK(A_is)) and Sec. III-B writes an
+ * off-diagonal block as C_ij = sum_s A_is A_js^T, with the transpose fused into
+ * the local kernel so A^T is never materialised.  Sec. V-F (Eq. (spmv))
+ * defines the stored lower part C_L *including the diagonal* and the full
+ * matrix C = C_L + C_L^T - D.
+ *
+ *   spsyrk_lower   : C_L = tril(A A^T)       (entries with column <= row)
+ *   spsyrk_offdiag : C   = A_i A_j^T         (full rectangular block, no prune)
+ *   spsyrk_mirror  : C   = C_L + C_L^T - D   (symmetric completion of C_L)
+ *
+ * Structure is the pattern product: C(i,j) is stored iff rows i and j share a
+ * stored column (stored zeros of A count as structure; computed zeros are
+ * kept).  Output rows keep the input row order and columns ascend strictly
+ * within each row, so the diagonal is the last entry of every non-empty row of
+ * C_L.
+ *
+ * Conventions common to all calls
+ * -------------------------------
+ * - Matrices are canonical CSR, 0-based: row_ptr is int64[nrows + 1] with
+ *   row_ptr[0] == 0, non-decreasing, row_ptr[nrows] == nnz; col_idx is
+ *   int32[nnz], strictly increasing within each row, in [0, ncols).
+ * - All pointers inside spsyrk_csr / spsyrk_csr_out are DEVICE pointers on the
+ *   current HIP device.  The struct pointers themselves are host pointers.
+ * - Inputs are owned by the caller and are only read.
+ * - Every output array and every temporary buffer is obtained through the
+ *   allocator passed in (or hipMallocAsync / hipFreeAsync on the stream when
+ *   the allocator is NULL).  On SPSYRK_OK the output arrays belong to the
+ *   caller, who releases them with the same allocator.  On any error every
+ *   allocation made by the call has been released and *C is zeroed.
+ * - Work is ordered on hip_stream (a hipStream_t; NULL means the default
+ *   stream).  A call blocks the host until it knows the output size; it
+ *   returns with the output's row_ptr and nnz final and the remaining work
+ *   enqueued on hip_stream (synchronise the stream before reading values).
+ * - Limits: nrows, ncols < 2^31 and nnz(A) < 2^31 (SPSYRK_ERR_SHAPE
+ *   otherwise).  Output nnz is int64.
+ * - Thread safety: calls on different streams may run concurrently; error
+ *   detail strings are thread-local.
+ */
+#ifndef SPSYRK_H
+#define SPSYRK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPSYRK_ABI_VERSION 1
+
+typedef enum spsyrk_status {
+    SPSYRK_OK = 0,
+    SPSYRK_ERR_INVALID_ARG = 1,   /* null pointer, negative size, Ai/Aj inner dimensions differ */
+    SPSYRK_ERR_NOT_CANONICAL = 2, /* row_ptr or col_idx violate the canonical CSR rules above, or
+                                     spsyrk_mirror got an entry above the diagonal */
+    SPSYRK_ERR_SHAPE = 3,         /* a dimension or nnz(A) is 2^31 or more */
+    SPSYRK_ERR_OOM = 4,           /* the allocator returned NULL */
+    SPSYRK_ERR_OVERFLOW = 5,      /* an internal count would overflow its integer type */
+    SPSYRK_ERR_HIP = 6            /* a HIP runtime call failed; see spsyrk_last_error_detail() */
+} spsyrk_status;
+
+/*
+ * Value semiring.  Products and sums follow the usual (+, *) except:
+ *   F32: inputs are float; products are formed and summed in double and
+ *        rounded to float once per output entry.
+ *   COUNT_I32: values are ignored (may be NULL); C(i,j) = |S(i) and S(j)|, the
+ *        number of shared stored columns (the overlap count used for
+ *        k-mer overlap detection, Sec. I), as int32.
+ *   COUNT_I32_JACCARD_F32: as COUNT, then J(i,j) = c / (|S(i)| + |S(j)| - c)
+ *        as one correctly rounded float division (Jaccard similarity, Sec. I);
+ *        output values are float.  The diagonal of C_L is exactly 1.
+ * Output value types: F64 -> double, F32 -> float, COUNT_I32 -> int32,
+ * COUNT_I32_JACCARD_F32 -> float.
+ */
+typedef enum spsyrk_semiring {
+    SPSYRK_PLUS_TIMES_F64 = 0,
+    SPSYRK_PLUS_TIMES_F32 = 1,
+    SPSYRK_COUNT_I32 = 2,
+    SPSYRK_COUNT_I32_JACCARD_F32 = 3
+} spsyrk_semiring;
+
+/* Input CSR (device arrays, read only). */
+typedef struct spsyrk_csr {
+    int64_t nrows;
+    int64_t ncols;
+    int64_t nnz;
+    const int64_t* row_ptr; /* [nrows + 1] */
+    const int32_t* col_idx; /* [nnz] */
+    const void* values;     /* [nnz] of double (F64) or float (F32); may be NULL for COUNT* */
+} spsyrk_csr;
+
+/* Output CSR (device arrays allocated by the call through the allocator). */
+typedef struct spsyrk_csr_out {
+    int64_t nrows;
+    int64_t ncols;
+    int64_t nnz;            /* entries in the result */
+    int64_t capacity;       /* entries allocated in col_idx / values (>= nnz) */
+    int64_t* row_ptr;       /* [nrows + 1] */
+    int32_t* col_idx;       /* [capacity] */
+    void* values;           /* [capacity] of the semiring's output type */
+} spsyrk_csr_out;
+
+/* Device-memory allocator.  alloc returns a device pointer aligned to at least
+ * 256 bytes or NULL; free releases it (stream-ordered use on hip_stream is
+ * assumed: memory freed by the call may be reused by later work on that
+ * stream). */
+typedef struct spsyrk_allocator {
+    void* (*alloc)(void* ctx, size_t bytes);
+    void (*free)(void* ctx, void* p);
+    void* ctx;
+} spsyrk_allocator;
+
+/*
+ * C_L = tril(A A^T), lower triangle with the diagonal (Sec. III-A, Eq. (spmv)).
+ * A: m x n.  C: m x m, C->nrows = C->ncols = m.
+ * Errors: INVALID_ARG (A, C null; A->values null for PLUS_TIMES), SHAPE,
+ * NOT_CANONICAL, OOM, OVERFLOW, HIP.
+ */
+spsyrk_status spsyrk_lower(const spsyrk_csr* A, spsyrk_semiring sr, const spsyrk_allocator* al,
+                           void* hip_stream, spsyrk_csr_out* C);
+
+/*
+ * C = A_i A_j^T, the full rectangular off-diagonal block C_ij of Sec. III-B with
+ * the transpose fused into the kernel (A_j is read in CSR; no A_j^T is formed
+ * by the caller).  A_i: m_i x n, A_j: m_j x n.  C: m_i x m_j.  For the Jaccard
+ * semiring |S(j)| is the row length in A_j.
+ * Errors: as spsyrk_lower, plus INVALID_ARG if A_i->ncols != A_j->ncols.
+ */
+spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_semiring sr,
+                             const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C);
+
+/*
+ * C = C_L + C_L^T - D (Eq. (spmv)): the full symmetric matrix from a stored
+ * lower part (for example the output of spsyrk_lower).  Row i of the result is
+ * row i of C_L followed by the entries (r, i) of the strict lower part with
+ * r > i in ascending r.  Values (of the semiring's OUTPUT type; ignored when
+ * NULL) are copied bit for bit, so C(i,j) and C(j,i) are bitwise equal.
+ * C_lower: m x m.  C_full: m x m, nnz = 2 nnz(C_L) - (number of diagonal entries).
+ * Errors: INVALID_ARG (non-square), NOT_CANONICAL (including any entry with
+ * column > row), SHAPE, OOM, OVERFLOW, HIP.
+ */
+spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const spsyrk_allocator* al,
+                            void* hip_stream, spsyrk_csr_out* C_full);
+
+/* Static description of a status code. */
+const char* spsyrk_status_string(spsyrk_status s);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char* spsyrk_last_error_detail(void);
+
+/* Counters from the last successful call on the calling thread. */
+typedef struct spsyrk_stats {
+    int64_t nnz_out;          /* entries in the result */
+    int64_t csc_entries;      /* entries kept in the column index built from the right operand */
+    int64_t heavy_rows;       /* rows routed to the dense-tile accumulator */
+    int64_t light_rows;       /* rows handled by the batched ordered-bucket accumulator */
+    int64_t products;         /* multiply-adds formed off the diagonal (lower) or in total (offdiag) */
+    int32_t group_shift;      /* log2 of columns per directory group */
+    int32_t row_bits;         /* bits of the row id inside a packed column key */
+} spsyrk_stats;
+
+spsyrk_status spsyrk_last_stats(spsyrk_stats* out);
+
+/* ABI version the library was built with (SPSYRK_ABI_VERSION). */
+int spsyrk_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPSYRK_H */

@@ -1,0 +1,244 @@
+"""Local sparse SYRK on one MI355X: tril(A A^T), A_i A_j^T and the mirror.
+
+Thin binding over ``libspsyrk.so`` (C-ABI in ``include/spsyrk.h``).  This module
+only marshals arguments: device memory and streams come from PyTorch, every
+step of the computation runs in the library's HIP kernels, and a missing or
+unloadable library raises instead of falling back to anything else.
+
+    import torch, paper_2608_09713_amd as sp
+    A = sp.DeviceCSR.from_host(csr, device="cuda:0")
+    C = sp.lower(A, "jaccard")          # tril(A A^T), Jaccard values
+    F = sp.mirror(C, "jaccard")         # full symmetric matrix
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libspsyrk.so")
+
+SEMIRINGS = {"f64": 0, "f32": 1, "count": 2, "jaccard": 3}
+# dtype of A's values each semiring reads, and of the output values
+_IN_DTYPE = {0: "float64", 1: "float32", 2: None, 3: None}
+_OUT_DTYPE = {0: "float64", 1: "float32", 2: "int32", 3: "float32"}
+
+STATUS = {0: "ok", 1: "invalid argument", 2: "not canonical", 3: "shape", 4: "out of memory",
+          5: "overflow", 6: "hip error"}
+
+
+class SpsyrkError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"spsyrk: {STATUS.get(status, status)}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class _Csr(ctypes.Structure):
+    _fields_ = [("nrows", ctypes.c_int64), ("ncols", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p), ("values", ctypes.c_void_p)]
+
+
+class _CsrOut(ctypes.Structure):
+    _fields_ = [("nrows", ctypes.c_int64), ("ncols", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("capacity", ctypes.c_int64), ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p),
+                ("values", ctypes.c_void_p)]
+
+
+_ALLOC = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t)
+_FREE = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class _Allocator(ctypes.Structure):
+    _fields_ = [("alloc", _ALLOC), ("free", _FREE), ("ctx", ctypes.c_void_p)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("nnz_out", ctypes.c_int64), ("csc_entries", ctypes.c_int64), ("heavy_rows", ctypes.c_int64),
+                ("light_rows", ctypes.c_int64), ("products", ctypes.c_int64), ("group_shift", ctypes.c_int32),
+                ("row_bits", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+_lib = None
+_lib_lock = threading.Lock()
+
+
+def library():
+    """The loaded C library; raises if it has not been built."""
+    global _lib
+    with _lib_lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2608_09713_amd.build` "
+                                  "(or __graft_entry__.build()) first")
+            lib = ctypes.CDLL(LIB_PATH)
+            for name in ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror"):
+                getattr(lib, name).restype = ctypes.c_int
+            lib.spsyrk_lower.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
+                                         ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_offdiag.argtypes = [ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), ctypes.c_int,
+                                           ctypes.POINTER(_Allocator), ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_mirror.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
+                                          ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_status_string.argtypes = [ctypes.c_int]
+            lib.spsyrk_status_string.restype = ctypes.c_char_p
+            lib.spsyrk_last_error_detail.argtypes = []
+            lib.spsyrk_last_error_detail.restype = ctypes.c_char_p
+            lib.spsyrk_last_stats.argtypes = [ctypes.POINTER(Stats)]
+            lib.spsyrk_last_stats.restype = ctypes.c_int
+            lib.spsyrk_abi_version.restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror", "spsyrk_status_string",
+           "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version")
+
+
+@dataclass
+class DeviceCSR:
+    """CSR whose arrays are torch tensors on one GPU."""
+    nrows: int
+    ncols: int
+    row_ptr: "object"            # torch.int64 [nrows + 1]
+    col_idx: "object"            # torch.int32 [>= nnz]
+    values: "object" = None      # torch tensor [>= nnz] or None
+    nnz: Optional[int] = None
+
+    def __post_init__(self):
+        if self.nnz is None:
+            self.nnz = int(self.row_ptr[-1].item()) if self.nrows >= 0 and self.row_ptr.numel() else 0
+
+    @staticmethod
+    def from_host(A, device="cuda:0", value_dtype=None) -> "DeviceCSR":
+        """Upload a host CSR (any object with nrows, ncols, row_ptr, col_idx, values)."""
+        import torch
+        rp = torch.from_numpy(np.ascontiguousarray(A.row_ptr, dtype=np.int64)).to(device)
+        ci = torch.from_numpy(np.ascontiguousarray(A.col_idx, dtype=np.int32)).to(device)
+        v = None
+        if A.values is not None:
+            vals = np.ascontiguousarray(A.values)
+            if value_dtype is not None:
+                vals = vals.astype(value_dtype)
+            v = torch.from_numpy(vals).to(device)
+        return DeviceCSR(A.nrows, A.ncols, rp, ci, v, int(A.row_ptr[-1]) if len(A.row_ptr) else 0)
+
+    def to_host(self):
+        """(row_ptr, col_idx, values) as numpy arrays of exactly nnz entries."""
+        rp = self.row_ptr.cpu().numpy()
+        ci = self.col_idx[: self.nnz].cpu().numpy()
+        v = self.values[: self.nnz].cpu().numpy() if self.values is not None else None
+        return rp, ci, v
+
+
+class _TorchArena:
+    """Device allocations for one call, backed by torch's caching allocator on
+    the call's stream.  Pointers handed to the library map to their tensors."""
+
+    def __init__(self, device):
+        import torch
+        self.torch = torch
+        self.device = device
+        self.live = {}
+        self._alloc = _ALLOC(self._do_alloc)
+        self._free = _FREE(self._do_free)
+        self.struct = _Allocator(self._alloc, self._free, None)
+
+    def _do_alloc(self, ctx, nbytes):
+        try:
+            t = self.torch.empty(int(nbytes), dtype=self.torch.uint8, device=self.device)
+        except Exception:  # out of memory: report NULL, the library returns SPSYRK_ERR_OOM
+            return None
+        p = t.data_ptr()
+        self.live[p] = t
+        return p
+
+    def _do_free(self, ctx, p):
+        self.live.pop(p, None)
+
+    def take(self, p, dtype, count):
+        if not p:
+            return None
+        t = self.live.pop(p)
+        return t.view(dtype)[:count] if count > 0 else t.view(dtype)[:0]
+
+
+def _csr_struct(A: DeviceCSR, sr: int, need_values: bool):
+    import torch
+    if A.row_ptr.dtype != torch.int64 or A.col_idx.dtype != torch.int32:
+        raise TypeError("row_ptr must be int64 and col_idx int32")
+    for t in (A.row_ptr, A.col_idx):
+        if not t.is_cuda or not t.is_contiguous():
+            raise TypeError("CSR arrays must be contiguous device tensors")
+    vp = None
+    if need_values and _IN_DTYPE[sr] is not None:
+        if A.values is None:
+            raise TypeError("values are required for plus-times semirings")
+        want = getattr(torch, _IN_DTYPE[sr])
+        if A.values.dtype != want or not A.values.is_contiguous():
+            raise TypeError(f"values must be a contiguous {want} tensor")
+        vp = A.values.data_ptr()
+    elif not need_values and A.values is not None:
+        vp = A.values.data_ptr()
+    return _Csr(A.nrows, A.ncols, A.nnz, A.row_ptr.data_ptr(), A.col_idx.data_ptr() if A.col_idx.numel() else 0, vp)
+
+
+def _sr(semiring) -> int:
+    return SEMIRINGS[semiring] if isinstance(semiring, str) else int(semiring)
+
+
+def _call(fn_name, args, sr, device, out_has_values=True):
+    import torch
+    lib = library()
+    arena = _TorchArena(device)
+    out = _CsrOut()
+    stream = torch.cuda.current_stream(device).cuda_stream
+    rc = getattr(lib, fn_name)(*args(arena), ctypes.c_void_p(stream), ctypes.byref(out))
+    if rc != 0:
+        raise SpsyrkError(rc, lib.spsyrk_last_error_detail().decode())
+    odt = getattr(torch, _OUT_DTYPE[sr])
+    rp = arena.take(out.row_ptr, torch.int64, out.nrows + 1)
+    ci = arena.take(out.col_idx, torch.int32, out.capacity)
+    v = arena.take(out.values, odt, out.capacity) if out.values else None
+    if arena.live:
+        raise RuntimeError("library left allocations unreleased")
+    return DeviceCSR(out.nrows, out.ncols, rp, ci, v, out.nnz)
+
+
+def lower(A: DeviceCSR, semiring="f64") -> DeviceCSR:
+    """C_L = tril(A A^T) with the diagonal (spsyrk_lower)."""
+    sr = _sr(semiring)
+    a = _csr_struct(A, sr, True)
+    return _call("spsyrk_lower", lambda ar: (ctypes.byref(a), sr, ctypes.byref(ar.struct)), sr, A.row_ptr.device)
+
+
+def offdiag(Ai: DeviceCSR, Aj: DeviceCSR, semiring="f64") -> DeviceCSR:
+    """C = A_i A_j^T, full rectangular block (spsyrk_offdiag)."""
+    sr = _sr(semiring)
+    a = _csr_struct(Ai, sr, True)
+    b = _csr_struct(Aj, sr, True)
+    return _call("spsyrk_offdiag", lambda ar: (ctypes.byref(a), ctypes.byref(b), sr, ctypes.byref(ar.struct)),
+                 sr, Ai.row_ptr.device)
+
+
+def mirror(C_lower: DeviceCSR, semiring="f64") -> DeviceCSR:
+    """C = C_L + C_L^T - D from a stored lower part (spsyrk_mirror)."""
+    sr = _sr(semiring)
+    a = _csr_struct(C_lower, sr, False)
+    return _call("spsyrk_mirror", lambda ar: (ctypes.byref(a), sr, ctypes.byref(ar.struct)), sr,
+                 C_lower.row_ptr.device)
+
+
+def stats() -> dict:
+    """Counters of the last successful call on this thread."""
+    s = Stats()
+    library().spsyrk_last_stats(ctypes.byref(s))
+    return s.as_dict()

@@ -1,0 +1,595 @@
+// C-ABI entry points: argument checks, device-side validation, workspace and
+// output allocation through the caller's allocator, and the kernel sequence.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "internal.h"
+#include "spsyrk.h"
+
+using namespace spsyrk;
+
+namespace {
+
+thread_local std::string g_detail;
+thread_local spsyrk_stats g_stats;
+thread_local bool g_stats_valid = false;
+
+constexpr int64_t kLimit = int64_t(1) << 31;
+
+void set_detail(const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_detail = buf;
+}
+
+struct Fail {
+    spsyrk_status st;
+};
+
+#define HIPCHK(call)                                                                          \
+    do {                                                                                      \
+        hipError_t e_ = (call);                                                               \
+        if (e_ != hipSuccess) {                                                               \
+            set_detail("%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, __LINE__); \
+            throw Fail{SPSYRK_ERR_HIP};                                                       \
+        }                                                                                     \
+    } while (0)
+
+// Allocations of one call.  Workspace is released at the end of the call
+// (stream-ordered); outputs are released only if the call fails.
+class Arena {
+   public:
+    Arena(const spsyrk_allocator* al, hipStream_t s) : al_(al), s_(s) {}
+    bool touched() const { return touched_; }
+    ~Arena() { release_all(); }
+
+    void* get(size_t bytes, bool output = false) {
+        touched_ = true;
+        if (bytes == 0) bytes = 256;
+        bytes = (bytes + 255) & ~size_t(255);
+        void* p = nullptr;
+        if (al_ && al_->alloc) {
+            p = al_->alloc(al_->ctx, bytes);
+        } else {
+            hipError_t e = hipMallocAsync(&p, bytes, s_);
+            if (e != hipSuccess) p = nullptr;
+        }
+        if (!p) {
+            set_detail("allocation of %zu bytes failed", bytes);
+            throw Fail{SPSYRK_ERR_OOM};
+        }
+        (output ? outputs_ : work_).push_back(p);
+        return p;
+    }
+    template <typename T>
+    T* get_t(int64_t count, bool output = false) {
+        return static_cast<T*>(get(size_t(count) * sizeof(T), output));
+    }
+    void release(void* p) {
+        for (auto& q : work_)
+            if (q == p) {
+                free_one(q);
+                q = nullptr;
+            }
+    }
+    void keep_outputs() { outputs_.clear(); }
+    void release_all() {
+        for (void* p : work_)
+            if (p) free_one(p);
+        for (void* p : outputs_)
+            if (p) free_one(p);
+        work_.clear();
+        outputs_.clear();
+    }
+
+   private:
+    void free_one(void* p) {
+        if (al_ && al_->free)
+            al_->free(al_->ctx, p);
+        else if (!al_)
+            (void)hipFreeAsync(p, s_);
+    }
+    const spsyrk_allocator* al_;
+    hipStream_t s_;
+    std::vector<void*> work_, outputs_;
+    bool touched_ = false;
+};
+
+// small block of device scalars read back at the synchronisation points
+struct Ctl {
+    uint32_t err;
+    int32_t heavy_count;
+    unsigned long long products;
+    int64_t total;
+    int64_t nkept;
+    int64_t total2;
+    int32_t queue;
+    int32_t pad[5];
+};
+
+struct HostCtl {
+    Ctl* h = nullptr;
+    HostCtl() {
+        if (hipHostMalloc(reinterpret_cast<void**>(&h), sizeof(Ctl), hipHostMallocDefault) != hipSuccess) h = nullptr;
+    }
+    ~HostCtl() {
+        if (h) (void)hipHostFree(h);
+    }
+};
+
+Ctl read_ctl(const Ctl* d, hipStream_t s) {
+    thread_local HostCtl pin;
+    if (!pin.h) {
+        set_detail("pinned host buffer unavailable");
+        throw Fail{SPSYRK_ERR_HIP};
+    }
+    HIPCHK(hipMemcpyAsync(pin.h, d, sizeof(Ctl), hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+    return *pin.h;
+}
+
+void check_launch() {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        set_detail("kernel launch failed: %s", hipGetErrorString(e));
+        throw Fail{SPSYRK_ERR_HIP};
+    }
+}
+
+void check_input(const spsyrk_csr* A, int sr, bool need_values, const char* name) {
+    if (!A) {
+        set_detail("%s is null", name);
+        throw Fail{SPSYRK_ERR_INVALID_ARG};
+    }
+    if (A->nrows < 0 || A->ncols < 0 || A->nnz < 0) {
+        set_detail("%s has a negative size", name);
+        throw Fail{SPSYRK_ERR_INVALID_ARG};
+    }
+    if (A->nrows >= kLimit || A->ncols >= kLimit || A->nnz >= kLimit) {
+        set_detail("%s: nrows, ncols and nnz must be below 2^31", name);
+        throw Fail{SPSYRK_ERR_SHAPE};
+    }
+    if (!A->row_ptr || (A->nnz > 0 && !A->col_idx)) {
+        set_detail("%s: null row_ptr or col_idx", name);
+        throw Fail{SPSYRK_ERR_INVALID_ARG};
+    }
+    if (need_values && A->nnz > 0 && !A->values && (sr == kF64 || sr == kF32)) {
+        set_detail("%s: values are required for plus-times semirings", name);
+        throw Fail{SPSYRK_ERR_INVALID_ARG};
+    }
+}
+
+void check_semiring(int sr) {
+    if (sr < 0 || sr > 3) {
+        set_detail("unknown semiring %d", sr);
+        throw Fail{SPSYRK_ERR_INVALID_ARG};
+    }
+}
+
+DevCsr dev(const spsyrk_csr* A) {
+    DevCsr d;
+    d.m = A->nrows;
+    d.n = A->ncols;
+    d.nnz = A->nnz;
+    d.rp = A->row_ptr;
+    d.ci = A->col_idx;
+    d.v = A->values;
+    return d;
+}
+
+void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name) {
+    uint32_t* bits = static_cast<uint32_t*>(ar.get(validate_tmp_bytes(A)));
+    validate_csr(A, upper_forbidden, bits, &ctl->err, s);
+    check_launch();
+    Ctl h = read_ctl(ctl, s);
+    if (h.err) {
+        set_detail("%s is not canonical CSR (flags 0x%x:%s%s%s%s)", name, h.err, (h.err & kErrRowPtr) ? " row_ptr" : "",
+                   (h.err & kErrColRange) ? " column-range" : "", (h.err & kErrColOrder) ? " column-order" : "",
+                   (h.err & kErrUpper) ? " above-diagonal" : "");
+        throw Fail{SPSYRK_ERR_NOT_CANONICAL};
+    }
+    ar.release(bits);
+}
+
+// Build the column index of B (sorted by column, packed keys, directory).
+ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s) {
+    ColIndex cx;
+    cx.n = B.n;
+    cx.m = B.m;
+    cx.rowbits = bit_width_u64(B.m > 1 ? uint64_t(B.m - 1) : 1);
+    const int64_t N = B.nnz;
+    // about 16 entries per directory group, limited by the key width
+    int gs = 0;
+    if (B.n > 0) {
+        const double target = 16.0 * double(B.n) / double(N > 0 ? N : 1);
+        while (gs < 31 && double(int64_t(1) << (gs + 1)) <= target) ++gs;
+    }
+    const int maxgs = 32 - cx.rowbits;
+    if (gs > maxgs) gs = maxgs;
+    const int nbits_n = bit_width_u64(B.n > 1 ? uint64_t(B.n - 1) : 0);
+    if (gs > nbits_n) gs = nbits_n;
+    cx.gs = gs;
+    cx.ngroups = B.n > 0 ? ((B.n + (int64_t(1) << gs) - 1) >> gs) : 0;
+    const int vb = (sr == kF64) ? 8 : (sr == kF32 ? 4 : 0);
+    const int vb_out = csc_value_bytes(sr);
+
+    cx.gptr = ar.get_t<uint32_t>(cx.ngroups + 1);
+    cx.key = ar.get_t<uint32_t>(N > 0 ? N : 1);
+    cx.val = vb_out ? ar.get(size_t(N > 0 ? N : 1) * vb_out) : nullptr;
+
+    uint32_t *ka = nullptr, *kb = nullptr, *ra = nullptr, *rb = nullptr;
+    void *va = nullptr, *vbuf = nullptr;
+    if (N > 0) {
+        ka = ar.get_t<uint32_t>(N);
+        kb = ar.get_t<uint32_t>(N);
+        ra = ar.get_t<uint32_t>(N);
+        rb = ar.get_t<uint32_t>(N);
+        if (vb) {
+            va = ar.get(size_t(N) * vb);
+            vbuf = ar.get(size_t(N) * vb);
+        }
+        HIPCHK(hipMemcpyAsync(ka, B.ci, size_t(N) * 4, hipMemcpyDeviceToDevice, s));
+        if (vb) HIPCHK(hipMemcpyAsync(va, B.v, size_t(N) * vb, hipMemcpyDeviceToDevice, s));
+        entry_rows(B, ra, s);
+        check_launch();
+        void* tmp = ar.get(radix_tmp_bytes(N));
+        const int which = radix_sort(ka, kb, ra, rb, va, vbuf, vb, N, nbits_n, tmp, s);
+        check_launch();
+        ar.release(tmp);
+        uint32_t* sk = which ? kb : ka;
+        uint32_t* sr_ = which ? rb : ra;
+        void* sv = which ? vbuf : va;
+        void* ctmp = ar.get(colindex_tmp_bytes(N));
+        build_colindex(sk, sr_, sv, N, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, s);
+        check_launch();
+        ar.release(ctmp);
+        ar.release(ka);
+        ar.release(kb);
+        ar.release(ra);
+        ar.release(rb);
+        if (va) ar.release(va);
+        if (vbuf) ar.release(vbuf);
+    } else {
+        void* ctmp = ar.get(colindex_tmp_bytes(0));
+        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, s);
+        check_launch();
+        ar.release(ctmp);
+    }
+    return cx;
+}
+
+void zero_ctl(Ctl* ctl, hipStream_t s) { HIPCHK(hipMemsetAsync(ctl, 0, sizeof(Ctl), s)); }
+
+spsyrk_status finish(spsyrk_status st) {
+    if (st == SPSYRK_OK) g_detail.clear();
+    return st;
+}
+
+// C = tril(L R^T) (lower) or L R^T (offdiag), with R = L for lower.
+void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
+    Ctl* ctl = ar.get_t<Ctl>(1);
+    zero_ctl(ctl, s);
+    validate(L, false, ar, ctl, s, lower ? "A" : "Ai");
+    if (!lower) validate(R, false, ar, ctl, s, "Aj");
+
+    const int64_t m = L.m;
+    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
+    spsyrk_stats st{};
+    if (m == 0 || L.nnz == 0 || R.nnz == 0) {
+        HIPCHK(hipMemsetAsync(c_rp, 0, size_t(m + 1) * sizeof(int64_t), s));
+        C->nrows = m;
+        C->ncols = R.m;
+        C->row_ptr = c_rp;
+        C->col_idx = ar.get_t<int32_t>(1, true);
+        C->values = ar.get(4 * 2, true);
+        C->nnz = 0;
+        C->capacity = 0;
+        HIPCHK(hipStreamSynchronize(s));
+        g_stats = st;
+        g_stats_valid = true;
+        return;
+    }
+
+    ColIndex cx = build_index(R, lower, sr, ar, ctl, s);
+
+    // symbolic
+    int32_t* heavy_rows = ar.get_t<int32_t>(m);
+    HIPCHK(hipMemsetAsync(c_rp + m, 0, sizeof(int64_t), s));
+    LightArgs la;
+    la.m = m;
+    la.rp = L.rp;
+    la.ci = L.ci;
+    la.val = L.v;
+    la.cx = cx;
+    la.m_right = R.m;
+    la.lower = lower;
+    la.sr = sr;
+    la.row_nnz = c_rp;
+    la.heavy_rows = heavy_rows;
+    la.heavy_count = &ctl->heavy_count;
+    la.products = &ctl->products;
+    light_symbolic(la, s);
+    check_launch();
+    Ctl h = read_ctl(ctl, s);
+    const int64_t nheavy = h.heavy_count;
+
+    HeavyArgs ha;
+    ha.m = m;
+    ha.rp = L.rp;
+    ha.ci = L.ci;
+    ha.val = L.v;
+    ha.cx = cx;
+    ha.m_right = R.m;
+    ha.rp_right = R.rp;
+    ha.lower = lower;
+    ha.sr = sr;
+    ha.heavy_rows = heavy_rows;
+    ha.heavy_count = &ctl->heavy_count;
+    ha.heavy_max = nheavy;
+    ha.products = &ctl->products;
+    ha.row_nnz = c_rp;
+    if (nheavy > 0) {
+        ha.run_lo = ar.get_t<uint32_t>(L.nnz);
+        ha.run_hi = ar.get_t<uint32_t>(L.nnz);
+        ha.cursor = ar.get_t<uint32_t>(L.nnz);
+        heavy_symbolic(ha, &ctl->queue, s);
+        check_launch();
+    }
+    void* stmp = ar.get(scan_tmp_bytes(m + 1));
+    scan_i64(c_rp, c_rp, m + 1, &ctl->total, stmp, s);
+    check_launch();
+    h = read_ctl(ctl, s);
+    ar.release(stmp);
+    const int64_t total = h.total;
+    if (total >= (int64_t(1) << 62)) {
+        set_detail("output size overflow");
+        throw Fail{SPSYRK_ERR_OVERFLOW};
+    }
+    int32_t* c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
+    void* c_val = ar.get(size_t(total > 0 ? total : 1) * out_value_bytes(sr), true);
+
+    la.c_rp = c_rp;
+    la.c_ci = c_ci;
+    la.c_val = c_val;
+    light_numeric(la, s);
+    check_launch();
+    if (nheavy > 0) {
+        ha.c_rp = c_rp;
+        ha.c_ci = c_ci;
+        ha.c_val = c_val;
+        heavy_numeric(ha, &ctl->queue, s);
+        check_launch();
+    }
+    C->nrows = m;
+    C->ncols = R.m;
+    C->nnz = total;
+    C->capacity = total;
+    C->row_ptr = c_rp;
+    C->col_idx = c_ci;
+    C->values = c_val;
+
+    st.nnz_out = total;
+    st.csc_entries = h.nkept;
+    st.heavy_rows = nheavy;
+    st.light_rows = m - nheavy;
+    st.products = int64_t(h.products);
+    st.group_shift = cx.gs;
+    st.row_bits = cx.rowbits;
+    g_stats = st;
+    g_stats_valid = true;
+}
+
+void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
+    Ctl* ctl = ar.get_t<Ctl>(1);
+    zero_ctl(ctl, s);
+    validate(L, true, ar, ctl, s, "C_lower");
+    const int64_t m = L.m;
+    const int vb = L.v ? out_value_bytes(sr) : 0;
+    MirrorArgs ma;
+    ma.m = m;
+    ma.nnz = L.nnz;
+    ma.rp = L.rp;
+    ma.ci = L.ci;
+    ma.val = L.v;
+    ma.vbytes = vb;
+
+    int64_t* f_rp = ar.get_t<int64_t>(m + 1, true);
+    int64_t* full_len = f_rp;  // lengths first, scanned in place
+    int64_t* colcnt = ar.get_t<int64_t>(m + 1);
+    HIPCHK(hipMemsetAsync(full_len, 0, size_t(m + 1) * sizeof(int64_t), s));
+    HIPCHK(hipMemsetAsync(colcnt, 0, size_t(m + 1) * sizeof(int64_t), s));
+    mirror_counts(ma, full_len, s);
+    mirror_col_counts(ma, full_len, colcnt, s);
+    check_launch();
+    void* stmp = ar.get(scan_tmp_bytes(m + 1));
+    scan_i64(colcnt, colcnt, m + 1, &ctl->total2, stmp, s);  // colcnt -> cstart
+    scan_i64(full_len, f_rp, m + 1, &ctl->total, stmp, s);
+    check_launch();
+    Ctl h = read_ctl(ctl, s);
+    const int64_t total = h.total, nstrict = h.total2;
+    int32_t* f_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
+    void* f_val = vb ? ar.get(size_t(total > 0 ? total : 1) * vb, true) : nullptr;
+    mirror_copy_lower(ma, f_rp, f_ci, f_val, s);
+    check_launch();
+
+    if (nstrict > 0) {
+        // column slabs of at most kSlab strict-lower entries (the whole range
+        // when it fits; a slab always holds at least one column)
+        const int64_t kSlab = int64_t(1) << 30;
+        std::vector<int64_t> bounds{0};
+        if (nstrict <= kSlab) {
+            bounds.push_back(m);
+        } else {
+            std::vector<int64_t> cst(size_t(m) + 1);
+            HIPCHK(hipMemcpyAsync(cst.data(), colcnt, size_t(m + 1) * sizeof(int64_t), hipMemcpyDeviceToHost, s));
+            HIPCHK(hipStreamSynchronize(s));
+            int64_t c0 = 0;
+            while (c0 < m) {
+                int64_t c1 = c0 + 1;
+                int64_t lo = c0 + 1, hi = m;  // largest c1 with cst[c1] - cst[c0] <= kSlab
+                while (lo <= hi) {
+                    const int64_t mid = (lo + hi) / 2;
+                    if (cst[mid] - cst[c0] <= kSlab) {
+                        c1 = mid;
+                        lo = mid + 1;
+                    } else {
+                        hi = mid - 1;
+                    }
+                }
+                if (cst[c1] - cst[c0] > kSlab && c1 == c0 + 1 && cst[c1] - cst[c0] >= kLimit) {
+                    set_detail("a single column of the lower part holds 2^31 or more entries");
+                    throw Fail{SPSYRK_ERR_SHAPE};
+                }
+                bounds.push_back(c1);
+                c0 = c1;
+            }
+        }
+        int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
+        int64_t* row_lo = ar.get_t<int64_t>(m);
+        void* rtmp_scan = ar.get(scan_tmp_bytes(m + 1));
+        const int64_t cap = nstrict < kSlab ? nstrict : kSlab;
+        uint32_t* ka = ar.get_t<uint32_t>(cap);
+        uint32_t* kb = ar.get_t<uint32_t>(cap);
+        uint32_t* ra = ar.get_t<uint32_t>(cap);
+        uint32_t* rb = ar.get_t<uint32_t>(cap);
+        void* va = vb ? ar.get(size_t(cap) * vb) : nullptr;
+        void* vbb = vb ? ar.get(size_t(cap) * vb) : nullptr;
+        void* rtmp = ar.get(radix_tmp_bytes(cap));
+        for (size_t k = 0; k + 1 < bounds.size(); ++k) {
+            const int64_t c0 = bounds[k], c1 = bounds[k + 1];
+            HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
+            mirror_slab_counts(ma, c0, c1, row_cnt, row_lo, s);
+            scan_i64(row_cnt, row_cnt, m + 1, &ctl->total, rtmp_scan, s);
+            check_launch();
+            h = read_ctl(ctl, s);
+            const int64_t nrec = h.total;
+            if (nrec == 0) continue;
+            mirror_slab_extract(ma, c0, c1, row_cnt, row_lo, ka, ra, va, s);
+            const int nbits = bit_width_u64(c1 - c0 > 1 ? uint64_t(c1 - c0 - 1) : 0);
+            const int which = radix_sort(ka, kb, ra, rb, va, vbb, vb, nrec, nbits, rtmp, s);
+            mirror_slab_place(ma, c0, nrec, which ? kb : ka, which ? rb : ra, which ? vbb : va, colcnt, f_rp, f_ci,
+                              f_val, s);
+            check_launch();
+        }
+    }
+    HIPCHK(hipStreamSynchronize(s));
+    C->nrows = m;
+    C->ncols = m;
+    C->nnz = total;
+    C->capacity = total;
+    C->row_ptr = f_rp;
+    C->col_idx = f_ci;
+    C->values = f_val;
+    spsyrk_stats st{};
+    st.nnz_out = total;
+    g_stats = st;
+    g_stats_valid = true;
+}
+
+template <typename F>
+spsyrk_status guarded(spsyrk_csr_out* C, const spsyrk_allocator* al, void* stream, F body) {
+    g_stats_valid = false;
+    if (!C) {
+        set_detail("output struct is null");
+        return SPSYRK_ERR_INVALID_ARG;
+    }
+    std::memset(C, 0, sizeof(*C));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    Arena ar(al, s);
+    try {
+        body(ar, s);
+        ar.keep_outputs();
+    } catch (const Fail& f) {
+        ar.release_all();
+        std::memset(C, 0, sizeof(*C));
+        if (ar.touched()) (void)hipStreamSynchronize(s);
+        return f.st;
+    } catch (...) {
+        ar.release_all();
+        std::memset(C, 0, sizeof(*C));
+        set_detail("unexpected host exception");
+        return SPSYRK_ERR_HIP;
+    }
+    ar.release_all();
+    return finish(SPSYRK_OK);
+}
+
+}  // namespace
+
+extern "C" {
+
+spsyrk_status spsyrk_lower(const spsyrk_csr* A, spsyrk_semiring sr, const spsyrk_allocator* al, void* hip_stream,
+                           spsyrk_csr_out* C) {
+    return guarded(C, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        check_input(A, int(sr), true, "A");
+        const DevCsr d = dev(A);
+        syrk(d, d, true, int(sr), ar, s, C);
+    });
+}
+
+spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_semiring sr,
+                             const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C) {
+    return guarded(C, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        check_input(Ai, int(sr), true, "Ai");
+        check_input(Aj, int(sr), true, "Aj");
+        if (Ai->ncols != Aj->ncols) {
+            set_detail("Ai has %lld columns, Aj has %lld", (long long)Ai->ncols, (long long)Aj->ncols);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        syrk(dev(Ai), dev(Aj), false, int(sr), ar, s, C);
+    });
+}
+
+spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const spsyrk_allocator* al,
+                            void* hip_stream, spsyrk_csr_out* C_full) {
+    return guarded(C_full, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        check_input(C_lower, int(sr), false, "C_lower");
+        if (C_lower->nrows != C_lower->ncols) {
+            set_detail("C_lower must be square (%lld x %lld)", (long long)C_lower->nrows,
+                       (long long)C_lower->ncols);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        mirror(dev(C_lower), int(sr), ar, s, C_full);
+    });
+}
+
+const char* spsyrk_status_string(spsyrk_status s) {
+    switch (s) {
+        case SPSYRK_OK: return "ok";
+        case SPSYRK_ERR_INVALID_ARG: return "invalid argument";
+        case SPSYRK_ERR_NOT_CANONICAL: return "input is not canonical CSR";
+        case SPSYRK_ERR_SHAPE: return "shape out of range";
+        case SPSYRK_ERR_OOM: return "out of device memory";
+        case SPSYRK_ERR_OVERFLOW: return "count overflow";
+        case SPSYRK_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* spsyrk_last_error_detail(void) { return g_detail.c_str(); }
+
+spsyrk_status spsyrk_last_stats(spsyrk_stats* out) {
+    if (!out) return SPSYRK_ERR_INVALID_ARG;
+    if (!g_stats_valid) {
+        std::memset(out, 0, sizeof(*out));
+        return SPSYRK_ERR_INVALID_ARG;
+    }
+    *out = g_stats;
+    return SPSYRK_OK;
+}
+
+int spsyrk_abi_version(void) { return SPSYRK_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+// Device and host helpers shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace spsyrk {
+
+constexpr int kWave = 64;        // gfx950 wavefront width
+constexpr int kBlock = 256;      // threads per workgroup used by most kernels
+constexpr int kWavesPerBlock = kBlock / kWave;
+
+// error bits raised by validation kernels (OR-ed into one device word)
+enum ErrBits : uint32_t {
+    kErrRowPtr = 1u,        // row_ptr not monotone / wrong ends
+    kErrColRange = 2u,      // column id outside [0, ncols)
+    kErrColOrder = 4u,      // column ids not strictly increasing within a row
+    kErrUpper = 8u,         // entry above the diagonal (mirror input)
+};
+
+// number of bits needed to write x (0 -> 0)
+__host__ __device__ inline int bit_width_u64(uint64_t x) {
+    int b = 0;
+    while (x) {
+        ++b;
+        x >>= 1;
+    }
+    return b;
+}
+
+__device__ inline int lane_id() { return __lane_id(); }
+
+__device__ inline uint64_t lanemask_lt() { return (uint64_t(1) << lane_id()) - 1; }
+
+// inclusive scan across a wavefront (64 lanes)
+template <typename T>
+__device__ inline T wave_inclusive_scan(T v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        T u = __shfl_up(v, d, kWave);
+        if (lane_id() >= d) v += u;
+    }
+    return v;
+}
+
+template <typename T>
+__device__ inline T wave_reduce_sum(T v) {
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) v += __shfl_xor(v, d, kWave);
+    return v;
+}
+
+template <typename T>
+__device__ inline T wave_reduce_max(T v) {
+#pragma unroll
+    for (int d = kWave / 2; d > 0; d >>= 1) {
+        T u = __shfl_xor(v, d, kWave);
+        v = u > v ? u : v;
+    }
+    return v;
+}
+
+// Exclusive scan of a block of kBlock values, one per thread.  `warp_tot`
+// is LDS scratch of kWavesPerBlock entries.  Returns the exclusive prefix of
+// this thread and writes the block total to *total (all threads).
+template <typename T>
+__device__ inline T block_exclusive_scan(T v, T* warp_tot, T* total) {
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    T inc = wave_inclusive_scan(v);
+    if (lane == kWave - 1) warp_tot[w] = inc;
+    __syncthreads();
+    T off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kWavesPerBlock; ++i) {
+        T t = warp_tot[i];
+        if (i < w) off += t;
+        tot += t;
+    }
+    __syncthreads();
+    *total = tot;
+    return off + inc - v;
+}
+
+// Exclusive scan in place of an LDS array of length n (any n) by the whole
+// block; returns the total.  `warp_tot` is LDS scratch of kWavesPerBlock.
+template <typename T>
+__device__ inline T block_exclusive_scan_array(T* a, int n, T* warp_tot) {
+    const int per = (n + kBlock - 1) / kBlock;
+    const int lo = min(n, int(threadIdx.x) * per);
+    const int hi = min(n, lo + per);
+    T s = 0;
+    for (int i = lo; i < hi; ++i) s += a[i];
+    T tot;
+    T off = block_exclusive_scan(s, warp_tot, &tot);
+    for (int i = lo; i < hi; ++i) {
+        T x = a[i];
+        a[i] = off;
+        off += x;
+    }
+    __syncthreads();
+    return tot;
+}
+
+// first index in [lo, hi) with a[idx] > x (a non-decreasing), else hi
+template <typename T>
+__device__ inline int upper_bound_lds(const T* a, int lo, int hi, T x) {
+    while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (a[mid] <= x)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// first index in [lo, hi) with key[idx] >= x, for non-decreasing uint32 keys in global memory
+__device__ inline int64_t lower_bound_u32(const uint32_t* key, int64_t lo, int64_t hi, uint64_t x) {
+    while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        if (uint64_t(key[mid]) < x)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+}  // namespace spsyrk

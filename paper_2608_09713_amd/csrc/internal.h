@@ -1,0 +1,157 @@
+// Internal interfaces between the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace spsyrk {
+
+// semiring codes (same values as the public enum)
+enum Sr : int { kF64 = 0, kF32 = 1, kCount = 2, kJaccard = 3 };
+
+// bytes of the per-entry value carried by the column index of the right operand
+inline int csc_value_bytes(int sr) { return sr == kF64 ? 8 : (sr == kF32 ? 4 : (sr == kJaccard ? 4 : 0)); }
+// bytes of an output value
+inline int out_value_bytes(int sr) { return sr == kF64 ? 8 : 4; }
+
+struct DevCsr {
+    int64_t m = 0, n = 0, nnz = 0;
+    const int64_t* rp = nullptr;
+    const int32_t* ci = nullptr;
+    const void* v = nullptr;
+};
+
+// Column index of the right operand B (B = A for the lower triangle, B = A_j
+// off the diagonal): the entries of B grouped by column, rows ascending inside
+// a column, packed as key = (col mod 2^gs) << rowbits | row, plus a directory
+// of 2^gs-column groups: the entries of group g occupy [gptr[g], gptr[g+1]).
+// In lower mode the last (largest-row) entry of every column is left out: it
+// is never the partner j < i of another row.
+struct ColIndex {
+    int64_t n = 0;          // columns of B
+    int64_t m = 0;          // rows of B
+    int gs = 0;             // log2 columns per group
+    int rowbits = 1;        // bits of a row id inside a key
+    int64_t ngroups = 0;    // groups; gptr has ngroups + 1 entries
+    int64_t nkept = 0;      // entries kept (device-side value is authoritative until synced)
+    uint32_t* key = nullptr;
+    void* val = nullptr;    // double / float values of B, or int32 row lengths of B (Jaccard)
+    uint32_t* gptr = nullptr;
+};
+
+// ---- scan.hip
+// Exclusive scan out[i] = sum_{k<i} in[i]; out may alias in.  If total is not
+// null it receives the sum (device pointer).  tmp needs scan_tmp_bytes(n).
+size_t scan_tmp_bytes(int64_t n);
+void scan_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total, void* tmp, hipStream_t s);
+void scan_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp, hipStream_t s);
+
+// ---- validate.hip
+// ORs ErrBits into *err.  upper_forbidden: also flag entries with col > row.
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* row_start_bits, uint32_t* err,
+                  hipStream_t s);
+size_t validate_tmp_bytes(const DevCsr& A);
+void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
+// row id of every entry: rows[e] = i for rp[i] <= e < rp[i+1]
+void entry_rows(const DevCsr& A, uint32_t* rows, hipStream_t s);
+
+// ---- radix.hip
+// Stable LSD sort of (key, row, value) records by the low `nbits` of key.
+// Buffers *_a hold the input and the result is returned in the buffer
+// reported by the return value (0 -> *_a, 1 -> *_b).  vbytes in {0, 4, 8}.
+size_t radix_tmp_bytes(int64_t n);
+int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a,
+               void* val_b, int vbytes, int64_t n, int nbits, void* tmp, hipStream_t s);
+
+// ---- colindex.hip
+// From records sorted by column: keep flags, packing and directory.
+size_t colindex_tmp_bytes(int64_t n);
+void build_colindex(const uint32_t* scol, const uint32_t* srow, const void* sval, int64_t n_entries,
+                    bool drop_last, int vbytes_in, int sr, const int64_t* rp_b, ColIndex& ci,
+                    void* tmp, int64_t* d_nkept, hipStream_t s);
+
+// ---- light.hip
+struct LightArgs {
+    // left operand (rows of the output)
+    int64_t m = 0;
+    const int64_t* rp = nullptr;
+    const int32_t* ci = nullptr;
+    const void* val = nullptr;
+    // right operand's column index
+    ColIndex cx;
+    int64_t m_right = 0;          // output columns
+    bool lower = true;
+    int sr = kF64;
+    // symbolic outputs
+    int64_t* row_nnz = nullptr;   // [m]
+    uint8_t* heavy_flag = nullptr;  // [m]
+    int32_t* heavy_rows = nullptr;  // list of heavy rows
+    int32_t* heavy_count = nullptr; // device counter
+    unsigned long long* products = nullptr;  // device counter of products formed (light rows)
+    // numeric outputs
+    const int64_t* c_rp = nullptr;
+    int32_t* c_ci = nullptr;
+    void* c_val = nullptr;
+};
+void light_symbolic(const LightArgs& a, hipStream_t s);
+void light_numeric(const LightArgs& a, hipStream_t s);
+
+// ---- heavy.hip
+struct HeavyArgs {
+    int64_t m = 0;
+    const int64_t* rp = nullptr;
+    const int32_t* ci = nullptr;
+    const void* val = nullptr;
+    ColIndex cx;
+    int64_t m_right = 0;
+    const int64_t* rp_right = nullptr;  // row lengths of the right operand (Jaccard)
+    bool lower = true;
+    int sr = kF64;
+    const int32_t* heavy_rows = nullptr;
+    const int32_t* heavy_count = nullptr;
+    int64_t heavy_max = 0;              // upper bound of heavy rows (grid sizing)
+    // per-entry run bounds (sized nnz of the left operand), written by the symbolic pass
+    uint32_t* run_lo = nullptr;
+    uint32_t* run_hi = nullptr;
+    uint32_t* cursor = nullptr;
+    unsigned long long* products = nullptr;
+    int64_t* row_nnz = nullptr;
+    const int64_t* c_rp = nullptr;
+    int32_t* c_ci = nullptr;
+    void* c_val = nullptr;
+};
+// queue: one device int of scratch (work counter)
+void heavy_symbolic(const HeavyArgs& a, int* queue, hipStream_t s);
+void heavy_numeric(const HeavyArgs& a, int* queue, hipStream_t s);
+
+// ---- mirror.hip
+struct MirrorArgs {
+    int64_t m = 0;
+    int64_t nnz = 0;
+    const int64_t* rp = nullptr;
+    const int32_t* ci = nullptr;
+    const void* val = nullptr;
+    int vbytes = 0;
+};
+// per-row length of the full matrix: lower length + strict-lower count of column i
+// (full_len is used as 64-bit atomic counters)
+void mirror_counts(const MirrorArgs& a, int64_t* full_len, hipStream_t s);
+void mirror_copy_lower(const MirrorArgs& a, const int64_t* f_rp, int32_t* f_ci, void* f_val, hipStream_t s);
+// records of the strict lower part with col in [c0, c1): (col - c0, row, value),
+// written in row-major order at positions given by rec_rp (exclusive scan of
+// per-row counts); counts written by mirror_slab_counts.
+void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,
+                        hipStream_t s);
+void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t c1, const int64_t* rec_rp, const int64_t* row_lo,
+                         uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s);
+// place sorted records: record s of column c goes to f_rp[c] + lower_len(c) + (s - (cstart[c] - cstart[c0]))
+// where cstart is the exclusive scan of strict-lower counts per column
+void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint32_t* skey, const uint32_t* srow,
+                       const void* sval, const int64_t* cstart, const int64_t* f_rp, int32_t* f_ci, void* f_val,
+                       hipStream_t s);
+// strict-lower count per column: colcnt[c] = full_len[c] - lower_len[c]
+void mirror_col_counts(const MirrorArgs& a, const int64_t* full_len, int64_t* colcnt, hipStream_t s);
+
+}  // namespace spsyrk

@@ -1,0 +1,186 @@
+// Stable least-significant-digit radix sort of (key, row, value) records by
+// key bits, 8 bits per pass.  Used to group the entries of a CSR matrix by
+// column while keeping rows ascending inside each column (the input is in row
+// order and every pass is stable).
+//
+// Per pass: (1) per-tile digit histograms, (2) exclusive scan of the
+// digit-major (digit, tile) count matrix, (3) stable scatter: every wave ranks
+// its contiguous 1024-record segment with ballot-based digit matching and
+// per-wave LDS counters, the tile is reordered through LDS, then written out
+// so that consecutive threads store consecutive addresses of a digit's run.
+#include "common.h"
+#include "internal.h"
+
+namespace spsyrk {
+namespace {
+
+constexpr int kRBits = 8;
+constexpr int kDigits = 1 << kRBits;
+constexpr int kRItems = 16;
+constexpr int kRTile = kBlock * kRItems;  // 4096 records per tile
+constexpr int kSeg = kWave * kRItems;     // 1024 records per wave
+
+template <int VB>
+struct ValT {
+    using T = uint32_t;
+};
+template <>
+struct ValT<8> {
+    using T = uint64_t;
+};
+
+__global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
+                                                     uint32_t mask, uint32_t* __restrict__ hist, int64_t ntiles) {
+    __shared__ uint32_t cnt[kDigits];
+    cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = int64_t(blockIdx.x) * kRTile;
+#pragma unroll 4
+    for (int k = 0; k < kRItems; ++k) {
+        const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
+        if (i < n) atomicAdd(&cnt[(keys[i] >> shift) & mask], 1u);
+    }
+    __syncthreads();
+    hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+template <int VB>
+__global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restrict__ key_in,
+                                                        const uint32_t* __restrict__ row_in,
+                                                        const typename ValT<VB>::T* __restrict__ val_in,
+                                                        uint32_t* __restrict__ key_out, uint32_t* __restrict__ row_out,
+                                                        typename ValT<VB>::T* __restrict__ val_out, int64_t n, int shift,
+                                                        uint32_t mask, const uint32_t* __restrict__ offs,
+                                                        int64_t ntiles) {
+    using V = typename ValT<VB>::T;
+    __shared__ uint32_t wcnt[kWavesPerBlock][kDigits];
+    __shared__ uint32_t tstart[kDigits];
+    __shared__ uint32_t wt[kWavesPerBlock];
+    __shared__ uint32_t ex_key[kRTile];
+    __shared__ uint32_t ex_row[kRTile];
+    __shared__ V ex_val[VB ? kRTile : 1];
+
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) wcnt[q][threadIdx.x] = 0;
+    __syncthreads();
+
+    const int64_t base = int64_t(blockIdx.x) * kRTile;
+    const int64_t segbase = base + int64_t(w) * kSeg;
+    uint32_t kr[kRItems], rr[kRItems], loc[kRItems];
+    V vr[kRItems];
+    const uint64_t lt = lanemask_lt();
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k) {
+        const int64_t idx = segbase + int64_t(k) * kWave + lane;
+        const bool valid = idx < n;
+        const uint32_t key = valid ? key_in[idx] : 0u;
+        const uint32_t d = (key >> shift) & mask;
+        uint64_t peers = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < kRBits; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bal = __ballot(bit);
+            peers &= bit ? bal : ~bal;
+        }
+        uint32_t cur = 0;
+        if (valid) cur = wcnt[w][d];
+        const uint32_t rank = __popcll(peers & lt);
+        loc[k] = cur + rank;
+        if (valid && rank == 0) wcnt[w][d] = cur + uint32_t(__popcll(peers));
+        kr[k] = key;
+        rr[k] = valid ? row_in[idx] : 0u;
+        if constexpr (VB != 0) vr[k] = valid ? val_in[idx] : V(0);
+    }
+    __syncthreads();
+    {
+        const int d = threadIdx.x;
+        uint32_t c[kWavesPerBlock];
+        uint32_t tot = 0;
+#pragma unroll
+        for (int q = 0; q < kWavesPerBlock; ++q) {
+            c[q] = wcnt[q][d];
+            tot += c[q];
+        }
+        uint32_t all;
+        uint32_t off = block_exclusive_scan(tot, wt, &all);
+        tstart[d] = off;
+#pragma unroll
+        for (int q = 0; q < kWavesPerBlock; ++q) {
+            wcnt[q][d] = off;
+            off += c[q];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k) {
+        const int64_t idx = segbase + int64_t(k) * kWave + lane;
+        if (idx < n) {
+            const uint32_t d = (kr[k] >> shift) & mask;
+            const uint32_t pos = wcnt[w][d] + loc[k];
+            ex_key[pos] = kr[k];
+            ex_row[pos] = rr[k];
+            if constexpr (VB != 0) ex_val[pos] = vr[k];
+        }
+    }
+    __syncthreads();
+    const int tile_n = int(min(int64_t(kRTile), n - base));
+    for (int i = threadIdx.x; i < tile_n; i += kBlock) {
+        const uint32_t key = ex_key[i];
+        const uint32_t d = (key >> shift) & mask;
+        const int64_t g = int64_t(offs[int64_t(d) * ntiles + blockIdx.x]) + (i - tstart[d]);
+        key_out[g] = key;
+        row_out[g] = ex_row[i];
+        if constexpr (VB != 0) val_out[g] = ex_val[i];
+    }
+}
+
+template <int VB>
+void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
+              int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s) {
+    using V = typename ValT<VB>::T;
+    const int64_t ntiles = (n + kRTile - 1) / kRTile;
+    radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
+    scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
+    radix_scatter<VB><<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(
+        ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles);
+}
+
+}  // namespace
+
+size_t radix_tmp_bytes(int64_t n) {
+    const int64_t ntiles = (n + kRTile - 1) / kRTile;
+    const size_t hist = size_t(ntiles) * kDigits * sizeof(uint32_t);
+    return ((hist + 255) & ~size_t(255)) + scan_tmp_bytes(ntiles * kDigits);
+}
+
+int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a, void* val_b,
+               int vbytes, int64_t n, int nbits, void* tmp, hipStream_t s) {
+    if (n <= 1 || nbits <= 0) return 0;
+    const int64_t ntiles = (n + kRTile - 1) / kRTile;
+    uint32_t* hist = static_cast<uint32_t*>(tmp);
+    const size_t hist_bytes = (size_t(ntiles) * kDigits * sizeof(uint32_t) + 255) & ~size_t(255);
+    void* scan_tmp = static_cast<char*>(tmp) + hist_bytes;
+    int cur = 0;
+    for (int shift = 0; shift < nbits; shift += kRBits) {
+        const int bits = nbits - shift < kRBits ? nbits - shift : kRBits;
+        const uint32_t mask = (1u << bits) - 1u;
+        uint32_t* ki = cur ? key_b : key_a;
+        uint32_t* ko = cur ? key_a : key_b;
+        uint32_t* ri = cur ? row_b : row_a;
+        uint32_t* ro = cur ? row_a : row_b;
+        void* vi = cur ? val_b : val_a;
+        void* vo = cur ? val_a : val_b;
+        if (vbytes == 8)
+            run_pass<8>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+        else if (vbytes == 4)
+            run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+        else
+            run_pass<0>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+        cur ^= 1;
+    }
+    return cur;
+}
+
+}  // namespace spsyrk

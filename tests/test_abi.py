@@ -1,0 +1,91 @@
+"""The C-ABI library builds, loads and exports every symbol of include/spsyrk.h;
+host-side argument errors are reported without touching the GPU."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_09713_amd as sp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spsyrk.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(sp.LIB_PATH):
+        from paper_2608_09713_amd import build
+        build.build()
+    return sp.library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(spsyrk_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for f in ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror", "spsyrk_status_string",
+              "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version"):
+        assert f in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.check_output(["nm", "-D", "--defined-only", sp.LIB_PATH]).decode()
+    exported = set(re.findall(r"\bT (spsyrk_\w+)", out))
+    missing = [f for f in declared_functions() if f not in exported]
+    assert not missing, missing
+    for f in declared_functions():
+        getattr(lib, f)
+    assert set(sp.EXPORTS) == set(declared_functions())
+
+
+def test_status_strings_and_version(lib):
+    assert lib.spsyrk_abi_version() == 1
+    for code in range(7):
+        assert lib.spsyrk_status_string(code)
+    assert lib.spsyrk_status_string(99) == b"unknown status"
+
+
+def _csr(nrows, ncols, nnz, rp=1, ci=1, v=None):
+    return sp._Csr(nrows, ncols, nnz, rp, ci, v)
+
+
+def _call_lower(lib, A, sr=0, out=True):
+    o = sp._CsrOut()
+    return lib.spsyrk_lower(ctypes.byref(A) if A is not None else None, sr, None, None,
+                            ctypes.byref(o) if out else None)
+
+
+def test_host_side_errors(lib):
+    # none of these reach the device: the checks run before any allocation
+    assert _call_lower(lib, None) == 1
+    assert b"null" in lib.spsyrk_last_error_detail()
+    assert _call_lower(lib, _csr(4, 4, 2, v=1), sr=7) == 1
+    assert _call_lower(lib, _csr(-1, 4, 0)) == 1
+    assert _call_lower(lib, _csr(1 << 31, 4, 0)) == 3
+    assert _call_lower(lib, _csr(4, 1 << 31, 0)) == 3
+    assert _call_lower(lib, _csr(4, 4, 1 << 31)) == 3
+    assert _call_lower(lib, _csr(4, 4, 3, rp=None)) == 1
+    assert _call_lower(lib, _csr(4, 4, 3, v=None), sr=0) == 1   # plus-times needs values
+    assert _call_lower(lib, _csr(4, 4, 3, v=1), out=False) == 1
+    a, b = _csr(4, 5, 1, v=1), _csr(4, 6, 1, v=1)
+    o = sp._CsrOut()
+    assert lib.spsyrk_offdiag(ctypes.byref(a), ctypes.byref(b), 0, None, None, ctypes.byref(o)) == 1
+    assert b"columns" in lib.spsyrk_last_error_detail()
+    c = _csr(4, 5, 1, v=1)
+    assert lib.spsyrk_mirror(ctypes.byref(c), 0, None, None, ctypes.byref(o)) == 1
+    assert b"square" in lib.spsyrk_last_error_detail()
+    st = sp.Stats()
+    assert lib.spsyrk_last_stats(ctypes.byref(st)) == 1  # no successful call yet on this thread
+
+
+def test_binding_refuses_to_run_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(sp, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(sp, "_lib", None)
+    with pytest.raises(ImportError):
+        sp.library()

@@ -1,0 +1,221 @@
+"""GPU parity: the HIP library through its C-ABI against the CPU oracle.
+
+Inputs are seeded and synthetic: hand-worked fixtures, random matrices with
+empty rows, stored zeros and negative values, the degenerate shapes, rows
+that overflow the light path (long rows, rows with many products), and the
+five workloads at reduced size (several tiles and a ragged tail each).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_09713_amd as sp
+from paper_2608_09713_amd import workloads as W
+from paper_2608_09713_amd.workloads import CSR
+from tests.helpers import csr_from_dense, random_csr
+from tests.parity import compare_full
+
+pytestmark = pytest.mark.gpu
+
+SEMIRINGS = ["f64", "f32", "count", "jaccard"]
+VDT = {"f64": np.float64, "f32": np.float32, "count": None, "jaccard": None}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available()
+    sp.library()
+    return "cuda:0"
+
+
+def upload(A, semiring, dev):
+    vals = None
+    if VDT[semiring] is not None:
+        vals = (A.values if A.values is not None else np.ones(A.nnz)).astype(VDT[semiring])
+    return sp.DeviceCSR.from_host(A.with_values(vals), dev)
+
+
+def run_lower(A, semiring, dev, what):
+    print(f"[lower {semiring}] {what} m={A.nrows} n={A.ncols} nnz={A.nnz}", flush=True)
+    C = sp.lower(upload(A, semiring, dev), semiring)
+    ref = oracle.lower(A.with_values(None if VDT[semiring] is None else A.values.astype(VDT[semiring])), semiring)
+    compare_full(C, ref, semiring, what)
+    return C
+
+
+def test_golden_on_gpu(dev):
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "hand_small.json")))
+    P = CSR(4, 5, np.array(g["P"]["row_ptr"]), np.array(g["P"]["col_idx"], dtype=np.int32),
+            np.array(g["P"]["values"]))
+    C = sp.lower(upload(P, "f64", dev), "f64")
+    rp, ci, v = C.to_host()
+    e = g["P"]["lower_f64"]
+    np.testing.assert_array_equal(rp, e["row_ptr"])
+    np.testing.assert_array_equal(ci, e["col_idx"])
+    np.testing.assert_array_equal(v, e["values"])
+    M = sp.mirror(C, "f64")
+    rp, ci, v = M.to_host()
+    e = g["P"]["mirror_f64"]
+    np.testing.assert_array_equal(rp, e["row_ptr"])
+    np.testing.assert_array_equal(ci, e["col_idx"])
+    np.testing.assert_array_equal(v, e["values"])
+    C = sp.lower(upload(P, "jaccard", dev), "jaccard")
+    e = g["P"]["lower_jaccard"]
+    want = (np.float32(e["numerator"]) / np.float32(e["denominator"])).view(np.uint32)
+    np.testing.assert_array_equal(C.to_host()[2].view(np.uint32), want)
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_random_small(dev, semiring):
+    rng = np.random.default_rng(2024)
+    for t in range(12):
+        m = int(rng.integers(1, 300))
+        n = int(rng.integers(1, 400))
+        A = random_csr(rng, m, n, float(rng.choice([0.005, 0.03, 0.1])), zeros=0.05)
+        run_lower(A, semiring, dev, f"random case {t}")
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_degenerate_shapes(dev, semiring):
+    cases = {
+        "empty_matrix": CSR(7, 5, np.zeros(8, np.int64), np.zeros(0, np.int32), np.zeros(0)),
+        "one_row": csr_from_dense(np.array([[1.0, 0.0, 2.0]])),
+        "one_column": csr_from_dense(np.ones((9, 1))),
+        "identity": csr_from_dense(np.eye(33)),
+        "empty_rows_between": csr_from_dense(np.array([[0, 0, 0], [1.0, 2.0, 0], [0, 0, 0], [3.0, 0, 4.0],
+                                                       [0, 0, 0]])),
+    }
+    for name, A in cases.items():
+        run_lower(A, semiring, dev, name)
+    E0 = CSR(0, 3, np.zeros(1, np.int64), np.zeros(0, np.int32), np.zeros(0))
+    C = sp.lower(upload(E0, semiring, dev), semiring)
+    assert C.nnz == 0 and C.row_ptr.numel() == 1
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_dense_column_uses_heavy_rows(dev, semiring):
+    # one all-ones column over 2500 rows: row i has i products, so rows past
+    # the light limit go to the dense-tile path; output is the full lower triangle
+    m = 2500
+    D = np.zeros((m, 4))
+    D[:, 2] = 1.0
+    D[::3, 0] = 0.5
+    A = csr_from_dense(D)
+    run_lower(A, semiring, dev, "dense column")
+    assert sp.stats()["heavy_rows"] > 0
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_long_rows_use_heavy_rows(dev, semiring):
+    rng = np.random.default_rng(7)
+    m, n = 300, 5000
+    D = np.zeros((m, n))
+    P = rng.random((m, n)) < 0.01
+    P[5, :1200] = True          # more entries than the light path takes
+    P[200, ::3] = True
+    D[P] = rng.random(P.sum()) + 0.5
+    A = csr_from_dense(D, pattern=P)
+    run_lower(A, semiring, dev, "long rows")
+    assert sp.stats()["heavy_rows"] >= 2
+
+
+WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
+             ("offdiag_f64", 5)]
+
+
+@pytest.mark.parametrize("name,shift", WORKLOADS)
+def test_workloads_reduced(dev, name, shift):
+    w = W.make(name, 1, shift)
+    A = w["A"]
+    sr = w["semiring"]
+    C = run_lower(A, sr, dev, f"{name}>>{shift}")
+    if "mirror" in w["ops"]:
+        M = sp.mirror(C, sr)
+        rp, ci, v = C.to_host()
+        ref = oracle.mirror(A.nrows, rp, ci, v)
+        compare_full(M, ref, "count" if sr == "count" else sr, f"{name} mirror")
+    if "offdiag" in w["ops"]:
+        Ai, Aj = w["A"], w["B"]
+        O = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
+        compare_full(O, oracle.offdiag(Ai, Aj, sr), sr, f"{name} offdiag")
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_offdiag_random(dev, semiring):
+    rng = np.random.default_rng(31)
+    for t in range(6):
+        mi, mj, n = int(rng.integers(1, 200)), int(rng.integers(1, 200)), int(rng.integers(1, 300))
+        Ai = random_csr(rng, mi, n, 0.04, signed=True)
+        Aj = random_csr(rng, mj, n, 0.04, signed=True)
+        if VDT[semiring] is not None:
+            Ai = Ai.with_values(Ai.values.astype(VDT[semiring]))
+            Aj = Aj.with_values(Aj.values.astype(VDT[semiring]))
+        O = sp.offdiag(upload(Ai, semiring, dev), upload(Aj, semiring, dev), semiring)
+        compare_full(O, oracle.offdiag(Ai if VDT[semiring] else Ai.with_values(None),
+                                       Aj if VDT[semiring] else Aj.with_values(None), semiring),
+                     semiring, f"offdiag case {t}")
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_mirror_matches_oracle(dev, semiring):
+    rng = np.random.default_rng(77)
+    A = random_csr(rng, 400, 600, 0.02, signed=False)
+    C = sp.lower(upload(A, semiring, dev), semiring)
+    M = sp.mirror(C, semiring)
+    rp, ci, v = C.to_host()
+    ref = oracle.mirror(A.nrows, rp, ci, v)
+    compare_full(M, ref, "count" if semiring == "count" else semiring, "mirror")
+    # offdiag(A, A) is the full product: same structure as the mirror
+    O = sp.offdiag(upload(A, semiring, dev), upload(A, semiring, dev), semiring)
+    np.testing.assert_array_equal(O.to_host()[0], M.to_host()[0])
+    np.testing.assert_array_equal(O.to_host()[1], M.to_host()[1])
+
+
+def test_mirror_structure_only(dev):
+    import torch
+    rng = np.random.default_rng(5)
+    A = random_csr(rng, 100, 80, 0.05)
+    C = sp.lower(upload(A, "count", dev), "count")
+    C_nov = sp.DeviceCSR(C.nrows, C.ncols, C.row_ptr, C.col_idx, None, C.nnz)
+    M = sp.mirror(C_nov, "count")
+    assert M.values is None
+    rp, ci, v = C.to_host()
+    ref = oracle.mirror(A.nrows, rp, ci, v)
+    np.testing.assert_array_equal(M.to_host()[0], ref.row_ptr)
+    np.testing.assert_array_equal(M.to_host()[1], ref.col_idx)
+    del torch
+
+
+def test_deterministic(dev):
+    A = W.make("kmer_i32", 1, 6)["A"]
+    X = sp.lower(upload(A, "count", dev), "count").to_host()
+    Y = sp.lower(upload(A, "count", dev), "count").to_host()
+    for a, b in zip(X, Y):
+        np.testing.assert_array_equal(a, b)
+
+
+def _raw(dev, rp, ci, n, vals=None):
+    import torch
+    return sp.DeviceCSR(len(rp) - 1, n, torch.tensor(rp, dtype=torch.int64, device=dev),
+                        torch.tensor(ci, dtype=torch.int32, device=dev),
+                        None if vals is None else torch.tensor(vals, dtype=torch.float64, device=dev), rp[-1])
+
+
+def test_rejects_non_canonical_on_device(dev):
+    bad = [
+        ([0, 2, 3], [1, 0, 2], 4),   # unsorted row
+        ([0, 2, 3], [1, 1, 2], 4),   # duplicate column
+        ([0, 2, 3], [1, 7, 2], 4),   # column out of range
+        ([0, 3, 2], [1, 2, 3], 4),   # row_ptr decreasing
+    ]
+    for rp, ci, n in bad:
+        with pytest.raises(sp.SpsyrkError) as ei:
+            sp.lower(_raw(dev, rp, ci, n, np.ones(len(ci))), "f64")
+        assert ei.value.status == 2
+    with pytest.raises(sp.SpsyrkError) as ei:   # entry above the diagonal
+        sp.mirror(_raw(dev, [0, 2, 3], [0, 1, 0], 2, np.ones(3)), "f64")
+    assert ei.value.status == 2
