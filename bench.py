@@ -1,0 +1,276 @@
+#!/usr/bin/env python3
+"""Benchmark: tril(A A^T) on one MI355X.
+
+A step is one pass of the hot path over the workload with its inputs already
+resident in HBM: spsyrk_lower (validation, column index, symbolic pass, row
+pointers, numeric pass with the semiring's finalisation), plus spsyrk_mirror
+or spsyrk_offdiag where the workload asks for them.  The default workload is
+the largest one: 2^23 x 2^28, 16 Zipf(0.9) columns per row with columns of
+more than 50 entries dropped, int32 overlap counts finalised to fp32 Jaccard.
+
+Prints one JSON line: useful GFLOP/s (2 per lower-triangle multiply-add,
+integer semirings counted the same way), output nnz/s, the HBM roofline of the
+dominant kernel (measured with HIP events on the library's stream inside the
+timed region) and of the whole call, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak, GB/s
+METRIC = "useful GFLOP/s + output nnz/s for tril(A*A^T); % of HBM roofline, 1 GPU"
+V_IN = {"f64": 8, "f32": 4, "count": 0, "jaccard": 0}       # bytes per value of A
+V_OUT = {"f64": 8, "f32": 4, "count": 4, "jaccard": 4}      # bytes per value of C
+V_CX = {"f64": 8, "f32": 4, "count": 0, "jaccard": 4}       # bytes per value in the column index
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="jaccard_large")
+    p.add_argument("--seed", type=int, default=1)
+    p.add_argument("--scale-shift", type=int, default=0, help="shrink the workload by 2^k (testing only)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=0, help="rows in the oracle sample (0: automatic)")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    p.add_argument("--json-out", default="")
+    return p.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_09713_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(kernel_phase, workload):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        t = json.load(open(path))
+    except Exception:
+        return None
+    if t.get("source_hash") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    k = t.get("kernels", {}).get(kernel_phase)
+    if not k:
+        return None
+    return k.get("hbm_bytes_per_launch")
+
+
+def column_stats(A):
+    c = np.bincount(A.col_idx, minlength=A.ncols)
+    c = c.astype(np.int64)
+    F_L = int((c * (c + 1) // 2).sum())
+    n_ne = int(np.count_nonzero(c))
+    return F_L, n_ne
+
+
+def alg_bytes_phase(phase, sz, sr):
+    """Algorithmic bytes of one launch: every array the kernel must touch,
+    counted once."""
+    m, nnz = sz["m"], sz["nnz_A"]
+    a_rows = 8 * (m + 1)
+    a_ent = nnz * (4 + V_IN[sr])
+    cx = sz["csc_entries"] * 4 + 4 * (sz["ngroups"] + 1)
+    if phase == "light_symbolic":
+        return a_rows + nnz * 4 + cx + 8 * m
+    if phase == "light_numeric":
+        return a_rows + a_ent + cx + sz["csc_entries"] * V_CX[sr] + 8 * (m + 1) + sz["nnz_C"] * (4 + V_OUT[sr])
+    return None
+
+
+def whole_call_bytes(sz, sr, mirror_nnz=None):
+    """B_alg of the call: A read once, A's column-major copy written and read
+    once, C_L written once (and, with the mirror, C_L read and C written)."""
+    m, nnz, v = sz["m"], sz["nnz_A"], V_IN[sr]
+    B_A = 8 * (m + 1) + nnz * (4 + v)
+    B_AT = 2 * (8 * (sz["n_ne"] + 1) + nnz * (4 + v))
+    B_C = 8 * (m + 1) + sz["nnz_C"] * (4 + V_OUT[sr])
+    b = B_A + B_AT + B_C
+    if mirror_nnz is not None:
+        b += B_C + 8 * (m + 1) + mirror_nnz * (4 + V_OUT[sr])
+    return b
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor()
+
+
+def cpu_baseline(A, sr, rows_n, seed):
+    """The oracle as it stands, single-threaded, on a seeded row sample."""
+    import oracle
+    oracle.build()
+    rng = np.random.default_rng(seed + 1000)
+    rows = np.sort(rng.choice(A.nrows, size=min(rows_n, A.nrows), replace=False))
+    Ain = A if sr in ("f64", "f32") else A.with_values(None)
+    t0 = time.perf_counter()
+    R = oracle.lower(Ain, sr, rows=rows)
+    t = time.perf_counter() - t0
+    flops = 2 * int(R.count.astype(np.int64).sum())
+    return {
+        "value": flops / t / 1e9,
+        "unit": "GFLOP/s",
+        "cores": 1,
+        "kind": "oracle",
+        "nnz_per_s": R.nnz / t,
+        "seconds": t,
+        "sample": f"{len(rows)} of {A.nrows} rows (seeded), full column-major copy of A built inside the "
+                  f"timed call; single thread; host {cpu_model()} with {os.cpu_count()} logical CPUs",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "gpus_requested": args.gpus}))
+        sys.exit(2)
+    import torch
+    import paper_2608_09713_amd as sp
+    from paper_2608_09713_amd import workloads as W
+
+    sp.library()  # fails loudly if the HIP library is not built
+    dev = "cuda:0"
+    t0 = time.perf_counter()
+    w = W.make(args.workload, args.seed, args.scale_shift)
+    A = w["A"]
+    sr = w["semiring"]
+    print(f"[bench] generated {args.workload} m={A.nrows} n={A.ncols} nnz={A.nnz} in "
+          f"{time.perf_counter() - t0:.1f}s", file=sys.stderr, flush=True)
+    vdt = {"f64": np.float64, "f32": np.float32}.get(sr)
+    Ad = sp.DeviceCSR.from_host(A if vdt else A.with_values(None), dev, vdt)
+    Bd = sp.DeviceCSR.from_host(w["B"] if vdt else w["B"].with_values(None), dev, vdt) if "B" in w else None
+    F_L, n_ne = column_stats(A)
+
+    def step():
+        C = sp.lower(Ad, sr)
+        st = sp.stats()
+        M = sp.mirror(C, sr) if "mirror" in w["ops"] else None
+        O = sp.offdiag(Ad, Bd, sr) if "offdiag" in w["ops"] else None
+        return C, st, M, O
+
+    for _ in range(args.warmup):
+        out = step()
+        del out
+    torch.cuda.synchronize()
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    sp.timing_begin()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    last = None
+    for _ in range(args.steps):
+        last = None
+        last = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    phases = sp.timing_end()
+    C, st, M, O = last
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    t_step = ms_step / 1e3
+
+    sz = {"m": A.nrows, "nnz_A": A.nnz, "nnz_C": C.nnz, "csc_entries": st["csc_entries"],
+          "ngroups": (A.ncols + (1 << st["group_shift"]) - 1) >> st["group_shift"], "n_ne": n_ne}
+    flops = 2 * F_L
+    value = flops / t_step / 1e9
+    mirror_nnz = M.nnz if M is not None else None
+    B_alg = whole_call_bytes(sz, sr, mirror_nnz)
+
+    # dominant single-kernel phase and its roofline
+    single = {k: v for k, v in phases.items() if k in ("light_symbolic", "light_numeric", "heavy_symbolic",
+                                                       "heavy_numeric")}
+    dom = max(single, key=lambda k: single[k][0] / max(1, single[k][1])) if single else None
+    roof = None
+    if dom is not None:
+        ms, n = phases[dom]
+        avg_s = ms / n / 1e3
+        ab = alg_bytes_phase(dom, sz, sr)
+        if ab is not None:
+            ach = ab / avg_s / 1e9
+            tr = traffic_from_profiles(dom, args.workload)
+            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": ach / HBM_PEAK_GBS, "traffic": tr, "kernel": dom,
+                    "kernel_avg_ms": ms / n, "alg_bytes_per_launch": ab}
+    phase_ms = {k: v[0] / v[1] for k, v in phases.items()}
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"f64": "f64", "f32": "f32 in, f64 accumulate", "count": "i32",
+                  "jaccard": "i32 counts, f32 Jaccard"}[sr],
+        "data": "synthetic (seeded generator)",
+        "config": {"workload": f"{args.workload}: {W.WORKLOADS[args.workload]}" +
+                               (f" (scaled down by 2^{args.scale_shift})" if args.scale_shift else ""),
+                   "nrows": A.nrows, "ncols": A.ncols, "nnz_A": A.nnz, "F_L": F_L, "nnz_C_L": C.nnz,
+                   "ops": w["ops"], "seed": args.seed},
+        "nnz_per_s": C.nnz / t_step,
+        "hbm_roofline_whole_call": {"B_alg": B_alg, "achieved_GBs": B_alg / t_step / 1e9,
+                                    "frac": B_alg / t_step / 1e9 / HBM_PEAK_GBS},
+        "roofline": roof,
+        "phase_ms": phase_ms,
+        "library_stats": st,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if mirror_nnz is not None:
+        line["config"]["nnz_C_full"] = mirror_nnz
+    if O is not None:
+        line["config"]["nnz_offdiag"] = O.nnz
+    del C, M, O, last
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        rows_n = args.cpu_rows or max(1, A.nrows // 8)
+        print(f"[bench] oracle on {rows_n} rows ...", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(A, sr, rows_n, args.seed)
+    else:
+        line["cpu_baseline"] = None
+    s = json.dumps(line)
+    print(s, flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(s + "\n")
+
+
+if __name__ == "__main__":
+    main()

@@ -40,8 +40,9 @@
  *   stream).  A call blocks the host until it knows the output size; it
  *   returns with the output's row_ptr and nnz final and the remaining work
  *   enqueued on hip_stream (synchronise the stream before reading values).
- * - Limits: nrows, ncols < 2^31 and nnz(A) < 2^31 (SPSYRK_ERR_SHAPE
- *   otherwise).  Output nnz is int64.
+ * - Limits: nrows, ncols < 2^31 and, for the inputs of spsyrk_lower and
+ *   spsyrk_offdiag, nnz < 2^31 (SPSYRK_ERR_SHAPE otherwise).  Output nnz and
+ *   the nnz of spsyrk_mirror's input are int64 (below 2^62).
  * - Thread safety: calls on different streams may run concurrently; error
  *   detail strings are thread-local.
  */
@@ -169,6 +170,37 @@ typedef struct spsyrk_stats {
 } spsyrk_stats;
 
 spsyrk_status spsyrk_last_stats(spsyrk_stats* out);
+
+/*
+ * Phase timing (profiling aid).  Between spsyrk_timing_begin() and
+ * spsyrk_timing_end() every call on the calling thread records a pair of HIP
+ * events on its stream around each phase below; the light and heavy phases
+ * are one kernel launch each.  spsyrk_timing_end waits for the recorded
+ * events, returns the summed milliseconds and the number of timed launches
+ * per phase, releases the events and stops recording.  Recording adds no
+ * synchronisation to the calls themselves.
+ */
+typedef enum spsyrk_phase {
+    SPSYRK_PHASE_VALIDATE = 0,       /* canonical-CSR checks of the inputs */
+    SPSYRK_PHASE_COLINDEX = 1,       /* column index of the right operand (sort, pack, directory) */
+    SPSYRK_PHASE_LIGHT_SYMBOLIC = 2, /* row lengths of rows with few products */
+    SPSYRK_PHASE_HEAVY_SYMBOLIC = 3, /* row lengths of rows with many products */
+    SPSYRK_PHASE_SCAN = 4,           /* row pointers of the output */
+    SPSYRK_PHASE_LIGHT_NUMERIC = 5,  /* columns and values of rows with few products */
+    SPSYRK_PHASE_HEAVY_NUMERIC = 6,  /* columns and values of rows with many products */
+    SPSYRK_PHASE_MIRROR_COUNT = 7,   /* spsyrk_mirror: row lengths of the full matrix */
+    SPSYRK_PHASE_MIRROR_COPY = 8,    /* spsyrk_mirror: lower rows copied into place */
+    SPSYRK_PHASE_MIRROR_TRANSPOSE = 9, /* spsyrk_mirror: strict lower part transposed into place */
+    SPSYRK_NUM_PHASES = 10
+} spsyrk_phase;
+
+typedef struct spsyrk_phase_times {
+    double ms[SPSYRK_NUM_PHASES];        /* summed event time per phase */
+    int64_t launches[SPSYRK_NUM_PHASES]; /* timed occurrences per phase */
+} spsyrk_phase_times;
+
+spsyrk_status spsyrk_timing_begin(void);
+spsyrk_status spsyrk_timing_end(spsyrk_phase_times* out);
 
 /* ABI version the library was built with (SPSYRK_ABI_VERSION). */
 int spsyrk_abi_version(void);

@@ -95,12 +95,23 @@ def library():
             lib.spsyrk_last_stats.argtypes = [ctypes.POINTER(Stats)]
             lib.spsyrk_last_stats.restype = ctypes.c_int
             lib.spsyrk_abi_version.restype = ctypes.c_int
+            lib.spsyrk_timing_begin.restype = ctypes.c_int
+            lib.spsyrk_timing_end.argtypes = [ctypes.POINTER(_PhaseTimes)]
+            lib.spsyrk_timing_end.restype = ctypes.c_int
             _lib = lib
     return _lib
 
 
 EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror", "spsyrk_status_string",
-           "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version")
+           "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
+           "spsyrk_timing_end")
+
+PHASES = ("validate", "colindex", "light_symbolic", "heavy_symbolic", "scan", "light_numeric", "heavy_numeric",
+          "mirror_count", "mirror_copy", "mirror_transpose")
+
+
+class _PhaseTimes(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * len(PHASES)), ("launches", ctypes.c_int64 * len(PHASES))]
 
 
 @dataclass
@@ -242,3 +253,17 @@ def stats() -> dict:
     s = Stats()
     library().spsyrk_last_stats(ctypes.byref(s))
     return s.as_dict()
+
+
+def timing_begin() -> None:
+    """Start recording HIP events around every phase of the calls on this thread."""
+    library().spsyrk_timing_begin()
+
+
+def timing_end() -> dict:
+    """Stop recording; {phase: (summed ms, timed launches)} for the phases seen."""
+    t = _PhaseTimes()
+    rc = library().spsyrk_timing_end(ctypes.byref(t))
+    if rc != 0:
+        raise SpsyrkError(rc, library().spsyrk_last_error_detail().decode())
+    return {name: (t.ms[k], t.launches[k]) for k, name in enumerate(PHASES) if t.launches[k]}

@@ -104,6 +104,34 @@ class Arena {
     bool touched_ = false;
 };
 
+// ---- phase timing: event pairs recorded on the call's stream
+struct PhaseMark {
+    int phase;
+    hipEvent_t a, b;
+};
+thread_local bool g_timing = false;
+thread_local std::vector<PhaseMark> g_marks;
+
+class Phase {
+   public:
+    Phase(int phase, hipStream_t s) : s_(s) {
+        if (!g_timing) return;
+        m_.phase = phase;
+        if (hipEventCreate(&m_.a) != hipSuccess || hipEventCreate(&m_.b) != hipSuccess) return;
+        if (hipEventRecord(m_.a, s_) != hipSuccess) return;
+        on_ = true;
+    }
+    ~Phase() {
+        if (!on_) return;
+        if (hipEventRecord(m_.b, s_) == hipSuccess) g_marks.push_back(m_);
+    }
+
+   private:
+    hipStream_t s_;
+    PhaseMark m_{};
+    bool on_ = false;
+};
+
 // small block of device scalars read back at the synchronisation points
 struct Ctl {
     uint32_t err;
@@ -145,7 +173,7 @@ void check_launch() {
     }
 }
 
-void check_input(const spsyrk_csr* A, int sr, bool need_values, const char* name) {
+void check_input(const spsyrk_csr* A, int sr, bool need_values, const char* name, int64_t nnz_limit = kLimit) {
     if (!A) {
         set_detail("%s is null", name);
         throw Fail{SPSYRK_ERR_INVALID_ARG};
@@ -154,8 +182,8 @@ void check_input(const spsyrk_csr* A, int sr, bool need_values, const char* name
         set_detail("%s has a negative size", name);
         throw Fail{SPSYRK_ERR_INVALID_ARG};
     }
-    if (A->nrows >= kLimit || A->ncols >= kLimit || A->nnz >= kLimit) {
-        set_detail("%s: nrows, ncols and nnz must be below 2^31", name);
+    if (A->nrows >= kLimit || A->ncols >= kLimit || A->nnz >= nnz_limit) {
+        set_detail("%s: nrows and ncols must be below 2^31 and nnz below %lld", name, (long long)nnz_limit);
         throw Fail{SPSYRK_ERR_SHAPE};
     }
     if (!A->row_ptr || (A->nnz > 0 && !A->col_idx)) {
@@ -278,8 +306,11 @@ spsyrk_status finish(spsyrk_status st) {
 void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
     Ctl* ctl = ar.get_t<Ctl>(1);
     zero_ctl(ctl, s);
-    validate(L, false, ar, ctl, s, lower ? "A" : "Ai");
-    if (!lower) validate(R, false, ar, ctl, s, "Aj");
+    {
+        Phase ph(SPSYRK_PHASE_VALIDATE, s);
+        validate(L, false, ar, ctl, s, lower ? "A" : "Ai");
+        if (!lower) validate(R, false, ar, ctl, s, "Aj");
+    }
 
     const int64_t m = L.m;
     int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
@@ -299,7 +330,11 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         return;
     }
 
-    ColIndex cx = build_index(R, lower, sr, ar, ctl, s);
+    ColIndex cx;
+    {
+        Phase ph(SPSYRK_PHASE_COLINDEX, s);
+        cx = build_index(R, lower, sr, ar, ctl, s);
+    }
 
     // symbolic
     int32_t* heavy_rows = ar.get_t<int32_t>(m);
@@ -317,7 +352,10 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     la.heavy_rows = heavy_rows;
     la.heavy_count = &ctl->heavy_count;
     la.products = &ctl->products;
-    light_symbolic(la, s);
+    {
+        Phase ph(SPSYRK_PHASE_LIGHT_SYMBOLIC, s);
+        light_symbolic(la, s);
+    }
     check_launch();
     Ctl h = read_ctl(ctl, s);
     const int64_t nheavy = h.heavy_count;
@@ -341,11 +379,17 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         ha.run_lo = ar.get_t<uint32_t>(L.nnz);
         ha.run_hi = ar.get_t<uint32_t>(L.nnz);
         ha.cursor = ar.get_t<uint32_t>(L.nnz);
-        heavy_symbolic(ha, &ctl->queue, s);
+        {
+            Phase ph(SPSYRK_PHASE_HEAVY_SYMBOLIC, s);
+            heavy_symbolic(ha, &ctl->queue, s);
+        }
         check_launch();
     }
     void* stmp = ar.get(scan_tmp_bytes(m + 1));
-    scan_i64(c_rp, c_rp, m + 1, &ctl->total, stmp, s);
+    {
+        Phase ph(SPSYRK_PHASE_SCAN, s);
+        scan_i64(c_rp, c_rp, m + 1, &ctl->total, stmp, s);
+    }
     check_launch();
     h = read_ctl(ctl, s);
     ar.release(stmp);
@@ -360,13 +404,19 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     la.c_rp = c_rp;
     la.c_ci = c_ci;
     la.c_val = c_val;
-    light_numeric(la, s);
+    {
+        Phase ph(SPSYRK_PHASE_LIGHT_NUMERIC, s);
+        light_numeric(la, s);
+    }
     check_launch();
     if (nheavy > 0) {
         ha.c_rp = c_rp;
         ha.c_ci = c_ci;
         ha.c_val = c_val;
-        heavy_numeric(ha, &ctl->queue, s);
+        {
+            Phase ph(SPSYRK_PHASE_HEAVY_NUMERIC, s);
+            heavy_numeric(ha, &ctl->queue, s);
+        }
         check_launch();
     }
     C->nrows = m;
@@ -391,7 +441,10 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
 void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
     Ctl* ctl = ar.get_t<Ctl>(1);
     zero_ctl(ctl, s);
-    validate(L, true, ar, ctl, s, "C_lower");
+    {
+        Phase ph(SPSYRK_PHASE_VALIDATE, s);
+        validate(L, true, ar, ctl, s, "C_lower");
+    }
     const int64_t m = L.m;
     const int vb = L.v ? out_value_bytes(sr) : 0;
     MirrorArgs ma;
@@ -407,18 +460,23 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     int64_t* colcnt = ar.get_t<int64_t>(m + 1);
     HIPCHK(hipMemsetAsync(full_len, 0, size_t(m + 1) * sizeof(int64_t), s));
     HIPCHK(hipMemsetAsync(colcnt, 0, size_t(m + 1) * sizeof(int64_t), s));
-    mirror_counts(ma, full_len, s);
-    mirror_col_counts(ma, full_len, colcnt, s);
-    check_launch();
     void* stmp = ar.get(scan_tmp_bytes(m + 1));
-    scan_i64(colcnt, colcnt, m + 1, &ctl->total2, stmp, s);  // colcnt -> cstart
-    scan_i64(full_len, f_rp, m + 1, &ctl->total, stmp, s);
+    {
+        Phase ph(SPSYRK_PHASE_MIRROR_COUNT, s);
+        mirror_counts(ma, full_len, s);
+        mirror_col_counts(ma, full_len, colcnt, s);
+        scan_i64(colcnt, colcnt, m + 1, &ctl->total2, stmp, s);  // colcnt -> cstart
+        scan_i64(full_len, f_rp, m + 1, &ctl->total, stmp, s);
+    }
     check_launch();
     Ctl h = read_ctl(ctl, s);
     const int64_t total = h.total, nstrict = h.total2;
     int32_t* f_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
     void* f_val = vb ? ar.get(size_t(total > 0 ? total : 1) * vb, true) : nullptr;
-    mirror_copy_lower(ma, f_rp, f_ci, f_val, s);
+    {
+        Phase ph(SPSYRK_PHASE_MIRROR_COPY, s);
+        mirror_copy_lower(ma, f_rp, f_ci, f_val, s);
+    }
     check_launch();
 
     if (nstrict > 0) {
@@ -473,6 +531,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
             h = read_ctl(ctl, s);
             const int64_t nrec = h.total;
             if (nrec == 0) continue;
+            Phase ph(SPSYRK_PHASE_MIRROR_TRANSPOSE, s);
             mirror_slab_extract(ma, c0, c1, row_cnt, row_lo, ka, ra, va, s);
             const int nbits = bit_width_u64(c1 - c0 > 1 ? uint64_t(c1 - c0 - 1) : 0);
             const int which = radix_sort(ka, kb, ra, rb, va, vbb, vb, nrec, nbits, rtmp, s);
@@ -555,7 +614,7 @@ spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const
                             void* hip_stream, spsyrk_csr_out* C_full) {
     return guarded(C_full, al, hip_stream, [&](Arena& ar, hipStream_t s) {
         check_semiring(int(sr));
-        check_input(C_lower, int(sr), false, "C_lower");
+        check_input(C_lower, int(sr), false, "C_lower", int64_t(1) << 62);
         if (C_lower->nrows != C_lower->ncols) {
             set_detail("C_lower must be square (%lld x %lld)", (long long)C_lower->nrows,
                        (long long)C_lower->ncols);
@@ -591,5 +650,35 @@ spsyrk_status spsyrk_last_stats(spsyrk_stats* out) {
 }
 
 int spsyrk_abi_version(void) { return SPSYRK_ABI_VERSION; }
+
+spsyrk_status spsyrk_timing_begin(void) {
+    for (auto& mk : g_marks) {
+        (void)hipEventDestroy(mk.a);
+        (void)hipEventDestroy(mk.b);
+    }
+    g_marks.clear();
+    g_timing = true;
+    return SPSYRK_OK;
+}
+
+spsyrk_status spsyrk_timing_end(spsyrk_phase_times* out) {
+    g_timing = false;
+    spsyrk_status st = SPSYRK_OK;
+    if (out) std::memset(out, 0, sizeof(*out));
+    for (auto& mk : g_marks) {
+        float ms = 0.f;
+        if (hipEventSynchronize(mk.b) != hipSuccess || hipEventElapsedTime(&ms, mk.a, mk.b) != hipSuccess) {
+            set_detail("phase event query failed");
+            st = SPSYRK_ERR_HIP;
+        } else if (out && mk.phase >= 0 && mk.phase < SPSYRK_NUM_PHASES) {
+            out->ms[mk.phase] += ms;
+            out->launches[mk.phase] += 1;
+        }
+        (void)hipEventDestroy(mk.a);
+        (void)hipEventDestroy(mk.b);
+    }
+    g_marks.clear();
+    return st;
+}
 
 }  // extern "C"

@@ -1,0 +1,135 @@
+"""Parity at the workloads' full sizes, in the launch configuration the
+benchmark times: sampled rows are compared element by element with the oracle
+computing those rows one by one, and whole-result properties that hold at any
+size are checked on the device output (exact count sums, diagonal, entry
+counts, symmetry of sampled mirrored rows)."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_09713_amd as sp
+from paper_2608_09713_amd import workloads as W
+from tests.parity import compare_rows, device_rows
+
+pytestmark = pytest.mark.gpu
+
+VDT = {"f64": np.float64, "f32": np.float32, "count": None, "jaccard": None}
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available()
+    sp.library()
+    return "cuda:0"
+
+
+def upload(A, sr, dev):
+    vdt = VDT[sr]
+    return sp.DeviceCSR.from_host(A.with_values(A.values.astype(vdt) if vdt else None), dev)
+
+
+def sample_rows(A, k, seed, extra=()):
+    rng = np.random.default_rng(seed)
+    rows = set(int(r) for r in rng.choice(A.nrows, size=min(k, A.nrows), replace=False))
+    rows.update(int(r) for r in extra)
+    rows.update([0, A.nrows - 1])
+    return np.array(sorted(rows), dtype=np.int64)
+
+
+def col_counts(A):
+    return np.bincount(A.col_idx, minlength=A.ncols).astype(np.int64)
+
+
+def check_lower(A, sr, dev, rows, what):
+    print(f"[full {what}] m={A.nrows} n={A.ncols} nnz={A.nnz}", flush=True)
+    C = sp.lower(upload(A, sr, dev), sr)
+    st = sp.stats()
+    Ain = A.with_values(A.values.astype(VDT[sr]) if VDT[sr] else None)
+    ref = oracle.lower(Ain, sr, rows=rows)
+    compare_rows(C, ref, rows, sr, what)
+    # entry count of every row is at least 1 for non-empty rows, the diagonal is last
+    rp = C.row_ptr.cpu().numpy()
+    lens = np.diff(A.row_ptr)
+    ne = np.flatnonzero(lens > 0)
+    assert np.all(np.diff(rp)[lens == 0] == 0)
+    import torch
+    last = torch.from_numpy(rp[ne + 1] - 1).to(C.col_idx.device)
+    assert torch.equal(C.col_idx[last].cpu(), torch.from_numpy(ne.astype(np.int32)))
+    return C, st, ne, last
+
+
+@pytest.mark.parametrize("name", ["kmer_i32", "jaccard_large"])
+def test_kmer_shapes_full(dev, name):
+    import torch
+    w = W.make(name, 1, 0)
+    A, sr = w["A"], w["semiring"]
+    rows = sample_rows(A, 400, 11)
+    C, st, ne, last = check_lower(A, sr, dev, rows, name)
+    c = col_counts(A)
+    F_L = int((c * (c + 1) // 2).sum())
+    assert st["products"] + A.nnz == F_L  # half-work identity: formed products = F_L exactly
+    if sr == "count":
+        assert int(C.values[: C.nnz].to(torch.int64).sum().item()) == F_L
+        assert torch.equal(C.values[last].cpu(), torch.from_numpy(np.diff(A.row_ptr)[ne].astype(np.int32)))
+    else:
+        v = C.values[: C.nnz]
+        assert bool(((v > 0) & (v <= 1)).all().item())
+        assert bool((C.values[last] == 1.0).all().item())
+        # count semiring on the same input: the Jaccard structure is the count structure
+        K = sp.lower(upload(A, "count", dev), "count")
+        assert K.nnz == C.nnz and torch.equal(K.row_ptr, C.row_ptr)
+        assert torch.equal(K.col_idx[: K.nnz], C.col_idx[: C.nnz])
+        assert int(K.values[: K.nnz].to(torch.int64).sum().item()) == F_L
+
+
+def test_rmat_full_lower_and_mirror(dev):
+    import torch
+    w = W.make("rmat20_f32", 1, 0)
+    A, sr = w["A"], w["semiring"]
+    lens = np.diff(A.row_ptr)
+    heavy = np.argsort(lens)[-3:]  # hub rows: the longest rows
+    rows = sample_rows(A, 60, 12, extra=heavy)
+    C, st, ne, last = check_lower(A, sr, dev, rows, "rmat20")
+    assert st["heavy_rows"] > 0
+    # diagonal = squared row norm (float64 on the host, float32 on the device)
+    sq = np.add.reduceat(A.values.astype(np.float64) ** 2, A.row_ptr[ne])
+    d = C.values[last].cpu().numpy().astype(np.float64)
+    np.testing.assert_allclose(d, sq, rtol=1e-6)
+    nnz_L = C.nnz
+    M = sp.mirror(C, sr)
+    del C
+    torch.cuda.empty_cache()
+    assert M.nnz == 2 * nnz_L - len(ne)
+    # sampled full rows: the same structure as A A^T computed directly by the oracle,
+    # values within the fp32 bound; C(i, j) and C(j, i) bitwise equal
+    ref = oracle.offdiag(A, A, "f32", rows=rows)
+    compare_rows(M, ref, rows, "f32", "rmat20 mirror rows")
+    mrp, mci, mv = device_rows(M, rows)
+    rp_full = M.row_ptr.cpu().numpy()
+    for q, i in enumerate(rows[:20]):
+        cols = mci[mrp[q]:mrp[q + 1]]
+        vals = mv[mrp[q]:mrp[q + 1]]
+        js = cols[:8]
+        jr, jc, jv = device_rows(M, js)
+        for t, j in enumerate(js):
+            seg_c = jc[jr[t]:jr[t + 1]]
+            seg_v = jv[jr[t]:jr[t + 1]]
+            k = np.searchsorted(seg_c, i)
+            assert seg_c[k] == i and seg_v.view(np.uint32)[k] == vals.view(np.uint32)[t]
+    del rp_full
+
+
+def test_offdiag_full(dev):
+    import torch
+    w = W.make("offdiag_f64", 1, 0)
+    Ai, Aj, sr = w["A"], w["B"], w["semiring"]
+    rows = sample_rows(Ai, 400, 13)
+    O = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
+    compare_rows(O, oracle.offdiag(Ai, Aj, sr, rows=rows), rows, sr, "offdiag full")
+    ci, cj = col_counts(Ai), col_counts(Aj)
+    assert sp.stats()["products"] == int((ci * cj).sum())
+    # count semiring: sum of the block = sum_k c^i_k c^j_k
+    K = sp.offdiag(upload(Ai, "count", dev), upload(Aj, "count", dev), "count")
+    assert int(K.values[: K.nnz].to(torch.int64).sum().item()) == int((ci * cj).sum())
+    check_lower(Ai, sr, dev, rows, "offdiag diagonal block")
