@@ -191,7 +191,9 @@ typedef enum spsyrk_phase {
     SPSYRK_PHASE_MIRROR_COUNT = 7,   /* spsyrk_mirror: row lengths of the full matrix */
     SPSYRK_PHASE_MIRROR_COPY = 8,    /* spsyrk_mirror: lower rows copied into place */
     SPSYRK_PHASE_MIRROR_TRANSPOSE = 9, /* spsyrk_mirror: strict lower part transposed into place */
-    SPSYRK_NUM_PHASES = 10
+    SPSYRK_PHASE_RUNS = 10,          /* row classes and the partner run of every entry */
+    SPSYRK_PHASE_COMPACT = 11,       /* light rows moved from their staging slots into place */
+    SPSYRK_NUM_PHASES = 12
 } spsyrk_phase;
 
 typedef struct spsyrk_phase_times {

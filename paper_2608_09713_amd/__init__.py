@@ -107,7 +107,7 @@ EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror", "spsyrk_status_str
            "spsyrk_timing_end")
 
 PHASES = ("validate", "colindex", "light_symbolic", "heavy_symbolic", "scan", "light_numeric", "heavy_numeric",
-          "mirror_count", "mirror_copy", "mirror_transpose")
+          "mirror_count", "mirror_copy", "mirror_transpose", "runs", "compact")
 
 
 class _PhaseTimes(ctypes.Structure):

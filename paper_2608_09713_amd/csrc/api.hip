@@ -4,6 +4,7 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -19,6 +20,12 @@ namespace {
 thread_local std::string g_detail;
 thread_local spsyrk_stats g_stats;
 thread_local bool g_stats_valid = false;
+// lower triangle through the two-pass kernels instead of the single pass
+// (SPSYRK_LOWER_TWO_PASS=1; used to cross-check the two implementations)
+const bool g_two_pass = [] {
+    const char* e = std::getenv("SPSYRK_LOWER_TWO_PASS");
+    return e && e[0] == '1';
+}();
 
 constexpr int64_t kLimit = int64_t(1) << 31;
 
@@ -141,7 +148,11 @@ struct Ctl {
     int64_t nkept;
     int64_t total2;
     int32_t queue;
-    int32_t pad[5];
+    int32_t pad0;
+    unsigned long long light_cap;
+    unsigned long long heavy_total;
+    unsigned long long chunk_counter;
+    int64_t pad[3];
 };
 
 struct HostCtl {
@@ -229,7 +240,8 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 }
 
 // Build the column index of B (sorted by column, packed keys, directory).
-ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s) {
+ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
+                     unsigned long long* prod = nullptr) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -277,7 +289,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         uint32_t* sr_ = which ? rb : ra;
         void* sv = which ? vbuf : va;
         void* ctmp = ar.get(colindex_tmp_bytes(N));
-        build_colindex(sk, sr_, sv, N, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, s);
+        build_colindex(sk, sr_, sv, N, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, prod, s);
         check_launch();
         ar.release(ctmp);
         ar.release(ka);
@@ -288,7 +300,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         if (vbuf) ar.release(vbuf);
     } else {
         void* ctmp = ar.get(colindex_tmp_bytes(0));
-        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, s);
+        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, prod, s);
         check_launch();
         ar.release(ctmp);
     }
@@ -302,6 +314,149 @@ spsyrk_status finish(spsyrk_status st) {
     return st;
 }
 
+// Rows per wavefront chunk of the light-row kernel (SPSYRK_ROWS_PER_CHUNK
+// overrides it for tuning); a chunk splits into as many LDS batches as needed.
+int rows_per_chunk(double) {
+    if (const char* e = std::getenv("SPSYRK_ROWS_PER_CHUNK")) {
+        const int v = std::atoi(e);
+        if (v >= 1 && v <= kFusedRows) return v;
+    }
+    return kFusedRows;
+}
+
+// C_L = tril(A A^T): column index with per-row product counts, row classes,
+// partner runs of all entries, dense-tile lengths of the heavy rows, the
+// light rows computed once into upper-bound staging slots with their exact
+// lengths, row pointers, compaction of the light rows, heavy rows' values.
+void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, spsyrk_csr_out* C) {
+    const int64_t m = L.m;
+    const int vbo = out_value_bytes(sr);
+    unsigned long long* prod = ar.get_t<unsigned long long>(m);
+    HIPCHK(hipMemsetAsync(prod, 0, size_t(m) * sizeof(unsigned long long), s));
+    ColIndex cx;
+    {
+        Phase ph(SPSYRK_PHASE_COLINDEX, s);
+        cx = build_index(L, true, sr, ar, ctl, s, prod);
+    }
+    int32_t* heavy_rows = ar.get_t<int32_t>(m);
+    int64_t* ub = ar.get_t<int64_t>(m + 1);
+    uint32_t* run_lo = ar.get_t<uint32_t>(L.nnz);
+    uint32_t* run_hi = ar.get_t<uint32_t>(L.nnz);
+    HIPCHK(hipMemsetAsync(ub + m, 0, sizeof(int64_t), s));
+    {
+        Phase ph(SPSYRK_PHASE_RUNS, s);
+        classify_rows(L.rp, prod, m, true, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s);
+        partner_runs(L, cx, true, prod, run_lo, run_hi, s);
+    }
+    check_launch();
+    Ctl h = read_ctl(ctl, s);
+    const int64_t nheavy = h.heavy_count;
+    const int64_t light_cap = int64_t(h.light_cap);
+    HeavyArgs ha;
+    int64_t* heavy_nnz = nullptr;
+    if (nheavy > 0) {
+        heavy_nnz = ar.get_t<int64_t>(m);
+        ha.m = m;
+        ha.rp = L.rp;
+        ha.ci = L.ci;
+        ha.val = L.v;
+        ha.cx = cx;
+        ha.m_right = L.m;
+        ha.rp_right = L.rp;
+        ha.lower = true;
+        ha.sr = sr;
+        ha.heavy_rows = heavy_rows;
+        ha.heavy_count = &ctl->heavy_count;
+        ha.heavy_max = nheavy;
+        ha.row_nnz = heavy_nnz;
+        ha.run_lo = run_lo;
+        ha.run_hi = run_hi;
+        ha.runs_ready = true;
+        ha.cursor = ar.get_t<uint32_t>(L.nnz);
+        Phase ph(SPSYRK_PHASE_HEAVY_SYMBOLIC, s);
+        heavy_symbolic(ha, &ctl->queue, s);
+    }
+    check_launch();
+    int64_t* ubp = ub;
+    void* stmp = ar.get(scan_tmp_bytes(m + 1));
+    {
+        Phase ph(SPSYRK_PHASE_SCAN, s);
+        scan_i64(ub, ubp, m + 1, &ctl->total2, stmp, s);
+    }
+    int32_t* s_ci = ar.get_t<int32_t>(light_cap > 0 ? light_cap : 1);
+    void* s_val = ar.get(size_t(light_cap > 0 ? light_cap : 1) * vbo);
+    int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
+    HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
+
+    FusedArgs fa;
+    fa.m = m;
+    fa.rp = L.rp;
+    fa.ci = L.ci;
+    fa.val = L.v;
+    fa.cx = cx;
+    fa.m_right = L.m;
+    fa.lower = true;
+    fa.sr = sr;
+    fa.prod = prod;
+    fa.run_lo = run_lo;
+    fa.run_hi = run_hi;
+    fa.heavy_nnz = heavy_nnz;
+    fa.ubp = ubp;
+    fa.row_cnt = row_cnt;
+    const int64_t nlight = m - nheavy;
+    fa.rows_per_chunk = rows_per_chunk(nlight > 0 ? double(light_cap) / double(nlight) : 1.0);
+    fa.nchunks = (m + fa.rows_per_chunk - 1) / fa.rows_per_chunk;
+    fa.c_ci = s_ci;
+    fa.c_val = s_val;
+    {
+        Phase ph(SPSYRK_PHASE_LIGHT_NUMERIC, s);
+        light_fused(fa, s);
+    }
+    check_launch();
+    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
+    {
+        Phase ph(SPSYRK_PHASE_SCAN, s);
+        scan_i64(row_cnt, c_rp, m + 1, &ctl->total, stmp, s);
+    }
+    check_launch();
+    h = read_ctl(ctl, s);
+    const int64_t total = h.total;
+    int32_t* c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
+    void* c_val = ar.get(size_t(total > 0 ? total : 1) * vbo, true);
+    {
+        Phase ph(SPSYRK_PHASE_COMPACT, s);
+        compact_rows(m, light_cap, ubp, row_cnt, c_rp, s_ci, s_val, vbo, c_ci, c_val, s);
+    }
+    check_launch();
+    if (nheavy > 0) {
+        ha.c_rp = c_rp;
+        ha.c_ci = c_ci;
+        ha.c_val = c_val;
+        {
+            Phase ph(SPSYRK_PHASE_HEAVY_NUMERIC, s);
+            heavy_numeric(ha, &ctl->queue, s);
+        }
+        check_launch();
+    }
+    C->nrows = m;
+    C->ncols = m;
+    C->nnz = total;
+    C->capacity = total;
+    C->row_ptr = c_rp;
+    C->col_idx = c_ci;
+    C->values = c_val;
+    spsyrk_stats st{};
+    st.nnz_out = total;
+    st.csc_entries = h.nkept;
+    st.heavy_rows = nheavy;
+    st.light_rows = nlight;
+    st.products = int64_t(h.products);
+    st.group_shift = cx.gs;
+    st.row_bits = cx.rowbits;
+    g_stats = st;
+    g_stats_valid = true;
+}
+
 // C = tril(L R^T) (lower) or L R^T (offdiag), with R = L for lower.
 void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
     Ctl* ctl = ar.get_t<Ctl>(1);
@@ -313,9 +468,9 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     }
 
     const int64_t m = L.m;
-    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
     spsyrk_stats st{};
     if (m == 0 || L.nnz == 0 || R.nnz == 0) {
+        int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
         HIPCHK(hipMemsetAsync(c_rp, 0, size_t(m + 1) * sizeof(int64_t), s));
         C->nrows = m;
         C->ncols = R.m;
@@ -330,6 +485,11 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         return;
     }
 
+    if (lower && !g_two_pass) {
+        syrk_lower(L, sr, ar, ctl, s, C);
+        return;
+    }
+    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
     ColIndex cx;
     {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);

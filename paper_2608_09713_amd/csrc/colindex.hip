@@ -1,12 +1,19 @@
-// Column index of the right operand from its column-sorted records: packs
-// (column-in-group, row) keys, drops the last entry of every column when only
-// partners with a smaller row are ever needed, and builds the group
-// directory by binary search over the sorted columns.
+// Column index of the right operand from its column-sorted records.
+//
+// `pack` writes (column-in-group, row) keys, drops the last entry of every
+// column when only partners with a smaller row are ever needed, and fills the
+// group directory: the first entry of every column that opens a new group
+// writes the directory slots of the groups between the previous column's
+// group and its own.  In lower mode it also adds every entry's rank inside
+// its column (the number of partners j < i it has) to its row's product
+// count, so that the rows can be classified before any row is processed.
 #include "common.h"
 #include "internal.h"
 
 namespace spsyrk {
 namespace {
+
+constexpr int kPTile = 2048;  // positions per pack workgroup
 
 __global__ __launch_bounds__(kBlock) void start_flags(const uint32_t* __restrict__ scol, int64_t n,
                                                       uint32_t* __restrict__ st) {
@@ -19,28 +26,98 @@ template <int VB, bool JAC>
 __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol, const uint32_t* __restrict__ srow,
                                                const void* __restrict__ sval, int64_t n,
                                                const uint32_t* __restrict__ excl, bool drop_last, int gs, int rowbits,
-                                               const int64_t* __restrict__ rp_b, uint32_t* __restrict__ key,
-                                               void* __restrict__ val) {
-    const int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (p >= n) return;
-    const uint32_t col = scol[p];
-    const bool start = p == 0 || scol[p - 1] != col;
-    const bool last = p == n - 1 || scol[p + 1] != col;
-    int64_t q = p;
-    if (drop_last) {
-        if (last) return;
-        const int64_t cidx = int64_t(excl[p]) + (start ? 1 : 0) - 1;  // columns before this one
-        q = p - cidx;
+                                               int64_t ngroups, const int64_t* __restrict__ nkept,
+                                               const int64_t* __restrict__ rp_b,
+                                               uint32_t* __restrict__ key, void* __restrict__ val,
+                                               uint32_t* __restrict__ gptr, unsigned long long* __restrict__ prod) {
+    __shared__ int64_t colstart[kPTile];
+    __shared__ int64_t wt[kWavesPerBlock];
+    __shared__ int64_t carry_s;
+    const int64_t base = int64_t(blockIdx.x) * kPTile;
+    const int64_t end = min(n, base + kPTile);
+    // column start of the tile's first position (its column may begin in an earlier tile)
+    if (threadIdx.x == 0 && prod) {
+        const uint32_t c0 = scol[base];
+        int64_t lo = 0, hi = base;
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (scol[mid] < c0)
+                lo = mid + 1;
+            else
+                hi = mid;
+        }
+        carry_s = lo;
+    }
+    if (prod) {
+        // inclusive max-scan of "position if it starts a column" over the tile
+        constexpr int kPer = kPTile / kBlock;
+        int64_t v[kPer];
+        int64_t mx = -1;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int64_t p = base + int64_t(threadIdx.x) * kPer + k;
+            int64_t s = -1;
+            if (p < end && (p == 0 || scol[p] != scol[p - 1])) s = p;
+            mx = s > mx ? s : mx;
+            v[k] = mx;
+        }
+        // exclusive max over the preceding threads
+        int64_t inc = mx;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const int64_t u = __shfl_up(inc, d, kWave);
+            if (lane_id() >= d) inc = u > inc ? u : inc;
+        }
+        if (lane_id() == kWave - 1) wt[threadIdx.x / kWave] = inc;
+        __syncthreads();
+        int64_t before = carry_s;
+        const int w = threadIdx.x / kWave;
+        for (int q = 0; q < w; ++q) before = wt[q] > before ? wt[q] : before;
+        int64_t prev = __shfl_up(inc, 1, kWave);
+        if (lane_id() > 0) before = prev > before ? prev : before;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int64_t cs = v[k] > before ? v[k] : before;
+            colstart[threadIdx.x * kPer + k] = cs;
+        }
+        __syncthreads();
     }
     const uint32_t gmask = (gs >= 32) ? 0xffffffffu : ((1u << gs) - 1u);
-    const uint32_t row = srow[p];
-    key[q] = ((col & gmask) << rowbits) | row;
-    if constexpr (JAC) {
-        static_cast<int32_t*>(val)[q] = int32_t(rp_b[row + 1] - rp_b[row]);
-    } else if constexpr (VB == 8) {
-        static_cast<uint64_t*>(val)[q] = static_cast<const uint64_t*>(sval)[p];
-    } else if constexpr (VB == 4) {
-        static_cast<uint32_t*>(val)[q] = static_cast<const uint32_t*>(sval)[p];
+    for (int64_t p = base + threadIdx.x; p < end; p += kBlock) {
+        const uint32_t col = scol[p];
+        const bool start = p == 0 || scol[p - 1] != col;
+        const bool last = p == n - 1 || scol[p + 1] != col;
+        const uint32_t row = srow[p];
+        // kept entries before p: every column entirely before p lost its last entry
+        const int64_t cols_before = int64_t(excl[p]) + (start ? 1 : 0) - 1;
+        if (prod) {
+            const int64_t rank = p - colstart[p - base];
+            if (rank > 0) atomicAdd(&prod[row], (unsigned long long)rank);
+        }
+        if (start) {
+            // directory slots of the groups opened by this column
+            const int64_t q0 = drop_last ? p - cols_before : p;
+            const int64_t g = int64_t(col >> gs);
+            const int64_t gprev = p == 0 ? -1 : int64_t(scol[p - 1] >> gs);
+            for (int64_t x = gprev + 1; x <= g; ++x) gptr[x] = uint32_t(q0);
+        }
+        if (p == n - 1) {
+            const uint32_t kept = uint32_t(*nkept);
+            for (int64_t x = int64_t(col >> gs) + 1; x <= ngroups; ++x) gptr[x] = kept;
+        }
+        int64_t q = p;
+        if (drop_last) {
+            if (last) continue;
+            q = p - cols_before;
+        }
+        key[q] = ((col & gmask) << rowbits) | row;
+        if constexpr (JAC) {
+            static_cast<int32_t*>(val)[q] = int32_t(rp_b[row + 1] - rp_b[row]);
+        } else if constexpr (VB == 8) {
+            static_cast<uint64_t*>(val)[q] = static_cast<const uint64_t*>(sval)[p];
+        } else if constexpr (VB == 4) {
+            static_cast<uint32_t*>(val)[q] = static_cast<const uint32_t*>(sval)[p];
+        }
     }
 }
 
@@ -48,24 +125,9 @@ __global__ void kept_count(int64_t n, const uint32_t* ncols_distinct, bool drop_
     *nkept = drop_last ? n - int64_t(*ncols_distinct) : n;
 }
 
-__global__ __launch_bounds__(kBlock) void directory(const uint32_t* __restrict__ scol, int64_t n,
-                                                    const uint32_t* __restrict__ excl, bool drop_last, int gs,
-                                                    int64_t ngroups, const int64_t* __restrict__ nkept,
-                                                    uint32_t* __restrict__ gptr) {
+__global__ __launch_bounds__(kBlock) void empty_directory(int64_t ngroups, uint32_t* __restrict__ gptr) {
     const int64_t g = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (g > ngroups) return;
-    const uint64_t target = uint64_t(g) << gs;
-    int64_t lo = 0, hi = n;
-    while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (uint64_t(scol[mid]) < target)
-            lo = mid + 1;
-        else
-            hi = mid;
-    }
-    int64_t q = lo;
-    if (drop_last) q = (lo < n) ? lo - int64_t(excl[lo]) : *nkept;
-    gptr[g] = uint32_t(q);
+    if (g <= ngroups) gptr[g] = 0;
 }
 
 }  // namespace
@@ -76,35 +138,37 @@ size_t colindex_tmp_bytes(int64_t n) {
 
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const void* sval, int64_t n_entries, bool drop_last,
                     int vbytes_in, int sr, const int64_t* rp_b, ColIndex& cx, void* tmp, int64_t* d_nkept,
-                    hipStream_t s) {
+                    unsigned long long* prod, hipStream_t s) {
     uint32_t* excl = static_cast<uint32_t*>(tmp);
     char* after = static_cast<char*>(tmp) + ((size_t(n_entries) * 4 + 255) & ~size_t(255));
     uint32_t* ncols = reinterpret_cast<uint32_t*>(after);
     void* scan_tmp = after + 256;
     const int64_t n = n_entries;
-    if (n > 0) {
-        const unsigned nb = unsigned((n + kBlock - 1) / kBlock);
-        start_flags<<<nb, kBlock, 0, s>>>(scol, n, excl);
-        scan_u32(excl, excl, n, ncols, scan_tmp, s);
-        const bool jac = sr == kJaccard;
-        if (jac)
-            pack<0, true><<<nb, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, rp_b, cx.key,
-                                                cx.val);
-        else if (vbytes_in == 8)
-            pack<8, false><<<nb, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, rp_b, cx.key,
-                                                 cx.val);
-        else if (vbytes_in == 4)
-            pack<4, false><<<nb, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, rp_b, cx.key,
-                                                 cx.val);
-        else
-            pack<0, false><<<nb, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, rp_b, cx.key,
-                                                 cx.val);
-        kept_count<<<1, 1, 0, s>>>(n, ncols, drop_last, d_nkept);
-    } else {
+    if (n == 0) {
         (void)hipMemsetAsync(d_nkept, 0, sizeof(int64_t), s);
+        const unsigned ng = unsigned((cx.ngroups + 1 + kBlock - 1) / kBlock);
+        empty_directory<<<ng, kBlock, 0, s>>>(cx.ngroups, cx.gptr);
+        return;
     }
-    const unsigned ng = unsigned((cx.ngroups + 1 + kBlock - 1) / kBlock);
-    directory<<<ng, kBlock, 0, s>>>(scol, n, excl, drop_last, cx.gs, cx.ngroups, d_nkept, cx.gptr);
+    const unsigned nb = unsigned((n + kBlock - 1) / kBlock);
+    start_flags<<<nb, kBlock, 0, s>>>(scol, n, excl);
+    scan_u32(excl, excl, n, ncols, scan_tmp, s);
+    // the number of distinct columns fixes the kept count and the directory's end
+    kept_count<<<1, 1, 0, s>>>(n, ncols, drop_last, d_nkept);
+    const unsigned np = unsigned((n + kPTile - 1) / kPTile);
+    const bool jac = sr == kJaccard;
+    if (jac)
+        pack<0, true><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
+                                            d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+    else if (vbytes_in == 8)
+        pack<8, false><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
+                                             d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+    else if (vbytes_in == 4)
+        pack<4, false><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
+                                             d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+    else
+        pack<0, false><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
+                                             d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
 }
 
 }  // namespace spsyrk

@@ -20,14 +20,7 @@ enum ErrBits : uint32_t {
 };
 
 // number of bits needed to write x (0 -> 0)
-__host__ __device__ inline int bit_width_u64(uint64_t x) {
-    int b = 0;
-    while (x) {
-        ++b;
-        x >>= 1;
-    }
-    return b;
-}
+__host__ __device__ inline int bit_width_u64(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
 
 __device__ inline int lane_id() { return __lane_id(); }
 

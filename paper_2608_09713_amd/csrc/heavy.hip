@@ -73,7 +73,7 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
         uint64_t prod_local = 0;
         for (int64_t e = e0 + tid; e < e1; e += kBlock) {
             uint32_t st, len;
-            if constexpr (!NUM) {
+            if (!NUM && !a.runs_ready) {
                 partner_run(key, a.cx.gptr, a.cx.gs, a.cx.rowbits, uint32_t(a.ci[e]), uint32_t(i), LOWER, st, len);
                 a.run_lo[e] = st;
                 a.run_hi[e] = st + len;
@@ -85,7 +85,7 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
         }
         if constexpr (!NUM) {
             uint64_t tot = wave_reduce_sum(prod_local);
-            if (lane == 0 && tot) atomicAdd(a.products, (unsigned long long)tot);
+            if (lane == 0 && tot && a.products) atomicAdd(a.products, (unsigned long long)tot);
         }
         __threadfence_block();
         __syncthreads();
@@ -184,7 +184,10 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
         }
         // diagonal (lower triangle only; a heavy row is never empty)
         if constexpr (!NUM) {
-            if (tid == 0) a.row_nnz[i] = count + (LOWER ? 1 : 0);
+            if (tid == 0) {
+                a.row_nnz[i] = count + (LOWER ? 1 : 0);
+                if (a.nnz_total) atomicAdd(a.nnz_total, (unsigned long long)(count + (LOWER ? 1 : 0)));
+            }
         } else if (LOWER) {
             Out dv;
             if constexpr (kVal) {

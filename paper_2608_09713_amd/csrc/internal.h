@@ -66,11 +66,13 @@ int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_
                void* val_b, int vbytes, int64_t n, int nbits, void* tmp, hipStream_t s);
 
 // ---- colindex.hip
-// From records sorted by column: keep flags, packing and directory.
+// From records sorted by column: keep flags, packing and directory.  With
+// prod non-null (lower mode) every entry's rank in its column is added to
+// prod[row] (the row's off-diagonal product count; prod must start at zero).
 size_t colindex_tmp_bytes(int64_t n);
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const void* sval, int64_t n_entries,
                     bool drop_last, int vbytes_in, int sr, const int64_t* rp_b, ColIndex& ci,
-                    void* tmp, int64_t* d_nkept, hipStream_t s);
+                    void* tmp, int64_t* d_nkept, unsigned long long* prod, hipStream_t s);
 
 // ---- light.hip
 struct LightArgs {
@@ -98,6 +100,54 @@ struct LightArgs {
 void light_symbolic(const LightArgs& a, hipStream_t s);
 void light_numeric(const LightArgs& a, hipStream_t s);
 
+// ---- light_fused.hip
+// Light-row limits of the single-pass kernel: a row is light when it has at
+// most kFusedEntries entries and kFusedProducts off-diagonal products.
+constexpr int kFusedEntries = 256;
+constexpr int kFusedProducts = 512;
+constexpr int kFusedRows = 32;
+struct FusedArgs {
+    int64_t m = 0;
+    const int64_t* rp = nullptr;
+    const int32_t* ci = nullptr;
+    const void* val = nullptr;
+    ColIndex cx;
+    int64_t m_right = 0;
+    bool lower = true;
+    int sr = kF64;
+    const unsigned long long* prod = nullptr;  // off-diagonal products per row
+    const uint32_t* run_lo = nullptr;          // partner run of every entry (runs kernel)
+    const uint32_t* run_hi = nullptr;
+    const int64_t* heavy_nnz = nullptr;        // output lengths of heavy rows
+    const int64_t* ubp = nullptr;              // staging slot of every row (prefix of upper bounds)
+    int64_t* row_cnt = nullptr;                // exact output length of every row
+    int rows_per_chunk = 8;
+    int64_t nchunks = 0;
+    int32_t* c_ci = nullptr;                   // staging columns
+    void* c_val = nullptr;                     // staging values
+};
+// light rows: columns and values at the staging slots, exact lengths in row_cnt
+// (heavy rows: their length from heavy_nnz)
+void light_fused(const FusedArgs& a, hipStream_t s);
+// heavy rows (over the limits) into a list; light capacity sum(prod + diagonal) and
+// the sum of prod over all rows into the two counters
+// and ub[i] = products + diagonal for light rows, 0 for heavy rows
+void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m, bool lower, int32_t* heavy_rows,
+                   int32_t* heavy_count, unsigned long long* light_cap, unsigned long long* prod_sum, int64_t* ub,
+                   hipStream_t s);
+
+// ---- runs.hip
+// Partner run [run_lo[e], run_hi[e]) of every entry of the left operand
+// (entries of rows with no products get an empty run without a lookup when
+// prod is given).
+void partner_runs(const DevCsr& A, const ColIndex& cx, bool lower, const unsigned long long* prod, uint32_t* run_lo,
+                  uint32_t* run_hi, hipStream_t s);
+// Copy the staged rows to their final places: the element at staging slot
+// ubp[i] + x (x < row_cnt[i]) goes to c_rp[i] + x.  ubp is non-decreasing
+// with ubp[m] = staged; rows with no staging room (heavy rows) copy nothing.
+void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
+                  const int32_t* s_ci, const void* s_val, int vbytes, int32_t* c_ci, void* c_val, hipStream_t s);
+
 // ---- heavy.hip
 struct HeavyArgs {
     int64_t m = 0;
@@ -115,9 +165,11 @@ struct HeavyArgs {
     // per-entry run bounds (sized nnz of the left operand), written by the symbolic pass
     uint32_t* run_lo = nullptr;
     uint32_t* run_hi = nullptr;
+    bool runs_ready = false;            // run_lo/run_hi already filled (the symbolic pass skips its lookups)
     uint32_t* cursor = nullptr;
-    unsigned long long* products = nullptr;
+    unsigned long long* products = nullptr;  // optional: add the products formed
     int64_t* row_nnz = nullptr;
+    unsigned long long* nnz_total = nullptr; // optional: add the heavy rows' lengths
     const int64_t* c_rp = nullptr;
     int32_t* c_ci = nullptr;
     void* c_val = nullptr;
