@@ -226,8 +226,7 @@ DevCsr dev(const spsyrk_csr* A) {
 }
 
 void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name) {
-    uint32_t* bits = static_cast<uint32_t*>(ar.get(validate_tmp_bytes(A)));
-    validate_csr(A, upper_forbidden, bits, &ctl->err, s);
+    validate_csr(A, upper_forbidden, &ctl->err, s);
     check_launch();
     Ctl h = read_ctl(ctl, s);
     if (h.err) {
@@ -236,12 +235,12 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
                    (h.err & kErrUpper) ? " above-diagonal" : "");
         throw Fail{SPSYRK_ERR_NOT_CANONICAL};
     }
-    ar.release(bits);
 }
 
 // Build the column index of B (sorted by column, packed keys, directory).
+// With run (zeroed beforehand; lower mode) every entry's partner run is written.
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                     unsigned long long* prod = nullptr) {
+                     uint2* run = nullptr) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -266,41 +265,36 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
     cx.key = ar.get_t<uint32_t>(N > 0 ? N : 1);
     cx.val = vb_out ? ar.get(size_t(N > 0 ? N : 1) * vb_out) : nullptr;
 
-    uint32_t *ka = nullptr, *kb = nullptr, *ra = nullptr, *rb = nullptr;
-    void *va = nullptr, *vbuf = nullptr;
     if (N > 0) {
-        ka = ar.get_t<uint32_t>(N);
-        kb = ar.get_t<uint32_t>(N);
-        ra = ar.get_t<uint32_t>(N);
-        rb = ar.get_t<uint32_t>(N);
-        if (vb) {
-            va = ar.get(size_t(N) * vb);
-            vbuf = ar.get(size_t(N) * vb);
-        }
-        HIPCHK(hipMemcpyAsync(ka, B.ci, size_t(N) * 4, hipMemcpyDeviceToDevice, s));
-        if (vb) HIPCHK(hipMemcpyAsync(va, B.v, size_t(N) * vb, hipMemcpyDeviceToDevice, s));
-        entry_rows(B, ra, s);
-        check_launch();
+        // records (column, row, entry index) sorted by column; values are
+        // gathered by entry index when the keys are packed
+        uint32_t* ka = ar.get_t<uint32_t>(N);
+        uint32_t* kb = ar.get_t<uint32_t>(N);
+        uint32_t* ra = ar.get_t<uint32_t>(N);
+        uint32_t* rb = ar.get_t<uint32_t>(N);
+        uint32_t* ea = ar.get_t<uint32_t>(N);
+        uint32_t* eb = ar.get_t<uint32_t>(N);
         void* tmp = ar.get(radix_tmp_bytes(N));
-        const int which = radix_sort(ka, kb, ra, rb, va, vbuf, vb, N, nbits_n, tmp, s);
+        // Jaccard keeps the row lengths in the row field's spare bits
+        const int lenbits = sr == kJaccard ? 32 - cx.rowbits : 0;
+        const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
+                                         s);
         check_launch();
         ar.release(tmp);
-        uint32_t* sk = which ? kb : ka;
-        uint32_t* sr_ = which ? rb : ra;
-        void* sv = which ? vbuf : va;
         void* ctmp = ar.get(colindex_tmp_bytes(N));
-        build_colindex(sk, sr_, sv, N, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, prod, s);
+        build_colindex(which ? kb : ka, which ? rb : ra, which ? eb : ea, N, drop_last, vb, sr, B.v, B.rp, lenbits, cx,
+                       ctmp, &ctl->nkept, run, s);
         check_launch();
         ar.release(ctmp);
         ar.release(ka);
         ar.release(kb);
         ar.release(ra);
         ar.release(rb);
-        if (va) ar.release(va);
-        if (vbuf) ar.release(vbuf);
+        ar.release(ea);
+        ar.release(eb);
     } else {
         void* ctmp = ar.get(colindex_tmp_bytes(0));
-        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.rp, cx, ctmp, &ctl->nkept, prod, s);
+        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.v, B.rp, 0, cx, ctmp, &ctl->nkept, nullptr, s);
         check_launch();
         ar.release(ctmp);
     }
@@ -324,29 +318,30 @@ int rows_per_chunk(double) {
     return kFusedRows;
 }
 
-// C_L = tril(A A^T): column index with per-row product counts, row classes,
-// partner runs of all entries, dense-tile lengths of the heavy rows, the
-// light rows computed once into upper-bound staging slots with their exact
-// lengths, row pointers, compaction of the light rows, heavy rows' values.
+// C_L = tril(A A^T): column index with the partner run of every entry,
+// per-row product counts, row classes, dense-tile lengths of the heavy rows,
+// the light rows computed once into upper-bound staging slots with their
+// exact lengths, row pointers, compaction of the light rows, heavy rows'
+// values.
 void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, spsyrk_csr_out* C) {
     const int64_t m = L.m;
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
     HIPCHK(hipMemsetAsync(prod, 0, size_t(m) * sizeof(unsigned long long), s));
+    uint2* run = ar.get_t<uint2>(L.nnz);
+    HIPCHK(hipMemsetAsync(run, 0, size_t(L.nnz) * sizeof(uint2), s));
     ColIndex cx;
     {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
-        cx = build_index(L, true, sr, ar, ctl, s, prod);
+        cx = build_index(L, true, sr, ar, ctl, s, run);
     }
     int32_t* heavy_rows = ar.get_t<int32_t>(m);
     int64_t* ub = ar.get_t<int64_t>(m + 1);
-    uint32_t* run_lo = ar.get_t<uint32_t>(L.nnz);
-    uint32_t* run_hi = ar.get_t<uint32_t>(L.nnz);
     HIPCHK(hipMemsetAsync(ub + m, 0, sizeof(int64_t), s));
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
+        row_products(L.rp, m, L.nnz, run, prod, s);
         classify_rows(L.rp, prod, m, true, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s);
-        partner_runs(L, cx, true, prod, run_lo, run_hi, s);
     }
     check_launch();
     Ctl h = read_ctl(ctl, s);
@@ -369,8 +364,7 @@ void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, sps
         ha.heavy_count = &ctl->heavy_count;
         ha.heavy_max = nheavy;
         ha.row_nnz = heavy_nnz;
-        ha.run_lo = run_lo;
-        ha.run_hi = run_hi;
+        ha.run = run;
         ha.runs_ready = true;
         ha.cursor = ar.get_t<uint32_t>(L.nnz);
         Phase ph(SPSYRK_PHASE_HEAVY_SYMBOLIC, s);
@@ -398,8 +392,7 @@ void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, sps
     fa.lower = true;
     fa.sr = sr;
     fa.prod = prod;
-    fa.run_lo = run_lo;
-    fa.run_hi = run_hi;
+    fa.run = run;
     fa.heavy_nnz = heavy_nnz;
     fa.ubp = ubp;
     fa.row_cnt = row_cnt;
@@ -536,8 +529,7 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     ha.products = &ctl->products;
     ha.row_nnz = c_rp;
     if (nheavy > 0) {
-        ha.run_lo = ar.get_t<uint32_t>(L.nnz);
-        ha.run_hi = ar.get_t<uint32_t>(L.nnz);
+        ha.run = ar.get_t<uint2>(L.nnz);
         ha.cursor = ar.get_t<uint32_t>(L.nnz);
         {
             Phase ph(SPSYRK_PHASE_HEAVY_SYMBOLIC, s);

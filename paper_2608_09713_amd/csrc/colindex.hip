@@ -4,9 +4,9 @@
 // column when only partners with a smaller row are ever needed, and fills the
 // group directory: the first entry of every column that opens a new group
 // writes the directory slots of the groups between the previous column's
-// group and its own.  In lower mode it also adds every entry's rank inside
-// its column (the number of partners j < i it has) to its row's product
-// count, so that the rows can be classified before any row is processed.
+// group and its own.  In lower mode it also writes every entry's partner run
+// (the entries of its column with a smaller row, which open the column) at
+// the entry's index, so the rows never search the index.
 #include "common.h"
 #include "internal.h"
 
@@ -24,19 +24,19 @@ __global__ __launch_bounds__(kBlock) void start_flags(const uint32_t* __restrict
 
 template <int VB, bool JAC>
 __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol, const uint32_t* __restrict__ srow,
-                                               const void* __restrict__ sval, int64_t n,
-                                               const uint32_t* __restrict__ excl, bool drop_last, int gs, int rowbits,
-                                               int64_t ngroups, const int64_t* __restrict__ nkept,
-                                               const int64_t* __restrict__ rp_b,
+                                               const uint32_t* __restrict__ sent, const void* __restrict__ vals_b,
+                                               uint2* __restrict__ run, int64_t n, const uint32_t* __restrict__ excl,
+                                               bool drop_last, int gs, int rowbits, int lenbits, int64_t ngroups,
+                                               const int64_t* __restrict__ nkept, const int64_t* __restrict__ rp_b,
                                                uint32_t* __restrict__ key, void* __restrict__ val,
-                                               uint32_t* __restrict__ gptr, unsigned long long* __restrict__ prod) {
+                                               uint32_t* __restrict__ gptr) {
     __shared__ int64_t colstart[kPTile];
     __shared__ int64_t wt[kWavesPerBlock];
     __shared__ int64_t carry_s;
     const int64_t base = int64_t(blockIdx.x) * kPTile;
     const int64_t end = min(n, base + kPTile);
     // column start of the tile's first position (its column may begin in an earlier tile)
-    if (threadIdx.x == 0 && prod) {
+    if (threadIdx.x == 0 && run) {
         const uint32_t c0 = scol[base];
         int64_t lo = 0, hi = base;
         while (lo < hi) {
@@ -48,7 +48,7 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
         }
         carry_s = lo;
     }
-    if (prod) {
+    if (run) {
         // inclusive max-scan of "position if it starts a column" over the tile
         constexpr int kPer = kPTile / kBlock;
         int64_t v[kPer];
@@ -56,9 +56,9 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
             const int64_t p = base + int64_t(threadIdx.x) * kPer + k;
-            int64_t s = -1;
-            if (p < end && (p == 0 || scol[p] != scol[p - 1])) s = p;
-            mx = s > mx ? s : mx;
+            int64_t st = -1;
+            if (p < end && (p == 0 || scol[p] != scol[p - 1])) st = p;
+            mx = st > mx ? st : mx;
             v[k] = mx;
         }
         // exclusive max over the preceding threads
@@ -83,16 +83,23 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
         __syncthreads();
     }
     const uint32_t gmask = (gs >= 32) ? 0xffffffffu : ((1u << gs) - 1u);
+    const uint32_t rowmask = rowbits >= 32 ? 0xffffffffu : ((1u << rowbits) - 1u);
+    const uint32_t lmax = lenbits > 0 ? (1u << lenbits) - 1u : 0u;
     for (int64_t p = base + threadIdx.x; p < end; p += kBlock) {
         const uint32_t col = scol[p];
         const bool start = p == 0 || scol[p - 1] != col;
         const bool last = p == n - 1 || scol[p + 1] != col;
-        const uint32_t row = srow[p];
+        const uint32_t field = srow[p];
+        const uint32_t row = field & rowmask;
         // kept entries before p: every column entirely before p lost its last entry
         const int64_t cols_before = int64_t(excl[p]) + (start ? 1 : 0) - 1;
-        if (prod) {
+        if (run) {
+            // partners of this entry (j < row): the kept entries that open its column
             const int64_t rank = p - colstart[p - base];
-            if (rank > 0) atomicAdd(&prod[row], (unsigned long long)rank);
+            if (rank > 0) {
+                const int64_t first_kept = drop_last ? colstart[p - base] - cols_before : colstart[p - base];
+                run[sent[p]] = make_uint2(uint32_t(first_kept), uint32_t(first_kept + rank));
+            }
         }
         if (start) {
             // directory slots of the groups opened by this column
@@ -112,11 +119,12 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
         }
         key[q] = ((col & gmask) << rowbits) | row;
         if constexpr (JAC) {
-            static_cast<int32_t*>(val)[q] = int32_t(rp_b[row + 1] - rp_b[row]);
+            const uint32_t lf = lenbits > 0 ? field >> rowbits : lmax;
+            static_cast<int32_t*>(val)[q] = lf < lmax ? int32_t(lf) : int32_t(rp_b[row + 1] - rp_b[row]);
         } else if constexpr (VB == 8) {
-            static_cast<uint64_t*>(val)[q] = static_cast<const uint64_t*>(sval)[p];
+            static_cast<uint64_t*>(val)[q] = static_cast<const uint64_t*>(vals_b)[sent[p]];
         } else if constexpr (VB == 4) {
-            static_cast<uint32_t*>(val)[q] = static_cast<const uint32_t*>(sval)[p];
+            static_cast<uint32_t*>(val)[q] = static_cast<const uint32_t*>(vals_b)[sent[p]];
         }
     }
 }
@@ -136,9 +144,9 @@ size_t colindex_tmp_bytes(int64_t n) {
     return ((size_t(n) * 4 + 255) & ~size_t(255)) + 256 + scan_tmp_bytes(n);
 }
 
-void build_colindex(const uint32_t* scol, const uint32_t* srow, const void* sval, int64_t n_entries, bool drop_last,
-                    int vbytes_in, int sr, const int64_t* rp_b, ColIndex& cx, void* tmp, int64_t* d_nkept,
-                    unsigned long long* prod, hipStream_t s) {
+void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries, bool drop_last,
+                    int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits, ColIndex& cx, void* tmp,
+                    int64_t* d_nkept, uint2* run, hipStream_t s) {
     uint32_t* excl = static_cast<uint32_t*>(tmp);
     char* after = static_cast<char*>(tmp) + ((size_t(n_entries) * 4 + 255) & ~size_t(255));
     uint32_t* ncols = reinterpret_cast<uint32_t*>(after);
@@ -156,19 +164,18 @@ void build_colindex(const uint32_t* scol, const uint32_t* srow, const void* sval
     // the number of distinct columns fixes the kept count and the directory's end
     kept_count<<<1, 1, 0, s>>>(n, ncols, drop_last, d_nkept);
     const unsigned np = unsigned((n + kPTile - 1) / kPTile);
-    const bool jac = sr == kJaccard;
-    if (jac)
-        pack<0, true><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
-                                            d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+#define SPSYRK_PACK(VBv, JACv)                                                                                    \
+    pack<VBv, JACv><<<np, kBlock, 0, s>>>(scol, srow, sent, vals_b, run, n, excl, drop_last, cx.gs, cx.rowbits,   \
+                                          lenbits, cx.ngroups, d_nkept, rp_b, cx.key, cx.val, cx.gptr)
+    if (sr == kJaccard)
+        SPSYRK_PACK(0, true);
     else if (vbytes_in == 8)
-        pack<8, false><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
-                                             d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+        SPSYRK_PACK(8, false);
     else if (vbytes_in == 4)
-        pack<4, false><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
-                                             d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+        SPSYRK_PACK(4, false);
     else
-        pack<0, false><<<np, kBlock, 0, s>>>(scol, srow, sval, n, excl, drop_last, cx.gs, cx.rowbits, cx.ngroups,
-                                             d_nkept, rp_b, cx.key, cx.val, cx.gptr, prod);
+        SPSYRK_PACK(0, false);
+#undef SPSYRK_PACK
 }
 
 }  // namespace spsyrk

@@ -75,11 +75,10 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
             uint32_t st, len;
             if (!NUM && !a.runs_ready) {
                 partner_run(key, a.cx.gptr, a.cx.gs, a.cx.rowbits, uint32_t(a.ci[e]), uint32_t(i), LOWER, st, len);
-                a.run_lo[e] = st;
-                a.run_hi[e] = st + len;
+                a.run[e] = make_uint2(st, st + len);
                 prod_local += len;
             } else {
-                st = a.run_lo[e];
+                st = a.run[e].x;
             }
             a.cursor[e] = st;
         }
@@ -104,14 +103,14 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
                 __syncthreads();
                 for (int64_t e = c0 + tid; e < c1; e += kBlock) {
                     const uint32_t c = a.cursor[e];
-                    if (c < a.run_hi[e] && int64_t(key[c] & rowmask) < W1) act[atomicAdd(&nact_s, 1)] = int32_t(e - e0);
+                    if (c < a.run[e].y && int64_t(key[c] & rowmask) < W1) act[atomicAdd(&nact_s, 1)] = int32_t(e - e0);
                 }
                 __syncthreads();
                 const int nact = nact_s;
                 for (int q = w; q < nact; q += kWavesPerBlock) {
                     const int64_t e = e0 + act[q];
                     uint32_t c = a.cursor[e];
-                    const uint32_t hi = a.run_hi[e];
+                    const uint32_t hi = a.run[e].y;
                     double av = 0.0;
                     if constexpr (kVal && NUM) av = double(static_cast<const In*>(a.val)[e]);
                     while (c < hi) {

@@ -50,29 +50,36 @@ void scan_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* 
 
 // ---- validate.hip
 // ORs ErrBits into *err.  upper_forbidden: also flag entries with col > row.
-void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* row_start_bits, uint32_t* err,
-                  hipStream_t s);
-size_t validate_tmp_bytes(const DevCsr& A);
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, hipStream_t s);
 void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
-// row id of every entry: rows[e] = i for rp[i] <= e < rp[i+1]
-void entry_rows(const DevCsr& A, uint32_t* rows, hipStream_t s);
 
 // ---- radix.hip
 // Stable LSD sort of (key, row, value) records by the low `nbits` of key.
 // Buffers *_a hold the input and the result is returned in the buffer
 // reported by the return value (0 -> *_a, 1 -> *_b).  vbytes in {0, 4, 8}.
 size_t radix_tmp_bytes(int64_t n);
+// Stable sort of the entries of a CSR matrix by column: the records
+// (column, row field, entry index) are formed inside the first pass.  The row
+// field is the row in its low rowbits bits and, if lenbits > 0, the row's
+// length saturated at 2^lenbits - 1 above them.  Returns 0 if the result is in
+// the *_a buffers, 1 for *_b.
+int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
+                   uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
+                   int nbits, void* tmp, hipStream_t s);
 int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a,
                void* val_b, int vbytes, int64_t n, int nbits, void* tmp, hipStream_t s);
 
 // ---- colindex.hip
-// From records sorted by column: keep flags, packing and directory.  With
-// prod non-null (lower mode) every entry's rank in its column is added to
-// prod[row] (the row's off-diagonal product count; prod must start at zero).
+// From the entries of B sorted by column (column, row field as written by
+// radix_sort_csr, entry index): keep flags, packed keys, values gathered by
+// entry index from vals_b (the row length |S(row)| for Jaccard) and the group
+// directory.  With run non-null (lower mode) the partner run {first, end} of
+// every entry with partners is written at its entry index (run must start
+// zeroed: the other entries keep empty runs).
 size_t colindex_tmp_bytes(int64_t n);
-void build_colindex(const uint32_t* scol, const uint32_t* srow, const void* sval, int64_t n_entries,
-                    bool drop_last, int vbytes_in, int sr, const int64_t* rp_b, ColIndex& ci,
-                    void* tmp, int64_t* d_nkept, unsigned long long* prod, hipStream_t s);
+void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries,
+                    bool drop_last, int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits,
+                    ColIndex& ci, void* tmp, int64_t* d_nkept, uint2* run, hipStream_t s);
 
 // ---- light.hip
 struct LightArgs {
@@ -116,8 +123,7 @@ struct FusedArgs {
     bool lower = true;
     int sr = kF64;
     const unsigned long long* prod = nullptr;  // off-diagonal products per row
-    const uint32_t* run_lo = nullptr;          // partner run of every entry (runs kernel)
-    const uint32_t* run_hi = nullptr;
+    const uint2* run = nullptr;                // partner run {first, end} of every entry
     const int64_t* heavy_nnz = nullptr;        // output lengths of heavy rows
     const int64_t* ubp = nullptr;              // staging slot of every row (prefix of upper bounds)
     int64_t* row_cnt = nullptr;                // exact output length of every row
@@ -137,11 +143,10 @@ void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m,
                    hipStream_t s);
 
 // ---- runs.hip
-// Partner run [run_lo[e], run_hi[e]) of every entry of the left operand
-// (entries of rows with no products get an empty run without a lookup when
-// prod is given).
-void partner_runs(const DevCsr& A, const ColIndex& cx, bool lower, const unsigned long long* prod, uint32_t* run_lo,
-                  uint32_t* run_hi, hipStream_t s);
+// prod[i] = sum over the entries e of row i of run[e].y - run[e].x (prod
+// must start zeroed).
+void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, unsigned long long* prod,
+                  hipStream_t s);
 // Copy the staged rows to their final places: the element at staging slot
 // ubp[i] + x (x < row_cnt[i]) goes to c_rp[i] + x.  ubp is non-decreasing
 // with ubp[m] = staged; rows with no staging room (heavy rows) copy nothing.
@@ -163,9 +168,8 @@ struct HeavyArgs {
     const int32_t* heavy_count = nullptr;
     int64_t heavy_max = 0;              // upper bound of heavy rows (grid sizing)
     // per-entry run bounds (sized nnz of the left operand), written by the symbolic pass
-    uint32_t* run_lo = nullptr;
-    uint32_t* run_hi = nullptr;
-    bool runs_ready = false;            // run_lo/run_hi already filled (the symbolic pass skips its lookups)
+    uint2* run = nullptr;               // partner run {first, end} of every entry
+    bool runs_ready = false;            // run already filled (the symbolic pass skips its lookups)
     uint32_t* cursor = nullptr;
     unsigned long long* products = nullptr;  // optional: add the products formed
     int64_t* row_nnz = nullptr;

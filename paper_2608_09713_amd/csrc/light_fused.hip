@@ -4,15 +4,18 @@
 // works alone in its own slice of LDS (no workgroup barriers), in batches of
 // consecutive light rows that fit the LDS budget:
 //
-//   1. partner runs of the batch's entries (found beforehand, read in entry
-//      order);
+//   1. partner runs of the batch's entries (written by the column-index
+//      build, read in entry order; the next batch's runs are loaded while
+//      this batch's keys are in flight);
 //   2. products flattened over the entries (the owner entry of every product
 //      comes from a scatter of run starts and a max-scan), every key loaded
 //      in one round;
-//   3. ordered buckets per row (bucket order = column order): count, scan,
-//      scatter; inside a bucket each product learns whether it is the first of
-//      its column (the leader), the leader's rank among the bucket's distinct
-//      columns, and its column's value (terms summed in product order);
+//   3. ordered buckets per row (bucket order = column order, about one
+//      product per bucket): count, scan, scatter; each small bucket is sorted
+//      by (column, product index) in one lane's registers and its equal
+//      columns merged (terms summed in product order); the rare large bucket
+//      is resolved by the whole wavefront (leader = first product of a
+//      column, its rank among the bucket's distinct columns, its value);
 //   4. the row is written at its staging slot (row upper bound = products +
 //      diagonal, known from the column index), its exact length recorded.
 //
@@ -33,6 +36,12 @@ constexpr int kFR = kFusedRows;      // rows per chunk (upper limit)
 constexpr int kFB = kFP + kFR;       // buckets per batch
 constexpr int kWavesF = 2;           // wavefronts per workgroup
 constexpr int kMaxBatches = kFR;
+constexpr int kRunRegs = kFE / kWave;  // partner runs per lane held in registers
+constexpr int kSmall = 4;              // buckets up to this size are merged in registers
+constexpr int kTBits = 9;              // product index bits in s_t (row above them)
+constexpr uint32_t kTMask = (1u << kTBits) - 1u;
+static_assert(kFP <= (1 << kTBits), "product index must fit kTBits");
+static_assert(kFR <= (1 << (16 - kTBits)), "chunk row must fit above the product index");
 
 
 __device__ inline void wave_sync() {
@@ -71,7 +80,10 @@ struct WaveLds {
     int16_t owner[kFP];
     uint32_t s_j[kFP];
     uint16_t s_t[kFP];
-    uint16_t s_rank[kFP];     // 0xffff marks a product that is not its column's leader
+    uint16_t s_rank[kFP];     // large buckets: rank of a leader, 0xffff for the other products
+    uint16_t big[kFP / (kSmall + 1) + 1];  // large buckets of the batch
+    uint32_t nbig;
+    int64_t rbase[kFR];
     Item s_v[kFP];
     uint32_t hist[kFB + 1];
     uint32_t ucnt[kFB + 1];
@@ -118,31 +130,46 @@ struct Chunk {
         jbits_right = bit_width_u64(a.m_right > 1 ? uint64_t(a.m_right - 1) : 0);
     }
 
-    // Partner runs, buckets, leaders and per-bucket distinct counts for the
-    // light rows [ra, rb).  The batch's products stay in LDS, sorted by
-    // (row, bucket).  If add is set, every row's off-diagonal count is added
-    // to rcnt.  Returns the number of products.
-    __device__ int batch(int ra, int rb, bool add) {
+    // Issue the loads of the partner runs of the light rows [ra, rb) (entry
+    // lane + kWave * u in rn[u]); they are consumed by the batch's first step.
+    __device__ void fetch_runs(int ra, int rb, uint2 (&rn)[kRunRegs]) {
+        const int64_t ebase = L.rp[ra];
+        const int ne = int(L.rp[rb] - ebase);
+#pragma unroll
+        for (int u = 0; u < kRunRegs; ++u) {
+            const int x = lane + u * kWave;
+            rn[u] = x < ne ? a.run[ebase + x] : make_uint2(0u, 0u);
+        }
+    }
+
+    // Partner runs, buckets, merged columns and per-bucket distinct counts
+    // for the light rows [ra, rb), whose runs were fetched into rn.  The
+    // batch's columns stay in LDS, grouped by (row, bucket).  The runs of the
+    // next batch [na, nb) (if na >= 0) are fetched into rn while the batch's
+    // keys are in flight.  Returns the number of buckets.
+    __device__ int batch(int ra, int rb, uint2 (&rn)[kRunRegs], int na, int nbx) {
         const int64_t ebase = L.rp[ra];
         const int ne = int(L.rp[rb] - ebase);
         const uint32_t* __restrict__ key = a.cx.key;
-        // partner runs of the batch's entries, found beforehand (runs kernel)
-        for (int x = lane; x < ne; x += kWave) {
-            const int64_t e = ebase + x;
-            int lo = ra, hi = rb - 1;  // last row of the batch starting at or before e
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (L.rp[mid] <= e)
-                    lo = mid;
-                else
-                    hi = mid - 1;
+#pragma unroll
+        for (int u = 0; u < kRunRegs; ++u) {
+            const int x = lane + u * kWave;
+            if (x < ne) {
+                const int64_t e = ebase + x;
+                int lo = ra, hi = rb - 1;  // last row of the batch starting at or before e
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (L.rp[mid] <= e)
+                        lo = mid;
+                    else
+                        hi = mid - 1;
+                }
+                const uint32_t len = rn[u].y - rn[u].x;
+                L.ent_start[x] = rn[u].x;
+                L.ent_len[x] = uint16_t(len);
+                L.ent_row[x] = uint8_t(lo);
+                L.ent_poff[x] = uint16_t(len);
             }
-            const uint32_t st = a.run_lo[e];
-            const uint32_t len = a.run_hi[e] - st;
-            L.ent_start[x] = st;
-            L.ent_len[x] = uint16_t(len);
-            L.ent_row[x] = uint8_t(lo);
-            L.ent_poff[x] = uint16_t(len);
         }
         wave_sync();
         const int P = int(wave_scan_lds(L.ent_poff, ne));
@@ -215,6 +242,7 @@ struct Chunk {
                 pb[v] = uint32_t(L.ent_row[x]);
             }
         }
+        if (na >= 0) fetch_runs(na, nbx, rn);
 #pragma unroll
         for (int v = 0; v < kPV; ++v) {
             const int t = lane + v * kWave;
@@ -222,110 +250,190 @@ struct Chunk {
                 const uint32_t j = pj[v] & rowmask;
                 const int r = int(pb[v]);
                 pj[v] = j;
-                pb[v] = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
-                atomicAdd(&L.hist[pb[v]], 1u);
+                const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
+                pb[v] = b | (uint32_t(r) << 16);
+                atomicAdd(&L.hist[b], 1u);
             }
         }
         wave_sync();
         wave_scan_lds(L.hist, int(B));
-        // scatter into buckets; hist[b] ends as the end of bucket b
+        // scatter into buckets; hist[b] ends as the end of bucket b.  s_t keeps
+        // the product index and, above it, the row (one row per bucket)
 #pragma unroll
         for (int v = 0; v < kPV; ++v) {
             const int t = lane + v * kWave;
             if (t < P) {
-                const uint32_t q = atomicAdd(&L.hist[pb[v]], 1u);
+                const uint32_t q = atomicAdd(&L.hist[pb[v] & 0xffffu], 1u);
                 L.s_j[q] = pj[v];
-                L.s_t[q] = uint16_t(t);
+                L.s_t[q] = uint16_t(uint32_t(t) | ((pb[v] >> 16) << kTBits));
                 if constexpr (SR == kJaccard || kVal) L.s_v[q] = pv[v];
             }
         }
+        if (lane == 0) L.nbig = 0;
         wave_sync();
-        // leaders: the first product (in product order) of each column
-        for (int q = lane; q < P; q += kWave) {
-            const uint32_t j = L.s_j[q];
-            const uint32_t t = L.s_t[q];
-            const int r = L.ent_row[L.owner[t]];
-            const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
+        // small buckets (up to kSmall products), one per lane: sorted by
+        // (column, product index) in registers, equal columns merged (terms
+        // summed in product order), the distinct columns written back in order
+        // at the bucket's start; ucnt[b] = distinct columns.  Larger buckets
+        // are listed for the cooperative pass below.
+        for (uint32_t b = lane; b < B; b += kWave) {
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            bool lead = true;
-            if (hi - lo > 1)
-                for (uint32_t u = lo; u < hi; ++u)
-                    if (L.s_j[u] == j && L.s_t[u] < t) lead = false;
-            L.s_rank[q] = lead ? 0 : 0xffff;
-        }
-        wave_sync();
-        // rank among the bucket's distinct columns, and the column's value
-        for (int q = lane; q < P; q += kWave) {
-            if (L.s_rank[q] == 0xffff) continue;
-            const uint32_t j = L.s_j[q];
-            const uint32_t t = L.s_t[q];
-            const int r = L.ent_row[L.owner[t]];
-            const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
-            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            uint32_t rank = 0, cnt = 1;
-            if (hi - lo > 1) {
-                cnt = 0;
-                for (uint32_t u = lo; u < hi; ++u) {
-                    const uint32_t ju = L.s_j[u];
-                    rank += (ju < j && L.s_rank[u] != 0xffff) ? 1u : 0u;
-                    cnt += ju == j ? 1u : 0u;
+            const uint32_t sz = hi - lo;
+            uint32_t d = sz;
+            if (sz > uint32_t(kSmall)) {
+                L.big[atomicAdd(&L.nbig, 1u)] = uint16_t(b);
+                d = 0;
+            } else if (sz > 0) {
+                uint64_t k[kSmall];
+                Item v[kSmall];
+#pragma unroll
+                for (int u = 0; u < kSmall; ++u) {
+                    const bool in = uint32_t(u) < sz;
+                    k[u] = in ? ((uint64_t(L.s_j[lo + u]) << 16) | L.s_t[lo + u]) : ~uint64_t(0);
+                    v[u] = in ? L.s_v[lo + u] : Item(0);
                 }
-            }
-            if constexpr (kVal) {
-                double sum = L.s_v[q];
-                uint32_t last = t;
-                for (uint32_t c = 1; c < cnt; ++c) {
-                    uint32_t best = 0xffffffffu, bu = q;
-                    for (uint32_t u = lo; u < hi; ++u) {
-                        const uint32_t tu = L.s_t[u];
-                        if (L.s_j[u] == j && tu > last && tu < best) {
-                            best = tu;
-                            bu = u;
+                cswap(k, v, 0, 1);
+                cswap(k, v, 2, 3);
+                cswap(k, v, 0, 2);
+                cswap(k, v, 1, 3);
+                cswap(k, v, 1, 2);
+                const int r = int((k[0] & 0xffffu) >> kTBits);
+                const int64_t len_i = L.rp[r + 1] - L.rp[r];
+                d = 0;
+                uint32_t gj = uint32_t(k[0] >> 16);
+                Item acc = v[0];
+                int32_t cnt = 1;
+#pragma unroll
+                for (int u = 1; u <= kSmall; ++u) {
+                    const bool in = uint32_t(u) < sz;
+                    const uint32_t j = in ? uint32_t(k[u < kSmall ? u : 0] >> 16) : 0u;
+                    if (in && j == gj) {
+                        ++cnt;
+                        if constexpr (kVal) acc += v[u < kSmall ? u : 0];
+                    } else if (uint32_t(u) <= sz) {
+                        // the group of gj ends: emit it
+                        L.s_j[lo + d] = gj;
+                        L.s_v[lo + d] = finish(acc, cnt, len_i);
+                        ++d;
+                        if (in) {
+                            gj = j;
+                            acc = v[u < kSmall ? u : 0];
+                            cnt = 1;
                         }
                     }
-                    sum += L.s_v[bu];
-                    last = best;
                 }
-                L.s_v[q] = sum;
-            } else if constexpr (SR == kCount) {
-                L.s_v[q] = int32_t(cnt);
-            } else {
-                const int64_t len_i = L.rp[r + 1] - L.rp[r];
-                L.s_v[q] = __float_as_int(jaccard(int32_t(cnt), len_i, L.s_v[q]));
             }
-            atomicAdd(&L.ucnt[b], 1u);
-            L.s_rank[q] = uint16_t(rank);
+            L.ucnt[b] = d;
         }
         wave_sync();
+        // larger buckets, one at a time by the whole wavefront: leaders (first
+        // product of each column), their rank among the bucket's distinct
+        // columns and their column's value; ucnt[b] = leaders
+        const int nbig = int(L.nbig);
+        for (int g = 0; g < nbig; ++g) {
+            const uint32_t b = L.big[g];
+            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
+            for (uint32_t q = lo + lane; q < hi; q += kWave) {
+                const uint32_t j = L.s_j[q];
+                const uint32_t t = L.s_t[q] & kTMask;
+                bool lead = true;
+                for (uint32_t u = lo; u < hi; ++u)
+                    if (L.s_j[u] == j && (L.s_t[u] & kTMask) < t) lead = false;
+                L.s_rank[q] = lead ? 0 : 0xffff;
+            }
+            wave_sync();
+            uint32_t leaders = 0;
+            for (uint32_t q0 = lo; q0 < hi; q0 += kWave) {
+                const uint32_t q = q0 + lane;
+                bool lead = false;
+                Item val = Item(0);
+                uint32_t rank = 0;
+                if (q < hi && L.s_rank[q] == 0) {
+                    lead = true;
+                    const uint32_t j = L.s_j[q];
+                    const uint32_t t = L.s_t[q] & kTMask;
+                    const int r = int(L.s_t[q] >> kTBits);
+                    int32_t cnt = 0;
+                    for (uint32_t u = lo; u < hi; ++u) {
+                        const uint32_t ju = L.s_j[u];
+                        rank += (ju < j && L.s_rank[u] != 0xffff) ? 1u : 0u;
+                        cnt += ju == j ? 1 : 0;
+                    }
+                    Item acc = L.s_v[q];
+                    if constexpr (kVal) {
+                        // terms of column j in product order
+                        uint32_t last = t;
+                        for (int c = 1; c < cnt; ++c) {
+                            uint32_t best = 0xffffffffu, bu = q;
+                            for (uint32_t u = lo; u < hi; ++u) {
+                                const uint32_t tu = L.s_t[u] & kTMask;
+                                if (L.s_j[u] == j && tu > last && tu < best) {
+                                    best = tu;
+                                    bu = u;
+                                }
+                            }
+                            acc += L.s_v[bu];
+                            last = best;
+                        }
+                    }
+                    val = finish(acc, cnt, L.rp[r + 1] - L.rp[r]);
+                }
+                leaders += uint32_t(__popcll(__ballot(lead)));
+                wave_sync();
+                if (lead) {
+                    L.s_v[q] = val;
+                    L.s_rank[q] = uint16_t(rank);
+                }
+            }
+            if (lane == 0) L.ucnt[b] = leaders;
+            wave_sync();
+        }
         const uint32_t U = wave_scan_lds(L.ucnt, int(B));
         if (lane == 0) L.ucnt[B] = U;
         wave_sync();
-        if (add && lane < nrb) {
-            const int r = ra + lane;
-            L.rcnt[r] += int64_t(L.ucnt[L.rbb[r] + L.rnb[r]] - L.ucnt[L.rbb[r]]);
-        }
+        // first output slot of every row minus its first bucket's offset
+        if (lane < nrb) L.rbase[ra + lane] = L.rcnt[ra + lane] - int64_t(L.ucnt[L.rbb[ra + lane]]);
         wave_sync();
-        return P;
+        return int(B);
+    }
+
+    // value of a merged column: the sum (plus-times), the count, or the
+    // Jaccard bits from the count and the two row lengths
+    __device__ static Item finish(Item acc, int32_t cnt, int64_t len_i) {
+        if constexpr (kVal)
+            return acc;
+        else if constexpr (SR == kCount)
+            return cnt;
+        else
+            return __float_as_int(jaccard(cnt, len_i, acc));
+    }
+
+    __device__ static void cswap(uint64_t (&k)[kSmall], Item (&v)[kSmall], int x, int y) {
+        const bool sw = k[y] < k[x];
+        const uint64_t kx = sw ? k[y] : k[x], ky = sw ? k[x] : k[y];
+        const Item vx = sw ? v[y] : v[x], vy = sw ? v[x] : v[y];
+        k[x] = kx;
+        k[y] = ky;
+        v[x] = vx;
+        v[y] = vy;
     }
 
     // Write the batch left in LDS by batch(ra, rb, ...): rcnt holds each row's
-    // first output slot.
-    __device__ void write(int ra, int rb, int P) {
-        for (int q = lane; q < P; q += kWave) {
-            if (L.s_rank[q] == 0xffff) continue;
-            const uint32_t j = L.s_j[q];
-            const int r = L.ent_row[L.owner[L.s_t[q]]];
-            const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
-            const int64_t p = L.rcnt[r] + int64_t(L.ucnt[b] - L.ucnt[L.rbb[r]]) + L.s_rank[q];
-            a.c_ci[p] = int32_t(j);
-            Out ov;
-            if constexpr (kVal)
-                ov = Out(L.s_v[q]);
-            else if constexpr (SR == kCount)
-                ov = L.s_v[q];
-            else
-                ov = __int_as_float(L.s_v[q]);
-            static_cast<Out*>(a.c_val)[p] = ov;
+    // first output slot, rbase that slot minus the offset of the row's first
+    // bucket.
+    __device__ void write(int ra, int rb, int B) {
+        for (int b = lane; b < B; b += kWave) {
+            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
+            if (hi == lo) continue;
+            const int r = int(L.s_t[lo] >> kTBits);
+            const int64_t base = L.rbase[r] + int64_t(L.ucnt[b]);
+            if (hi - lo <= uint32_t(kSmall)) {
+                const uint32_t d = L.ucnt[b + 1] - L.ucnt[b];
+                for (uint32_t k = 0; k < d; ++k) emit(base + k, L.s_j[lo + k], L.s_v[lo + k]);
+            } else {
+                for (uint32_t u = lo; u < hi; ++u)
+                    if (L.s_rank[u] != 0xffff) emit(base + L.s_rank[u], L.s_j[u], L.s_v[u]);
+            }
         }
         // diagonals (lower triangle): the last entry of every non-empty row
         if (LOWER && lane < rb - ra) {
@@ -353,19 +461,41 @@ struct Chunk {
         wave_sync();
     }
 
+    __device__ void emit(int64_t p, uint32_t j, Item v) {
+        a.c_ci[p] = int32_t(j);
+        Out ov;
+        if constexpr (kVal)
+            ov = Out(v);
+        else if constexpr (SR == kCount)
+            ov = v;
+        else
+            ov = __int_as_float(v);
+        static_cast<Out*>(a.c_val)[p] = ov;
+    }
+
     __device__ void run(int64_t c) {
         const int R = a.rows_per_chunk;
         r0 = c * R;
         const int nr = int(min(int64_t(R), a.m - r0));
-        if (lane <= nr) L.rp[lane] = a.rp[r0 + lane];
-        wave_sync();
+        // the chunk's row pointers, product counts and staging slots in one round
+        int64_t rpv = 0, ubv = 0;
+        uint64_t pr = 0;
+        if (lane <= nr) rpv = a.rp[r0 + lane];
         if (lane < nr) {
-            const int64_t len = L.rp[lane + 1] - L.rp[lane];
-            const uint64_t pr = a.prod[r0 + lane];
-            const bool light = pr <= uint64_t(kFP) && len <= kFE;
+            pr = a.prod[r0 + lane];
+            ubv = a.ubp[r0 + lane];
+        }
+        if (lane <= nr) L.rp[lane] = rpv;
+        wave_sync();
+        int64_t len = 0;
+        bool light = false;
+        if (lane < nr) {
+            len = L.rp[lane + 1] - rpv;
+            light = pr <= uint64_t(kFP) && len <= kFE;
             L.rlight[lane] = light ? 1 : 0;
             L.rprod[lane] = light ? uint16_t(pr) : 0;
-            L.rcnt[lane] = light ? ((LOWER && len > 0) ? 1 : 0) : a.heavy_nnz[r0 + lane];
+            // light rows are written at their upper-bound slots (products + diagonal)
+            L.rcnt[lane] = ubv;
         }
         wave_sync();
         // batches of consecutive light rows (same decision in every lane)
@@ -394,17 +524,17 @@ struct Chunk {
             }
         }
         wave_sync();
-        // light rows are written at their upper-bound slots (products + diagonal)
-        if (lane < nr) L.rcnt[lane] = a.ubp[r0 + lane];
-        wave_sync();
         int64_t cnt = 0;  // exact length of this lane's row
-        if (lane < nr) cnt = L.rlight[lane] ? ((LOWER && L.rp[lane + 1] > L.rp[lane]) ? 1 : 0) : a.heavy_nnz[r0 + lane];
+        if (lane < nr) cnt = light ? ((LOWER && len > 0) ? 1 : 0) : a.heavy_nnz[r0 + lane];
+        uint2 rn[kRunRegs];
+        if (nbatch > 0) fetch_runs(L.bra[0], L.brb[0], rn);
         for (int k = 0; k < nbatch; ++k) {
             const int ra = L.bra[k], rb = L.brb[k];
-            const int P = batch(ra, rb, false);
+            const bool more = k + 1 < nbatch;
+            const int B = batch(ra, rb, rn, more ? int(L.bra[k + 1]) : -1, more ? int(L.brb[k + 1]) : 0);
             if (lane >= ra && lane < rb)
                 cnt += int64_t(L.ucnt[L.rbb[lane] + L.rnb[lane]] - L.ucnt[L.rbb[lane]]);
-            write(ra, rb, P);
+            write(ra, rb, B);
         }
         if (lane < nr) a.row_cnt[r0 + lane] = cnt;
     }

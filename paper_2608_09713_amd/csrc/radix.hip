@@ -44,15 +44,35 @@ __global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict_
     hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-template <int VB>
+constexpr int kRowWin = 1024;
+
+__device__ inline int64_t last_leq_i64(const int64_t* a, int64_t lo, int64_t hi, int64_t x) {
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (a[mid] <= x)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    return lo;
+}
+
+// FIRST: the records come straight from a CSR matrix: key = column, row from
+// the row pointers (rp, m), value = the entry's index (VB must be 4).  With
+// lenbits > 0 the row field also carries the row's length, saturated at
+// 2^lenbits - 1, above its low rowbits bits.
+template <int VB, bool FIRST>
 __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restrict__ key_in,
                                                         const uint32_t* __restrict__ row_in,
                                                         const typename ValT<VB>::T* __restrict__ val_in,
                                                         uint32_t* __restrict__ key_out, uint32_t* __restrict__ row_out,
                                                         typename ValT<VB>::T* __restrict__ val_out, int64_t n, int shift,
                                                         uint32_t mask, const uint32_t* __restrict__ offs,
-                                                        int64_t ntiles) {
+                                                        int64_t ntiles, const int64_t* __restrict__ rp, int64_t m,
+                                                        int rowbits, int lenbits) {
     using V = typename ValT<VB>::T;
+    __shared__ int64_t rwin[FIRST ? kRowWin + 1 : 1];
+    __shared__ int64_t rbounds[2];
     __shared__ uint32_t wcnt[kWavesPerBlock][kDigits];
     __shared__ uint32_t tstart[kDigits];
     __shared__ uint32_t wt[kWavesPerBlock];
@@ -68,6 +88,21 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 
     const int64_t base = int64_t(blockIdx.x) * kRTile;
     const int64_t segbase = base + int64_t(w) * kSeg;
+    int64_t rlo = 0, rhi = 0;
+    bool rstaged = false;
+    if constexpr (FIRST) {
+        if (threadIdx.x == 0) {
+            rbounds[0] = last_leq_i64(rp, 0, m, base);
+            rbounds[1] = last_leq_i64(rp, 0, m, min(n, base + kRTile) - 1);
+        }
+        __syncthreads();
+        rlo = rbounds[0];
+        rhi = rbounds[1];
+        rstaged = rhi - rlo + 2 <= kRowWin + 1;
+        if (rstaged)
+            for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) rwin[k] = rp[rlo + k];
+        __syncthreads();
+    }
     uint32_t kr[kRItems], rr[kRItems], loc[kRItems];
     V vr[kRItems];
     const uint64_t lt = lanemask_lt();
@@ -90,8 +125,30 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         loc[k] = cur + rank;
         if (valid && rank == 0) wcnt[w][d] = cur + uint32_t(__popcll(peers));
         kr[k] = key;
-        rr[k] = valid ? row_in[idx] : 0u;
-        if constexpr (VB != 0) vr[k] = valid ? val_in[idx] : V(0);
+        if constexpr (FIRST) {
+            uint32_t field = 0;
+            if (valid) {
+                int64_t r, len;
+                if (rstaged) {
+                    const int64_t rl = last_leq_i64(rwin, 0, rhi - rlo, idx);
+                    r = rlo + rl;
+                    len = rwin[rl + 1] - rwin[rl];
+                } else {
+                    r = last_leq_i64(rp, rlo, rhi, idx);
+                    len = rp[r + 1] - rp[r];
+                }
+                field = uint32_t(r);
+                if (lenbits > 0) {
+                    const int64_t lmax = (int64_t(1) << lenbits) - 1;
+                    field |= uint32_t(len < lmax ? len : lmax) << rowbits;
+                }
+            }
+            rr[k] = field;
+            vr[k] = V(idx);
+        } else {
+            rr[k] = valid ? row_in[idx] : 0u;
+            if constexpr (VB != 0) vr[k] = valid ? val_in[idx] : V(0);
+        }
     }
     __syncthreads();
     {
@@ -136,15 +193,16 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     }
 }
 
-template <int VB>
+template <int VB, bool FIRST = false>
 void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
-              int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s) {
+              int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s, const int64_t* rp = nullptr,
+              int64_t m = 0, int rowbits = 0, int lenbits = 0) {
     using V = typename ValT<VB>::T;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
     scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
-    radix_scatter<VB><<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(
-        ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles);
+    radix_scatter<VB, FIRST><<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(
+        ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, rowbits, lenbits);
 }
 
 }  // namespace
@@ -153,6 +211,34 @@ size_t radix_tmp_bytes(int64_t n) {
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     const size_t hist = size_t(ntiles) * kDigits * sizeof(uint32_t);
     return ((hist + 255) & ~size_t(255)) + scan_tmp_bytes(ntiles * kDigits);
+}
+
+int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
+                   uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
+                   int nbits, void* tmp, hipStream_t s) {
+    if (n <= 0) return 0;
+    const int64_t ntiles = (n + kRTile - 1) / kRTile;
+    uint32_t* hist = static_cast<uint32_t*>(tmp);
+    const size_t hist_bytes = (size_t(ntiles) * kDigits * sizeof(uint32_t) + 255) & ~size_t(255);
+    void* scan_tmp = static_cast<char*>(tmp) + hist_bytes;
+    // first pass straight from the CSR arrays (into the b buffers), at least one pass
+    const int bits0 = nbits < kRBits ? nbits : kRBits;
+    run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, 0,
+                      (1u << bits0) - 1u, hist, scan_tmp, s, rp, m, rowbits, lenbits);
+    int cur = 1;
+    for (int shift = kRBits; shift < nbits; shift += kRBits) {
+        const int bits = nbits - shift < kRBits ? nbits - shift : kRBits;
+        const uint32_t mask = (1u << bits) - 1u;
+        uint32_t* ki = cur ? key_b : key_a;
+        uint32_t* ko = cur ? key_a : key_b;
+        uint32_t* ri = cur ? row_b : row_a;
+        uint32_t* ro = cur ? row_a : row_b;
+        uint32_t* vi = cur ? ent_b : ent_a;
+        uint32_t* vo = cur ? ent_a : ent_b;
+        run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+        cur ^= 1;
+    }
+    return cur;
 }
 
 int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a, void* val_b,

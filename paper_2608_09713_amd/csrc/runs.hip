@@ -1,13 +1,7 @@
-// Partner runs of all entries, and the compaction of staged light rows.
-//
-// The runs kernel is the memory-latency-bound half of the light path: one
-// thread per entry, no LDS beyond a window of row pointers, so many
-// wavefronts keep their directory and key loads in flight together.  Its
-// output (two words per entry) is read back in entry order by the light-row
-// kernel.
+// Per-row product counts from the partner runs, and the compaction of the
+// staged light rows into the final CSR arrays.
 #include "common.h"
 #include "internal.h"
-#include "lookup.h"
 
 namespace spsyrk {
 namespace {
@@ -27,59 +21,96 @@ __device__ inline int64_t last_leq(const int64_t* a, int64_t lo, int64_t hi, int
     return lo;
 }
 
-template <bool LOWER>
-__global__ __launch_bounds__(kBlock) void runs_kernel(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
-                                                      int64_t m, int64_t nnz, const uint32_t* __restrict__ key,
-                                                      const uint32_t* __restrict__ gptr, int gs, int rowbits,
-                                                      const unsigned long long* __restrict__ prod,
-                                                      uint32_t* __restrict__ run_lo, uint32_t* __restrict__ run_hi) {
-    __shared__ int64_t win[kWin + 1];
+// prod[i] = sum of the run lengths of row i's entries.  Every thread walks a
+// contiguous stretch of kPerT entries of the workgroup's tile, adding up the
+// lengths row by row.  A row that lies inside the stretch is stored at once;
+// the partial sums of rows cut by a stretch's ends meet in LDS, and a row cut
+// by the tile's ends is added atomically (prod starts at zero).
+constexpr int kPerT = 8;
+constexpr int kTileP = kBlock * kPerT;
+constexpr int kWinP = 1024;
+
+__global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
+                                                         const uint2* __restrict__ run,
+                                                         unsigned long long* __restrict__ prod) {
+    __shared__ int64_t win[kWinP + 1];
+    __shared__ unsigned long long part[kWinP];
+    __shared__ uint32_t cut[kWinP];
     __shared__ int64_t bounds[2];
-    const int64_t e0 = int64_t(blockIdx.x) * kTileE;
-    const int64_t e1 = min(nnz, e0 + kTileE);
+    const int64_t e0 = int64_t(blockIdx.x) * kTileP;
+    const int64_t e1 = min(nnz, e0 + kTileP);
     if (threadIdx.x == 0) {
         bounds[0] = last_leq(rp, 0, m, e0);
         bounds[1] = last_leq(rp, 0, m, e1 - 1);
     }
     __syncthreads();
     const int64_t rlo = bounds[0], rhi = bounds[1];
-    const bool staged = rhi - rlo + 2 <= kWin + 1;
+    const int64_t nrw = rhi - rlo + 1;
+    const bool staged = nrw <= kWinP;
     if (staged)
-        for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) win[k] = rp[rlo + k];
-    __syncthreads();
-    constexpr int kPer = kTileE / kBlock;
-    uint32_t kk[kPer];
-    int64_t row[kPer];
-    bool need[kPer];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        const int64_t e = e0 + u * kBlock + threadIdx.x;
-        need[u] = e < e1;
-        kk[u] = need[u] ? uint32_t(ci[e]) : 0u;
-        int64_t r = 0;
-        if (need[u]) r = staged ? rlo + last_leq(win, 0, rhi - rlo, e) : last_leq(rp, rlo, rhi, e);
-        row[u] = r;
-    }
-    if (prod) {
-#pragma unroll
-        for (int u = 0; u < kPer; ++u)
-            if (need[u] && prod[row[u]] == 0) {
-                need[u] = false;
-                const int64_t e = e0 + u * kBlock + threadIdx.x;
-                run_lo[e] = 0;
-                run_hi[e] = 0;
+        for (int64_t k = threadIdx.x; k <= nrw; k += kBlock) {
+            win[k] = rp[rlo + k];
+            if (k < nrw) {
+                part[k] = 0;
+                cut[k] = 0;
             }
-    }
+        }
+    __syncthreads();
+    const int64_t a = e0 + int64_t(threadIdx.x) * kPerT;
+    const int64_t b = min(e1, a + kPerT);
+    if (a < b) {
+        uint2 rn[kPerT];
 #pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-        if (!need[u]) continue;
-        const int64_t e = e0 + u * kBlock + threadIdx.x;
-        uint32_t st, len;
-        partner_run(key, gptr, gs, rowbits, kk[u], uint32_t(row[u]), LOWER, st, len);
-        run_lo[e] = st;
-        run_hi[e] = st + len;
+        for (int u = 0; u < kPerT; ++u) rn[u] = a + u < b ? run[a + u] : make_uint2(0u, 0u);
+        // row of the stretch's first entry and its bounds
+        int64_t r = staged ? rlo + last_leq(win, 0, rhi - rlo, a) : last_leq(rp, rlo, rhi, a);
+        int64_t rstart = staged ? win[r - rlo] : rp[r];
+        int64_t rend = staged ? win[r - rlo + 1] : rp[r + 1];
+        unsigned long long acc = 0;
+        for (int u = 0; u < kPerT; ++u) {
+            const int64_t e = a + u;
+            if (e >= b) break;
+            if (e >= rend) {
+                // the finished row ends inside the stretch
+                if (rstart >= a) {
+                    prod[r] = acc;
+                } else if (staged) {
+                    atomicAdd(&part[r - rlo], acc);
+                    cut[r - rlo] = 1;
+                } else if (acc) {
+                    atomicAdd(&prod[r], acc);
+                }
+                acc = 0;
+                do {  // the row of e (empty rows keep their zero)
+                    ++r;
+                    rstart = rend;
+                    rend = staged ? win[r - rlo + 1] : rp[r + 1];
+                } while (rend <= e);
+            }
+            acc += rn[u].y - rn[u].x;
+        }
+        if (rstart >= a && rend <= b) {
+            prod[r] = acc;
+        } else if (staged) {
+            atomicAdd(&part[r - rlo], acc);
+            cut[r - rlo] = 1;
+        } else if (acc) {
+            atomicAdd(&prod[r], acc);
+        }
     }
+    __syncthreads();
+    if (staged)
+        for (int64_t k = threadIdx.x; k < nrw; k += kBlock) {
+            if (!cut[k]) continue;
+            if (win[k] >= e0 && win[k + 1] <= e1)
+                prod[rlo + k] = part[k];
+            else if (part[k])
+                atomicAdd(&prod[rlo + k], part[k]);
+        }
 }
+
+constexpr int kCTile = 4096;  // staging slots per compaction workgroup
+constexpr int kCWin = 512;    // rows held in LDS by a compaction workgroup
 
 template <int VB>
 __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t staged, const int64_t* __restrict__ ubp,
@@ -87,25 +118,41 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
                                                          const int64_t* __restrict__ c_rp,
                                                          const int32_t* __restrict__ s_ci, const void* __restrict__ s_val,
                                                          int32_t* __restrict__ c_ci, void* __restrict__ c_val) {
-    __shared__ int64_t win[kWin + 1];
+    __shared__ int64_t wub[kCWin + 1];  // staging slot of the window's rows
+    __shared__ int64_t wend[kCWin];     // end of each row's valid staged entries
+    __shared__ int64_t wdel[kCWin];     // final position minus staging slot
     __shared__ int64_t bounds[2];
-    const int64_t s0 = int64_t(blockIdx.x) * kTileE;
-    const int64_t s1 = min(staged, s0 + kTileE);
+    const int64_t s0 = int64_t(blockIdx.x) * kCTile;
+    const int64_t s1 = min(staged, s0 + kCTile);
     if (threadIdx.x == 0) {
         bounds[0] = last_leq(ubp, 0, m, s0);
         bounds[1] = last_leq(ubp, 0, m, s1 - 1);
     }
     __syncthreads();
     const int64_t rlo = bounds[0], rhi = bounds[1];
-    const bool win_ok = rhi - rlo + 2 <= kWin + 1;
+    const int64_t nrw = rhi - rlo + 1;
+    const bool win_ok = nrw <= kCWin;
     if (win_ok)
-        for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) win[k] = ubp[rlo + k];
+        for (int64_t k = threadIdx.x; k < nrw; k += kBlock) {
+            const int64_t u = ubp[rlo + k];
+            wub[k] = u;
+            wend[k] = u + row_cnt[rlo + k];
+            wdel[k] = c_rp[rlo + k] - u;
+        }
     __syncthreads();
     for (int64_t sl = s0 + threadIdx.x; sl < s1; sl += kBlock) {
-        const int64_t i = win_ok ? rlo + last_leq(win, 0, rhi - rlo, sl) : last_leq(ubp, rlo, rhi, sl);
-        const int64_t off = sl - ubp[i];
-        if (off >= row_cnt[i]) continue;
-        const int64_t p = c_rp[i] + off;
+        int64_t end, del;
+        if (win_ok) {
+            const int64_t k = last_leq(wub, 0, nrw - 1, sl);
+            end = wend[k];
+            del = wdel[k];
+        } else {
+            const int64_t i = last_leq(ubp, rlo, rhi, sl);
+            end = ubp[i] + row_cnt[i];
+            del = c_rp[i] - ubp[i];
+        }
+        if (sl >= end) continue;
+        const int64_t p = sl + del;
         c_ci[p] = s_ci[sl];
         if constexpr (VB == 8) static_cast<uint64_t*>(c_val)[p] = static_cast<const uint64_t*>(s_val)[sl];
         if constexpr (VB == 4) static_cast<uint32_t*>(c_val)[p] = static_cast<const uint32_t*>(s_val)[sl];
@@ -114,22 +161,17 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
 
 }  // namespace
 
-void partner_runs(const DevCsr& A, const ColIndex& cx, bool lower, const unsigned long long* prod, uint32_t* run_lo,
-                  uint32_t* run_hi, hipStream_t s) {
-    if (A.nnz <= 0) return;
-    const unsigned nb = unsigned((A.nnz + kTileE - 1) / kTileE);
-    if (lower)
-        runs_kernel<true><<<nb, kBlock, 0, s>>>(A.rp, A.ci, A.m, A.nnz, cx.key, cx.gptr, cx.gs, cx.rowbits, prod,
-                                                run_lo, run_hi);
-    else
-        runs_kernel<false><<<nb, kBlock, 0, s>>>(A.rp, A.ci, A.m, A.nnz, cx.key, cx.gptr, cx.gs, cx.rowbits, prod,
-                                                 run_lo, run_hi);
+void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, unsigned long long* prod,
+                  hipStream_t s) {
+    if (nnz <= 0 || m <= 0) return;
+    const unsigned nb = unsigned((nnz + kTileP - 1) / kTileP);
+    rowprod_kernel<<<nb, kBlock, 0, s>>>(rp, m, nnz, run, prod);
 }
 
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
                   const int32_t* s_ci, const void* s_val, int vbytes, int32_t* c_ci, void* c_val, hipStream_t s) {
     if (staged <= 0 || m <= 0) return;
-    const unsigned nb = unsigned((staged + kTileE - 1) / kTileE);
+    const unsigned nb = unsigned((staged + kCTile - 1) / kCTile);
     if (vbytes == 8)
         compact_kernel<8><<<nb, kBlock, 0, s>>>(m, staged, ubp, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
     else if (vbytes == 4)

@@ -1,65 +1,26 @@
-// Canonical-CSR checks and the entry -> row map.
+// Canonical-CSR checks.
+//
+// One kernel checks both arrays: workgroup b checks the row pointers of rows
+// [b*kTileR, (b+1)*kTileR) and the column ids of entries [b*kTileE,
+// (b+1)*kTileE).  Every thread walks a contiguous stretch of entries row by
+// row, starting from the row of its first entry (searched in an LDS window of
+// the row pointers).  On a malformed row_ptr the searches still stay in bounds (their
+// results are then meaningless, but the row check has raised its flag).
 #include "common.h"
 #include "internal.h"
 
 namespace spsyrk {
 namespace {
 
-// row_ptr[0] == 0, non-decreasing, row_ptr[m] == nnz; marks row starts.
-__global__ __launch_bounds__(kBlock) void check_rows(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
-                                                     uint32_t* __restrict__ start_bits, uint32_t* err) {
-    const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (i > m) return;
-    const int64_t a = rp[i];
-    if (i == 0 && a != 0) atomicOr(err, kErrRowPtr);
-    if (i == m) {
-        if (a != nnz) atomicOr(err, kErrRowPtr);
-        return;
-    }
-    const int64_t b = rp[i + 1];
-    if (b < a || a < 0 || b > nnz) {
-        atomicOr(err, kErrRowPtr);
-        return;
-    }
-    if (b > a) atomicOr(&start_bits[a >> 5], 1u << (a & 31));
-}
-
-// column range, strict increase inside rows, optional col <= row
-__global__ __launch_bounds__(kBlock) void check_cols(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
-                                                     int64_t m, int64_t n, int64_t nnz,
-                                                     const uint32_t* __restrict__ start_bits, bool upper_forbidden,
-                                                     uint32_t* err) {
-    const int64_t e = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (e >= nnz) return;
-    const int32_t c = ci[e];
-    uint32_t bad = 0;
-    if (c < 0 || int64_t(c) >= n) bad |= kErrColRange;
-    const bool is_start = (start_bits[e >> 5] >> (e & 31)) & 1u;
-    if (e > 0 && !is_start && ci[e - 1] >= c) bad |= kErrColOrder;
-    if (upper_forbidden) {
-        // row of e: last i with rp[i] <= e (only needed for this check)
-        int64_t lo = 0, hi = m;
-        while (lo < hi) {
-            int64_t mid = (lo + hi + 1) >> 1;
-            if (rp[mid] <= e)
-                lo = mid;
-            else
-                hi = mid - 1;
-        }
-        if (int64_t(c) > lo) bad |= kErrUpper;
-    }
-    if (bad) atomicOr(err, bad);
-}
-
-// rows[e] for the entries of one tile of kTileE entries; the tile's row_ptr
-// window is staged in LDS when it fits, otherwise rows are searched in place.
-constexpr int kTileE = 4096;
-constexpr int kRowWin = 4096;
+constexpr int kTileR = 4096;  // row pointers per workgroup
+constexpr int kTileE = 4096;  // entries per workgroup
+constexpr int kWinV = 2048;   // rows held in LDS
+constexpr int kPerE = kTileE / kBlock;
 
 __device__ inline int64_t find_row(const int64_t* rp, int64_t lo, int64_t hi, int64_t e) {
-    // largest i in [lo, hi] with rp[i] <= e
+    // largest i in [lo, hi] with rp[i] <= e (for a non-decreasing rp)
     while (lo < hi) {
-        int64_t mid = (lo + hi + 1) >> 1;
+        const int64_t mid = (lo + hi + 1) >> 1;
         if (rp[mid] <= e)
             lo = mid;
         else
@@ -68,36 +29,64 @@ __device__ inline int64_t find_row(const int64_t* rp, int64_t lo, int64_t hi, in
     return lo;
 }
 
-__global__ __launch_bounds__(kBlock) void rows_of_entries(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
-                                                          uint32_t* __restrict__ rows) {
-    __shared__ int64_t win[kRowWin + 1];
-    __shared__ int64_t r_lo_s, r_hi_s;
+__global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
+                                                    int64_t m, int64_t n, int64_t nnz, bool upper_forbidden,
+                                                    uint32_t* err) {
+    __shared__ int64_t win[kWinV + 1];
+    __shared__ int64_t bounds[2];
+    __shared__ uint32_t bad_s;
+    if (threadIdx.x == 0) bad_s = 0;
+    uint32_t bad = 0;
+    // row pointers: rp[0] == 0, non-decreasing, inside [0, nnz], rp[m] == nnz
+    for (int64_t i = int64_t(blockIdx.x) * kTileR + threadIdx.x;
+         i <= m && i < int64_t(blockIdx.x + 1) * kTileR; i += kBlock) {
+        const int64_t a = rp[i];
+        if (a < 0 || a > nnz || (i == 0 && a != 0) || (i == m && a != nnz)) bad |= kErrRowPtr;
+        if (i < m && rp[i + 1] < a) bad |= kErrRowPtr;
+    }
     const int64_t e0 = int64_t(blockIdx.x) * kTileE;
     const int64_t e1 = min(nnz, e0 + kTileE);
-    if (threadIdx.x == 0) {
-        r_lo_s = find_row(rp, 0, m, e0);
-        r_hi_s = find_row(rp, 0, m, e1 - 1);
-    }
-    __syncthreads();
-    const int64_t r_lo = r_lo_s, r_hi = r_hi_s;
-    const int64_t nwin = r_hi - r_lo + 2;  // rp[r_lo .. r_hi + 1]
-    if (nwin <= kRowWin + 1) {
-        for (int64_t k = threadIdx.x; k < nwin; k += kBlock) win[k] = rp[r_lo + k];
-        __syncthreads();
-        for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-            int lo = 0, hi = int(nwin - 2);
-            while (lo < hi) {
-                int mid = (lo + hi + 1) >> 1;
-                if (win[mid] <= e)
-                    lo = mid;
-                else
-                    hi = mid - 1;
-            }
-            rows[e] = uint32_t(r_lo + lo);
+    if (e0 < e1) {
+        if (threadIdx.x == 0) {
+            bounds[0] = find_row(rp, 0, m, e0);
+            bounds[1] = find_row(rp, 0, m, e1 - 1);
         }
-    } else {
-        for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) rows[e] = uint32_t(find_row(rp, r_lo, r_hi, e));
+        __syncthreads();
+        const int64_t rlo = bounds[0], rhi = bounds[1];
+        // (rhi < m always holds for a valid row_ptr; the window reads rp[rhi + 1])
+        const bool staged = rhi >= rlo && rhi < m && rhi - rlo + 2 <= kWinV + 1;
+        if (staged)
+            for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) win[k] = rp[rlo + k];
+        __syncthreads();
+        // every thread walks kPerE contiguous entries, row by row
+        const int64_t ea = e0 + int64_t(threadIdx.x) * kPerE;
+        const int64_t eb = min(e1, ea + kPerE);
+        if (ea < eb) {
+            int64_t r = staged ? rlo + find_row(win, 0, rhi - rlo, ea) : find_row(rp, 0, m, ea);
+            int64_t rend = r < m ? (staged ? win[r - rlo + 1] : rp[r + 1]) : nnz;
+            int32_t prev = ea > 0 ? ci[ea - 1] : -1;
+            bool first = staged ? win[r - rlo] == ea : rp[r] == ea;
+            for (int64_t e = ea; e < eb; ++e) {
+                const int32_t c = ci[e];
+                if (e >= rend) {
+                    // next non-empty row (a malformed row_ptr ends the walk at row m)
+                    while (e >= rend && r < m) {
+                        ++r;
+                        rend = r < m ? (staged && r <= rhi ? win[r - rlo + 1] : rp[r + 1]) : nnz;
+                    }
+                    first = true;
+                }
+                if (c < 0 || int64_t(c) >= n) bad |= kErrColRange;
+                if (!first && prev >= c) bad |= kErrColOrder;
+                if (upper_forbidden && int64_t(c) > r) bad |= kErrUpper;
+                prev = c;
+                first = false;
+            }
+        }
     }
+    if (bad) atomicOr(&bad_s, bad);
+    __syncthreads();
+    if (threadIdx.x == 0 && bad_s) atomicOr(err, bad_s);
 }
 
 __global__ void fill_u32_kernel(uint32_t* p, int64_t n, uint32_t v) {
@@ -108,8 +97,6 @@ __global__ void fill_u32_kernel(uint32_t* p, int64_t n, uint32_t v) {
 
 }  // namespace
 
-size_t validate_tmp_bytes(const DevCsr& A) { return size_t((A.nnz + 31) / 32 + 1) * sizeof(uint32_t); }
-
 void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
     if (n <= 0) return;
     int64_t blocks = (n + kBlock - 1) / kBlock;
@@ -117,21 +104,11 @@ void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
     fill_u32_kernel<<<dim3(unsigned(blocks)), dim3(kBlock), 0, s>>>(p, n, v);
 }
 
-void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* start_bits, uint32_t* err, hipStream_t s) {
-    fill_u32(start_bits, (A.nnz + 31) / 32 + 1, 0u, s);
-    const int64_t nb_rows = (A.m + 1 + kBlock - 1) / kBlock;
-    check_rows<<<dim3(unsigned(nb_rows)), dim3(kBlock), 0, s>>>(A.rp, A.m, A.nnz, start_bits, err);
-    if (A.nnz > 0) {
-        const int64_t nb = (A.nnz + kBlock - 1) / kBlock;
-        check_cols<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.ci, A.m, A.n, A.nnz, start_bits,
-                                                              upper_forbidden, err);
-    }
-}
-
-void entry_rows(const DevCsr& A, uint32_t* rows, hipStream_t s) {
-    if (A.nnz <= 0) return;
-    const int64_t nb = (A.nnz + kTileE - 1) / kTileE;
-    rows_of_entries<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.m, A.nnz, rows);
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, hipStream_t s) {
+    const int64_t rb = (A.m + 1 + kTileR - 1) / kTileR;
+    const int64_t eb = (A.nnz + kTileE - 1) / kTileE;
+    const int64_t nb = rb > eb ? rb : eb;
+    check_csr<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.ci, A.m, A.n, A.nnz, upper_forbidden, err);
 }
 
 }  // namespace spsyrk
