@@ -87,15 +87,22 @@ def column_stats(A):
 
 def alg_bytes_phase(phase, sz, sr):
     """Algorithmic bytes of one launch: every array the kernel must touch,
-    counted once."""
+    counted once.
+
+    light_numeric (the single-pass light-row kernel) reads the row pointers,
+    the per-row product counts and staging slots (8 B each per row), the
+    partner run of every entry (8 B), the values of A (fp semirings), every
+    kept column-index key and value once; it writes every output entry
+    (column + value) at its staging slot and the exact row lengths (8 B per
+    row).  compact reads and writes every output entry once plus three 8-B
+    words per row."""
     m, nnz = sz["m"], sz["nnz_A"]
-    a_rows = 8 * (m + 1)
-    a_ent = nnz * (4 + V_IN[sr])
-    cx = sz["csc_entries"] * 4 + 4 * (sz["ngroups"] + 1)
-    if phase == "light_symbolic":
-        return a_rows + nnz * 4 + cx + 8 * m
+    out = sz["nnz_C"] * (4 + V_OUT[sr])
     if phase == "light_numeric":
-        return a_rows + a_ent + cx + sz["csc_entries"] * V_CX[sr] + 8 * (m + 1) + sz["nnz_C"] * (4 + V_OUT[sr])
+        return (8 * (m + 1) + 8 * m + 8 * m + 8 * nnz + nnz * V_IN[sr]
+                + sz["csc_entries"] * (4 + V_CX[sr]) + out + 8 * m)
+    if phase == "compact":
+        return 2 * out + 3 * 8 * m
     return None
 
 
@@ -211,8 +218,8 @@ def main():
     B_alg = whole_call_bytes(sz, sr, mirror_nnz)
 
     # dominant single-kernel phase and its roofline
-    single = {k: v for k, v in phases.items() if k in ("light_symbolic", "light_numeric", "heavy_symbolic",
-                                                       "heavy_numeric")}
+    single = {k: v for k, v in phases.items() if k in ("light_numeric", "heavy_symbolic", "heavy_numeric",
+                                                       "compact")}
     dom = max(single, key=lambda k: single[k][0] / max(1, single[k][1])) if single else None
     roof = None
     if dom is not None:

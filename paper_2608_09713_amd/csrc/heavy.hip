@@ -1,16 +1,19 @@
-// Gustavson accumulation for rows with many products (hub rows of power-law
-// graphs): one workgroup per row, taken from a work queue.  The row's output
-// column range is swept in tiles; a tile is a dense accumulator in LDS (a
-// value per column plus an occupancy byte), so the tile's output comes out in
-// column order with no sort.  Every partner run is sorted by row, so each run
-// is consumed front to back through a per-entry cursor: a tile only touches
-// the runs whose next element falls inside it, and those are read with whole
-// wavefronts over contiguous keys.
+// Gustavson accumulation for rows with many products (rows of power-law
+// graphs that meet hub columns): one workgroup per row, taken from a work
+// queue.
 //
-// The symbolic pass finds the partner runs (kept per entry for the numeric
-// pass) and counts distinct columns per tile with occupancy bytes only; the
-// numeric pass accumulates values with LDS atomics and writes each tile's
-// occupied columns in order.
+// The row's output column range is swept in windows of kWin columns.  In a
+// window the row's distinct columns are first marked in an LDS bitmap; a scan
+// of the words' popcounts gives every marked column its rank, i.e. its
+// position among the row's output entries, so the window's column indices are
+// written straight from the bitmap, in order.  The values are then summed in
+// LDS over the compacted ranks (tiles of kAcc ranks), so the accumulator only
+// spans columns that occur.  Every partner run is sorted by row, so each run
+// is consumed front to back through a per-entry cursor: a short stretch of a
+// run by one lane, a long one by a whole wavefront over contiguous keys.
+//
+// The symbolic pass builds the bitmaps only and counts the row's columns; the
+// numeric pass rebuilds them, writes the column indices and the values.
 #include "common.h"
 #include "internal.h"
 #include "lookup.h"
@@ -18,33 +21,62 @@
 namespace spsyrk {
 namespace {
 
-constexpr int kChunkE = 1024;  // entries scanned per activity round
+constexpr int kHB = 512;                 // threads per workgroup
+constexpr int kHW = kHB / kWave;         // wavefronts per workgroup
+constexpr int kChunkE = 1024;            // entries examined per activity round
+constexpr int kLongU = 2;                // keys per lane per step of a long walk
+constexpr int kHeavyGroups = 1024;       // workgroups of a heavy-row launch
 
+// Output columns per window and ranks per value tile: the symbolic pass
+// holds a 32 KiB bitmap; the numeric pass a 16 KiB bitmap, the words' ranks
+// and a 32 KiB value tile.
 template <int SR, bool NUM>
-struct TileCfg {
-    // columns per tile: 32 KiB of occupancy bytes for counting, 32 KiB of
-    // accumulators (8 or 4 bytes each) plus their occupancy for values, so
-    // that three workgroups share a compute unit
-    static constexpr int kW = !NUM ? 32768 : ((SR == kF64 || SR == kF32) ? 4096 : 8192);
+struct HeavyCfg {
+    using Acc = typename SrTraits<SR>::Acc;
+    static constexpr int kWin = NUM ? (1 << 17) : (1 << 18);
+    static constexpr int kWords = kWin / 32;
+    static constexpr int kAcc = 32768 / int(sizeof(Acc));
 };
 
+// exclusive scan over the kHB threads of a workgroup; *total gets the sum
+__device__ inline uint32_t scan_hb(uint32_t v, uint32_t* wt, uint32_t* total) {
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const uint32_t inc = wave_inclusive_scan(v);
+    if (lane == kWave - 1) wt[w] = inc;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int q = 0; q < kHW; ++q) {
+        const uint32_t t = wt[q];
+        if (q < w) off += t;
+        tot += t;
+    }
+    __syncthreads();
+    *total = tot;
+    return off + inc - v;
+}
+
 template <int SR, bool NUM, bool LOWER>
-__global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) {
+__global__ __launch_bounds__(kHB, NUM ? 4 : 8) void heavy_kernel(HeavyArgs a, int* queue) {
     using Tr = SrTraits<SR>;
     using In = typename Tr::In;
     using Acc = typename Tr::Acc;
     using Out = typename Tr::Out;
-    constexpr int kW = TileCfg<SR, NUM>::kW;
+    constexpr int kAcc = HeavyCfg<SR, NUM>::kAcc;
+    constexpr int kWin = HeavyCfg<SR, NUM>::kWin;
+    constexpr int kWords = HeavyCfg<SR, NUM>::kWords;
     constexpr bool kVal = (SR == kF64 || SR == kF32);
 
-    __shared__ uint8_t occ[kW];
-    __shared__ Acc acc[NUM ? kW : 1];
-    __shared__ int32_t act[kChunkE];
-    __shared__ int nact_s;
+    __shared__ uint32_t bits[kWords];
+    __shared__ uint32_t prefw[NUM ? kWords : 1];  // rank of each word's first column in the window
+    __shared__ Acc acc[NUM ? kAcc : 1];
+    __shared__ int32_t act_short[kChunkE];
+    __shared__ int32_t act_long[kChunkE];
+    __shared__ int nshort_s, nlong_s;
     __shared__ int row_s;
-    __shared__ uint32_t wt[kWavesPerBlock];
-    __shared__ uint64_t wt64[kWavesPerBlock];
-    __shared__ double wtd[kWavesPerBlock];
+    __shared__ uint32_t wt[kHW];
+    __shared__ double wtd[kHW];
 
     const int tid = threadIdx.x;
     const int w = tid / kWave;
@@ -53,9 +85,134 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
     const uint32_t rowmask = a.cx.rowbits >= 32 ? 0xffffffffu : ((1u << a.cx.rowbits) - 1u);
     const int nheavy = *a.heavy_count;
 
-    if constexpr (NUM) {
-        for (int x = tid; x < kW; x += kBlock) acc[x] = Acc(0);
-    }
+    // rank of column j of the current window among the window's columns
+    auto rank_of = [&](int64_t B0, uint32_t j) -> uint32_t {
+        if constexpr (!NUM) return 0u;  // (ranks exist in the numeric pass only)
+        const uint32_t x = uint32_t(int64_t(j) - B0);
+        return prefw[x >> 5] + uint32_t(__popc(bits[x >> 5] & ((1u << (x & 31)) - 1u)));
+    };
+
+    // Walk the partner runs of entries [c0, c1) from their cursors through
+    // the partners below column B1 (and, for values, of rank below T0 + tl):
+    // mark them in the bitmap, or add their terms to the value tile.  Short
+    // stretches (under a wavefront of partners) are walked by one lane each,
+    // long ones by whole wavefronts.  The cursors move if advance is set.
+    // Called by all threads.
+    auto walk = [&](int64_t c0, int64_t c1, int64_t B0, int64_t B1, bool value, uint32_t T0, uint32_t tl,
+                    bool advance) {
+        if (tid == 0) {
+            nshort_s = 0;
+            nlong_s = 0;
+        }
+        __syncthreads();
+        const uint32_t rlim = T0 + tl;
+        for (int64_t e = c0 + tid; e < c1; e += kHB) {
+            const uint32_t c = a.cursor[e];
+            const uint32_t hi = a.run[e].y;
+            if (c >= hi) continue;
+            const uint32_t j = key[c] & rowmask;
+            if (int64_t(j) >= B1 || (value && rank_of(B0, j) >= rlim)) continue;
+            bool lng = c + uint32_t(kWave) <= hi;
+            if (lng) {
+                const uint32_t jl = key[c + kWave - 1] & rowmask;
+                lng = int64_t(jl) < B1 && !(value && rank_of(B0, jl) >= rlim);
+            }
+            if (lng)
+                act_long[atomicAdd(&nlong_s, 1)] = int32_t(e - c0);
+            else
+                act_short[atomicAdd(&nshort_s, 1)] = int32_t(e - c0);
+        }
+        __syncthreads();
+        const int nshort = nshort_s, nlong = nlong_s;
+        // short stretches: one lane each, four keys per round
+        for (int q = tid; q < nshort; q += kHB) {
+            const int64_t e = c0 + act_short[q];
+            uint32_t c = a.cursor[e];
+            const uint32_t hi = a.run[e].y;
+            double av = 0.0;
+            if constexpr (kVal) av = value ? double(static_cast<const In*>(a.val)[e]) : 0.0;
+            bool stop = false;
+            while (!stop) {
+                uint32_t jj[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) jj[u] = c + u < hi ? (key[c + u] & rowmask) : 0xffffffffu;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (stop) break;
+                    if (c >= hi || int64_t(jj[u]) >= B1) {
+                        stop = true;
+                        break;
+                    }
+                    const uint32_t x = uint32_t(int64_t(jj[u]) - B0);
+                    if (value) {
+                        const uint32_t rk = rank_of(B0, jj[u]);
+                        if (rk >= rlim || rk < T0) {
+                            stop = true;
+                            break;
+                        }
+                        if constexpr (NUM) {
+                            if constexpr (kVal)
+                                atomicAdd(&acc[rk - T0], av * double(static_cast<const In*>(a.cx.val)[c]));
+                            else
+                                atomicAdd(&acc[rk - T0], 1);
+                        }
+                    } else {
+                        atomicOr(&bits[x >> 5], 1u << (x & 31));
+                    }
+                    ++c;
+                }
+            }
+            if (advance) a.cursor[e] = c;
+        }
+        // long stretches: a wavefront each, kLongU keys per lane per step
+        for (int q = w; q < nlong; q += kHW) {
+            const int64_t e = c0 + act_long[q];
+            uint32_t c = a.cursor[e];
+            const uint32_t hi = a.run[e].y;
+            double av = 0.0;
+            if constexpr (kVal) av = value ? double(static_cast<const In*>(a.val)[e]) : 0.0;
+            while (c < hi) {
+                uint32_t jj[kLongU];
+#pragma unroll
+                for (int u = 0; u < kLongU; ++u) {
+                    const uint32_t p = c + uint32_t(u * kWave) + lane;
+                    jj[u] = p < hi ? (key[p] & rowmask) : 0xffffffffu;
+                }
+                uint32_t took = 0;
+                bool full = true;
+#pragma unroll
+                for (int u = 0; u < kLongU; ++u) {
+                    const uint32_t p = c + uint32_t(u * kWave) + lane;
+                    bool in = false;
+                    if (full && int64_t(jj[u]) < B1) {
+                        const uint32_t x = uint32_t(int64_t(jj[u]) - B0);
+                        if (value) {
+                            const uint32_t rk = rank_of(B0, jj[u]);
+                            in = rk >= T0 && rk < rlim;
+                            if (in) {
+                                if constexpr (NUM) {
+                                    if constexpr (kVal)
+                                        atomicAdd(&acc[rk - T0], av * double(static_cast<const In*>(a.cx.val)[p]));
+                                    else
+                                        atomicAdd(&acc[rk - T0], 1);
+                                }
+                            }
+                        } else {
+                            in = true;
+                            atomicOr(&bits[x >> 5], 1u << (x & 31));
+                        }
+                    }
+                    const uint32_t t = uint32_t(__popcll(__ballot(in)));
+                    took += t;
+                    full = full && t == uint32_t(kWave);
+                }
+                c += took;
+                if (!full) break;
+            }
+            if (advance && lane == 0) a.cursor[e] = c;
+        }
+        __syncthreads();
+    };
 
     while (true) {
         if (tid == 0) {
@@ -71,7 +228,7 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
 
         // partner runs and cursors
         uint64_t prod_local = 0;
-        for (int64_t e = e0 + tid; e < e1; e += kBlock) {
+        for (int64_t e = e0 + tid; e < e1; e += kHB) {
             uint32_t st, len;
             if (!NUM && !a.runs_ready) {
                 partner_run(key, a.cx.gptr, a.cx.gs, a.cx.rowbits, uint32_t(a.ci[e]), uint32_t(i), LOWER, st, len);
@@ -83,7 +240,7 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
             a.cursor[e] = st;
         }
         if constexpr (!NUM) {
-            uint64_t tot = wave_reduce_sum(prod_local);
+            const uint64_t tot = wave_reduce_sum(prod_local);
             if (lane == 0 && tot && a.products) atomicAdd(a.products, (unsigned long long)tot);
         }
         __threadfence_block();
@@ -91,94 +248,68 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
 
         const int64_t jmax = LOWER ? int64_t(i) : a.m_right;
         int64_t count = 0;                          // symbolic: distinct columns so far
-        int64_t outp = NUM ? a.c_rp[i] : 0;         // numeric: next output slot
-        for (int64_t W0 = 0; W0 < jmax; W0 += kW) {
-            const int64_t W1 = min(jmax, W0 + int64_t(kW));
-            const int span = int(W1 - W0);
-            for (int x = tid; x < span; x += kBlock) occ[x] = 0;
+        int64_t outp = NUM ? a.c_rp[i] : 0;         // numeric: first output slot of the window
+        for (int64_t B0 = 0; B0 < jmax; B0 += kWin) {
+            const int64_t B1 = min(jmax, B0 + int64_t(kWin));
+            const int nw = int((B1 - B0 + 31) >> 5);
+            for (int x = tid; x < nw; x += kHB) bits[x] = 0;
             __syncthreads();
-            for (int64_t c0 = e0; c0 < e1; c0 += kChunkE) {
-                const int64_t c1 = min(e1, c0 + int64_t(kChunkE));
-                if (tid == 0) nact_s = 0;
-                __syncthreads();
-                for (int64_t e = c0 + tid; e < c1; e += kBlock) {
-                    const uint32_t c = a.cursor[e];
-                    if (c < a.run[e].y && int64_t(key[c] & rowmask) < W1) act[atomicAdd(&nact_s, 1)] = int32_t(e - e0);
-                }
-                __syncthreads();
-                const int nact = nact_s;
-                for (int q = w; q < nact; q += kWavesPerBlock) {
-                    const int64_t e = e0 + act[q];
-                    uint32_t c = a.cursor[e];
-                    const uint32_t hi = a.run[e].y;
-                    double av = 0.0;
-                    if constexpr (kVal && NUM) av = double(static_cast<const In*>(a.val)[e]);
-                    while (c < hi) {
-                        const uint32_t p = c + lane;
-                        bool in = false;
-                        uint32_t j = 0;
-                        if (p < hi) {
-                            j = key[p] & rowmask;
-                            in = int64_t(j) < W1;
-                        }
-                        const uint64_t m = __ballot(in);
-                        if (in) {
-                            const int x = int(j - W0);
-                            occ[x] = 1;
-                            if constexpr (NUM) {
-                                if constexpr (kVal)
-                                    atomicAdd(&acc[x], av * double(static_cast<const In*>(a.cx.val)[p]));
-                                else
-                                    atomicAdd(&acc[x], 1);
-                            }
-                        }
-                        const uint32_t took = uint32_t(__popcll(m));
-                        c += took;
-                        if (took < uint32_t(kWave)) break;
-                    }
-                    if (lane == 0) a.cursor[e] = c;
-                }
-                __syncthreads();
-            }
-            // tile result
+
+            // mark the window's columns; the numeric pass walks the runs again
+            // for the values, so only the symbolic pass moves the cursors here
+            for (int64_t c0 = e0; c0 < e1; c0 += kChunkE)
+                walk(c0, min(e1, c0 + int64_t(kChunkE)), B0, B1, false, 0u, 0u, !NUM);
+
+            // ranks: every thread owns a contiguous stretch of words
+            constexpr int kPer = (kWords + kHB - 1) / kHB;
+            const int wlo = min(nw, tid * kPer), whi = min(nw, wlo + kPer);
+            uint32_t s = 0;
+            for (int x = wlo; x < whi; ++x) s += uint32_t(__popc(bits[x]));
+            uint32_t Nw;
+            uint32_t off = scan_hb(s, wt, &Nw);
             if constexpr (!NUM) {
-                uint32_t s = 0;
-                for (int x = tid; x < span; x += kBlock) s += occ[x];
-                uint32_t tot;
-                s = wave_reduce_sum(s);
-                if (lane == 0) wt[w] = s;
+                count += Nw;
                 __syncthreads();
-                tot = 0;
-                for (int q = 0; q < kWavesPerBlock; ++q) tot += wt[q];
-                __syncthreads();
-                count += tot;
             } else {
-                // each thread owns a contiguous run of columns of the tile
-                const int per = (span + kBlock - 1) / kBlock;
-                const int lo = min(span, tid * per), hi = min(span, lo + per);
-                uint32_t s = 0;
-                for (int x = lo; x < hi; ++x) s += occ[x];
-                uint32_t tot;
-                uint32_t off = block_exclusive_scan(s, wt, &tot);
-                int64_t p = outp + off;
-                for (int x = lo; x < hi; ++x) {
-                    if (!occ[x]) continue;
-                    const int32_t j = int32_t(W0 + x);
-                    a.c_ci[p] = j;
-                    Out ov;
-                    if constexpr (kVal) {
-                        ov = Out(acc[x]);
-                    } else if constexpr (SR == kCount) {
-                        ov = acc[x];
-                    } else {
-                        ov = jaccard(acc[x], E, a.rp_right[j + 1] - a.rp_right[j]);
+                for (int x = wlo; x < whi; ++x) {
+                    prefw[x] = off;
+                    uint32_t b = bits[x];
+                    // the window's column indices, in order
+                    while (b) {
+                        const int t = __ffs(b) - 1;
+                        b &= b - 1;
+                        a.c_ci[outp + off] = int32_t(B0 + 32 * x + t);
+                        ++off;
                     }
-                    static_cast<Out*>(a.c_val)[p] = ov;
-                    acc[x] = Acc(0);
-                    ++p;
                 }
-                outp += tot;
+                // (the barrier orders these writes for the workgroup's reads below)
                 __syncthreads();
+
+                // values over the compacted ranks, kAcc ranks at a time; an
+                // entry joins a value tile only if its next partner's rank
+                // falls inside it
+                for (uint32_t T0 = 0; T0 < Nw; T0 += uint32_t(kAcc)) {
+                    const uint32_t tl = min(Nw - T0, uint32_t(kAcc));
+                    for (uint32_t x = tid; x < tl; x += kHB) acc[x] = Acc(0);
+                    __syncthreads();
+                    for (int64_t c0 = e0; c0 < e1; c0 += kChunkE)
+                        walk(c0, min(e1, c0 + int64_t(kChunkE)), B0, B1, true, T0, tl, true);
+                    for (uint32_t x = tid; x < tl; x += kHB) {
+                        const int64_t p = outp + T0 + x;
+                        Out ov;
+                        if constexpr (kVal) {
+                            ov = Out(acc[x]);
+                        } else if constexpr (SR == kCount) {
+                            ov = acc[x];
+                        } else {
+                            const int32_t j = a.c_ci[p];
+                            ov = jaccard(acc[x], E, a.rp_right[j + 1] - a.rp_right[j]);
+                        }
+                        static_cast<Out*>(a.c_val)[p] = ov;
+                    }
+                    __syncthreads();
+                }
+                outp += Nw;
             }
         }
         // diagonal (lower triangle only; a heavy row is never empty)
@@ -192,7 +323,7 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
             if constexpr (kVal) {
                 // fixed-order reduction of the squared entries
                 double s = 0.0;
-                for (int64_t e = e0 + tid; e < e1; e += kBlock) {
+                for (int64_t e = e0 + tid; e < e1; e += kHB) {
                     const double v = double(static_cast<const In*>(a.val)[e]);
                     s += v * v;
                 }
@@ -200,7 +331,7 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
                 if (lane == 0) wtd[w] = s;
                 __syncthreads();
                 double t = 0.0;
-                for (int q = 0; q < kWavesPerBlock; ++q) t += wtd[q];
+                for (int q = 0; q < kHW; ++q) t += wtd[q];
                 dv = Out(t);
                 __syncthreads();
             } else if constexpr (SR == kCount) {
@@ -215,18 +346,18 @@ __global__ __launch_bounds__(kBlock) void heavy_kernel(HeavyArgs a, int* queue) 
         }
         __syncthreads();
     }
-    (void)wt64;
 }
 
 template <int SR, bool NUM>
 void launch(const HeavyArgs& a, int* queue, hipStream_t s) {
     if (a.heavy_max <= 0) return;
     (void)hipMemsetAsync(queue, 0, sizeof(int), s);
-    int64_t grid = a.heavy_max < 2048 ? a.heavy_max : 2048;
+    const int64_t grid = a.heavy_max < kHeavyGroups ? a.heavy_max : kHeavyGroups;
+
     if (a.lower)
-        heavy_kernel<SR, NUM, true><<<unsigned(grid), kBlock, 0, s>>>(a, queue);
+        heavy_kernel<SR, NUM, true><<<unsigned(grid), kHB, 0, s>>>(a, queue);
     else
-        heavy_kernel<SR, NUM, false><<<unsigned(grid), kBlock, 0, s>>>(a, queue);
+        heavy_kernel<SR, NUM, false><<<unsigned(grid), kHB, 0, s>>>(a, queue);
 }
 
 template <bool NUM>

@@ -37,7 +37,7 @@ constexpr int kFB = kFP + kFR;       // buckets per batch
 constexpr int kWavesF = 2;           // wavefronts per workgroup
 constexpr int kMaxBatches = kFR;
 constexpr int kRunRegs = kFE / kWave;  // partner runs per lane held in registers
-constexpr int kSmall = 4;              // buckets up to this size are merged in registers
+constexpr int kSmall = 8;              // buckets up to this size are merged in registers
 constexpr int kTBits = 9;              // product index bits in s_t (row above them)
 constexpr uint32_t kTMask = (1u << kTBits) - 1u;
 static_assert(kFP <= (1 << kTBits), "product index must fit kTBits");
@@ -185,7 +185,14 @@ struct Chunk {
             if (range > 0 && uint64_t(range) < want) want = uint64_t(range);
             nb = uint32_t(want);
             L.rnb[r] = uint16_t(nb);
-            L.rscale[r] = range > 0 ? (uint64_t(nb) << 32) / uint64_t(range) : 0;
+            // floor(nb 2^32 / range) rounded down by one more: bucket < nb for
+            // every j < range (the quotient's error is far below one)
+            uint64_t sc = 0;
+            if (range > 0) {
+                sc = uint64_t(ldexp(double(nb), 32) / double(range));
+                sc = sc > 0 ? sc - 1 : 0;
+            }
+            L.rscale[r] = sc;
         }
         const uint32_t inc = wave_inclusive_scan(nb);
         if (lane < nrb) L.rbb[ra + lane] = uint16_t(inc - nb);
@@ -274,54 +281,22 @@ struct Chunk {
         // small buckets (up to kSmall products), one per lane: sorted by
         // (column, product index) in registers, equal columns merged (terms
         // summed in product order), the distinct columns written back in order
-        // at the bucket's start; ucnt[b] = distinct columns.  Larger buckets
-        // are listed for the cooperative pass below.
+        // at the bucket's start with their term counts in s_rank; ucnt[b] =
+        // distinct columns.  Larger buckets are listed for the cooperative
+        // pass below.
         for (uint32_t b = lane; b < B; b += kWave) {
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
             const uint32_t sz = hi - lo;
             uint32_t d = sz;
-            if (sz > uint32_t(kSmall)) {
+            if (sz == 1) {
+                L.s_rank[lo] = 1;
+            } else if (sz > uint32_t(kSmall)) {
                 L.big[atomicAdd(&L.nbig, 1u)] = uint16_t(b);
                 d = 0;
-            } else if (sz > 0) {
-                uint64_t k[kSmall];
-                Item v[kSmall];
-#pragma unroll
-                for (int u = 0; u < kSmall; ++u) {
-                    const bool in = uint32_t(u) < sz;
-                    k[u] = in ? ((uint64_t(L.s_j[lo + u]) << 16) | L.s_t[lo + u]) : ~uint64_t(0);
-                    v[u] = in ? L.s_v[lo + u] : Item(0);
-                }
-                cswap(k, v, 0, 1);
-                cswap(k, v, 2, 3);
-                cswap(k, v, 0, 2);
-                cswap(k, v, 1, 3);
-                cswap(k, v, 1, 2);
-                const int r = int((k[0] & 0xffffu) >> kTBits);
-                const int64_t len_i = L.rp[r + 1] - L.rp[r];
-                d = 0;
-                uint32_t gj = uint32_t(k[0] >> 16);
-                Item acc = v[0];
-                int32_t cnt = 1;
-#pragma unroll
-                for (int u = 1; u <= kSmall; ++u) {
-                    const bool in = uint32_t(u) < sz;
-                    const uint32_t j = in ? uint32_t(k[u < kSmall ? u : 0] >> 16) : 0u;
-                    if (in && j == gj) {
-                        ++cnt;
-                        if constexpr (kVal) acc += v[u < kSmall ? u : 0];
-                    } else if (uint32_t(u) <= sz) {
-                        // the group of gj ends: emit it
-                        L.s_j[lo + d] = gj;
-                        L.s_v[lo + d] = finish(acc, cnt, len_i);
-                        ++d;
-                        if (in) {
-                            gj = j;
-                            acc = v[u < kSmall ? u : 0];
-                            cnt = 1;
-                        }
-                    }
-                }
+            } else if (sz > uint32_t(kSmall / 2)) {
+                d = merge_small<kSmall>(lo, sz);
+            } else if (sz > 1) {
+                d = merge_small<kSmall / 2>(lo, sz);
             }
             L.ucnt[b] = d;
         }
@@ -397,6 +372,59 @@ struct Chunk {
         return int(B);
     }
 
+    // Sort the sz (<= N) products at [lo, lo + sz) by (column, product index)
+    // in registers, merge equal columns and write the distinct ones back from
+    // lo on: column, merged term (the sum for plus-times, |S(j)| for Jaccard)
+    // and term count.  Returns the number of distinct columns.
+    template <int N>
+    __device__ uint32_t merge_small(uint32_t lo, uint32_t sz) {
+        uint64_t k[N];
+        Item v[N];
+#pragma unroll
+        for (int u = 0; u < N; ++u) {
+            const bool in = uint32_t(u) < sz;
+            k[u] = in ? ((uint64_t(L.s_j[lo + u]) << 16) | L.s_t[lo + u]) : ~uint64_t(0);
+            v[u] = in ? L.s_v[lo + u] : Item(0);
+        }
+        if constexpr (N == 4) {
+            cswap(k, v, 0, 1); cswap(k, v, 2, 3); cswap(k, v, 0, 2); cswap(k, v, 1, 3); cswap(k, v, 1, 2);
+        } else {
+            static_assert(N == 8, "networks for 4 and 8 products");
+            cswap(k, v, 0, 1); cswap(k, v, 2, 3); cswap(k, v, 4, 5); cswap(k, v, 6, 7);
+            cswap(k, v, 0, 2); cswap(k, v, 1, 3); cswap(k, v, 4, 6); cswap(k, v, 5, 7);
+            cswap(k, v, 1, 2); cswap(k, v, 5, 6); cswap(k, v, 0, 4); cswap(k, v, 3, 7);
+            cswap(k, v, 1, 5); cswap(k, v, 2, 6);
+            cswap(k, v, 1, 4); cswap(k, v, 3, 6);
+            cswap(k, v, 2, 4); cswap(k, v, 3, 5);
+            cswap(k, v, 3, 4);
+        }
+        uint32_t d = 0;
+        uint32_t gj = uint32_t(k[0] >> 16);
+        Item acc = v[0];
+        uint32_t cnt = 1;
+#pragma unroll
+        for (int u = 1; u <= N; ++u) {
+            const bool in = uint32_t(u) < sz;
+            const uint32_t j = in ? uint32_t(k[u < N ? u : 0] >> 16) : 0u;
+            if (in && j == gj) {
+                ++cnt;
+                if constexpr (kVal) acc += v[u < N ? u : 0];
+            } else if (uint32_t(u) <= sz) {
+                // the group of gj ends
+                L.s_j[lo + d] = gj;
+                L.s_v[lo + d] = acc;
+                L.s_rank[lo + d] = uint16_t(cnt);
+                ++d;
+                if (in) {
+                    gj = j;
+                    acc = v[u < N ? u : 0];
+                    cnt = 1;
+                }
+            }
+        }
+        return d;
+    }
+
     // value of a merged column: the sum (plus-times), the count, or the
     // Jaccard bits from the count and the two row lengths
     __device__ static Item finish(Item acc, int32_t cnt, int64_t len_i) {
@@ -408,7 +436,8 @@ struct Chunk {
             return __float_as_int(jaccard(cnt, len_i, acc));
     }
 
-    __device__ static void cswap(uint64_t (&k)[kSmall], Item (&v)[kSmall], int x, int y) {
+    template <int N>
+    __device__ static void cswap(uint64_t (&k)[N], Item (&v)[N], int x, int y) {
         const bool sw = k[y] < k[x];
         const uint64_t kx = sw ? k[y] : k[x], ky = sw ? k[x] : k[y];
         const Item vx = sw ? v[y] : v[x], vy = sw ? v[x] : v[y];
@@ -429,7 +458,9 @@ struct Chunk {
             const int64_t base = L.rbase[r] + int64_t(L.ucnt[b]);
             if (hi - lo <= uint32_t(kSmall)) {
                 const uint32_t d = L.ucnt[b + 1] - L.ucnt[b];
-                for (uint32_t k = 0; k < d; ++k) emit(base + k, L.s_j[lo + k], L.s_v[lo + k]);
+                const int64_t len_i = L.rp[r + 1] - L.rp[r];
+                for (uint32_t k = 0; k < d; ++k)
+                    emit(base + k, L.s_j[lo + k], finish(L.s_v[lo + k], int32_t(L.s_rank[lo + k]), len_i));
             } else {
                 for (uint32_t u = lo; u < hi; ++u)
                     if (L.s_rank[u] != 0xffff) emit(base + L.s_rank[u], L.s_j[u], L.s_v[u]);
@@ -473,18 +504,31 @@ struct Chunk {
         static_cast<Out*>(a.c_val)[p] = ov;
     }
 
-    __device__ void run(int64_t c) {
+    // A chunk's row pointers, product counts and staging slots (lane = row),
+    // loaded in one round, ahead of the chunk.
+    struct Head {
+        int64_t rpv = 0, ubv = 0;
+        uint64_t pr = 0;
+    };
+    __device__ Head head(int64_t c) const {
+        const int R = a.rows_per_chunk;
+        const int64_t rs = c * R;
+        const int nr = int(min(int64_t(R), a.m - rs));
+        Head h;
+        if (lane <= nr) h.rpv = a.rp[rs + lane];
+        if (lane < nr) {
+            h.pr = a.prod[rs + lane];
+            h.ubv = a.ubp[rs + lane];
+        }
+        return h;
+    }
+
+    __device__ void run(int64_t c, const Head& h) {
         const int R = a.rows_per_chunk;
         r0 = c * R;
         const int nr = int(min(int64_t(R), a.m - r0));
-        // the chunk's row pointers, product counts and staging slots in one round
-        int64_t rpv = 0, ubv = 0;
-        uint64_t pr = 0;
-        if (lane <= nr) rpv = a.rp[r0 + lane];
-        if (lane < nr) {
-            pr = a.prod[r0 + lane];
-            ubv = a.ubp[r0 + lane];
-        }
+        const int64_t rpv = h.rpv, ubv = h.ubv;
+        const uint64_t pr = h.pr;
         if (lane <= nr) L.rp[lane] = rpv;
         wave_sync();
         int64_t len = 0;
@@ -546,17 +590,44 @@ __global__ __launch_bounds__(kWave* kWavesF) void fused_kernel(FusedArgs a) {
     __shared__ WaveLds<Item> lds[kWavesF];
     WaveLds<Item>& L = lds[threadIdx.x / kWave];
     Chunk<SR, LOWER> ch(a, L);
-    const int64_t c = int64_t(blockIdx.x) * kWavesF + threadIdx.x / kWave;
-    if (c < a.nchunks) ch.run(c);
+    // persistent wavefronts: chunks c, c + stride, ...; the next chunk's head
+    // is loaded while the current chunk runs
+    const int64_t stride = int64_t(gridDim.x) * kWavesF;
+    int64_t c = int64_t(blockIdx.x) * kWavesF + threadIdx.x / kWave;
+    if (c >= a.nchunks) return;
+    auto h = ch.head(c);
+    while (true) {
+        const int64_t cn = c + stride;
+        decltype(h) hn;
+        if (cn < a.nchunks) hn = ch.head(cn);
+        ch.run(c, h);
+        if (cn >= a.nchunks) break;
+        c = cn;
+        h = hn;
+    }
+}
+
+// Workgroups resident on the whole device at once (at least one).
+template <typename K>
+int resident_groups(K kernel) {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 1;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, kWave * kWavesF, 0) != hipSuccess) return 1;
+    const int g = cus * per;
+    return g > 0 ? g : 1;
 }
 
 template <int SR>
 void launch(const FusedArgs& a, int grid, hipStream_t s) {
     if (grid <= 0) return;
-    if (a.lower)
-        fused_kernel<SR, true><<<grid, kWave * kWavesF, 0, s>>>(a);
-    else
-        fused_kernel<SR, false><<<grid, kWave * kWavesF, 0, s>>>(a);
+    if (a.lower) {
+        static const int res = resident_groups(fused_kernel<SR, true>);
+        fused_kernel<SR, true><<<grid < res ? grid : res, kWave * kWavesF, 0, s>>>(a);
+    } else {
+        static const int res = resident_groups(fused_kernel<SR, false>);
+        fused_kernel<SR, false><<<grid < res ? grid : res, kWave * kWavesF, 0, s>>>(a);
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void classify_kernel(const int64_t* __restrict__ rp,

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     __shared__ int64_t rwin[FIRST ? kRowWin + 1 : 1];
     __shared__ int64_t rbounds[2];
     __shared__ uint32_t wcnt[kWavesPerBlock][kDigits];
-    __shared__ uint32_t tstart[kDigits];
+    __shared__ int64_t gofs[kDigits];  // global position of the tile's digit run minus its tile start
     __shared__ uint32_t wt[kWavesPerBlock];
     __shared__ uint32_t ex_key[kRTile];
     __shared__ uint32_t ex_row[kRTile];
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         }
         uint32_t all;
         uint32_t off = block_exclusive_scan(tot, wt, &all);
-        tstart[d] = off;
+        gofs[d] = int64_t(offs[int64_t(d) * ntiles + blockIdx.x]) - int64_t(off);
 #pragma unroll
         for (int q = 0; q < kWavesPerBlock; ++q) {
             wcnt[q][d] = off;
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     for (int i = threadIdx.x; i < tile_n; i += kBlock) {
         const uint32_t key = ex_key[i];
         const uint32_t d = (key >> shift) & mask;
-        const int64_t g = int64_t(offs[int64_t(d) * ntiles + blockIdx.x]) + (i - tstart[d]);
+        const int64_t g = gofs[d] + i;
         key_out[g] = key;
         row_out[g] = ex_row[i];
         if constexpr (VB != 0) val_out[g] = ex_val[i];
@@ -205,6 +205,17 @@ void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* 
         ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, rowbits, lenbits);
 }
 
+// Digit widths of the passes for an nbits-bit key: as few passes as 8-bit
+// digits need, the bits spread evenly over them (narrower digits give each
+// tile longer runs per digit, so fuller lines are written).  Returns the
+// number of passes (at least one).
+int digit_plan(int nbits, int (&width)[8]) {
+    const int passes = nbits > 0 ? (nbits + kRBits - 1) / kRBits : 1;
+    const int base = nbits / passes, extra = nbits % passes;
+    for (int i = 0; i < passes; ++i) width[i] = base + (i < extra ? 1 : 0);
+    return passes;
+}
+
 }  // namespace
 
 size_t radix_tmp_bytes(int64_t n) {
@@ -221,14 +232,15 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     uint32_t* hist = static_cast<uint32_t*>(tmp);
     const size_t hist_bytes = (size_t(ntiles) * kDigits * sizeof(uint32_t) + 255) & ~size_t(255);
     void* scan_tmp = static_cast<char*>(tmp) + hist_bytes;
+    int width[8];
+    const int passes = digit_plan(nbits, width);
     // first pass straight from the CSR arrays (into the b buffers), at least one pass
-    const int bits0 = nbits < kRBits ? nbits : kRBits;
     run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, 0,
-                      (1u << bits0) - 1u, hist, scan_tmp, s, rp, m, rowbits, lenbits);
+                      (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, rowbits, lenbits);
     int cur = 1;
-    for (int shift = kRBits; shift < nbits; shift += kRBits) {
-        const int bits = nbits - shift < kRBits ? nbits - shift : kRBits;
-        const uint32_t mask = (1u << bits) - 1u;
+    int shift = width[0];
+    for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
+        const uint32_t mask = (1u << width[ps]) - 1u;
         uint32_t* ki = cur ? key_b : key_a;
         uint32_t* ko = cur ? key_a : key_b;
         uint32_t* ri = cur ? row_b : row_a;
@@ -248,10 +260,12 @@ int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_
     uint32_t* hist = static_cast<uint32_t*>(tmp);
     const size_t hist_bytes = (size_t(ntiles) * kDigits * sizeof(uint32_t) + 255) & ~size_t(255);
     void* scan_tmp = static_cast<char*>(tmp) + hist_bytes;
+    int width[8];
+    const int passes = digit_plan(nbits, width);
     int cur = 0;
-    for (int shift = 0; shift < nbits; shift += kRBits) {
-        const int bits = nbits - shift < kRBits ? nbits - shift : kRBits;
-        const uint32_t mask = (1u << bits) - 1u;
+    int shift = 0;
+    for (int ps = 0; ps < passes; shift += width[ps], ++ps) {
+        const uint32_t mask = (1u << width[ps]) - 1u;
         uint32_t* ki = cur ? key_b : key_a;
         uint32_t* ko = cur ? key_a : key_b;
         uint32_t* ri = cur ? row_b : row_a;
