@@ -256,12 +256,16 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
     if (gs > maxgs) gs = maxgs;
     const int nbits_n = bit_width_u64(B.n > 1 ? uint64_t(B.n - 1) : 0);
     if (gs > nbits_n) gs = nbits_n;
+    // with every partner run given (lower mode) nothing is ever looked up:
+    // no directory, and the keys hold the row only
+    const bool runs_given = run != nullptr;
+    if (runs_given) gs = 0;
     cx.gs = gs;
     cx.ngroups = B.n > 0 ? ((B.n + (int64_t(1) << gs) - 1) >> gs) : 0;
     const int vb = (sr == kF64) ? 8 : (sr == kF32 ? 4 : 0);
     const int vb_out = csc_value_bytes(sr);
 
-    cx.gptr = ar.get_t<uint32_t>(cx.ngroups + 1);
+    cx.gptr = runs_given ? nullptr : ar.get_t<uint32_t>(cx.ngroups + 1);
     cx.key = ar.get_t<uint32_t>(N > 0 ? N : 1);
     cx.val = vb_out ? ar.get(size_t(N > 0 ? N : 1) * vb_out) : nullptr;
 

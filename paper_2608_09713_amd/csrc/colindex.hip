@@ -101,14 +101,14 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
                 run[sent[p]] = make_uint2(uint32_t(first_kept), uint32_t(first_kept + rank));
             }
         }
-        if (start) {
+        if (start && gptr) {
             // directory slots of the groups opened by this column
             const int64_t q0 = drop_last ? p - cols_before : p;
             const int64_t g = int64_t(col >> gs);
             const int64_t gprev = p == 0 ? -1 : int64_t(scol[p - 1] >> gs);
             for (int64_t x = gprev + 1; x <= g; ++x) gptr[x] = uint32_t(q0);
         }
-        if (p == n - 1) {
+        if (p == n - 1 && gptr) {
             const uint32_t kept = uint32_t(*nkept);
             for (int64_t x = int64_t(col >> gs) + 1; x <= ngroups; ++x) gptr[x] = kept;
         }
@@ -154,8 +154,10 @@ void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* 
     const int64_t n = n_entries;
     if (n == 0) {
         (void)hipMemsetAsync(d_nkept, 0, sizeof(int64_t), s);
-        const unsigned ng = unsigned((cx.ngroups + 1 + kBlock - 1) / kBlock);
-        empty_directory<<<ng, kBlock, 0, s>>>(cx.ngroups, cx.gptr);
+        if (cx.gptr) {
+            const unsigned ng = unsigned((cx.ngroups + 1 + kBlock - 1) / kBlock);
+            empty_directory<<<ng, kBlock, 0, s>>>(cx.ngroups, cx.gptr);
+        }
         return;
     }
     const unsigned nb = unsigned((n + kBlock - 1) / kBlock);

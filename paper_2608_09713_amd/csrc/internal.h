@@ -38,7 +38,7 @@ struct ColIndex {
     int64_t nkept = 0;      // entries kept (device-side value is authoritative until synced)
     uint32_t* key = nullptr;
     void* val = nullptr;    // double / float values of B, or int32 row lengths of B (Jaccard)
-    uint32_t* gptr = nullptr;
+    uint32_t* gptr = nullptr;  // null when every entry's partner run is given (no lookups)
 };
 
 // ---- scan.hip

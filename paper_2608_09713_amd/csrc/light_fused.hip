@@ -72,6 +72,8 @@ struct WaveLds {
     uint16_t rbb[kFR + 1];    // first bucket of the row in the current batch
     uint64_t rscale[kFR];     // bucket of column j: (j * rscale) >> 32 spreads [0, range) evenly
     uint8_t rlight[kFR];
+    uint32_t rpp[kFR + 1];    // products of the chunk's light rows before each row
+    uint8_t rnext[kFR];       // end of a batch opened at each light row
     uint8_t bra[kMaxBatches + 1], brb[kMaxBatches + 1];  // batches [bra, brb) of the chunk
     uint32_t ent_start[kFE];
     uint16_t ent_len[kFE];
@@ -542,30 +544,40 @@ struct Chunk {
             L.rcnt[lane] = ubv;
         }
         wave_sync();
-        // batches of consecutive light rows (same decision in every lane)
-        int nbatch = 0;
+        // batches of consecutive light rows, found in parallel: every light
+        // row knows where a batch opened at it must end (at the next heavy
+        // row, or where its entries or products would overflow the LDS
+        // budget); the batch starts are then chained (same in every lane)
+        const uint64_t lightmask = __ballot(lane < nr && light);
         {
-            int ra = 0;
-            while (ra < nr) {
-                while (ra < nr && !L.rlight[ra]) ++ra;
-                if (ra >= nr) break;
-                int rb = ra;
-                int64_t e = 0;
-                uint32_t p = 0;
-                while (rb < nr && L.rlight[rb]) {
-                    const int64_t len = L.rp[rb + 1] - L.rp[rb];
-                    if (e + len > kFE || p + L.rprod[rb] > uint32_t(kFP)) break;
-                    e += len;
-                    p += L.rprod[rb];
-                    ++rb;
-                }
-                if (lane == 0) {
-                    L.bra[nbatch] = uint8_t(ra);
-                    L.brb[nbatch] = uint8_t(rb);
-                }
-                ++nbatch;
-                ra = rb;
+            const uint32_t pinc = wave_inclusive_scan((lane < nr && light) ? uint32_t(pr) : 0u);
+            if (lane < nr) L.rpp[lane + 1] = pinc;
+            if (lane == 0) L.rpp[0] = 0;
+        }
+        wave_sync();
+        if (lane < nr && light) {
+            const uint64_t later = ~lightmask & ((uint64_t(1) << nr) - 1) & (~uint64_t(0) << (lane + 1));
+            int lo = lane + 1, hi = later ? __ffsll((unsigned long long)later) - 1 : nr;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (L.rp[mid] - L.rp[lane] <= kFE && L.rpp[mid] - L.rpp[lane] <= uint32_t(kFP))
+                    lo = mid;
+                else
+                    hi = mid - 1;
             }
+            L.rnext[lane] = uint8_t(lo);
+        }
+        wave_sync();
+        int nbatch = 0;
+        for (uint64_t rest = lightmask; rest;) {
+            const int ra = __ffsll((unsigned long long)rest) - 1;
+            const int rb = L.rnext[ra];
+            if (lane == 0) {
+                L.bra[nbatch] = uint8_t(ra);
+                L.brb[nbatch] = uint8_t(rb);
+            }
+            ++nbatch;
+            rest = lightmask & (~uint64_t(0) << rb);
         }
         wave_sync();
         int64_t cnt = 0;  // exact length of this lane's row
