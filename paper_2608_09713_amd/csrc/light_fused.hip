@@ -84,7 +84,7 @@ struct WaveLds {
     uint16_t s_t[kFP];
     uint16_t s_rank[kFP];     // large buckets: rank of a leader, 0xffff for the other products
     uint16_t big[kFP / (kSmall + 1) + 1];  // large buckets of the batch
-    uint32_t nbig;
+    uint32_t nbig, nmid, nsmall;
     int64_t rbase[kFR];
     Item s_v[kFP];
     uint32_t hist[kFB + 1];
@@ -278,14 +278,22 @@ struct Chunk {
                 if constexpr (SR == kJaccard || kVal) L.s_v[q] = pv[v];
             }
         }
-        if (lane == 0) L.nbig = 0;
+        if (lane == 0) {
+            L.nbig = 0;
+            L.nmid = 0;
+            L.nsmall = 0;
+        }
         wave_sync();
-        // small buckets (up to kSmall products), one per lane: sorted by
-        // (column, product index) in registers, equal columns merged (terms
-        // summed in product order), the distinct columns written back in order
-        // at the bucket's start with their term counts in s_rank; ucnt[b] =
-        // distinct columns.  Larger buckets are listed for the cooperative
-        // pass below.
+        // Buckets by size: empty and single-product buckets are done at once;
+        // the others are listed by size class so that every class runs with
+        // full lanes.  Small buckets (up to kSmall products), one per lane:
+        // sorted by (column, product index) in registers, equal columns merged
+        // (terms summed in product order), the distinct columns written back
+        // in order at the bucket's start with their term counts in s_rank;
+        // ucnt[b] = distinct columns.  Larger buckets go to the cooperative
+        // pass below.  (The entry arrays are free by now and hold the lists.)
+        uint16_t* list_small = reinterpret_cast<uint16_t*>(L.ent_start);
+        uint16_t* list_mid = L.ent_len;
         for (uint32_t b = lane; b < B; b += kWave) {
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
             const uint32_t sz = hi - lo;
@@ -296,11 +304,22 @@ struct Chunk {
                 L.big[atomicAdd(&L.nbig, 1u)] = uint16_t(b);
                 d = 0;
             } else if (sz > uint32_t(kSmall / 2)) {
-                d = merge_small<kSmall>(lo, sz);
+                list_mid[atomicAdd(&L.nmid, 1u)] = uint16_t(b);
             } else if (sz > 1) {
-                d = merge_small<kSmall / 2>(lo, sz);
+                list_small[atomicAdd(&L.nsmall, 1u)] = uint16_t(b);
             }
             L.ucnt[b] = d;
+        }
+        wave_sync();
+        for (uint32_t q = lane; q < L.nsmall; q += kWave) {
+            const uint32_t b = list_small[q];
+            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
+            L.ucnt[b] = merge_small<kSmall / 2>(lo, hi - lo);
+        }
+        for (uint32_t q = lane; q < L.nmid; q += kWave) {
+            const uint32_t b = list_mid[q];
+            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
+            L.ucnt[b] = merge_small<kSmall>(lo, hi - lo);
         }
         wave_sync();
         // larger buckets, one at a time by the whole wavefront: leaders (first
@@ -453,20 +472,32 @@ struct Chunk {
     // first output slot, rbase that slot minus the offset of the row's first
     // bucket.
     __device__ void write(int ra, int rb, int B) {
+        // every output of the batch, in output order, points at its column's
+        // slot (the top bit marks a value already final: large buckets); the
+        // owner array is free by now and holds the map
+        uint16_t* omap = reinterpret_cast<uint16_t*>(L.owner);
         for (int b = lane; b < B; b += kWave) {
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
             if (hi == lo) continue;
-            const int r = int(L.s_t[lo] >> kTBits);
-            const int64_t base = L.rbase[r] + int64_t(L.ucnt[b]);
+            const uint32_t u0 = L.ucnt[b];
             if (hi - lo <= uint32_t(kSmall)) {
-                const uint32_t d = L.ucnt[b + 1] - L.ucnt[b];
-                const int64_t len_i = L.rp[r + 1] - L.rp[r];
-                for (uint32_t k = 0; k < d; ++k)
-                    emit(base + k, L.s_j[lo + k], finish(L.s_v[lo + k], int32_t(L.s_rank[lo + k]), len_i));
+                const uint32_t d = L.ucnt[b + 1] - u0;
+                for (uint32_t k = 0; k < d; ++k) omap[u0 + k] = uint16_t(lo + k);
             } else {
                 for (uint32_t u = lo; u < hi; ++u)
-                    if (L.s_rank[u] != 0xffff) emit(base + L.s_rank[u], L.s_j[u], L.s_v[u]);
+                    if (L.s_rank[u] != 0xffff) omap[u0 + L.s_rank[u]] = uint16_t(u | 0x8000u);
             }
+        }
+        wave_sync();
+        // outputs written by consecutive lanes to consecutive slots of a row
+        const uint32_t U = L.ucnt[B];
+        for (uint32_t o = lane; o < U; o += kWave) {
+            const uint32_t mo = omap[o];
+            const uint32_t src = mo & 0x7fffu;
+            const int r = int(L.s_t[src] >> kTBits);
+            Item v = L.s_v[src];
+            if (!(mo & 0x8000u)) v = finish(v, int32_t(L.s_rank[src]), L.rp[r + 1] - L.rp[r]);
+            emit(L.rbase[r] + int64_t(o), L.s_j[src], v);
         }
         // diagonals (lower triangle): the last entry of every non-empty row
         if (LOWER && lane < rb - ra) {
