@@ -614,13 +614,13 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     int64_t* f_rp = ar.get_t<int64_t>(m + 1, true);
     int64_t* full_len = f_rp;  // lengths first, scanned in place
     int64_t* colcnt = ar.get_t<int64_t>(m + 1);
-    HIPCHK(hipMemsetAsync(full_len, 0, size_t(m + 1) * sizeof(int64_t), s));
-    HIPCHK(hipMemsetAsync(colcnt, 0, size_t(m + 1) * sizeof(int64_t), s));
+    uint32_t* cnt32 = ar.get_t<uint32_t>(m > 0 ? m : 1);
+    HIPCHK(hipMemsetAsync(full_len + m, 0, sizeof(int64_t), s));
+    HIPCHK(hipMemsetAsync(colcnt + m, 0, sizeof(int64_t), s));
     void* stmp = ar.get(scan_tmp_bytes(m + 1));
     {
         Phase ph(SPSYRK_PHASE_MIRROR_COUNT, s);
-        mirror_counts(ma, full_len, s);
-        mirror_col_counts(ma, full_len, colcnt, s);
+        mirror_counts(ma, cnt32, full_len, colcnt, s);
         scan_i64(colcnt, colcnt, m + 1, &ctl->total2, stmp, s);  // colcnt -> cstart
         scan_i64(full_len, f_rp, m + 1, &ctl->total, stmp, s);
     }
@@ -638,7 +638,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     if (nstrict > 0) {
         // column slabs of at most kSlab strict-lower entries (the whole range
         // when it fits; a slab always holds at least one column)
-        const int64_t kSlab = int64_t(1) << 30;
+        const int64_t kSlab = int64_t(1) << 31;
         std::vector<int64_t> bounds{0};
         if (nstrict <= kSlab) {
             bounds.push_back(m);
@@ -688,7 +688,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
             const int64_t nrec = h.total;
             if (nrec == 0) continue;
             Phase ph(SPSYRK_PHASE_MIRROR_TRANSPOSE, s);
-            mirror_slab_extract(ma, c0, c1, row_cnt, row_lo, ka, ra, va, s);
+            mirror_slab_extract(ma, c0, nrec, row_cnt, row_lo, ka, ra, va, s);
             const int nbits = bit_width_u64(c1 - c0 > 1 ? uint64_t(c1 - c0 - 1) : 0);
             const int which = radix_sort(ka, kb, ra, rb, va, vbb, vb, nrec, nbits, rtmp, s);
             mirror_slab_place(ma, c0, nrec, which ? kb : ka, which ? rb : ra, which ? vbb : va, colcnt, f_rp, f_ci,

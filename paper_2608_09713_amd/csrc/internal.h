@@ -191,23 +191,22 @@ struct MirrorArgs {
     const void* val = nullptr;
     int vbytes = 0;
 };
-// per-row length of the full matrix: lower length + strict-lower count of column i
-// (full_len is used as 64-bit atomic counters)
-void mirror_counts(const MirrorArgs& a, int64_t* full_len, hipStream_t s);
+// per-row length of the full matrix (lower length + strict-lower entries of
+// column i) and the strict-lower entries of every column; cnt is m words of
+// scratch (32-bit counters)
+void mirror_counts(const MirrorArgs& a, uint32_t* cnt, int64_t* full_len, int64_t* colcnt, hipStream_t s);
 void mirror_copy_lower(const MirrorArgs& a, const int64_t* f_rp, int32_t* f_ci, void* f_val, hipStream_t s);
-// records of the strict lower part with col in [c0, c1): (col - c0, row, value),
-// written in row-major order at positions given by rec_rp (exclusive scan of
-// per-row counts); counts written by mirror_slab_counts.
+// per-row counts and first entries of the strict lower part with col in [c0, c1)
 void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,
                         hipStream_t s);
-void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t c1, const int64_t* rec_rp, const int64_t* row_lo,
+// records (col - c0, row, value) of the slab, in row-major order at positions
+// given by rec_rp (exclusive scan of the per-row counts), nrec in all
+void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t nrec, const int64_t* rec_rp, const int64_t* row_lo,
                          uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s);
 // place sorted records: record s of column c goes to f_rp[c] + lower_len(c) + (s - (cstart[c] - cstart[c0]))
 // where cstart is the exclusive scan of strict-lower counts per column
 void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint32_t* skey, const uint32_t* srow,
                        const void* sval, const int64_t* cstart, const int64_t* f_rp, int32_t* f_ci, void* f_val,
                        hipStream_t s);
-// strict-lower count per column: colcnt[c] = full_len[c] - lower_len[c]
-void mirror_col_counts(const MirrorArgs& a, const int64_t* full_len, int64_t* colcnt, hipStream_t s);
 
 }  // namespace spsyrk

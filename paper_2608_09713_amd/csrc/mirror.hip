@@ -73,24 +73,45 @@ __device__ inline RowFinder make_finder(const int64_t* rp, int64_t m, int64_t e0
     return f;
 }
 
-__global__ __launch_bounds__(kBlock) void init_lower_len(const int64_t* __restrict__ rp, int64_t m,
-                                                         int64_t* __restrict__ len) {
-    const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (i < m) len[i] = rp[i + 1] - rp[i];
-}
+// Strict-lower entries per column (32-bit counters; a column holds fewer than
+// 2^31 entries).  Every thread walks kPerC contiguous entries row by row, so
+// the diagonal (the last entry of a row, col == row) is recognised without a
+// search per entry.
+constexpr int kPerC = 16;
+constexpr int kTileC = kBlock * kPerC;
 
 __global__ __launch_bounds__(kBlock) void count_transposed(const int64_t* __restrict__ rp,
                                                            const int32_t* __restrict__ ci, int64_t m, int64_t nnz,
-                                                           unsigned long long* __restrict__ len) {
+                                                           uint32_t* __restrict__ cnt) {
     __shared__ int64_t win[kWin + 1];
     __shared__ int64_t bounds[2];
-    const int64_t e0 = int64_t(blockIdx.x) * kTileE;
-    const int64_t e1 = min(nnz, e0 + kTileE);
+    const int64_t e0 = int64_t(blockIdx.x) * kTileC;
+    const int64_t e1 = min(nnz, e0 + kTileC);
     RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-        const int64_t c = ci[e];
-        if (c < f.row_of(e)) atomicAdd(&len[c], 1ull);
+    const int64_t ea = e0 + int64_t(threadIdx.x) * kPerC;
+    const int64_t eb = min(e1, ea + kPerC);
+    if (ea >= eb) return;
+    int64_t r = f.row_of(ea);
+    int64_t rend = rp[r + 1];
+    for (int64_t e = ea; e < eb; ++e) {
+        while (e >= rend) {  // next row (empty rows skipped)
+            ++r;
+            rend = rp[r + 1];
+        }
+        const int32_t c = ci[e];
+        if (int64_t(c) < r) atomicAdd(&cnt[c], 1u);
     }
+}
+
+// full_len[i] = lower length of row i + strict-lower entries of column i;
+// colcnt[i] = the latter
+__global__ __launch_bounds__(kBlock) void full_lengths(const int64_t* __restrict__ rp, int64_t m,
+                                                       const uint32_t* __restrict__ cnt,
+                                                       int64_t* __restrict__ full_len, int64_t* __restrict__ colcnt) {
+    const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (i >= m) return;
+    full_len[i] = (rp[i + 1] - rp[i]) + int64_t(cnt[i]);
+    colcnt[i] = int64_t(cnt[i]);
 }
 
 template <int VB>
@@ -140,23 +161,24 @@ __global__ __launch_bounds__(kBlock) void slab_counts(const int64_t* __restrict_
     lo_out[r] = lo;
 }
 
+// Records [0, nrec) of a slab in row-major order: record p of row r (rows
+// found in an LDS window of rec_rp) is entry row_lo[r] + (p - rec_rp[r]), so
+// the slab reads only its own entries.
 template <int VB>
-__global__ __launch_bounds__(kBlock) void slab_extract(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
-                                                       const void* __restrict__ val, int64_t m, int64_t nnz,
-                                                       int64_t c0, int64_t c1, const int64_t* __restrict__ rec_rp,
+__global__ __launch_bounds__(kBlock) void slab_extract(const int32_t* __restrict__ ci, const void* __restrict__ val,
+                                                       int64_t m, int64_t c0, int64_t nrec,
+                                                       const int64_t* __restrict__ rec_rp,
                                                        const int64_t* __restrict__ row_lo, uint32_t* __restrict__ rkey,
                                                        uint32_t* __restrict__ rrow, void* __restrict__ rval) {
     __shared__ int64_t win[kWin + 1];
     __shared__ int64_t bounds[2];
-    const int64_t e0 = int64_t(blockIdx.x) * kTileE;
-    const int64_t e1 = min(nnz, e0 + kTileE);
-    RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-        const int64_t c = ci[e];
-        const int64_t r = f.row_of(e);
-        if (c < c0 || c >= c1 || c >= r) continue;
-        const int64_t p = rec_rp[r] + (e - row_lo[r]);
-        rkey[p] = uint32_t(c - c0);
+    const int64_t p0 = int64_t(blockIdx.x) * kTileE;
+    const int64_t p1 = min(nrec, p0 + kTileE);
+    RowFinder f = make_finder(rec_rp, m, p0, p1, win, bounds);
+    for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
+        const int64_t r = f.row_of(p);
+        const int64_t e = row_lo[r] + (p - rec_rp[r]);
+        rkey[p] = uint32_t(int64_t(ci[e]) - c0);
         rrow[p] = uint32_t(r);
         if constexpr (VB == 8) static_cast<uint64_t*>(rval)[p] = static_cast<const uint64_t*>(val)[e];
         if constexpr (VB == 4) static_cast<uint32_t*>(rval)[p] = static_cast<const uint32_t*>(val)[e];
@@ -180,23 +202,16 @@ __global__ __launch_bounds__(kBlock) void slab_place(const int64_t* __restrict__
     if constexpr (VB == 4) static_cast<uint32_t*>(f_val)[p] = static_cast<const uint32_t*>(sval)[s];
 }
 
-__global__ __launch_bounds__(kBlock) void col_counts(const int64_t* __restrict__ rp, int64_t m,
-                                                     const int64_t* __restrict__ full_len,
-                                                     int64_t* __restrict__ colcnt) {
-    const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (i < m) colcnt[i] = full_len[i] - (rp[i + 1] - rp[i]);
-}
-
 inline unsigned blocks_for(int64_t n, int64_t per) { return unsigned((n + per - 1) / per); }
 
 }  // namespace
 
-void mirror_counts(const MirrorArgs& a, int64_t* full_len, hipStream_t s) {
+void mirror_counts(const MirrorArgs& a, uint32_t* cnt, int64_t* full_len, int64_t* colcnt, hipStream_t s) {
     if (a.m <= 0) return;
-    init_lower_len<<<blocks_for(a.m, kBlock), kBlock, 0, s>>>(a.rp, a.m, full_len);
-    if (a.nnz <= 0) return;
-    count_transposed<<<blocks_for(a.nnz, kTileE), kBlock, 0, s>>>(
-        a.rp, a.ci, a.m, a.nnz, reinterpret_cast<unsigned long long*>(full_len));
+    (void)hipMemsetAsync(cnt, 0, size_t(a.m) * sizeof(uint32_t), s);
+    if (a.nnz > 0)
+        count_transposed<<<blocks_for(a.nnz, kTileC), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, cnt);
+    full_lengths<<<blocks_for(a.m, kBlock), kBlock, 0, s>>>(a.rp, a.m, cnt, full_len, colcnt);
 }
 
 void mirror_copy_lower(const MirrorArgs& a, const int64_t* f_rp, int32_t* f_ci, void* f_val, hipStream_t s) {
@@ -217,17 +232,16 @@ void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* ro
     slab_counts<<<blocks_for(a.m, kBlock), kBlock, 0, s>>>(a.rp, a.ci, a.m, c0, c1, row_cnt, row_lo);
 }
 
-void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t c1, const int64_t* rec_rp, const int64_t* row_lo,
+void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t nrec, const int64_t* rec_rp, const int64_t* row_lo,
                          uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s) {
-    const int64_t nnz = a.nnz;
-    if (nnz <= 0) return;
-    const unsigned nb = blocks_for(nnz, kTileE);
+    if (nrec <= 0) return;
+    const unsigned nb = blocks_for(nrec, kTileE);
     if (a.vbytes == 8 && a.val)
-        slab_extract<8><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, nnz, c0, c1, rec_rp, row_lo, rkey, rrow, rval);
+        slab_extract<8><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, rkey, rrow, rval);
     else if (a.vbytes == 4 && a.val)
-        slab_extract<4><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, nnz, c0, c1, rec_rp, row_lo, rkey, rrow, rval);
+        slab_extract<4><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, rkey, rrow, rval);
     else
-        slab_extract<0><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, nnz, c0, c1, rec_rp, row_lo, rkey, rrow, rval);
+        slab_extract<0><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, rkey, rrow, rval);
 }
 
 void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint32_t* skey, const uint32_t* srow,
@@ -241,11 +255,6 @@ void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint
         slab_place<4><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, cstart, f_rp, f_ci, f_val);
     else
         slab_place<0><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, cstart, f_rp, f_ci, f_val);
-}
-
-void mirror_col_counts(const MirrorArgs& a, const int64_t* full_len, int64_t* colcnt, hipStream_t s) {
-    if (a.m <= 0) return;
-    col_counts<<<blocks_for(a.m, kBlock), kBlock, 0, s>>>(a.rp, a.m, full_len, colcnt);
 }
 
 }  // namespace spsyrk
