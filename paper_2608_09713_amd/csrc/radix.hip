@@ -76,9 +76,9 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     __shared__ uint32_t wcnt[kWavesPerBlock][kDigits];
     __shared__ int64_t gofs[kDigits];  // global position of the tile's digit run minus its tile start
     __shared__ uint32_t wt[kWavesPerBlock];
-    __shared__ uint32_t ex_key[kRTile];
-    __shared__ uint32_t ex_row[kRTile];
-    __shared__ V ex_val[VB ? kRTile : 1];
+    // the tile is reordered through one buffer, a field at a time
+    __shared__ V ex[kRTile];
+    __shared__ uint8_t dig[kRTile];
 
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -170,26 +170,33 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         }
     }
     __syncthreads();
+    // tile positions of the records (registers), then keys, rows and values in turn
 #pragma unroll
     for (int k = 0; k < kRItems; ++k) {
         const int64_t idx = segbase + int64_t(k) * kWave + lane;
         if (idx < n) {
             const uint32_t d = (kr[k] >> shift) & mask;
-            const uint32_t pos = wcnt[w][d] + loc[k];
-            ex_key[pos] = kr[k];
-            ex_row[pos] = rr[k];
-            if constexpr (VB != 0) ex_val[pos] = vr[k];
+            loc[k] += wcnt[w][d];
+            ex[loc[k]] = V(kr[k]);
+            dig[loc[k]] = uint8_t(d);
         }
     }
     __syncthreads();
     const int tile_n = int(min(int64_t(kRTile), n - base));
-    for (int i = threadIdx.x; i < tile_n; i += kBlock) {
-        const uint32_t key = ex_key[i];
-        const uint32_t d = (key >> shift) & mask;
-        const int64_t g = gofs[d] + i;
-        key_out[g] = key;
-        row_out[g] = ex_row[i];
-        if constexpr (VB != 0) val_out[g] = ex_val[i];
+    for (int i = threadIdx.x; i < tile_n; i += kBlock) key_out[gofs[dig[i]] + i] = uint32_t(ex[i]);
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k)
+        if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = V(rr[k]);
+    __syncthreads();
+    for (int i = threadIdx.x; i < tile_n; i += kBlock) row_out[gofs[dig[i]] + i] = uint32_t(ex[i]);
+    if constexpr (VB != 0) {
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k)
+            if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = vr[k];
+        __syncthreads();
+        for (int i = threadIdx.x; i < tile_n; i += kBlock) val_out[gofs[dig[i]] + i] = ex[i];
     }
 }
 
