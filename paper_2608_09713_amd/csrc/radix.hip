@@ -16,7 +16,7 @@ namespace {
 
 constexpr int kRBits = 8;
 constexpr int kDigits = 1 << kRBits;
-constexpr int kRItems = 16;
+constexpr int kRItems = 12;
 constexpr int kRTile = kBlock * kRItems;  // 4096 records per tile
 constexpr int kSeg = kWave * kRItems;     // 1024 records per wave
 
