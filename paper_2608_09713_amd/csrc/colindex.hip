@@ -15,23 +15,31 @@ namespace {
 
 constexpr int kPTile = 2048;  // positions per pack workgroup
 
-__global__ __launch_bounds__(kBlock) void start_flags(const uint32_t* __restrict__ scol, int64_t n,
-                                                      uint32_t* __restrict__ st) {
-    const int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (p >= n) return;
-    st[p] = (p == 0 || scol[p] != scol[p - 1]) ? 1u : 0u;
+// column starts (first entry of a column) in every pack tile
+__global__ __launch_bounds__(kBlock) void tile_starts(const uint32_t* __restrict__ scol, int64_t n,
+                                                      uint32_t* __restrict__ tcnt) {
+    __shared__ uint32_t wt[kWavesPerBlock];
+    const int64_t base = int64_t(blockIdx.x) * kPTile;
+    const int64_t end = min(n, base + kPTile);
+    uint32_t c = 0;
+    for (int64_t p = base + threadIdx.x; p < end; p += kBlock) c += (p == 0 || scol[p] != scol[p - 1]) ? 1u : 0u;
+    uint32_t tot;
+    (void)block_exclusive_scan(c, wt, &tot);
+    if (threadIdx.x == 0) tcnt[blockIdx.x] = tot;
 }
 
 template <int VB, bool JAC>
 __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol, const uint32_t* __restrict__ srow,
                                                const uint32_t* __restrict__ sent, const void* __restrict__ vals_b,
-                                               uint2* __restrict__ run, int64_t n, const uint32_t* __restrict__ excl,
+                                               uint2* __restrict__ run, int64_t n, const uint32_t* __restrict__ tbase,
                                                bool drop_last, int gs, int rowbits, int lenbits, int64_t ngroups,
                                                const int64_t* __restrict__ nkept, const int64_t* __restrict__ rp_b,
                                                uint32_t* __restrict__ key, void* __restrict__ val,
                                                uint32_t* __restrict__ gptr) {
     __shared__ int64_t colstart[kPTile];
+    __shared__ uint32_t excl[kPTile];  // column starts before each position
     __shared__ int64_t wt[kWavesPerBlock];
+    __shared__ uint32_t wt32[kWavesPerBlock];
     __shared__ int64_t carry_s;
     const int64_t base = int64_t(blockIdx.x) * kPTile;
     const int64_t end = min(n, base + kPTile);
@@ -47,6 +55,23 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
                 hi = mid;
         }
         carry_s = lo;
+    }
+    {
+        // column starts before each position: the tile's base plus a block scan
+        constexpr int kPer = kPTile / kBlock;
+        uint32_t sc[kPer];
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int64_t p = base + int64_t(threadIdx.x) * kPer + k;
+            sc[k] = cnt;
+            cnt += (p < end && (p == 0 || scol[p] != scol[p - 1])) ? 1u : 0u;
+        }
+        uint32_t tot;
+        const uint32_t pre = block_exclusive_scan(cnt, wt32, &tot) + tbase[blockIdx.x];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) excl[threadIdx.x * kPer + k] = pre + sc[k];
+        __syncthreads();
     }
     if (run) {
         // inclusive max-scan of "position if it starts a column" over the tile
@@ -92,7 +117,7 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
         const uint32_t field = srow[p];
         const uint32_t row = field & rowmask;
         // kept entries before p: every column entirely before p lost its last entry
-        const int64_t cols_before = int64_t(excl[p]) + (start ? 1 : 0) - 1;
+        const int64_t cols_before = int64_t(excl[p - base]) + (start ? 1 : 0) - 1;
         if (run) {
             // partners of this entry (j < row): the kept entries that open its column
             const int64_t rank = p - colstart[p - base];
@@ -141,14 +166,16 @@ __global__ __launch_bounds__(kBlock) void empty_directory(int64_t ngroups, uint3
 }  // namespace
 
 size_t colindex_tmp_bytes(int64_t n) {
-    return ((size_t(n) * 4 + 255) & ~size_t(255)) + 256 + scan_tmp_bytes(n);
+    const int64_t nt = (n + kPTile - 1) / kPTile;
+    return ((size_t(nt + 1) * 4 + 255) & ~size_t(255)) + 256 + scan_tmp_bytes(nt + 1);
 }
 
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries, bool drop_last,
                     int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits, ColIndex& cx, void* tmp,
                     int64_t* d_nkept, uint2* run, hipStream_t s) {
-    uint32_t* excl = static_cast<uint32_t*>(tmp);
-    char* after = static_cast<char*>(tmp) + ((size_t(n_entries) * 4 + 255) & ~size_t(255));
+    const int64_t ntp = (n_entries + kPTile - 1) / kPTile;
+    uint32_t* tbase = static_cast<uint32_t*>(tmp);
+    char* after = static_cast<char*>(tmp) + ((size_t(ntp + 1) * 4 + 255) & ~size_t(255));
     uint32_t* ncols = reinterpret_cast<uint32_t*>(after);
     void* scan_tmp = after + 256;
     const int64_t n = n_entries;
@@ -160,14 +187,13 @@ void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* 
         }
         return;
     }
-    const unsigned nb = unsigned((n + kBlock - 1) / kBlock);
-    start_flags<<<nb, kBlock, 0, s>>>(scol, n, excl);
-    scan_u32(excl, excl, n, ncols, scan_tmp, s);
+    const unsigned np = unsigned(ntp);
+    tile_starts<<<np, kBlock, 0, s>>>(scol, n, tbase);
+    scan_u32(tbase, tbase, ntp, ncols, scan_tmp, s);
     // the number of distinct columns fixes the kept count and the directory's end
     kept_count<<<1, 1, 0, s>>>(n, ncols, drop_last, d_nkept);
-    const unsigned np = unsigned((n + kPTile - 1) / kPTile);
 #define SPSYRK_PACK(VBv, JACv)                                                                                    \
-    pack<VBv, JACv><<<np, kBlock, 0, s>>>(scol, srow, sent, vals_b, run, n, excl, drop_last, cx.gs, cx.rowbits,   \
+    pack<VBv, JACv><<<np, kBlock, 0, s>>>(scol, srow, sent, vals_b, run, n, tbase, drop_last, cx.gs, cx.rowbits,  \
                                           lenbits, cx.ngroups, d_nkept, rp_b, cx.key, cx.val, cx.gptr)
     if (sr == kJaccard)
         SPSYRK_PACK(0, true);

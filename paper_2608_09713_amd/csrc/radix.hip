@@ -17,8 +17,8 @@ namespace {
 constexpr int kRBits = 8;
 constexpr int kDigits = 1 << kRBits;
 constexpr int kRItems = 12;
-constexpr int kRTile = kBlock * kRItems;  // 4096 records per tile
-constexpr int kSeg = kWave * kRItems;     // 1024 records per wave
+constexpr int kRTile = kBlock * kRItems;  // records per tile
+constexpr int kSeg = kWave * kRItems;     // records per wave
 
 template <int VB>
 struct ValT {

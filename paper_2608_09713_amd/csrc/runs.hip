@@ -60,8 +60,19 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
     const int64_t b = min(e1, a + kPerT);
     if (a < b) {
         uint2 rn[kPerT];
+        if (b - a == kPerT && (reinterpret_cast<uintptr_t>(run + a) & 15) == 0) {
+            // whole stretch: 16-byte loads
+            const uint4* v4 = reinterpret_cast<const uint4*>(run + a);
 #pragma unroll
-        for (int u = 0; u < kPerT; ++u) rn[u] = a + u < b ? run[a + u] : make_uint2(0u, 0u);
+            for (int u = 0; u < kPerT / 2; ++u) {
+                const uint4 q = v4[u];
+                rn[2 * u] = make_uint2(q.x, q.y);
+                rn[2 * u + 1] = make_uint2(q.z, q.w);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kPerT; ++u) rn[u] = a + u < b ? run[a + u] : make_uint2(0u, 0u);
+        }
         // row of the stretch's first entry and its bounds
         int64_t r = staged ? rlo + last_leq(win, 0, rhi - rlo, a) : last_leq(rp, rlo, rhi, a);
         int64_t rstart = staged ? win[r - rlo] : rp[r];

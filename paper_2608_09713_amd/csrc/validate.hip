@@ -66,8 +66,27 @@ __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ 
             int64_t rend = r < m ? (staged ? win[r - rlo + 1] : rp[r + 1]) : nnz;
             int32_t prev = ea > 0 ? ci[ea - 1] : -1;
             bool first = staged ? win[r - rlo] == ea : rp[r] == ea;
-            for (int64_t e = ea; e < eb; ++e) {
-                const int32_t c = ci[e];
+            // the stretch's column ids, by 16-byte loads when whole and aligned
+            int32_t cc[kPerE];
+            if (eb - ea == kPerE && (reinterpret_cast<uintptr_t>(ci + ea) & 15) == 0) {
+                const int4* v4 = reinterpret_cast<const int4*>(ci + ea);
+#pragma unroll
+                for (int u = 0; u < kPerE / 4; ++u) {
+                    const int4 q = v4[u];
+                    cc[4 * u] = q.x;
+                    cc[4 * u + 1] = q.y;
+                    cc[4 * u + 2] = q.z;
+                    cc[4 * u + 3] = q.w;
+                }
+            } else {
+#pragma unroll
+                for (int u = 0; u < kPerE; ++u) cc[u] = ea + u < eb ? ci[ea + u] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < kPerE; ++u) {
+                const int64_t e = ea + u;
+                if (e >= eb) break;
+                const int32_t c = cc[u];
                 if (e >= rend) {
                     // next non-empty row (a malformed row_ptr ends the walk at row m)
                     while (e >= rend && r < m) {
