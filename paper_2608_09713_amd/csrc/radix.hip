@@ -99,8 +99,39 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         rlo = rbounds[0];
         rhi = rbounds[1];
         rstaged = rhi - rlo + 2 <= kRowWin + 1;
-        if (rstaged)
+        if (rstaged) {
             for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) rwin[k] = rp[rlo + k];
+            // window row of every tile position (in the exchange buffer, free
+            // until the records are reordered): every non-empty row marks its
+            // first position, then a max-scan over the tile
+            uint32_t* rowof = reinterpret_cast<uint32_t*>(ex);
+            for (int i = threadIdx.x; i < kRTile; i += kBlock) rowof[i] = 0;
+            __syncthreads();
+            for (int64_t k = 1 + threadIdx.x; k <= rhi - rlo; k += kBlock)
+                if (rwin[k] < rwin[k + 1]) rowof[rwin[k] - base] = uint32_t(k);
+            __syncthreads();
+            uint32_t run_max = 0;
+#pragma unroll
+            for (int k = 0; k < kRItems; ++k) run_max = max(run_max, rowof[threadIdx.x * kRItems + k]);
+            // exclusive max over the preceding threads
+            uint32_t inc = run_max;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const uint32_t u = __shfl_up(inc, d, kWave);
+                if (lane >= d) inc = max(inc, u);
+            }
+            if (lane == kWave - 1) wt[w] = inc;
+            __syncthreads();
+            uint32_t before = 0;
+            for (int q = 0; q < w; ++q) before = max(before, wt[q]);
+            const uint32_t prev = __shfl_up(inc, 1, kWave);
+            if (lane > 0) before = max(before, prev);
+#pragma unroll
+            for (int k = 0; k < kRItems; ++k) {
+                before = max(before, rowof[threadIdx.x * kRItems + k]);
+                rowof[threadIdx.x * kRItems + k] = before;
+            }
+        }
         __syncthreads();
     }
     uint32_t kr[kRItems], rr[kRItems], loc[kRItems];
@@ -130,7 +161,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             if (valid) {
                 int64_t r, len;
                 if (rstaged) {
-                    const int64_t rl = last_leq_i64(rwin, 0, rhi - rlo, idx);
+                    const int64_t rl = reinterpret_cast<const uint32_t*>(ex)[idx - base];
                     r = rlo + rl;
                     len = rwin[rl + 1] - rwin[rl];
                 } else {
