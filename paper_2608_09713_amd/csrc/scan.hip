@@ -63,23 +63,35 @@ template <typename T>
 __global__ __launch_bounds__(kBlock) void tile_scan(const T* __restrict__ in, T* __restrict__ out, int64_t n,
                                                     const T* __restrict__ sums) {
     __shared__ T wt[kWavesPerBlock];
+    __shared__ T buf[kTile];
     const int64_t base = int64_t(blockIdx.x) * kTile;
-    // blocked arrangement: thread t holds kItems consecutive elements
+    // coalesced loads into LDS, then a blocked arrangement: thread t holds
+    // kItems consecutive elements
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+        const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
+        buf[k * kBlock + threadIdx.x] = i < n ? in[i] : T(0);
+    }
+    __syncthreads();
     T v[kItems];
     T s = 0;
 #pragma unroll
     for (int k = 0; k < kItems; ++k) {
-        int64_t i = base + int64_t(threadIdx.x) * kItems + k;
-        v[k] = i < n ? in[i] : T(0);
+        v[k] = buf[threadIdx.x * kItems + k];
         s += v[k];
     }
     T tot;
     T off = block_exclusive_scan(s, wt, &tot) + sums[blockIdx.x];
 #pragma unroll
     for (int k = 0; k < kItems; ++k) {
-        int64_t i = base + int64_t(threadIdx.x) * kItems + k;
-        if (i < n) out[i] = off;
+        buf[threadIdx.x * kItems + k] = off;
         off += v[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kItems; ++k) {
+        const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
+        if (i < n) out[i] = buf[k * kBlock + threadIdx.x];
     }
 }
 
