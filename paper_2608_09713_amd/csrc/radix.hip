@@ -31,17 +31,30 @@ struct ValT<8> {
 
 __global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
                                                      uint32_t mask, uint32_t* __restrict__ hist, int64_t ntiles) {
-    __shared__ uint32_t cnt[kDigits];
-    cnt[threadIdx.x] = 0;
+    // one sub-histogram per wavefront keeps the LDS atomics of different
+    // wavefronts apart
+    __shared__ uint32_t cnt[kWavesPerBlock][kDigits];
+    const int w = threadIdx.x / kWave;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) cnt[q][threadIdx.x] = 0;
     __syncthreads();
     const int64_t base = int64_t(blockIdx.x) * kRTile;
-#pragma unroll 4
+    uint32_t kk[kRItems];
+#pragma unroll
     for (int k = 0; k < kRItems; ++k) {
         const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
-        if (i < n) atomicAdd(&cnt[(keys[i] >> shift) & mask], 1u);
+        kk[k] = i < n ? keys[i] : 0xffffffffu;
+    }
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k) {
+        const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
+        if (i < n) atomicAdd(&cnt[w][(kk[k] >> shift) & mask], 1u);
     }
     __syncthreads();
-    hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
+    uint32_t t = 0;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) t += cnt[q][threadIdx.x];
+    hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = t;
 }
 
 constexpr int kRowWin = 1024;
