@@ -132,6 +132,8 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     __shared__ int64_t wub[kCWin + 1];  // staging slot of the window's rows
     __shared__ int64_t wend[kCWin];     // end of each row's valid staged entries
     __shared__ int64_t wdel[kCWin];     // final position minus staging slot
+    __shared__ uint16_t rowof[kCTile];  // window row of every slot of the tile
+    __shared__ uint32_t wt[kWavesPerBlock];
     __shared__ int64_t bounds[2];
     const int64_t s0 = int64_t(blockIdx.x) * kCTile;
     const int64_t s1 = min(staged, s0 + kCTile);
@@ -143,18 +145,50 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     const int64_t rlo = bounds[0], rhi = bounds[1];
     const int64_t nrw = rhi - rlo + 1;
     const bool win_ok = nrw <= kCWin;
-    if (win_ok)
+    if (win_ok) {
+        for (int x = threadIdx.x; x < kCTile; x += kBlock) rowof[x] = 0;
         for (int64_t k = threadIdx.x; k < nrw; k += kBlock) {
             const int64_t u = ubp[rlo + k];
             wub[k] = u;
             wend[k] = u + row_cnt[rlo + k];
             wdel[k] = c_rp[rlo + k] - u;
         }
+        __syncthreads();
+        // every row with staging room marks its first slot in the tile (a row
+        // without room shares its slot with a later row and marks nothing),
+        // then a max-scan gives each slot its row
+        for (int64_t k = 1 + threadIdx.x; k < nrw; k += kBlock)
+            if (k == nrw - 1 || wub[k] < wub[k + 1]) rowof[wub[k] - s0] = uint16_t(k);
+        __syncthreads();
+        constexpr int kPer = kCTile / kBlock;
+        const int lane = lane_id();
+        const int w = threadIdx.x / kWave;
+        uint32_t run_max = 0;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) run_max = max(run_max, uint32_t(rowof[threadIdx.x * kPer + q]));
+        uint32_t inc = run_max;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t u = __shfl_up(inc, d, kWave);
+            if (lane >= d) inc = max(inc, u);
+        }
+        if (lane == kWave - 1) wt[w] = inc;
+        __syncthreads();
+        uint32_t before = 0;
+        for (int q = 0; q < w; ++q) before = max(before, wt[q]);
+        const uint32_t prev = __shfl_up(inc, 1, kWave);
+        if (lane > 0) before = max(before, prev);
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            before = max(before, uint32_t(rowof[threadIdx.x * kPer + q]));
+            rowof[threadIdx.x * kPer + q] = uint16_t(before);
+        }
+    }
     __syncthreads();
     for (int64_t sl = s0 + threadIdx.x; sl < s1; sl += kBlock) {
         int64_t end, del;
         if (win_ok) {
-            const int64_t k = last_leq(wub, 0, nrw - 1, sl);
+            const int k = rowof[sl - s0];
             end = wend[k];
             del = wdel[k];
         } else {
