@@ -84,7 +84,7 @@ struct WaveLds {
     uint16_t s_t[kFP];
     uint16_t s_rank[kFP];     // large buckets: rank of a leader, 0xffff for the other products
     uint16_t big[kFP / (kSmall + 1) + 1];  // large buckets of the batch
-    uint32_t nbig, nmid, nsmall;
+    uint32_t nbig;
     int64_t rbase[kFR];
     Item s_v[kFP];
     uint32_t hist[kFB + 1];
@@ -278,11 +278,6 @@ struct Chunk {
                 if constexpr (SR == kJaccard || kVal) L.s_v[q] = pv[v];
             }
         }
-        if (lane == 0) {
-            L.nbig = 0;
-            L.nmid = 0;
-            L.nsmall = 0;
-        }
         wave_sync();
         // Buckets by size: empty and single-product buckets are done at once;
         // the others are listed by size class so that every class runs with
@@ -292,32 +287,46 @@ struct Chunk {
         // in order at the bucket's start with their term counts in s_rank;
         // ucnt[b] = distinct columns.  Larger buckets go to the cooperative
         // pass below.  (The entry arrays are free by now and hold the lists.)
-        uint16_t* list_small = reinterpret_cast<uint16_t*>(L.ent_start);
-        uint16_t* list_mid = L.ent_len;
-        for (uint32_t b = lane; b < B; b += kWave) {
-            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            const uint32_t sz = hi - lo;
-            uint32_t d = sz;
-            if (sz == 1) {
-                L.s_rank[lo] = 1;
-            } else if (sz > uint32_t(kSmall)) {
-                L.big[atomicAdd(&L.nbig, 1u)] = uint16_t(b);
-                d = 0;
-            } else if (sz > uint32_t(kSmall / 2)) {
-                list_mid[atomicAdd(&L.nmid, 1u)] = uint16_t(b);
-            } else if (sz > 1) {
-                list_small[atomicAdd(&L.nsmall, 1u)] = uint16_t(b);
+        uint16_t* list2 = reinterpret_cast<uint16_t*>(L.ent_start);       // 2 products
+        uint16_t* list4 = reinterpret_cast<uint16_t*>(L.ent_start) + kFE;  // 3 or 4
+        uint16_t* list8 = L.ent_len;                                       // 5 to 8
+        uint32_t n2 = 0, n4 = 0, n8 = 0, nlarge = 0;  // (wave-uniform list lengths)
+        const uint64_t lt = lanemask_lt();
+        for (uint32_t b0 = 0; b0 < B; b0 += kWave) {
+            const uint32_t b = b0 + lane;
+            uint32_t sz = 0, lo = 0;
+            if (b < B) {
+                lo = b ? L.hist[b - 1] : 0u;
+                sz = L.hist[b] - lo;
+                if (sz == 1) L.s_rank[lo] = 1;
+                L.ucnt[b] = sz <= 1 ? sz : 0u;
             }
-            L.ucnt[b] = d;
+            // wave-aggregated appends
+            const uint64_t m2 = __ballot(sz == 2), m4 = __ballot(sz == 3 || sz == 4);
+            const uint64_t m8 = __ballot(sz > 4 && sz <= uint32_t(kSmall)), mb = __ballot(sz > uint32_t(kSmall));
+            if (sz == 2) list2[n2 + __popcll(m2 & lt)] = uint16_t(b);
+            if (sz == 3 || sz == 4) list4[n4 + __popcll(m4 & lt)] = uint16_t(b);
+            if (sz > 4 && sz <= uint32_t(kSmall)) list8[n8 + __popcll(m8 & lt)] = uint16_t(b);
+            if (sz > uint32_t(kSmall)) L.big[nlarge + __popcll(mb & lt)] = uint16_t(b);
+            n2 += __popcll(m2);
+            n4 += __popcll(m4);
+            n8 += __popcll(m8);
+            nlarge += __popcll(mb);
         }
+        if (lane == 0) L.nbig = nlarge;
         wave_sync();
-        for (uint32_t q = lane; q < L.nsmall; q += kWave) {
-            const uint32_t b = list_small[q];
+        for (uint32_t q = lane; q < n2; q += kWave) {
+            const uint32_t b = list2[q];
+            const uint32_t lo = b ? L.hist[b - 1] : 0u;
+            L.ucnt[b] = merge_two(lo);
+        }
+        for (uint32_t q = lane; q < n4; q += kWave) {
+            const uint32_t b = list4[q];
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
             L.ucnt[b] = merge_small<kSmall / 2>(lo, hi - lo);
         }
-        for (uint32_t q = lane; q < L.nmid; q += kWave) {
-            const uint32_t b = list_mid[q];
+        for (uint32_t q = lane; q < n8; q += kWave) {
+            const uint32_t b = list8[q];
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
             L.ucnt[b] = merge_small<kSmall>(lo, hi - lo);
         }
@@ -444,6 +453,33 @@ struct Chunk {
             }
         }
         return d;
+    }
+
+    // A bucket of two products at lo: ordered by (column, product index),
+    // merged if the columns are equal.  Returns the distinct columns.
+    __device__ uint32_t merge_two(uint32_t lo) {
+        uint32_t j0 = L.s_j[lo], j1 = L.s_j[lo + 1];
+        uint32_t t0 = L.s_t[lo], t1 = L.s_t[lo + 1];
+        Item v0 = L.s_v[lo], v1 = L.s_v[lo + 1];
+        if (j0 == j1) {
+            if constexpr (kVal) {
+                // terms in product order
+                L.s_v[lo] = t0 < t1 ? v0 + v1 : v1 + v0;
+            }
+            L.s_rank[lo] = 2;
+            return 1;
+        }
+        if (j1 < j0) {
+            L.s_j[lo] = j1;
+            L.s_j[lo + 1] = j0;
+            L.s_t[lo] = uint16_t(t1);
+            L.s_t[lo + 1] = uint16_t(t0);
+            L.s_v[lo] = v1;
+            L.s_v[lo + 1] = v0;
+        }
+        L.s_rank[lo] = 1;
+        L.s_rank[lo + 1] = 1;
+        return 2;
     }
 
     // value of a merged column: the sum (plus-times), the count, or the
