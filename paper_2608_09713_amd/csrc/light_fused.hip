@@ -148,7 +148,7 @@ struct Chunk {
     // for the light rows [ra, rb), whose runs were fetched into rn.  The
     // batch's columns stay in LDS, grouped by (row, bucket).  The runs of the
     // next batch [na, nb) (if na >= 0) are fetched into rn while the batch's
-    // keys are in flight.  Returns the number of buckets.
+    // keys are in flight.  Returns the number of products.
     __device__ int batch(int ra, int rb, uint2 (&rn)[kRunRegs], int na, int nbx) {
         const int64_t ebase = L.rp[ra];
         const int ne = int(L.rp[rb] - ebase);
@@ -273,6 +273,8 @@ struct Chunk {
             const int t = lane + v * kWave;
             if (t < P) {
                 const uint32_t q = atomicAdd(&L.hist[pb[v] & 0xffffu], 1u);
+                // (the owner array is free by now: it keeps every slot's bucket)
+                reinterpret_cast<uint16_t*>(L.owner)[q] = uint16_t(pb[v] & 0xffffu);
                 L.s_j[q] = pj[v];
                 L.s_t[q] = uint16_t(uint32_t(t) | ((pb[v] >> 16) << kTBits));
                 if constexpr (SR == kJaccard || kVal) L.s_v[q] = pv[v];
@@ -399,7 +401,7 @@ struct Chunk {
         // first output slot of every row minus its first bucket's offset
         if (lane < nrb) L.rbase[ra + lane] = L.rcnt[ra + lane] - int64_t(L.ucnt[L.rbb[ra + lane]]);
         wave_sync();
-        return int(B);
+        return P;
     }
 
     // Sort the sz (<= N) products at [lo, lo + sz) by (column, product index)
@@ -504,36 +506,32 @@ struct Chunk {
         v[y] = vy;
     }
 
-    // Write the batch left in LDS by batch(ra, rb, ...): rcnt holds each row's
-    // first output slot, rbase that slot minus the offset of the row's first
-    // bucket.
-    __device__ void write(int ra, int rb, int B) {
-        // every output of the batch, in output order, points at its column's
-        // slot (the top bit marks a value already final: large buckets); the
-        // owner array is free by now and holds the map
-        uint16_t* omap = reinterpret_cast<uint16_t*>(L.owner);
-        for (int b = lane; b < B; b += kWave) {
+    // Write the batch left in LDS by batch(ra, rb, ...) (nprod products):
+    // rcnt holds each row's first output slot, rbase that slot minus the
+    // offset of the row's first bucket.
+    __device__ void write(int ra, int rb, int nprod) {
+        // outputs in slot order (about output order), each found from its
+        // slot's bucket: consecutive lanes write consecutive slots of a row
+        const uint16_t* sbk = reinterpret_cast<const uint16_t*>(L.owner);
+        for (int q = lane; q < nprod; q += kWave) {
+            const uint32_t b = sbk[q];
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            if (hi == lo) continue;
             const uint32_t u0 = L.ucnt[b];
-            if (hi - lo <= uint32_t(kSmall)) {
-                const uint32_t d = L.ucnt[b + 1] - u0;
-                for (uint32_t k = 0; k < d; ++k) omap[u0 + k] = uint16_t(lo + k);
+            uint32_t k;
+            bool out;
+            const bool small = hi - lo <= uint32_t(kSmall);
+            if (small) {
+                k = uint32_t(q) - lo;
+                out = k < L.ucnt[b + 1] - u0;
             } else {
-                for (uint32_t u = lo; u < hi; ++u)
-                    if (L.s_rank[u] != 0xffff) omap[u0 + L.s_rank[u]] = uint16_t(u | 0x8000u);
+                k = L.s_rank[q];
+                out = k != 0xffffu;
             }
-        }
-        wave_sync();
-        // outputs written by consecutive lanes to consecutive slots of a row
-        const uint32_t U = L.ucnt[B];
-        for (uint32_t o = lane; o < U; o += kWave) {
-            const uint32_t mo = omap[o];
-            const uint32_t src = mo & 0x7fffu;
-            const int r = int(L.s_t[src] >> kTBits);
-            Item v = L.s_v[src];
-            if (!(mo & 0x8000u)) v = finish(v, int32_t(L.s_rank[src]), L.rp[r + 1] - L.rp[r]);
-            emit(L.rbase[r] + int64_t(o), L.s_j[src], v);
+            if (!out) continue;
+            const int r = int(L.s_t[q] >> kTBits);
+            Item v = L.s_v[q];
+            if (small) v = finish(v, int32_t(L.s_rank[q]), L.rp[r + 1] - L.rp[r]);
+            emit(L.rbase[r] + int64_t(u0 + k), L.s_j[q], v);
         }
         // diagonals (lower triangle): the last entry of every non-empty row
         if (LOWER && lane < rb - ra) {
@@ -654,10 +652,10 @@ struct Chunk {
         for (int k = 0; k < nbatch; ++k) {
             const int ra = L.bra[k], rb = L.brb[k];
             const bool more = k + 1 < nbatch;
-            const int B = batch(ra, rb, rn, more ? int(L.bra[k + 1]) : -1, more ? int(L.brb[k + 1]) : 0);
+            const int P = batch(ra, rb, rn, more ? int(L.bra[k + 1]) : -1, more ? int(L.brb[k + 1]) : 0);
             if (lane >= ra && lane < rb)
                 cnt += int64_t(L.ucnt[L.rbb[lane] + L.rnb[lane]] - L.ucnt[L.rbb[lane]]);
-            write(ra, rb, B);
+            write(ra, rb, P);
         }
         if (lane < nr) a.row_cnt[r0 + lane] = cnt;
     }

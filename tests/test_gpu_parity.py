@@ -123,6 +123,25 @@ def test_long_rows_use_heavy_rows(dev, semiring):
     assert sp.stats()["heavy_rows"] >= 2
 
 
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_light_rows_with_many_shared_columns(dev, semiring):
+    # few columns, so that pairs of rows share several of them: the light
+    # rows' buckets hold repeated columns (merges of 2..8 terms and larger)
+    rng = np.random.default_rng(11)
+    m, n, d = 300, 24, 8
+    D = np.zeros((m, n))
+    for i in range(m):
+        D[i, rng.choice(n, size=d, replace=False)] = rng.random(d) + 0.25
+    run_lower(csr_from_dense(D), semiring, dev, "shared columns")
+    assert sp.stats()["light_rows"] > 0
+    # identical rows: every output of a light row sums 10 terms of one column
+    # index, more than a register-sorted bucket holds
+    E = np.zeros((60, 50))
+    E[:, 5:15] = rng.random((60, 10)) + 0.25
+    run_lower(csr_from_dense(E), semiring, dev, "identical rows")
+    assert sp.stats()["light_rows"] > 0
+
+
 WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
              ("offdiag_f64", 5)]
 
