@@ -20,12 +20,13 @@ namespace {
 thread_local std::string g_detail;
 thread_local spsyrk_stats g_stats;
 thread_local bool g_stats_valid = false;
-// lower triangle through the two-pass kernels instead of the single pass
-// (SPSYRK_LOWER_TWO_PASS=1; used to cross-check the two implementations)
-const bool g_two_pass = [] {
-    const char* e = std::getenv("SPSYRK_LOWER_TWO_PASS");
+// the two-pass kernels (symbolic, then numeric, partner runs looked up in a
+// directory) instead of the single pass, for both calls (SPSYRK_TWO_PASS=1,
+// read at every call; used to cross-check the two implementations)
+bool two_pass() {
+    const char* e = std::getenv("SPSYRK_TWO_PASS");
     return e && e[0] == '1';
-}();
+}
 
 constexpr int64_t kLimit = int64_t(1) << 31;
 
@@ -239,8 +240,9 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 
 // Build the column index of B (sorted by column, packed keys, directory).
 // With run (zeroed beforehand; lower mode) every entry's partner run is written.
+// need_dir: build the group directory for partner-run lookups.
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                     uint2* run = nullptr) {
+                     uint2* run = nullptr, bool need_dir = true) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -256,9 +258,9 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
     if (gs > maxgs) gs = maxgs;
     const int nbits_n = bit_width_u64(B.n > 1 ? uint64_t(B.n - 1) : 0);
     if (gs > nbits_n) gs = nbits_n;
-    // with every partner run given (lower mode) nothing is ever looked up:
-    // no directory, and the keys hold the row only
-    const bool runs_given = run != nullptr;
+    // with every partner run given nothing is ever looked up: no directory,
+    // and the keys hold the row only
+    const bool runs_given = run != nullptr || !need_dir;
     if (runs_given) gs = 0;
     cx.gs = gs;
     cx.ngroups = B.n > 0 ? ((B.n + (int64_t(1) << gs) - 1) >> gs) : 0;
@@ -322,22 +324,38 @@ int rows_per_chunk(double) {
     return kFusedRows;
 }
 
-// C_L = tril(A A^T): column index with the partner run of every entry,
-// per-row product counts, row classes, dense-tile lengths of the heavy rows,
-// the light rows computed once into upper-bound staging slots with their
-// exact lengths, row pointers, compaction of the light rows, heavy rows'
-// values.
-void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, spsyrk_csr_out* C) {
+constexpr int64_t kDenseColumns = int64_t(1) << 26;  // dense column starts: at most 256 MB
+
+// C_L = tril(A A^T) (lower, R = L) or L R^T: column index with the partner
+// run of every entry, per-row product counts, row classes, exact lengths of
+// the heavy rows, the light rows computed once into upper-bound staging slots
+// with their exact lengths, row pointers, compaction of the light rows, heavy
+// rows' values.  Off the diagonal the column index of R keeps every entry and
+// the partner run of an entry of L in column k is the whole column k of R,
+// read from dense column starts.
+
+void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
+                spsyrk_csr_out* C) {
     const int64_t m = L.m;
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
     HIPCHK(hipMemsetAsync(prod, 0, size_t(m) * sizeof(unsigned long long), s));
     uint2* run = ar.get_t<uint2>(L.nnz);
-    HIPCHK(hipMemsetAsync(run, 0, size_t(L.nnz) * sizeof(uint2), s));
     ColIndex cx;
-    {
+    if (lower) {
+        HIPCHK(hipMemsetAsync(run, 0, size_t(L.nnz) * sizeof(uint2), s));
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
         cx = build_index(L, true, sr, ar, ctl, s, run);
+    } else {
+        Phase ph(SPSYRK_PHASE_COLINDEX, s);
+        cx = build_index(R, false, sr, ar, ctl, s, nullptr, false);
+        uint32_t* cptr = ar.get_t<uint32_t>(R.n + 1);
+        void* ctmp = ar.get(scan_tmp_bytes(R.n + 1));
+        column_starts(R.ci, R.nnz, R.n, cptr, ctmp, s);
+        offdiag_runs(L.ci, L.nnz, cptr, run, s);
+        check_launch();
+        ar.release(ctmp);
+        ar.release(cptr);
     }
     int32_t* heavy_rows = ar.get_t<int32_t>(m);
     int64_t* ub = ar.get_t<int64_t>(m + 1);
@@ -345,7 +363,7 @@ void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, sps
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
         row_products(L.rp, m, L.nnz, run, prod, s);
-        classify_rows(L.rp, prod, m, true, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s);
+        classify_rows(L.rp, prod, m, lower, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s);
     }
     check_launch();
     Ctl h = read_ctl(ctl, s);
@@ -360,9 +378,9 @@ void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, sps
         ha.ci = L.ci;
         ha.val = L.v;
         ha.cx = cx;
-        ha.m_right = L.m;
-        ha.rp_right = L.rp;
-        ha.lower = true;
+        ha.m_right = R.m;
+        ha.rp_right = R.rp;
+        ha.lower = lower;
         ha.sr = sr;
         ha.heavy_rows = heavy_rows;
         ha.heavy_count = &ctl->heavy_count;
@@ -392,8 +410,8 @@ void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, sps
     fa.ci = L.ci;
     fa.val = L.v;
     fa.cx = cx;
-    fa.m_right = L.m;
-    fa.lower = true;
+    fa.m_right = R.m;
+    fa.lower = lower;
     fa.sr = sr;
     fa.prod = prod;
     fa.run = run;
@@ -436,7 +454,7 @@ void syrk_lower(const DevCsr& L, int sr, Arena& ar, Ctl* ctl, hipStream_t s, sps
         check_launch();
     }
     C->nrows = m;
-    C->ncols = m;
+    C->ncols = R.m;
     C->nnz = total;
     C->capacity = total;
     C->row_ptr = c_rp;
@@ -482,8 +500,10 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         return;
     }
 
-    if (lower && !g_two_pass) {
-        syrk_lower(L, sr, ar, ctl, s, C);
+    // single pass over the light rows; off the diagonal when the right
+    // operand's column starts fit a dense array (else the two-pass path)
+    if (!two_pass() && (lower || R.n <= kDenseColumns)) {
+        syrk_fused(L, R, lower, sr, ar, ctl, s, C);
         return;
     }
     int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);

@@ -143,6 +143,11 @@ void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m,
                    hipStream_t s);
 
 // ---- runs.hip
+// Dense column starts of a CSR matrix's column-sorted copy: cptr[c] =
+// entries in columns before c (n + 1 words; scan_tmp: scan_tmp_bytes(n + 1)).
+void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, void* scan_tmp, hipStream_t s);
+// Off-diagonal partner runs: run[e] = {cptr[ci[e]], cptr[ci[e] + 1]}.
+void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* run, hipStream_t s);
 // prod[i] = sum over the entries e of row i of run[e].y - run[e].x (prod
 // must start zeroed).
 void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, unsigned long long* prod,

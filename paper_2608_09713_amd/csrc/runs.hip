@@ -204,7 +204,40 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     }
 }
 
+// entries per column (scanned into column starts by the caller)
+__global__ __launch_bounds__(kBlock) void count_columns(const int32_t* __restrict__ ci, int64_t nnz,
+                                                        uint32_t* __restrict__ cnt) {
+    for (int64_t e = int64_t(blockIdx.x) * kBlock + threadIdx.x; e < nnz; e += int64_t(gridDim.x) * kBlock)
+        atomicAdd(&cnt[ci[e]], 1u);
+}
+
+// the partners of entry e of the left operand are the whole column ci[e] of
+// the right operand
+__global__ __launch_bounds__(kBlock) void offdiag_runs_kernel(const int32_t* __restrict__ ci, int64_t nnz,
+                                                              const uint32_t* __restrict__ cptr,
+                                                              uint2* __restrict__ run) {
+    const int64_t e = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (e >= nnz) return;
+    const int32_t c = ci[e];
+    run[e] = make_uint2(cptr[c], cptr[c + 1]);
+}
+
 }  // namespace
+
+void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, void* scan_tmp, hipStream_t s) {
+    (void)hipMemsetAsync(cptr, 0, size_t(n + 1) * sizeof(uint32_t), s);
+    if (nnz > 0) {
+        int64_t grid = (nnz + kBlock - 1) / kBlock;
+        if (grid > 65536) grid = 65536;
+        count_columns<<<unsigned(grid), kBlock, 0, s>>>(ci, nnz, cptr);
+    }
+    scan_u32(cptr, cptr, n + 1, nullptr, scan_tmp, s);
+}
+
+void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* run, hipStream_t s) {
+    if (nnz <= 0) return;
+    offdiag_runs_kernel<<<unsigned((nnz + kBlock - 1) / kBlock), kBlock, 0, s>>>(ci, nnz, cptr, run);
+}
 
 void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, unsigned long long* prod,
                   hipStream_t s) {

@@ -142,6 +142,30 @@ def test_light_rows_with_many_shared_columns(dev, semiring):
     assert sp.stats()["light_rows"] > 0
 
 
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_two_pass_path(dev, semiring, monkeypatch):
+    # the two-pass kernels (directory lookups, symbolic then numeric) that the
+    # off-diagonal call takes when the right operand has too many columns for
+    # dense column starts; forced here on small inputs, light and heavy rows
+    monkeypatch.setenv("SPSYRK_TWO_PASS", "1")
+    rng = np.random.default_rng(99)
+    A = random_csr(rng, 250, 300, 0.05, zeros=0.05)
+    run_lower(A, semiring, dev, "two-pass lower")
+    m = 2500
+    D = np.zeros((m, 4))
+    D[:, 2] = 1.0
+    D[::3, 0] = 0.5
+    run_lower(csr_from_dense(D), semiring, dev, "two-pass heavy rows")
+    assert sp.stats()["heavy_rows"] > 0
+    Ai = random_csr(rng, 120, 200, 0.05, signed=True)
+    Aj = random_csr(rng, 90, 200, 0.05, signed=True)
+    vdt = VDT[semiring]
+    O = sp.offdiag(upload(Ai, semiring, dev), upload(Aj, semiring, dev), semiring)
+    ref = oracle.offdiag(Ai.with_values(None if vdt is None else Ai.values.astype(vdt)),
+                         Aj.with_values(None if vdt is None else Aj.values.astype(vdt)), semiring)
+    compare_full(O, ref, semiring, "two-pass offdiag")
+
+
 WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
              ("offdiag_f64", 5)]
 
