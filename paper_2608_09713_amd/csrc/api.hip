@@ -2,10 +2,12 @@
 // output allocation through the caller's allocator, and the kernel sequence.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -614,6 +616,66 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     g_stats_valid = true;
 }
 
+// Strict-lower records per transpose slab: 2^31 (SPSYRK_MIRROR_SLAB, read at
+// every call, lowers it to exercise the multi-slab path on small inputs).
+int64_t mirror_slab_cap() {
+    if (const char* e = std::getenv("SPSYRK_MIRROR_SLAB")) {
+        const long long v = std::atoll(e);
+        if (v >= 1 && v < (1LL << 31)) return int64_t(v);
+    }
+    return int64_t(1) << 31;
+}
+
+// columns [c0, c1) of the strict lower part, nrec of its entries, and the
+// strict-lower entries in the columns before c0
+struct Slab {
+    int64_t c0, c1, nrec, before;
+};
+
+// Column slabs of at most cap strict-lower entries (a single column may hold
+// more: it is a slab of its own), chosen from bucket histograms; a bucket
+// over the cap is split by a finer histogram of its own columns.
+std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, Arena& ar, hipStream_t s) {
+    unsigned long long* hist = ar.get_t<unsigned long long>(kMirrorBins);
+    std::vector<unsigned long long> h(kMirrorBins);
+    std::vector<Slab> pieces;  // buckets (or single columns) in column order
+    std::function<void(int64_t, int64_t)> refine = [&](int64_t lo, int64_t hi) {
+        const int64_t w = hi - lo;
+        int cb = 0;
+        while (((w + (int64_t(1) << cb) - 1) >> cb) > kMirrorBins) ++cb;
+        const int nb = int((w + (int64_t(1) << cb) - 1) >> cb);
+        mirror_coarse_hist(ma, lo, cb, nb, hist, s);
+        check_launch();
+        HIPCHK(hipMemcpyAsync(h.data(), hist, size_t(nb) * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
+        HIPCHK(hipStreamSynchronize(s));
+        const std::vector<unsigned long long> hb(h.begin(), h.begin() + nb);
+        for (int b = 0; b < nb; ++b) {
+            const int64_t blo = lo + (int64_t(b) << cb);
+            const int64_t bhi = std::min(hi, blo + (int64_t(1) << cb));
+            if (int64_t(hb[size_t(b)]) > cap && bhi - blo > 1)
+                refine(blo, bhi);
+            else
+                pieces.push_back({blo, bhi, int64_t(hb[size_t(b)]), 0});
+        }
+    };
+    if (ma.m > 0) refine(0, ma.m);
+    std::vector<Slab> out;
+    Slab cur{0, 0, 0, 0};
+    int64_t before = 0;
+    for (const Slab& p : pieces) {
+        if (cur.c1 > cur.c0 && cur.nrec + p.nrec > cap) {
+            out.push_back(cur);
+            cur = {p.c0, p.c0, 0, before};
+        }
+        cur.c1 = p.c1;
+        cur.nrec += p.nrec;
+        before += p.nrec;
+    }
+    out.push_back(cur);
+    ar.release(hist);
+    return out;
+}
+
 void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
     Ctl* ctl = ar.get_t<Ctl>(1);
     zero_ctl(ctl, s);
@@ -631,91 +693,87 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     ma.val = L.v;
     ma.vbytes = vb;
 
-    int64_t* f_rp = ar.get_t<int64_t>(m + 1, true);
-    int64_t* full_len = f_rp;  // lengths first, scanned in place
-    int64_t* colcnt = ar.get_t<int64_t>(m + 1);
-    uint32_t* cnt32 = ar.get_t<uint32_t>(m > 0 ? m : 1);
-    HIPCHK(hipMemsetAsync(full_len + m, 0, sizeof(int64_t), s));
-    HIPCHK(hipMemsetAsync(colcnt + m, 0, sizeof(int64_t), s));
+    // The strict lower part is transposed in column slabs: records (column,
+    // row, value) extracted row-major, sorted stably by column, each column's
+    // record range read off the sorted keys, which gives the full row lengths
+    // and starts of the slab's rows, and every record placed after the lower
+    // part of its row.  The lower rows are copied once all starts are known.
+    const int64_t cap = mirror_slab_cap();
+    int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
+    int64_t* row_lo = ar.get_t<int64_t>(m > 0 ? m : 1);
     void* stmp = ar.get(scan_tmp_bytes(m + 1));
+    std::vector<Slab> slabs;
     {
         Phase ph(SPSYRK_PHASE_MIRROR_COUNT, s);
-        mirror_counts(ma, cnt32, full_len, colcnt, s);
-        scan_i64(colcnt, colcnt, m + 1, &ctl->total2, stmp, s);  // colcnt -> cstart
-        scan_i64(full_len, f_rp, m + 1, &ctl->total, stmp, s);
+        if (L.nnz <= cap) {
+            // one slab; its record count is the strict-lower count
+            HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
+            mirror_slab_counts(ma, 0, m, row_cnt, row_lo, s);
+            scan_i64(row_cnt, row_cnt, m + 1, &ctl->total, stmp, s);
+            check_launch();
+            const Ctl h = read_ctl(ctl, s);
+            slabs.push_back({0, m, h.total, 0});
+        } else {
+            slabs = plan_slabs(ma, cap, ar, s);
+        }
     }
-    check_launch();
-    Ctl h = read_ctl(ctl, s);
-    const int64_t total = h.total, nstrict = h.total2;
+    int64_t nstrict = 0, rec_max = 0, w_max = 0;
+    for (const Slab& sl : slabs) {
+        nstrict += sl.nrec;
+        rec_max = std::max(rec_max, sl.nrec);
+        w_max = std::max(w_max, sl.c1 - sl.c0);
+    }
+    const int64_t total = L.nnz + nstrict;
+    int64_t* f_rp = ar.get_t<int64_t>(m + 1, true);
     int32_t* f_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
     void* f_val = vb ? ar.get(size_t(total > 0 ? total : 1) * vb, true) : nullptr;
-    {
-        Phase ph(SPSYRK_PHASE_MIRROR_COPY, s);
-        mirror_copy_lower(ma, f_rp, f_ci, f_val, s);
-    }
-    check_launch();
+    HIPCHK(hipMemsetAsync(f_rp, 0, sizeof(int64_t), s));  // m == 0: the only row start
 
-    if (nstrict > 0) {
-        // column slabs of at most kSlab strict-lower entries (the whole range
-        // when it fits; a slab always holds at least one column)
-        const int64_t kSlab = int64_t(1) << 31;
-        std::vector<int64_t> bounds{0};
-        if (nstrict <= kSlab) {
-            bounds.push_back(m);
-        } else {
-            std::vector<int64_t> cst(size_t(m) + 1);
-            HIPCHK(hipMemcpyAsync(cst.data(), colcnt, size_t(m + 1) * sizeof(int64_t), hipMemcpyDeviceToHost, s));
-            HIPCHK(hipStreamSynchronize(s));
-            int64_t c0 = 0;
-            while (c0 < m) {
-                int64_t c1 = c0 + 1;
-                int64_t lo = c0 + 1, hi = m;  // largest c1 with cst[c1] - cst[c0] <= kSlab
-                while (lo <= hi) {
-                    const int64_t mid = (lo + hi) / 2;
-                    if (cst[mid] - cst[c0] <= kSlab) {
-                        c1 = mid;
-                        lo = mid + 1;
-                    } else {
-                        hi = mid - 1;
-                    }
-                }
-                if (cst[c1] - cst[c0] > kSlab && c1 == c0 + 1 && cst[c1] - cst[c0] >= kLimit) {
-                    set_detail("a single column of the lower part holds 2^31 or more entries");
-                    throw Fail{SPSYRK_ERR_SHAPE};
-                }
-                bounds.push_back(c1);
-                c0 = c1;
+    uint32_t* first = ar.get_t<uint32_t>(w_max > 0 ? w_max : 1);
+    uint32_t* endc = ar.get_t<uint32_t>(w_max > 0 ? w_max : 1);
+    uint32_t* ka = ar.get_t<uint32_t>(rec_max > 0 ? rec_max : 1);
+    uint32_t* kb = ar.get_t<uint32_t>(rec_max > 0 ? rec_max : 1);
+    uint32_t* ra = ar.get_t<uint32_t>(rec_max > 0 ? rec_max : 1);
+    uint32_t* rb = ar.get_t<uint32_t>(rec_max > 0 ? rec_max : 1);
+    void* va = vb ? ar.get(size_t(rec_max > 0 ? rec_max : 1) * vb) : nullptr;
+    void* vbb = vb ? ar.get(size_t(rec_max > 0 ? rec_max : 1) * vb) : nullptr;
+    void* rtmp = ar.get(radix_tmp_bytes(rec_max > 0 ? rec_max : 1));
+    for (size_t k = 0; k < slabs.size(); ++k) {
+        const Slab& sl = slabs[k];
+        if (sl.c1 <= sl.c0) continue;
+        Phase ph(SPSYRK_PHASE_MIRROR_TRANSPOSE, s);
+        if (k > 0 || L.nnz > cap) {
+            HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
+            mirror_slab_counts(ma, sl.c0, sl.c1, row_cnt, row_lo, s);
+            scan_i64(row_cnt, row_cnt, m + 1, &ctl->total, stmp, s);
+            check_launch();
+            if (read_ctl(ctl, s).total != sl.nrec) {  // the record buffers are sized from the histogram
+                set_detail("mirror: slab record count disagrees with the column histogram");
+                throw Fail{SPSYRK_ERR_HIP};
             }
         }
-        int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
-        int64_t* row_lo = ar.get_t<int64_t>(m);
-        void* rtmp_scan = ar.get(scan_tmp_bytes(m + 1));
-        const int64_t cap = nstrict < kSlab ? nstrict : kSlab;
-        uint32_t* ka = ar.get_t<uint32_t>(cap);
-        uint32_t* kb = ar.get_t<uint32_t>(cap);
-        uint32_t* ra = ar.get_t<uint32_t>(cap);
-        uint32_t* rb = ar.get_t<uint32_t>(cap);
-        void* va = vb ? ar.get(size_t(cap) * vb) : nullptr;
-        void* vbb = vb ? ar.get(size_t(cap) * vb) : nullptr;
-        void* rtmp = ar.get(radix_tmp_bytes(cap));
-        for (size_t k = 0; k + 1 < bounds.size(); ++k) {
-            const int64_t c0 = bounds[k], c1 = bounds[k + 1];
-            HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
-            mirror_slab_counts(ma, c0, c1, row_cnt, row_lo, s);
-            scan_i64(row_cnt, row_cnt, m + 1, &ctl->total, rtmp_scan, s);
-            check_launch();
-            h = read_ctl(ctl, s);
-            const int64_t nrec = h.total;
-            if (nrec == 0) continue;
-            Phase ph(SPSYRK_PHASE_MIRROR_TRANSPOSE, s);
-            mirror_slab_extract(ma, c0, nrec, row_cnt, row_lo, ka, ra, va, s);
-            const int nbits = bit_width_u64(c1 - c0 > 1 ? uint64_t(c1 - c0 - 1) : 0);
-            const int which = radix_sort(ka, kb, ra, rb, va, vbb, vb, nrec, nbits, rtmp, s);
-            mirror_slab_place(ma, c0, nrec, which ? kb : ka, which ? rb : ra, which ? vbb : va, colcnt, f_rp, f_ci,
-                              f_val, s);
-            check_launch();
+        const uint32_t* skey = ka;
+        const uint32_t* srow = ra;
+        const void* sval = va;
+        if (sl.nrec > 0) {
+            mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, ka, ra, va, s);
+            const int nbits = bit_width_u64(sl.c1 - sl.c0 > 1 ? uint64_t(sl.c1 - sl.c0 - 1) : 0);
+            if (radix_sort(ka, kb, ra, rb, va, vbb, vb, sl.nrec, nbits, rtmp, s)) {
+                skey = kb;
+                srow = rb;
+                sval = vbb;
+            }
         }
+        // row_cnt is free again: full lengths of the slab's rows
+        mirror_slab_columns(ma, sl.c0, sl.c1, skey, sl.nrec, first, endc, row_cnt, sl.before, f_rp, stmp, s);
+        mirror_slab_place(ma, sl.c0, sl.nrec, skey, srow, sval, first, f_rp, f_ci, f_val, s);
+        check_launch();
     }
+    {
+        Phase ph(SPSYRK_PHASE_MIRROR_COPY, s);
+        mirror_copy_lower(ma, 0, L.nnz, f_rp, f_ci, f_val, s);
+    }
+    check_launch();
     HIPCHK(hipStreamSynchronize(s));
     C->nrows = m;
     C->ncols = m;

@@ -196,11 +196,11 @@ struct MirrorArgs {
     const void* val = nullptr;
     int vbytes = 0;
 };
-// per-row length of the full matrix (lower length + strict-lower entries of
-// column i) and the strict-lower entries of every column; cnt is m words of
-// scratch (32-bit counters)
-void mirror_counts(const MirrorArgs& a, uint32_t* cnt, int64_t* full_len, int64_t* colcnt, hipStream_t s);
-void mirror_copy_lower(const MirrorArgs& a, const int64_t* f_rp, int32_t* f_ci, void* f_val, hipStream_t s);
+// strict-lower entries with clo <= col < clo + nb * 2^cb per bucket of 2^cb
+// columns (nb <= kMirrorBins), added into hist (zeroed here)
+constexpr int kMirrorBins = 4096;
+void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsigned long long* hist,
+                        hipStream_t s);
 // per-row counts and first entries of the strict lower part with col in [c0, c1)
 void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,
                         hipStream_t s);
@@ -208,10 +208,20 @@ void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* ro
 // given by rec_rp (exclusive scan of the per-row counts), nrec in all
 void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t nrec, const int64_t* rec_rp, const int64_t* row_lo,
                          uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s);
-// place sorted records: record s of column c goes to f_rp[c] + lower_len(c) + (s - (cstart[c] - cstart[c0]))
-// where cstart is the exclusive scan of strict-lower counts per column
+// from the slab's records sorted by column (keys skey): first[k] / end[k],
+// the record range of slab column k, and the full row starts f_rp[c0..c1]
+// (fl: w + 1 words of scratch; strict_before: strict-lower entries in the
+// columns before c0; first / end: w words each)
+void mirror_slab_columns(const MirrorArgs& a, int64_t c0, int64_t c1, const uint32_t* skey, int64_t nrec,
+                         uint32_t* first, uint32_t* end, int64_t* fl, int64_t strict_before, int64_t* f_rp,
+                         void* scan_tmp, hipStream_t s);
+// place sorted records: record s of slab column k goes to
+// f_rp[c0 + k] + lower_len(c0 + k) + (s - first[k])
 void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint32_t* skey, const uint32_t* srow,
-                       const void* sval, const int64_t* cstart, const int64_t* f_rp, int32_t* f_ci, void* f_val,
+                       const void* sval, const uint32_t* first, const int64_t* f_rp, int32_t* f_ci, void* f_val,
                        hipStream_t s);
+// lower rows' entries [ebeg, eend) to their places f_rp[row] + offset in row
+void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const int64_t* f_rp, int32_t* f_ci,
+                       void* f_val, hipStream_t s);
 
 }  // namespace spsyrk

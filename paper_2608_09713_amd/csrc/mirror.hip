@@ -73,56 +73,22 @@ __device__ inline RowFinder make_finder(const int64_t* rp, int64_t m, int64_t e0
     return f;
 }
 
-// Strict-lower entries per column (32-bit counters; a column holds fewer than
-// 2^31 entries).  Every thread walks kPerC contiguous entries row by row, so
-// the diagonal (the last entry of a row, col == row) is recognised without a
-// search per entry.
+// Every thread of a strict-lower walk takes kPerC contiguous entries row by
+// row, so the diagonal (the last entry of a row, col == row) is recognised
+// without a search per entry.
 constexpr int kPerC = 16;
 constexpr int kTileC = kBlock * kPerC;
 
-__global__ __launch_bounds__(kBlock) void count_transposed(const int64_t* __restrict__ rp,
-                                                           const int32_t* __restrict__ ci, int64_t m, int64_t nnz,
-                                                           uint32_t* __restrict__ cnt) {
-    __shared__ int64_t win[kWin + 1];
-    __shared__ int64_t bounds[2];
-    const int64_t e0 = int64_t(blockIdx.x) * kTileC;
-    const int64_t e1 = min(nnz, e0 + kTileC);
-    RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
-    const int64_t ea = e0 + int64_t(threadIdx.x) * kPerC;
-    const int64_t eb = min(e1, ea + kPerC);
-    if (ea >= eb) return;
-    int64_t r = f.row_of(ea);
-    int64_t rend = rp[r + 1];
-    for (int64_t e = ea; e < eb; ++e) {
-        while (e >= rend) {  // next row (empty rows skipped)
-            ++r;
-            rend = rp[r + 1];
-        }
-        const int32_t c = ci[e];
-        if (int64_t(c) < r) atomicAdd(&cnt[c], 1u);
-    }
-}
-
-// full_len[i] = lower length of row i + strict-lower entries of column i;
-// colcnt[i] = the latter
-__global__ __launch_bounds__(kBlock) void full_lengths(const int64_t* __restrict__ rp, int64_t m,
-                                                       const uint32_t* __restrict__ cnt,
-                                                       int64_t* __restrict__ full_len, int64_t* __restrict__ colcnt) {
-    const int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (i >= m) return;
-    full_len[i] = (rp[i + 1] - rp[i]) + int64_t(cnt[i]);
-    colcnt[i] = int64_t(cnt[i]);
-}
-
+// lower rows' entries [ebeg, eend) to their places in the full rows
 template <int VB>
 __global__ __launch_bounds__(kBlock) void copy_lower(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
-                                                     const void* __restrict__ val, int64_t m, int64_t nnz,
-                                                     const int64_t* __restrict__ f_rp, int32_t* __restrict__ f_ci,
-                                                     void* __restrict__ f_val) {
+                                                     const void* __restrict__ val, int64_t m, int64_t ebeg,
+                                                     int64_t eend, const int64_t* __restrict__ f_rp,
+                                                     int32_t* __restrict__ f_ci, void* __restrict__ f_val) {
     __shared__ int64_t win[kWin + 1];
     __shared__ int64_t bounds[2];
-    const int64_t e0 = int64_t(blockIdx.x) * kTileE;
-    const int64_t e1 = min(nnz, e0 + kTileE);
+    const int64_t e0 = ebeg + int64_t(blockIdx.x) * kTileE;
+    const int64_t e1 = min(eend, e0 + kTileE);
     RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
     for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
         const int64_t r = f.row_of(e);
@@ -154,8 +120,11 @@ __global__ __launch_bounds__(kBlock) void slab_counts(const int64_t* __restrict_
     const int64_t hi_col = min(c1, r);
     int64_t lo = a, hi = a;
     if (hi_col > c0) {
-        lo = lower_bound_i32(ci, a, b, c0);
-        hi = lower_bound_i32(ci, lo, b, hi_col);
+        lo = c0 == 0 ? a : lower_bound_i32(ci, a, b, c0);
+        if (c1 >= r)  // every column of the row below the diagonal is in the slab
+            hi = (b > lo && int64_t(ci[b - 1]) == r) ? b - 1 : b;
+        else
+            hi = lower_bound_i32(ci, lo, b, hi_col);
     }
     cnt[r] = hi - lo;
     lo_out[r] = lo;
@@ -189,41 +158,131 @@ template <int VB>
 __global__ __launch_bounds__(kBlock) void slab_place(const int64_t* __restrict__ rp, int64_t c0, int64_t nrec,
                                                      const uint32_t* __restrict__ skey,
                                                      const uint32_t* __restrict__ srow, const void* __restrict__ sval,
-                                                     const int64_t* __restrict__ cstart,
+                                                     const uint32_t* __restrict__ first,
                                                      const int64_t* __restrict__ f_rp, int32_t* __restrict__ f_ci,
                                                      void* __restrict__ f_val) {
     const int64_t s = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     if (s >= nrec) return;
-    const int64_t c = c0 + int64_t(skey[s]);
-    const int64_t rank = s - (cstart[c] - cstart[c0]);
+    const uint32_t k = skey[s];
+    const int64_t c = c0 + int64_t(k);
+    const int64_t rank = s - int64_t(first[k]);
     const int64_t p = f_rp[c] + (rp[c + 1] - rp[c]) + rank;
     f_ci[p] = int32_t(srow[s]);
     if constexpr (VB == 8) static_cast<uint64_t*>(f_val)[p] = static_cast<const uint64_t*>(sval)[s];
     if constexpr (VB == 4) static_cast<uint32_t*>(f_val)[p] = static_cast<const uint32_t*>(sval)[s];
 }
 
+// Strict-lower entries with clo <= col < clo + nb * 2^cb per bucket of 2^cb
+// columns (nb <= kMirrorBins), for choosing column slabs: LDS counters per
+// workgroup over a grid-stride walk of tiles, then one global add per
+// non-empty bucket.
+__global__ __launch_bounds__(kBlock) void coarse_hist(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
+                                                      int64_t m, int64_t nnz, int64_t clo, int cb, int nb,
+                                                      unsigned long long* __restrict__ hist) {
+    __shared__ uint32_t cnt[kMirrorBins];
+    __shared__ int64_t win[kWin + 1];
+    __shared__ int64_t bounds[2];
+    for (int x = threadIdx.x; x < nb; x += kBlock) cnt[x] = 0;
+    __syncthreads();
+    for (int64_t e0 = int64_t(blockIdx.x) * kTileC; e0 < nnz; e0 += int64_t(gridDim.x) * kTileC) {
+        const int64_t e1 = min(nnz, e0 + kTileC);
+        RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
+        const int64_t ea = e0 + int64_t(threadIdx.x) * kPerC;
+        const int64_t eb = min(e1, ea + kPerC);
+        if (ea < eb) {
+            int64_t r = f.row_of(ea);
+            int64_t rend = rp[r + 1];
+            // columns ascend inside a row: count runs of one bucket, add once per run
+            int64_t run_b = -1;
+            uint32_t run_n = 0;
+            for (int64_t e = ea; e < eb; ++e) {
+                while (e >= rend) {
+                    ++r;
+                    rend = rp[r + 1];
+                }
+                const int64_t c = int64_t(ci[e]);
+                const int64_t b = (c - clo) >> cb;
+                if (c < r && c >= clo && b < nb) {
+                    if (b != run_b) {
+                        if (run_n) atomicAdd(&cnt[run_b], run_n);
+                        run_b = b;
+                        run_n = 0;
+                    }
+                    ++run_n;
+                }
+            }
+            if (run_n) atomicAdd(&cnt[run_b], run_n);
+        }
+        __syncthreads();
+    }
+    for (int x = threadIdx.x; x < nb; x += kBlock)
+        if (cnt[x]) atomicAdd(&hist[x], (unsigned long long)cnt[x]);
+}
+
+// column runs of a sorted slab: first[k] / end[k] = first / one-past-last
+// record of slab column k (both zero for a column without records)
+__global__ __launch_bounds__(kBlock) void slab_col_runs(const uint32_t* __restrict__ skey, int64_t nrec,
+                                                        uint32_t* __restrict__ first, uint32_t* __restrict__ end) {
+    const int64_t s = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (s >= nrec) return;
+    const uint32_t k = skey[s];
+    if (s == 0 || skey[s - 1] != k) first[k] = uint32_t(s);
+    if (s == nrec - 1 || skey[s + 1] != k) end[k] = uint32_t(s + 1);
+}
+
+// full row lengths of the slab's columns (lower length + strict-lower
+// count), and a zero after them so that the scan also gives the next start
+__global__ __launch_bounds__(kBlock) void slab_full_len(const int64_t* __restrict__ rp, int64_t c0, int64_t w,
+                                                        const uint32_t* __restrict__ first,
+                                                        const uint32_t* __restrict__ end, int64_t* __restrict__ fl) {
+    const int64_t k = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (k > w) return;
+    fl[k] = k == w ? 0 : (rp[c0 + k + 1] - rp[c0 + k]) + int64_t(end[k] - first[k]);
+}
+
+// start of the slab's first full row: the lower entries of the rows before
+// c0 (rp[c0]) and the strict-lower entries of the columns before c0
+__global__ __launch_bounds__(kBlock) void add_carry(int64_t* __restrict__ a, int64_t w,
+                                                    const int64_t* __restrict__ rp_c0, int64_t strict_before) {
+    const int64_t k = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (k < w) a[k] += *rp_c0 + strict_before;
+}
+
 inline unsigned blocks_for(int64_t n, int64_t per) { return unsigned((n + per - 1) / per); }
 
 }  // namespace
 
-void mirror_counts(const MirrorArgs& a, uint32_t* cnt, int64_t* full_len, int64_t* colcnt, hipStream_t s) {
-    if (a.m <= 0) return;
-    (void)hipMemsetAsync(cnt, 0, size_t(a.m) * sizeof(uint32_t), s);
-    if (a.nnz > 0)
-        count_transposed<<<blocks_for(a.nnz, kTileC), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, cnt);
-    full_lengths<<<blocks_for(a.m, kBlock), kBlock, 0, s>>>(a.rp, a.m, cnt, full_len, colcnt);
+void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const int64_t* f_rp, int32_t* f_ci,
+                       void* f_val, hipStream_t s) {
+    if (eend <= ebeg) return;
+    const unsigned nb = blocks_for(eend - ebeg, kTileE);
+    if (a.vbytes == 8 && a.val)
+        copy_lower<8><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, f_rp, f_ci, f_val);
+    else if (a.vbytes == 4 && a.val)
+        copy_lower<4><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, f_rp, f_ci, f_val);
+    else
+        copy_lower<0><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, f_rp, f_ci, f_val);
 }
 
-void mirror_copy_lower(const MirrorArgs& a, const int64_t* f_rp, int32_t* f_ci, void* f_val, hipStream_t s) {
-    const int64_t nnz = a.nnz;
-    if (nnz <= 0) return;
-    const unsigned nb = blocks_for(nnz, kTileE);
-    if (a.vbytes == 8 && a.val)
-        copy_lower<8><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, nnz, f_rp, f_ci, f_val);
-    else if (a.vbytes == 4 && a.val)
-        copy_lower<4><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, nnz, f_rp, f_ci, f_val);
-    else
-        copy_lower<0><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, nnz, f_rp, f_ci, f_val);
+void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsigned long long* hist,
+                        hipStream_t s) {
+    (void)hipMemsetAsync(hist, 0, size_t(nb) * sizeof(unsigned long long), s);
+    if (a.nnz <= 0) return;
+    int64_t grid = (a.nnz + kTileC - 1) / kTileC;
+    if (grid > 2048) grid = 2048;
+    coarse_hist<<<unsigned(grid), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, clo, cb, nb, hist);
+}
+
+void mirror_slab_columns(const MirrorArgs& a, int64_t c0, int64_t c1, const uint32_t* skey, int64_t nrec,
+                         uint32_t* first, uint32_t* end, int64_t* fl, int64_t strict_before, int64_t* f_rp,
+                         void* scan_tmp, hipStream_t s) {
+    const int64_t w = c1 - c0;
+    (void)hipMemsetAsync(first, 0, size_t(w) * sizeof(uint32_t), s);
+    (void)hipMemsetAsync(end, 0, size_t(w) * sizeof(uint32_t), s);
+    if (nrec > 0) slab_col_runs<<<blocks_for(nrec, kBlock), kBlock, 0, s>>>(skey, nrec, first, end);
+    slab_full_len<<<blocks_for(w + 1, kBlock), kBlock, 0, s>>>(a.rp, c0, w, first, end, fl);
+    scan_i64(fl, f_rp + c0, w + 1, nullptr, scan_tmp, s);
+    add_carry<<<blocks_for(w + 1, kBlock), kBlock, 0, s>>>(f_rp + c0, w + 1, a.rp + c0, strict_before);
 }
 
 void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,
@@ -245,16 +304,16 @@ void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t nrec, const in
 }
 
 void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint32_t* skey, const uint32_t* srow,
-                       const void* sval, const int64_t* cstart, const int64_t* f_rp, int32_t* f_ci, void* f_val,
+                       const void* sval, const uint32_t* first, const int64_t* f_rp, int32_t* f_ci, void* f_val,
                        hipStream_t s) {
     if (nrec <= 0) return;
     const unsigned nb = blocks_for(nrec, kBlock);
     if (a.vbytes == 8 && a.val)
-        slab_place<8><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, cstart, f_rp, f_ci, f_val);
+        slab_place<8><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, first, f_rp, f_ci, f_val);
     else if (a.vbytes == 4 && a.val)
-        slab_place<4><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, cstart, f_rp, f_ci, f_val);
+        slab_place<4><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, first, f_rp, f_ci, f_val);
     else
-        slab_place<0><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, cstart, f_rp, f_ci, f_val);
+        slab_place<0><<<nb, kBlock, 0, s>>>(a.rp, c0, nrec, skey, srow, sval, first, f_rp, f_ci, f_val);
 }
 
 }  // namespace spsyrk

@@ -218,6 +218,41 @@ def test_mirror_matches_oracle(dev, semiring):
     np.testing.assert_array_equal(O.to_host()[1], M.to_host()[1])
 
 
+def _random_lower(rng, m, per_row, hub):
+    # lower-triangular CSR: about per_row random columns below the diagonal,
+    # the hub column in every row past it, the diagonal in every other row
+    rows_c = []
+    for i in range(m):
+        c = set(rng.integers(0, i, size=min(per_row, i)).tolist()) if i > 0 else set()
+        if i > hub:
+            c.add(hub)
+        if i % 2 == 0:
+            c.add(i)
+        rows_c.append(sorted(c))
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum([len(c) for c in rows_c])
+    ci = np.array([x for c in rows_c for x in c], dtype=np.int32)
+    return rp, ci, rng.standard_normal(len(ci))
+
+
+@pytest.mark.parametrize("cap", [1, 700, 5000])
+def test_mirror_column_slabs(dev, cap, monkeypatch):
+    # the transpose in many column slabs (slab size lowered from 2^31 records),
+    # a hub column holding more records than a slab, and histogram buckets
+    # over the slab size split by finer histograms of their columns
+    monkeypatch.setenv("SPSYRK_MIRROR_SLAB", str(cap))
+    rng = np.random.default_rng(cap)
+    m = 300 if cap == 1 else 9000
+    rp, ci, v = _random_lower(rng, m, 12, 5)
+    print(f"[mirror slabs] cap={cap} m={m} nnz={len(ci)}", flush=True)
+    ref = oracle.mirror(m, rp, ci, v)
+    M = sp.mirror(_raw(dev, rp, ci, m, v), "f64")
+    compare_full(M, ref, "f64", f"mirror slabs {cap}")
+    M = sp.mirror(_raw(dev, rp, ci, m, None), "count")
+    np.testing.assert_array_equal(M.to_host()[0], ref.row_ptr)
+    np.testing.assert_array_equal(M.to_host()[1], ref.col_idx)
+
+
 def test_mirror_structure_only(dev):
     import torch
     rng = np.random.default_rng(5)
