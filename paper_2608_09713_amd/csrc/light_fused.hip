@@ -87,9 +87,20 @@ struct WaveLds {
     uint32_t nbig;
     int64_t rbase[kFR];
     Item s_v[kFP];
-    uint32_t hist[kFB + 1];
-    uint32_t ucnt[kFB + 1];
+    // per bucket (16 bits: every count and offset is at most kFP + kFR)
+    alignas(4) uint16_t hist[kFB + 2];
+    uint16_t ucnt[kFB + 2];
 };
+
+static_assert(kFP + kFR < (1 << 16), "bucket counters are 16 bits");
+
+// atomic add of one to the 16-bit counter h[b] (two counters share a 32-bit
+// LDS word; no counter reaches 2^16); returns the old value
+__device__ inline uint32_t add16(uint16_t* h, uint32_t b) {
+    uint32_t* w = reinterpret_cast<uint32_t*>(h) + (b >> 1);
+    const uint32_t sh = (b & 1u) * 16u;
+    return (atomicAdd(w, 1u << sh) >> sh) & 0xffffu;
+}
 
 // exclusive scan in place of a[0..n) by one wavefront (lane = contiguous segment)
 template <typename T>
@@ -261,7 +272,7 @@ struct Chunk {
                 pj[v] = j;
                 const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
                 pb[v] = b | (uint32_t(r) << 16);
-                atomicAdd(&L.hist[b], 1u);
+                add16(L.hist, b);
             }
         }
         wave_sync();
@@ -272,7 +283,7 @@ struct Chunk {
         for (int v = 0; v < kPV; ++v) {
             const int t = lane + v * kWave;
             if (t < P) {
-                const uint32_t q = atomicAdd(&L.hist[pb[v] & 0xffffu], 1u);
+                const uint32_t q = add16(L.hist, pb[v] & 0xffffu);
                 // (the owner array is free by now: it keeps every slot's bucket)
                 reinterpret_cast<uint16_t*>(L.owner)[q] = uint16_t(pb[v] & 0xffffu);
                 L.s_j[q] = pj[v];
