@@ -1,11 +1,12 @@
 // Stable least-significant-digit radix sort of (key, row, value) records by
-// key bits, 8 bits per pass.  Used to group the entries of a CSR matrix by
-// column while keeping rows ascending inside each column (the input is in row
-// order and every pass is stable).
+// key bits, at most 8 bits per pass (the key's bits spread evenly over the
+// passes).  Used to group the entries of a CSR matrix by column while keeping
+// rows ascending inside each column (the input is in row order and every pass
+// is stable).
 //
 // Per pass: (1) per-tile digit histograms, (2) exclusive scan of the
 // digit-major (digit, tile) count matrix, (3) stable scatter: every wave ranks
-// its contiguous 1024-record segment with ballot-based digit matching and
+// its contiguous kSeg-record segment with ballot-based digit matching and
 // per-wave LDS counters, the tile is reordered through LDS, then written out
 // so that consecutive threads store consecutive addresses of a digit's run.
 #include "common.h"
@@ -39,16 +40,31 @@ __global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict_
     for (int q = 0; q < kWavesPerBlock; ++q) cnt[q][threadIdx.x] = 0;
     __syncthreads();
     const int64_t base = int64_t(blockIdx.x) * kRTile;
-    uint32_t kk[kRItems];
+    if (base + kRTile <= n && (reinterpret_cast<uintptr_t>(keys) & 15) == 0) {
+        // whole tile, 16-byte loads (the tile starts at a multiple of 16 bytes)
+        uint4 kv[kRItems / 4];
 #pragma unroll
-    for (int k = 0; k < kRItems; ++k) {
-        const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
-        kk[k] = i < n ? keys[i] : 0xffffffffu;
-    }
+        for (int k = 0; k < kRItems / 4; ++k)
+            kv[k] = reinterpret_cast<const uint4*>(keys + base)[k * kBlock + threadIdx.x];
 #pragma unroll
-    for (int k = 0; k < kRItems; ++k) {
-        const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
-        if (i < n) atomicAdd(&cnt[w][(kk[k] >> shift) & mask], 1u);
+        for (int k = 0; k < kRItems / 4; ++k) {
+            atomicAdd(&cnt[w][(kv[k].x >> shift) & mask], 1u);
+            atomicAdd(&cnt[w][(kv[k].y >> shift) & mask], 1u);
+            atomicAdd(&cnt[w][(kv[k].z >> shift) & mask], 1u);
+            atomicAdd(&cnt[w][(kv[k].w >> shift) & mask], 1u);
+        }
+    } else {
+        uint32_t kk[kRItems];
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
+            kk[k] = i < n ? keys[i] : 0xffffffffu;
+        }
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
+            if (i < n) atomicAdd(&cnt[w][(kk[k] >> shift) & mask], 1u);
+        }
     }
     __syncthreads();
     uint32_t t = 0;
