@@ -362,13 +362,15 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     int32_t* heavy_rows = ar.get_t<int32_t>(m);
     int64_t* ub = ar.get_t<int64_t>(m + 1);
     HIPCHK(hipMemsetAsync(ub + m, 0, sizeof(int64_t), s));
+    void* ptmp = ar.get(row_products_tmp_bytes(L.nnz));
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
-        row_products(L.rp, m, L.nnz, run, prod, s);
+        row_products(L.rp, m, L.nnz, run, ptmp, prod, s);
         classify_rows(L.rp, prod, m, lower, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s);
     }
     check_launch();
     Ctl h = read_ctl(ctl, s);
+    ar.release(ptmp);
     const int64_t nheavy = h.heavy_count;
     const int64_t light_cap = int64_t(h.light_cap);
     HeavyArgs ha;
@@ -442,7 +444,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     void* c_val = ar.get(size_t(total > 0 ? total : 1) * vbo, true);
     {
         Phase ph(SPSYRK_PHASE_COMPACT, s);
-        compact_rows(m, light_cap, ubp, row_cnt, c_rp, s_ci, s_val, vbo, c_ci, c_val, s);
+        void* ctmp = ar.get(compact_tmp_bytes(light_cap));
+        compact_rows(m, light_cap, ubp, row_cnt, c_rp, s_ci, s_val, vbo, ctmp, c_ci, c_val, s);
     }
     check_launch();
     if (nheavy > 0) {

@@ -150,13 +150,21 @@ void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, vo
 void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* run, hipStream_t s);
 // prod[i] = sum over the entries e of row i of run[e].y - run[e].x (prod
 // must start zeroed).
-void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, unsigned long long* prod,
+// tmp: row_products_tmp_bytes(nnz) of scratch
+size_t row_products_tmp_bytes(int64_t nnz);
+void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, void* tmp, unsigned long long* prod,
                   hipStream_t s);
 // Copy the staged rows to their final places: the element at staging slot
 // ubp[i] + x (x < row_cnt[i]) goes to c_rp[i] + x.  ubp is non-decreasing
 // with ubp[m] = staged; rows with no staging room (heavy rows) copy nothing.
+// tmp: compact_tmp_bytes(staged) of scratch
+size_t compact_tmp_bytes(int64_t staged);
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
-                  const int32_t* s_ci, const void* s_val, int vbytes, int32_t* c_ci, void* c_val, hipStream_t s);
+                  const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
+                  hipStream_t s);
+// Row of every tile start: trow[t] = the row r with rp[r] <= t T < rp[r + 1],
+// for t T < rp[m] (rp non-decreasing; trow: ceil(rp[m] / T) words).
+void tile_first_rows(const int64_t* rp, int64_t m, int64_t T, int64_t* trow, hipStream_t s);
 
 // ---- heavy.hip
 struct HeavyArgs {

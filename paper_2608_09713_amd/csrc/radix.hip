@@ -98,7 +98,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
                                                         typename ValT<VB>::T* __restrict__ val_out, int64_t n, int shift,
                                                         uint32_t mask, const uint32_t* __restrict__ offs,
                                                         int64_t ntiles, const int64_t* __restrict__ rp, int64_t m,
-                                                        int rowbits, int lenbits) {
+                                                        const int64_t* __restrict__ trow, int rowbits, int lenbits) {
     using V = typename ValT<VB>::T;
     __shared__ int64_t rwin[FIRST ? kRowWin + 1 : 1];
     __shared__ int64_t rbounds[2];
@@ -121,8 +121,11 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     bool rstaged = false;
     if constexpr (FIRST) {
         if (threadIdx.x == 0) {
-            rbounds[0] = last_leq_i64(rp, 0, m, base);
-            rbounds[1] = last_leq_i64(rp, 0, m, min(n, base + kRTile) - 1);
+            // rows of the tile's first entry and (at most one row past the
+            // tile) of its end, from the tile table; the last tile searches
+            const int64_t lo = trow[blockIdx.x];
+            rbounds[0] = lo;
+            rbounds[1] = base + kRTile < n ? trow[blockIdx.x + 1] : last_leq_i64(rp, lo, m, n - 1);
         }
         __syncthreads();
         rlo = rbounds[0];
@@ -137,7 +140,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             for (int i = threadIdx.x; i < kRTile; i += kBlock) rowof[i] = 0;
             __syncthreads();
             for (int64_t k = 1 + threadIdx.x; k <= rhi - rlo; k += kBlock)
-                if (rwin[k] < rwin[k + 1]) rowof[rwin[k] - base] = uint32_t(k);
+                if (rwin[k] < rwin[k + 1] && rwin[k] - base < kRTile) rowof[rwin[k] - base] = uint32_t(k);
             __syncthreads();
             uint32_t run_max = 0;
 #pragma unroll
@@ -263,13 +266,14 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 template <int VB, bool FIRST = false>
 void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
               int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s, const int64_t* rp = nullptr,
-              int64_t m = 0, int rowbits = 0, int lenbits = 0) {
+              int64_t m = 0, const int64_t* trow = nullptr, int rowbits = 0, int lenbits = 0) {
     using V = typename ValT<VB>::T;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
     scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
     radix_scatter<VB, FIRST><<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(
-        ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, rowbits, lenbits);
+        ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, trow, rowbits,
+        lenbits);
 }
 
 // Digit widths of the passes for an nbits-bit key: as few passes as 8-bit
@@ -288,7 +292,8 @@ int digit_plan(int nbits, int (&width)[8]) {
 size_t radix_tmp_bytes(int64_t n) {
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     const size_t hist = size_t(ntiles) * kDigits * sizeof(uint32_t);
-    return ((hist + 255) & ~size_t(255)) + scan_tmp_bytes(ntiles * kDigits);
+    const size_t table = size_t(ntiles + 1) * sizeof(int64_t);
+    return ((hist + 255) & ~size_t(255)) + ((table + 255) & ~size_t(255)) + scan_tmp_bytes(ntiles * kDigits);
 }
 
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
@@ -298,12 +303,16 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     uint32_t* hist = static_cast<uint32_t*>(tmp);
     const size_t hist_bytes = (size_t(ntiles) * kDigits * sizeof(uint32_t) + 255) & ~size_t(255);
-    void* scan_tmp = static_cast<char*>(tmp) + hist_bytes;
+    const size_t table_bytes = (size_t(ntiles + 1) * sizeof(int64_t) + 255) & ~size_t(255);
+    int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + hist_bytes);
+    void* scan_tmp = static_cast<char*>(tmp) + hist_bytes + table_bytes;
     int width[8];
     const int passes = digit_plan(nbits, width);
-    // first pass straight from the CSR arrays (into the b buffers), at least one pass
+    // first pass straight from the CSR arrays (into the b buffers), at least
+    // one pass; the row of every tile's first entry comes from a table
+    tile_first_rows(rp, m, kRTile, trow, s);
     run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, 0,
-                      (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, rowbits, lenbits);
+                      (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
     int cur = 1;
     int shift = width[0];
     for (int ps = 1; ps < passes; shift += width[ps], ++ps) {

@@ -30,8 +30,19 @@ constexpr int kPerT = 8;
 constexpr int kTileP = kBlock * kPerT;
 constexpr int kWinP = 1024;
 
+// trow[t] = the row holding position t * T, for every tile start t * T <
+// rp[m] (each such position lies in exactly one non-empty row, which writes it)
+__global__ __launch_bounds__(kBlock) void tile_rows(const int64_t* __restrict__ rp, int64_t m, int64_t T,
+                                                    int64_t* __restrict__ trow) {
+    const int64_t r = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (r >= m) return;
+    const int64_t a = rp[r], b = rp[r + 1];
+    for (int64_t t = (a + T - 1) / T; t * T < b; ++t) trow[t] = r;
+}
+
 __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
                                                          const uint2* __restrict__ run,
+                                                         const int64_t* __restrict__ trow,
                                                          unsigned long long* __restrict__ prod) {
     __shared__ int64_t win[kWinP + 1];
     __shared__ unsigned long long part[kWinP];
@@ -40,8 +51,11 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
     const int64_t e0 = int64_t(blockIdx.x) * kTileP;
     const int64_t e1 = min(nnz, e0 + kTileP);
     if (threadIdx.x == 0) {
-        bounds[0] = last_leq(rp, 0, m, e0);
-        bounds[1] = last_leq(rp, 0, m, e1 - 1);
+        // rows of the tile's first entry and (at most one row past the tile)
+        // of its end, from the tile table; the last tile searches for its end
+        const int64_t lo = trow[blockIdx.x];
+        bounds[0] = lo;
+        bounds[1] = e1 < nnz ? trow[blockIdx.x + 1] : last_leq(rp, lo, m, e1 - 1);
     }
     __syncthreads();
     const int64_t rlo = bounds[0], rhi = bounds[1];
@@ -125,6 +139,7 @@ constexpr int kCWin = 512;    // rows held in LDS by a compaction workgroup
 
 template <int VB>
 __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t staged, const int64_t* __restrict__ ubp,
+                                                         const int64_t* __restrict__ trow,
                                                          const int64_t* __restrict__ row_cnt,
                                                          const int64_t* __restrict__ c_rp,
                                                          const int32_t* __restrict__ s_ci, const void* __restrict__ s_val,
@@ -138,8 +153,11 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     const int64_t s0 = int64_t(blockIdx.x) * kCTile;
     const int64_t s1 = min(staged, s0 + kCTile);
     if (threadIdx.x == 0) {
-        bounds[0] = last_leq(ubp, 0, m, s0);
-        bounds[1] = last_leq(ubp, 0, m, s1 - 1);
+        // rows of the tile's first slot and (at most one row past the tile)
+        // of its end, from the tile table; the last tile searches for its end
+        const int64_t lo = trow[blockIdx.x];
+        bounds[0] = lo;
+        bounds[1] = s1 < staged ? trow[blockIdx.x + 1] : last_leq(ubp, lo, m, s1 - 1);
     }
     __syncthreads();
     const int64_t rlo = bounds[0], rhi = bounds[1];
@@ -147,18 +165,19 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     const bool win_ok = nrw <= kCWin;
     if (win_ok) {
         for (int x = threadIdx.x; x < kCTile; x += kBlock) rowof[x] = 0;
-        for (int64_t k = threadIdx.x; k < nrw; k += kBlock) {
+        for (int64_t k = threadIdx.x; k <= nrw; k += kBlock) {
             const int64_t u = ubp[rlo + k];
             wub[k] = u;
+            if (k == nrw) break;
             wend[k] = u + row_cnt[rlo + k];
             wdel[k] = c_rp[rlo + k] - u;
         }
         __syncthreads();
-        // every row with staging room marks its first slot in the tile (a row
+        // every row with staging room in the tile marks its first slot (a row
         // without room shares its slot with a later row and marks nothing),
         // then a max-scan gives each slot its row
         for (int64_t k = 1 + threadIdx.x; k < nrw; k += kBlock)
-            if (k == nrw - 1 || wub[k] < wub[k + 1]) rowof[wub[k] - s0] = uint16_t(k);
+            if (wub[k] < wub[k + 1] && wub[k] < s1) rowof[wub[k] - s0] = uint16_t(k);
         __syncthreads();
         constexpr int kPer = kCTile / kBlock;
         const int lane = lane_id();
@@ -224,6 +243,11 @@ __global__ __launch_bounds__(kBlock) void offdiag_runs_kernel(const int32_t* __r
 
 }  // namespace
 
+void tile_first_rows(const int64_t* rp, int64_t m, int64_t T, int64_t* trow, hipStream_t s) {
+    if (m <= 0) return;
+    tile_rows<<<unsigned((m + kBlock - 1) / kBlock), kBlock, 0, s>>>(rp, m, T, trow);
+}
+
 void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, void* scan_tmp, hipStream_t s) {
     (void)hipMemsetAsync(cptr, 0, size_t(n + 1) * sizeof(uint32_t), s);
     if (nnz > 0) {
@@ -239,23 +263,32 @@ void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* r
     offdiag_runs_kernel<<<unsigned((nnz + kBlock - 1) / kBlock), kBlock, 0, s>>>(ci, nnz, cptr, run);
 }
 
-void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, unsigned long long* prod,
+size_t row_products_tmp_bytes(int64_t nnz) { return size_t((nnz + kTileP - 1) / kTileP + 1) * sizeof(int64_t); }
+
+void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, void* tmp, unsigned long long* prod,
                   hipStream_t s) {
     if (nnz <= 0 || m <= 0) return;
     const unsigned nb = unsigned((nnz + kTileP - 1) / kTileP);
-    rowprod_kernel<<<nb, kBlock, 0, s>>>(rp, m, nnz, run, prod);
+    int64_t* trow = static_cast<int64_t*>(tmp);
+    tile_first_rows(rp, m, kTileP, trow, s);
+    rowprod_kernel<<<nb, kBlock, 0, s>>>(rp, m, nnz, run, trow, prod);
 }
 
+size_t compact_tmp_bytes(int64_t staged) { return size_t((staged + kCTile - 1) / kCTile + 1) * sizeof(int64_t); }
+
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
-                  const int32_t* s_ci, const void* s_val, int vbytes, int32_t* c_ci, void* c_val, hipStream_t s) {
+                  const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
+                  hipStream_t s) {
     if (staged <= 0 || m <= 0) return;
     const unsigned nb = unsigned((staged + kCTile - 1) / kCTile);
+    int64_t* trow = static_cast<int64_t*>(tmp);
+    tile_first_rows(ubp, m, kCTile, trow, s);
     if (vbytes == 8)
-        compact_kernel<8><<<nb, kBlock, 0, s>>>(m, staged, ubp, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
+        compact_kernel<8><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
     else if (vbytes == 4)
-        compact_kernel<4><<<nb, kBlock, 0, s>>>(m, staged, ubp, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
+        compact_kernel<4><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
     else
-        compact_kernel<0><<<nb, kBlock, 0, s>>>(m, staged, ubp, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
+        compact_kernel<0><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
 }
 
 }  // namespace spsyrk
