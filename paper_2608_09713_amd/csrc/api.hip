@@ -229,9 +229,11 @@ DevCsr dev(const spsyrk_csr* A) {
 }
 
 void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name) {
-    validate_csr(A, upper_forbidden, &ctl->err, s);
+    void* vtmp = ar.get(validate_tmp_bytes(A.nnz));
+    validate_csr(A, upper_forbidden, &ctl->err, vtmp, s);
     check_launch();
     Ctl h = read_ctl(ctl, s);
+    ar.release(vtmp);
     if (h.err) {
         set_detail("%s is not canonical CSR (flags 0x%x:%s%s%s%s)", name, h.err, (h.err & kErrRowPtr) ? " row_ptr" : "",
                    (h.err & kErrColRange) ? " column-range" : "", (h.err & kErrColOrder) ? " column-order" : "",
@@ -638,7 +640,7 @@ struct Slab {
 // Column slabs of at most cap strict-lower entries (a single column may hold
 // more: it is a slab of its own), chosen from bucket histograms; a bucket
 // over the cap is split by a finer histogram of its own columns.
-std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, Arena& ar, hipStream_t s) {
+std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, const int64_t* trow, Arena& ar, hipStream_t s) {
     unsigned long long* hist = ar.get_t<unsigned long long>(kMirrorBins);
     std::vector<unsigned long long> h(kMirrorBins);
     std::vector<Slab> pieces;  // buckets (or single columns) in column order
@@ -647,7 +649,7 @@ std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, Arena& ar, hipSt
         int cb = 0;
         while (((w + (int64_t(1) << cb) - 1) >> cb) > kMirrorBins) ++cb;
         const int nb = int((w + (int64_t(1) << cb) - 1) >> cb);
-        mirror_coarse_hist(ma, lo, cb, nb, hist, s);
+        mirror_coarse_hist(ma, lo, cb, nb, trow, hist, s);
         check_launch();
         HIPCHK(hipMemcpyAsync(h.data(), hist, size_t(nb) * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
         HIPCHK(hipStreamSynchronize(s));
@@ -702,6 +704,9 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     // and starts of the slab's rows, and every record placed after the lower
     // part of its row.  The lower rows are copied once all starts are known.
     const int64_t cap = mirror_slab_cap();
+    // row of every tile start of the walks over C_L's entries
+    int64_t* trow = ar.get_t<int64_t>(int64_t(mirror_tile_bytes(L.nnz) / sizeof(int64_t)));
+    mirror_tile_rows(L.rp, m, trow, s);
     int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
     int64_t* row_lo = ar.get_t<int64_t>(m > 0 ? m : 1);
     void* stmp = ar.get(scan_tmp_bytes(m + 1));
@@ -717,7 +722,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
             const Ctl h = read_ctl(ctl, s);
             slabs.push_back({0, m, h.total, 0});
         } else {
-            slabs = plan_slabs(ma, cap, ar, s);
+            slabs = plan_slabs(ma, cap, trow, ar, s);
         }
     }
     int64_t nstrict = 0, rec_max = 0, w_max = 0;
@@ -741,6 +746,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     void* va = vb ? ar.get(size_t(rec_max > 0 ? rec_max : 1) * vb) : nullptr;
     void* vbb = vb ? ar.get(size_t(rec_max > 0 ? rec_max : 1) * vb) : nullptr;
     void* rtmp = ar.get(radix_tmp_bytes(rec_max > 0 ? rec_max : 1));
+    int64_t* strow = ar.get_t<int64_t>(int64_t(mirror_tile_bytes(rec_max) / sizeof(int64_t)));
     for (size_t k = 0; k < slabs.size(); ++k) {
         const Slab& sl = slabs[k];
         if (sl.c1 <= sl.c0) continue;
@@ -759,7 +765,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
         const uint32_t* srow = ra;
         const void* sval = va;
         if (sl.nrec > 0) {
-            mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, ka, ra, va, s);
+            mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, strow, ka, ra, va, s);
             const int nbits = bit_width_u64(sl.c1 - sl.c0 > 1 ? uint64_t(sl.c1 - sl.c0 - 1) : 0);
             if (radix_sort(ka, kb, ra, rb, va, vbb, vb, sl.nrec, nbits, rtmp, s)) {
                 skey = kb;
@@ -774,7 +780,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     }
     {
         Phase ph(SPSYRK_PHASE_MIRROR_COPY, s);
-        mirror_copy_lower(ma, 0, L.nnz, f_rp, f_ci, f_val, s);
+        mirror_copy_lower(ma, 0, L.nnz, trow, f_rp, f_ci, f_val, s);
     }
     check_launch();
     HIPCHK(hipStreamSynchronize(s));

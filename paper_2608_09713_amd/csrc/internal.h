@@ -50,7 +50,9 @@ void scan_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* 
 
 // ---- validate.hip
 // ORs ErrBits into *err.  upper_forbidden: also flag entries with col > row.
-void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, hipStream_t s);
+// tmp: validate_tmp_bytes(nnz) of scratch.
+size_t validate_tmp_bytes(int64_t nnz);
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, void* tmp, hipStream_t s);
 void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 
 // ---- radix.hip
@@ -207,15 +209,20 @@ struct MirrorArgs {
 // strict-lower entries with clo <= col < clo + nb * 2^cb per bucket of 2^cb
 // columns (nb <= kMirrorBins), added into hist (zeroed here)
 constexpr int kMirrorBins = 4096;
-void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsigned long long* hist,
-                        hipStream_t s);
+void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, const int64_t* trow,
+                        unsigned long long* hist, hipStream_t s);
+// row of every tile start of the mirror's walks over positions [0, rp[m])
+// (trow: mirror_tile_bytes(rp[m]))
+size_t mirror_tile_bytes(int64_t positions);
+void mirror_tile_rows(const int64_t* rp, int64_t m, int64_t* trow, hipStream_t s);
 // per-row counts and first entries of the strict lower part with col in [c0, c1)
 void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,
                         hipStream_t s);
 // records (col - c0, row, value) of the slab, in row-major order at positions
 // given by rec_rp (exclusive scan of the per-row counts), nrec in all
+// (trow: mirror_tile_bytes(nrec) of scratch)
 void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t nrec, const int64_t* rec_rp, const int64_t* row_lo,
-                         uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s);
+                         int64_t* trow, uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s);
 // from the slab's records sorted by column (keys skey): first[k] / end[k],
 // the record range of slab column k, and the full row starts f_rp[c0..c1]
 // (fl: w + 1 words of scratch; strict_before: strict-lower entries in the
@@ -229,7 +236,8 @@ void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint
                        const void* sval, const uint32_t* first, const int64_t* f_rp, int32_t* f_ci, void* f_val,
                        hipStream_t s);
 // lower rows' entries [ebeg, eend) to their places f_rp[row] + offset in row
-void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const int64_t* f_rp, int32_t* f_ci,
-                       void* f_val, hipStream_t s);
+// (trow: the table of mirror_tile_rows over the lower rows, or null)
+void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const int64_t* trow, const int64_t* f_rp,
+                       int32_t* f_ci, void* f_val, hipStream_t s);
 
 }  // namespace spsyrk

@@ -56,11 +56,20 @@ __device__ inline int64_t last_row_leq(const int64_t* rp, int64_t m, int64_t e) 
     return lo;
 }
 
+// Rows of the tile [e0, e1) (tile t of kTileE positions, total positions in
+// all): from the tile table trow (the row of every tile start; the upper
+// bound may then be the row of e1, one past the tile), or by searches.
 __device__ inline RowFinder make_finder(const int64_t* rp, int64_t m, int64_t e0, int64_t e1, int64_t* win,
-                                        int64_t* bounds) {
+                                        int64_t* bounds, const int64_t* trow, int64_t t, int64_t total) {
     if (threadIdx.x == 0) {
-        bounds[0] = last_row_leq(rp, m, e0);
-        bounds[1] = last_row_leq(rp, m, e1 - 1);
+        if (trow) {
+            const int64_t lo = trow[t];
+            bounds[0] = lo;
+            bounds[1] = e1 < total ? trow[t + 1] : last_row_leq(rp, m, e1 - 1);
+        } else {
+            bounds[0] = last_row_leq(rp, m, e0);
+            bounds[1] = last_row_leq(rp, m, e1 - 1);
+        }
     }
     __syncthreads();
     RowFinder f{rp, bounds[0], bounds[1], false, win};
@@ -78,18 +87,20 @@ __device__ inline RowFinder make_finder(const int64_t* rp, int64_t m, int64_t e0
 // without a search per entry.
 constexpr int kPerC = 16;
 constexpr int kTileC = kBlock * kPerC;
+static_assert(kTileC == kTileE, "one tile table serves the walks and the copies");
 
 // lower rows' entries [ebeg, eend) to their places in the full rows
 template <int VB>
 __global__ __launch_bounds__(kBlock) void copy_lower(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
                                                      const void* __restrict__ val, int64_t m, int64_t ebeg,
-                                                     int64_t eend, const int64_t* __restrict__ f_rp,
-                                                     int32_t* __restrict__ f_ci, void* __restrict__ f_val) {
+                                                     int64_t eend, const int64_t* __restrict__ trow,
+                                                     const int64_t* __restrict__ f_rp, int32_t* __restrict__ f_ci,
+                                                     void* __restrict__ f_val) {
     __shared__ int64_t win[kWin + 1];
     __shared__ int64_t bounds[2];
     const int64_t e0 = ebeg + int64_t(blockIdx.x) * kTileE;
     const int64_t e1 = min(eend, e0 + kTileE);
-    RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
+    RowFinder f = make_finder(rp, m, e0, e1, win, bounds, trow, blockIdx.x, eend);
     for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
         const int64_t r = f.row_of(e);
         const int64_t p = f_rp[r] + (e - rp[r]);
@@ -137,13 +148,14 @@ template <int VB>
 __global__ __launch_bounds__(kBlock) void slab_extract(const int32_t* __restrict__ ci, const void* __restrict__ val,
                                                        int64_t m, int64_t c0, int64_t nrec,
                                                        const int64_t* __restrict__ rec_rp,
-                                                       const int64_t* __restrict__ row_lo, uint32_t* __restrict__ rkey,
-                                                       uint32_t* __restrict__ rrow, void* __restrict__ rval) {
+                                                       const int64_t* __restrict__ row_lo, const int64_t* __restrict__ trow,
+                                                       uint32_t* __restrict__ rkey, uint32_t* __restrict__ rrow,
+                                                       void* __restrict__ rval) {
     __shared__ int64_t win[kWin + 1];
     __shared__ int64_t bounds[2];
     const int64_t p0 = int64_t(blockIdx.x) * kTileE;
     const int64_t p1 = min(nrec, p0 + kTileE);
-    RowFinder f = make_finder(rec_rp, m, p0, p1, win, bounds);
+    RowFinder f = make_finder(rec_rp, m, p0, p1, win, bounds, trow, blockIdx.x, nrec);
     for (int64_t p = p0 + threadIdx.x; p < p1; p += kBlock) {
         const int64_t r = f.row_of(p);
         const int64_t e = row_lo[r] + (p - rec_rp[r]);
@@ -178,6 +190,7 @@ __global__ __launch_bounds__(kBlock) void slab_place(const int64_t* __restrict__
 // non-empty bucket.
 __global__ __launch_bounds__(kBlock) void coarse_hist(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
                                                       int64_t m, int64_t nnz, int64_t clo, int cb, int nb,
+                                                      const int64_t* __restrict__ trow,
                                                       unsigned long long* __restrict__ hist) {
     __shared__ uint32_t cnt[kMirrorBins];
     __shared__ int64_t win[kWin + 1];
@@ -186,7 +199,7 @@ __global__ __launch_bounds__(kBlock) void coarse_hist(const int64_t* __restrict_
     __syncthreads();
     for (int64_t e0 = int64_t(blockIdx.x) * kTileC; e0 < nnz; e0 += int64_t(gridDim.x) * kTileC) {
         const int64_t e1 = min(nnz, e0 + kTileC);
-        RowFinder f = make_finder(rp, m, e0, e1, win, bounds);
+        RowFinder f = make_finder(rp, m, e0, e1, win, bounds, trow, e0 / kTileC, nnz);
         const int64_t ea = e0 + int64_t(threadIdx.x) * kPerC;
         const int64_t eb = min(e1, ea + kPerC);
         if (ea < eb) {
@@ -252,25 +265,32 @@ inline unsigned blocks_for(int64_t n, int64_t per) { return unsigned((n + per - 
 
 }  // namespace
 
-void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const int64_t* f_rp, int32_t* f_ci,
-                       void* f_val, hipStream_t s) {
-    if (eend <= ebeg) return;
-    const unsigned nb = blocks_for(eend - ebeg, kTileE);
-    if (a.vbytes == 8 && a.val)
-        copy_lower<8><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, f_rp, f_ci, f_val);
-    else if (a.vbytes == 4 && a.val)
-        copy_lower<4><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, f_rp, f_ci, f_val);
-    else
-        copy_lower<0><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, f_rp, f_ci, f_val);
+size_t mirror_tile_bytes(int64_t positions) { return size_t((positions + kTileE - 1) / kTileE + 1) * sizeof(int64_t); }
+
+void mirror_tile_rows(const int64_t* rp, int64_t m, int64_t* trow, hipStream_t s) {
+    tile_first_rows(rp, m, kTileE, trow, s);
 }
 
-void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsigned long long* hist,
-                        hipStream_t s) {
+void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const int64_t* trow, const int64_t* f_rp,
+                       int32_t* f_ci, void* f_val, hipStream_t s) {
+    if (eend <= ebeg) return;
+    const unsigned nb = blocks_for(eend - ebeg, kTileE);
+    if (ebeg != 0) trow = nullptr;  // (the table's tiles start at entry 0)
+    if (a.vbytes == 8 && a.val)
+        copy_lower<8><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, trow, f_rp, f_ci, f_val);
+    else if (a.vbytes == 4 && a.val)
+        copy_lower<4><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, trow, f_rp, f_ci, f_val);
+    else
+        copy_lower<0><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, trow, f_rp, f_ci, f_val);
+}
+
+void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, const int64_t* trow,
+                        unsigned long long* hist, hipStream_t s) {
     (void)hipMemsetAsync(hist, 0, size_t(nb) * sizeof(unsigned long long), s);
     if (a.nnz <= 0) return;
     int64_t grid = (a.nnz + kTileC - 1) / kTileC;
     if (grid > 2048) grid = 2048;
-    coarse_hist<<<unsigned(grid), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, clo, cb, nb, hist);
+    coarse_hist<<<unsigned(grid), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, clo, cb, nb, trow, hist);
 }
 
 void mirror_slab_columns(const MirrorArgs& a, int64_t c0, int64_t c1, const uint32_t* skey, int64_t nrec,
@@ -292,15 +312,16 @@ void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* ro
 }
 
 void mirror_slab_extract(const MirrorArgs& a, int64_t c0, int64_t nrec, const int64_t* rec_rp, const int64_t* row_lo,
-                         uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s) {
+                         int64_t* trow, uint32_t* rkey, uint32_t* rrow, void* rval, hipStream_t s) {
     if (nrec <= 0) return;
     const unsigned nb = blocks_for(nrec, kTileE);
+    tile_first_rows(rec_rp, a.m, kTileE, trow, s);
     if (a.vbytes == 8 && a.val)
-        slab_extract<8><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, rkey, rrow, rval);
+        slab_extract<8><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, trow, rkey, rrow, rval);
     else if (a.vbytes == 4 && a.val)
-        slab_extract<4><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, rkey, rrow, rval);
+        slab_extract<4><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, trow, rkey, rrow, rval);
     else
-        slab_extract<0><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, rkey, rrow, rval);
+        slab_extract<0><<<nb, kBlock, 0, s>>>(a.ci, a.val, a.m, c0, nrec, rec_rp, row_lo, trow, rkey, rrow, rval);
 }
 
 void mirror_slab_place(const MirrorArgs& a, int64_t c0, int64_t nrec, const uint32_t* skey, const uint32_t* srow,

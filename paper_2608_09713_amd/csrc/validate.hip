@@ -4,7 +4,10 @@
 // [b*kTileR, (b+1)*kTileR) and the column ids of entries [b*kTileE,
 // (b+1)*kTileE).  Every thread walks a contiguous stretch of entries row by
 // row, starting from the row of its first entry (searched in an LDS window of
-// the row pointers).  On a malformed row_ptr the searches still stay in bounds (their
+// the row pointers).  The rows of the workgroup's first entry and of its end
+// come from a table written by the rows themselves; a row with out-of-range
+// pointers writes nothing, and a missing or inconsistent entry falls back to
+// a search.  On a malformed row_ptr every access still stays in bounds (the
 // results are then meaningless, but the row check has raised its flag).
 #include "common.h"
 #include "internal.h"
@@ -29,9 +32,24 @@ __device__ inline int64_t find_row(const int64_t* rp, int64_t lo, int64_t hi, in
     return lo;
 }
 
+// trow[t] = the row holding entry t * kTileE (trow starts at -1).  Rows whose
+// pointers lie outside [0, nnz] or decrease write nothing, and a row writes
+// at most kRowTiles entries (so a malformed row_ptr costs bounded work; the
+// tiles a longer row would cover search for their row instead).
+constexpr int64_t kRowTiles = 64;
+__global__ __launch_bounds__(kBlock) void entry_tile_rows(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
+                                                          int64_t ntiles, int64_t* __restrict__ trow) {
+    const int64_t r = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (r >= m) return;
+    const int64_t a = rp[r], b = rp[r + 1];
+    if (a < 0 || b < a || b > nnz) return;
+    const int64_t t0 = (a + kTileE - 1) / kTileE;
+    for (int64_t t = t0; t < ntiles && t * kTileE < b && t < t0 + kRowTiles; ++t) trow[t] = r;
+}
+
 __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
                                                     int64_t m, int64_t n, int64_t nnz, bool upper_forbidden,
-                                                    uint32_t* err) {
+                                                    const int64_t* __restrict__ trow, uint32_t* err) {
     __shared__ int64_t win[kWinV + 1];
     __shared__ int64_t bounds[2];
     __shared__ uint32_t bad_s;
@@ -48,8 +66,13 @@ __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ 
     const int64_t e1 = min(nnz, e0 + kTileE);
     if (e0 < e1) {
         if (threadIdx.x == 0) {
-            bounds[0] = find_row(rp, 0, m, e0);
-            bounds[1] = find_row(rp, 0, m, e1 - 1);
+            // row of e0, and a row at or past the row of e1 - 1 (the row of e1)
+            int64_t lo = trow[blockIdx.x];
+            if (lo < 0 || lo >= m) lo = find_row(rp, 0, m, e0);
+            int64_t hi = e1 < nnz ? trow[blockIdx.x + 1] : -1;
+            if (hi < lo || hi >= m) hi = find_row(rp, 0, m, e1 - 1);
+            bounds[0] = lo;
+            bounds[1] = hi;
         }
         __syncthreads();
         const int64_t rlo = bounds[0], rhi = bounds[1];
@@ -123,11 +146,19 @@ void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
     fill_u32_kernel<<<dim3(unsigned(blocks)), dim3(kBlock), 0, s>>>(p, n, v);
 }
 
-void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, hipStream_t s) {
+size_t validate_tmp_bytes(int64_t nnz) { return size_t((nnz + kTileE - 1) / kTileE + 1) * sizeof(int64_t); }
+
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, void* tmp, hipStream_t s) {
     const int64_t rb = (A.m + 1 + kTileR - 1) / kTileR;
     const int64_t eb = (A.nnz + kTileE - 1) / kTileE;
     const int64_t nb = rb > eb ? rb : eb;
-    check_csr<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.ci, A.m, A.n, A.nnz, upper_forbidden, err);
+    int64_t* trow = static_cast<int64_t*>(tmp);
+    if (eb > 0) {
+        fill_u32(reinterpret_cast<uint32_t*>(trow), 2 * eb, 0xffffffffu, s);
+        if (A.m > 0)
+            entry_tile_rows<<<unsigned((A.m + kBlock - 1) / kBlock), kBlock, 0, s>>>(A.rp, A.m, A.nnz, eb, trow);
+    }
+    check_csr<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.ci, A.m, A.n, A.nnz, upper_forbidden, trow, err);
 }
 
 }  // namespace spsyrk
