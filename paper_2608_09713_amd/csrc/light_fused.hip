@@ -40,6 +40,15 @@ constexpr int kRunRegs = kFE / kWave;  // partner runs per lane held in register
 constexpr int kSmall = 8;              // buckets up to this size are merged in registers
 constexpr int kTBits = 9;              // product index bits in s_t (row above them)
 constexpr uint32_t kTMask = (1u << kTBits) - 1u;
+// Output tag of a slot once its bucket is merged: the slot's output index in
+// the bucket (low kKBits bits) and, for a small bucket, the number of terms
+// merged into it (above them; 0 when the value is already final), or 0xffff
+// for a slot that writes nothing.
+constexpr int kKBits = 9;
+constexpr uint32_t kKMask = (1u << kKBits) - 1u;
+constexpr uint32_t kNoOut = 0xffffu;
+static_assert(kFP <= (1 << kKBits), "an output index must fit kKBits");
+static_assert(((kSmall + 1) << kKBits) < int(kNoOut), "a tag must fit 16 bits");
 static_assert(kFP <= (1 << kTBits), "product index must fit kTBits");
 static_assert(kFR <= (1 << (16 - kTBits)), "chunk row must fit above the product index");
 
@@ -79,10 +88,11 @@ struct WaveLds {
     uint16_t ent_len[kFE];
     uint16_t ent_poff[kFE + 1];
     uint8_t ent_row[kFE];
+    int32_t rlen[kFR];        // entries of every row of the batch
     int16_t owner[kFP];
     uint32_t s_j[kFP];
     uint16_t s_t[kFP];
-    uint16_t s_rank[kFP];     // large buckets: rank of a leader, 0xffff for the other products
+    uint16_t s_rank[kFP];     // output tag of every slot (see kKBits)
     uint16_t big[kFP / (kSmall + 1) + 1];  // large buckets of the batch
     uint32_t nbig;
     int64_t rbase[kFR];
@@ -193,6 +203,7 @@ struct Chunk {
         uint32_t nb = 0;
         if (lane < nrb) {
             const int r = ra + lane;
+            L.rlen[r] = int32_t(L.rp[r + 1] - L.rp[r]);
             const int64_t range = LOWER ? (r0 + r) : a.m_right;
             uint64_t want = L.rprod[r] > 0 ? L.rprod[r] : 1;
             if (range > 0 && uint64_t(range) < want) want = uint64_t(range);
@@ -311,7 +322,7 @@ struct Chunk {
             if (b < B) {
                 lo = b ? L.hist[b - 1] : 0u;
                 sz = L.hist[b] - lo;
-                if (sz == 1) L.s_rank[lo] = 1;
+                if (sz == 1) L.s_rank[lo] = uint16_t(1u << kKBits);
                 L.ucnt[b] = sz <= 1 ? sz : 0u;
             }
             // wave-aggregated appends
@@ -456,7 +467,7 @@ struct Chunk {
                 // the group of gj ends
                 L.s_j[lo + d] = gj;
                 L.s_v[lo + d] = acc;
-                L.s_rank[lo + d] = uint16_t(cnt);
+                L.s_rank[lo + d] = uint16_t((cnt << kKBits) | d);
                 ++d;
                 if (in) {
                     gj = j;
@@ -465,6 +476,10 @@ struct Chunk {
                 }
             }
         }
+        // the slots past the distinct columns write nothing
+#pragma unroll
+        for (int u = 1; u < N; ++u)
+            if (uint32_t(u) >= d && uint32_t(u) < sz) L.s_rank[lo + u] = uint16_t(kNoOut);
         return d;
     }
 
@@ -479,7 +494,8 @@ struct Chunk {
                 // terms in product order
                 L.s_v[lo] = t0 < t1 ? v0 + v1 : v1 + v0;
             }
-            L.s_rank[lo] = 2;
+            L.s_rank[lo] = uint16_t(2u << kKBits);
+            L.s_rank[lo + 1] = uint16_t(kNoOut);
             return 1;
         }
         if (j1 < j0) {
@@ -490,8 +506,8 @@ struct Chunk {
             L.s_v[lo] = v1;
             L.s_v[lo + 1] = v0;
         }
-        L.s_rank[lo] = 1;
-        L.s_rank[lo + 1] = 1;
+        L.s_rank[lo] = uint16_t(1u << kKBits);
+        L.s_rank[lo + 1] = uint16_t((1u << kKBits) | 1u);
         return 2;
     }
 
@@ -525,24 +541,14 @@ struct Chunk {
         // slot's bucket: consecutive lanes write consecutive slots of a row
         const uint16_t* sbk = reinterpret_cast<const uint16_t*>(L.owner);
         for (int q = lane; q < nprod; q += kWave) {
+            const uint32_t tag = L.s_rank[q];
+            if (tag == kNoOut) continue;
             const uint32_t b = sbk[q];
-            const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            const uint32_t u0 = L.ucnt[b];
-            uint32_t k;
-            bool out;
-            const bool small = hi - lo <= uint32_t(kSmall);
-            if (small) {
-                k = uint32_t(q) - lo;
-                out = k < L.ucnt[b + 1] - u0;
-            } else {
-                k = L.s_rank[q];
-                out = k != 0xffffu;
-            }
-            if (!out) continue;
             const int r = int(L.s_t[q] >> kTBits);
             Item v = L.s_v[q];
-            if (small) v = finish(v, int32_t(L.s_rank[q]), L.rp[r + 1] - L.rp[r]);
-            emit(L.rbase[r] + int64_t(u0 + k), L.s_j[q], v);
+            const uint32_t cnt = tag >> kKBits;
+            if (cnt) v = finish(v, int32_t(cnt), L.rlen[r]);
+            emit(L.rbase[r] + int64_t(uint32_t(L.ucnt[b]) + (tag & kKMask)), L.s_j[q], v);
         }
         // diagonals (lower triangle): the last entry of every non-empty row
         if (LOWER && lane < rb - ra) {
