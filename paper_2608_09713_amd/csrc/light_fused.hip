@@ -87,7 +87,7 @@ struct WaveLds {
     uint32_t ent_start[kFE];
     uint16_t ent_len[kFE];
     uint16_t ent_poff[kFE + 1];
-    uint8_t ent_row[kFE];
+    alignas(4) uint8_t ent_row[kFE];
     int32_t rlen[kFR];        // entries of every row of the batch
     int16_t owner[kFP];
     uint32_t s_j[kFP];
@@ -174,25 +174,40 @@ struct Chunk {
         const int64_t ebase = L.rp[ra];
         const int ne = int(L.rp[rb] - ebase);
         const uint32_t* __restrict__ key = a.cx.key;
+        // row of every entry: every non-empty row marks its first entry, then
+        // a max-scan (four entries per lane, one LDS word)
+        static_assert(kFE == 4 * kWave, "one word of entry rows per lane");
+        reinterpret_cast<uint32_t*>(L.ent_row)[lane] = 0u;
+        wave_sync();
+        if (lane < rb - ra) {
+            const int r = ra + lane;
+            if (L.rp[r + 1] > L.rp[r]) L.ent_row[L.rp[r] - ebase] = uint8_t(r);
+        }
 #pragma unroll
         for (int u = 0; u < kRunRegs; ++u) {
             const int x = lane + u * kWave;
             if (x < ne) {
-                const int64_t e = ebase + x;
-                int lo = ra, hi = rb - 1;  // last row of the batch starting at or before e
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (L.rp[mid] <= e)
-                        lo = mid;
-                    else
-                        hi = mid - 1;
-                }
                 const uint32_t len = rn[u].y - rn[u].x;
                 L.ent_start[x] = rn[u].x;
                 L.ent_len[x] = uint16_t(len);
-                L.ent_row[x] = uint8_t(lo);
                 L.ent_poff[x] = uint16_t(len);
             }
+        }
+        wave_sync();
+        {
+            const uint32_t wv = reinterpret_cast<const uint32_t*>(L.ent_row)[lane];
+            const uint32_t m0 = wv & 0xffu, m1 = max(m0, (wv >> 8) & 0xffu);
+            const uint32_t m2 = max(m1, (wv >> 16) & 0xffu), m3 = max(m2, wv >> 24);
+            uint32_t inc = m3;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) {
+                const uint32_t o = __shfl_up(inc, d, kWave);
+                if (lane >= d) inc = max(inc, o);
+            }
+            uint32_t before = __shfl_up(inc, 1, kWave);
+            if (lane == 0) before = 0;
+            reinterpret_cast<uint32_t*>(L.ent_row)[lane] = max(before, m0) | (max(before, m1) << 8) |
+                                                           (max(before, m2) << 16) | (max(before, m3) << 24);
         }
         wave_sync();
         const int P = int(wave_scan_lds(L.ent_poff, ne));
