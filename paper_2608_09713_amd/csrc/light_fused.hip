@@ -89,7 +89,7 @@ struct WaveLds {
     uint16_t ent_poff[kFE + 1];
     alignas(4) uint8_t ent_row[kFE];
     int32_t rlen[kFR];        // entries of every row of the batch
-    int16_t owner[kFP];
+    alignas(16) int16_t owner[kFP];
     uint32_t s_j[kFP];
     uint16_t s_t[kFP];
     uint16_t s_rank[kFP];     // output tag of every slot (see kKBits)
@@ -98,7 +98,7 @@ struct WaveLds {
     int64_t rbase[kFR];
     Item s_v[kFP];
     // per bucket (16 bits: every count and offset is at most kFP + kFR)
-    alignas(4) uint16_t hist[kFB + 2];
+    alignas(16) uint16_t hist[(kFB + 8) & ~7];
     uint16_t ucnt[kFB + 2];
 };
 
@@ -236,22 +236,29 @@ struct Chunk {
         const uint32_t inc = wave_inclusive_scan(nb);
         if (lane < nrb) L.rbb[ra + lane] = uint16_t(inc - nb);
         const uint32_t B = __shfl(inc, kWave - 1, kWave);
-        for (uint32_t b = lane; b <= B; b += kWave) {
-            L.hist[b] = 0;
-            L.ucnt[b] = 0;
-        }
-        // owner entry of every product: run starts scattered, then max-scan
-        for (int t = lane; t < P; t += kWave) L.owner[t] = -1;
+        // bucket counters zeroed eight at a time (every bucket's distinct count
+        // is set when the buckets are sorted by size)
+        for (uint32_t g = lane; 8 * g <= B; g += kWave) reinterpret_cast<uint4*>(L.hist)[g] = make_uint4(0, 0, 0, 0);
+        // owner entry of every product: run starts scattered, then a max-scan
+        // (eight products per lane, one 16-byte LDS word)
+        static_assert(kFP == 8 * kWave, "one 16-byte word of owners per lane");
+        reinterpret_cast<uint4*>(L.owner)[lane] = make_uint4(~0u, ~0u, ~0u, ~0u);
         wave_sync();
         for (int x = lane; x < ne; x += kWave)
             if (L.ent_len[x]) L.owner[L.ent_poff[x]] = int16_t(x);
         wave_sync();
         {
-            const int per = (P + kWave - 1) / kWave;
-            const int lo = min(P, lane * per), hi = min(P, lo + per);
-            int mx = -1;
-            for (int x = lo; x < hi; ++x) mx = max(mx, int(L.owner[x]));
-            int incm = mx;
+            const uint4 wv = reinterpret_cast<const uint4*>(L.owner)[lane];
+            const uint32_t wd[4] = {wv.x, wv.y, wv.z, wv.w};
+            int o[8];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                o[2 * k] = int(int16_t(wd[k] & 0xffffu));
+                o[2 * k + 1] = int(int16_t(wd[k] >> 16));
+            }
+#pragma unroll
+            for (int k = 1; k < 8; ++k) o[k] = max(o[k], o[k - 1]);
+            int incm = o[7];
 #pragma unroll
             for (int d = 1; d < kWave; d <<= 1) {
                 const int u = __shfl_up(incm, d, kWave);
@@ -259,10 +266,11 @@ struct Chunk {
             }
             int run = __shfl_up(incm, 1, kWave);
             if (lane == 0) run = -1;
-            for (int x = lo; x < hi; ++x) {
-                run = max(run, int(L.owner[x]));
-                L.owner[x] = int16_t(run);
-            }
+            uint32_t od[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                od[k] = (uint32_t(max(o[2 * k], run)) & 0xffffu) | (uint32_t(max(o[2 * k + 1], run)) << 16);
+            reinterpret_cast<uint4*>(L.owner)[lane] = make_uint4(od[0], od[1], od[2], od[3]);
         }
         wave_sync();
         // products: every key (and partner value) of the lane loaded in one round,
