@@ -427,6 +427,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     const int64_t nlight = m - nheavy;
     fa.rows_per_chunk = rows_per_chunk(nlight > 0 ? double(light_cap) / double(nlight) : 1.0);
     fa.nchunks = (m + fa.rows_per_chunk - 1) / fa.rows_per_chunk;
+    HIPCHK(hipMemsetAsync(&ctl->chunk_counter, 0, sizeof(ctl->chunk_counter), s));
+    fa.chunk_counter = &ctl->chunk_counter;
     fa.c_ci = s_ci;
     fa.c_val = s_val;
     {

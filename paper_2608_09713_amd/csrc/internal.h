@@ -131,6 +131,7 @@ struct FusedArgs {
     int64_t* row_cnt = nullptr;                // exact output length of every row
     int rows_per_chunk = 8;
     int64_t nchunks = 0;
+    unsigned long long* chunk_counter = nullptr;  // zeroed: chunks handed out so far
     int32_t* c_ci = nullptr;                   // staging columns
     void* c_val = nullptr;                     // staging values
 };

@@ -35,6 +35,7 @@ constexpr int kFP = kFusedProducts;  // products per batch
 constexpr int kFR = kFusedRows;      // rows per chunk (upper limit)
 constexpr int kFB = kFP + kFR;       // buckets per batch
 constexpr int kWavesF = 2;           // wavefronts per workgroup
+constexpr int kDealtBelow = 16;      // chunks per launched wavefront below which chunks are dealt out
 constexpr int kMaxBatches = kFR;
 constexpr int kRunRegs = kFE / kWave;  // partner runs per lane held in registers
 constexpr int kSmall = 8;              // buckets up to this size are merged in registers
@@ -707,14 +708,39 @@ __global__ __launch_bounds__(kWave* kWavesF) void fused_kernel(FusedArgs a) {
     __shared__ WaveLds<Item> lds[kWavesF];
     WaveLds<Item>& L = lds[threadIdx.x / kWave];
     Chunk<SR, LOWER> ch(a, L);
-    // persistent wavefronts: chunks c, c + stride, ...; the next chunk's head
-    // is loaded while the current chunk runs
-    const int64_t stride = int64_t(gridDim.x) * kWavesF;
-    int64_t c = int64_t(blockIdx.x) * kWavesF + threadIdx.x / kWave;
+    // Persistent wavefronts.  With few chunks per launched wavefront the
+    // chunks are dealt out in turn (c, c + stride, ...).  With many, the
+    // wavefronts take runs of consecutive chunks from a counter, so that
+    // every wavefront the device holds keeps busy however many of the
+    // launched ones are resident at once and however the chunks' costs vary:
+    // a run is a quarter of the chunks left per launched wavefront (as last
+    // seen), at least one, so the runs shrink towards the end.  The next
+    // chunk is taken and its head loaded while the current chunk runs.
+    const int lane = lane_id();
+    const int64_t nwaves = int64_t(gridDim.x) * kWavesF;
+    const bool dealt = a.nchunks < kDealtBelow * nwaves;
+    int64_t seen = 0, rend = 0;
+    auto take = [&]() -> int64_t {
+        if (dealt) {
+            const int64_t c = seen ? rend + nwaves - 1 : int64_t(blockIdx.x) * kWavesF + threadIdx.x / kWave;
+            seen = 1;
+            rend = c + 1;
+            return c;
+        }
+        int64_t g = (a.nchunks - seen) / (4 * nwaves);
+        g = g < 1 ? 1 : g;
+        unsigned long long c0 = 0;
+        if (lane == 0) c0 = atomicAdd(a.chunk_counter, (unsigned long long)g);
+        const int64_t c = int64_t(__shfl(c0, 0, kWave));
+        seen = c + g;
+        rend = c + g;
+        return c;
+    };
+    int64_t c = take();
     if (c >= a.nchunks) return;
     auto h = ch.head(c);
     while (true) {
-        const int64_t cn = c + stride;
+        const int64_t cn = c + 1 < rend ? c + 1 : take();
         decltype(h) hn;
         if (cn < a.nchunks) hn = ch.head(cn);
         ch.run(c, h);
