@@ -87,10 +87,10 @@ struct WaveLds {
     uint8_t bra[kMaxBatches + 1], brb[kMaxBatches + 1];  // batches [bra, brb) of the chunk
     uint32_t ent_start[kFE];
     uint16_t ent_len[kFE];
-    uint16_t ent_poff[kFE + 1];
     alignas(4) uint8_t ent_row[kFE];
     int32_t rlen[kFR];        // entries of every row of the batch
     alignas(16) int16_t owner[kFP];
+    alignas(16) uint16_t ent_poff[kFE + 1];
     uint32_t s_j[kFP];
     uint16_t s_t[kFP];
     uint16_t s_rank[kFP];     // output tag of every slot (see kKBits)
@@ -100,8 +100,12 @@ struct WaveLds {
     Item s_v[kFP];
     // per bucket (16 bits: every count and offset is at most kFP + kFR)
     alignas(16) uint16_t hist[(kFB + 8) & ~7];
-    uint16_t ucnt[kFB + 2];
+    alignas(16) uint16_t ucnt[kFB + 2];
 };
+// Two wavefronts' slices must stay within 26880 bytes for six workgroups per
+// compute unit (a few bytes more and only five fit, while the occupancy
+// query still reports six).
+static_assert(sizeof(WaveLds<int32_t>) * kWavesF <= 26880, "LDS slice of the count and Jaccard kernels");
 
 static_assert(kFP + kFR < (1 << 16), "bucket counters are 16 bits");
 
@@ -113,24 +117,45 @@ __device__ inline uint32_t add16(uint16_t* h, uint32_t b) {
     return (atomicAdd(w, 1u << sh) >> sh) & 0xffffu;
 }
 
-// exclusive scan in place of a[0..n) by one wavefront (lane = contiguous segment)
-template <typename T>
-__device__ inline uint32_t wave_scan_lds(T* a, int n) {
+// exclusive scan in place of the 16-bit a[0..n) by one wavefront, eight
+// elements per lane on 16-byte LDS words (a is 16-byte aligned and holds n
+// rounded up to eight; elements past n read as zero); returns the total
+__device__ inline uint32_t wave_scan16(uint16_t* a, int n) {
     const int lane = lane_id();
-    const int per = (n + kWave - 1) / kWave;
-    const int lo = min(n, lane * per), hi = min(n, lo + per);
-    uint32_t s = 0;
-    for (int x = lo; x < hi; ++x) s += uint32_t(a[x]);
-    const uint32_t inc = wave_inclusive_scan(s);
-    uint32_t off = inc - s;
-    const uint32_t tot = __shfl(inc, kWave - 1, kWave);
-    for (int x = lo; x < hi; ++x) {
-        const uint32_t v = uint32_t(a[x]);
-        a[x] = T(off);
-        off += v;
+    uint32_t carry = 0;
+    for (int base = 0; base < n; base += 8 * kWave) {
+        const int i0 = base + 8 * lane;
+        uint32_t v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (i0 < n) {
+            const uint4 w = *reinterpret_cast<const uint4*>(a + i0);
+            const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                v[2 * k] = i0 + 2 * k < n ? (wd[k] & 0xffffu) : 0u;
+                v[2 * k + 1] = i0 + 2 * k + 1 < n ? (wd[k] >> 16) : 0u;
+            }
+        }
+        uint32_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) sum += v[k];
+        const uint32_t inc = wave_inclusive_scan(sum);
+        uint32_t off = carry + inc - sum;
+        if (i0 < n) {
+            uint32_t od[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t lo16 = off;
+                off += v[2 * k];
+                const uint32_t hi16 = off;
+                off += v[2 * k + 1];
+                od[k] = (lo16 & 0xffffu) | (hi16 << 16);
+            }
+            *reinterpret_cast<uint4*>(a + i0) = make_uint4(od[0], od[1], od[2], od[3]);
+        }
+        carry += __shfl(inc, kWave - 1, kWave);
     }
     wave_sync();
-    return tot;
+    return carry;
 }
 
 template <int SR, bool LOWER>
@@ -211,7 +236,7 @@ struct Chunk {
                                                            (max(before, m2) << 16) | (max(before, m3) << 24);
         }
         wave_sync();
-        const int P = int(wave_scan_lds(L.ent_poff, ne));
+        const int P = int(wave_scan16(L.ent_poff, ne));
         if (lane == 0) L.ent_poff[ne] = uint16_t(P);
         // per-row buckets: one per product (at most one per possible column);
         // bucket of column j = floor(j * nb / range), monotone in j
@@ -311,7 +336,7 @@ struct Chunk {
             }
         }
         wave_sync();
-        wave_scan_lds(L.hist, int(B));
+        wave_scan16(L.hist, int(B));
         // scatter into buckets; hist[b] ends as the end of bucket b.  s_t keeps
         // the product index and, above it, the row (one row per bucket)
 #pragma unroll
@@ -441,7 +466,7 @@ struct Chunk {
             if (lane == 0) L.ucnt[b] = leaders;
             wave_sync();
         }
-        const uint32_t U = wave_scan_lds(L.ucnt, int(B));
+        const uint32_t U = wave_scan16(L.ucnt, int(B));
         if (lane == 0) L.ucnt[B] = U;
         wave_sync();
         // first output slot of every row minus its first bucket's offset
