@@ -166,6 +166,20 @@ def test_two_pass_path(dev, semiring, monkeypatch):
     compare_full(O, ref, semiring, "two-pass offdiag")
 
 
+def test_many_chunks_full_parity(dev):
+    # 2^21 rows: enough chunks per wavefront that the light-row kernel takes
+    # runs of chunks from its counter; every row is compared with the oracle
+    rng = np.random.default_rng(2024)
+    m, n, per_row = 1 << 21, 1 << 22, 4
+    c = np.sort(rng.integers(0, n, size=(m, per_row)), axis=1)
+    keep = np.ones_like(c, dtype=bool)
+    keep[:, 1:] = c[:, 1:] != c[:, :-1]
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(keep.sum(axis=1))
+    A = CSR(m, n, rp, c[keep].astype(np.int32), None)
+    run_lower(A, "count", dev, "2^21 rows, 4 columns each")
+
+
 WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
              ("offdiag_f64", 5)]
 
