@@ -1,13 +1,11 @@
-// Per-row product counts from the partner runs, and the compaction of the
-// staged light rows into the final CSR arrays.
+// Per-row product counts from the partner runs, the compaction of the staged
+// light rows into the final CSR arrays, the row of every tile start, and the
+// partner runs of an off-diagonal block from dense column starts.
 #include "common.h"
 #include "internal.h"
 
 namespace spsyrk {
 namespace {
-
-constexpr int kTileE = 2048;
-constexpr int kWin = 2048;
 
 __device__ inline int64_t last_leq(const int64_t* a, int64_t lo, int64_t hi, int64_t x) {
     // largest i in [lo, hi] with a[i] <= x (a non-decreasing, a[lo] <= x)
