@@ -284,7 +284,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         uint32_t* rb = ar.get_t<uint32_t>(N);
         uint32_t* ea = ar.get_t<uint32_t>(N);
         uint32_t* eb = ar.get_t<uint32_t>(N);
-        void* tmp = ar.get(radix_tmp_bytes(N));
+        void* tmp = ar.get(radix_csr_tmp_bytes(N, nbits_n));
         // Jaccard keeps the row lengths in the row field's spare bits
         const int lenbits = sr == kJaccard ? 32 - cx.rowbits : 0;
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,

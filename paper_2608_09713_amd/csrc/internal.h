@@ -60,6 +60,8 @@ void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 // Buffers *_a hold the input and the result is returned in the buffer
 // reported by the return value (0 -> *_a, 1 -> *_b).  vbytes in {0, 4, 8}.
 size_t radix_tmp_bytes(int64_t n);
+// scratch of radix_sort_csr for n entries and nbits-bit columns
+size_t radix_csr_tmp_bytes(int64_t n, int nbits);
 // Stable sort of the entries of a CSR matrix by column: the records
 // (column, row field, entry index) are formed inside the first pass.  The row
 // field is the row in its low rowbits bits and, if lenbits > 0, the row's

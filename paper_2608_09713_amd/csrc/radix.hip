@@ -9,6 +9,8 @@
 // its contiguous kSeg-record segment with ballot-based digit matching and
 // per-wave LDS counters, the tile is reordered through LDS, then written out
 // so that consecutive threads store consecutive addresses of a digit's run.
+#include <cstdlib>
+
 #include "common.h"
 #include "internal.h"
 
@@ -263,6 +265,205 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     }
 }
 
+// ---- local sort of the low key bits inside groups of equal high bits
+//
+// After stable passes over the high bits [L, nbits) the records of every
+// value v of the high bits form one contiguous group, in input order.  One
+// workgroup per v sorts its group stably by the low L <= kLBits bits: in LDS
+// (the low bits and the records' indices in the group, 6-bit digits), then
+// gathers the records into place; a group too large for LDS is sorted by the
+// same workgroup over global memory, tile by tile.
+
+constexpr int kLBits = 12;       // low bits sorted locally
+constexpr int kLCap = 4096;      // records of a group sorted in LDS
+constexpr int kLDig = 6;         // bits per local digit
+constexpr uint32_t kNoGroup = 0xffffffffu;
+
+// first and end position of every group of equal high bits (groups that do
+// not occur keep kNoGroup)
+__global__ __launch_bounds__(kBlock) void group_bounds(const uint32_t* __restrict__ key, int64_t n, int L,
+                                                       uint32_t* __restrict__ gstart, uint32_t* __restrict__ gend) {
+    const int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (p >= n) return;
+    const uint32_t v = key[p] >> L;
+    if (p == 0 || (key[p - 1] >> L) != v) {
+        gstart[v] = uint32_t(p);
+        if (p > 0) gend[key[p - 1] >> L] = uint32_t(p);
+    }
+    if (p == n - 1) gend[v] = uint32_t(n);
+}
+
+// one stable pass of the LDS sort: (dig, idx) of S <= kLCap records by bits
+// [sh, sh + w) of dig, from the *_in arrays to the *_out arrays
+__device__ inline void lds_pass(const uint16_t* dig_in, const uint16_t* idx_in, uint16_t* dig_out, uint16_t* idx_out,
+                                int S, int sh, int w, uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
+    constexpr int kCh = kLCap / kWavesPerBlock / kWave;  // chunks of a wave's segment
+    const int wv = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const uint32_t m = (1u << w) - 1u;
+    const int seg = ((S + kWavesPerBlock - 1) / kWavesPerBlock + kWave - 1) / kWave * kWave;
+    const int s0 = wv * seg, s1 = min(S, s0 + seg);
+    wcnt[wv][lane] = 0;
+    __syncthreads();
+    const uint64_t lt = lanemask_lt();
+    const int nch = seg / kWave;  // (the same in every wavefront)
+    uint32_t loc[kCh];
+    uint32_t dd[kCh];
+#pragma unroll
+    for (int c = 0; c < kCh; ++c) {
+        if (c >= nch) break;
+        const int i = s0 + c * kWave + lane;
+        const bool valid = i < s1;
+        const uint32_t d = valid ? (uint32_t(dig_in[i]) >> sh) & m : 0u;
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < w; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bal = __ballot(bit);
+            peers &= bit ? bal : ~bal;
+        }
+        uint32_t cur = 0;
+        if (valid) cur = wcnt[wv][d];
+        const uint32_t rank = __popcll(peers & lt);
+        loc[c] = cur + rank;
+        dd[c] = d;
+        if (valid && rank == 0) wcnt[wv][d] = cur + uint32_t(__popcll(peers));
+    }
+    __syncthreads();
+    {
+        // exclusive offsets in (digit, wavefront) order: thread t = digit * waves + wave
+        const int d = threadIdx.x / kWavesPerBlock, q = threadIdx.x % kWavesPerBlock;
+        const uint32_t v = wcnt[q][d];
+        uint32_t tot;
+        const uint32_t off = block_exclusive_scan(v, wt, &tot);
+        __syncthreads();
+        wcnt[q][d] = off;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < kCh; ++c) {
+        if (c >= nch) break;
+        const int i = s0 + c * kWave + lane;
+        if (i < s1) {
+            const uint32_t dest = wcnt[wv][dd[c]] + loc[c];
+            dig_out[dest] = dig_in[i];
+            idx_out[dest] = idx_in[i];
+        }
+    }
+    __syncthreads();
+}
+
+// one stable pass of the global-memory sort of a large group [b0, b0 + S):
+// by bits [sh, sh + w) of the key, from the *i arrays to the *o arrays, in
+// tiles of kBlock records in order
+__device__ inline void group_pass(const uint32_t* ki, const uint32_t* ri, const uint32_t* ei, uint32_t* ko, uint32_t* ro,
+                                  uint32_t* eo, int64_t b0, int64_t S, int sh, int w, uint32_t* base,
+                                  uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
+    const int wv = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const uint32_t m = (1u << w) - 1u;
+    if (threadIdx.x < (1 << kLDig)) base[threadIdx.x] = 0;
+    __syncthreads();
+    for (int64_t i = threadIdx.x; i < S; i += kBlock) atomicAdd(&base[(ki[b0 + i] >> sh) & m], 1u);
+    __syncthreads();
+    {
+        const uint32_t v = threadIdx.x < (1 << kLDig) ? base[threadIdx.x] : 0u;
+        uint32_t tot;
+        const uint32_t off = block_exclusive_scan(v, wt, &tot);
+        __syncthreads();
+        if (threadIdx.x < (1 << kLDig)) base[threadIdx.x] = off;
+    }
+    __syncthreads();
+    const uint64_t lt = lanemask_lt();
+    for (int64_t t0 = 0; t0 < S; t0 += kBlock) {
+        const int64_t i = t0 + threadIdx.x;
+        const bool valid = i < S;
+        const uint32_t kv = valid ? ki[b0 + i] : 0u;
+        const uint32_t d = (kv >> sh) & m;
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < w; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bal = __ballot(bit);
+            peers &= bit ? bal : ~bal;
+        }
+        const uint32_t rank = __popcll(peers & lt);
+        wcnt[wv][lane] = 0;
+        __syncthreads();
+        if (valid && rank == 0) wcnt[wv][d] = uint32_t(__popcll(peers));
+        __syncthreads();
+        uint32_t before = 0;
+        for (int q = 0; q < wv; ++q) before += wcnt[q][d];
+        if (valid) {
+            const int64_t dest = b0 + int64_t(base[d] + before + rank);
+            ko[dest] = kv;
+            ro[dest] = ri[b0 + i];
+            eo[dest] = ei[b0 + i];
+        }
+        __syncthreads();
+        if (threadIdx.x < (1 << kLDig)) {
+            uint32_t add = 0;
+            for (int q = 0; q < kWavesPerBlock; ++q) add += wcnt[q][threadIdx.x];
+            base[threadIdx.x] += add;
+        }
+        __syncthreads();
+    }
+}
+
+// Group v = blockIdx.x: sort [gstart[v], gend[v]) of (kx, rx, ex) stably by
+// the low L bits of the key into (ky, ry, ey).  A group over kLCap records
+// uses x and y in turn over global memory and ends in y.
+__global__ __launch_bounds__(kBlock) void local_sort(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
+                                                     uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
+                                                     uint32_t* __restrict__ ry, uint32_t* __restrict__ ey,
+                                                     const uint32_t* __restrict__ gstart,
+                                                     const uint32_t* __restrict__ gend, int L) {
+    __shared__ uint16_t dg[2][kLCap];
+    __shared__ uint16_t ix[2][kLCap];
+    __shared__ uint32_t wcnt[kWavesPerBlock][1 << kLDig];
+    __shared__ uint32_t base[1 << kLDig];
+    __shared__ uint32_t wt[kWavesPerBlock];
+    static_assert(kWavesPerBlock * (1 << kLDig) == kBlock, "one thread per (digit, wavefront)");
+    static_assert(kLCap <= 65536, "indices in a group are 16 bits");
+    const uint32_t g0 = gstart[blockIdx.x];
+    if (g0 == kNoGroup) return;
+    const int64_t b0 = g0;
+    const int64_t S = int64_t(gend[blockIdx.x]) - b0;
+    const uint32_t lmask = (1u << L) - 1u;
+    if (S <= kLCap) {
+        for (int i = threadIdx.x; i < S; i += kBlock) {
+            dg[0][i] = uint16_t(kx[b0 + i] & lmask);
+            ix[0][i] = uint16_t(i);
+        }
+        __syncthreads();
+        int cur = 0;
+        for (int sh = 0; sh < L; sh += kLDig) {
+            lds_pass(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], int(S), sh, min(kLDig, L - sh), wcnt, wt);
+            cur ^= 1;
+        }
+        for (int j = threadIdx.x; j < S; j += kBlock) {
+            const int64_t src = b0 + ix[cur][j];
+            ky[b0 + j] = kx[src];
+            ry[b0 + j] = rx[src];
+            ey[b0 + j] = ex[src];
+        }
+        return;
+    }
+    // a large group: passes over global memory, x -> y -> x ..., ending in y
+    int npass = 0;
+    for (int sh = 0; sh < L; sh += kLDig) {
+        const bool to_y = (npass & 1) == 0;
+        group_pass(to_y ? kx : ky, to_y ? rx : ry, to_y ? ex : ey, to_y ? ky : kx, to_y ? ry : rx, to_y ? ey : ex, b0,
+                   S, sh, min(kLDig, L - sh), base, wcnt, wt);
+        ++npass;
+    }
+    if ((npass & 1) == 0) {
+        for (int64_t i = threadIdx.x; i < S; i += kBlock) {
+            ky[b0 + i] = kx[b0 + i];
+            ry[b0 + i] = rx[b0 + i];
+            ey[b0 + i] = ex[b0 + i];
+        }
+    }
+}
+
 template <int VB, bool FIRST = false>
 void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
               int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s, const int64_t* rp = nullptr,
@@ -289,6 +490,30 @@ int digit_plan(int nbits, int (&width)[8]) {
 
 }  // namespace
 
+// Local-sort plan of a CSR column sort: the high h = nbits - L bits by passes,
+// the low L (1..kLBits) bits inside groups of equal high bits, about 2048
+// records per group on average.  Used for wide keys over many entries
+// (SPSYRK_LOCAL_SORT=1 forces it wherever it applies, =0 turns it off; read
+// at every call).  Returns L, or 0 for passes over all bits.
+int local_bits(int64_t n, int nbits) {
+    const char* e = std::getenv("SPSYRK_LOCAL_SORT");
+    const bool force = e && e[0] == '1';
+    if (e && e[0] == '0') return 0;
+    if (!force && (nbits < 22 || n < (int64_t(1) << 20))) return 0;
+    int h = nbits - kLBits;
+    const int hg = bit_width_u64(uint64_t(n / 2048));  // groups of about 2048 records
+    if (hg > h) h = hg;
+    if (h < 1) h = 1;
+    const int L = nbits - h;
+    return L >= 1 ? L : 0;
+}
+
+size_t radix_csr_tmp_bytes(int64_t n, int nbits) {
+    const int L = local_bits(n, nbits);
+    const size_t groups = L ? (size_t(1) << (nbits - L)) : 0;
+    return radix_tmp_bytes(n) + 2 * ((groups * sizeof(uint32_t) + 255) & ~size_t(255));
+}
+
 size_t radix_tmp_bytes(int64_t n) {
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     const size_t hist = size_t(ntiles) * kDigits * sizeof(uint32_t);
@@ -306,15 +531,17 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     const size_t table_bytes = (size_t(ntiles + 1) * sizeof(int64_t) + 255) & ~size_t(255);
     int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + hist_bytes);
     void* scan_tmp = static_cast<char*>(tmp) + hist_bytes + table_bytes;
+    // passes over all bits, or over the high bits followed by the local sort
+    const int L = local_bits(n, nbits);
     int width[8];
-    const int passes = digit_plan(nbits, width);
+    const int passes = digit_plan(nbits - L, width);
     // first pass straight from the CSR arrays (into the b buffers), at least
     // one pass; the row of every tile's first entry comes from a table
     tile_first_rows(rp, m, kRTile, trow, s);
-    run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, 0,
+    run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
                       (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
     int cur = 1;
-    int shift = width[0];
+    int shift = L + width[0];
     for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
         const uint32_t mask = (1u << width[ps]) - 1u;
         uint32_t* ki = cur ? key_b : key_a;
@@ -326,7 +553,20 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
         run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
         cur ^= 1;
     }
-    return cur;
+    if (L == 0) return cur;
+    // groups of equal high bits, each sorted by the low L bits into the other buffers
+    const size_t groups = size_t(1) << (nbits - L);
+    const size_t base_bytes = radix_tmp_bytes(n);
+    uint32_t* gstart = reinterpret_cast<uint32_t*>(static_cast<char*>(tmp) + base_bytes);
+    uint32_t* gend = gstart + (((groups * sizeof(uint32_t) + 255) & ~size_t(255)) / sizeof(uint32_t));
+    fill_u32(gstart, int64_t(groups), kNoGroup, s);
+    uint32_t* kx = cur ? key_b : key_a;
+    uint32_t* rx = cur ? row_b : row_a;
+    uint32_t* ex = cur ? ent_b : ent_a;
+    group_bounds<<<unsigned((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(kx, n, L, gstart, gend);
+    local_sort<<<unsigned(groups), kBlock, 0, s>>>(kx, rx, ex, cur ? key_a : key_b, cur ? row_a : row_b,
+                                                   cur ? ent_a : ent_b, gstart, gend, L);
+    return cur ^ 1;
 }
 
 int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a, void* val_b,

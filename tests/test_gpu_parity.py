@@ -180,6 +180,35 @@ def test_many_chunks_full_parity(dev):
     run_lower(A, "count", dev, "2^21 rows, 4 columns each")
 
 
+def _rows_csr(rng, m, n, per_row, dtype=np.float64):
+    c = np.sort(rng.integers(0, n, size=(m, per_row)), axis=1)
+    keep = np.ones_like(c, dtype=bool)
+    keep[:, 1:] = c[:, 1:] != c[:, :-1]
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(keep.sum(axis=1))
+    ci = c[keep].astype(np.int32)
+    return CSR(m, n, rp, ci, rng.random(len(ci)).astype(dtype) + 0.5)
+
+
+@pytest.mark.parametrize("semiring", ["f64", "count", "jaccard"])
+def test_local_sort_path(dev, semiring, monkeypatch):
+    # the column sort's local pass (high bits by passes, low bits inside
+    # groups), forced on small inputs: 2^20 columns give 256 groups sorted in
+    # LDS; 8192 columns give two groups of about 6000 entries, sorted over
+    # global memory
+    monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
+    rng = np.random.default_rng(31)
+    for m, n, per in ((3000, 1 << 20, 6), (3000, 8192, 4)):
+        A = _rows_csr(rng, m, n, per)
+        run_lower(A, semiring, dev, f"local sort m={m} n={n}")
+        B = _rows_csr(rng, 2000, n, per)
+        vdt = VDT[semiring]
+        O = sp.offdiag(upload(A, semiring, dev), upload(B, semiring, dev), semiring)
+        ref = oracle.offdiag(A.with_values(None if vdt is None else A.values.astype(vdt)),
+                             B.with_values(None if vdt is None else B.values.astype(vdt)), semiring)
+        compare_full(O, ref, semiring, f"local sort offdiag n={n}")
+
+
 WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
              ("offdiag_f64", 5)]
 
