@@ -281,16 +281,39 @@ constexpr uint32_t kNoGroup = 0xffffffffu;
 
 // first and end position of every group of equal high bits (groups that do
 // not occur keep kNoGroup)
+// (eight keys per thread, read with 16-byte loads when the keys are aligned)
 __global__ __launch_bounds__(kBlock) void group_bounds(const uint32_t* __restrict__ key, int64_t n, int L,
                                                        uint32_t* __restrict__ gstart, uint32_t* __restrict__ gend) {
-    const int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (p >= n) return;
-    const uint32_t v = key[p] >> L;
-    if (p == 0 || (key[p - 1] >> L) != v) {
-        gstart[v] = uint32_t(p);
-        if (p > 0) gend[key[p - 1] >> L] = uint32_t(p);
+    const int64_t p0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * 8;
+    if (p0 >= n) return;
+    uint32_t k[9];  // key p0 - 1 (or none), then keys p0 .. p0 + 7
+    k[0] = p0 > 0 ? key[p0 - 1] : 0u;
+    if (p0 + 8 <= n && (reinterpret_cast<uintptr_t>(key + p0) & 15) == 0) {
+        const uint4 a = reinterpret_cast<const uint4*>(key + p0)[0];
+        const uint4 b = reinterpret_cast<const uint4*>(key + p0)[1];
+        k[1] = a.x;
+        k[2] = a.y;
+        k[3] = a.z;
+        k[4] = a.w;
+        k[5] = b.x;
+        k[6] = b.y;
+        k[7] = b.z;
+        k[8] = b.w;
+    } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) k[u + 1] = p0 + u < n ? key[p0 + u] : 0u;
     }
-    if (p == n - 1) gend[v] = uint32_t(n);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int64_t p = p0 + u;
+        if (p >= n) break;
+        const uint32_t v = k[u + 1] >> L;
+        if (p == 0 || (k[u] >> L) != v) {
+            gstart[v] = uint32_t(p);
+            if (p > 0) gend[k[u] >> L] = uint32_t(p);
+        }
+        if (p == n - 1) gend[v] = uint32_t(n);
+    }
 }
 
 // one stable pass of the LDS sort: (dig, idx) of S <= kLCap records by bits
@@ -563,7 +586,7 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     uint32_t* kx = cur ? key_b : key_a;
     uint32_t* rx = cur ? row_b : row_a;
     uint32_t* ex = cur ? ent_b : ent_a;
-    group_bounds<<<unsigned((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(kx, n, L, gstart, gend);
+    group_bounds<<<unsigned((n + 8 * kBlock - 1) / (8 * kBlock)), kBlock, 0, s>>>(kx, n, L, gstart, gend);
     local_sort<<<unsigned(groups), kBlock, 0, s>>>(kx, rx, ex, cur ? key_a : key_b, cur ? row_a : row_b,
                                                    cur ? ent_a : ent_b, gstart, gend, L);
     return cur ^ 1;
