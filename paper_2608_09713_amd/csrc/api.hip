@@ -287,15 +287,34 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         void* tmp = ar.get(radix_csr_tmp_bytes(N, nbits_n));
         // Jaccard keeps the row lengths in the row field's spare bits
         const int lenbits = sr == kJaccard ? 32 - cx.rowbits : 0;
+        // with no directory a local sort writes the index itself (keys and
+        // values at sorted positions, partner runs, the kept count)
+        LocalPack pk;
+        if (runs_given) {
+            pk.run = run;
+            pk.key = cx.key;
+            pk.val = cx.val;
+            pk.vals_b = B.v;
+            pk.rp_b = B.rp;
+            pk.vbytes = vb;
+            pk.jac = sr == kJaccard;
+            pk.rowbits = cx.rowbits;
+            pk.lenbits = lenbits;
+            pk.drop_last = drop_last;
+            pk.kept = &ctl->nkept;
+            HIPCHK(hipMemsetAsync(&ctl->nkept, 0, sizeof(int64_t), s));
+        }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
-                                         s);
+                                         s, runs_given ? &pk : nullptr);
         check_launch();
         ar.release(tmp);
-        void* ctmp = ar.get(colindex_tmp_bytes(N));
-        build_colindex(which ? kb : ka, which ? rb : ra, which ? eb : ea, N, drop_last, vb, sr, B.v, B.rp, lenbits, cx,
-                       ctmp, &ctl->nkept, run, s);
-        check_launch();
-        ar.release(ctmp);
+        if (which >= 0) {
+            void* ctmp = ar.get(colindex_tmp_bytes(N));
+            build_colindex(which ? kb : ka, which ? rb : ra, which ? eb : ea, N, drop_last, vb, sr, B.v, B.rp, lenbits,
+                           cx, ctmp, &ctl->nkept, run, s);
+            check_launch();
+            ar.release(ctmp);
+        }
         ar.release(ka);
         ar.release(kb);
         ar.release(ra);

@@ -67,9 +67,28 @@ size_t radix_csr_tmp_bytes(int64_t n, int nbits);
 // field is the row in its low rowbits bits and, if lenbits > 0, the row's
 // length saturated at 2^lenbits - 1 above them.  Returns 0 if the result is in
 // the *_a buffers, 1 for *_b.
+// The column index in partner-run form, written by the sort itself when it
+// takes the local path: key (the row) and value of every entry at its sorted
+// position, and (run non-null, zeroed) every entry's partner run {first
+// position of its column, its own position}.  *kept (zeroed) gets the kept
+// entries (all, or all but the last of every column with drop_last).
+struct LocalPack {
+    uint2* run = nullptr;
+    uint32_t* key = nullptr;
+    void* val = nullptr;
+    const void* vals_b = nullptr;  // values of B by entry index (vbytes 4 or 8)
+    const int64_t* rp_b = nullptr; // row pointers of B (Jaccard lengths)
+    int vbytes = 0;
+    bool jac = false;
+    int rowbits = 1, lenbits = 0;
+    bool drop_last = false;
+    int64_t* kept = nullptr;
+};
+// pk non-null: write the column index as above when the local path is taken
+// and return -1 (no sorted copy); otherwise as described.
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
-                   int nbits, void* tmp, hipStream_t s);
+                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk = nullptr);
 int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a,
                void* val_b, int vbytes, int64_t n, int nbits, void* tmp, hipStream_t s);
 

@@ -487,6 +487,151 @@ __global__ __launch_bounds__(kBlock) void local_sort(uint32_t* __restrict__ kx, 
     }
 }
 
+// ---- the column index in partner-run form, straight from the local sort
+//
+// Instead of a sorted copy of the records, the workgroup of a group writes
+// the key (the row) and value of every entry at its sorted position, and in
+// lower mode every entry's partner run {first position of its column, its
+// own position}: the entries of its column with a smaller row.  (The last
+// entry of a column is never a partner; its slot is written but not read.)
+
+template <int VB, bool JAC>
+__device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t field, uint32_t ent, int64_t cstart) {
+    const uint32_t rowmask = pk.rowbits >= 32 ? 0xffffffffu : ((1u << pk.rowbits) - 1u);
+    const uint32_t row = field & rowmask;
+    pk.key[pos] = row;
+    if constexpr (JAC) {
+        const uint32_t lmax = pk.lenbits > 0 ? (1u << pk.lenbits) - 1u : 0u;
+        const uint32_t lf = pk.lenbits > 0 ? field >> pk.rowbits : lmax;
+        static_cast<int32_t*>(pk.val)[pos] = lf < lmax ? int32_t(lf) : int32_t(pk.rp_b[row + 1] - pk.rp_b[row]);
+    } else if constexpr (VB == 8) {
+        static_cast<uint64_t*>(pk.val)[pos] = static_cast<const uint64_t*>(pk.vals_b)[ent];
+    } else if constexpr (VB == 4) {
+        static_cast<uint32_t*>(pk.val)[pos] = static_cast<const uint32_t*>(pk.vals_b)[ent];
+    }
+    if (pk.run && pos > cstart) pk.run[ent] = make_uint2(uint32_t(cstart), uint32_t(pos));
+}
+
+// maximum of v over the threads before this one in the workgroup (0 for the
+// first thread); *all gets the maximum over every thread
+__device__ inline uint32_t block_exclusive_max(uint32_t v, uint32_t* wt, uint32_t* all) {
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    uint32_t inc = v;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t u = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc = max(inc, u);
+    }
+    if (lane == kWave - 1) wt[w] = inc;
+    __syncthreads();
+    uint32_t before = 0, mx = 0;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) {
+        const uint32_t t = wt[q];
+        if (q < w) before = max(before, t);
+        mx = max(mx, t);
+    }
+    __syncthreads();
+    const uint32_t prev = __shfl_up(inc, 1, kWave);
+    if (lane > 0) before = max(before, prev);
+    *all = mx;
+    return before;
+}
+
+template <int VB, bool JAC>
+__global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
+                                                          uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
+                                                          uint32_t* __restrict__ ry, uint32_t* __restrict__ ey,
+                                                          const uint32_t* __restrict__ gstart,
+                                                          const uint32_t* __restrict__ gend, int L, LocalPack pk) {
+    __shared__ uint16_t dg[2][kLCap];
+    __shared__ uint16_t ix[2][kLCap];
+    __shared__ uint32_t wcnt[kWavesPerBlock][1 << kLDig];
+    __shared__ uint32_t base[1 << kLDig];
+    __shared__ uint32_t wt[kWavesPerBlock];
+    constexpr int kPer = kLCap / kBlock;
+    const uint32_t g0 = gstart[blockIdx.x];
+    if (g0 == kNoGroup) return;
+    const int64_t b0 = g0;
+    const int64_t S = int64_t(gend[blockIdx.x]) - b0;
+    const uint32_t lmask = (1u << L) - 1u;
+    uint32_t distinct = 0;
+    if (S <= kLCap) {
+        for (int i = threadIdx.x; i < S; i += kBlock) {
+            dg[0][i] = uint16_t(kx[b0 + i] & lmask);
+            ix[0][i] = uint16_t(i);
+        }
+        __syncthreads();
+        int cur = 0;
+        for (int sh = 0; sh < L; sh += kLDig) {
+            lds_pass(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], int(S), sh, min(kLDig, L - sh), wcnt, wt);
+            cur ^= 1;
+        }
+        // first position of every entry's column: the positions where the low
+        // bits change, then a max-scan (kPer consecutive positions per thread)
+        uint16_t* cs = dg[cur ^ 1];
+        {
+            const int j0 = threadIdx.x * kPer;
+            uint32_t run[kPer];
+            uint32_t mx = 0, nst = 0;
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const int j = j0 + k;
+                if (j < S && (j == 0 || dg[cur][j - 1] != dg[cur][j])) {
+                    mx = uint32_t(j);
+                    ++nst;
+                }
+                run[k] = mx;
+            }
+            uint32_t all;
+            const uint32_t before = block_exclusive_max(mx, wt, &all);
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const int j = j0 + k;
+                if (j < S) cs[j] = uint16_t(max(run[k], before));
+            }
+            uint32_t tot;
+            (void)block_exclusive_scan(nst, wt, &tot);
+            distinct = tot;
+        }
+        __syncthreads();
+        for (int j = threadIdx.x; j < S; j += kBlock) {
+            const int64_t src = b0 + ix[cur][j];
+            emit_entry<VB, JAC>(pk, b0 + j, rx[src], ex[src], b0 + cs[j]);
+        }
+    } else {
+        // a large group: passes over global memory, x -> y -> x ..., ending in y
+        int npass = 0;
+        for (int sh = 0; sh < L; sh += kLDig) {
+            const bool to_y = (npass & 1) == 0;
+            group_pass(to_y ? kx : ky, to_y ? rx : ry, to_y ? ex : ey, to_y ? ky : kx, to_y ? ry : rx,
+                       to_y ? ey : ex, b0, S, sh, min(kLDig, L - sh), base, wcnt, wt);
+            ++npass;
+        }
+        const uint32_t* ks = (npass & 1) ? ky : kx;
+        const uint32_t* rs = (npass & 1) ? ry : rx;
+        const uint32_t* es = (npass & 1) ? ey : ex;
+        // the same output, a tile at a time, the column start carried over
+        uint32_t carry = 0;
+        for (int64_t t0 = 0; t0 < S; t0 += kBlock) {
+            const int64_t j = t0 + threadIdx.x;
+            const bool st = j < S && (j == 0 || ks[b0 + j - 1] != ks[b0 + j]);
+            const uint32_t v = st ? uint32_t(j) : 0u;
+            uint32_t all;
+            const uint32_t cstart = max(max(block_exclusive_max(v, wt, &all), v), carry);
+            uint32_t tot;
+            (void)block_exclusive_scan(st ? 1u : 0u, wt, &tot);
+            distinct += tot;
+            if (j < S) emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart);
+            carry = max(carry, all);
+        }
+    }
+    if (threadIdx.x == 0 && pk.kept)
+        atomicAdd(reinterpret_cast<unsigned long long*>(pk.kept),
+                  (unsigned long long)(pk.drop_last ? S - int64_t(distinct) : S));
+}
+
 template <int VB, bool FIRST = false>
 void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
               int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s, const int64_t* rp = nullptr,
@@ -546,7 +691,7 @@ size_t radix_tmp_bytes(int64_t n) {
 
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
-                   int nbits, void* tmp, hipStream_t s) {
+                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk) {
     if (n <= 0) return 0;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     uint32_t* hist = static_cast<uint32_t*>(tmp);
@@ -587,8 +732,22 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     uint32_t* rx = cur ? row_b : row_a;
     uint32_t* ex = cur ? ent_b : ent_a;
     group_bounds<<<unsigned((n + 8 * kBlock - 1) / (8 * kBlock)), kBlock, 0, s>>>(kx, n, L, gstart, gend);
-    local_sort<<<unsigned(groups), kBlock, 0, s>>>(kx, rx, ex, cur ? key_a : key_b, cur ? row_a : row_b,
-                                                   cur ? ent_a : ent_b, gstart, gend, L);
+    uint32_t* ky = cur ? key_a : key_b;
+    uint32_t* ry = cur ? row_a : row_b;
+    uint32_t* ey = cur ? ent_a : ent_b;
+    if (pk) {
+        const unsigned g = unsigned(groups);
+        if (pk->jac)
+            local_sort_pack<0, true><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
+        else if (pk->vbytes == 8)
+            local_sort_pack<8, false><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
+        else if (pk->vbytes == 4)
+            local_sort_pack<4, false><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
+        else
+            local_sort_pack<0, false><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
+        return -1;
+    }
+    local_sort<<<unsigned(groups), kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L);
     return cur ^ 1;
 }
 
