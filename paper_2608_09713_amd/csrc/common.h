@@ -10,6 +10,7 @@ namespace spsyrk {
 constexpr int kWave = 64;        // gfx950 wavefront width
 constexpr int kBlock = 256;      // threads per workgroup used by most kernels
 constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kXcds = 8;         // XCDs of the chip; workgroups are dealt to them round-robin
 
 // error bits raised by validation kernels (OR-ed into one device word)
 enum ErrBits : uint32_t {

@@ -102,6 +102,11 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
                                                         int64_t ntiles, const int64_t* __restrict__ rp, int64_t m,
                                                         const int64_t* __restrict__ trow, int rowbits, int lenbits) {
     using V = typename ValT<VB>::T;
+    // consecutive tiles on one XCD (workgroups go round-robin over the XCDs),
+    // so the partial lines where their digit runs meet merge in one L2
+    const int64_t per = (ntiles + kXcds - 1) / kXcds;
+    const int64_t tile = int64_t(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+    if (tile >= ntiles) return;
     __shared__ int64_t rwin[FIRST ? kRowWin + 1 : 1];
     __shared__ int64_t rbounds[2];
     __shared__ uint32_t wcnt[kWavesPerBlock][kDigits];
@@ -117,7 +122,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     for (int q = 0; q < kWavesPerBlock; ++q) wcnt[q][threadIdx.x] = 0;
     __syncthreads();
 
-    const int64_t base = int64_t(blockIdx.x) * kRTile;
+    const int64_t base = tile * kRTile;
     const int64_t segbase = base + int64_t(w) * kSeg;
     int64_t rlo = 0, rhi = 0;
     bool rstaged = false;
@@ -125,9 +130,9 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         if (threadIdx.x == 0) {
             // rows of the tile's first entry and (at most one row past the
             // tile) of its end, from the tile table; the last tile searches
-            const int64_t lo = trow[blockIdx.x];
+            const int64_t lo = trow[tile];
             rbounds[0] = lo;
-            rbounds[1] = base + kRTile < n ? trow[blockIdx.x + 1] : last_leq_i64(rp, lo, m, n - 1);
+            rbounds[1] = base + kRTile < n ? trow[tile + 1] : last_leq_i64(rp, lo, m, n - 1);
         }
         __syncthreads();
         rlo = rbounds[0];
@@ -227,7 +232,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         }
         uint32_t all;
         uint32_t off = block_exclusive_scan(tot, wt, &all);
-        gofs[d] = int64_t(offs[int64_t(d) * ntiles + blockIdx.x]) - int64_t(off);
+        gofs[d] = int64_t(offs[int64_t(d) * ntiles + tile]) - int64_t(off);
 #pragma unroll
         for (int q = 0; q < kWavesPerBlock; ++q) {
             wcnt[q][d] = off;
@@ -495,8 +500,18 @@ __global__ __launch_bounds__(kBlock) void local_sort(uint32_t* __restrict__ kx, 
 // own position}: the entries of its column with a smaller row.  (The last
 // entry of a column is never a partner; its slot is written but not read.)
 
+template <int VB>
+__device__ inline typename ValT<VB>::T entry_value(const LocalPack& pk, uint32_t ent) {
+    if constexpr (VB == 0)
+        return 0;
+    else
+        return static_cast<const typename ValT<VB>::T*>(pk.vals_b)[ent];
+}
+
+// v: the entry's value (VB 4 or 8), read by the caller
 template <int VB, bool JAC>
-__device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t field, uint32_t ent, int64_t cstart) {
+__device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t field, uint32_t ent, int64_t cstart,
+                                  typename ValT<VB>::T v) {
     const uint32_t rowmask = pk.rowbits >= 32 ? 0xffffffffu : ((1u << pk.rowbits) - 1u);
     const uint32_t row = field & rowmask;
     pk.key[pos] = row;
@@ -504,10 +519,8 @@ __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t fie
         const uint32_t lmax = pk.lenbits > 0 ? (1u << pk.lenbits) - 1u : 0u;
         const uint32_t lf = pk.lenbits > 0 ? field >> pk.rowbits : lmax;
         static_cast<int32_t*>(pk.val)[pos] = lf < lmax ? int32_t(lf) : int32_t(pk.rp_b[row + 1] - pk.rp_b[row]);
-    } else if constexpr (VB == 8) {
-        static_cast<uint64_t*>(pk.val)[pos] = static_cast<const uint64_t*>(pk.vals_b)[ent];
-    } else if constexpr (VB == 4) {
-        static_cast<uint32_t*>(pk.val)[pos] = static_cast<const uint32_t*>(pk.vals_b)[ent];
+    } else if constexpr (VB != 0) {
+        static_cast<typename ValT<VB>::T*>(pk.val)[pos] = v;
     }
     if (pk.run && pos > cstart) pk.run[ent] = make_uint2(uint32_t(cstart), uint32_t(pos));
 }
@@ -558,15 +571,41 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
     const uint32_t lmask = (1u << L) - 1u;
     uint32_t distinct = 0;
     if (S <= kLCap) {
-        for (int i = threadIdx.x; i < S; i += kBlock) {
-            dg[0][i] = uint16_t(kx[b0 + i] & lmask);
-            ix[0][i] = uint16_t(i);
+        // every global access of the group is issued as one batch per thread
+        // (kPer records, unrolled), so a workgroup waits on memory a few
+        // times rather than once per record stride
+        {
+            uint32_t kv[kPer];
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const int i = threadIdx.x + k * kBlock;
+                kv[k] = i < S ? kx[b0 + i] : 0u;
+            }
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) {
+                const int i = threadIdx.x + k * kBlock;
+                if (i < S) {
+                    dg[0][i] = uint16_t(kv[k] & lmask);
+                    ix[0][i] = uint16_t(i);
+                }
+            }
         }
         __syncthreads();
         int cur = 0;
         for (int sh = 0; sh < L; sh += kLDig) {
             lds_pass(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], int(S), sh, min(kLDig, L - sh), wcnt, wt);
             cur ^= 1;
+        }
+        // row fields and entry indices in sorted order (in flight during the scan below)
+        uint32_t rv[kPer], ev[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int j = threadIdx.x + k * kBlock;
+            if (j < S) {
+                const int64_t src = b0 + ix[cur][j];
+                rv[k] = rx[src];
+                ev[k] = ex[src];
+            }
         }
         // first position of every entry's column: the positions where the low
         // bits change, then a max-scan (kPer consecutive positions per thread)
@@ -596,9 +635,14 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
             distinct = tot;
         }
         __syncthreads();
-        for (int j = threadIdx.x; j < S; j += kBlock) {
-            const int64_t src = b0 + ix[cur][j];
-            emit_entry<VB, JAC>(pk, b0 + j, rx[src], ex[src], b0 + cs[j]);
+        typename ValT<VB>::T vv[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+            if (threadIdx.x + k * kBlock < S) vv[k] = entry_value<VB>(pk, ev[k]);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int j = threadIdx.x + k * kBlock;
+            if (j < S) emit_entry<VB, JAC>(pk, b0 + j, rv[k], ev[k], b0 + cs[j], vv[k]);
         }
     } else {
         // a large group: passes over global memory, x -> y -> x ..., ending in y
@@ -623,7 +667,9 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
             uint32_t tot;
             (void)block_exclusive_scan(st ? 1u : 0u, wt, &tot);
             distinct += tot;
-            if (j < S) emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart);
+            if (j < S)
+                emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart,
+                                    entry_value<VB>(pk, es[b0 + j]));
             carry = max(carry, all);
         }
     }
@@ -640,7 +686,7 @@ void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* 
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
     scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
-    radix_scatter<VB, FIRST><<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(
+    radix_scatter<VB, FIRST><<<dim3(unsigned((ntiles + kXcds - 1) / kXcds * kXcds)), dim3(kBlock), 0, s>>>(
         ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, trow, rowbits,
         lenbits);
 }
