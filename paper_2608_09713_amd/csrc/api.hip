@@ -245,8 +245,10 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 // Build the column index of B (sorted by column, packed keys, directory).
 // With run (zeroed beforehand; lower mode) every entry's partner run is written.
 // need_dir: build the group directory for partner-run lookups.
+// ccount (zeroed, B.n entries, with no directory only): the entries of every
+// column, written when the local sort builds the index (*counted is then set)
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                     uint2* run = nullptr, bool need_dir = true) {
+                     uint2* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -302,12 +304,14 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
             pk.lenbits = lenbits;
             pk.drop_last = drop_last;
             pk.kept = &ctl->nkept;
+            pk.ccount = ccount;
             HIPCHK(hipMemsetAsync(&ctl->nkept, 0, sizeof(int64_t), s));
         }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
                                          s, runs_given ? &pk : nullptr);
         check_launch();
         ar.release(tmp);
+        if (counted) *counted = which < 0 && ccount;
         if (which >= 0) {
             void* ctmp = ar.get(colindex_tmp_bytes(N));
             build_colindex(which ? kb : ka, which ? rb : ra, which ? eb : ea, N, drop_last, vb, sr, B.v, B.rp, lenbits,
@@ -371,10 +375,16 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         cx = build_index(L, true, sr, ar, ctl, s, run);
     } else {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
-        cx = build_index(R, false, sr, ar, ctl, s, nullptr, false);
+        // column starts of R: from the counts the local sort writes, else by counting
         uint32_t* cptr = ar.get_t<uint32_t>(R.n + 1);
+        HIPCHK(hipMemsetAsync(cptr, 0, size_t(R.n + 1) * sizeof(uint32_t), s));
+        bool counted = false;
+        cx = build_index(R, false, sr, ar, ctl, s, nullptr, false, cptr, &counted);
         void* ctmp = ar.get(scan_tmp_bytes(R.n + 1));
-        column_starts(R.ci, R.nnz, R.n, cptr, ctmp, s);
+        if (counted)
+            scan_u32(cptr, cptr, R.n + 1, nullptr, ctmp, s);
+        else
+            column_starts(R.ci, R.nnz, R.n, cptr, ctmp, s);
         offdiag_runs(L.ci, L.nnz, cptr, run, s);
         check_launch();
         ar.release(ctmp);

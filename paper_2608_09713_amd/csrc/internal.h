@@ -83,6 +83,7 @@ struct LocalPack {
     int rowbits = 1, lenbits = 0;
     bool drop_last = false;
     int64_t* kept = nullptr;
+    uint32_t* ccount = nullptr;  // non-null (zeroed, one per column): entries of every column
 };
 // pk non-null: write the column index as above when the local path is taken
 // and return -1 (no sorted copy); otherwise as described.

@@ -508,10 +508,12 @@ __device__ inline typename ValT<VB>::T entry_value(const LocalPack& pk, uint32_t
         return static_cast<const typename ValT<VB>::T*>(pk.vals_b)[ent];
 }
 
-// v: the entry's value (VB 4 or 8), read by the caller
+// v: the entry's value (VB 4 or 8), read by the caller; last: the entry ends
+// column col
 template <int VB, bool JAC>
 __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t field, uint32_t ent, int64_t cstart,
-                                  typename ValT<VB>::T v) {
+                                  typename ValT<VB>::T v, bool last, uint32_t col) {
+    if (pk.ccount && last) pk.ccount[col] = uint32_t(pos - cstart + 1);
     const uint32_t rowmask = pk.rowbits >= 32 ? 0xffffffffu : ((1u << pk.rowbits) - 1u);
     const uint32_t row = field & rowmask;
     pk.key[pos] = row;
@@ -639,10 +641,15 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
 #pragma unroll
         for (int k = 0; k < kPer; ++k)
             if (threadIdx.x + k * kBlock < S) vv[k] = entry_value<VB>(pk, ev[k]);
+        const uint32_t hi = kx[b0] & ~lmask;  // the group's high column bits
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
             const int j = threadIdx.x + k * kBlock;
-            if (j < S) emit_entry<VB, JAC>(pk, b0 + j, rv[k], ev[k], b0 + cs[j], vv[k]);
+            if (j < S) {
+                const uint32_t lo = dg[cur][j];
+                const bool last = j == S - 1 || dg[cur][j + 1] != lo;
+                emit_entry<VB, JAC>(pk, b0 + j, rv[k], ev[k], b0 + cs[j], vv[k], last, hi | lo);
+            }
         }
     } else {
         // a large group: passes over global memory, x -> y -> x ..., ending in y
@@ -667,9 +674,12 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
             uint32_t tot;
             (void)block_exclusive_scan(st ? 1u : 0u, wt, &tot);
             distinct += tot;
-            if (j < S)
-                emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart,
-                                    entry_value<VB>(pk, es[b0 + j]));
+            if (j < S) {
+                const uint32_t col = ks[b0 + j];
+                const bool last = j == S - 1 || ks[b0 + j + 1] != col;
+                emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart, entry_value<VB>(pk, es[b0 + j]),
+                                    last, col);
+            }
             carry = max(carry, all);
         }
     }
