@@ -54,6 +54,7 @@ __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ 
     __shared__ int64_t bounds[2];
     __shared__ uint32_t bad_s;
     if (threadIdx.x == 0) bad_s = 0;
+    __syncthreads();  // (a workgroup with no entries meets no other barrier before its atomics)
     uint32_t bad = 0;
     // row pointers: rp[0] == 0, non-decreasing, inside [0, nnz], rp[m] == nnz
     for (int64_t i = int64_t(blockIdx.x) * kTileR + threadIdx.x;
