@@ -173,14 +173,23 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         }
         __syncthreads();
     }
-    uint32_t kr[kRItems], rr[kRItems], loc[kRItems];
-    V vr[kRItems];
+    // keys and tile positions stay in registers; the first pass also keeps
+    // its row fields (computed from the LDS window, which the exchange
+    // buffer overwrites), other passes load rows and values only when they
+    // are exchanged (fewer registers, more workgroups per compute unit)
+    uint32_t kr[kRItems], rr[FIRST ? kRItems : 1], loc[kRItems];
     const uint64_t lt = lanemask_lt();
+    // all of the segment's keys in flight at once, then the ranking
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k) {
+        const int64_t idx = segbase + int64_t(k) * kWave + lane;
+        kr[k] = idx < n ? key_in[idx] : 0u;
+    }
 #pragma unroll
     for (int k = 0; k < kRItems; ++k) {
         const int64_t idx = segbase + int64_t(k) * kWave + lane;
         const bool valid = idx < n;
-        const uint32_t key = valid ? key_in[idx] : 0u;
+        const uint32_t key = kr[k];
         const uint32_t d = (key >> shift) & mask;
         uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -194,7 +203,6 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         const uint32_t rank = __popcll(peers & lt);
         loc[k] = cur + rank;
         if (valid && rank == 0) wcnt[w][d] = cur + uint32_t(__popcll(peers));
-        kr[k] = key;
         if constexpr (FIRST) {
             uint32_t field = 0;
             if (valid) {
@@ -214,10 +222,6 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
                 }
             }
             rr[k] = field;
-            vr[k] = V(idx);
-        } else {
-            rr[k] = valid ? row_in[idx] : 0u;
-            if constexpr (VB != 0) vr[k] = valid ? val_in[idx] : V(0);
         }
     }
     __syncthreads();
@@ -255,16 +259,37 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     const int tile_n = int(min(int64_t(kRTile), n - base));
     for (int i = threadIdx.x; i < tile_n; i += kBlock) key_out[gofs[dig[i]] + i] = uint32_t(ex[i]);
     __syncthreads();
+    if constexpr (FIRST) {
 #pragma unroll
-    for (int k = 0; k < kRItems; ++k)
-        if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = V(rr[k]);
+        for (int k = 0; k < kRItems; ++k)
+            if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = V(rr[k]);
+    } else {
+        uint32_t rv[kRItems];
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t idx = segbase + int64_t(k) * kWave + lane;
+            rv[k] = idx < n ? row_in[idx] : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k)
+            if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = V(rv[k]);
+    }
     __syncthreads();
     for (int i = threadIdx.x; i < tile_n; i += kBlock) row_out[gofs[dig[i]] + i] = uint32_t(ex[i]);
     if constexpr (VB != 0) {
+        V vv[kRItems];
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t idx = segbase + int64_t(k) * kWave + lane;
+            if constexpr (FIRST)
+                vv[k] = V(idx);
+            else
+                vv[k] = idx < n ? val_in[idx] : V(0);
+        }
         __syncthreads();
 #pragma unroll
         for (int k = 0; k < kRItems; ++k)
-            if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = vr[k];
+            if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = vv[k];
         __syncthreads();
         for (int i = threadIdx.x; i < tile_n; i += kBlock) val_out[gofs[dig[i]] + i] = ex[i];
     }

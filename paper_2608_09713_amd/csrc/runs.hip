@@ -133,6 +133,14 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
 }
 
 constexpr int kCTile = 4096;  // staging slots per compaction workgroup
+template <int VB>
+struct SlotT {  // a staged value of VB bytes (a placeholder for VB 0)
+    using T = uint32_t;
+};
+template <>
+struct SlotT<8> {
+    using T = uint64_t;
+};
 constexpr int kCWin = 512;    // rows held in LDS by a compaction workgroup
 
 template <int VB>
@@ -202,6 +210,38 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
         }
     }
     __syncthreads();
+    if (win_ok && s1 - s0 == kCTile) {
+        // a whole tile: the slots of a thread in batches of kBatch, every
+        // batch's loads in flight together before its stores
+        using V = typename SlotT<VB>::T;
+        constexpr int kBatch = 8;
+        static_assert(kCTile % (kBlock * kBatch) == 0, "whole batches per tile");
+#pragma unroll
+        for (int b = 0; b < kCTile / (kBlock * kBatch); ++b) {
+            int32_t cv[kBatch];
+            V vv[kBatch];
+            bool live[kBatch];
+#pragma unroll
+            for (int q = 0; q < kBatch; ++q) {
+                const int x = (b * kBatch + q) * kBlock + threadIdx.x;
+                live[q] = s0 + x < wend[rowof[x]];
+                if (live[q]) {
+                    cv[q] = s_ci[s0 + x];
+                    if constexpr (VB != 0) vv[q] = static_cast<const V*>(s_val)[s0 + x];
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < kBatch; ++q) {
+                const int x = (b * kBatch + q) * kBlock + threadIdx.x;
+                if (live[q]) {
+                    const int64_t p = s0 + x + wdel[rowof[x]];
+                    c_ci[p] = cv[q];
+                    if constexpr (VB != 0) static_cast<V*>(c_val)[p] = vv[q];
+                }
+            }
+        }
+        return;
+    }
     for (int64_t sl = s0 + threadIdx.x; sl < s1; sl += kBlock) {
         int64_t end, del;
         if (win_ok) {
