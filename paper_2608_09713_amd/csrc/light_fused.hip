@@ -356,9 +356,10 @@ struct Chunk {
         // the others are listed by size class so that every class runs with
         // full lanes.  Small buckets (up to kSmall products), one per lane:
         // sorted by (column, product index) in registers, equal columns merged
-        // (terms summed in product order), the distinct columns written back
-        // in order at the bucket's start with their term counts in s_rank;
-        // ucnt[b] = distinct columns.  Larger buckets go to the cooperative
+        // (terms summed in product order); every column's first product keeps
+        // its slot and gets the column's tag in s_rank (term count, index among
+        // the bucket's distinct columns), the others are marked as writing
+        // nothing; ucnt[b] = distinct columns.  Larger buckets go to the cooperative
         // pass below.  (The entry arrays are free by now and hold the lists.)
         uint16_t* list2 = reinterpret_cast<uint16_t*>(L.ent_start);       // 2 products
         uint16_t* list4 = reinterpret_cast<uint16_t*>(L.ent_start) + kFE;  // 3 or 4
@@ -476,17 +477,20 @@ struct Chunk {
     }
 
     // Sort the sz (<= N) products at [lo, lo + sz) by (column, product index)
-    // in registers, merge equal columns and write the distinct ones back from
-    // lo on: column, merged term (the sum for plus-times, |S(j)| for Jaccard)
-    // and term count.  Returns the number of distinct columns.
+    // in registers, each key carrying its slot.  The first product of every
+    // column takes the column's tag (term count, index among the bucket's
+    // distinct columns) and, for plus-times with several terms, their sum in
+    // product order; the other products of the column write nothing.  Returns
+    // the number of distinct columns.
     template <int N>
     __device__ uint32_t merge_small(uint32_t lo, uint32_t sz) {
+        static_assert(N <= 16, "slots in four bits");
         uint64_t k[N];
         Item v[N];
 #pragma unroll
         for (int u = 0; u < N; ++u) {
             const bool in = uint32_t(u) < sz;
-            k[u] = in ? ((uint64_t(L.s_j[lo + u]) << 16) | L.s_t[lo + u]) : ~uint64_t(0);
+            k[u] = in ? ((((uint64_t(L.s_j[lo + u]) << 16) | L.s_t[lo + u]) << 4) | uint64_t(u)) : ~uint64_t(0);
             v[u] = in ? L.s_v[lo + u] : Item(0);
         }
         if constexpr (N == 4) {
@@ -502,62 +506,55 @@ struct Chunk {
             cswap(k, v, 3, 4);
         }
         uint32_t d = 0;
-        uint32_t gj = uint32_t(k[0] >> 16);
+        uint32_t gj = uint32_t(k[0] >> 20);
+        uint32_t gs = uint32_t(k[0] & 15u);
         Item acc = v[0];
         uint32_t cnt = 1;
 #pragma unroll
         for (int u = 1; u <= N; ++u) {
             const bool in = uint32_t(u) < sz;
-            const uint32_t j = in ? uint32_t(k[u < N ? u : 0] >> 16) : 0u;
+            const uint64_t ku = k[u < N ? u : 0];
+            const uint32_t j = in ? uint32_t(ku >> 20) : 0u;
             if (in && j == gj) {
                 ++cnt;
                 if constexpr (kVal) acc += v[u < N ? u : 0];
+                L.s_rank[lo + uint32_t(ku & 15u)] = uint16_t(kNoOut);
             } else if (uint32_t(u) <= sz) {
                 // the group of gj ends
-                L.s_j[lo + d] = gj;
-                L.s_v[lo + d] = acc;
-                L.s_rank[lo + d] = uint16_t((cnt << kKBits) | d);
+                L.s_rank[lo + gs] = uint16_t((cnt << kKBits) | d);
+                if constexpr (kVal)
+                    if (cnt > 1) L.s_v[lo + gs] = acc;
                 ++d;
                 if (in) {
                     gj = j;
+                    gs = uint32_t(ku & 15u);
                     acc = v[u < N ? u : 0];
                     cnt = 1;
                 }
             }
         }
-        // the slots past the distinct columns write nothing
-#pragma unroll
-        for (int u = 1; u < N; ++u)
-            if (uint32_t(u) >= d && uint32_t(u) < sz) L.s_rank[lo + u] = uint16_t(kNoOut);
         return d;
     }
 
-    // A bucket of two products at lo: ordered by (column, product index),
-    // merged if the columns are equal.  Returns the distinct columns.
+    // A bucket of two products at lo.  Distinct columns keep their slots and
+    // get their output order in their tags; equal columns merge into the
+    // first slot (terms in product order).  Returns the distinct columns.
     __device__ uint32_t merge_two(uint32_t lo) {
-        uint32_t j0 = L.s_j[lo], j1 = L.s_j[lo + 1];
-        uint32_t t0 = L.s_t[lo], t1 = L.s_t[lo + 1];
-        Item v0 = L.s_v[lo], v1 = L.s_v[lo + 1];
-        if (j0 == j1) {
-            if constexpr (kVal) {
-                // terms in product order
-                L.s_v[lo] = t0 < t1 ? v0 + v1 : v1 + v0;
-            }
-            L.s_rank[lo] = uint16_t(2u << kKBits);
-            L.s_rank[lo + 1] = uint16_t(kNoOut);
-            return 1;
+        const uint32_t j0 = L.s_j[lo], j1 = L.s_j[lo + 1];
+        if (j0 != j1) {
+            const uint32_t f = j1 < j0 ? 1u : 0u;
+            L.s_rank[lo] = uint16_t((1u << kKBits) | f);
+            L.s_rank[lo + 1] = uint16_t((1u << kKBits) | (f ^ 1u));
+            return 2;
         }
-        if (j1 < j0) {
-            L.s_j[lo] = j1;
-            L.s_j[lo + 1] = j0;
-            L.s_t[lo] = uint16_t(t1);
-            L.s_t[lo + 1] = uint16_t(t0);
-            L.s_v[lo] = v1;
-            L.s_v[lo + 1] = v0;
+        if constexpr (kVal) {
+            const uint32_t t0 = L.s_t[lo], t1 = L.s_t[lo + 1];
+            const Item v0 = L.s_v[lo], v1 = L.s_v[lo + 1];
+            L.s_v[lo] = t0 < t1 ? v0 + v1 : v1 + v0;
         }
-        L.s_rank[lo] = uint16_t(1u << kKBits);
-        L.s_rank[lo + 1] = uint16_t((1u << kKBits) | 1u);
-        return 2;
+        L.s_rank[lo] = uint16_t(2u << kKBits);
+        L.s_rank[lo + 1] = uint16_t(kNoOut);
+        return 1;
     }
 
     // value of a merged column: the sum (plus-times), the count, or the
@@ -728,7 +725,9 @@ struct Chunk {
 };
 
 template <int SR, bool LOWER>
-__global__ __launch_bounds__(kWave* kWavesF) void fused_kernel(FusedArgs a) {
+// (plus-times: at most 168 VGPRs, three wavefronts per SIMD)
+__global__ __launch_bounds__(kWave* kWavesF) __attribute__((amdgpu_waves_per_eu(SR == kF64 || SR == kF32 ? 3 : 1)))
+void fused_kernel(FusedArgs a) {
     using Item = typename ItemOf<SR>::T;
     __shared__ WaveLds<Item> lds[kWavesF];
     WaveLds<Item>& L = lds[threadIdx.x / kWave];
