@@ -140,6 +140,29 @@ spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_
                              const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C);
 
 /*
+ * One half of an off-diagonal block, as the two processes of a symmetric pair
+ * split C_ij = C_ji^T between them (Sec. III-A, Algorithm 3): the process
+ * below the diagonal computes the top rows of its block, its partner above
+ * the diagonal the right columns of its own.  Row r of C_ij is column r of
+ * C_ji, so the top half of C_ij and the right half of C_ji are disjoint and
+ * together hold the whole pair.
+ *   SPSYRK_HALF_TOP:   rows [0, floor(m_i / 2)) of A_i A_j^T.
+ *                      C: floor(m_i / 2) x m_j.
+ *   SPSYRK_HALF_RIGHT: columns [floor(m_j / 2), m_j) of A_i A_j^T, every row
+ *                      of A_i.  C: m_i x m_j, column ids in the block's own
+ *                      numbering (all of them >= floor(m_j / 2)).
+ * Values, semirings and ordering as spsyrk_offdiag.  The call reads row_ptr at
+ * the split row on the host (one more synchronisation) and checks the row
+ * range it multiplies.
+ * Errors: as spsyrk_offdiag, plus INVALID_ARG for an unknown half.
+ */
+typedef enum spsyrk_half { SPSYRK_HALF_TOP = 0, SPSYRK_HALF_RIGHT = 1 } spsyrk_half;
+
+spsyrk_status spsyrk_offdiag_half(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_half half,
+                                  spsyrk_semiring sr, const spsyrk_allocator* al, void* hip_stream,
+                                  spsyrk_csr_out* C);
+
+/*
  * C = C_L + C_L^T - D (Eq. (spmv)): the full symmetric matrix from a stored
  * lower part (for example the output of spsyrk_lower).  Row i of the result is
  * row i of C_L followed by the entries (r, i) of the strict lower part with

@@ -158,6 +158,26 @@ def offdiag(Ai, Aj, semiring, rows=None, lib=None) -> Result:
     return _run(1, Ai, Aj, semiring, rows, lib)
 
 
+def offdiag_half(Ai, Aj, half, semiring, lib=None) -> Result:
+    """One half of the block C_ij = A_i A_j^T, as the two processes of a
+    symmetric pair split it (Sec. III-A, Algorithm 3): ``"top"`` is rows
+    [0, m_i // 2) of C_ij; ``"right"`` is columns [m_j // 2, m_j) of every row,
+    with column ids in the block's numbering.  Written as the restriction of
+    the full block to those rows or columns."""
+    if half == "top":
+        return offdiag(Ai, Aj, semiring, rows=np.arange(Ai.nrows // 2), lib=lib)
+    if half != "right":
+        raise ValueError(half)
+    full = offdiag(Ai, Aj, semiring, lib=lib)
+    keep = full.col_idx >= Aj.nrows // 2
+    rows = np.repeat(np.arange(full.nrows), np.diff(full.row_ptr))
+    rp = np.zeros(full.nrows + 1, dtype=np.int64)
+    np.cumsum(np.bincount(rows[keep], minlength=full.nrows), out=rp[1:])
+    return Result(full.nrows, full.ncols, rp, full.col_idx[keep], full.values[keep],
+                  None if full.sum_abs is None else full.sum_abs[keep],
+                  None if full.count is None else full.count[keep])
+
+
 def mirror(m: int, row_ptr, col_idx, values, lib=None) -> Result:
     """Full symmetric CSR from the stored lower part (values copied bit for bit)."""
     lib = lib or _load()

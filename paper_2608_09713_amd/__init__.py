@@ -80,12 +80,15 @@ def library():
                 raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2608_09713_amd.build` "
                                   "(or __graft_entry__.build()) first")
             lib = ctypes.CDLL(LIB_PATH)
-            for name in ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror"):
+            for name in ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror"):
                 getattr(lib, name).restype = ctypes.c_int
             lib.spsyrk_lower.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
                                          ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
             lib.spsyrk_offdiag.argtypes = [ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), ctypes.c_int,
                                            ctypes.POINTER(_Allocator), ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_offdiag_half.argtypes = [ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), ctypes.c_int,
+                                                ctypes.c_int, ctypes.POINTER(_Allocator), ctypes.c_void_p,
+                                                ctypes.POINTER(_CsrOut)]
             lib.spsyrk_mirror.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
                                           ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
             lib.spsyrk_status_string.argtypes = [ctypes.c_int]
@@ -102,7 +105,7 @@ def library():
     return _lib
 
 
-EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_mirror", "spsyrk_status_string",
+EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror", "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
            "spsyrk_timing_end")
 
@@ -238,6 +241,22 @@ def offdiag(Ai: DeviceCSR, Aj: DeviceCSR, semiring="f64") -> DeviceCSR:
     b = _csr_struct(Aj, sr, True)
     return _call("spsyrk_offdiag", lambda ar: (ctypes.byref(a), ctypes.byref(b), sr, ctypes.byref(ar.struct)),
                  sr, Ai.row_ptr.device)
+
+
+HALVES = {"top": 0, "right": 1}
+
+
+def offdiag_half(Ai: DeviceCSR, Aj: DeviceCSR, half: str, semiring="f64") -> DeviceCSR:
+    """One half of C = A_i A_j^T (spsyrk_offdiag_half): ``half="top"`` gives rows
+    [0, m_i // 2); ``half="right"`` gives columns [m_j // 2, m_j) of every row,
+    with column ids in the block's numbering."""
+    sr = _sr(semiring)
+    h = HALVES[half]
+    a = _csr_struct(Ai, sr, True)
+    b = _csr_struct(Aj, sr, True)
+    return _call("spsyrk_offdiag_half",
+                 lambda ar: (ctypes.byref(a), ctypes.byref(b), h, sr, ctypes.byref(ar.struct)), sr,
+                 Ai.row_ptr.device)
 
 
 def mirror(C_lower: DeviceCSR, semiring="f64") -> DeviceCSR:

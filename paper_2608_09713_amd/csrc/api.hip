@@ -828,6 +828,67 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     g_stats_valid = true;
 }
 
+// one device int64 read back to the host (one synchronisation)
+int64_t read_i64(const int64_t* d, hipStream_t s) {
+    struct Pinned {
+        int64_t* h = nullptr;
+        Pinned() {
+            if (hipHostMalloc(reinterpret_cast<void**>(&h), sizeof(int64_t), hipHostMallocDefault) != hipSuccess)
+                h = nullptr;
+        }
+        ~Pinned() {
+            if (h) (void)hipHostFree(h);
+        }
+    };
+    thread_local Pinned pin;
+    if (!pin.h) {
+        set_detail("pinned host buffer unavailable");
+        throw Fail{SPSYRK_ERR_HIP};
+    }
+    HIPCHK(hipMemcpyAsync(pin.h, d, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+    return *pin.h;
+}
+
+// Half of an off-diagonal block (Algorithm 3): the top rows [0, floor(m_i/2))
+// of A_i A_j^T, or its right columns [floor(m_j/2), m_j).  Both are the
+// off-diagonal product of a row range of one operand; the right half's
+// column ids are shifted back to the block's numbering.
+void offdiag_half(const DevCsr& L, const DevCsr& R, int half, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
+    const int vb = (sr == kF64) ? 8 : (sr == kF32 ? 4 : 0);
+    if (half == SPSYRK_HALF_TOP) {
+        DevCsr T = L;
+        T.m = L.m / 2;
+        // (the row pointer prefix is the top rows' own; their nnz is rp[m/2])
+        T.nnz = read_i64(L.rp + T.m, s);
+        if (T.nnz < 0 || T.nnz > L.nnz) {
+            set_detail("Ai is not canonical CSR (row_ptr[%lld] = %lld)", (long long)T.m, (long long)T.nnz);
+            throw Fail{SPSYRK_ERR_NOT_CANONICAL};
+        }
+        syrk(T, R, false, sr, ar, s, C);
+        return;
+    }
+    const int64_t c0 = R.m / 2;
+    const int64_t e0 = read_i64(R.rp + c0, s);
+    if (e0 < 0 || e0 > R.nnz) {
+        set_detail("Aj is not canonical CSR (row_ptr[%lld] = %lld)", (long long)c0, (long long)e0);
+        throw Fail{SPSYRK_ERR_NOT_CANONICAL};
+    }
+    DevCsr B = R;
+    B.m = R.m - c0;
+    B.nnz = R.nnz - e0;
+    int64_t* rp = ar.get_t<int64_t>(B.m + 1);
+    rebase_rows(R.rp, c0, B.m, rp, s);
+    check_launch();
+    B.rp = rp;
+    B.ci = R.ci + e0;
+    B.v = R.v ? static_cast<const char*>(R.v) + e0 * vb : nullptr;
+    syrk(L, B, false, sr, ar, s, C);
+    shift_columns(C->col_idx, C->nnz, int32_t(c0), s);
+    check_launch();
+    C->ncols = R.m;
+}
+
 template <typename F>
 spsyrk_status guarded(spsyrk_csr_out* C, const spsyrk_allocator* al, void* stream, F body) {
     g_stats_valid = false;
@@ -881,6 +942,25 @@ spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_
             throw Fail{SPSYRK_ERR_INVALID_ARG};
         }
         syrk(dev(Ai), dev(Aj), false, int(sr), ar, s, C);
+    });
+}
+
+spsyrk_status spsyrk_offdiag_half(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_half half,
+                                  spsyrk_semiring sr, const spsyrk_allocator* al, void* hip_stream,
+                                  spsyrk_csr_out* C) {
+    return guarded(C, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        check_input(Ai, int(sr), true, "Ai");
+        check_input(Aj, int(sr), true, "Aj");
+        if (Ai->ncols != Aj->ncols) {
+            set_detail("Ai has %lld columns, Aj has %lld", (long long)Ai->ncols, (long long)Aj->ncols);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        if (half != SPSYRK_HALF_TOP && half != SPSYRK_HALF_RIGHT) {
+            set_detail("unknown half %d", int(half));
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        offdiag_half(dev(Ai), dev(Aj), int(half), int(sr), ar, s, C);
     });
 }
 

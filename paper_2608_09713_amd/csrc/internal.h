@@ -171,6 +171,11 @@ void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m,
 // Dense column starts of a CSR matrix's column-sorted copy: cptr[c] =
 // entries in columns before c (n + 1 words; scan_tmp: scan_tmp_bytes(n + 1)).
 void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, void* scan_tmp, hipStream_t s);
+// Row pointers of rows [r0, r0 + m) of a CSR matrix, rebased to start at 0
+// (out: m + 1 words).
+void rebase_rows(const int64_t* rp, int64_t r0, int64_t m, int64_t* out, hipStream_t s);
+// ci[p] += off for p < nnz.
+void shift_columns(int32_t* ci, int64_t nnz, int32_t off, hipStream_t s);
 // Off-diagonal partner runs: run[e] = {cptr[ci[e]], cptr[ci[e] + 1]}.
 void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* run, hipStream_t s);
 // prod[i] = sum over the entries e of row i of run[e].y - run[e].x (prod

@@ -279,7 +279,31 @@ __global__ __launch_bounds__(kBlock) void offdiag_runs_kernel(const int32_t* __r
     run[e] = make_uint2(cptr[c], cptr[c + 1]);
 }
 
+// out[k] = rp[r0 + k] - rp[r0] for k in [0, m]: the row pointers of rows
+// [r0, r0 + m) of a CSR matrix as a matrix of their own
+__global__ __launch_bounds__(kBlock) void rebase_rows_kernel(const int64_t* __restrict__ rp, int64_t r0, int64_t m,
+                                                             int64_t* __restrict__ out) {
+    const int64_t k = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (k <= m) out[k] = rp[r0 + k] - rp[r0];
+}
+
+__global__ __launch_bounds__(kBlock) void shift_columns_kernel(int32_t* __restrict__ ci, int64_t nnz, int32_t off) {
+    for (int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x; p < nnz; p += int64_t(gridDim.x) * kBlock)
+        ci[p] += off;
+}
+
 }  // namespace
+
+void rebase_rows(const int64_t* rp, int64_t r0, int64_t m, int64_t* out, hipStream_t s) {
+    rebase_rows_kernel<<<unsigned((m + 1 + kBlock - 1) / kBlock), kBlock, 0, s>>>(rp, r0, m, out);
+}
+
+void shift_columns(int32_t* ci, int64_t nnz, int32_t off, hipStream_t s) {
+    if (nnz <= 0 || off == 0) return;
+    int64_t blocks = (nnz + kBlock - 1) / kBlock;
+    if (blocks > 65536) blocks = 65536;
+    shift_columns_kernel<<<unsigned(blocks), kBlock, 0, s>>>(ci, nnz, off);
+}
 
 void tile_first_rows(const int64_t* rp, int64_t m, int64_t T, int64_t* trow, hipStream_t s) {
     if (m <= 0) return;

@@ -133,3 +133,30 @@ def test_offdiag_full(dev):
     K = sp.offdiag(upload(Ai, "count", dev), upload(Aj, "count", dev), "count")
     assert int(K.values[: K.nnz].to(torch.int64).sum().item()) == int((ci * cj).sum())
     check_lower(Ai, sr, dev, rows, "offdiag diagonal block")
+
+
+def test_offdiag_halves_full(dev):
+    # Algorithm 3's half blocks at the off-diagonal workload's size: sampled
+    # rows of each half against the oracle's restriction of the block, and
+    # entry counts that add up to the full block's
+    w = W.make("offdiag_f64", 1, 0)
+    Ai, Aj, sr = w["A"], w["B"], w["semiring"]
+    print(f"[full offdiag halves] m_i={Ai.nrows} m_j={Aj.nrows} nnz={Ai.nnz}+{Aj.nnz}", flush=True)
+    top = sp.offdiag_half(upload(Ai, sr, dev), upload(Aj, sr, dev), "top", sr)
+    right = sp.offdiag_half(upload(Ai, sr, dev), upload(Aj, sr, dev), "right", sr)
+    rows = sample_rows(Ai, 300, 17)
+    top_rows = rows[rows < Ai.nrows // 2]
+    compare_rows(top, oracle.offdiag(Ai, Aj, sr, rows=top_rows), top_rows, sr, "top half")
+    ref = oracle.offdiag(Ai, Aj, sr, rows=rows)
+    keep = ref.col_idx >= Aj.nrows // 2
+    rr = np.repeat(np.arange(len(rows)), np.diff(ref.row_ptr))
+    rp = np.zeros(len(rows) + 1, dtype=np.int64)
+    np.cumsum(np.bincount(rr[keep], minlength=len(rows)), out=rp[1:])
+    ref_right = oracle.Result(len(rows), Aj.nrows, rp, ref.col_idx[keep], ref.values[keep],
+                              None if ref.sum_abs is None else ref.sum_abs[keep])
+    compare_rows(right, ref_right, rows, sr, "right half")
+    # the top half plus the bottom rows' right columns plus their left columns
+    # make the block; here: the halves' nnz against the full block's rows
+    full = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
+    frp = full.row_ptr.cpu().numpy()
+    assert top.nnz == frp[Ai.nrows // 2]

@@ -247,6 +247,60 @@ def test_offdiag_random(dev, semiring):
 
 
 @pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_offdiag_half(dev, semiring):
+    # Algorithm 3's half blocks: odd and even row counts, a single row (empty
+    # top half), an empty operand, and enough rows for several tiles
+    rng = np.random.default_rng(43)
+    vdt = VDT[semiring]
+    for t, (mi, mj, n) in enumerate([(37, 23, 60), (1, 5, 10), (2, 1, 10), (0, 4, 7), (3001, 2999, 4000)]):
+        Ai = random_csr(rng, mi, n, 0.01 if mi > 100 else 0.1, signed=True)
+        Aj = random_csr(rng, mj, n, 0.01 if mj > 100 else 0.1, signed=True)
+        if vdt is not None:
+            Ai, Aj = Ai.with_values(Ai.values.astype(vdt)), Aj.with_values(Aj.values.astype(vdt))
+        else:
+            Ai, Aj = Ai.with_values(None), Aj.with_values(None)
+        for half in ("top", "right"):
+            print(f"[offdiag_half {semiring}] case {t} {half} mi={mi} mj={mj}", flush=True)
+            O = sp.offdiag_half(upload(Ai, semiring, dev), upload(Aj, semiring, dev), half, semiring)
+            assert (O.nrows, O.ncols) == ((mi // 2 if half == "top" else mi), mj)
+            compare_full(O, oracle.offdiag_half(Ai, Aj, half, semiring), semiring, f"half {half} case {t}")
+
+
+def test_offdiag_halves_cover_on_device(dev, monkeypatch):
+    # the top half of C_ij and the transposed right half of C_ji rebuild the
+    # device's own full block bit for bit; the second case takes the column
+    # sort's local path (2^20 columns), where the right operand's arrays start
+    # at an entry offset
+    import torch
+    import scipy.sparse as ssp
+    rng = np.random.default_rng(44)
+    for case, (mi, mj, n, local) in enumerate([(301, 199, 500, False), (3001, 2001, 1 << 20, True)]):
+        if local:
+            monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
+        if local:
+            Ai, Aj = _rows_csr(rng, mi, n, 5), _rows_csr(rng, mj, n, 5)
+        else:
+            Ai, Aj = random_csr(rng, mi, n, 0.02), random_csr(rng, mj, n, 0.02)
+        full = sp.offdiag(upload(Ai, "f64", dev), upload(Aj, "f64", dev), "f64")
+        top = sp.offdiag_half(upload(Ai, "f64", dev), upload(Aj, "f64", dev), "top", "f64")
+        right = sp.offdiag_half(upload(Aj, "f64", dev), upload(Ai, "f64", dev), "right", "f64")
+        frp, fci, fv = full.to_host()
+        trp, tci, tv = top.to_host()
+        rrp, rci, rv = right.to_host()
+        cut = frp[mi // 2]
+        np.testing.assert_array_equal(trp, frp[:mi // 2 + 1])
+        np.testing.assert_array_equal(tci, fci[:cut])
+        np.testing.assert_array_equal(tv.view(np.uint64), fv[:cut].view(np.uint64))
+        R = ssp.csr_matrix((rv, rci, rrp), shape=(mj, mi)).T.tocsr()
+        R.sort_indices()
+        assert R.indptr[mi // 2] == 0
+        np.testing.assert_array_equal(R.indptr[mi // 2:], frp[mi // 2:] - cut)
+        np.testing.assert_array_equal(R.indices, fci[cut:])
+        # (the same products, summed over k in the same order on both sides)
+        np.testing.assert_allclose(R.data, fv[cut:], rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
 def test_mirror_matches_oracle(dev, semiring):
     rng = np.random.default_rng(77)
     A = random_csr(rng, 400, 600, 0.02, signed=False)

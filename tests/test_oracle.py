@@ -303,6 +303,61 @@ def test_offdiag_transpose_identity():
     np.testing.assert_allclose(Xs.data, Yt.data, rtol=1e-12)
 
 
+def _transpose_result(R, ncols):
+    S = sp.csr_matrix((R.values, R.col_idx, R.row_ptr), shape=(R.nrows, ncols)).T.tocsr()
+    S.sort_indices()
+    return S
+
+
+def test_offdiag_halves_cover_the_pair():
+    # Sec. III-A / Algorithm 3: the lower process of a pair computes the top
+    # rows of C_ij, its partner the right columns of C_ji; row r of C_ij is
+    # column r of C_ji, so the two halves are disjoint and hold all of C_ij
+    rng = np.random.default_rng(12)
+    for mi, mj in ((37, 23), (1, 5), (2, 1), (40, 40), (0, 3)):
+        Ai = random_csr(rng, mi, 30, 0.12)
+        Aj = random_csr(rng, mj, 30, 0.12)
+        full = oracle.offdiag(Ai, Aj, "f64")
+        top = oracle.offdiag_half(Ai, Aj, "top", "f64")
+        right = oracle.offdiag_half(Aj, Ai, "right", "f64")  # part of C_ji, m_j x m_i
+        assert top.nrows == mi // 2 and right.nrows == mj
+        assert np.all(right.col_idx >= mi // 2)
+        # the top rows are the full block's first rows, unchanged
+        cut = full.row_ptr[mi // 2]
+        np.testing.assert_array_equal(top.row_ptr, full.row_ptr[:mi // 2 + 1])
+        np.testing.assert_array_equal(top.col_idx, full.col_idx[:cut])
+        np.testing.assert_array_equal(top.values, full.values[:cut])
+        # the right half of C_ji, transposed, is the rest of C_ij (same products
+        # in the same order of k, so bit for bit)
+        rt = _transpose_result(right, mi)   # m_i x m_j, rows < m_i // 2 empty
+        assert rt.indptr[mi // 2] == 0
+        np.testing.assert_array_equal(rt.indptr[mi // 2:] , full.row_ptr[mi // 2:] - cut)
+        np.testing.assert_array_equal(rt.indices, full.col_idx[cut:])
+        np.testing.assert_array_equal(rt.data, full.values[cut:])
+
+
+def test_offdiag_half_brute_force():
+    rng = np.random.default_rng(13)
+    for t in range(20):
+        mi, mj, n = int(rng.integers(0, 20)), int(rng.integers(0, 20)), int(rng.integers(1, 30))
+        Ai = random_csr(rng, mi, n, 0.2)
+        Aj = random_csr(rng, mj, n, 0.2)
+        Di, Pi = dense_of(Ai)
+        Dj, Pj = dense_of(Aj)
+        P = (Pi.astype(int) @ Pj.T.astype(int)) > 0
+        D = Di @ Dj.T
+        top = oracle.offdiag_half(Ai, Aj, "top", "f64")
+        TD, TP = result_to_dense(top, mj)
+        np.testing.assert_array_equal(TP, P[:mi // 2])
+        np.testing.assert_allclose(TD, D[:mi // 2], rtol=1e-12, atol=1e-12)
+        right = oracle.offdiag_half(Ai, Aj, "right", "f64")
+        RD, RP = result_to_dense(right, mj)
+        want = P.copy()
+        want[:, :mj // 2] = False
+        np.testing.assert_array_equal(RP, want)
+        np.testing.assert_allclose(RD, np.where(want, D, 0.0), rtol=1e-12, atol=1e-12)
+
+
 def test_concatenation_sums_stages():
     # C_ii = sum_s SYRK(A_is) (Sec. III-A): lower([A1 A2]) = lower(A1) + lower(A2)
     rng = np.random.default_rng(8)
