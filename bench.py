@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     p.add_argument("--json-out", default="")
+    p.add_argument("--no-side", action="store_true",
+                   help="skip the side measurements (copy bandwidth, lower vs offdiag(A, A), half blocks)")
     return p.parse_args()
 
 
@@ -150,6 +152,49 @@ def cpu_baseline(A, sr, rows_n, seed):
         "sample": f"{len(rows)} of {A.nrows} rows (seeded), full column-major copy of A built inside the "
                   f"timed call; single thread; host {cpu_model()} with {os.cpu_count()} logical CPUs",
     }
+
+
+def timed_call(torch, fn, reps=3):
+    """Median wall time (ms) of a whole library call, device work included."""
+    out = fn()
+    del out
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        out = fn()
+        torch.cuda.synchronize()
+        ts.append((time.perf_counter() - t0) * 1e3)
+        del out
+    return float(np.median(ts))
+
+
+def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
+    """Figures reported beside the metric (outside the timed steps): a plain
+    device copy's bandwidth and the whole call against it; t(lower(A)) over
+    t(offdiag(A, A)) (ideal about 0.5: half the products and about half the
+    output); for a workload with a right operand, the two half blocks of
+    Algorithm 3 against the full off-diagonal block."""
+    side = {}
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    ms = timed_call(torch, lambda: dst.copy_(src), reps=5)
+    del src, dst
+    copy_GBs = 2 * (1 << 30) / (ms / 1e3) / 1e9
+    side["copy_GBs"] = copy_GBs
+    side["whole_call_vs_copy"] = whole_call_GBs / copy_GBs
+    t_low = timed_call(torch, lambda: sp.lower(Ad, sr))
+    t_full = timed_call(torch, lambda: sp.offdiag(Ad, Ad, sr))
+    side["lower_ms"] = t_low
+    side["offdiag_AA_ms"] = t_full
+    side["lower_over_offdiag_AA"] = t_low / t_full
+    if Bd is not None:
+        side["offdiag_ms"] = timed_call(torch, lambda: sp.offdiag(Ad, Bd, sr))
+        side["half_top_ms"] = timed_call(torch, lambda: sp.offdiag_half(Ad, Bd, "top", sr))
+        side["half_right_ms"] = timed_call(torch, lambda: sp.offdiag_half(Ad, Bd, "right", sr))
+    print(f"[bench] side: {side}", file=sys.stderr, flush=True)
+    return side
 
 
 def main():
@@ -266,6 +311,9 @@ def main():
         line["config"]["nnz_offdiag"] = O.nnz
     del C, M, O, last
     torch.cuda.empty_cache()
+    if not args.no_side:
+        line["side"] = side_measurements(sp, torch, dev, Ad, Bd, sr, w, B_alg / t_step / 1e9)
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         rows_n = args.cpu_rows or max(1, A.nrows // 8)
         print(f"[bench] oracle on {rows_n} rows ...", file=sys.stderr, flush=True)

@@ -412,6 +412,12 @@ struct Chunk {
         for (int g = 0; g < nbig; ++g) {
             const uint32_t b = L.big[g];
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
+            if (hi - lo <= uint32_t(kWave)) {
+                const uint32_t u = merge_wave(lo, hi - lo);
+                if (lane == 0) L.ucnt[b] = u;
+                wave_sync();
+                continue;
+            }
             for (uint32_t q = lo + lane; q < hi; q += kWave) {
                 const uint32_t j = L.s_j[q];
                 const uint32_t t = L.s_t[q] & kTMask;
@@ -474,6 +480,70 @@ struct Chunk {
         if (lane < nrb) L.rbase[ra + lane] = L.rcnt[ra + lane] - int64_t(L.ucnt[L.rbb[ra + lane]]);
         wave_sync();
         return P;
+    }
+
+    // A bucket of up to a wavefront of products at lo, one per lane: a bitonic
+    // sort across the lanes by (column, product index, slot), then the first
+    // product of every column takes the column's value (terms summed in
+    // product order, then finished) and its index among the bucket's distinct
+    // columns; the others write nothing.  Returns the distinct columns (the
+    // same on every lane).
+    __device__ uint32_t merge_wave(uint32_t lo, uint32_t sz) {
+        const bool in = uint32_t(lane) < sz;
+        uint64_t key = ~uint64_t(0);
+        Item v = Item(0);
+        if (in) {
+            const uint32_t q = lo + uint32_t(lane);
+            key = (uint64_t(L.s_j[q]) << 32) | (uint64_t(L.s_t[q] & kTMask) << 6) | uint64_t(lane);
+            v = L.s_v[q];
+        }
+#pragma unroll
+        for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+            for (int d = k >> 1; d > 0; d >>= 1) {
+                const uint64_t pk = (uint64_t(uint32_t(__shfl_xor(uint32_t(key >> 32), d, kWave))) << 32) |
+                                    uint64_t(uint32_t(__shfl_xor(uint32_t(key), d, kWave)));
+                const Item pv = __shfl_xor(v, d, kWave);
+                // keep the smaller key where this lane is the low end of an
+                // ascending pair or the high end of a descending one
+                const bool keep_min = ((lane & k) == 0) == ((lane & d) == 0);
+                if (keep_min ? pk < key : pk > key) {
+                    key = pk;
+                    v = pv;
+                }
+            }
+        }
+        const bool valid = uint32_t(lane) < sz;
+        const uint32_t j = uint32_t(key >> 32);
+        const uint32_t jp = __shfl_up(j, 1, kWave);
+        const bool head = valid && (lane == 0 || jp != j);
+        const uint64_t hm = __ballot(head);
+        const uint32_t rank = uint32_t(__popcll(hm & lanemask_lt()));
+        // the column's terms are this lane's and the next ones up to the next head
+        const uint64_t above = lane + 1 < kWave ? hm >> (lane + 1) : 0;
+        const uint32_t cnt = above ? uint32_t(__ffsll((long long)above)) : sz - uint32_t(lane);
+        Item acc = v;
+        if constexpr (kVal) {
+            uint32_t cmax = head ? cnt : 1u;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) cmax = max(cmax, uint32_t(__shfl_xor(cmax, d, kWave)));
+            for (uint32_t c = 1; c < cmax; ++c) {
+                const Item w = __shfl_down(v, c, kWave);
+                if (head && c < cnt) acc += w;
+            }
+        }
+        if (valid) {
+            const uint32_t q = lo + uint32_t(key & 63u);
+            if (head) {
+                const int r = int(L.s_t[q] >> kTBits);
+                L.s_v[q] = finish(acc, int32_t(cnt), L.rp[r + 1] - L.rp[r]);
+                L.s_rank[q] = uint16_t(rank);
+            } else {
+                L.s_rank[q] = uint16_t(kNoOut);
+            }
+        }
+        wave_sync();
+        return uint32_t(__popcll(hm));
     }
 
     // Sort the sz (<= N) products at [lo, lo + sz) by (column, product index)

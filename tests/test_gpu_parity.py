@@ -266,6 +266,26 @@ def test_offdiag_half(dev, semiring):
             compare_full(O, oracle.offdiag_half(Ai, Aj, half, semiring), semiring, f"half {half} case {t}")
 
 
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_offdiag_self_product(dev, semiring):
+    # offdiag(A, A): every row meets itself in each of its columns, so the
+    # diagonal entry merges as many terms as the row has entries (buckets of
+    # 1 to 90 products: the small, one-per-lane and whole-bucket merges)
+    rng = np.random.default_rng(45)
+    vdt = VDT[semiring]
+    m, n = 600, 20000  # (few entries per column: the rows stay light)
+    lens = rng.integers(0, 91, size=m)
+    rows = [np.sort(rng.choice(n, size=int(k), replace=False)) for k in lens]
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(lens)
+    ci = np.concatenate(rows).astype(np.int32)
+    A = CSR(m, n, rp, ci, rng.standard_normal(len(ci)))
+    Ah = A.with_values(A.values.astype(vdt) if vdt is not None else None)
+    print(f"[offdiag self {semiring}] m={m} nnz={A.nnz}", flush=True)
+    O = sp.offdiag(upload(A, semiring, dev), upload(A, semiring, dev), semiring)
+    compare_full(O, oracle.offdiag(Ah, Ah, semiring), semiring, "offdiag(A, A)")
+
+
 def test_offdiag_halves_cover_on_device(dev, monkeypatch):
     # the top half of C_ij and the transposed right half of C_ji rebuild the
     # device's own full block bit for bit; the second case takes the column
