@@ -175,6 +175,29 @@ spsyrk_status spsyrk_offdiag_half(const spsyrk_csr* Ai, const spsyrk_csr* Aj, sp
 spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const spsyrk_allocator* al,
                             void* hip_stream, spsyrk_csr_out* C_full);
 
+/*
+ * Y = C X for the symmetric C = C_L + C_L^T - D, reading only the stored
+ * lower part (Eq. (spmv) for one column, Eq. (spgemm) for several): C_L X
+ * plus (X^T C_L)^T minus D X, with no transpose of C_L formed.
+ * C_lower: m x m canonical CSR with no entry above the diagonal (for example
+ * the output of spsyrk_lower), values of the semiring's OUTPUT type (double,
+ * float, int32 or float; NULL only when nnz is 0).
+ * X: device array, m x k row-major with leading dimension ldx >= k;
+ * Y: device array, m x k row-major with leading dimension ldy >= k, written
+ * (every element of the m x k part; the rest of each row is left alone).
+ * X and Y hold double for PLUS_TIMES_F64 and COUNT_I32, float for
+ * PLUS_TIMES_F32 and COUNT_I32_JACCARD_F32.  Products and sums are formed in
+ * double and Y is rounded once; the sums are accumulated with atomic adds, so
+ * their order (and the last bits of Y) may differ from run to run.
+ * Workspace: m k doubles and a small tile table from the allocator, released
+ * before return.  The call returns after Y is complete.
+ * Errors: INVALID_ARG (non-square C_lower, k < 0, ldx or ldy < k, null
+ * arrays), NOT_CANONICAL (including an entry above the diagonal), SHAPE, OOM,
+ * HIP.
+ */
+spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t k, const void* X, int64_t ldx,
+                          void* Y, int64_t ldy, const spsyrk_allocator* al, void* hip_stream);
+
 /* Static description of a status code. */
 const char* spsyrk_status_string(spsyrk_status s);
 

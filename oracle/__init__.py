@@ -204,6 +204,26 @@ def mirror(m: int, row_ptr, col_idx, values, lib=None) -> Result:
     return Result(m, m, out_rp, out_ci, out_v)
 
 
+def symm(m: int, row_ptr, col_idx, values, X):
+    """Y = C X for the symmetric C = C_L + C_L^T - D, from the stored lower
+    part C_L (row_ptr, col_idx, values) as Eq. (spmv) writes it: the product
+    with C_L, plus every strict-lower C_L(i, j) X(i, :) added to row j.  fp64.
+    Returns (Y, S) with S = |C| |X| elementwise (the tolerance scale)."""
+    rp = np.asarray(row_ptr, dtype=np.int64)
+    ci = np.asarray(col_idx, dtype=np.int64)[: rp[-1]]
+    c = np.asarray(values)[: rp[-1]].astype(np.float64)
+    X = np.asarray(X, dtype=np.float64).reshape(m, -1)
+    rows = np.repeat(np.arange(m), np.diff(rp))
+    Y = np.zeros_like(X)
+    S = np.zeros_like(X)
+    np.add.at(Y, rows, c[:, None] * X[ci])
+    np.add.at(S, rows, np.abs(c[:, None] * X[ci]))
+    off = ci != rows
+    np.add.at(Y, ci[off], c[off, None] * X[rows[off]])
+    np.add.at(S, ci[off], np.abs(c[off, None] * X[rows[off]]))
+    return Y, S
+
+
 def is_canonical(A) -> bool:
     lib = _load()
     rp = np.ascontiguousarray(A.row_ptr, dtype=np.int64)

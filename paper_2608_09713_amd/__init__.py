@@ -91,6 +91,10 @@ def library():
                                                 ctypes.POINTER(_CsrOut)]
             lib.spsyrk_mirror.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
                                           ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_symm.restype = ctypes.c_int
+            lib.spsyrk_symm.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
+                                        ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(_Allocator),
+                                        ctypes.c_void_p]
             lib.spsyrk_status_string.argtypes = [ctypes.c_int]
             lib.spsyrk_status_string.restype = ctypes.c_char_p
             lib.spsyrk_last_error_detail.argtypes = []
@@ -105,7 +109,8 @@ def library():
     return _lib
 
 
-EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror", "spsyrk_status_string",
+EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror", "spsyrk_symm",
+           "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
            "spsyrk_timing_end")
 
@@ -257,6 +262,35 @@ def offdiag_half(Ai: DeviceCSR, Aj: DeviceCSR, half: str, semiring="f64") -> Dev
     return _call("spsyrk_offdiag_half",
                  lambda ar: (ctypes.byref(a), ctypes.byref(b), h, sr, ctypes.byref(ar.struct)), sr,
                  Ai.row_ptr.device)
+
+
+def symm(C_lower: DeviceCSR, X, semiring="f64"):
+    """Y = C X with C = C_L + C_L^T - D from the stored lower part only
+    (spsyrk_symm).  X: a device tensor of m or m x k (row-major rows may be
+    padded: its stride is passed as the leading dimension), float64 for the
+    f64 and count semirings, float32 for f32 and jaccard.  Returns Y shaped
+    like X (contiguous)."""
+    import torch
+    sr = _sr(semiring)
+    want = torch.float64 if sr in (0, 2) else torch.float32
+    if X.dtype != want:
+        raise TypeError(f"X must be {want} for semiring {semiring}")
+    X2 = X.unsqueeze(1) if X.dim() == 1 else X
+    if X2.dim() != 2 or X2.shape[0] != C_lower.nrows or X2.stride(1) != 1:
+        raise ValueError("X must be m or m x k with unit column stride")
+    m, k = X2.shape
+    Y2 = torch.empty((m, k), dtype=want, device=X.device)
+    lib = library()
+    arena = _TorchArena(X.device)
+    a = _csr_struct(C_lower, sr, False)
+    stream = torch.cuda.current_stream(X.device).cuda_stream
+    rc = lib.spsyrk_symm(ctypes.byref(a), sr, k, ctypes.c_void_p(X2.data_ptr()), X2.stride(0),
+                         ctypes.c_void_p(Y2.data_ptr()), k, ctypes.byref(arena.struct), ctypes.c_void_p(stream))
+    if rc != 0:
+        raise SpsyrkError(rc, lib.spsyrk_last_error_detail().decode())
+    if arena.live:
+        raise RuntimeError("library left allocations unreleased")
+    return Y2.squeeze(1) if X.dim() == 1 else Y2
 
 
 def mirror(C_lower: DeviceCSR, semiring="f64") -> DeviceCSR:

@@ -964,6 +964,41 @@ spsyrk_status spsyrk_offdiag_half(const spsyrk_csr* Ai, const spsyrk_csr* Aj, sp
     });
 }
 
+spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t k, const void* X, int64_t ldx,
+                          void* Y, int64_t ldy, const spsyrk_allocator* al, void* hip_stream) {
+    spsyrk_csr_out unused;
+    return guarded(&unused, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        check_input(C_lower, int(sr), false, "C_lower", int64_t(1) << 62);
+        if (C_lower->nrows != C_lower->ncols) {
+            set_detail("C_lower must be square (%lld x %lld)", (long long)C_lower->nrows,
+                       (long long)C_lower->ncols);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        if (k < 0 || ldx < k || ldy < k) {
+            set_detail("need 0 <= k <= ldx, ldy (k %lld, ldx %lld, ldy %lld)", (long long)k, (long long)ldx,
+                       (long long)ldy);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        const int64_t m = C_lower->nrows;
+        if (m == 0 || k == 0) return;
+        if (!X || !Y || (C_lower->nnz > 0 && !C_lower->values)) {
+            set_detail("X, Y and the values of C_lower are required");
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        const DevCsr c = dev(C_lower);
+        {
+            Ctl* ctl = ar.get_t<Ctl>(1);
+            zero_ctl(ctl, s);
+            validate(c, true, ar, ctl, s, "C_lower");
+        }
+        void* tmp = ar.get(symm_tmp_bytes(m, k, c.nnz));
+        symm_product(c, int(sr), X, ldx, k, Y, ldy, tmp, s);
+        check_launch();
+        HIPCHK(hipStreamSynchronize(s));
+    });
+}
+
 spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const spsyrk_allocator* al,
                             void* hip_stream, spsyrk_csr_out* C_full) {
     return guarded(C_full, al, hip_stream, [&](Arena& ar, hipStream_t s) {

@@ -225,6 +225,15 @@ struct HeavyArgs {
 void heavy_symbolic(const HeavyArgs& a, int* queue, hipStream_t s);
 void heavy_numeric(const HeavyArgs& a, int* queue, hipStream_t s);
 
+// ---- symm.hip
+// Y = C X with C = C_L + C_L^T - D from the stored lower part C (canonical,
+// nothing above the diagonal, values of the semiring's output type).  X and
+// Y: m x k row-major (ldx, ldy), double for F64 and COUNT, float otherwise.
+// tmp: symm_tmp_bytes(m, k, nnz).
+size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz);
+void symm_product(const DevCsr& C, int sr, const void* x, int64_t ldx, int64_t k, void* y, int64_t ldy, void* tmp,
+                  hipStream_t s);
+
 // ---- mirror.hip
 struct MirrorArgs {
     int64_t m = 0;

@@ -160,3 +160,28 @@ def test_offdiag_halves_full(dev):
     full = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
     frp = full.row_ptr.cpu().numpy()
     assert top.nnz == frp[Ai.nrows // 2]
+
+
+@pytest.mark.parametrize("name", ["jaccard_large", "kmer_i32"])
+def test_symm_full(dev, name):
+    # Y = C x from the device's C_L at full size; sampled rows of Y against the
+    # oracle's rows of the full product A A^T (the mirrored rows) times x
+    import torch
+    w = W.make(name, 1, 0)
+    A, sr = w["A"], w["semiring"]
+    print(f"[full symm {name}] m={A.nrows} nnz={A.nnz}", flush=True)
+    C = sp.lower(upload(A, sr, dev), sr)
+    xdt = np.float64 if sr in ("f64", "count") else np.float32
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(A.nrows).astype(xdt)
+    y = sp.symm(C, torch.from_numpy(x).to(dev), sr).cpu().numpy().astype(np.float64)
+    rows = sample_rows(A, 200, 23)
+    Ain = A.with_values(A.values.astype(VDT[sr]) if VDT[sr] else None)
+    R = oracle.offdiag(Ain, Ain, sr, rows=rows)
+    rr = np.repeat(np.arange(len(rows)), np.diff(R.row_ptr))
+    terms = R.values.astype(np.float64) * x.astype(np.float64)[R.col_idx]
+    ref = np.bincount(rr, weights=terms, minlength=len(rows))
+    scale = np.bincount(rr, weights=np.abs(terms), minlength=len(rows))
+    tol = 1e-12 if sr in ("f64", "count") else 2.0 ** -24
+    err = np.abs(y[rows] - ref)
+    assert np.all(err <= tol * np.maximum(scale, np.abs(ref)) + 1e-300), float(err.max())

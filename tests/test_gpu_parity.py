@@ -320,6 +320,61 @@ def test_offdiag_halves_cover_on_device(dev, monkeypatch):
         np.testing.assert_allclose(R.data, fv[cut:], rtol=1e-12, atol=0)
 
 
+SYMM_TOL = {"f64": 1e-12, "count": 1e-12, "jaccard": 2.0 ** -24, "f32": 1e-5 + 2.0 ** -24}
+
+
+def _symm_ref(L, X):
+    """The oracle's Y and its tolerance scale: sum over the terms of
+    |C_L entry scale| |x|, where an entry's scale is the sum of |products|
+    behind it (C_L on the device agrees with the oracle's to the lower
+    product's bar: bit for bit for counts and Jaccard, 1e-12 / 1e-5 of that
+    sum for f64 / f32), and Y is rounded once from double."""
+    m = L.nrows
+    ref, _ = oracle.symm(m, L.row_ptr, L.col_idx, L.values, X)
+    ent = L.sum_abs if L.sum_abs is not None else np.abs(L.values.astype(np.float64))
+    scale, _ = oracle.symm(m, L.row_ptr, L.col_idx, ent, np.abs(X))
+    return ref, np.maximum(scale, np.abs(ref))
+
+
+def _check_symm(Y, ref, scale, semiring, what):
+    err = np.abs(Y.astype(np.float64) - ref)
+    bad = err > SYMM_TOL[semiring] * scale + 1e-300
+    assert not bad.any(), f"{what}: {int(bad.sum())} elements out of tolerance, max err {float(err.max())!r}"
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_symm_matches_oracle(dev, semiring):
+    # Y = C X from C_L only (Eq. (spmv), (spgemm)): 1, 3, 8 and 11 columns (the
+    # column blocks of 8, 2 and 1), a padded leading dimension, empty rows
+    import torch
+    rng = np.random.default_rng(46)
+    vdt = VDT[semiring]
+    xdt = np.float64 if semiring in ("f64", "count") else np.float32
+    A = random_csr(rng, 700, 900, 0.01, signed=True)
+    Ah = A.with_values(A.values.astype(vdt) if vdt is not None else None)
+    C = sp.lower(upload(A, semiring, dev), semiring)
+    L = oracle.lower(Ah, semiring)
+    for k in (1, 3, 8, 11):
+        print(f"[symm {semiring}] k={k}", flush=True)
+        X = rng.standard_normal((A.nrows, k + 2)).astype(xdt)
+        Xd = torch.from_numpy(X).to(dev)[:, :k]  # row stride k + 2
+        Y = sp.symm(C, Xd, semiring).cpu().numpy()
+        ref, scale = _symm_ref(L, X[:, :k].astype(np.float64))
+        _check_symm(Y, ref, scale, semiring, f"symm k={k}")
+    # a vector
+    x = rng.standard_normal(A.nrows).astype(xdt)
+    y = sp.symm(C, torch.from_numpy(x).to(dev), semiring).cpu().numpy()
+    ref, scale = _symm_ref(L, x.astype(np.float64)[:, None])
+    _check_symm(y[:, None], ref, scale, semiring, "symm vector")
+
+
+def test_symm_rejects_upper_entries(dev):
+    import torch
+    P = csr_from_dense(np.array([[1.0, 2.0], [0.0, 3.0]]))
+    with pytest.raises(sp.SpsyrkError):
+        sp.symm(sp.DeviceCSR.from_host(P, dev), torch.ones(2, dtype=torch.float64, device=dev), "f64")
+
+
 @pytest.mark.parametrize("semiring", SEMIRINGS)
 def test_mirror_matches_oracle(dev, semiring):
     rng = np.random.default_rng(77)

@@ -358,6 +358,40 @@ def test_offdiag_half_brute_force():
         np.testing.assert_allclose(RD, np.where(want, D, 0.0), rtol=1e-12, atol=1e-12)
 
 
+def test_symm_is_A_times_AT_x():
+    # Eq. (spmv) on C_L = tril(A A^T): C X = A (A^T X), the route that never
+    # forms C (Sec. V-F), a different summation entirely
+    rng = np.random.default_rng(21)
+    for m, n, k in ((40, 30, 1), (25, 60, 3), (1, 5, 2), (30, 1, 4)):
+        A = random_csr(rng, m, n, 0.15)
+        D, _ = dense_of(A)
+        X = rng.standard_normal((m, k))
+        L = oracle.lower(A, "f64")
+        Y, S = oracle.symm(m, L.row_ptr, L.col_idx, L.values, X)
+        want = D @ (D.T @ X)
+        np.testing.assert_allclose(Y, want, rtol=0, atol=1e-12 * max(1.0, float(np.abs(D).sum() ** 2)))
+        assert np.all(S >= np.abs(Y) - 1e-12)
+
+
+def test_symm_matches_mirrored_matrix():
+    # against the materialised full matrix (the mirror) times X, and unit
+    # vectors pick out columns of C
+    rng = np.random.default_rng(22)
+    m = 35
+    A = random_csr(rng, m, 50, 0.1)
+    L = oracle.lower(A, "f64")
+    M = oracle.mirror(m, L.row_ptr, L.col_idx, L.values)
+    C = sp.csr_matrix((M.values, M.col_idx, M.row_ptr), shape=(m, m)).toarray()
+    X = rng.standard_normal((m, 5))
+    Y, _ = oracle.symm(m, L.row_ptr, L.col_idx, L.values, X)
+    np.testing.assert_allclose(Y, C @ X, rtol=1e-12, atol=1e-12)
+    E, _ = oracle.symm(m, L.row_ptr, L.col_idx, L.values, np.eye(m))
+    np.testing.assert_array_equal(E, C)
+    # an empty lower part gives zeros
+    Z, _ = oracle.symm(3, np.zeros(4, np.int64), np.zeros(0, np.int32), np.zeros(0), np.ones((3, 2)))
+    np.testing.assert_array_equal(Z, 0.0)
+
+
 def test_concatenation_sums_stages():
     # C_ii = sum_s SYRK(A_is) (Sec. III-A): lower([A1 A2]) = lower(A1) + lower(A2)
     rng = np.random.default_rng(8)
