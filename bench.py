@@ -173,7 +173,8 @@ def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
     """Figures reported beside the metric (outside the timed steps): a plain
     device copy's bandwidth and the whole call against it; t(lower(A)) over
     t(offdiag(A, A)) (ideal about 0.5: half the products and about half the
-    output); for a workload with a right operand, the two half blocks of
+    output); Y = C X for 1 and 8 columns from C_L alone (Eq. (spmv)), with its
+    HBM figure; for a workload with a right operand, the two half blocks of
     Algorithm 3 against the full off-diagonal block."""
     side = {}
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -189,6 +190,21 @@ def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
     side["lower_ms"] = t_low
     side["offdiag_AA_ms"] = t_full
     side["lower_over_offdiag_AA"] = t_low / t_full
+    # Y = C X from C_L alone (Eq. (spmv) / (spgemm)): algorithmic bytes are
+    # C_L read once, X read once and Y written once
+    C = sp.lower(Ad, sr)
+    xdt = torch.float64 if sr in ("f64", "count") else torch.float32
+    vC = 8 if sr == "f64" else 4
+    gen = torch.Generator(device=dev).manual_seed(7)
+    for k in (1, 8):
+        X = torch.randn((C.nrows, k), dtype=xdt, device=dev, generator=gen)
+        ms = timed_call(torch, lambda: sp.symm(C, X, sr))
+        B = 8 * (C.nrows + 1) + C.nnz * (4 + vC) + 2 * C.nrows * k * X.element_size()
+        side[f"symm_k{k}_ms"] = ms
+        side[f"symm_k{k}_GBs"] = B / (ms / 1e3) / 1e9
+        side[f"symm_k{k}_frac"] = B / (ms / 1e3) / 1e9 / HBM_PEAK_GBS
+        del X
+    del C
     if Bd is not None:
         side["offdiag_ms"] = timed_call(torch, lambda: sp.offdiag(Ad, Bd, sr))
         side["half_top_ms"] = timed_call(torch, lambda: sp.offdiag_half(Ad, Bd, "top", sr))

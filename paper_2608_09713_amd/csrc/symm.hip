@@ -64,6 +64,14 @@ __global__ __launch_bounds__(kBlock) void symm_kernel(const int64_t* __restrict_
         cj[u] = a + u < b ? ci[a + u] : 0;
         cvv[u] = a + u < b ? double(cv[a + u]) : 0.0;
     }
+    // X rows of the stretch's columns, gathered together (up to two columns
+    // per entry held ahead; wider blocks read them in the loop)
+    constexpr int KP = KB <= 2 ? KB : 1;
+    double xj[kPerS][KP];
+#pragma unroll
+    for (int u = 0; u < kPerS; ++u)
+#pragma unroll
+        for (int q = 0; q < KP; ++q) xj[u][q] = a + u < b ? double(x[int64_t(cj[u]) * ldx + q0 + q]) : 0.0;
     int64_t r = staged ? rlo + last_leq_s(win, 0, rhi - rlo, a) : last_leq_s(rp, rlo, rhi, a);
     int64_t rend = staged ? win[r - rlo + 1] : rp[r + 1];
     double xi[KB], dot[KB];
@@ -93,7 +101,8 @@ __global__ __launch_bounds__(kBlock) void symm_kernel(const int64_t* __restrict_
         const double c = cvv[u];
 #pragma unroll
         for (int q = 0; q < KB; ++q) {
-            dot[q] += c * double(x[j * ldx + q0 + q]);
+            const double xv = q < KP ? xj[u][q < KP ? q : 0] : double(x[j * ldx + q0 + q]);
+            dot[q] += c * xv;
             if (j != r) atomicAdd(&w[j * k + q0 + q], c * xi[q]);
         }
     }
