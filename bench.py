@@ -174,8 +174,9 @@ def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
     device copy's bandwidth and the whole call against it; t(lower(A)) over
     t(offdiag(A, A)) (ideal about 0.5: half the products and about half the
     output); Y = C X for 1 and 8 columns from C_L alone (Eq. (spmv)), with its
-    HBM figure; for a workload with a right operand, the two half blocks of
-    Algorithm 3 against the full off-diagonal block."""
+    HBM figure; two stages (A's columns split in half) accumulated one call
+    at a time against the one-shot lower part; for a workload with a right
+    operand, the two half blocks of Algorithm 3 against the full block."""
     side = {}
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
@@ -205,6 +206,29 @@ def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
         side[f"symm_k{k}_frac"] = B / (ms / 1e3) / 1e9 / HBM_PEAK_GBS
         del X
     del C
+    # two stages (the columns of A split in half) accumulated one at a time
+    # (Sec. III-A, C = sum over stages of SYRK(A_s)); Jaccard values do not
+    # add, so that workload accumulates its overlap counts
+    A = w["A"]
+    sa = "count" if sr == "jaccard" else sr
+    vdt = {"f64": np.float64, "f32": np.float32}.get(sa)
+    half = A.ncols // 2
+    rows = np.repeat(np.arange(A.nrows), np.diff(A.row_ptr))
+    stages = []
+    for lo, hi in ((0, half), (half, A.ncols)):
+        sel = (A.col_idx >= lo) & (A.col_idx < hi)
+        rp = np.zeros(A.nrows + 1, dtype=np.int64)
+        np.cumsum(np.bincount(rows[sel], minlength=A.nrows), out=rp[1:])
+        vals = A.values[sel].astype(vdt) if (vdt is not None and A.values is not None) else None
+        S = type(A)(A.nrows, hi - lo, rp, (A.col_idx[sel] - lo).astype(np.int32), vals)
+        stages.append(sp.DeviceCSR.from_host(S, dev, vdt))
+    Afull = sp.DeviceCSR.from_host(A if vdt else A.with_values(None), dev, vdt)
+    C1 = sp.lower(stages[0], sa)
+    side["stage_semiring"] = sa
+    side["stage1_lower_ms"] = timed_call(torch, lambda: sp.lower(stages[0], sa))
+    side["stage2_accumulate_ms"] = timed_call(torch, lambda: sp.lower_accumulate(C1, stages[1], sa))
+    side["one_shot_lower_ms"] = timed_call(torch, lambda: sp.lower(Afull, sa))
+    del C1, stages, Afull
     if Bd is not None:
         side["offdiag_ms"] = timed_call(torch, lambda: sp.offdiag(Ad, Bd, sr))
         side["half_top_ms"] = timed_call(torch, lambda: sp.offdiag_half(Ad, Bd, "top", sr))

@@ -140,6 +140,25 @@ spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_
                              const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C);
 
 /*
+ * C = C_prev + tril(A_s A_s^T): one stage's update added to the lower part
+ * accumulated so far, as a diagonal block sums its stages (Sec. III-A:
+ * C_ii = sum over s of SYRK(A_is)).  Accumulating the stages of A = [A_1 ...
+ * A_q] one call at a time gives tril(A A^T) (structure exactly; values up to
+ * the order of the sums).
+ * C_prev: m x m canonical CSR with no entry above the diagonal and values of
+ * the semiring's output type (for example an earlier spsyrk_lower or
+ * spsyrk_lower_accumulate result; an empty m x m matrix starts a sum).
+ * A_s: m x n_s, as for spsyrk_lower.  C: m x m, the union of the two patterns
+ * with shared entries summed (F64; F32 as one float addition; COUNT_I32).
+ * The Jaccard semiring does not add (its values are ratios): accumulate
+ * COUNT_I32 instead; it returns INVALID_ARG.
+ * Errors: as spsyrk_lower, plus INVALID_ARG (shapes, Jaccard, missing values)
+ * and NOT_CANONICAL for C_prev.
+ */
+spsyrk_status spsyrk_lower_accumulate(const spsyrk_csr* C_prev, const spsyrk_csr* A_s, spsyrk_semiring sr,
+                                      const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C);
+
+/*
  * One half of an off-diagonal block, as the two processes of a symmetric pair
  * split C_ij = C_ji^T between them (Sec. III-A, Algorithm 3): the process
  * below the diagonal computes the top rows of its block, its partner above

@@ -204,6 +204,35 @@ def mirror(m: int, row_ptr, col_idx, values, lib=None) -> Result:
     return Result(m, m, out_rp, out_ci, out_v)
 
 
+def lower_accumulate(P: Result, A_s, semiring, lib=None) -> Result:
+    """P + tril(A_s A_s^T) (Sec. III-A: a diagonal block is the sum over stages
+    of SYRK(A_is)): the union of the two patterns, shared entries summed (fp64
+    for f64, one float addition for f32, integers for count)."""
+    T = lower(A_s, semiring, lib=lib)
+    m = A_s.nrows
+    rows_p = np.repeat(np.arange(m), np.diff(P.row_ptr))
+    rows_t = np.repeat(np.arange(m), np.diff(T.row_ptr))
+    keys = np.concatenate([rows_p * m + P.col_idx[: P.row_ptr[-1]], rows_t * m + T.col_idx])
+    uk, inv = np.unique(keys, return_inverse=True)
+    vals = np.concatenate([P.values[: P.row_ptr[-1]], T.values])
+    if semiring == "count":
+        out = np.zeros(len(uk), dtype=np.int64)
+        np.add.at(out, inv, vals.astype(np.int64))
+        out = out.astype(np.int32)
+    else:
+        out = np.zeros(len(uk), dtype=np.float64)
+        np.add.at(out, inv, vals.astype(np.float64))
+        out = out.astype(np.float32 if semiring == "f32" else np.float64)
+    sa = None
+    if T.sum_abs is not None:
+        pa = P.sum_abs if P.sum_abs is not None else np.abs(P.values[: P.row_ptr[-1]].astype(np.float64))
+        sa = np.zeros(len(uk))
+        np.add.at(sa, inv, np.concatenate([pa, T.sum_abs]))
+    rp = np.zeros(m + 1, dtype=np.int64)
+    np.cumsum(np.bincount(uk // m, minlength=m), out=rp[1:])
+    return Result(m, m, rp, (uk % m).astype(np.int32), out, sa)
+
+
 def symm(m: int, row_ptr, col_idx, values, X):
     """Y = C X for the symmetric C = C_L + C_L^T - D, from the stored lower
     part C_L (row_ptr, col_idx, values) as Eq. (spmv) writes it: the product

@@ -91,6 +91,10 @@ def library():
                                                 ctypes.POINTER(_CsrOut)]
             lib.spsyrk_mirror.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
                                           ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_lower_accumulate.restype = ctypes.c_int
+            lib.spsyrk_lower_accumulate.argtypes = [ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), ctypes.c_int,
+                                                    ctypes.POINTER(_Allocator), ctypes.c_void_p,
+                                                    ctypes.POINTER(_CsrOut)]
             lib.spsyrk_symm.restype = ctypes.c_int
             lib.spsyrk_symm.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
                                         ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(_Allocator),
@@ -109,7 +113,8 @@ def library():
     return _lib
 
 
-EXPORTS = ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror", "spsyrk_symm",
+EXPORTS = ("spsyrk_lower", "spsyrk_lower_accumulate", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror",
+           "spsyrk_symm",
            "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
            "spsyrk_timing_end")
@@ -237,6 +242,16 @@ def lower(A: DeviceCSR, semiring="f64") -> DeviceCSR:
     sr = _sr(semiring)
     a = _csr_struct(A, sr, True)
     return _call("spsyrk_lower", lambda ar: (ctypes.byref(a), sr, ctypes.byref(ar.struct)), sr, A.row_ptr.device)
+
+
+def lower_accumulate(C_prev: DeviceCSR, A_s: DeviceCSR, semiring="f64") -> DeviceCSR:
+    """C_prev + tril(A_s A_s^T), one stage added to an accumulated lower part
+    (spsyrk_lower_accumulate; f64, f32 or count)."""
+    sr = _sr(semiring)
+    p = _csr_struct(C_prev, sr, False)
+    a = _csr_struct(A_s, sr, True)
+    return _call("spsyrk_lower_accumulate", lambda ar: (ctypes.byref(p), ctypes.byref(a), sr, ctypes.byref(ar.struct)),
+                 sr, A_s.row_ptr.device)
 
 
 def offdiag(Ai: DeviceCSR, Aj: DeviceCSR, semiring="f64") -> DeviceCSR:

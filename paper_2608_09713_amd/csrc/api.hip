@@ -91,6 +91,14 @@ class Arena {
                 q = nullptr;
             }
     }
+    // release an allocation made as an output (an intermediate result)
+    void release_output(void* p) {
+        for (auto& q : outputs_)
+            if (q == p) {
+                free_one(q);
+                q = nullptr;
+            }
+    }
     void keep_outputs() { outputs_.clear(); }
     void release_all() {
         for (void* p : work_)
@@ -996,6 +1004,73 @@ spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t
         symm_product(c, int(sr), X, ldx, k, Y, ldy, tmp, s);
         check_launch();
         HIPCHK(hipStreamSynchronize(s));
+    });
+}
+
+spsyrk_status spsyrk_lower_accumulate(const spsyrk_csr* C_prev, const spsyrk_csr* A_s, spsyrk_semiring sr,
+                                      const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C) {
+    return guarded(C, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        if (sr == SPSYRK_COUNT_I32_JACCARD_F32) {
+            set_detail("Jaccard values do not add across stages; accumulate overlap counts (COUNT_I32)");
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        check_input(C_prev, int(sr), false, "C_prev", int64_t(1) << 62);
+        check_input(A_s, int(sr), true, "A_s");
+        if (C_prev->nrows != C_prev->ncols || C_prev->nrows != A_s->nrows) {
+            set_detail("C_prev must be m x m with m = A_s rows (%lld x %lld, %lld)", (long long)C_prev->nrows,
+                       (long long)C_prev->ncols, (long long)A_s->nrows);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        if (C_prev->nnz > 0 && !C_prev->values) {
+            set_detail("C_prev values are required");
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        const int64_t m = A_s->nrows;
+        const DevCsr P = dev(C_prev);
+        {
+            Ctl* ctl = ar.get_t<Ctl>(1);
+            zero_ctl(ctl, s);
+            validate(P, true, ar, ctl, s, "C_prev");
+        }
+        // this stage's lower part, an intermediate result
+        spsyrk_csr_out t{};
+        syrk(dev(A_s), dev(A_s), true, int(sr), ar, s, &t);
+        DevCsr T;
+        T.m = m;
+        T.n = m;
+        T.nnz = t.nnz;
+        T.rp = t.row_ptr;
+        T.ci = t.col_idx;
+        T.v = t.values;
+        // union of the two patterns, row by row: counts, row pointers, merge
+        int64_t* cnt = ar.get_t<int64_t>(m + 1);
+        HIPCHK(hipMemsetAsync(cnt + m, 0, sizeof(int64_t), s));
+        merge_lower(false, int(sr), m, P, T, cnt, nullptr, nullptr, nullptr, s);
+        check_launch();
+        int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
+        void* stmp = ar.get(scan_tmp_bytes(m + 1));
+        scan_i64(cnt, c_rp, m + 1, nullptr, stmp, s);
+        check_launch();
+        const int64_t total = m > 0 ? read_i64(c_rp + m, s) : 0;
+        ar.release(stmp);
+        const int vb = out_value_bytes(int(sr));
+        int32_t* c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
+        void* c_val = ar.get(size_t(total > 0 ? total : 1) * vb, true);
+        merge_lower(true, int(sr), m, P, T, nullptr, c_rp, c_ci, c_val, s);
+        check_launch();
+        HIPCHK(hipStreamSynchronize(s));
+        ar.release(cnt);
+        ar.release_output(t.row_ptr);
+        ar.release_output(t.col_idx);
+        ar.release_output(t.values);
+        C->nrows = m;
+        C->ncols = m;
+        C->nnz = total;
+        C->capacity = total;
+        C->row_ptr = c_rp;
+        C->col_idx = c_ci;
+        C->values = c_val;
     });
 }
 

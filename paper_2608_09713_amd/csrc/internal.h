@@ -225,6 +225,13 @@ struct HeavyArgs {
 void heavy_symbolic(const HeavyArgs& a, int* queue, hipStream_t s);
 void heavy_numeric(const HeavyArgs& a, int* queue, hipStream_t s);
 
+// ---- accumulate.hip
+// Row-wise union of two lower parts P and T (m rows, canonical): write false
+// sets cnt[i] = distinct columns of row i; write true writes the merged rows
+// (columns ascending, shared entries summed) at crp.  sr: F64, F32 or COUNT.
+void merge_lower(bool write, int sr, int64_t m, const DevCsr& P, const DevCsr& T, int64_t* cnt, const int64_t* crp,
+                 int32_t* cci, void* cv, hipStream_t s);
+
 // ---- symm.hip
 // Y = C X with C = C_L + C_L^T - D from the stored lower part C (canonical,
 // nothing above the diagonal, values of the semiring's output type).  X and

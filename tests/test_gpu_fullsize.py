@@ -185,3 +185,31 @@ def test_symm_full(dev, name):
     tol = 1e-12 if sr in ("f64", "count") else 2.0 ** -24
     err = np.abs(y[rows] - ref)
     assert np.all(err <= tol * np.maximum(scale, np.abs(ref)) + 1e-300), float(err.max())
+
+
+def test_accumulate_full_columns_split(dev):
+    # jaccard_large's pattern as two stages (its columns split in half): the
+    # overlap counts accumulated stage by stage equal the one-shot lower part
+    # bit for bit
+    import torch
+    from paper_2608_09713_amd.workloads import CSR
+    w = W.make("jaccard_large", 1, 0)
+    A = w["A"]
+    print(f"[full accumulate] m={A.nrows} nnz={A.nnz}", flush=True)
+    half = A.ncols // 2
+    rows = np.repeat(np.arange(A.nrows), np.diff(A.row_ptr))
+    parts = []
+    for lo, hi in ((0, half), (half, A.ncols)):
+        sel = (A.col_idx >= lo) & (A.col_idx < hi)
+        rp = np.zeros(A.nrows + 1, dtype=np.int64)
+        np.cumsum(np.bincount(rows[sel], minlength=A.nrows), out=rp[1:])
+        parts.append(CSR(A.nrows, hi - lo, rp, (A.col_idx[sel] - lo).astype(np.int32), None))
+    full = sp.lower(upload(A, "count", dev), "count")
+    first = sp.lower(upload(parts[0], "count", dev), "count")
+    acc = sp.lower_accumulate(first, upload(parts[1], "count", dev), "count")
+    del first
+    assert acc.nnz == full.nnz
+    assert torch.equal(acc.row_ptr, full.row_ptr)
+    n = full.nnz
+    assert torch.equal(acc.col_idx[:n], full.col_idx[:n])
+    assert torch.equal(acc.values[:n], full.values[:n])

@@ -336,6 +336,51 @@ def _symm_ref(L, X):
     return ref, np.maximum(scale, np.abs(ref))
 
 
+def _hcat(A1, A2):
+    D1 = np.zeros((A1.nrows, A1.ncols)); P1 = np.zeros_like(D1, dtype=bool)
+    D2 = np.zeros((A2.nrows, A2.ncols)); P2 = np.zeros_like(D2, dtype=bool)
+    for A, D, P in ((A1, D1, P1), (A2, D2, P2)):
+        r = np.repeat(np.arange(A.nrows), np.diff(A.row_ptr))
+        D[r, A.col_idx] = A.values
+        P[r, A.col_idx] = True
+    return csr_from_dense(np.hstack([D1, D2]), pattern=np.hstack([P1, P2]))
+
+
+@pytest.mark.parametrize("semiring", ["f64", "f32", "count"])
+def test_lower_accumulate(dev, semiring):
+    # stage accumulation against the oracle, starting from an empty sum and
+    # from a previous stage; rows of several wavefront lengths
+    rng = np.random.default_rng(47)
+    vdt = VDT[semiring]
+    m = 500
+    A1 = random_csr(rng, m, 300, 0.03, signed=True)
+    A2 = random_csr(rng, m, 200, 0.05, signed=True)
+    cast = (lambda A: A.with_values(A.values.astype(vdt))) if vdt is not None else (lambda A: A.with_values(None))
+    empty = sp.DeviceCSR.from_host(CSR(m, m, np.zeros(m + 1, np.int64), np.zeros(0, np.int32),
+                                       np.zeros(0, dtype={"f64": np.float64, "f32": np.float32,
+                                                          "count": np.int32}[semiring])), dev)
+    print(f"[accumulate {semiring}] m={m}", flush=True)
+    C1 = sp.lower_accumulate(empty, upload(A1, semiring, dev), semiring)
+    R1 = oracle.lower(cast(A1), semiring)
+    compare_full(C1, R1, semiring, "first stage")
+    C2 = sp.lower_accumulate(C1, upload(A2, semiring, dev), semiring)
+    R2 = oracle.lower_accumulate(R1, cast(A2), semiring)
+    compare_full(C2, R2, semiring, "second stage")
+    # the same as the lower part of the concatenated stages (structure exactly)
+    L = sp.lower(upload(_hcat(A1, A2), semiring, dev), semiring)
+    rp2, ci2, _ = C2.to_host()
+    rpl, cil, _ = L.to_host()
+    np.testing.assert_array_equal(rp2, rpl)
+    np.testing.assert_array_equal(ci2, cil)
+
+
+def test_lower_accumulate_rejects_jaccard(dev):
+    A = random_csr(np.random.default_rng(48), 10, 10, 0.3)
+    C = sp.lower(upload(A, "jaccard", dev), "jaccard")
+    with pytest.raises(sp.SpsyrkError):
+        sp.lower_accumulate(C, upload(A, "jaccard", dev), "jaccard")
+
+
 def _check_symm(Y, ref, scale, semiring, what):
     err = np.abs(Y.astype(np.float64) - ref)
     bad = err > SYMM_TOL[semiring] * scale + 1e-300

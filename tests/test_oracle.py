@@ -392,6 +392,44 @@ def test_symm_matches_mirrored_matrix():
     np.testing.assert_array_equal(Z, 0.0)
 
 
+def _hcat(A1, A2):
+    D1, P1 = dense_of(A1)
+    D2, P2 = dense_of(A2)
+    return csr_from_dense(np.hstack([D1, D2]), pattern=np.hstack([P1, P2]))
+
+
+def test_accumulate_is_concatenation():
+    # one stage at a time: lower(A1) + tril(A2 A2^T) = lower([A1 A2]) (Sec. III-A)
+    rng = np.random.default_rng(31)
+    for m in (30, 1, 17):
+        A1 = random_csr(rng, m, 20, 0.15)
+        A2 = random_csr(rng, m, 25, 0.15)
+        A3 = random_csr(rng, m, 9, 0.3)
+        for sr in ("f64", "count"):
+            acc = oracle.lower(A1 if sr == "f64" else A1.with_values(None), sr)
+            for Ak in (A2, A3):
+                acc = oracle.lower_accumulate(acc, Ak if sr == "f64" else Ak.with_values(None), sr)
+            A = _hcat(_hcat(A1, A2), A3)
+            ref = oracle.lower(A if sr == "f64" else A.with_values(None), sr)
+            np.testing.assert_array_equal(acc.row_ptr, ref.row_ptr)
+            np.testing.assert_array_equal(acc.col_idx, ref.col_idx)
+            if sr == "count":
+                np.testing.assert_array_equal(acc.values, ref.values)
+            else:
+                np.testing.assert_allclose(acc.values, ref.values, rtol=1e-12, atol=1e-12)
+
+
+def test_accumulate_from_empty():
+    rng = np.random.default_rng(32)
+    A = random_csr(rng, 25, 30, 0.12)
+    empty = oracle.Result(25, 25, np.zeros(26, np.int64), np.zeros(0, np.int32), np.zeros(0))
+    acc = oracle.lower_accumulate(empty, A, "f64")
+    ref = oracle.lower(A, "f64")
+    np.testing.assert_array_equal(acc.row_ptr, ref.row_ptr)
+    np.testing.assert_array_equal(acc.col_idx, ref.col_idx)
+    np.testing.assert_array_equal(acc.values, ref.values)
+
+
 def test_concatenation_sums_stages():
     # C_ii = sum_s SYRK(A_is) (Sec. III-A): lower([A1 A2]) = lower(A1) + lower(A2)
     rng = np.random.default_rng(8)
