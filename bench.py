@@ -173,7 +173,8 @@ def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
     """Figures reported beside the metric (outside the timed steps): a plain
     device copy's bandwidth and the whole call against it; t(lower(A)) over
     t(offdiag(A, A)) (ideal about 0.5: half the products and about half the
-    output); Y = C X for 1 and 8 columns from C_L alone (Eq. (spmv)), with its
+    output); a planned product for new values of the same pattern; Y = C X
+    for 1 and 8 columns from C_L alone (Eq. (spmv)), with its
     HBM figure; two stages (A's columns split in half) accumulated one call
     at a time against the one-shot lower part; for a workload with a right
     operand, the two half blocks of Algorithm 3 against the full block."""
@@ -191,6 +192,11 @@ def side_measurements(sp, torch, dev, Ad, Bd, sr, w, whole_call_GBs):
     side["lower_ms"] = t_low
     side["offdiag_AA_ms"] = t_full
     side["lower_over_offdiag_AA"] = t_low / t_full
+    # the two-phase use: a plan, then products for new values of the pattern
+    plan, C0 = sp.lower_plan(Ad, sr)
+    del C0
+    side["plan_execute_ms"] = timed_call(torch, lambda: plan.execute(Ad.values))
+    plan.close()
     # Y = C X from C_L alone (Eq. (spmv) / (spgemm)): algorithmic bytes are
     # C_L read once, X read once and Y written once
     C = sp.lower(Ad, sr)

@@ -17,6 +17,11 @@
  *   spsyrk_offdiag : C   = A_i A_j^T         (full rectangular block, no prune)
  *   spsyrk_mirror  : C   = C_L + C_L^T - D   (symmetric completion of C_L)
  *
+ * Reproducibility: structure and the count semirings are the same bit for
+ * bit on every run; plus-times values of rows with many products (the
+ * dense-tile accumulator) are summed in an order that may change from run to
+ * run, so their last bits may differ (within the stated tolerances).
+ *
  * Structure is the pattern product: C(i,j) is stored iff rows i and j share a
  * stored column (stored zeros of A count as structure; computed zeros are
  * kept).  Output rows keep the input row order and columns ascend strictly
@@ -138,6 +143,36 @@ spsyrk_status spsyrk_lower(const spsyrk_csr* A, spsyrk_semiring sr, const spsyrk
  */
 spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_semiring sr,
                              const spsyrk_allocator* al, void* hip_stream, spsyrk_csr_out* C);
+
+/*
+ * Two-phase use for repeated products on one pattern (new values on an
+ * unchanged matrix).  spsyrk_lower_plan computes C_L = tril(A A^T) as
+ * spsyrk_lower does and also returns a plan that keeps every pattern-only
+ * result on the device: copies of A's row_ptr and col_idx, the column index
+ * of A, the partner runs, product counts, row classes and C_L's row_ptr.
+ * spsyrk_lower_execute then computes C_L for new values of the same pattern
+ * (values: nnz entries in A's entry order, double for F64, float for F32,
+ * ignored by the COUNT semirings): the index's values are gathered from the
+ * new ones and the numeric pass writes every row straight into its final
+ * place.  It neither sorts nor waits on the host (the output size is known),
+ * and returns with the work enqueued on hip_stream.  The output has the
+ * plan's structure and the semiring it was made with.
+ * The plan's buffers come from the allocator passed to spsyrk_lower_plan
+ * (hipMalloc when NULL) and stay allocated until spsyrk_plan_destroy, which
+ * frees them with that allocator (or hipFree after a device synchronisation).
+ * Executions of one plan must not overlap (they share its counters and the
+ * index's values); the plan may be used from any stream once the creating
+ * call has returned.
+ * Errors: as spsyrk_lower; spsyrk_lower_execute: INVALID_ARG (null plan or
+ * missing values), OOM, HIP.
+ */
+typedef struct spsyrk_plan_s spsyrk_plan;
+
+spsyrk_status spsyrk_lower_plan(const spsyrk_csr* A, spsyrk_semiring sr, const spsyrk_allocator* al,
+                                void* hip_stream, spsyrk_plan** plan, spsyrk_csr_out* C);
+spsyrk_status spsyrk_lower_execute(spsyrk_plan* plan, const void* values, const spsyrk_allocator* al,
+                                   void* hip_stream, spsyrk_csr_out* C);
+spsyrk_status spsyrk_plan_destroy(spsyrk_plan* plan);
 
 /*
  * C = C_prev + tril(A_s A_s^T): one stage's update added to the lower part

@@ -91,6 +91,15 @@ def library():
                                                 ctypes.POINTER(_CsrOut)]
             lib.spsyrk_mirror.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
                                           ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_lower_plan.restype = ctypes.c_int
+            lib.spsyrk_lower_plan.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
+                                              ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p),
+                                              ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_lower_execute.restype = ctypes.c_int
+            lib.spsyrk_lower_execute.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(_Allocator),
+                                                 ctypes.c_void_p, ctypes.POINTER(_CsrOut)]
+            lib.spsyrk_plan_destroy.restype = ctypes.c_int
+            lib.spsyrk_plan_destroy.argtypes = [ctypes.c_void_p]
             lib.spsyrk_lower_accumulate.restype = ctypes.c_int
             lib.spsyrk_lower_accumulate.argtypes = [ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), ctypes.c_int,
                                                     ctypes.POINTER(_Allocator), ctypes.c_void_p,
@@ -113,7 +122,8 @@ def library():
     return _lib
 
 
-EXPORTS = ("spsyrk_lower", "spsyrk_lower_accumulate", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror",
+EXPORTS = ("spsyrk_lower", "spsyrk_lower_plan", "spsyrk_lower_execute", "spsyrk_plan_destroy",
+           "spsyrk_lower_accumulate", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror",
            "spsyrk_symm",
            "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
@@ -219,6 +229,15 @@ def _sr(semiring) -> int:
     return SEMIRINGS[semiring] if isinstance(semiring, str) else int(semiring)
 
 
+def _take_out(arena, out, sr):
+    import torch
+    odt = getattr(torch, _OUT_DTYPE[sr])
+    rp = arena.take(out.row_ptr, torch.int64, out.nrows + 1)
+    ci = arena.take(out.col_idx, torch.int32, out.capacity)
+    v = arena.take(out.values, odt, out.capacity) if out.values else None
+    return DeviceCSR(out.nrows, out.ncols, rp, ci, v, out.nnz)
+
+
 def _call(fn_name, args, sr, device, out_has_values=True):
     import torch
     lib = library()
@@ -228,13 +247,70 @@ def _call(fn_name, args, sr, device, out_has_values=True):
     rc = getattr(lib, fn_name)(*args(arena), ctypes.c_void_p(stream), ctypes.byref(out))
     if rc != 0:
         raise SpsyrkError(rc, lib.spsyrk_last_error_detail().decode())
-    odt = getattr(torch, _OUT_DTYPE[sr])
-    rp = arena.take(out.row_ptr, torch.int64, out.nrows + 1)
-    ci = arena.take(out.col_idx, torch.int32, out.capacity)
-    v = arena.take(out.values, odt, out.capacity) if out.values else None
+    C = _take_out(arena, out, sr)
     if arena.live:
         raise RuntimeError("library left allocations unreleased")
-    return DeviceCSR(out.nrows, out.ncols, rp, ci, v, out.nnz)
+    return C
+
+
+class Plan:
+    """A lower product's pattern-only results kept on the device
+    (spsyrk_lower_plan); ``execute(values)`` recomputes C_L for new values of
+    the same pattern (spsyrk_lower_execute).  ``close()`` (or garbage
+    collection) releases the plan (spsyrk_plan_destroy)."""
+
+    def __init__(self, handle, arena, sr, nnz, device):
+        self._h = handle
+        self._arena = arena  # owns the plan's device buffers
+        self.sr = sr
+        self.nnz = nnz
+        self.device = device
+
+    def execute(self, values=None) -> DeviceCSR:
+        import torch
+        if self._h is None:
+            raise RuntimeError("plan is closed")
+        vp = None
+        if _IN_DTYPE[self.sr] is not None:
+            want = getattr(torch, _IN_DTYPE[self.sr])
+            if values is None or values.dtype != want or not values.is_contiguous() or values.numel() < self.nnz:
+                raise TypeError(f"values must be a contiguous {want} tensor of {self.nnz} entries")
+            vp = values.data_ptr()
+        return _call("spsyrk_lower_execute",
+                     lambda ar: (self._h, ctypes.c_void_p(vp), ctypes.byref(ar.struct)), self.sr, self.device)
+
+    def close(self):
+        if self._h is not None:
+            library().spsyrk_plan_destroy(self._h)
+            self._h = None
+            if self._arena.live:
+                raise RuntimeError("plan buffers left unreleased")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def lower_plan(A: DeviceCSR, semiring="f64"):
+    """(plan, C_L): C_L = tril(A A^T) and a plan for new values of A's pattern
+    (spsyrk_lower_plan)."""
+    import torch
+    sr = _sr(semiring)
+    lib = library()
+    a = _csr_struct(A, sr, True)
+    dev = A.row_ptr.device
+    arena = _TorchArena(dev)
+    out = _CsrOut()
+    h = ctypes.c_void_p()
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = lib.spsyrk_lower_plan(ctypes.byref(a), sr, ctypes.byref(arena.struct), ctypes.c_void_p(stream),
+                               ctypes.byref(h), ctypes.byref(out))
+    if rc != 0:
+        raise SpsyrkError(rc, lib.spsyrk_last_error_detail().decode())
+    C = _take_out(arena, out, sr)
+    return Plan(h, arena, sr, A.nnz, dev), C
 
 
 def lower(A: DeviceCSR, semiring="f64") -> DeviceCSR:

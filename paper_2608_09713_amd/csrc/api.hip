@@ -91,6 +91,15 @@ class Arena {
                 q = nullptr;
             }
     }
+    // keep a work allocation past the call (it becomes the caller's, like an output)
+    void* keep(void* p) {
+        for (auto& q : work_)
+            if (q == p) {
+                q = nullptr;
+                outputs_.push_back(p);
+            }
+        return p;
+    }
     // release an allocation made as an output (an intermediate result)
     void release_output(void* p) {
         for (auto& q : outputs_)
@@ -254,9 +263,11 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 // With run (zeroed beforehand; lower mode) every entry's partner run is written.
 // need_dir: build the group directory for partner-run lookups.
 // ccount (zeroed, B.n entries, with no directory only): the entries of every
-// column, written when the local sort builds the index (*counted is then set)
+// column, written when the local sort builds the index (*counted is then set).
+// vsrc (N entries): the entry of B behind every position of the index.
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                     uint2* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr) {
+                     uint2* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr,
+                     uint32_t* vsrc = nullptr) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -313,6 +324,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
             pk.drop_last = drop_last;
             pk.kept = &ctl->nkept;
             pk.ccount = ccount;
+            pk.vsrc = vsrc;
             HIPCHK(hipMemsetAsync(&ctl->nkept, 0, sizeof(int64_t), s));
         }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
@@ -323,7 +335,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         if (which >= 0) {
             void* ctmp = ar.get(colindex_tmp_bytes(N));
             build_colindex(which ? kb : ka, which ? rb : ra, which ? eb : ea, N, drop_last, vb, sr, B.v, B.rp, lenbits,
-                           cx, ctmp, &ctl->nkept, run, s);
+                           cx, ctmp, &ctl->nkept, run, s, vsrc);
             check_launch();
             ar.release(ctmp);
         }
@@ -361,6 +373,31 @@ int rows_per_chunk(double) {
 
 constexpr int64_t kDenseColumns = int64_t(1) << 26;  // dense column starts: at most 256 MB
 
+// What a lower product keeps for later products with new values on the same
+// pattern: everything that depends on the pattern only (the column index and
+// the entry behind each of its positions, partner runs, product counts, row
+// classes, heavy rows' lengths and cursors, the output row pointers).
+struct LowerPlan {
+    int sr = 0;
+    int64_t m = 0, n = 0, nnz = 0;
+    bool empty = false;  // no products: every execution gives the empty result
+    int64_t* rp = nullptr;  // copies of the pattern
+    int32_t* ci = nullptr;
+    ColIndex cx;
+    uint32_t* vsrc = nullptr;  // entry of A behind every position of the index (nnz)
+    uint2* run = nullptr;
+    unsigned long long* prod = nullptr;
+    int32_t* heavy_rows = nullptr;
+    int64_t nheavy = 0;
+    int64_t* heavy_nnz = nullptr;
+    uint32_t* cursor = nullptr;
+    Ctl* ctl = nullptr;
+    int64_t* c_rp = nullptr;
+    int64_t total = 0;
+    int rows_per_chunk = 0;
+    int64_t nchunks = 0;
+};
+
 // C_L = tril(A A^T) (lower, R = L) or L R^T: column index with the partner
 // run of every entry, per-row product counts, row classes, exact lengths of
 // the heavy rows, the light rows computed once into upper-bound staging slots
@@ -370,7 +407,7 @@ constexpr int64_t kDenseColumns = int64_t(1) << 26;  // dense column starts: at 
 // read from dense column starts.
 
 void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                spsyrk_csr_out* C) {
+                spsyrk_csr_out* C, LowerPlan* plan = nullptr) {
     const int64_t m = L.m;
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
@@ -380,7 +417,13 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     if (lower) {
         HIPCHK(hipMemsetAsync(run, 0, size_t(L.nnz) * sizeof(uint2), s));
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
-        cx = build_index(L, true, sr, ar, ctl, s, run);
+        uint32_t* vsrc = nullptr;
+        if (plan) {
+            vsrc = ar.get_t<uint32_t>(L.nnz);
+            HIPCHK(hipMemsetAsync(vsrc, 0, size_t(L.nnz) * sizeof(uint32_t), s));
+            plan->vsrc = vsrc;
+        }
+        cx = build_index(L, true, sr, ar, ctl, s, run, true, nullptr, nullptr, vsrc);
     } else {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
         // column starts of R: from the counts the local sort writes, else by counting
@@ -506,6 +549,26 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     C->row_ptr = c_rp;
     C->col_idx = c_ci;
     C->values = c_val;
+    if (plan) {
+        plan->cx = cx;
+        plan->run = static_cast<uint2*>(ar.keep(run));
+        plan->prod = static_cast<unsigned long long*>(ar.keep(prod));
+        ar.keep(cx.key);
+        if (cx.val) ar.keep(cx.val);
+        ar.keep(plan->vsrc);
+        plan->heavy_rows = static_cast<int32_t*>(ar.keep(heavy_rows));
+        plan->nheavy = nheavy;
+        if (nheavy > 0) {
+            plan->heavy_nnz = static_cast<int64_t*>(ar.keep(heavy_nnz));
+            plan->cursor = static_cast<uint32_t*>(ar.keep(ha.cursor));
+        }
+        plan->ctl = static_cast<Ctl*>(ar.keep(ctl));
+        plan->c_rp = ar.get_t<int64_t>(m + 1, true);
+        HIPCHK(hipMemcpyAsync(plan->c_rp, c_rp, size_t(m + 1) * sizeof(int64_t), hipMemcpyDeviceToDevice, s));
+        plan->total = total;
+        plan->rows_per_chunk = fa.rows_per_chunk;
+        plan->nchunks = fa.nchunks;
+    }
     spsyrk_stats st{};
     st.nnz_out = total;
     st.csc_entries = h.nkept;
@@ -519,7 +582,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
 }
 
 // C = tril(L R^T) (lower) or L R^T (offdiag), with R = L for lower.
-void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
+void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C,
+          LowerPlan* plan = nullptr) {
     Ctl* ctl = ar.get_t<Ctl>(1);
     zero_ctl(ctl, s);
     {
@@ -543,13 +607,14 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         HIPCHK(hipStreamSynchronize(s));
         g_stats = st;
         g_stats_valid = true;
+        if (plan) plan->empty = true;
         return;
     }
 
     // single pass over the light rows; off the diagonal when the right
     // operand's column starts fit a dense array (else the two-pass path)
-    if (!two_pass() && (lower || R.n <= kDenseColumns)) {
-        syrk_fused(L, R, lower, sr, ar, ctl, s, C);
+    if ((plan || !two_pass()) && (lower || R.n <= kDenseColumns)) {
+        syrk_fused(L, R, lower, sr, ar, ctl, s, C, plan);
         return;
     }
     int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
@@ -897,6 +962,88 @@ void offdiag_half(const DevCsr& L, const DevCsr& R, int half, int sr, Arena& ar,
     C->ncols = R.m;
 }
 
+// A lower product on a planned pattern with new values: the values of the
+// column index gathered from the new values, then the light rows written
+// straight into their final places (their lengths are known) and the heavy
+// rows; no sort, no symbolic pass, no staging, no compaction, no host wait.
+void lower_execute(const LowerPlan& P, const void* vals, Arena& ar, hipStream_t s, spsyrk_csr_out* C) {
+    const int64_t m = P.m;
+    const int vbo = out_value_bytes(P.sr);
+    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
+    const int64_t total = P.empty ? 0 : P.total;
+    int32_t* c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
+    void* c_val = ar.get(size_t(total > 0 ? total : 1) * vbo, true);
+    C->nrows = m;
+    C->ncols = m;
+    C->nnz = total;
+    C->capacity = total;
+    C->row_ptr = c_rp;
+    C->col_idx = c_ci;
+    C->values = c_val;
+    if (P.empty) {
+        HIPCHK(hipMemsetAsync(c_rp, 0, size_t(m + 1) * sizeof(int64_t), s));
+        return;
+    }
+    HIPCHK(hipMemcpyAsync(c_rp, P.c_rp, size_t(m + 1) * sizeof(int64_t), hipMemcpyDeviceToDevice, s));
+    const int vb = (P.sr == kF64) ? 8 : (P.sr == kF32 ? 4 : 0);
+    if (vb) {
+        gather_values(P.cx.val, vals, P.vsrc, P.nnz, vb, s);
+        check_launch();
+    }
+    int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
+    FusedArgs fa;
+    fa.m = m;
+    fa.rp = P.rp;
+    fa.ci = P.ci;
+    fa.val = vals;
+    fa.cx = P.cx;
+    fa.m_right = m;
+    fa.lower = true;
+    fa.sr = P.sr;
+    fa.prod = P.prod;
+    fa.run = P.run;
+    fa.heavy_nnz = P.heavy_nnz;
+    fa.ubp = P.c_rp;  // the final row starts: the light rows land in place
+    fa.row_cnt = row_cnt;
+    fa.rows_per_chunk = P.rows_per_chunk;
+    fa.nchunks = P.nchunks;
+    HIPCHK(hipMemsetAsync(&P.ctl->chunk_counter, 0, sizeof(P.ctl->chunk_counter), s));
+    fa.chunk_counter = &P.ctl->chunk_counter;
+    fa.c_ci = c_ci;
+    fa.c_val = c_val;
+    {
+        Phase ph(SPSYRK_PHASE_LIGHT_NUMERIC, s);
+        light_fused(fa, s);
+    }
+    check_launch();
+    if (P.nheavy > 0) {
+        HeavyArgs ha;
+        ha.m = m;
+        ha.rp = P.rp;
+        ha.ci = P.ci;
+        ha.val = vals;
+        ha.cx = P.cx;
+        ha.m_right = m;
+        ha.rp_right = P.rp;
+        ha.lower = true;
+        ha.sr = P.sr;
+        ha.heavy_rows = P.heavy_rows;
+        ha.heavy_count = &P.ctl->heavy_count;
+        ha.heavy_max = P.nheavy;
+        ha.row_nnz = P.heavy_nnz;
+        ha.run = P.run;
+        ha.runs_ready = true;
+        ha.cursor = P.cursor;
+        ha.c_rp = c_rp;
+        ha.c_ci = c_ci;
+        ha.c_val = c_val;
+        Phase ph(SPSYRK_PHASE_HEAVY_NUMERIC, s);
+        heavy_numeric(ha, &P.ctl->queue, s);
+    }
+    check_launch();
+    ar.release(row_cnt);
+}
+
 template <typename F>
 spsyrk_status guarded(spsyrk_csr_out* C, const spsyrk_allocator* al, void* stream, F body) {
     g_stats_valid = false;
@@ -926,6 +1073,14 @@ spsyrk_status guarded(spsyrk_csr_out* C, const spsyrk_allocator* al, void* strea
 }
 
 }  // namespace
+
+// the opaque plan handle of the C interface
+struct spsyrk_plan_s {
+    LowerPlan p;
+    spsyrk_allocator al{};
+    bool has_al = false;
+    std::vector<void*> bufs;  // device buffers owned by the plan
+};
 
 extern "C" {
 
@@ -1072,6 +1227,83 @@ spsyrk_status spsyrk_lower_accumulate(const spsyrk_csr* C_prev, const spsyrk_csr
         C->col_idx = c_ci;
         C->values = c_val;
     });
+}
+
+spsyrk_status spsyrk_lower_plan(const spsyrk_csr* A, spsyrk_semiring sr, const spsyrk_allocator* al,
+                                void* hip_stream, spsyrk_plan** plan, spsyrk_csr_out* C) {
+    if (!plan) {
+        set_detail("plan is null");
+        return SPSYRK_ERR_INVALID_ARG;
+    }
+    *plan = nullptr;
+    spsyrk_plan* made = nullptr;
+    const spsyrk_status st = guarded(C, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        check_semiring(int(sr));
+        check_input(A, int(sr), true, "A");
+        const DevCsr d = dev(A);
+        LowerPlan lp;
+        syrk(d, d, true, int(sr), ar, s, C, &lp);
+        lp.sr = int(sr);
+        lp.m = d.m;
+        lp.n = d.n;
+        lp.nnz = d.nnz;
+        lp.rp = ar.get_t<int64_t>(d.m + 1, true);
+        HIPCHK(hipMemcpyAsync(lp.rp, d.rp, size_t(d.m + 1) * sizeof(int64_t), hipMemcpyDeviceToDevice, s));
+        lp.ci = ar.get_t<int32_t>(d.nnz > 0 ? d.nnz : 1, true);
+        if (d.nnz > 0)
+            HIPCHK(hipMemcpyAsync(lp.ci, d.ci, size_t(d.nnz) * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+        HIPCHK(hipStreamSynchronize(s));
+        auto* h = new spsyrk_plan_s;
+        h->p = lp;
+        if (al) {
+            h->al = *al;
+            h->has_al = true;
+        }
+        for (void* q : {static_cast<void*>(lp.rp), static_cast<void*>(lp.ci), static_cast<void*>(lp.run),
+                        static_cast<void*>(lp.prod), static_cast<void*>(lp.cx.key), lp.cx.val,
+                        static_cast<void*>(lp.vsrc), static_cast<void*>(lp.heavy_rows),
+                        static_cast<void*>(lp.heavy_nnz), static_cast<void*>(lp.cursor),
+                        static_cast<void*>(lp.ctl), static_cast<void*>(lp.c_rp)})
+            if (q) h->bufs.push_back(q);
+        made = h;
+    });
+    if (st == SPSYRK_OK) *plan = made;
+    return st;
+}
+
+spsyrk_status spsyrk_lower_execute(spsyrk_plan* plan, const void* values, const spsyrk_allocator* al,
+                                   void* hip_stream, spsyrk_csr_out* C) {
+    return guarded(C, al, hip_stream, [&](Arena& ar, hipStream_t s) {
+        if (!plan) {
+            set_detail("plan is null");
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        const LowerPlan& P = plan->p;
+        if ((P.sr == kF64 || P.sr == kF32) && P.nnz > 0 && !values) {
+            set_detail("values are required for plus-times semirings");
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        lower_execute(P, values, ar, s, C);
+        spsyrk_stats st{};
+        st.nnz_out = C->nnz;
+        st.heavy_rows = P.nheavy;
+        st.light_rows = P.m - P.nheavy;
+        g_stats = st;
+        g_stats_valid = true;
+    });
+}
+
+spsyrk_status spsyrk_plan_destroy(spsyrk_plan* plan) {
+    if (!plan) return SPSYRK_OK;
+    if (plan->has_al) {
+        if (plan->al.free)
+            for (void* q : plan->bufs) plan->al.free(plan->al.ctx, q);
+    } else {
+        (void)hipDeviceSynchronize();
+        for (void* q : plan->bufs) (void)hipFree(q);
+    }
+    delete plan;
+    return SPSYRK_OK;
 }
 
 spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const spsyrk_allocator* al,

@@ -35,7 +35,7 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
                                                bool drop_last, int gs, int rowbits, int lenbits, int64_t ngroups,
                                                const int64_t* __restrict__ nkept, const int64_t* __restrict__ rp_b,
                                                uint32_t* __restrict__ key, void* __restrict__ val,
-                                               uint32_t* __restrict__ gptr) {
+                                               uint32_t* __restrict__ gptr, uint32_t* __restrict__ vsrc) {
     __shared__ int64_t colstart[kPTile];
     __shared__ uint32_t excl[kPTile];  // column starts before each position
     __shared__ int64_t wt[kWavesPerBlock];
@@ -143,6 +143,7 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
             q = p - cols_before;
         }
         key[q] = ((col & gmask) << rowbits) | row;
+        if (vsrc) vsrc[q] = sent[p];
         if constexpr (JAC) {
             const uint32_t lf = lenbits > 0 ? field >> rowbits : lmax;
             static_cast<int32_t*>(val)[q] = lf < lmax ? int32_t(lf) : int32_t(rp_b[row + 1] - rp_b[row]);
@@ -172,7 +173,7 @@ size_t colindex_tmp_bytes(int64_t n) {
 
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries, bool drop_last,
                     int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits, ColIndex& cx, void* tmp,
-                    int64_t* d_nkept, uint2* run, hipStream_t s) {
+                    int64_t* d_nkept, uint2* run, hipStream_t s, uint32_t* vsrc) {
     const int64_t ntp = (n_entries + kPTile - 1) / kPTile;
     uint32_t* tbase = static_cast<uint32_t*>(tmp);
     char* after = static_cast<char*>(tmp) + ((size_t(ntp + 1) * 4 + 255) & ~size_t(255));
@@ -194,7 +195,7 @@ void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* 
     kept_count<<<1, 1, 0, s>>>(n, ncols, drop_last, d_nkept);
 #define SPSYRK_PACK(VBv, JACv)                                                                                    \
     pack<VBv, JACv><<<np, kBlock, 0, s>>>(scol, srow, sent, vals_b, run, n, tbase, drop_last, cx.gs, cx.rowbits,  \
-                                          lenbits, cx.ngroups, d_nkept, rp_b, cx.key, cx.val, cx.gptr)
+                                          lenbits, cx.ngroups, d_nkept, rp_b, cx.key, cx.val, cx.gptr, vsrc)
     if (sr == kJaccard)
         SPSYRK_PACK(0, true);
     else if (vbytes_in == 8)

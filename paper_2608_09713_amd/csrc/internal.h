@@ -84,6 +84,7 @@ struct LocalPack {
     bool drop_last = false;
     int64_t* kept = nullptr;
     uint32_t* ccount = nullptr;  // non-null (zeroed, one per column): entries of every column
+    uint32_t* vsrc = nullptr;    // non-null: the entry index of every written position
 };
 // pk non-null: write the column index as above when the local path is taken
 // and return -1 (no sorted copy); otherwise as described.
@@ -103,7 +104,8 @@ int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_
 size_t colindex_tmp_bytes(int64_t n);
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries,
                     bool drop_last, int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits,
-                    ColIndex& ci, void* tmp, int64_t* d_nkept, uint2* run, hipStream_t s);
+                    ColIndex& ci, void* tmp, int64_t* d_nkept, uint2* run, hipStream_t s,
+                    uint32_t* vsrc = nullptr);
 
 // ---- light.hip
 struct LightArgs {
@@ -174,6 +176,8 @@ void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, vo
 // Row pointers of rows [r0, r0 + m) of a CSR matrix, rebased to start at 0
 // (out: m + 1 words).
 void rebase_rows(const int64_t* rp, int64_t r0, int64_t m, int64_t* out, hipStream_t s);
+// dst[p] = src[idx[p]] for p < n, elements of vb (4 or 8) bytes.
+void gather_values(void* dst, const void* src, const uint32_t* idx, int64_t n, int vb, hipStream_t s);
 // ci[p] += off for p < nnz.
 void shift_columns(int32_t* ci, int64_t nnz, int32_t off, hipStream_t s);
 // Off-diagonal partner runs: run[e] = {cptr[ci[e]], cptr[ci[e] + 1]}.

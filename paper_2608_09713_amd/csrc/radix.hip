@@ -539,6 +539,7 @@ template <int VB, bool JAC>
 __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t field, uint32_t ent, int64_t cstart,
                                   typename ValT<VB>::T v, bool last, uint32_t col) {
     if (pk.ccount && last) pk.ccount[col] = uint32_t(pos - cstart + 1);
+    if (pk.vsrc) pk.vsrc[pos] = ent;
     const uint32_t rowmask = pk.rowbits >= 32 ? 0xffffffffu : ((1u << pk.rowbits) - 1u);
     const uint32_t row = field & rowmask;
     pk.key[pos] = row;

@@ -292,7 +292,26 @@ __global__ __launch_bounds__(kBlock) void shift_columns_kernel(int32_t* __restri
         ci[p] += off;
 }
 
+template <typename T>
+__global__ __launch_bounds__(kBlock) void gather_kernel(T* __restrict__ dst, const T* __restrict__ src,
+                                                        const uint32_t* __restrict__ idx, int64_t n) {
+    for (int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x; p < n; p += int64_t(gridDim.x) * kBlock)
+        dst[p] = src[idx[p]];
+}
+
 }  // namespace
+
+void gather_values(void* dst, const void* src, const uint32_t* idx, int64_t n, int vb, hipStream_t s) {
+    if (n <= 0) return;
+    int64_t blocks = (n + kBlock - 1) / kBlock;
+    if (blocks > 65536) blocks = 65536;
+    if (vb == 8)
+        gather_kernel<uint64_t><<<unsigned(blocks), kBlock, 0, s>>>(static_cast<uint64_t*>(dst),
+                                                                     static_cast<const uint64_t*>(src), idx, n);
+    else
+        gather_kernel<uint32_t><<<unsigned(blocks), kBlock, 0, s>>>(static_cast<uint32_t*>(dst),
+                                                                     static_cast<const uint32_t*>(src), idx, n);
+}
 
 void rebase_rows(const int64_t* rp, int64_t r0, int64_t m, int64_t* out, hipStream_t s) {
     rebase_rows_kernel<<<unsigned((m + 1 + kBlock - 1) / kBlock), kBlock, 0, s>>>(rp, r0, m, out);

@@ -213,3 +213,26 @@ def test_accumulate_full_columns_split(dev):
     n = full.nnz
     assert torch.equal(acc.col_idx[:n], full.col_idx[:n])
     assert torch.equal(acc.values[:n], full.values[:n])
+
+
+@pytest.mark.parametrize("name", ["jaccard_large", "offdiag_f64"])
+def test_plan_execute_full(dev, name):
+    # a plan at full size: an execution with new values equals the one-shot
+    # product of those values bit for bit
+    import torch
+    w = W.make(name, 1, 0)
+    A, sr = w["A"], w["semiring"]
+    print(f"[full plan {name}] m={A.nrows} nnz={A.nnz}", flush=True)
+    plan, C = sp.lower_plan(upload(A, sr, dev), sr)
+    del C
+    rng = np.random.default_rng(9)
+    B = A.with_values(rng.random(A.nnz) + 0.5) if VDT[sr] else A
+    Bd = upload(B, sr, dev)
+    E = plan.execute(Bd.values)
+    L = sp.lower(Bd, sr)
+    assert E.nnz == L.nnz
+    assert torch.equal(E.row_ptr, L.row_ptr)
+    n = L.nnz
+    assert torch.equal(E.col_idx[:n], L.col_idx[:n])
+    assert torch.equal(E.values[:n].view(torch.uint8), L.values[:n].view(torch.uint8))
+    plan.close()

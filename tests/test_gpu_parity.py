@@ -374,6 +374,58 @@ def test_lower_accumulate(dev, semiring):
     np.testing.assert_array_equal(ci2, cil)
 
 
+def _with_long_rows(rng, m, n):
+    # short random rows plus a few long ones (heavy rows: many products)
+    A = _rows_csr(rng, m, n, 6)
+    D = np.zeros((m, n), dtype=bool)
+    r = np.repeat(np.arange(m), np.diff(A.row_ptr))
+    D[r, A.col_idx] = True
+    for i in rng.choice(m, size=6, replace=False):
+        D[i, rng.choice(n, size=min(n, 400), replace=False)] = True
+    return csr_from_dense(np.where(D, rng.random((m, n)) + 0.5, 0.0), pattern=D)
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+@pytest.mark.parametrize("local", [False, True])
+def test_plan_execute(dev, semiring, local, monkeypatch):
+    # the two-phase use: a plan from one set of values, executions with new
+    # values of the same pattern; each equals the one-shot product of those
+    # values (bit for bit for counts and Jaccard) and the oracle to the usual
+    # bar.  local: the column
+    # sort's local path (the entry behind each index position comes from it)
+    import torch
+    if local:
+        monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
+    rng = np.random.default_rng(49)
+    vdt = VDT[semiring]
+    A = _with_long_rows(rng, 900, 1200)
+    print(f"[plan {semiring} local={local}] m={A.nrows} nnz={A.nnz}", flush=True)
+    plan, C0 = sp.lower_plan(upload(A, semiring, dev), semiring)
+    compare_full(C0, oracle.lower(A.with_values(A.values.astype(vdt) if vdt else None), semiring), semiring, "plan")
+    assert sp.stats()["heavy_rows"] > 0
+    for t in range(2):
+        B = A.with_values(rng.standard_normal(A.nnz))
+        Bd = upload(B, semiring, dev)
+        E = plan.execute(Bd.values)
+        L = sp.lower(Bd, semiring)
+        assert E.nnz == L.nnz
+        assert torch.equal(E.row_ptr, L.row_ptr)
+        assert torch.equal(E.col_idx[: E.nnz], L.col_idx[: L.nnz])
+        if vdt is None:  # (plus-times sums of heavy rows may end in other bits from run to run)
+            assert torch.equal(E.values[: E.nnz].view(torch.uint8), L.values[: L.nnz].view(torch.uint8))
+        compare_full(E, oracle.lower(B.with_values(B.values.astype(vdt) if vdt else None), semiring), semiring,
+                     f"execute {t}")
+    plan.close()
+
+
+def test_plan_of_empty_matrix(dev):
+    A = CSR(5, 7, np.zeros(6, np.int64), np.zeros(0, np.int32), np.zeros(0))
+    plan, C = sp.lower_plan(upload(A, "f64", dev), "f64")
+    E = plan.execute(upload(A, "f64", dev).values)
+    assert C.nnz == 0 and E.nnz == 0 and E.nrows == 5
+    plan.close()
+
+
 def test_lower_accumulate_rejects_jaccard(dev):
     A = random_csr(np.random.default_rng(48), 10, 10, 0.3)
     C = sp.lower(upload(A, "jaccard", dev), "jaccard")
