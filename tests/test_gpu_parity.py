@@ -220,9 +220,11 @@ def test_workloads_reduced(dev, name, shift):
     sr = w["semiring"]
     C = run_lower(A, sr, dev, f"{name}>>{shift}")
     if "mirror" in w["ops"]:
+        # the device's C_L mirrored, against the oracle's own C_L mirrored (the
+        # workloads' values are positive: the entries' bar is relative)
         M = sp.mirror(C, sr)
-        rp, ci, v = C.to_host()
-        ref = oracle.mirror(A.nrows, rp, ci, v)
+        L = oracle.lower(A.with_values(A.values.astype(VDT[sr]) if VDT[sr] else None), sr)
+        ref = oracle.mirror(A.nrows, L.row_ptr, L.col_idx, L.values)
         compare_full(M, ref, "count" if sr == "count" else sr, f"{name} mirror")
     if "offdiag" in w["ops"]:
         Ai, Aj = w["A"], w["B"]
@@ -478,8 +480,9 @@ def test_mirror_matches_oracle(dev, semiring):
     A = random_csr(rng, 400, 600, 0.02, signed=False)
     C = sp.lower(upload(A, semiring, dev), semiring)
     M = sp.mirror(C, semiring)
-    rp, ci, v = C.to_host()
-    ref = oracle.mirror(A.nrows, rp, ci, v)
+    vdt = VDT[semiring]
+    L = oracle.lower(A.with_values(A.values.astype(vdt) if vdt is not None else None), semiring)
+    ref = oracle.mirror(A.nrows, L.row_ptr, L.col_idx, L.values)
     compare_full(M, ref, "count" if semiring == "count" else semiring, "mirror")
     # offdiag(A, A) is the full product: same structure as the mirror
     O = sp.offdiag(upload(A, semiring, dev), upload(A, semiring, dev), semiring)
@@ -530,8 +533,8 @@ def test_mirror_structure_only(dev):
     C_nov = sp.DeviceCSR(C.nrows, C.ncols, C.row_ptr, C.col_idx, None, C.nnz)
     M = sp.mirror(C_nov, "count")
     assert M.values is None
-    rp, ci, v = C.to_host()
-    ref = oracle.mirror(A.nrows, rp, ci, v)
+    L = oracle.lower(A.with_values(None), "count")
+    ref = oracle.mirror(A.nrows, L.row_ptr, L.col_idx, L.values)
     np.testing.assert_array_equal(M.to_host()[0], ref.row_ptr)
     np.testing.assert_array_equal(M.to_host()[1], ref.col_idx)
     del torch
