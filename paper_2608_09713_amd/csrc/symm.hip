@@ -4,9 +4,9 @@
 // the diagonal, C_L(i, j) X(i, :) to Y(j, :) (the vector-times-matrix term
 // X^T C_L, transposed); the diagonal counts once, which is the - D X.
 //
-// One pass over C_L in tiles of consecutive entries; every thread walks a
-// stretch of kPerS entries row by row (rows found in an LDS window of the row
-// pointers, as the row-product kernel does).  The row term is summed per row
+// One pass over C_L in tiles of consecutive entries; every group of lanes
+// walks a stretch of entries row by row (rows found in an LDS window of the
+// row pointers, as the row-product kernel does), one lane per column of X.  The row term is summed per row
 // stretch and added once; the transposed term is a scatter of atomic adds.
 // Everything accumulates in double in a zeroed m x k workspace, which a last
 // pass rounds into Y.
@@ -16,8 +16,7 @@
 namespace spsyrk {
 namespace {
 
-constexpr int kPerS = 8;                  // entries per thread
-constexpr int kTileS = kBlock * kPerS;    // entries per workgroup
+constexpr int kTileS = 2048;              // entries per workgroup
 constexpr int kWinS = 1024;               // rows held in LDS
 
 __device__ inline int64_t last_leq_s(const int64_t* a, int64_t lo, int64_t hi, int64_t x) {
@@ -32,12 +31,20 @@ __device__ inline int64_t last_leq_s(const int64_t* a, int64_t lo, int64_t hi, i
     return lo;
 }
 
-// columns [q0, q0 + KB) of X and of the workspace W (m x k, row-major)
+// Columns [q0, q0 + KB) of X and of the workspace W (m x k, row-major).  The
+// workgroup's tile is split into kBlock / KB groups of KB lanes; a group
+// walks a stretch of consecutive entries and its lane q takes column q0 + q,
+// so the KB columns of an entry are gathered, and added to, as one
+// contiguous run of a row of X and of W.
 template <typename V, typename XT, int KB>
 __global__ __launch_bounds__(kBlock) void symm_kernel(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
                                                       const int32_t* __restrict__ ci, const V* __restrict__ cv,
                                                       const int64_t* __restrict__ trow, const XT* __restrict__ x,
                                                       int64_t ldx, int64_t k, int64_t q0, double* __restrict__ w) {
+    constexpr int kGroups = kBlock / KB;
+    constexpr int kPerG = kTileS / kGroups;  // entries per group
+    constexpr int kBatch = 8;                // entries whose loads are issued together
+    static_assert(kPerG % kBatch == 0, "whole batches");
     __shared__ int64_t win[kWinS + 1];
     __shared__ int64_t bounds[2];
     const int64_t e0 = int64_t(blockIdx.x) * kTileS;
@@ -53,61 +60,44 @@ __global__ __launch_bounds__(kBlock) void symm_kernel(const int64_t* __restrict_
     if (staged)
         for (int64_t t = threadIdx.x; t <= rhi - rlo + 1 && rlo + t <= m; t += kBlock) win[t] = rp[rlo + t];
     __syncthreads();
-    const int64_t a = e0 + int64_t(threadIdx.x) * kPerS;
-    const int64_t b = min(e1, a + kPerS);
+    const int g = threadIdx.x / KB, q = threadIdx.x % KB;
+    const int64_t a = e0 + int64_t(g) * kPerG;
+    const int64_t b = min(e1, a + kPerG);
     if (a >= b) return;
-    // the stretch's columns and values, loaded together
-    int32_t cj[kPerS];
-    double cvv[kPerS];
-#pragma unroll
-    for (int u = 0; u < kPerS; ++u) {
-        cj[u] = a + u < b ? ci[a + u] : 0;
-        cvv[u] = a + u < b ? double(cv[a + u]) : 0.0;
-    }
-    // X rows of the stretch's columns, gathered together (up to two columns
-    // per entry held ahead; wider blocks read them in the loop)
-    constexpr int KP = KB <= 2 ? KB : 1;
-    double xj[kPerS][KP];
-#pragma unroll
-    for (int u = 0; u < kPerS; ++u)
-#pragma unroll
-        for (int q = 0; q < KP; ++q) xj[u][q] = a + u < b ? double(x[int64_t(cj[u]) * ldx + q0 + q]) : 0.0;
     int64_t r = staged ? rlo + last_leq_s(win, 0, rhi - rlo, a) : last_leq_s(rp, rlo, rhi, a);
     int64_t rend = staged ? win[r - rlo + 1] : rp[r + 1];
-    double xi[KB], dot[KB];
+    double xi = double(x[r * ldx + q0 + q]);
+    double dot = 0.0;
+    for (int64_t a0 = a; a0 < b; a0 += kBatch) {
+        int32_t cj[kBatch];
+        double cvv[kBatch], xj[kBatch];
 #pragma unroll
-    for (int q = 0; q < KB; ++q) {
-        xi[q] = double(x[r * ldx + q0 + q]);
-        dot[q] = 0.0;
-    }
-    for (int u = 0; u < kPerS; ++u) {
-        const int64_t e = a + u;
-        if (e >= b) break;
-        if (e >= rend) {
-            // the row ends inside the stretch: add its row term
+        for (int u = 0; u < kBatch; ++u) {
+            const bool in = a0 + u < b;
+            cj[u] = in ? ci[a0 + u] : 0;
+            cvv[u] = in ? double(cv[a0 + u]) : 0.0;
+        }
 #pragma unroll
-            for (int q = 0; q < KB; ++q) atomicAdd(&w[r * k + q0 + q], dot[q]);
-            do {  // the row of e (empty rows add nothing)
-                ++r;
-                rend = staged && r - rlo + 1 <= rhi - rlo + 1 ? win[r - rlo + 1] : rp[r + 1];
-            } while (rend <= e);
-#pragma unroll
-            for (int q = 0; q < KB; ++q) {
-                xi[q] = double(x[r * ldx + q0 + q]);
-                dot[q] = 0.0;
+        for (int u = 0; u < kBatch; ++u) xj[u] = a0 + u < b ? double(x[int64_t(cj[u]) * ldx + q0 + q]) : 0.0;
+        for (int u = 0; u < kBatch; ++u) {
+            const int64_t e = a0 + u;
+            if (e >= b) break;
+            if (e >= rend) {
+                // the row ends inside the stretch: add its row term
+                atomicAdd(&w[r * k + q0 + q], dot);
+                do {  // the row of e (empty rows add nothing)
+                    ++r;
+                    rend = staged && r <= rhi ? win[r - rlo + 1] : rp[r + 1];
+                } while (rend <= e);
+                xi = double(x[r * ldx + q0 + q]);
+                dot = 0.0;
             }
-        }
-        const int64_t j = cj[u];
-        const double c = cvv[u];
-#pragma unroll
-        for (int q = 0; q < KB; ++q) {
-            const double xv = q < KP ? xj[u][q < KP ? q : 0] : double(x[j * ldx + q0 + q]);
-            dot[q] += c * xv;
-            if (j != r) atomicAdd(&w[j * k + q0 + q], c * xi[q]);
+            const int64_t j = cj[u];
+            dot += cvv[u] * xj[u];
+            if (j != r) atomicAdd(&w[j * k + q0 + q], cvv[u] * xi);
         }
     }
-#pragma unroll
-    for (int q = 0; q < KB; ++q) atomicAdd(&w[r * k + q0 + q], dot[q]);
+    atomicAdd(&w[r * k + q0 + q], dot);
 }
 
 __global__ __launch_bounds__(kBlock) void zero_f64(double* __restrict__ p, int64_t n) {
