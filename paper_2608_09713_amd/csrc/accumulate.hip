@@ -15,6 +15,13 @@ namespace spsyrk {
 namespace {
 
 constexpr int kRowsPerBlock = kWavesPerBlock;  // one row per wavefront
+constexpr int kLdsRow = 512;                    // column ids of a list held in LDS
+
+__device__ inline void wave_sync_acc() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
 template <int SR>
 struct AccVal {
@@ -57,13 +64,25 @@ __global__ __launch_bounds__(kBlock) void merge_rows(int64_t m, const int64_t* _
                                                      const int64_t* __restrict__ crp, int32_t* __restrict__ cci,
                                                      void* __restrict__ cv) {
     using V = typename AccVal<SR>::T;
+    __shared__ int32_t la[kRowsPerBlock][kLdsRow];
+    __shared__ int32_t lb[kRowsPerBlock][kLdsRow];
     const int lane = lane_id();
-    const int64_t i = int64_t(blockIdx.x) * kRowsPerBlock + threadIdx.x / kWave;
+    const int wv = threadIdx.x / kWave;
+    const int64_t i = int64_t(blockIdx.x) * kRowsPerBlock + wv;
     if (i >= m) return;  // (whole wavefronts)
     const int64_t pa = prp[i], na = prp[i + 1] - pa;
     const int64_t ta = trp[i], nb = trp[i + 1] - ta;
     const int32_t* a = pci + pa;
     const int32_t* b = tci + ta;
+    if (na <= kLdsRow && nb <= kLdsRow) {
+        // short lists: staged in LDS by coalesced loads; the searches and the
+        // merge below then read LDS
+        for (int64_t t = lane; t < na; t += kWave) la[wv][t] = a[t];
+        for (int64_t t = lane; t < nb; t += kWave) lb[wv][t] = b[t];
+        wave_sync_acc();
+        a = la[wv];
+        b = lb[wv];
+    }
     // the merge with duplicates kept, in equal parts over the lanes
     const int64_t total = na + nb;
     const int64_t per = (total + kWave - 1) / kWave;
