@@ -84,6 +84,33 @@ def test_host_side_errors(lib):
     assert lib.spsyrk_last_stats(ctypes.byref(st)) == 1  # no successful call yet on this thread
 
 
+def test_host_side_errors_of_the_other_calls(lib):
+    # the half blocks, the product from C_L, stage accumulation and plans
+    # check their arguments before any device work
+    o = sp._CsrOut()
+    a, b = _csr(4, 5, 1, v=1), _csr(3, 5, 1, v=1)
+    assert lib.spsyrk_offdiag_half(ctypes.byref(a), ctypes.byref(b), 2, 0, None, None, ctypes.byref(o)) == 1
+    assert b"half" in lib.spsyrk_last_error_detail()
+    b6 = _csr(3, 6, 1, v=1)
+    assert lib.spsyrk_offdiag_half(ctypes.byref(a), ctypes.byref(b6), 0, 0, None, None, ctypes.byref(o)) == 1
+    c = _csr(4, 4, 1, v=1)
+    assert lib.spsyrk_symm(None, 0, 1, 1, 1, 1, 1, None, None) == 1
+    assert lib.spsyrk_symm(ctypes.byref(_csr(4, 5, 1, v=1)), 0, 1, 1, 1, 1, 1, None, None) == 1
+    assert b"square" in lib.spsyrk_last_error_detail()
+    assert lib.spsyrk_symm(ctypes.byref(c), 0, 2, 1, 1, 1, 2, None, None) == 1   # ldx < k
+    assert lib.spsyrk_symm(ctypes.byref(c), 0, -1, 1, 1, 1, 1, None, None) == 1  # k < 0
+    assert lib.spsyrk_lower_accumulate(ctypes.byref(c), ctypes.byref(c), 3, None, None, ctypes.byref(o)) == 1
+    assert b"Jaccard" in lib.spsyrk_last_error_detail()
+    assert lib.spsyrk_lower_accumulate(ctypes.byref(c), ctypes.byref(_csr(5, 4, 1, v=1)), 0, None, None,
+                                       ctypes.byref(o)) == 1
+    assert lib.spsyrk_lower_execute(None, 1, None, None, ctypes.byref(o)) == 1
+    assert lib.spsyrk_plan_destroy(None) == 0
+    h = ctypes.c_void_p()
+    assert lib.spsyrk_lower_plan(None, 0, None, None, ctypes.byref(h), ctypes.byref(o)) == 1
+    assert not h.value
+    assert lib.spsyrk_lower_plan(ctypes.byref(c), 0, None, None, None, ctypes.byref(o)) == 1
+
+
 def test_binding_refuses_to_run_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(sp, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(sp, "_lib", None)
