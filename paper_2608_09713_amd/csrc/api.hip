@@ -1198,24 +1198,43 @@ spsyrk_status spsyrk_lower_accumulate(const spsyrk_csr* C_prev, const spsyrk_csr
         T.rp = t.row_ptr;
         T.ci = t.col_idx;
         T.v = t.values;
-        // union of the two patterns, row by row: counts, row pointers, merge
-        int64_t* cnt = ar.get_t<int64_t>(m + 1);
-        HIPCHK(hipMemsetAsync(cnt + m, 0, sizeof(int64_t), s));
-        merge_lower(false, int(sr), m, P, T, cnt, nullptr, nullptr, nullptr, s);
+        // union of the two patterns, in chunks of rows and windows of long
+        // rows: counts, row pointers, merge
+        int64_t* fl = ar.get_t<int64_t>(m + 1);
+        void* stmp = ar.get(scan_tmp_bytes(m + 1));
+        merge_item_flags(m, P, T, fl, stmp, s);
+        check_launch();
+        const int64_t items = m > 0 ? read_i64(fl + m, s) : 0;
+        int64_t* crow = ar.get_t<int64_t>(items + 1);
+        int32_t* cwin = ar.get_t<int32_t>(items > 0 ? items : 1);
+        int64_t* wsum = ar.get_t<int64_t>(items > 0 ? items : 1);
+        merge_item_table(m, P, T, fl, crow, cwin, s);
+        check_launch();
+        int64_t* cnt = fl;  // the item counts are spent (same stream)
+        HIPCHK(hipMemsetAsync(cnt, 0, sizeof(int64_t) * size_t(m + 1), s));
+        merge_lower(false, int(sr), items, crow, cwin, P, T, cnt, wsum, nullptr, nullptr, nullptr, s);
         check_launch();
         int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
-        void* stmp = ar.get(scan_tmp_bytes(m + 1));
         scan_i64(cnt, c_rp, m + 1, nullptr, stmp, s);
         check_launch();
-        const int64_t total = m > 0 ? read_i64(c_rp + m, s) : 0;
         ar.release(stmp);
+        if (items > 0) {
+            void* wtmp = ar.get(scan_tmp_bytes(items));
+            scan_i64(wsum, wsum, items, nullptr, wtmp, s);
+            check_launch();
+            ar.release(wtmp);
+        }
+        const int64_t total = m > 0 ? read_i64(c_rp + m, s) : 0;
         const int vb = out_value_bytes(int(sr));
         int32_t* c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
         void* c_val = ar.get(size_t(total > 0 ? total : 1) * vb, true);
-        merge_lower(true, int(sr), m, P, T, nullptr, c_rp, c_ci, c_val, s);
+        merge_lower(true, int(sr), items, crow, cwin, P, T, nullptr, wsum, c_rp, c_ci, c_val, s);
         check_launch();
         HIPCHK(hipStreamSynchronize(s));
-        ar.release(cnt);
+        ar.release(wsum);
+        ar.release(cwin);
+        ar.release(crow);
+        ar.release(fl);
         ar.release_output(t.row_ptr);
         ar.release_output(t.col_idx);
         ar.release_output(t.values);

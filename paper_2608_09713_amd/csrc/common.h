@@ -77,6 +77,33 @@ __device__ inline T block_exclusive_scan(T v, T* warp_tot, T* total) {
     return off + inc - v;
 }
 
+// maximum of v over the threads before this one in the workgroup (0 for the
+// first thread); *all gets the maximum over every thread
+__device__ inline uint32_t block_exclusive_max(uint32_t v, uint32_t* wt, uint32_t* all) {
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    uint32_t inc = v;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t u = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc = max(inc, u);
+    }
+    if (lane == kWave - 1) wt[w] = inc;
+    __syncthreads();
+    uint32_t before = 0, mx = 0;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) {
+        const uint32_t t = wt[q];
+        if (q < w) before = max(before, t);
+        mx = max(mx, t);
+    }
+    __syncthreads();
+    const uint32_t prev = __shfl_up(inc, 1, kWave);
+    if (lane > 0) before = max(before, prev);
+    *all = mx;
+    return before;
+}
+
 // Exclusive scan in place of an LDS array of length n (any n) by the whole
 // block; returns the total.  `warp_tot` is LDS scratch of kWavesPerBlock.
 template <typename T>

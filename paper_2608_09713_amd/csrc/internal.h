@@ -230,11 +230,22 @@ void heavy_symbolic(const HeavyArgs& a, int* queue, hipStream_t s);
 void heavy_numeric(const HeavyArgs& a, int* queue, hipStream_t s);
 
 // ---- accumulate.hip
-// Row-wise union of two lower parts P and T (m rows, canonical): write false
-// sets cnt[i] = distinct columns of row i; write true writes the merged rows
-// (columns ascending, shared entries summed) at crp.  sr: F64, F32 or COUNT.
-void merge_lower(bool write, int sr, int64_t m, const DevCsr& P, const DevCsr& T, int64_t* cnt, const int64_t* crp,
-                 int32_t* cci, void* cv, hipStream_t s);
+// Row-wise union of two lower parts P and T (m rows, canonical), in work items
+// of at most a few thousand entries: chunks of short rows and windows of long
+// rows.  merge_item_flags leaves an exclusive scan of the per-row item counts
+// in fl (m + 1 words; the number of items in fl[m]; scan_tmp:
+// scan_tmp_bytes(m + 1)).  merge_item_table then writes the item table: crow
+// (items + 1 words), cwin (items words).  merge_lower with write false sets
+// cnt[i] = distinct columns of row i (cnt zeroed before) and wsum[q] = the
+// count of item q if it is a window, else 0; with wsum scanned (exclusive) and
+// write true it writes the merged rows (columns ascending, shared entries
+// summed) at crp.  sr: F64, F32 or COUNT.
+void merge_item_flags(int64_t m, const DevCsr& P, const DevCsr& T, int64_t* fl, void* scan_tmp, hipStream_t s);
+void merge_item_table(int64_t m, const DevCsr& P, const DevCsr& T, const int64_t* fl, int64_t* crow, int32_t* cwin,
+                      hipStream_t s);
+void merge_lower(bool write, int sr, int64_t items, const int64_t* crow, const int32_t* cwin, const DevCsr& P,
+                 const DevCsr& T, int64_t* cnt, int64_t* wsum, const int64_t* crp, int32_t* cci, void* cv,
+                 hipStream_t s);
 
 // ---- symm.hip
 // Y = C X with C = C_L + C_L^T - D from the stored lower part C (canonical,

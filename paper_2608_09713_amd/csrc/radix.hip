@@ -553,33 +553,6 @@ __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t fie
     if (pk.run && pos > cstart) pk.run[ent] = make_uint2(uint32_t(cstart), uint32_t(pos));
 }
 
-// maximum of v over the threads before this one in the workgroup (0 for the
-// first thread); *all gets the maximum over every thread
-__device__ inline uint32_t block_exclusive_max(uint32_t v, uint32_t* wt, uint32_t* all) {
-    const int lane = lane_id();
-    const int w = threadIdx.x / kWave;
-    uint32_t inc = v;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t u = __shfl_up(inc, d, kWave);
-        if (lane >= d) inc = max(inc, u);
-    }
-    if (lane == kWave - 1) wt[w] = inc;
-    __syncthreads();
-    uint32_t before = 0, mx = 0;
-#pragma unroll
-    for (int q = 0; q < kWavesPerBlock; ++q) {
-        const uint32_t t = wt[q];
-        if (q < w) before = max(before, t);
-        mx = max(mx, t);
-    }
-    __syncthreads();
-    const uint32_t prev = __shfl_up(inc, 1, kWave);
-    if (lane > 0) before = max(before, prev);
-    *all = mx;
-    return before;
-}
-
 template <int VB, bool JAC>
 __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
                                                           uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,

@@ -376,6 +376,32 @@ def test_lower_accumulate(dev, semiring):
     np.testing.assert_array_equal(ci2, cil)
 
 
+def _chunk_case(rng, m, n, hub_rows):
+    # sparse rows, a hub column shared by hub_rows rows (their lower rows grow
+    # past what a chunk of the merge holds), 2600 consecutive empty rows (more
+    # than a chunk's row limit) and a few more empty rows
+    D = rng.random((m, n)) < 0.002
+    D[2000:4600] = False
+    D[rng.choice(m, size=hub_rows, replace=False), 0] = True
+    D[rng.choice(m, size=40, replace=False), :] = False
+    return csr_from_dense(np.where(D, rng.standard_normal((m, n)), 0.0), pattern=D)
+
+
+@pytest.mark.parametrize("semiring", ["f64", "f32", "count"])
+def test_lower_accumulate_chunks(dev, semiring):
+    # the merge's chunks of rows: long rows alone in a chunk (up to 3000
+    # entries of the two parts), chunks cut by the row limit, empty rows
+    rng = np.random.default_rng(49)
+    vdt = VDT[semiring]
+    cast = (lambda A: A.with_values(A.values.astype(vdt))) if vdt is not None else (lambda A: A.with_values(None))
+    A1, A2 = _chunk_case(rng, 6000, 300, 1500), _chunk_case(rng, 6000, 300, 1500)
+    print(f"[accumulate chunks {semiring}] m=6000", flush=True)
+    R1 = oracle.lower(cast(A1), semiring)
+    C1 = sp.lower(upload(A1, semiring, dev), semiring)
+    C2 = sp.lower_accumulate(C1, upload(A2, semiring, dev), semiring)
+    compare_full(C2, oracle.lower_accumulate(R1, cast(A2), semiring), semiring, "chunks")
+
+
 def _with_long_rows(rng, m, n):
     # short random rows plus a few long ones (heavy rows: many products)
     A = _rows_csr(rng, m, n, 6)
