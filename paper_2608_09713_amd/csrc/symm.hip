@@ -10,6 +10,16 @@
 // stretch and added once; the transposed term is a scatter of atomic adds.
 // Everything accumulates in double in a zeroed m x k workspace, which a last
 // pass rounds into Y.
+//
+// For a single column (the product with a vector) the transposed term's
+// random atomic adds miss in L2 and bound the whole pass, so they are
+// bucketed instead: rows of Y are grouped in buckets of 2^12 to 2^14 rows; a counting
+// pass sizes every (bucket, workgroup) stretch of a bucket-major record array,
+// the row pass writes each term as a record (row in the bucket, value) into
+// its stretch, and a last pass sums every bucket's records in LDS and adds
+// the sums to the workspace.
+#include <cstdlib>
+
 #include "common.h"
 #include "internal.h"
 
@@ -100,6 +110,159 @@ __global__ __launch_bounds__(kBlock) void symm_kernel(const int64_t* __restrict_
     atomicAdd(&w[r * k + q0 + q], dot);
 }
 
+// Rows of Y per bucket: 2^BITS, BITS from 12 to 14 picked so that there are
+// at most 256 buckets where possible (a workgroup's records of one bucket
+// then form stretches of 256 or more); at most kMaxBkts buckets.
+constexpr int kMaxBkts = 1024;
+constexpr int kSub = 32;                        // tiles of kTileS entries per bucketing workgroup
+constexpr int64_t kPart = 65536;                // records summed per workgroup
+
+// Entries [blk * kSub * kTileS, +kSub * kTileS) of workgroup blk: the count of
+// its entries per bucket of their column, cnt[bucket * nblk + blk].  Every
+// entry counts, the diagonal too (its record holds zero).
+template <int BITS>
+__global__ __launch_bounds__(kBlock) void bucket_count(const int32_t* __restrict__ ci, int64_t nnz, int nbk,
+                                                       int64_t nblk, int64_t* __restrict__ cnt) {
+    __shared__ uint32_t h[kMaxBkts];
+    for (int b = threadIdx.x; b < nbk; b += kBlock) h[b] = 0;
+    __syncthreads();
+    const int64_t e0 = int64_t(blockIdx.x) * kSub * kTileS;
+    const int64_t e1 = min(nnz, e0 + int64_t(kSub) * kTileS);
+    for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) atomicAdd(&h[ci[e] >> BITS], 1u);
+    __syncthreads();
+    for (int b = threadIdx.x; b < nbk; b += kBlock) cnt[int64_t(b) * nblk + blockIdx.x] = h[b];
+}
+
+// The row pass for one column with the transposed terms written as records:
+// kSub tiles of kTileS entries per workgroup, one thread per stretch of
+// entries as in symm_kernel.  boff: the exclusive scan of bucket_count's
+// counts, so that this workgroup's records of bucket b go to
+// [boff[b * nblk + blk], ...), claimed through LDS cursors.
+template <typename V, typename XT, int BITS>
+__global__ __launch_bounds__(kBlock) void symm_records(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
+                                                       const int32_t* __restrict__ ci, const V* __restrict__ cv,
+                                                       const int64_t* __restrict__ trow, const XT* __restrict__ x,
+                                                       int64_t ldx, double* __restrict__ w,
+                                                       const int64_t* __restrict__ boff, int nbk, int64_t nblk,
+                                                       uint16_t* __restrict__ rj, double* __restrict__ rv) {
+    constexpr int kPerG = kTileS / kBlock;  // entries per thread and tile
+    constexpr int kBatch = 8;
+    static_assert(kPerG % kBatch == 0, "whole batches");
+    __shared__ int64_t cur[kMaxBkts];
+    __shared__ int64_t win[kWinS + 1];
+    __shared__ int64_t bounds[2];
+    for (int b = threadIdx.x; b < nbk; b += kBlock) cur[b] = boff[int64_t(b) * nblk + blockIdx.x];
+    const int64_t ntiles = (nnz + kTileS - 1) / kTileS;
+    for (int sub = 0; sub < kSub; ++sub) {
+        const int64_t tile = int64_t(blockIdx.x) * kSub + sub;
+        if (tile >= ntiles) break;  // uniform over the workgroup
+        const int64_t e0 = tile * kTileS;
+        const int64_t e1 = min(nnz, e0 + kTileS);
+        __syncthreads();  // the previous tile's window is spent; the cursors are set
+        if (threadIdx.x == 0) {
+            const int64_t lo = trow[tile];
+            bounds[0] = lo;
+            bounds[1] = e1 < nnz ? trow[tile + 1] : last_leq_s(rp, lo, m, e1 - 1);
+        }
+        __syncthreads();
+        const int64_t rlo = bounds[0], rhi = bounds[1];
+        const bool staged = rhi - rlo + 1 <= kWinS;
+        if (staged)
+            for (int64_t t = threadIdx.x; t <= rhi - rlo + 1 && rlo + t <= m; t += kBlock) win[t] = rp[rlo + t];
+        __syncthreads();
+        const int64_t a = e0 + int64_t(threadIdx.x) * kPerG;
+        const int64_t b = min(e1, a + kPerG);
+        if (a >= b) continue;
+        int64_t r = staged ? rlo + last_leq_s(win, 0, rhi - rlo, a) : last_leq_s(rp, rlo, rhi, a);
+        int64_t rend = staged ? win[r - rlo + 1] : rp[r + 1];
+        double xi = double(x[r * ldx]);
+        double dot = 0.0;
+        for (int64_t a0 = a; a0 < b; a0 += kBatch) {
+            int32_t cj[kBatch];
+            double cvv[kBatch], xj[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const bool in = a0 + u < b;
+                cj[u] = in ? ci[a0 + u] : 0;
+                cvv[u] = in ? double(cv[a0 + u]) : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) xj[u] = a0 + u < b ? double(x[int64_t(cj[u]) * ldx]) : 0.0;
+            for (int u = 0; u < kBatch; ++u) {
+                const int64_t e = a0 + u;
+                if (e >= b) break;
+                if (e >= rend) {
+                    atomicAdd(&w[r], dot);
+                    do {
+                        ++r;
+                        rend = staged && r <= rhi ? win[r - rlo + 1] : rp[r + 1];
+                    } while (rend <= e);
+                    xi = double(x[r * ldx]);
+                    dot = 0.0;
+                }
+                const int64_t j = cj[u];
+                dot += cvv[u] * xj[u];
+                const int64_t slot = atomicAdd(reinterpret_cast<unsigned long long*>(&cur[j >> BITS]), 1ull);
+                rj[slot] = uint16_t(j & ((1 << BITS) - 1));
+                rv[slot] = j != r ? cvv[u] * xi : 0.0;
+            }
+        }
+        atomicAdd(&w[r], dot);
+    }
+}
+
+// Records [p * kPart, +kPart) of the bucket-major array: each bucket's part
+// summed in LDS, then added to its rows of the workspace.
+template <int BITS>
+__global__ __launch_bounds__(kBlock) void bucket_sum(const int64_t* __restrict__ boff, int nbk, int64_t nblk,
+                                                     int64_t nrec, const uint16_t* __restrict__ rj,
+                                                     const double* __restrict__ rv, double* __restrict__ w) {
+    constexpr int kBkt = 1 << BITS;
+    __shared__ double acc[kBkt];
+    __shared__ int first;
+    const int64_t s0 = int64_t(blockIdx.x) * kPart, s1 = min(nrec, s0 + kPart);
+    if (threadIdx.x == 0) {
+        int lo = 0, hi = nbk - 1;  // the last bucket starting at or before s0
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (boff[int64_t(mid) * nblk] <= s0)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        first = lo;
+    }
+    __syncthreads();
+    for (int b = first; b < nbk; ++b) {
+        const int64_t bs = boff[int64_t(b) * nblk];
+        if (bs >= s1) break;  // uniform over the workgroup
+        const int64_t be = b + 1 < nbk ? boff[int64_t(b + 1) * nblk] : nrec;
+        const int64_t lo = max(s0, bs), hi = min(s1, be);
+        if (lo >= hi) continue;
+        for (int t = threadIdx.x; t < kBkt; t += kBlock) acc[t] = 0.0;
+        __syncthreads();
+        constexpr int kU = 4;
+        for (int64_t s = lo + threadIdx.x; s < hi; s += int64_t(kBlock) * kU) {
+            uint16_t jj[kU];
+            double vv[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int64_t q = s + int64_t(u) * kBlock;
+                jj[u] = q < hi ? rj[q] : 0;
+                vv[u] = q < hi ? rv[q] : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u)
+                if (s + int64_t(u) * kBlock < hi) atomicAdd(&acc[jj[u]], vv[u]);
+        }
+        __syncthreads();
+        const int64_t r0 = int64_t(b) << BITS;
+        for (int t = threadIdx.x; t < kBkt; t += kBlock)
+            if (acc[t] != 0.0) atomicAdd(&w[r0 + t], acc[t]);
+        __syncthreads();
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void zero_f64(double* __restrict__ p, int64_t n) {
     for (int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x; i < n; i += int64_t(gridDim.x) * kBlock) p[i] = 0.0;
 }
@@ -141,20 +304,110 @@ void launch_symm(const DevCsr& C, const XT* x, int64_t ldx, int64_t k, double* w
     }
 }
 
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+// The transposed term of a single column goes through buckets when its
+// workspace outgrows one XCD's L2 (4 MiB: 2^19 rows), where random atomic adds
+// miss, up to 2^21 rows: past that the buckets are too many for a workgroup's
+// stretches of records to fill whole cache lines, and the scattered record
+// writes cost as much as the atomic adds.  SPSYRK_SYMM_BUCKETS (read at every call) = 0 turns buckets off; = 1
+// takes them for every single column of up to 2^24 rows; = 12, 13 or 14 does
+// the same with buckets of 2^12, 2^13 or 2^14 rows.
+int forced_bits() {
+    const char* e = std::getenv("SPSYRK_SYMM_BUCKETS");
+    if (!e) return -1;
+    const int v = std::atoi(e);
+    return v == 0 || v == 1 || (v >= 12 && v <= 14) ? v : -1;
+}
+
+bool bucketed(int64_t m, int64_t k, int64_t nnz) {
+    if (k != 1 || nnz <= 0 || m > (int64_t(1) << 24)) return false;
+    const int f = forced_bits();
+    if (f == 0) return false;
+    return f > 0 || (m > (int64_t(1) << 19) && m <= (int64_t(1) << 21));
+}
+
+int bucket_bits(int64_t m) {
+    const int f = forced_bits();
+    if (f >= 12) return f;
+    const int lg = bit_width_u64(uint64_t(m - 1));  // ceil(log2 m)
+    return lg - 8 < 12 ? 12 : (lg - 8 > 14 ? 14 : lg - 8);
+}
+
+struct BucketLayout {
+    int bits;
+    int nbk;
+    int64_t nblk;
+    size_t boff, stmp, rj, rv, end;  // byte offsets after the workspace and the tile rows
+};
+
+BucketLayout bucket_layout(int64_t m, int64_t nnz, size_t base) {
+    BucketLayout L;
+    L.bits = bucket_bits(m);
+    L.nbk = int((m + (int64_t(1) << L.bits) - 1) >> L.bits);
+    const int64_t ntiles = (nnz + kTileS - 1) / kTileS;
+    L.nblk = (ntiles + kSub - 1) / kSub;
+    const int64_t ncnt = int64_t(L.nbk) * L.nblk;
+    L.boff = base;
+    L.stmp = L.boff + align256(size_t(ncnt) * sizeof(int64_t));
+    L.rj = L.stmp + align256(scan_tmp_bytes(ncnt));
+    L.rv = L.rj + align256(size_t(nnz) * sizeof(uint16_t));
+    L.end = L.rv + size_t(nnz) * sizeof(double);
+    return L;
+}
+
+size_t symm_base_bytes(int64_t m, int64_t k, int64_t nnz) {
+    return align256(size_t(m) * size_t(k) * sizeof(double)) +
+           align256(size_t((nnz + kTileS - 1) / kTileS + 1) * sizeof(int64_t));
+}
+
+template <typename V, typename XT, int BITS>
+void launch_bucketed_bits(const DevCsr& C, const XT* x, int64_t ldx, double* w, const int64_t* trow, char* tmp,
+                          const BucketLayout& L, hipStream_t s) {
+    int64_t* boff = reinterpret_cast<int64_t*>(tmp + L.boff);
+    uint16_t* rj = reinterpret_cast<uint16_t*>(tmp + L.rj);
+    double* rv = reinterpret_cast<double*>(tmp + L.rv);
+    bucket_count<BITS><<<unsigned(L.nblk), kBlock, 0, s>>>(C.ci, C.nnz, L.nbk, L.nblk, boff);
+    scan_i64(boff, boff, int64_t(L.nbk) * L.nblk, nullptr, tmp + L.stmp, s);
+    symm_records<V, XT, BITS><<<unsigned(L.nblk), kBlock, 0, s>>>(C.rp, C.m, C.nnz, C.ci,
+                                                                   static_cast<const V*>(C.v), trow, x, ldx, w, boff,
+                                                                   L.nbk, L.nblk, rj, rv);
+    const unsigned np = unsigned((C.nnz + kPart - 1) / kPart);
+    bucket_sum<BITS><<<np, kBlock, 0, s>>>(boff, L.nbk, L.nblk, C.nnz, rj, rv, w);
+}
+
+template <typename V, typename XT>
+void launch_bucketed(const DevCsr& C, const XT* x, int64_t ldx, double* w, const int64_t* trow, char* tmp,
+                     const BucketLayout& L, hipStream_t s) {
+    switch (L.bits) {
+        case 12: launch_bucketed_bits<V, XT, 12>(C, x, ldx, w, trow, tmp, L, s); break;
+        case 13: launch_bucketed_bits<V, XT, 13>(C, x, ldx, w, trow, tmp, L, s); break;
+        default: launch_bucketed_bits<V, XT, 14>(C, x, ldx, w, trow, tmp, L, s); break;
+    }
+}
+
 }  // namespace
 
 size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz) {
-    const size_t wb = (size_t(m) * size_t(k) * sizeof(double) + 255) & ~size_t(255);
-    return wb + size_t((nnz + kTileS - 1) / kTileS + 1) * sizeof(int64_t);
+    const size_t base = symm_base_bytes(m, k, nnz);
+    return bucketed(m, k, nnz) ? bucket_layout(m, nnz, base).end : base;
 }
 
 void symm_product(const DevCsr& C, int sr, const void* x, int64_t ldx, int64_t k, void* y, int64_t ldy, void* tmp,
                   hipStream_t s) {
     double* w = static_cast<double*>(tmp);
-    const size_t wb = (size_t(C.m) * size_t(k) * sizeof(double) + 255) & ~size_t(255);
-    int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + wb);
+    int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + align256(size_t(C.m) * size_t(k) * sizeof(double)));
     zero_f64<<<grid_for(C.m * k), kBlock, 0, s>>>(w, C.m * k);
-    if (C.nnz > 0) {
+    if (bucketed(C.m, k, C.nnz)) {
+        tile_first_rows(C.rp, C.m, kTileS, trow, s);
+        const BucketLayout L = bucket_layout(C.m, C.nnz, symm_base_bytes(C.m, k, C.nnz));
+        char* t = static_cast<char*>(tmp);
+        switch (sr) {
+            case kF64: launch_bucketed<double, double>(C, static_cast<const double*>(x), ldx, w, trow, t, L, s); break;
+            case kCount: launch_bucketed<int32_t, double>(C, static_cast<const double*>(x), ldx, w, trow, t, L, s); break;
+            default: launch_bucketed<float, float>(C, static_cast<const float*>(x), ldx, w, trow, t, L, s); break;
+        }
+    } else if (C.nnz > 0) {
         tile_first_rows(C.rp, C.m, kTileS, trow, s);
         switch (sr) {
             case kF64: launch_symm<double, double>(C, static_cast<const double*>(x), ldx, k, w, trow, s); break;

@@ -493,6 +493,37 @@ def test_symm_matches_oracle(dev, semiring):
     _check_symm(y[:, None], ref, scale, semiring, "symm vector")
 
 
+@pytest.mark.parametrize("semiring,bits", [("f64", "12"), ("f32", "13"), ("count", "14"), ("jaccard", "12"),
+                                           ("f64", "0")])
+def test_symm_vector_buckets(dev, semiring, bits, monkeypatch):
+    # the product with one column with its transposed term bucketed (forced at
+    # this size; buckets of 2^12 to 2^14 rows, so 3 to 1 of them), several
+    # counting workgroups and summing parts, empty rows; and with buckets off
+    import torch
+    monkeypatch.setenv("SPSYRK_SYMM_BUCKETS", bits)
+    rng = np.random.default_rng(50)
+    vdt = VDT[semiring]
+    xdt = np.float64 if semiring in ("f64", "count") else np.float32
+    A = _rows_csr(rng, 12000, 4000, 5)
+    A = A.with_values(rng.standard_normal(A.nnz))
+    keep = np.ones(A.nrows, dtype=bool)
+    keep[rng.choice(A.nrows, size=300, replace=False)] = False
+    D = np.zeros(A.nrows + 1, dtype=np.int64)
+    lens = np.diff(A.row_ptr) * keep
+    np.cumsum(lens, out=D[1:])
+    sel = np.repeat(keep, np.diff(A.row_ptr))
+    A = CSR(A.nrows, A.ncols, D, A.col_idx[sel], A.values[sel])
+    Ah = A.with_values(A.values.astype(vdt) if vdt is not None else None)
+    C = sp.lower(upload(A, semiring, dev), semiring)
+    L = oracle.lower(Ah, semiring)
+    print(f"[symm buckets {semiring} {bits}] m={A.nrows} nnz_L={L.nnz}", flush=True)
+    assert L.nnz > 3 * 65536
+    x = rng.standard_normal(A.nrows).astype(xdt)
+    y = sp.symm(C, torch.from_numpy(x).to(dev), semiring).cpu().numpy()
+    ref, scale = _symm_ref(L, x.astype(np.float64)[:, None])
+    _check_symm(y[:, None], ref, scale, semiring, "symm buckets")
+
+
 def test_symm_rejects_upper_entries(dev):
     import torch
     P = csr_from_dense(np.array([[1.0, 2.0], [0.0, 3.0]]))
