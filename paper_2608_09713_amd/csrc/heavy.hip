@@ -10,7 +10,8 @@
 // LDS over the compacted ranks (tiles of kAcc ranks), so the accumulator only
 // spans columns that occur.  Every partner run is sorted by row, so each run
 // is consumed front to back through a per-entry cursor: a short stretch of a
-// run by one lane, a long one by a whole wavefront over contiguous keys.
+// run by a group of kGrp lanes, a long one by a whole wavefront, both over
+// contiguous keys.
 //
 // The symbolic pass builds the bitmaps only and counts the row's columns; the
 // numeric pass rebuilds them, writes the column indices and the values.
@@ -26,6 +27,7 @@ constexpr int kHW = kHB / kWave;         // wavefronts per workgroup
 constexpr int kChunkE = 1024;            // entries examined per activity round
 constexpr int kLongU = 2;                // keys per lane per step of a long walk
 constexpr int kHeavyGroups = 1024;       // workgroups of a heavy-row launch
+constexpr int kGrp = 8;                  // lanes per short stretch of a walk
 
 // Output columns per window and ranks per value tile: the symbolic pass
 // holds a 32 KiB bitmap; the numeric pass a 16 KiB bitmap, the words' ranks
@@ -95,8 +97,8 @@ __global__ __launch_bounds__(kHB, NUM ? 4 : 8) void heavy_kernel(HeavyArgs a, in
     // Walk the partner runs of entries [c0, c1) from their cursors through
     // the partners below column B1 (and, for values, of rank below T0 + tl):
     // mark them in the bitmap, or add their terms to the value tile.  Short
-    // stretches (under a wavefront of partners) are walked by one lane each,
-    // long ones by whole wavefronts.  The cursors move if advance is set.
+    // stretches (under a wavefront of partners) are walked by groups of kGrp
+    // lanes, long ones by whole wavefronts.  The cursors move if advance is set.
     // Called by all threads.
     auto walk = [&](int64_t c0, int64_t c1, int64_t B0, int64_t B1, bool value, uint32_t T0, uint32_t tl,
                     bool advance) {
@@ -124,45 +126,45 @@ __global__ __launch_bounds__(kHB, NUM ? 4 : 8) void heavy_kernel(HeavyArgs a, in
         }
         __syncthreads();
         const int nshort = nshort_s, nlong = nlong_s;
-        // short stretches: one lane each, four keys per round
-        for (int q = tid; q < nshort; q += kHB) {
-            const int64_t e = c0 + act_short[q];
-            uint32_t c = a.cursor[e];
-            const uint32_t hi = a.run[e].y;
-            double av = 0.0;
-            if constexpr (kVal) av = value ? double(static_cast<const In*>(a.val)[e]) : 0.0;
-            bool stop = false;
-            while (!stop) {
-                uint32_t jj[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) jj[u] = c + u < hi ? (key[c + u] & rowmask) : 0xffffffffu;
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (stop) break;
-                    if (c >= hi || int64_t(jj[u]) >= B1) {
-                        stop = true;
-                        break;
-                    }
-                    const uint32_t x = uint32_t(int64_t(jj[u]) - B0);
-                    if (value) {
-                        const uint32_t rk = rank_of(B0, jj[u]);
-                        if (rk >= rlim || rk < T0) {
-                            stop = true;
-                            break;
+        // short stretches: a group of kGrp lanes each, kGrp consecutive keys
+        // per step (the keys in range form a prefix of the stretch)
+        {
+            const int gl = lane % kGrp;
+            for (int q = tid / kGrp; q < nshort; q += kHB / kGrp) {
+                const int64_t e = c0 + act_short[q];
+                uint32_t c = a.cursor[e];
+                const uint32_t hi = a.run[e].y;
+                double av = 0.0;
+                if constexpr (kVal) av = value ? double(static_cast<const In*>(a.val)[e]) : 0.0;
+                while (c < hi) {
+                    const uint32_t p = c + uint32_t(gl);
+                    const uint32_t jj = p < hi ? (key[p] & rowmask) : 0xffffffffu;
+                    bool in = false;
+                    if (int64_t(jj) < B1) {
+                        const uint32_t x = uint32_t(int64_t(jj) - B0);
+                        if (value) {
+                            const uint32_t rk = rank_of(B0, jj);
+                            in = rk >= T0 && rk < rlim;
+                            if (in) {
+                                if constexpr (NUM) {
+                                    if constexpr (kVal)
+                                        atomicAdd(&acc[rk - T0], av * double(static_cast<const In*>(a.cx.val)[p]));
+                                    else
+                                        atomicAdd(&acc[rk - T0], 1);
+                                }
+                            }
+                        } else {
+                            in = true;
+                            atomicOr(&bits[x >> 5], 1u << (x & 31));
                         }
-                        if constexpr (NUM) {
-                            if constexpr (kVal)
-                                atomicAdd(&acc[rk - T0], av * double(static_cast<const In*>(a.cx.val)[c]));
-                            else
-                                atomicAdd(&acc[rk - T0], 1);
-                        }
-                    } else {
-                        atomicOr(&bits[x >> 5], 1u << (x & 31));
                     }
-                    ++c;
+                    const uint64_t bal = __ballot(in);
+                    const uint32_t took = uint32_t(__popcll((bal >> (lane - gl)) & ((uint64_t(1) << kGrp) - 1)));
+                    c += took;
+                    if (took < uint32_t(kGrp)) break;
                 }
+                if (advance && gl == 0) a.cursor[e] = c;
             }
-            if (advance) a.cursor[e] = c;
         }
         // long stretches: a wavefront each, kLongU keys per lane per step
         for (int q = w; q < nlong; q += kHW) {
