@@ -323,7 +323,8 @@ def main():
             roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": ach / HBM_PEAK_GBS, "traffic": tr, "kernel": dom,
                     "kernel_avg_ms": ms / n, "alg_bytes_per_launch": ab}
-    phase_ms = {k: v[0] / v[1] for k, v in phases.items()}
+    phase_ms = {k: v[0] / v[1] for k, v in phases.items()}            # per launch of the phase
+    phase_ms_step = {k: v[0] / args.steps for k, v in phases.items()}  # per step (all its launches)
 
     line = {
         "metric": METRIC,
@@ -348,6 +349,7 @@ def main():
                                     "frac": B_alg / t_step / 1e9 / HBM_PEAK_GBS},
         "roofline": roof,
         "phase_ms": phase_ms,
+        "phase_ms_per_step": phase_ms_step,
         "library_stats": st,
         "kernel_source_hash": kernel_source_hash(),
     }

@@ -24,18 +24,20 @@ namespace {
 
 constexpr int kHB = 512;                 // threads per workgroup
 constexpr int kHW = kHB / kWave;         // wavefronts per workgroup
-constexpr int kChunkE = 1024;            // entries examined per activity round
+constexpr int kChunkE = 512;             // entries examined per activity round
 constexpr int kLongU = 2;                // keys per lane per step of a long walk
 constexpr int kHeavyGroups = 1024;       // workgroups of a heavy-row launch
 constexpr int kGrp = 8;                  // lanes per short stretch of a walk
 
 // Output columns per window and ranks per value tile: the symbolic pass
-// holds a 32 KiB bitmap; the numeric pass a 16 KiB bitmap, the words' ranks
-// and a 32 KiB value tile.
+// holds a 32 KiB bitmap; the numeric pass an 8 KiB bitmap, the words' ranks
+// and a 32 KiB value tile, about 52 KiB with the activity lists, so that three
+// workgroups share a compute unit (with 16 KiB bitmaps only two fit, and rows
+// wait longer on their walks' latency).
 template <int SR, bool NUM>
 struct HeavyCfg {
     using Acc = typename SrTraits<SR>::Acc;
-    static constexpr int kWin = NUM ? (1 << 17) : (1 << 18);
+    static constexpr int kWin = NUM ? (1 << 16) : (1 << 18);
     static constexpr int kWords = kWin / 32;
     static constexpr int kAcc = 32768 / int(sizeof(Acc));
 };
