@@ -386,10 +386,16 @@ def symm(C_lower: DeviceCSR, X, semiring="f64"):
 
 def mirror(C_lower: DeviceCSR, semiring="f64") -> DeviceCSR:
     """C = C_L + C_L^T - D from a stored lower part (spsyrk_mirror)."""
+    import torch
     sr = _sr(semiring)
     a = _csr_struct(C_lower, sr, False)
-    return _call("spsyrk_mirror", lambda ar: (ctypes.byref(a), sr, ctypes.byref(ar.struct)), sr,
-                 C_lower.row_ptr.device)
+    C = _call("spsyrk_mirror", lambda ar: (ctypes.byref(a), sr, ctypes.byref(ar.struct)), sr,
+              C_lower.row_ptr.device)
+    if C.values is None and C_lower.values is not None:
+        # an empty C_L's values reach the library as a null pointer (a pattern
+        # without values); its mirror still has (no) values of the output type
+        C.values = torch.empty(0, dtype=getattr(torch, _OUT_DTYPE[sr]), device=C_lower.row_ptr.device)
+    return C
 
 
 def stats() -> dict:
