@@ -244,7 +244,13 @@ spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const
  * double and Y is rounded once; the sums are accumulated with atomic adds, so
  * their order (and the last bits of Y) may differ from run to run.
  * Workspace: m k doubles and a small tile table from the allocator, released
- * before return.  The call returns after Y is complete.
+ * before return; for one column (k = 1) of a matrix of 2^19 to 2^21 rows the
+ * transposed terms go through buckets of rows instead of atomic adds to
+ * random rows, which takes 10 bytes per entry of C_lower more (records of
+ * (row in bucket, value)) and a table of per-bucket counts.  The variable
+ * SPSYRK_SYMM_BUCKETS (read at every call) overrides that choice: 0 never,
+ * 1 for every single column of up to 2^24 rows, 12 to 14 the same with
+ * buckets of 2^12 to 2^14 rows.  The call returns after Y is complete.
  * Errors: INVALID_ARG (non-square C_lower, k < 0, ldx or ldy < k, null
  * arrays), NOT_CANONICAL (including an entry above the diagonal), SHAPE, OOM,
  * HIP.
