@@ -371,7 +371,7 @@ int rows_per_chunk(double) {
     return kFusedRows;
 }
 
-constexpr int64_t kDenseColumns = int64_t(1) << 26;  // dense column starts: at most 256 MB
+constexpr int64_t kDenseColumns = int64_t(1) << 28;  // dense column starts: at most 1 GiB
 
 // What a lower product keeps for later products with new values on the same
 // pattern: everything that depends on the pattern only (the column index and

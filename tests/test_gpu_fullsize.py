@@ -236,3 +236,21 @@ def test_plan_execute_full(dev, name):
     assert torch.equal(E.col_idx[:n], L.col_idx[:n])
     assert torch.equal(E.values[:n].view(torch.uint8), L.values[:n].view(torch.uint8))
     plan.close()
+
+
+def test_offdiag_self_full_wide_columns(dev):
+    # offdiag(A, A) of jaccard_large's pattern (2^28 columns: dense column
+    # starts of 1 GiB) is the full product: the mirror of the lower part,
+    # counts bit for bit
+    import torch
+    w = W.make("jaccard_large", 1, 0)
+    A = w["A"]
+    print(f"[full offdiag(A, A)] m={A.nrows} n={A.ncols} nnz={A.nnz}", flush=True)
+    Ad = upload(A, "count", dev)
+    O = sp.offdiag(Ad, Ad, "count")
+    M = sp.mirror(sp.lower(Ad, "count"), "count")
+    assert O.nnz == M.nnz
+    assert torch.equal(O.row_ptr, M.row_ptr)
+    n = O.nnz
+    assert torch.equal(O.col_idx[:n], M.col_idx[:n])
+    assert torch.equal(O.values[:n], M.values[:n])
