@@ -19,10 +19,11 @@
 namespace spsyrk {
 namespace {
 
-constexpr int kLong = 512;                  // a row with more entries (P and T together) is split in windows
-constexpr int kCapStart = 1536;             // a chunk starts where (offset in P + offset in T) / kCapStart changes
-constexpr int kChunk = kCapStart + kLong;   // entries of an item, at most
-constexpr int kRowCap = 2048;               // rows of a chunk, at most
+constexpr int kLong = 256;                  // a row with more entries (P and T together) is split in windows
+constexpr int kCapStart = 768;              // a chunk starts where (offset in P + offset in T) / kCapStart changes
+constexpr int kChunk = kCapStart + kLong;   // entries of an item, at most (1024: about 20 KB of LDS,
+                                            // so that eight workgroups share a compute unit)
+constexpr int kRowCap = 1024;               // rows of a chunk, at most
 static_assert(kRowCap <= kChunk, "the row marks' array holds the per-row counts");
 
 template <int SR>
