@@ -26,7 +26,7 @@
 namespace spsyrk {
 namespace {
 
-constexpr int kTileS = 2048;              // entries per workgroup
+constexpr int kTileS = 4096;              // entries per workgroup (16 per thread with one column)
 constexpr int kWinS = 1024;               // rows held in LDS
 
 __device__ inline int64_t last_leq_s(const int64_t* a, int64_t lo, int64_t hi, int64_t x) {
