@@ -42,9 +42,30 @@
  *   caller, who releases them with the same allocator.  On any error every
  *   allocation made by the call has been released and *C is zeroed.
  * - Work is ordered on hip_stream (a hipStream_t; NULL means the default
- *   stream).  A call blocks the host until it knows the output size; it
- *   returns with the output's row_ptr and nnz final and the remaining work
- *   enqueued on hip_stream (synchronise the stream before reading values).
+ *   stream).  A call returns with the output's row_ptr and nnz final and the
+ *   remaining work enqueued on hip_stream (synchronise the stream before
+ *   reading values).  Before that it blocks the host on hip_stream a fixed
+ *   number of times, each time to read a few words that size the buffers
+ *   that follow:
+ *     spsyrk_lower, spsyrk_lower_plan: 3 -- the validation word of A, the
+ *       row classes (heavy rows, staging size), the output size;
+ *       spsyrk_lower_plan waits once more for the plan's copies;
+ *     spsyrk_offdiag: 4 -- one validation word per operand, the row classes,
+ *       the output size (A_j with 2^28 columns or more: validation words,
+ *       the index size, the output size); spsyrk_offdiag_half: one more,
+ *       for the split row;
+ *     spsyrk_mirror: 3 -- the validation word, the strict-lower count and
+ *       the end of the call (when nnz(C_L) exceeds 2^31 the strict lower
+ *       part is transposed in column slabs: one column histogram per
+ *       refinement and one record count per slab instead of the count);
+ *     spsyrk_lower_accumulate: the validation word of C_prev, the three of
+ *       spsyrk_lower for the stage, the merge item count, the output size
+ *       and the end of the call;
+ *     spsyrk_symm: the validation word and the end of the call (Y is
+ *       complete on return);
+ *     spsyrk_lower_execute: none.
+ *   Validation must finish before any kernel reads the input's indices,
+ *   which is why it is read on the host first.
  * - Limits: nrows, ncols < 2^31 and, for the inputs of spsyrk_lower and
  *   spsyrk_offdiag, nnz < 2^31 (SPSYRK_ERR_SHAPE otherwise).  Output nnz and
  *   the nnz of spsyrk_mirror's input are int64 (below 2^62).
@@ -61,7 +82,7 @@
 extern "C" {
 #endif
 
-#define SPSYRK_ABI_VERSION 1
+#define SPSYRK_ABI_VERSION 2
 
 typedef enum spsyrk_status {
     SPSYRK_OK = 0,
@@ -104,15 +125,16 @@ typedef struct spsyrk_csr {
     const void* values;     /* [nnz] of double (F64) or float (F32); may be NULL for COUNT* */
 } spsyrk_csr;
 
-/* Output CSR (device arrays allocated by the call through the allocator). */
+/* Output CSR (device arrays allocated by the call through the allocator).
+ * col_idx and values hold exactly nnz entries (one allocated entry when nnz
+ * is 0, so that the pointers are never null on success). */
 typedef struct spsyrk_csr_out {
     int64_t nrows;
     int64_t ncols;
     int64_t nnz;            /* entries in the result */
-    int64_t capacity;       /* entries allocated in col_idx / values (>= nnz) */
     int64_t* row_ptr;       /* [nrows + 1] */
-    int32_t* col_idx;       /* [capacity] */
-    void* values;           /* [capacity] of the semiring's output type */
+    int32_t* col_idx;       /* [nnz] */
+    void* values;           /* [nnz] of the semiring's output type */
 } spsyrk_csr_out;
 
 /* Device-memory allocator.  alloc returns a device pointer aligned to at least
@@ -158,8 +180,10 @@ spsyrk_status spsyrk_offdiag(const spsyrk_csr* Ai, const spsyrk_csr* Aj, spsyrk_
  * and returns with the work enqueued on hip_stream.  The output has the
  * plan's structure and the semiring it was made with.
  * The plan's buffers come from the allocator passed to spsyrk_lower_plan
- * (hipMalloc when NULL) and stay allocated until spsyrk_plan_destroy, which
- * frees them with that allocator (or hipFree after a device synchronisation).
+ * (hipMallocAsync on that call's stream when NULL) and stay allocated until
+ * spsyrk_plan_destroy, which frees them with that allocator (with none: it
+ * waits for the plan's device, returns the buffers with hipFreeAsync on the
+ * null stream and waits for that).
  * Executions of one plan must not overlap (they share its counters and the
  * index's values); the plan may be used from any stream once the creating
  * call has returned.

@@ -46,8 +46,7 @@ class _Csr(ctypes.Structure):
 
 class _CsrOut(ctypes.Structure):
     _fields_ = [("nrows", ctypes.c_int64), ("ncols", ctypes.c_int64), ("nnz", ctypes.c_int64),
-                ("capacity", ctypes.c_int64), ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p),
-                ("values", ctypes.c_void_p)]
+                ("row_ptr", ctypes.c_void_p), ("col_idx", ctypes.c_void_p), ("values", ctypes.c_void_p)]
 
 
 _ALLOC = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t)
@@ -233,8 +232,8 @@ def _take_out(arena, out, sr):
     import torch
     odt = getattr(torch, _OUT_DTYPE[sr])
     rp = arena.take(out.row_ptr, torch.int64, out.nrows + 1)
-    ci = arena.take(out.col_idx, torch.int32, out.capacity)
-    v = arena.take(out.values, odt, out.capacity) if out.values else None
+    ci = arena.take(out.col_idx, torch.int32, out.nnz)
+    v = arena.take(out.values, odt, out.nnz) if out.values else None
     return DeviceCSR(out.nrows, out.ncols, rp, ci, v, out.nnz)
 
 

@@ -545,7 +545,6 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     C->nrows = m;
     C->ncols = R.m;
     C->nnz = total;
-    C->capacity = total;
     C->row_ptr = c_rp;
     C->col_idx = c_ci;
     C->values = c_val;
@@ -603,7 +602,6 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         C->col_idx = ar.get_t<int32_t>(1, true);
         C->values = ar.get(4 * 2, true);
         C->nnz = 0;
-        C->capacity = 0;
         HIPCHK(hipStreamSynchronize(s));
         g_stats = st;
         g_stats_valid = true;
@@ -709,7 +707,6 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     C->nrows = m;
     C->ncols = R.m;
     C->nnz = total;
-    C->capacity = total;
     C->row_ptr = c_rp;
     C->col_idx = c_ci;
     C->values = c_val;
@@ -891,7 +888,6 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     C->nrows = m;
     C->ncols = m;
     C->nnz = total;
-    C->capacity = total;
     C->row_ptr = f_rp;
     C->col_idx = f_ci;
     C->values = f_val;
@@ -976,7 +972,6 @@ void lower_execute(const LowerPlan& P, const void* vals, Arena& ar, hipStream_t 
     C->nrows = m;
     C->ncols = m;
     C->nnz = total;
-    C->capacity = total;
     C->row_ptr = c_rp;
     C->col_idx = c_ci;
     C->values = c_val;
@@ -1079,6 +1074,7 @@ struct spsyrk_plan_s {
     LowerPlan p;
     spsyrk_allocator al{};
     bool has_al = false;
+    int device = 0;           // the device the buffers live on
     std::vector<void*> bufs;  // device buffers owned by the plan
 };
 
@@ -1155,8 +1151,9 @@ spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t
             zero_ctl(ctl, s);
             validate(c, true, ar, ctl, s, "C_lower");
         }
-        void* tmp = ar.get(symm_tmp_bytes(m, k, c.nnz));
-        symm_product(c, int(sr), X, ldx, k, Y, ldy, tmp, s);
+        const bool buckets = symm_use_buckets(m, k, c.nnz);
+        void* tmp = ar.get(symm_tmp_bytes(m, k, c.nnz, buckets));
+        symm_product(c, int(sr), X, ldx, k, Y, ldy, tmp, buckets, s);
         check_launch();
         HIPCHK(hipStreamSynchronize(s));
     });
@@ -1241,7 +1238,6 @@ spsyrk_status spsyrk_lower_accumulate(const spsyrk_csr* C_prev, const spsyrk_csr
         C->nrows = m;
         C->ncols = m;
         C->nnz = total;
-        C->capacity = total;
         C->row_ptr = c_rp;
         C->col_idx = c_ci;
         C->values = c_val;
@@ -1272,8 +1268,11 @@ spsyrk_status spsyrk_lower_plan(const spsyrk_csr* A, spsyrk_semiring sr, const s
         if (d.nnz > 0)
             HIPCHK(hipMemcpyAsync(lp.ci, d.ci, size_t(d.nnz) * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
         HIPCHK(hipStreamSynchronize(s));
+        int device = 0;
+        HIPCHK(hipGetDevice(&device));
         auto* h = new spsyrk_plan_s;
         h->p = lp;
+        h->device = device;
         if (al) {
             h->al = *al;
             h->has_al = true;
@@ -1318,8 +1317,15 @@ spsyrk_status spsyrk_plan_destroy(spsyrk_plan* plan) {
         if (plan->al.free)
             for (void* q : plan->bufs) plan->al.free(plan->al.ctx, q);
     } else {
+        // the buffers came from hipMallocAsync: stream-ordered frees once the
+        // device is idle, then a wait so that they are released on return
+        int cur = 0;
+        (void)hipGetDevice(&cur);
+        (void)hipSetDevice(plan->device);
         (void)hipDeviceSynchronize();
-        for (void* q : plan->bufs) (void)hipFree(q);
+        for (void* q : plan->bufs) (void)hipFreeAsync(q, nullptr);
+        (void)hipStreamSynchronize(nullptr);
+        (void)hipSetDevice(cur);
     }
     delete plan;
     return SPSYRK_OK;

@@ -22,6 +22,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "symm_layout.h"
 
 namespace spsyrk {
 namespace {
@@ -113,7 +114,7 @@ __global__ __launch_bounds__(kBlock) void symm_kernel(const int64_t* __restrict_
 // Rows of Y per bucket: 2^BITS, BITS from 12 to 14 picked so that there are
 // at most 256 buckets where possible (a workgroup's records of one bucket
 // then form stretches of 256 or more); at most kMaxBkts buckets.
-constexpr int kMaxBkts = 1024;
+constexpr int kMaxBkts = kSymmMaxBuckets;
 constexpr int kSub = 32;                        // tiles of kTileS entries per bucketing workgroup
 constexpr int64_t kPart = 65536;                // records summed per workgroup
 
@@ -310,9 +311,10 @@ size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 // workspace outgrows one XCD's L2 (4 MiB: 2^19 rows), where random atomic adds
 // miss, up to 2^21 rows: past that the buckets are too many for a workgroup's
 // stretches of records to fill whole cache lines, and the scattered record
-// writes cost as much as the atomic adds.  SPSYRK_SYMM_BUCKETS (read at every call) = 0 turns buckets off; = 1
-// takes them for every single column of up to 2^24 rows; = 12, 13 or 14 does
-// the same with buckets of 2^12, 2^13 or 2^14 rows.
+// writes cost as much as the atomic adds.  SPSYRK_SYMM_BUCKETS (read at every
+// call) = 0 turns buckets off; = 1 takes them for every single column of up to
+// 2^24 rows; = 12, 13 or 14 does the same with buckets of 2^12, 2^13 or 2^14
+// rows, raised where needed to keep the buckets at most kSymmMaxBuckets.
 int forced_bits() {
     const char* e = std::getenv("SPSYRK_SYMM_BUCKETS");
     if (!e) return -1;
@@ -320,19 +322,7 @@ int forced_bits() {
     return v == 0 || v == 1 || (v >= 12 && v <= 14) ? v : -1;
 }
 
-bool bucketed(int64_t m, int64_t k, int64_t nnz) {
-    if (k != 1 || nnz <= 0 || m > (int64_t(1) << 24)) return false;
-    const int f = forced_bits();
-    if (f == 0) return false;
-    return f > 0 || (m > (int64_t(1) << 19) && m <= (int64_t(1) << 21));
-}
-
-int bucket_bits(int64_t m) {
-    const int f = forced_bits();
-    if (f >= 12) return f;
-    const int lg = bit_width_u64(uint64_t(m - 1));  // ceil(log2 m)
-    return lg - 8 < 12 ? 12 : (lg - 8 > 14 ? 14 : lg - 8);
-}
+bool bucketed(int64_t m, int64_t k, int64_t nnz) { return symm_bucketed(m, k, nnz, forced_bits()); }
 
 struct BucketLayout {
     int bits;
@@ -343,8 +333,8 @@ struct BucketLayout {
 
 BucketLayout bucket_layout(int64_t m, int64_t nnz, size_t base) {
     BucketLayout L;
-    L.bits = bucket_bits(m);
-    L.nbk = int((m + (int64_t(1) << L.bits) - 1) >> L.bits);
+    L.bits = symm_bucket_bits(m, forced_bits());
+    L.nbk = symm_bucket_count(m, L.bits);  // <= kMaxBkts whenever bucketed() holds
     const int64_t ntiles = (nnz + kTileS - 1) / kTileS;
     L.nblk = (ntiles + kSub - 1) / kSub;
     const int64_t ncnt = int64_t(L.nbk) * L.nblk;
@@ -388,17 +378,19 @@ void launch_bucketed(const DevCsr& C, const XT* x, int64_t ldx, double* w, const
 
 }  // namespace
 
-size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz) {
+bool symm_use_buckets(int64_t m, int64_t k, int64_t nnz) { return bucketed(m, k, nnz); }
+
+size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz, bool buckets) {
     const size_t base = symm_base_bytes(m, k, nnz);
-    return bucketed(m, k, nnz) ? bucket_layout(m, nnz, base).end : base;
+    return buckets ? bucket_layout(m, nnz, base).end : base;
 }
 
 void symm_product(const DevCsr& C, int sr, const void* x, int64_t ldx, int64_t k, void* y, int64_t ldy, void* tmp,
-                  hipStream_t s) {
+                  bool buckets, hipStream_t s) {
     double* w = static_cast<double*>(tmp);
     int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + align256(size_t(C.m) * size_t(k) * sizeof(double)));
     zero_f64<<<grid_for(C.m * k), kBlock, 0, s>>>(w, C.m * k);
-    if (bucketed(C.m, k, C.nnz)) {
+    if (buckets && C.nnz > 0) {
         tile_first_rows(C.rp, C.m, kTileS, trow, s);
         const BucketLayout L = bucket_layout(C.m, C.nnz, symm_base_bytes(C.m, k, C.nnz));
         char* t = static_cast<char*>(tmp);

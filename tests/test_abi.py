@@ -45,7 +45,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings_and_version(lib):
-    assert lib.spsyrk_abi_version() == 1
+    assert lib.spsyrk_abi_version() == 2
     for code in range(7):
         assert lib.spsyrk_status_string(code)
     assert lib.spsyrk_status_string(99) == b"unknown status"

@@ -67,6 +67,21 @@ def test_golden_on_gpu(dev):
     e = g["P"]["lower_jaccard"]
     want = (np.float32(e["numerator"]) / np.float32(e["denominator"])).view(np.uint32)
     np.testing.assert_array_equal(C.to_host()[2].view(np.uint32), want)
+    # off-diagonal block whose operands' rows differ in length
+    h = g["offdiag_jaccard_pair"]
+    Ai, Aj = (CSR(h[k]["nrows"], h[k]["ncols"], np.array(h[k]["row_ptr"]), np.array(h[k]["col_idx"], dtype=np.int32),
+                  None) for k in ("Ai", "Aj"))
+    for sr in ("count", "jaccard"):
+        C = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
+        rp, ci, v = C.to_host()
+        e = h["offdiag_" + sr]
+        np.testing.assert_array_equal(rp, e["row_ptr"])
+        np.testing.assert_array_equal(ci, e["col_idx"])
+        if sr == "count":
+            np.testing.assert_array_equal(v, e["values"])
+        else:
+            want = (np.float32(e["numerator"]) / np.float32(e["denominator"])).view(np.uint32)
+            np.testing.assert_array_equal(v.view(np.uint32), want)
 
 
 @pytest.mark.parametrize("semiring", SEMIRINGS)

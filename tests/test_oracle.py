@@ -89,6 +89,21 @@ def check_golden(lib=None):
     np.testing.assert_array_equal(R.col_idx, e["col_idx"])
     np.testing.assert_array_equal(R.values, np.float32(e["values"]))
 
+    # off-diagonal block with row lengths that differ between the operands:
+    # |S(j)| of the Jaccard denominator is the length of row j of A_j
+    h = g["offdiag_jaccard_pair"]
+    Ai, Aj = _csr(h["Ai"], values=False), _csr(h["Aj"], values=False)
+    for sr in ("count", "jaccard"):
+        R = oracle.offdiag(Ai, Aj, sr, lib=lib)
+        e = h["offdiag_" + sr]
+        np.testing.assert_array_equal(R.row_ptr, e["row_ptr"])
+        np.testing.assert_array_equal(R.col_idx, e["col_idx"])
+        if sr == "count":
+            np.testing.assert_array_equal(R.values, e["values"])
+        else:
+            want = np.float32(e["numerator"]) / np.float32(e["denominator"])
+            np.testing.assert_array_equal(R.values.view(np.uint32), want.view(np.uint32))
+
 
 def test_golden_hand_worked():
     check_golden()
@@ -150,14 +165,40 @@ def check_offdiag_brute(lib=None):
     for t in range(30):
         mi, mj = int(rng.integers(0, 30)), int(rng.integers(0, 30))
         n = int(rng.integers(1, 50))
+        # the two operands have different densities, so their row lengths differ
         Ai = random_csr(rng, mi, n, 0.15)
-        Aj = random_csr(rng, mj, n, 0.15)
+        Aj = random_csr(rng, mj, n, float(rng.choice([0.05, 0.3])))
         Di, Pi = dense_of(Ai)
         Dj, Pj = dense_of(Aj)
         R = oracle.offdiag(Ai, Aj, "f64", lib=lib)
         RD, RP = result_to_dense(R, mj)
-        np.testing.assert_array_equal(RP, (Pi.astype(int) @ Pj.T.astype(int)) > 0)
+        S = (Pi.astype(int) @ Pj.T.astype(int)) > 0
+        np.testing.assert_array_equal(RP, S)
         np.testing.assert_allclose(RD, Di @ Dj.T, rtol=1e-12, atol=1e-12)
+        # counts: the integer pattern product
+        cnt = Pi.astype(np.int64) @ Pj.T.astype(np.int64)
+        R = oracle.offdiag(Ai.with_values(None), Aj.with_values(None), "count", lib=lib)
+        RD, RP = result_to_dense(R, mj)
+        np.testing.assert_array_equal(RP, S)
+        np.testing.assert_array_equal(RD.astype(np.int64), cnt)
+        # Jaccard: c / (|S_i| + |S_j| - c) in float32, |S_i| a row length of
+        # A_i and |S_j| one of A_j (the rows of the two operands differ)
+        R = oracle.offdiag(Ai.with_values(None), Aj.with_values(None), "jaccard", lib=lib)
+        rows = np.repeat(np.arange(mi), np.diff(R.row_ptr))
+        c = cnt[rows, R.col_idx]
+        li, lj = np.diff(Ai.row_ptr), np.diff(Aj.row_ptr)
+        want = np.float32(c) / np.float32(li[rows] + lj[R.col_idx] - c)
+        np.testing.assert_array_equal(R.col_idx, np.nonzero(S)[1])
+        np.testing.assert_array_equal(R.values.view(np.uint32), want.astype(np.float32).view(np.uint32))
+        # fp32: inputs rounded to float32, one rounding of the exact sum
+        Ai32 = Ai.with_values(Ai.values.astype(np.float32))
+        Aj32 = Aj.with_values(Aj.values.astype(np.float32))
+        D32 = dense_of(Ai32.with_values(Ai32.values.astype(np.float64)))[0] @ \
+            dense_of(Aj32.with_values(Aj32.values.astype(np.float64)))[0].T
+        R = oracle.offdiag(Ai32, Aj32, "f32", lib=lib)
+        RD, RP = result_to_dense(R, mj)
+        np.testing.assert_array_equal(RP, S)
+        np.testing.assert_allclose(RD, D32.astype(np.float32), rtol=2e-7, atol=1e-30)
 
 
 def test_offdiag_brute_force():
@@ -419,6 +460,40 @@ def test_accumulate_is_concatenation():
                 np.testing.assert_allclose(acc.values, ref.values, rtol=1e-12, atol=1e-12)
 
 
+def test_accumulate_f32_is_one_float_addition():
+    # F32 stages (Sec. III-A, C_ii = sum_s SYRK(A_is)): each stage is rounded to
+    # float32 once, and an entry present in both parts is one correctly rounded
+    # float32 addition of the two float32 values (numpy float32 arithmetic);
+    # an entry in one part keeps its value.  Against the one-shot lower part of
+    # the concatenation the result stays within the fp32 bar.
+    rng = np.random.default_rng(33)
+    for m in (30, 1, 17):
+        A1 = random_csr(rng, m, 20, 0.2, dtype=np.float32, signed=False)
+        A2 = random_csr(rng, m, 25, 0.2, dtype=np.float32, signed=False)
+        P = oracle.lower(A1, "f32")
+        T = oracle.lower(A2, "f32")
+        acc = oracle.lower_accumulate(P, A2, "f32")
+        want = {}
+        for R in (P, T):
+            rows = np.repeat(np.arange(m), np.diff(R.row_ptr))
+            for i, j, v in zip(rows, R.col_idx, R.values):
+                key = (int(i), int(j))
+                want[key] = np.float32(want[key] + v) if key in want else np.float32(v)
+        keys = sorted(want)
+        rp = np.zeros(m + 1, dtype=np.int64)
+        np.cumsum(np.bincount([k[0] for k in keys], minlength=m), out=rp[1:])
+        np.testing.assert_array_equal(acc.row_ptr, rp)
+        np.testing.assert_array_equal(acc.col_idx, [k[1] for k in keys])
+        got = np.asarray(acc.values, dtype=np.float32)
+        np.testing.assert_array_equal(got.view(np.uint32),
+                                      np.array([want[k] for k in keys], dtype=np.float32).view(np.uint32))
+        ref = oracle.lower(_hcat(A1, A2).with_values(None), "count")
+        np.testing.assert_array_equal(acc.col_idx, ref.col_idx)
+        A = _hcat(A1, A2)
+        one = oracle.lower(A.with_values(A.values.astype(np.float32)), "f32")
+        np.testing.assert_allclose(got, one.values, rtol=1e-5, atol=0)
+
+
 def test_accumulate_from_empty():
     rng = np.random.default_rng(32)
     A = random_csr(rng, 25, 30, 0.12)
@@ -534,6 +609,10 @@ MUTANTS = {
     "jaccard_len_i_twice": ("const int64_t len_j = B.rp[j + 1] - B.rp[j];", "const int64_t len_j = len_i;"),
     "mirror_skips_transposed": ("if (ci[e] < r) full[ci[e]].push_back", "if (ci[e] < r - 1) full[ci[e]].push_back"),
     "count_double": ("s.count += 1u;", "s.count += 2u;"),
+    # off the diagonal, |S(j)| taken from the left operand A_i instead of A_j
+    # (kept in range: only where A_i has at least as many rows)
+    "jaccard_len_j_from_left": ("emit_row(*R, acc, sr, A.rp[i + 1] - A.rp[i], B);",
+                                "emit_row(*R, acc, sr, A.rp[i + 1] - A.rp[i], (lower || A.m < B.m) ? B : A);"),
 }
 
 
