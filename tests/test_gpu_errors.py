@@ -155,8 +155,8 @@ def test_oom_at_every_allocation_mirror_slabs(dev, monkeypatch):
 def test_oom_at_every_allocation_two_pass(dev, monkeypatch):
     monkeypatch.setenv("SPSYRK_TWO_PASS", "1")
     lib = sp.library()
-    a = _struct(_dev_csr(_hub_matrix(4), dev))
-    b = _struct(_dev_csr(_hub_matrix(5, m=300), dev))
+    dA, dB = _dev_csr(_hub_matrix(4), dev), _dev_csr(_hub_matrix(5, m=300), dev)  # kept alive
+    a, b = _struct(dA), _struct(dB)
     s = _stream()
     _sweep(dev, lambda al, o: lib.spsyrk_lower(ctypes.byref(a), 0, ctypes.byref(al.struct), s, ctypes.byref(o)),
            "lower two-pass")
@@ -190,7 +190,8 @@ def test_oom_at_every_allocation_accumulate(dev, semiring):
         A1, A2 = A1.with_values(None), A2.with_values(None)
     P = sp.lower(_dev_csr(A1, dev), semiring)
     p = _struct(P)
-    a = _struct(_dev_csr(A2, dev))
+    dA = _dev_csr(A2, dev)  # kept alive for the calls
+    a = _struct(dA)
     s = _stream()
     _sweep(dev, lambda al, o: lib.spsyrk_lower_accumulate(ctypes.byref(p), ctypes.byref(a), sr,
                                                           ctypes.byref(al.struct), s, ctypes.byref(o)),
@@ -201,7 +202,8 @@ def test_oom_at_every_allocation_plan_and_execute(dev):
     import torch
     lib = sp.library()
     A = _hub_matrix(9)
-    a = _struct(_dev_csr(A, dev))
+    dA = _dev_csr(A, dev)  # kept alive for the calls
+    a = _struct(dA)
     s = _stream()
     handles = []
 
@@ -209,17 +211,18 @@ def test_oom_at_every_allocation_plan_and_execute(dev):
         h = ctypes.c_void_p()
         rc = lib.spsyrk_lower_plan(ctypes.byref(a), 0, ctypes.byref(al.struct), s, ctypes.byref(h), ctypes.byref(o))
         if rc == 0:
-            handles.append((h, al))
+            handles.append((h, al, {o.row_ptr, o.col_idx, o.values}))
         else:
             assert not h.value, "a failed plan call handed out a plan"
         return rc
     _sweep(dev, plan, "lower_plan")
-    h, al_plan = handles[0]
+    h, al_plan, c_arrays = handles[0]
     vals = torch.from_numpy(A.values * 2.0).to(dev)
     _sweep(dev, lambda al, o: lib.spsyrk_lower_execute(h, ctypes.c_void_p(vals.data_ptr()), ctypes.byref(al.struct),
                                                        s, ctypes.byref(o)), "lower_execute")
     assert lib.spsyrk_plan_destroy(h) == 0
-    assert not al_plan.live, "plan buffers left after spsyrk_plan_destroy"
+    # what stays is C_L itself (the caller's); every plan buffer was released
+    assert set(al_plan.live) == c_arrays, "plan buffers left after spsyrk_plan_destroy"
 
 
 def _hip():
@@ -258,7 +261,8 @@ def test_null_allocator_lower_and_plan(dev):
     import torch
     lib = sp.library()
     A = _hub_matrix(10)
-    a = _struct(_dev_csr(A, dev))
+    dA = _dev_csr(A, dev)  # kept alive for the calls
+    a = _struct(dA)
     s = _stream()
     ref = oracle.lower(A, "f64")
     out = sp._CsrOut()
