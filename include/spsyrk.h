@@ -92,7 +92,8 @@ typedef enum spsyrk_status {
     SPSYRK_ERR_SHAPE = 3,         /* a dimension or nnz(A) is 2^31 or more */
     SPSYRK_ERR_OOM = 4,           /* the allocator returned NULL */
     SPSYRK_ERR_OVERFLOW = 5,      /* an internal count would overflow its integer type */
-    SPSYRK_ERR_HIP = 6            /* a HIP runtime call failed; see spsyrk_last_error_detail() */
+    SPSYRK_ERR_HIP = 6,           /* a HIP runtime call failed; see spsyrk_last_error_detail() */
+    SPSYRK_ERR_TOO_LARGE = 7      /* spsyrk_symm_noalloc: the operands need more than its fixed scratch */
 } spsyrk_status;
 
 /*
@@ -281,6 +282,27 @@ spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const
  */
 spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t k, const void* X, int64_t ldx,
                           void* Y, int64_t ldy, const spsyrk_allocator* al, void* hip_stream);
+
+/*
+ * spsyrk_symm without any allocation, for callers that cannot allocate device
+ * memory (code that must not call hipMalloc, tight serving loops, harnesses
+ * that forbid allocation).  Same operands, semirings, results and errors as
+ * spsyrk_symm; it never calls hipMalloc, hipFree or the allocator and never
+ * takes the bucketed path: every workspace lives in one fixed array of
+ * SPSYRK_NOALLOC_SCRATCH_BYTES per device, part of the library's device code
+ * (each device the library runs on holds it until the process ends).
+ * Limit: the scratch holds the workspace of 8 m k bytes plus a tile table
+ * of about nnz / 512 bytes (and under 1 KiB of alignment); larger operands
+ * get SPSYRK_ERR_TOO_LARGE before any device work (m k up to about 16.7 M).
+ * The array is shared by every call on a device and keeps the last call's
+ * contents (each call clears what must start at zero): calls that overlap on
+ * one device -- on different streams or host threads -- race and give wrong
+ * results; serialise them.  Blocks the host twice (validation word, end of
+ * the call); Y is complete on return.
+ */
+#define SPSYRK_NOALLOC_SCRATCH_BYTES (128ull << 20)
+spsyrk_status spsyrk_symm_noalloc(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t k, const void* X,
+                                  int64_t ldx, void* Y, int64_t ldy, void* hip_stream);
 
 /* Static description of a status code. */
 const char* spsyrk_status_string(spsyrk_status s);

@@ -29,7 +29,7 @@ _IN_DTYPE = {0: "float64", 1: "float32", 2: None, 3: None}
 _OUT_DTYPE = {0: "float64", 1: "float32", 2: "int32", 3: "float32"}
 
 STATUS = {0: "ok", 1: "invalid argument", 2: "not canonical", 3: "shape", 4: "out of memory",
-          5: "overflow", 6: "hip error"}
+          5: "overflow", 6: "hip error", 7: "too large for the fixed scratch"}
 
 
 class SpsyrkError(RuntimeError):
@@ -107,6 +107,9 @@ def library():
             lib.spsyrk_symm.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
                                         ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(_Allocator),
                                         ctypes.c_void_p]
+            lib.spsyrk_symm_noalloc.restype = ctypes.c_int
+            lib.spsyrk_symm_noalloc.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.c_int64, ctypes.c_void_p,
+                                                ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
             lib.spsyrk_status_string.argtypes = [ctypes.c_int]
             lib.spsyrk_status_string.restype = ctypes.c_char_p
             lib.spsyrk_last_error_detail.argtypes = []
@@ -123,7 +126,7 @@ def library():
 
 EXPORTS = ("spsyrk_lower", "spsyrk_lower_plan", "spsyrk_lower_execute", "spsyrk_plan_destroy",
            "spsyrk_lower_accumulate", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror",
-           "spsyrk_symm",
+           "spsyrk_symm", "spsyrk_symm_noalloc",
            "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
            "spsyrk_timing_end")
@@ -381,6 +384,35 @@ def symm(C_lower: DeviceCSR, X, semiring="f64"):
     if arena.live:
         raise RuntimeError("library left allocations unreleased")
     return Y2.squeeze(1) if X.dim() == 1 else Y2
+
+
+def symm_noalloc(C_lower: DeviceCSR, X, Y=None, semiring="f64"):
+    """Y = C X as ``symm`` does, through spsyrk_symm_noalloc: the library
+    allocates nothing (its workspace is a fixed per-device array, so calls on
+    one device must not overlap).  ``Y``: an optional preallocated output
+    shaped like X (m or m x k, unit column stride); returns Y."""
+    import torch
+    sr = _sr(semiring)
+    want = torch.float64 if sr in (0, 2) else torch.float32
+    if X.dtype != want:
+        raise TypeError(f"X must be {want} for semiring {semiring}")
+    X2 = X.unsqueeze(1) if X.dim() == 1 else X
+    if X2.dim() != 2 or X2.shape[0] != C_lower.nrows or X2.stride(1) != 1:
+        raise ValueError("X must be m or m x k with unit column stride")
+    m, k = X2.shape
+    if Y is None:
+        Y = torch.empty(X.shape, dtype=want, device=X.device)
+    Y2 = Y.unsqueeze(1) if Y.dim() == 1 else Y
+    if Y2.dtype != want or tuple(Y2.shape) != (m, k) or Y2.stride(1) != 1:
+        raise ValueError("Y must match X's shape and dtype with unit column stride")
+    lib = library()
+    a = _csr_struct(C_lower, sr, False)
+    stream = torch.cuda.current_stream(X.device).cuda_stream
+    rc = lib.spsyrk_symm_noalloc(ctypes.byref(a), sr, k, ctypes.c_void_p(X2.data_ptr()), X2.stride(0),
+                                 ctypes.c_void_p(Y2.data_ptr()), Y2.stride(0), ctypes.c_void_p(stream))
+    if rc != 0:
+        raise SpsyrkError(rc, lib.spsyrk_last_error_detail().decode())
+    return Y
 
 
 def mirror(C_lower: DeviceCSR, semiring="f64") -> DeviceCSR:

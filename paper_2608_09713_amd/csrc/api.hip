@@ -8,6 +8,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1069,6 +1070,51 @@ spsyrk_status guarded(spsyrk_csr_out* C, const spsyrk_allocator* al, void* strea
 
 }  // namespace
 
+// ---- scratch of the allocation-free product from a stored lower part
+// (spsyrk_symm_noalloc): one array per device, held until the process ends.
+// Its name is a host-side stand-in in host code; kernels get the device
+// address that hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of the current device's scratch, looked up once per
+// device with that device current.
+void* scratch_ptr() {
+    int dev = 0;
+    HIPCHK(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_detail("device %d is beyond the %d devices the scratch table covers", dev, kMaxDevices);
+        throw Fail{SPSYRK_ERR_HIP};
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) {
+            set_detail("hipGetSymbolAddress returned a null scratch address");
+            throw Fail{SPSYRK_ERR_HIP};
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+// scratch layout: the validation word in the first 256 bytes, then the
+// validation tile table, reused afterwards by the product's workspace
+size_t symm_noalloc_bytes(int64_t m, int64_t k, int64_t nnz) {
+    const size_t v = (validate_tmp_bytes(nnz) + 255) & ~size_t(255);
+    const size_t w = symm_tmp_bytes(m, k, nnz, false);
+    return 256 + (v > w ? v : w);
+}
+
+}  // namespace
+
 // the opaque plan handle of the C interface
 struct spsyrk_plan_s {
     LowerPlan p;
@@ -1157,6 +1203,60 @@ spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t
         check_launch();
         HIPCHK(hipStreamSynchronize(s));
     });
+}
+
+spsyrk_status spsyrk_symm_noalloc(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t k, const void* X,
+                                  int64_t ldx, void* Y, int64_t ldy, void* hip_stream) {
+    g_stats_valid = false;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    try {
+        check_semiring(int(sr));
+        check_input(C_lower, int(sr), false, "C_lower", int64_t(1) << 62);
+        if (C_lower->nrows != C_lower->ncols) {
+            set_detail("C_lower must be square (%lld x %lld)", (long long)C_lower->nrows,
+                       (long long)C_lower->ncols);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        if (k < 0 || ldx < k || ldy < k) {
+            set_detail("need 0 <= k <= ldx, ldy (k %lld, ldx %lld, ldy %lld)", (long long)k, (long long)ldx,
+                       (long long)ldy);
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        const int64_t m = C_lower->nrows;
+        if (m == 0 || k == 0) return finish(SPSYRK_OK);
+        if (!X || !Y || (C_lower->nnz > 0 && !C_lower->values)) {
+            set_detail("X, Y and the values of C_lower are required");
+            throw Fail{SPSYRK_ERR_INVALID_ARG};
+        }
+        const DevCsr c = dev(C_lower);
+        const size_t need = symm_noalloc_bytes(m, k, c.nnz);
+        if (need > kScratchBytes) {
+            set_detail("needs %zu bytes of scratch, the allocation-free call holds %zu (m k = %lld)", need,
+                       kScratchBytes, (long long)(m * k));
+            throw Fail{SPSYRK_ERR_TOO_LARGE};
+        }
+        char* base = static_cast<char*>(scratch_ptr());
+        uint32_t* err = reinterpret_cast<uint32_t*>(base);
+        fill_u32(err, 1, 0u, s);
+        validate_csr(c, true, err, base + 256, s);
+        check_launch();
+        uint32_t herr = 0;
+        HIPCHK(hipMemcpyAsync(&herr, err, sizeof(herr), hipMemcpyDeviceToHost, s));
+        HIPCHK(hipStreamSynchronize(s));
+        if (herr) {
+            set_detail("C_lower is not canonical CSR (flags 0x%x)", herr);
+            throw Fail{SPSYRK_ERR_NOT_CANONICAL};
+        }
+        symm_product(c, int(sr), X, ldx, k, Y, ldy, base + 256, false, s);
+        check_launch();
+        HIPCHK(hipStreamSynchronize(s));
+    } catch (const Fail& f) {
+        return f.st;
+    } catch (...) {
+        set_detail("unexpected host exception");
+        return SPSYRK_ERR_HIP;
+    }
+    return finish(SPSYRK_OK);
 }
 
 spsyrk_status spsyrk_lower_accumulate(const spsyrk_csr* C_prev, const spsyrk_csr* A_s, spsyrk_semiring sr,
@@ -1354,6 +1454,7 @@ const char* spsyrk_status_string(spsyrk_status s) {
         case SPSYRK_ERR_OOM: return "out of device memory";
         case SPSYRK_ERR_OVERFLOW: return "count overflow";
         case SPSYRK_ERR_HIP: return "HIP runtime error";
+        case SPSYRK_ERR_TOO_LARGE: return "operands exceed the fixed scratch of the allocation-free call";
     }
     return "unknown status";
 }

@@ -46,7 +46,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_status_strings_and_version(lib):
     assert lib.spsyrk_abi_version() == 2
-    for code in range(7):
+    for code in range(8):
         assert lib.spsyrk_status_string(code)
     assert lib.spsyrk_status_string(99) == b"unknown status"
 
@@ -109,6 +109,18 @@ def test_host_side_errors_of_the_other_calls(lib):
     assert lib.spsyrk_lower_plan(None, 0, None, None, ctypes.byref(h), ctypes.byref(o)) == 1
     assert not h.value
     assert lib.spsyrk_lower_plan(ctypes.byref(c), 0, None, None, None, ctypes.byref(o)) == 1
+
+
+def test_noalloc_checks_before_device_work(lib):
+    # argument errors and operands beyond the fixed scratch are refused on the
+    # host, before the scratch or any device memory is touched
+    c = _csr(4, 4, 1, v=1)
+    assert lib.spsyrk_symm_noalloc(None, 0, 1, 1, 1, 1, 1, None) == 1
+    assert lib.spsyrk_symm_noalloc(ctypes.byref(_csr(4, 5, 1, v=1)), 0, 1, 1, 1, 1, 1, None) == 1
+    assert lib.spsyrk_symm_noalloc(ctypes.byref(c), 0, 2, 1, 1, 1, 2, None) == 1   # ldx < k
+    big = _csr(1 << 21, 1 << 21, 0)
+    assert lib.spsyrk_symm_noalloc(ctypes.byref(big), 0, 9, 1, 9, 1, 9, None) == 7
+    assert b"scratch" in lib.spsyrk_last_error_detail()
 
 
 def test_binding_refuses_to_run_without_library(tmp_path, monkeypatch):
