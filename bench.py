@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--scale-shift", type=int, default=0, help="shrink the workload by 2^k (testing only)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=0, help="rows in the oracle sample (0: automatic)")
+    p.add_argument("--cpu-full", action="store_true",
+                   help="also time the oracle over every row, on one thread and on all host threads")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     p.add_argument("--json-out", default="")
@@ -88,24 +90,46 @@ def column_stats(A):
 
 
 def alg_bytes_phase(phase, sz, sr):
-    """Algorithmic bytes of one launch: every array the kernel must touch,
-    counted once.
+    """Algorithmic bytes of one launch of a one-kernel phase: every array the
+    kernel must touch, counted once (per-product gathers of partner keys are
+    not counted; each key of the column index counts once).
 
     light_numeric (the single-pass light-row kernel) reads the row pointers,
     the per-row product counts and staging slots (8 B each per row), the
     partner run of every entry (8 B), the values of A (fp semirings), every
-    kept column-index key and value once; it writes every output entry
+    kept column-index key and value once; it writes every light output entry
     (column + value) at its staging slot and the exact row lengths (8 B per
-    row).  compact reads and writes every output entry once plus three 8-B
-    words per row."""
+    row).  compact reads and writes every light output entry once plus three
+    8-B words per row.  colindex_pack (the local sort that writes the column
+    index) reads every sorted record (column, row field, entry index: 12 B),
+    writes every entry's key and index value at its sorted position and the
+    partner run (8 B) of every entry that has partners (all but the first of
+    each column).  heavy_symbolic reads the heavy-row list, their row
+    pointers, their entries' runs and cursors (12 B), every kept index key
+    once, and writes a length per heavy row; heavy_numeric reads the same plus
+    the output row pointers, A's values and the index values, and writes the
+    heavy rows' output entries."""
     m, nnz = sz["m"], sz["nnz_A"]
-    out = sz["nnz_C"] * (4 + V_OUT[sr])
+    vo = 4 + V_OUT[sr]
+    nh, he, hout = sz["heavy_rows"], sz["heavy_entries"], sz["heavy_nnz_out"]
+    light_out = sz["nnz_C"] - hout
     if phase == "light_numeric":
         return (8 * (m + 1) + 8 * m + 8 * m + 8 * nnz + nnz * V_IN[sr]
-                + sz["csc_entries"] * (4 + V_CX[sr]) + out + 8 * m)
+                + sz["csc_entries"] * (4 + V_CX[sr]) + light_out * vo + 8 * m)
     if phase == "compact":
-        return 2 * out + 3 * 8 * m
+        return 2 * light_out * vo + 3 * 8 * m
+    if phase == "colindex_pack":
+        return 12 * nnz + nnz * (4 + V_CX[sr]) + 8 * (nnz - sz["n_ne"])
+    if phase == "heavy_symbolic":
+        return 4 * nh + 16 * nh + 12 * he + 4 * sz["csc_entries"] + 8 * nh
+    if phase == "heavy_numeric":
+        return (4 * nh + 16 * nh + 8 * nh + he * (12 + V_IN[sr]) + sz["csc_entries"] * (4 + V_CX[sr])
+                + hout * vo)
     return None
+
+
+# phases that are one kernel launch each (a roofline is quoted for one kernel)
+SINGLE_KERNEL_PHASES = ("light_numeric", "compact", "colindex_pack", "heavy_symbolic", "heavy_numeric")
 
 
 def whole_call_bytes(sz, sr, mirror_nnz=None):
@@ -131,27 +155,65 @@ def cpu_model():
     return platform.processor()
 
 
-def cpu_baseline(A, sr, rows_n, seed):
-    """The oracle as it stands, single-threaded, on a seeded row sample."""
+ORACLE_PRODUCTS_PER_S = 5e6   # rough single-thread oracle speed (map updates per second), for sizing samples
+
+
+def _oracle_leg(A, sr, rows, threads):
+    """Time the oracle over the given rows (None: all) on ``threads`` threads;
+    the column-major copy of A is built inside the timed call."""
     import oracle
-    oracle.build()
-    rng = np.random.default_rng(seed + 1000)
-    rows = np.sort(rng.choice(A.nrows, size=min(rows_n, A.nrows), replace=False))
     Ain = A if sr in ("f64", "f32") else A.with_values(None)
     t0 = time.perf_counter()
-    R = oracle.lower(Ain, sr, rows=rows)
+    R = oracle.lower(Ain, sr, rows=rows, threads=threads)
     t = time.perf_counter() - t0
     flops = 2 * int(R.count.astype(np.int64).sum())
-    return {
-        "value": flops / t / 1e9,
-        "unit": "GFLOP/s",
-        "cores": 1,
-        "kind": "oracle",
-        "nnz_per_s": R.nnz / t,
-        "seconds": t,
-        "sample": f"{len(rows)} of {A.nrows} rows (seeded), full column-major copy of A built inside the "
-                  f"timed call; single thread; host {cpu_model()} with {os.cpu_count()} logical CPUs",
-    }
+    nrows = A.nrows if rows is None else len(rows)
+    out = {"value": flops / t / 1e9, "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+           "nnz_per_s": R.nnz / t, "seconds": t, "rows": nrows, "flops": flops}
+    del R
+    return out
+
+
+def _sample(A, frac, seed):
+    if frac >= 1.0:
+        return None
+    rng = np.random.default_rng(seed + 1000)
+    k = max(1, int(A.nrows * frac))
+    return np.sort(rng.choice(A.nrows, size=k, replace=False))
+
+
+def cpu_baseline(A, sr, F_L, seed, rows_override=0):
+    """The oracle as it stands, timed on this host beside the GPU run, on a
+    bounded seeded row sample: on all host threads (the headline figure;
+    blocks of rows through the same per-row code) over a sample of about
+    25 s of single-thread work, and on one thread over about 8 s of work."""
+    import oracle
+    oracle.build()
+    threads = oracle.host_threads()
+    if rows_override:
+        f_multi = f_single = min(1.0, rows_override / A.nrows)
+    else:
+        f_multi = min(1.0, 25.0 * ORACLE_PRODUCTS_PER_S / max(1, F_L))
+        f_single = min(1.0, 8.0 * ORACLE_PRODUCTS_PER_S / max(1, F_L))
+    multi = _oracle_leg(A, sr, _sample(A, f_multi, seed), threads)
+    single = _oracle_leg(A, sr, _sample(A, f_single, seed + 1), 1)
+    host = f"host {cpu_model()} with {os.cpu_count()} logical CPUs ({threads} used)"
+    multi["sample"] = (f"{multi['rows']} of {A.nrows} rows (seeded), computed in blocks of rows on {threads} "
+                       f"threads, column-major copy of A built inside the timed call (one thread); {host}")
+    single["sample"] = f"{single['rows']} of {A.nrows} rows (seeded), one thread; {host}"
+    multi["single_thread"] = single
+    return multi
+
+
+def cpu_full(A, sr, seed, skip_single):
+    """Every row: one thread (unless skip_single) and all host threads."""
+    import oracle
+    oracle.build()
+    out = {"threads": oracle.host_threads(), "cpu": cpu_model(), "logical_cpus": os.cpu_count()}
+    out["all_threads"] = _oracle_leg(A, sr, None, out["threads"])
+    if not skip_single:
+        out["one_thread"] = _oracle_leg(A, sr, None, 1)
+    return out
 
 
 def timed_call(torch, fn, reps=3):
@@ -302,27 +364,33 @@ def main():
     t_step = ms_step / 1e3
 
     sz = {"m": A.nrows, "nnz_A": A.nnz, "nnz_C": C.nnz, "csc_entries": st["csc_entries"],
-          "ngroups": (A.ncols + (1 << st["group_shift"]) - 1) >> st["group_shift"], "n_ne": n_ne}
+          "ngroups": (A.ncols + (1 << st["group_shift"]) - 1) >> st["group_shift"], "n_ne": n_ne,
+          "heavy_rows": st["heavy_rows"], "heavy_entries": st["heavy_entries"],
+          "heavy_nnz_out": st["heavy_nnz_out"]}
     flops = 2 * F_L
     value = flops / t_step / 1e9
     mirror_nnz = M.nnz if M is not None else None
     B_alg = whole_call_bytes(sz, sr, mirror_nnz)
 
-    # dominant single-kernel phase and its roofline
-    single = {k: v for k, v in phases.items() if k in ("light_numeric", "heavy_symbolic", "heavy_numeric",
-                                                       "compact")}
-    dom = max(single, key=lambda k: single[k][0] / max(1, single[k][1])) if single else None
+    # the dominant one-kernel phase (most time per step) and its roofline;
+    # every one-kernel phase's figure is reported beside it
+    kernel_roofs = {}
+    for k in SINGLE_KERNEL_PHASES:
+        if k not in phases or k == "light_numeric" and sz["m"] == sz["heavy_rows"]:
+            continue
+        ms, n = phases[k]
+        ab = alg_bytes_phase(k, sz, sr)
+        if n and ab:
+            ach = ab / (ms / n / 1e3) / 1e9
+            kernel_roofs[k] = {"avg_ms": ms / n, "ms_per_step": ms / args.steps, "alg_bytes_per_launch": ab,
+                               "achieved_GBs": ach, "frac": ach / HBM_PEAK_GBS}
     roof = None
-    if dom is not None:
-        ms, n = phases[dom]
-        avg_s = ms / n / 1e3
-        ab = alg_bytes_phase(dom, sz, sr)
-        if ab is not None:
-            ach = ab / avg_s / 1e9
-            tr = traffic_from_profiles(dom, args.workload)
-            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": ach / HBM_PEAK_GBS, "traffic": tr, "kernel": dom,
-                    "kernel_avg_ms": ms / n, "alg_bytes_per_launch": ab}
+    if kernel_roofs:
+        dom = max(kernel_roofs, key=lambda k: kernel_roofs[k]["ms_per_step"])
+        kr = kernel_roofs[dom]
+        roof = {"bound": "hbm", "achieved": kr["achieved_GBs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": kr["frac"], "traffic": traffic_from_profiles(dom, args.workload), "kernel": dom,
+                "kernel_avg_ms": kr["avg_ms"], "alg_bytes_per_launch": kr["alg_bytes_per_launch"]}
     phase_ms = {k: v[0] / v[1] for k, v in phases.items()}            # per launch of the phase
     phase_ms_step = {k: v[0] / args.steps for k, v in phases.items()}  # per step (all its launches)
 
@@ -348,6 +416,7 @@ def main():
         "hbm_roofline_whole_call": {"B_alg": B_alg, "achieved_GBs": B_alg / t_step / 1e9,
                                     "frac": B_alg / t_step / 1e9 / HBM_PEAK_GBS},
         "roofline": roof,
+        "kernel_rooflines": kernel_roofs,
         "phase_ms": phase_ms,
         "phase_ms_per_step": phase_ms_step,
         "library_stats": st,
@@ -363,11 +432,13 @@ def main():
         line["side"] = side_measurements(sp, torch, dev, Ad, Bd, sr, w, B_alg / t_step / 1e9)
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        rows_n = args.cpu_rows or max(1, A.nrows // 8)
-        print(f"[bench] oracle on {rows_n} rows ...", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(A, sr, rows_n, args.seed)
+        print("[bench] oracle on a row sample ...", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(A, sr, F_L, args.seed, args.cpu_rows)
     else:
         line["cpu_baseline"] = None
+    if args.cpu_full:
+        print("[bench] oracle over every row ...", file=sys.stderr, flush=True)
+        line["cpu_full"] = cpu_full(A, sr, args.seed, skip_single=F_L > 2e9)
     s = json.dumps(line)
     print(s, flush=True)
     if args.json_out:

@@ -317,6 +317,8 @@ typedef struct spsyrk_stats {
     int64_t heavy_rows;       /* rows routed to the dense-tile accumulator */
     int64_t light_rows;       /* rows handled by the batched ordered-bucket accumulator */
     int64_t products;         /* multiply-adds formed off the diagonal (lower) or in total (offdiag) */
+    int64_t heavy_entries;    /* entries of the left operand in heavy rows */
+    int64_t heavy_nnz_out;    /* result entries of heavy rows */
     int32_t group_shift;      /* log2 of columns per directory group */
     int32_t row_bits;         /* bits of the row id inside a packed column key */
 } spsyrk_stats;
@@ -326,8 +328,9 @@ spsyrk_status spsyrk_last_stats(spsyrk_stats* out);
 /*
  * Phase timing (profiling aid).  Between spsyrk_timing_begin() and
  * spsyrk_timing_end() every call on the calling thread records a pair of HIP
- * events on its stream around each phase below; the light and heavy phases
- * are one kernel launch each.  spsyrk_timing_end waits for the recorded
+ * events on its stream around each phase below; the light and heavy numeric
+ * and symbolic phases, the compaction and COLINDEX_PACK are one kernel launch
+ * each.  spsyrk_timing_end waits for the recorded
  * events, returns the summed milliseconds and the number of timed launches
  * per phase, releases the events and stops recording.  Recording adds no
  * synchronisation to the calls themselves.
@@ -345,7 +348,11 @@ typedef enum spsyrk_phase {
     SPSYRK_PHASE_MIRROR_TRANSPOSE = 9, /* spsyrk_mirror: strict lower part transposed into place */
     SPSYRK_PHASE_RUNS = 10,          /* row classes and the partner run of every entry */
     SPSYRK_PHASE_COMPACT = 11,       /* light rows moved from their staging slots into place */
-    SPSYRK_NUM_PHASES = 12
+    SPSYRK_PHASE_COLINDEX_PASSES = 12, /* inside COLINDEX: the sorting passes over the high column bits
+                                          (histograms, scans, scatters) */
+    SPSYRK_PHASE_COLINDEX_PACK = 13, /* inside COLINDEX: the one-kernel local sort that writes the index
+                                        (wide column ids only) */
+    SPSYRK_NUM_PHASES = 14
 } spsyrk_phase;
 
 typedef struct spsyrk_phase_times {

@@ -8,7 +8,9 @@ nothing from the library.
 The arithmetic lives in ``spsyrk_oracle.cpp`` (single-threaded Gustavson with
 an ordered-map accumulator, written from the definition C = A A^T of Sec. II-A,
 the lower-triangle restriction of Sec. III-A and the symmetric completion
-C = C_L + C_L^T - D of Eq. (spmv)).  This module only marshals numpy arrays.
+C = C_L + C_L^T - D of Eq. (spmv)); a thin driver there runs the same per-row
+code on several threads, for timing and for checking large results.  This
+module only marshals numpy arrays.
 """
 from __future__ import annotations
 
@@ -35,7 +37,7 @@ def build(force: bool = False) -> str:
     """Compile the oracle with g++ (host only)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-o", tmp, _SRC])
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-pthread", "-o", tmp, _SRC])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -45,6 +47,8 @@ def _declare(lib):
     lib.oracle_syrk.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64p, i32p, vp,
                                 i64, i64, i64p, i32p, vp, i64p, i64, ctypes.POINTER(vp)]
     lib.oracle_syrk.restype = ctypes.c_int
+    lib.oracle_syrk_threads.argtypes = lib.oracle_syrk.argtypes[:-1] + [ctypes.c_int, ctypes.POINTER(vp)]
+    lib.oracle_syrk_threads.restype = ctypes.c_int
     lib.oracle_mirror.argtypes = [i64, i64p, i32p, vp, ctypes.c_int, ctypes.POINTER(vp)]
     lib.oracle_mirror.restype = ctypes.c_int
     lib.oracle_check_canonical.argtypes = [i64, i64, i64p, i32p]
@@ -125,7 +129,7 @@ def _take(lib, h, sr, nrows, ncols, with_aux=True) -> Result:
     return Result(nrows, ncols, rp, ci, val, sa, cnt)
 
 
-def _run(mode, A, B, semiring, rows, lib=None):
+def _run(mode, A, B, semiring, rows, lib=None, threads=1):
     lib = lib or _load()
     sr = SEMIRINGS[semiring] if isinstance(semiring, str) else int(semiring)
     rp, ci, v = _csr_args(A, sr)
@@ -137,25 +141,40 @@ def _run(mode, A, B, semiring, rows, lib=None):
         mb = nb = 0
     sel = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
     h = ctypes.c_void_p()
-    rc = lib.oracle_syrk(mode, sr, A.nrows, A.ncols, _p(rp, ctypes.c_int64), _p(ci, ctypes.c_int32),
-                         v.ctypes.data_as(ctypes.c_void_p) if v is not None else None,
-                         mb, nb, _p(rpb, ctypes.c_int64), _p(cib, ctypes.c_int32),
-                         vb.ctypes.data_as(ctypes.c_void_p) if vb is not None else None,
-                         _p(sel, ctypes.c_int64), 0 if sel is None else len(sel), ctypes.byref(h))
+    args = (mode, sr, A.nrows, A.ncols, _p(rp, ctypes.c_int64), _p(ci, ctypes.c_int32),
+            v.ctypes.data_as(ctypes.c_void_p) if v is not None else None,
+            mb, nb, _p(rpb, ctypes.c_int64), _p(cib, ctypes.c_int32),
+            vb.ctypes.data_as(ctypes.c_void_p) if vb is not None else None,
+            _p(sel, ctypes.c_int64), 0 if sel is None else len(sel))
+    if threads > 1:
+        rc = lib.oracle_syrk_threads(*args, int(threads), ctypes.byref(h))
+    else:
+        rc = lib.oracle_syrk(*args, ctypes.byref(h))
     if rc != 0:
         raise OracleError({1: "input not canonical", 2: "shape mismatch", 3: "out of memory"}.get(rc, str(rc)))
     nrows = A.nrows if sel is None else len(sel)
     return _take(lib, h, sr, nrows, A.nrows if B is None else B.nrows)
 
 
-def lower(A, semiring, rows=None, lib=None) -> Result:
-    """C_L = tril(A A^T) (diagonal included); ``rows`` restricts to a row subset."""
-    return _run(0, A, None, semiring, rows, lib)
+def lower(A, semiring, rows=None, lib=None, threads=1) -> Result:
+    """C_L = tril(A A^T) (diagonal included); ``rows`` restricts to a row
+    subset; ``threads`` > 1 computes blocks of rows on that many threads
+    (the same rows through the same code, joined in order)."""
+    return _run(0, A, None, semiring, rows, lib, threads)
 
 
-def offdiag(Ai, Aj, semiring, rows=None, lib=None) -> Result:
+def offdiag(Ai, Aj, semiring, rows=None, lib=None, threads=1) -> Result:
     """Rectangular C = A_i A_j^T with no triangle prune."""
-    return _run(1, Ai, Aj, semiring, rows, lib)
+    return _run(1, Ai, Aj, semiring, rows, lib, threads)
+
+
+def host_threads() -> int:
+    """Logical CPUs this process may run on (at most 16: the GPU machine's share)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def offdiag_half(Ai, Aj, half, semiring, lib=None) -> Result:

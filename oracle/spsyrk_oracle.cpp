@@ -19,6 +19,11 @@
 // The off-diagonal block (Sec. III-B, C_ij = sum_s A_is A_js^T) is the same
 // formula over rows of A_i and rows of A_j with no triangle prune.
 //
+// A thin driver (syrk_sharded) runs the same per-row code on several threads,
+// each taking blocks of consecutive rows, and joins the blocks in row order;
+// it is there to time the oracle on all host cores and to check large
+// results, and computes exactly what the single-threaded call does.
+//
 // Algorithm: Gustavson row by row.  A column-major copy of the right operand
 // is built with a two-pass counting transpose (row ids come out ascending in
 // each column), then for each output row a std::map keyed by output column
@@ -32,11 +37,14 @@
 //   2  count int32      : one per shared column (pattern only), uint32 wrap.
 //   3  count -> Jaccard : c / (|a| + |b| - c) as one IEEE float division,
 //                         |a|, |b| the stored lengths of the two rows.
+#include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
 #include <map>
 #include <new>
+#include <thread>
 #include <vector>
 
 namespace {
@@ -136,16 +144,12 @@ void emit_row(Result& R, const std::map<int32_t, Acc>& acc, int sr, int64_t len_
     }
 }
 
+// Output rows q in [q0, q1) of the product (row i = rows[q], or q), appended
+// to R (R->row_ptr[q + 1] set relative to R's own entries).
 // lower: right operand is A itself and only j <= i is kept.
-// rows/nsel: optional subset of output rows (in the given order).
-Result* syrk(bool lower, const Csr& A, const Csr& B, int sr, const int64_t* rows, int64_t nsel) {
-    Result* R = new Result();
-    const Csc T = counting_transpose(B, sr);
-    const int64_t nout = rows ? nsel : A.m;
-    R->nrows = nout;
-    R->ncols = B.m;
-    R->row_ptr.assign(static_cast<size_t>(nout) + 1, 0);
-    for (int64_t q = 0; q < nout; ++q) {
+void syrk_rows(bool lower, const Csr& A, const Csr& B, const Csc& T, int sr, const int64_t* rows, int64_t q0,
+               int64_t q1, Result& R) {
+    for (int64_t q = q0; q < q1; ++q) {
         const int64_t i = rows ? rows[q] : q;
         std::map<int32_t, Acc> acc;
         for (int64_t e = A.rp[i]; e < A.rp[i + 1]; ++e) {
@@ -161,9 +165,84 @@ Result* syrk(bool lower, const Csr& A, const Csr& B, int sr, const int64_t* rows
                 s.count += 1u;
             }
         }
-        emit_row(*R, acc, sr, A.rp[i + 1] - A.rp[i], B);
-        R->row_ptr[q + 1] = static_cast<int64_t>(R->col.size());
+        emit_row(R, acc, sr, A.rp[i + 1] - A.rp[i], B);
+        R.row_ptr[q - q0 + 1] = static_cast<int64_t>(R.col.size());
     }
+}
+
+// rows/nsel: optional subset of output rows (in the given order).
+Result* syrk(bool lower, const Csr& A, const Csr& B, int sr, const int64_t* rows, int64_t nsel) {
+    Result* R = new Result();
+    const Csc T = counting_transpose(B, sr);
+    const int64_t nout = rows ? nsel : A.m;
+    R->nrows = nout;
+    R->ncols = B.m;
+    R->row_ptr.assign(static_cast<size_t>(nout) + 1, 0);
+    syrk_rows(lower, A, B, T, sr, rows, 0, nout, *R);
+    return R;
+}
+
+// The same rows computed by nthreads threads, each taking blocks of
+// consecutive output rows from a shared counter; the blocks are joined in
+// row order.  A driver for timing and for checking large results: every
+// row goes through syrk_rows exactly as above.
+Result* syrk_sharded(bool lower, const Csr& A, const Csr& B, int sr, const int64_t* rows, int64_t nsel,
+                     int nthreads) {
+    const Csc T = counting_transpose(B, sr);
+    const int64_t nout = rows ? nsel : A.m;
+    constexpr int64_t kBlockRows = 8192;
+    const int64_t nblocks = (nout + kBlockRows - 1) / kBlockRows;
+    std::vector<Result> part(static_cast<size_t>(nblocks));
+    std::atomic<int64_t> next{0};
+    std::atomic<bool> failed{false};
+    auto work = [&]() {
+        try {
+            for (int64_t b = next++; b < nblocks && !failed; b = next++) {
+                const int64_t q0 = b * kBlockRows, q1 = std::min(nout, q0 + kBlockRows);
+                Result& P = part[static_cast<size_t>(b)];
+                P.row_ptr.assign(static_cast<size_t>(q1 - q0) + 1, 0);
+                syrk_rows(lower, A, B, T, sr, rows, q0, q1, P);
+            }
+        } catch (const std::bad_alloc&) {
+            failed = true;
+        }
+    };
+    std::vector<std::thread> pool;
+    for (int t = 1; t < nthreads; ++t) pool.emplace_back(work);
+    work();
+    for (auto& th : pool) th.join();
+    if (failed) throw std::bad_alloc();
+    // join: block offsets, then every block copied into place (in parallel)
+    Result* R = new Result();
+    R->nrows = nout;
+    R->ncols = B.m;
+    R->row_ptr.assign(static_cast<size_t>(nout) + 1, 0);
+    std::vector<size_t> base(static_cast<size_t>(nblocks) + 1, 0);
+    for (int64_t b = 0; b < nblocks; ++b)
+        base[static_cast<size_t>(b) + 1] = base[static_cast<size_t>(b)] + part[static_cast<size_t>(b)].col.size();
+    const size_t total = base.back();
+    R->col.resize(total);
+    R->val.resize(total);
+    R->sum_abs.resize(total);
+    R->count.resize(total);
+    next = 0;
+    auto join = [&]() {
+        for (int64_t b = next++; b < nblocks; b = next++) {
+            Result& P = part[static_cast<size_t>(b)];
+            const size_t o = base[static_cast<size_t>(b)];
+            for (size_t r = 1; r < P.row_ptr.size(); ++r)
+                R->row_ptr[static_cast<size_t>(b * kBlockRows) + r] = static_cast<int64_t>(o) + P.row_ptr[r];
+            std::copy(P.col.begin(), P.col.end(), R->col.begin() + static_cast<std::ptrdiff_t>(o));
+            std::copy(P.val.begin(), P.val.end(), R->val.begin() + static_cast<std::ptrdiff_t>(o));
+            std::copy(P.sum_abs.begin(), P.sum_abs.end(), R->sum_abs.begin() + static_cast<std::ptrdiff_t>(o));
+            std::copy(P.count.begin(), P.count.end(), R->count.begin() + static_cast<std::ptrdiff_t>(o));
+            P = Result();  // release the block
+        }
+    };
+    pool.clear();
+    for (int t = 1; t < nthreads; ++t) pool.emplace_back(join);
+    join();
+    for (auto& th : pool) th.join();
     return R;
 }
 
@@ -176,12 +255,13 @@ int oracle_check_canonical(int64_t m, int64_t n, const int64_t* rp, const int32_
     return check_canonical(A);
 }
 
-// mode 0: lower (B ignored), mode 1: offdiag A_i * A_j^T.
+// mode 0: lower (B ignored), mode 1: offdiag A_i * A_j^T.  nthreads > 1
+// computes the rows in blocks on that many threads (same rows, same values).
 // Returns 0 on success, 1 not canonical, 2 shape mismatch, 3 out of memory.
-int oracle_syrk(int mode, int semiring,
-                int64_t m_a, int64_t n, const int64_t* rp_a, const int32_t* ci_a, const void* v_a,
-                int64_t m_b, int64_t n_b, const int64_t* rp_b, const int32_t* ci_b, const void* v_b,
-                const int64_t* rows, int64_t nsel, void** out) {
+int oracle_syrk_threads(int mode, int semiring,
+                        int64_t m_a, int64_t n, const int64_t* rp_a, const int32_t* ci_a, const void* v_a,
+                        int64_t m_b, int64_t n_b, const int64_t* rp_b, const int32_t* ci_b, const void* v_b,
+                        const int64_t* rows, int64_t nsel, int nthreads, void** out) {
     *out = nullptr;
     Csr A{m_a, n, rp_a, ci_a, v_a};
     if (check_canonical(A)) return 1;
@@ -196,11 +276,20 @@ int oracle_syrk(int mode, int semiring,
             if (rows[q] < 0 || rows[q] >= m_a) return 2;
     }
     try {
-        *out = syrk(mode == 0, A, B, semiring, rows, nsel);
+        *out = nthreads > 1 ? syrk_sharded(mode == 0, A, B, semiring, rows, nsel, nthreads)
+                            : syrk(mode == 0, A, B, semiring, rows, nsel);
     } catch (const std::bad_alloc&) {
         return 3;
     }
     return 0;
+}
+
+int oracle_syrk(int mode, int semiring,
+                int64_t m_a, int64_t n, const int64_t* rp_a, const int32_t* ci_a, const void* v_a,
+                int64_t m_b, int64_t n_b, const int64_t* rp_b, const int32_t* ci_b, const void* v_b,
+                const int64_t* rows, int64_t nsel, void** out) {
+    return oracle_syrk_threads(mode, semiring, m_a, n, rp_a, ci_a, v_a, m_b, n_b, rp_b, ci_b, v_b, rows, nsel, 1,
+                               out);
 }
 
 // Full symmetric matrix from its stored lower part (Eq. (spmv): C = C_L + C_L^T - D):

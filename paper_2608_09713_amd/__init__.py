@@ -59,8 +59,8 @@ class _Allocator(ctypes.Structure):
 
 class Stats(ctypes.Structure):
     _fields_ = [("nnz_out", ctypes.c_int64), ("csc_entries", ctypes.c_int64), ("heavy_rows", ctypes.c_int64),
-                ("light_rows", ctypes.c_int64), ("products", ctypes.c_int64), ("group_shift", ctypes.c_int32),
-                ("row_bits", ctypes.c_int32)]
+                ("light_rows", ctypes.c_int64), ("products", ctypes.c_int64), ("heavy_entries", ctypes.c_int64),
+                ("heavy_nnz_out", ctypes.c_int64), ("group_shift", ctypes.c_int32), ("row_bits", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -132,7 +132,7 @@ EXPORTS = ("spsyrk_lower", "spsyrk_lower_plan", "spsyrk_lower_execute", "spsyrk_
            "spsyrk_timing_end")
 
 PHASES = ("validate", "colindex", "light_symbolic", "heavy_symbolic", "scan", "light_numeric", "heavy_numeric",
-          "mirror_count", "mirror_copy", "mirror_transpose", "runs", "compact")
+          "mirror_count", "mirror_copy", "mirror_transpose", "runs", "compact", "colindex_passes", "colindex_pack")
 
 
 class _PhaseTimes(ctypes.Structure):

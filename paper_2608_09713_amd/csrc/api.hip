@@ -140,25 +140,7 @@ struct PhaseMark {
 thread_local bool g_timing = false;
 thread_local std::vector<PhaseMark> g_marks;
 
-class Phase {
-   public:
-    Phase(int phase, hipStream_t s) : s_(s) {
-        if (!g_timing) return;
-        m_.phase = phase;
-        if (hipEventCreate(&m_.a) != hipSuccess || hipEventCreate(&m_.b) != hipSuccess) return;
-        if (hipEventRecord(m_.a, s_) != hipSuccess) return;
-        on_ = true;
-    }
-    ~Phase() {
-        if (!on_) return;
-        if (hipEventRecord(m_.b, s_) == hipSuccess) g_marks.push_back(m_);
-    }
-
-   private:
-    hipStream_t s_;
-    PhaseMark m_{};
-    bool on_ = false;
-};
+using Phase = PhaseTimer;
 
 // small block of device scalars read back at the synchronisation points
 struct Ctl {
@@ -171,9 +153,9 @@ struct Ctl {
     int32_t queue;
     int32_t pad0;
     unsigned long long light_cap;
-    unsigned long long heavy_total;
+    unsigned long long heavy_sums[2];  // entries of A and output entries of the heavy rows
     unsigned long long chunk_counter;
-    int64_t pad[3];
+    int64_t pad[2];
 };
 
 struct HostCtl {
@@ -522,6 +504,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         Phase ph(SPSYRK_PHASE_SCAN, s);
         scan_i64(row_cnt, c_rp, m + 1, &ctl->total, stmp, s);
     }
+    heavy_sums(heavy_rows, nheavy, L.rp, c_rp, ctl->heavy_sums, s);  // (counters for the statistics)
     check_launch();
     h = read_ctl(ctl, s);
     const int64_t total = h.total;
@@ -574,6 +557,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     st.csc_entries = h.nkept;
     st.heavy_rows = nheavy;
     st.light_rows = nlight;
+    st.heavy_entries = int64_t(h.heavy_sums[0]);
+    st.heavy_nnz_out = int64_t(h.heavy_sums[1]);
     st.products = int64_t(h.products);
     st.group_shift = cx.gs;
     st.row_bits = cx.rowbits;
@@ -676,6 +661,7 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         Phase ph(SPSYRK_PHASE_SCAN, s);
         scan_i64(c_rp, c_rp, m + 1, &ctl->total, stmp, s);
     }
+    heavy_sums(heavy_rows, nheavy, L.rp, c_rp, ctl->heavy_sums, s);  // (counters for the statistics)
     check_launch();
     h = read_ctl(ctl, s);
     ar.release(stmp);
@@ -716,6 +702,8 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     st.csc_entries = h.nkept;
     st.heavy_rows = nheavy;
     st.light_rows = m - nheavy;
+    st.heavy_entries = int64_t(h.heavy_sums[0]);
+    st.heavy_nnz_out = int64_t(h.heavy_sums[1]);
     st.products = int64_t(h.products);
     st.group_shift = cx.gs;
     st.row_bits = cx.rowbits;
@@ -1114,6 +1102,31 @@ size_t symm_noalloc_bytes(int64_t m, int64_t k, int64_t nnz) {
 }
 
 }  // namespace
+
+spsyrk::PhaseTimer::PhaseTimer(int phase, hipStream_t s) : s_(s), phase_(phase) {
+    if (!g_timing) return;
+    if (hipEventCreate(&a_) != hipSuccess) return;
+    if (hipEventCreate(&b_) != hipSuccess) {
+        (void)hipEventDestroy(a_);
+        return;
+    }
+    if (hipEventRecord(a_, s_) != hipSuccess) {
+        (void)hipEventDestroy(a_);
+        (void)hipEventDestroy(b_);
+        return;
+    }
+    on_ = true;
+}
+
+spsyrk::PhaseTimer::~PhaseTimer() {
+    if (!on_) return;
+    if (hipEventRecord(b_, s_) == hipSuccess) {
+        g_marks.push_back(PhaseMark{phase_, a_, b_});
+    } else {
+        (void)hipEventDestroy(a_);
+        (void)hipEventDestroy(b_);
+    }
+}
 
 // the opaque plan handle of the C interface
 struct spsyrk_plan_s {

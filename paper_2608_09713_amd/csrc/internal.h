@@ -6,7 +6,26 @@
 #include <cstddef>
 #include <cstdint>
 
+#include "spsyrk.h"
+
 namespace spsyrk {
+
+// A pair of HIP events around the work enqueued on stream s during its
+// lifetime, recorded while phase timing is on (spsyrk_timing_begin); phase is
+// a spsyrk_phase value.
+class PhaseTimer {
+   public:
+    PhaseTimer(int phase, hipStream_t s);
+    ~PhaseTimer();
+    PhaseTimer(const PhaseTimer&) = delete;
+    PhaseTimer& operator=(const PhaseTimer&) = delete;
+
+   private:
+    hipStream_t s_;
+    int phase_;
+    hipEvent_t a_{}, b_{};
+    bool on_ = false;
+};
 
 // semiring codes (same values as the public enum)
 enum Sr : int { kF64 = 0, kF32 = 1, kCount = 2, kJaccard = 3 };
@@ -196,6 +215,10 @@ size_t compact_tmp_bytes(int64_t staged);
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
                   const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
                   hipStream_t s);
+// Over the rows listed in rows[0..n): adds the entries of A (rp) to out[0]
+// and the output entries (c_rp) to out[1] (zeroed beforehand).
+void heavy_sums(const int32_t* rows, int64_t n, const int64_t* rp, const int64_t* c_rp, unsigned long long* out,
+                hipStream_t s);
 // Row of every tile start: trow[t] = the row r with rp[r] <= t T < rp[r + 1],
 // for t T < rp[m] (rp non-decreasing; trow: ceil(rp[m] / T) words).
 void tile_first_rows(const int64_t* rp, int64_t m, int64_t T, int64_t* trow, hipStream_t s);

@@ -760,21 +760,24 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     const int passes = digit_plan(nbits - L, width);
     // first pass straight from the CSR arrays (into the b buffers), at least
     // one pass; the row of every tile's first entry comes from a table
-    tile_first_rows(rp, m, kRTile, trow, s);
-    run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
-                      (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
     int cur = 1;
-    int shift = L + width[0];
-    for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
-        const uint32_t mask = (1u << width[ps]) - 1u;
-        uint32_t* ki = cur ? key_b : key_a;
-        uint32_t* ko = cur ? key_a : key_b;
-        uint32_t* ri = cur ? row_b : row_a;
-        uint32_t* ro = cur ? row_a : row_b;
-        uint32_t* vi = cur ? ent_b : ent_a;
-        uint32_t* vo = cur ? ent_a : ent_b;
-        run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
-        cur ^= 1;
+    {
+        PhaseTimer passes_timer(SPSYRK_PHASE_COLINDEX_PASSES, s);
+        tile_first_rows(rp, m, kRTile, trow, s);
+        run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
+                          (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
+        int shift = L + width[0];
+        for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
+            const uint32_t mask = (1u << width[ps]) - 1u;
+            uint32_t* ki = cur ? key_b : key_a;
+            uint32_t* ko = cur ? key_a : key_b;
+            uint32_t* ri = cur ? row_b : row_a;
+            uint32_t* ro = cur ? row_a : row_b;
+            uint32_t* vi = cur ? ent_b : ent_a;
+            uint32_t* vo = cur ? ent_a : ent_b;
+            run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+            cur ^= 1;
+        }
     }
     if (L == 0) return cur;
     // groups of equal high bits, each sorted by the low L bits into the other buffers
@@ -792,6 +795,7 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     uint32_t* ey = cur ? ent_a : ent_b;
     if (pk) {
         const unsigned g = unsigned(groups);
+        PhaseTimer pack_timer(SPSYRK_PHASE_COLINDEX_PACK, s);
         if (pk->jac)
             local_sort_pack<0, true><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
         else if (pk->vbytes == 8)

@@ -324,6 +324,34 @@ void shift_columns(int32_t* ci, int64_t nnz, int32_t off, hipStream_t s) {
     shift_columns_kernel<<<unsigned(blocks), kBlock, 0, s>>>(ci, nnz, off);
 }
 
+namespace {
+__global__ __launch_bounds__(kBlock) void heavy_sums_kernel(const int32_t* __restrict__ rows, int64_t n,
+                                                            const int64_t* __restrict__ rp,
+                                                            const int64_t* __restrict__ c_rp,
+                                                            unsigned long long* __restrict__ out) {
+    unsigned long long e = 0, o = 0;
+    for (int64_t q = int64_t(blockIdx.x) * kBlock + threadIdx.x; q < n; q += int64_t(gridDim.x) * kBlock) {
+        const int64_t r = rows[q];
+        e += (unsigned long long)(rp[r + 1] - rp[r]);
+        o += (unsigned long long)(c_rp[r + 1] - c_rp[r]);
+    }
+    e = wave_reduce_sum(e);
+    o = wave_reduce_sum(o);
+    if (lane_id() == 0 && (e | o)) {
+        atomicAdd(out, e);
+        atomicAdd(out + 1, o);
+    }
+}
+}  // namespace
+
+void heavy_sums(const int32_t* rows, int64_t n, const int64_t* rp, const int64_t* c_rp, unsigned long long* out,
+                hipStream_t s) {
+    if (n <= 0) return;
+    int64_t grid = (n + kBlock - 1) / kBlock;
+    if (grid > 256) grid = 256;
+    heavy_sums_kernel<<<unsigned(grid), kBlock, 0, s>>>(rows, n, rp, c_rp, out);
+}
+
 void tile_first_rows(const int64_t* rp, int64_t m, int64_t T, int64_t* trow, hipStream_t s) {
     if (m <= 0) return;
     tile_rows<<<unsigned((m + kBlock - 1) / kBlock), kBlock, 0, s>>>(rp, m, T, trow);

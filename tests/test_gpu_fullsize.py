@@ -1,15 +1,19 @@
 """Parity at the workloads' full sizes, in the launch configuration the
-benchmark times: sampled rows are compared element by element with the oracle
-computing those rows one by one, and whole-result properties that hold at any
-size are checked on the device output (exact count sums, diagonal, entry
-counts, symmetry of sampled mirrored rows)."""
+benchmark times.  The k-mer, Jaccard and off-diagonal workloads are compared
+with the oracle row for row over every row (the oracle's rows computed in
+blocks on all host threads); R-MAT's much larger result is compared on sampled
+rows.  Whole-result properties that hold at any size are checked on the device
+output too (exact count sums, diagonal, entry counts, symmetry of sampled
+mirrored rows)."""
+import functools
+
 import numpy as np
 import pytest
 
 import oracle
 import paper_2608_09713_amd as sp
 from paper_2608_09713_amd import workloads as W
-from tests.parity import compare_rows, device_rows
+from tests.parity import compare_full, compare_rows, device_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -22,6 +26,12 @@ def dev():
     assert torch.cuda.is_available()
     sp.library()
     return "cuda:0"
+
+
+@functools.lru_cache(maxsize=8)
+def make(name):
+    """A full-size workload, generated once per test session."""
+    return W.make(name, 1, 0)
 
 
 def upload(A, sr, dev):
@@ -42,12 +52,20 @@ def col_counts(A):
 
 
 def check_lower(A, sr, dev, rows, what):
+    """C_L on the device against the oracle: every row (rows is None) or the
+    listed rows."""
     print(f"[full {what}] m={A.nrows} n={A.ncols} nnz={A.nnz}", flush=True)
     C = sp.lower(upload(A, sr, dev), sr)
     st = sp.stats()
     Ain = A.with_values(A.values.astype(VDT[sr]) if VDT[sr] else None)
-    ref = oracle.lower(Ain, sr, rows=rows)
-    compare_rows(C, ref, rows, sr, what)
+    if rows is None:
+        ref = oracle.lower(Ain, sr, threads=oracle.host_threads())
+        print(f"[full {what}] oracle done: nnz={ref.nnz}; comparing every row", flush=True)
+        compare_full(C, ref, sr, what)
+        del ref
+    else:
+        ref = oracle.lower(Ain, sr, rows=rows)
+        compare_rows(C, ref, rows, sr, what)
     # entry count of every row is at least 1 for non-empty rows, the diagonal is last
     rp = C.row_ptr.cpu().numpy()
     lens = np.diff(A.row_ptr)
@@ -62,10 +80,9 @@ def check_lower(A, sr, dev, rows, what):
 @pytest.mark.parametrize("name", ["kmer_i32", "jaccard_large"])
 def test_kmer_shapes_full(dev, name):
     import torch
-    w = W.make(name, 1, 0)
+    w = make(name)
     A, sr = w["A"], w["semiring"]
-    rows = sample_rows(A, 400, 11)
-    C, st, ne, last = check_lower(A, sr, dev, rows, name)
+    C, st, ne, last = check_lower(A, sr, dev, None, name)
     c = col_counts(A)
     F_L = int((c * (c + 1) // 2).sum())
     assert st["products"] + A.nnz == F_L  # half-work identity: formed products = F_L exactly
@@ -85,7 +102,7 @@ def test_kmer_shapes_full(dev, name):
 
 def test_rmat_full_lower_and_mirror(dev):
     import torch
-    w = W.make("rmat20_f32", 1, 0)
+    w = make("rmat20_f32")
     A, sr = w["A"], w["semiring"]
     lens = np.diff(A.row_ptr)
     heavy = np.argsort(lens)[-3:]  # hub rows: the longest rows
@@ -122,44 +139,39 @@ def test_rmat_full_lower_and_mirror(dev):
 
 def test_offdiag_full(dev):
     import torch
-    w = W.make("offdiag_f64", 1, 0)
+    w = make("offdiag_f64")
     Ai, Aj, sr = w["A"], w["B"], w["semiring"]
-    rows = sample_rows(Ai, 400, 13)
+    print(f"[full offdiag] m_i={Ai.nrows} m_j={Aj.nrows} nnz={Ai.nnz}+{Aj.nnz}", flush=True)
     O = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
-    compare_rows(O, oracle.offdiag(Ai, Aj, sr, rows=rows), rows, sr, "offdiag full")
+    compare_full(O, oracle.offdiag(Ai, Aj, sr, threads=oracle.host_threads()), sr, "offdiag every row")
     ci, cj = col_counts(Ai), col_counts(Aj)
     assert sp.stats()["products"] == int((ci * cj).sum())
     # count semiring: sum of the block = sum_k c^i_k c^j_k
     K = sp.offdiag(upload(Ai, "count", dev), upload(Aj, "count", dev), "count")
     assert int(K.values[: K.nnz].to(torch.int64).sum().item()) == int((ci * cj).sum())
-    check_lower(Ai, sr, dev, rows, "offdiag diagonal block")
+    check_lower(Ai, sr, dev, None, "offdiag diagonal block")
 
 
 def test_offdiag_halves_full(dev):
-    # Algorithm 3's half blocks at the off-diagonal workload's size: sampled
-    # rows of each half against the oracle's restriction of the block, and
-    # entry counts that add up to the full block's
-    w = W.make("offdiag_f64", 1, 0)
+    # Algorithm 3's half blocks at the off-diagonal workload's size, every row
+    # of each half against the oracle's restriction of the whole block
+    w = make("offdiag_f64")
     Ai, Aj, sr = w["A"], w["B"], w["semiring"]
     print(f"[full offdiag halves] m_i={Ai.nrows} m_j={Aj.nrows} nnz={Ai.nnz}+{Aj.nnz}", flush=True)
     top = sp.offdiag_half(upload(Ai, sr, dev), upload(Aj, sr, dev), "top", sr)
     right = sp.offdiag_half(upload(Ai, sr, dev), upload(Aj, sr, dev), "right", sr)
-    rows = sample_rows(Ai, 300, 17)
-    top_rows = rows[rows < Ai.nrows // 2]
-    compare_rows(top, oracle.offdiag(Ai, Aj, sr, rows=top_rows), top_rows, sr, "top half")
-    ref = oracle.offdiag(Ai, Aj, sr, rows=rows)
+    ref = oracle.offdiag(Ai, Aj, sr, threads=oracle.host_threads())
+    h = Ai.nrows // 2
+    cut = int(ref.row_ptr[h])
+    ref_top = oracle.Result(h, Aj.nrows, ref.row_ptr[:h + 1].copy(), ref.col_idx[:cut], ref.values[:cut],
+                            ref.sum_abs[:cut])
+    compare_full(top, ref_top, sr, "top half")
     keep = ref.col_idx >= Aj.nrows // 2
-    rr = np.repeat(np.arange(len(rows)), np.diff(ref.row_ptr))
-    rp = np.zeros(len(rows) + 1, dtype=np.int64)
-    np.cumsum(np.bincount(rr[keep], minlength=len(rows)), out=rp[1:])
-    ref_right = oracle.Result(len(rows), Aj.nrows, rp, ref.col_idx[keep], ref.values[keep],
-                              None if ref.sum_abs is None else ref.sum_abs[keep])
-    compare_rows(right, ref_right, rows, sr, "right half")
-    # the top half plus the bottom rows' right columns plus their left columns
-    # make the block; here: the halves' nnz against the full block's rows
-    full = sp.offdiag(upload(Ai, sr, dev), upload(Aj, sr, dev), sr)
-    frp = full.row_ptr.cpu().numpy()
-    assert top.nnz == frp[Ai.nrows // 2]
+    rr = np.repeat(np.arange(Ai.nrows), np.diff(ref.row_ptr))
+    rp = np.zeros(Ai.nrows + 1, dtype=np.int64)
+    np.cumsum(np.bincount(rr[keep], minlength=Ai.nrows), out=rp[1:])
+    ref_right = oracle.Result(Ai.nrows, Aj.nrows, rp, ref.col_idx[keep], ref.values[keep], ref.sum_abs[keep])
+    compare_full(right, ref_right, sr, "right half")
 
 
 @pytest.mark.parametrize("name", ["jaccard_large", "kmer_i32"])
@@ -167,7 +179,7 @@ def test_symm_full(dev, name):
     # Y = C x from the device's C_L at full size; sampled rows of Y against the
     # oracle's rows of the full product A A^T (the mirrored rows) times x
     import torch
-    w = W.make(name, 1, 0)
+    w = make(name)
     A, sr = w["A"], w["semiring"]
     print(f"[full symm {name}] m={A.nrows} nnz={A.nnz}", flush=True)
     C = sp.lower(upload(A, sr, dev), sr)
@@ -193,7 +205,7 @@ def test_accumulate_full_columns_split(dev):
     # bit for bit
     import torch
     from paper_2608_09713_amd.workloads import CSR
-    w = W.make("jaccard_large", 1, 0)
+    w = make("jaccard_large")
     A = w["A"]
     print(f"[full accumulate] m={A.nrows} nnz={A.nnz}", flush=True)
     half = A.ncols // 2
@@ -220,7 +232,7 @@ def test_plan_execute_full(dev, name):
     # a plan at full size: an execution with new values equals the one-shot
     # product of those values bit for bit
     import torch
-    w = W.make(name, 1, 0)
+    w = make(name)
     A, sr = w["A"], w["semiring"]
     print(f"[full plan {name}] m={A.nrows} nnz={A.nnz}", flush=True)
     plan, C = sp.lower_plan(upload(A, sr, dev), sr)
@@ -243,7 +255,7 @@ def test_offdiag_self_full_wide_columns(dev):
     # starts of 1 GiB) is the full product: the mirror of the lower part,
     # counts bit for bit
     import torch
-    w = W.make("jaccard_large", 1, 0)
+    w = make("jaccard_large")
     A = w["A"]
     print(f"[full offdiag(A, A)] m={A.nrows} n={A.ncols} nnz={A.nnz}", flush=True)
     Ad = upload(A, "count", dev)

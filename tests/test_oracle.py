@@ -205,6 +205,28 @@ def test_offdiag_brute_force():
     check_offdiag_brute()
 
 
+def test_threads_give_the_same_result():
+    # the row-sharded driver runs the same per-row code: identical output,
+    # bit for bit, for every semiring, a row subset and the off-diagonal call
+    rng = np.random.default_rng(9)
+    A = random_csr(rng, 20000 // 100, 300, 0.03)
+    B = random_csr(rng, 150, 300, 0.03)
+    big = W.make("kmer_i32", 1, 6)["A"]
+    for Ain, sr in ((A, "f64"), (A.with_values(A.values.astype(np.float32)), "f32"),
+                    (big, "count"), (big, "jaccard")):
+        one = oracle.lower(Ain, sr)
+        many = oracle.lower(Ain, sr, threads=4)
+        for f in ("row_ptr", "col_idx", "sum_abs", "count"):
+            np.testing.assert_array_equal(getattr(one, f), getattr(many, f))
+        np.testing.assert_array_equal(one.values.view(np.uint8), many.values.view(np.uint8))
+    rows = np.array([17, 3, 3, 150, 0])
+    np.testing.assert_array_equal(oracle.lower(A, "f64", rows=rows).col_idx,
+                                  oracle.lower(A, "f64", rows=rows, threads=3).col_idx)
+    one, many = oracle.offdiag(A, B, "f64"), oracle.offdiag(A, B, "f64", threads=5)
+    np.testing.assert_array_equal(one.row_ptr, many.row_ptr)
+    np.testing.assert_array_equal(one.values, many.values)
+
+
 def test_row_subset_matches_full():
     rng = np.random.default_rng(3)
     A = random_csr(rng, 50, 40, 0.1)
@@ -611,8 +633,8 @@ MUTANTS = {
     "count_double": ("s.count += 1u;", "s.count += 2u;"),
     # off the diagonal, |S(j)| taken from the left operand A_i instead of A_j
     # (kept in range: only where A_i has at least as many rows)
-    "jaccard_len_j_from_left": ("emit_row(*R, acc, sr, A.rp[i + 1] - A.rp[i], B);",
-                                "emit_row(*R, acc, sr, A.rp[i + 1] - A.rp[i], (lower || A.m < B.m) ? B : A);"),
+    "jaccard_len_j_from_left": ("emit_row(R, acc, sr, A.rp[i + 1] - A.rp[i], B);",
+                                "emit_row(R, acc, sr, A.rp[i + 1] - A.rp[i], (lower || A.m < B.m) ? B : A);"),
 }
 
 
@@ -635,7 +657,7 @@ def test_planted_mistakes_fail(name, tmp_path):
     path = tmp_path / "mutant.cpp"
     path.write_text(src.replace(old, new))
     so = tmp_path / "libmutant.so"
-    subprocess.check_call(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", "-o", str(so), str(path)])
+    subprocess.check_call(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", "-pthread", "-o", str(so), str(path)])
     lib = oracle._load(str(so))
     with pytest.raises((AssertionError, oracle.OracleError)):
         _all_pins(lib)
