@@ -272,10 +272,15 @@ spsyrk_status spsyrk_mirror(const spsyrk_csr* C_lower, spsyrk_semiring sr, const
  * before return; for one column (k = 1) of a matrix of 2^19 to 2^21 rows the
  * transposed terms go through buckets of rows instead of atomic adds to
  * random rows, which takes 10 bytes per entry of C_lower more (records of
- * (row in bucket, value)) and a table of per-bucket counts.  The variable
- * SPSYRK_SYMM_BUCKETS (read at every call) overrides that choice: 0 never,
- * 1 for every single column of up to 2^24 rows, 12 to 14 the same with
- * buckets of 2^12 to 2^14 rows.  The call returns after Y is complete.
+ * (row in bucket, value)) and a table of per-bucket counts; past 2^21 rows
+ * they go through records grouped by ranges of 2^18 rows (12 bytes per entry
+ * of C_lower), each range then added on one XCD of the chip.  The variable
+ * SPSYRK_SYMM_BUCKETS (read at every call) overrides the bucket choice: 0
+ * never, 1 for every single column of up to 2^24 rows, 12 to 14 the same
+ * with buckets of 2^12 to 2^14 rows (raised where needed to keep at most
+ * 1024 buckets); SPSYRK_SYMM_SPLIT = 0 or 1 turns the range split off, or on
+ * for every single column not bucketed.  The call returns after Y is
+ * complete.
  * Errors: INVALID_ARG (non-square C_lower, k < 0, ldx or ldy < k, null
  * arrays), NOT_CANONICAL (including an entry above the diagonal), SHAPE, OOM,
  * HIP.

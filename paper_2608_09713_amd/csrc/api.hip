@@ -1097,7 +1097,7 @@ void* scratch_ptr() {
 // validation tile table, reused afterwards by the product's workspace
 size_t symm_noalloc_bytes(int64_t m, int64_t k, int64_t nnz) {
     const size_t v = (validate_tmp_bytes(nnz) + 255) & ~size_t(255);
-    const size_t w = symm_tmp_bytes(m, k, nnz, false);
+    const size_t w = symm_tmp_bytes(m, k, nnz, kSymmAtomics);
     return 256 + (v > w ? v : w);
 }
 
@@ -1210,9 +1210,9 @@ spsyrk_status spsyrk_symm(const spsyrk_csr* C_lower, spsyrk_semiring sr, int64_t
             zero_ctl(ctl, s);
             validate(c, true, ar, ctl, s, "C_lower");
         }
-        const bool buckets = symm_use_buckets(m, k, c.nnz);
-        void* tmp = ar.get(symm_tmp_bytes(m, k, c.nnz, buckets));
-        symm_product(c, int(sr), X, ldx, k, Y, ldy, tmp, buckets, s);
+        const int mode = symm_mode(m, k, c.nnz);
+        void* tmp = ar.get(symm_tmp_bytes(m, k, c.nnz, mode));
+        symm_product(c, int(sr), X, ldx, k, Y, ldy, tmp, mode, s);
         check_launch();
         HIPCHK(hipStreamSynchronize(s));
     });
@@ -1260,7 +1260,7 @@ spsyrk_status spsyrk_symm_noalloc(const spsyrk_csr* C_lower, spsyrk_semiring sr,
             set_detail("C_lower is not canonical CSR (flags 0x%x)", herr);
             throw Fail{SPSYRK_ERR_NOT_CANONICAL};
         }
-        symm_product(c, int(sr), X, ldx, k, Y, ldy, base + 256, false, s);
+        symm_product(c, int(sr), X, ldx, k, Y, ldy, base + 256, kSymmAtomics, s);
         check_launch();
         HIPCHK(hipStreamSynchronize(s));
     } catch (const Fail& f) {

@@ -274,13 +274,16 @@ void merge_lower(bool write, int sr, int64_t items, const int64_t* crow, const i
 // Y = C X with C = C_L + C_L^T - D from the stored lower part C (canonical,
 // nothing above the diagonal, values of the semiring's output type).  X and
 // Y: m x k row-major (ldx, ldy), double for F64 and COUNT, float otherwise.
-// buckets: take the bucketed path of a single column (symm_use_buckets
-// gives the default choice; the same value goes to both calls).
-// tmp: symm_tmp_bytes(m, k, nnz, buckets).
-bool symm_use_buckets(int64_t m, int64_t k, int64_t nnz);
-size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz, bool buckets);
+// mode: how the transposed term is added (symm_mode gives the default
+// choice; the same value goes to both calls): atomic adds to random rows,
+// LDS buckets of rows (one column, 2^19 to 2^21 rows), or records split by
+// row range and added per XCD (one column, past 2^21 rows).
+// tmp: symm_tmp_bytes(m, k, nnz, mode).
+enum SymmMode : int { kSymmAtomics = 0, kSymmBuckets = 1, kSymmSplit = 2 };
+int symm_mode(int64_t m, int64_t k, int64_t nnz);
+size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz, int mode);
 void symm_product(const DevCsr& C, int sr, const void* x, int64_t ldx, int64_t k, void* y, int64_t ldy, void* tmp,
-                  bool buckets, hipStream_t s);
+                  int mode, hipStream_t s);
 
 // ---- mirror.hip
 struct MirrorArgs {

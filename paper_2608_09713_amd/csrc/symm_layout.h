@@ -1,6 +1,6 @@
-// Host-side choice of the bucketed path of the product from a stored lower
-// part with one column: whether the transposed term goes through buckets of
-// rows, and how many rows a bucket holds.  Plain C++ (no HIP), so that the
+// Host-side choice of the paths of the product from a stored lower part with
+// one column: whether the transposed term goes through LDS buckets of rows
+// (and how many rows a bucket holds) or through records split by row range.  Plain C++ (no HIP), so that the
 // choice can be checked on any host.
 #pragma once
 
@@ -40,6 +40,29 @@ inline bool symm_bucketed(int64_t m, int64_t k, int64_t nnz, int forced) {
     if (k != 1 || nnz <= 0 || m > kSymmMaxBucketRows || forced == 0) return false;
     if (forced < 0 && !(m > (int64_t(1) << 19) && m <= (int64_t(1) << 21))) return false;
     return symm_bucket_count(m, symm_bucket_bits(m, forced)) <= kSymmMaxBuckets;
+}
+
+// Split path of a single column past 2^21 rows: the transposed terms are
+// written as records grouped by ranges of 2^bits rows of Y (2^14 rows, a
+// 128 KiB accumulator of doubles in LDS; at most kSymmSplitMax ranges), each
+// tile's records sorted by range so that every range gets one contiguous run,
+// then every range summed in LDS.
+constexpr int kSymmSplitMax = 1024;
+constexpr int kSymmSplitBits = 14;
+
+// forced: 0 for the default 2^14 rows per range, else that many bits (at
+// most 14)
+inline int symm_split_bits(int64_t, int forced) {
+    return forced > 0 && forced < kSymmSplitBits ? forced : kSymmSplitBits;
+}
+
+// forced: -1 unforced (past 2^21 rows), 0 never, 1 always (single columns);
+// never past kSymmSplitMax ranges of the range size
+inline bool symm_split(int64_t m, int64_t k, int64_t nnz, int forced, int forced_bits = 0) {
+    if (k != 1 || nnz <= 0 || m <= 0 || forced == 0) return false;
+    const int bits = symm_split_bits(m, forced_bits);
+    if (((m + (int64_t(1) << bits) - 1) >> bits) > kSymmSplitMax) return false;
+    return forced == 1 || m > (int64_t(1) << 21);
 }
 
 }  // namespace spsyrk

@@ -4,6 +4,7 @@
 // tables hold, and the bucket size stays in 2^12 .. 2^14 rows.
 #include <cstdio>
 #include <cstdint>
+#include <initializer_list>
 
 #include "symm_layout.h"
 
@@ -39,6 +40,24 @@ int main() {
             }
             // more than one column never takes buckets
             if (symm_bucketed(m, 2, 10, 1)) return 1;
+        }
+    }
+    // the range split: ranges of at most 2^14 rows (the LDS accumulator), at
+    // most kSymmSplitMax of them, covering all m rows
+    for (int p = 0; p <= 31; ++p) {
+        for (int64_t d = -1; d <= 1; ++d) {
+            const int64_t m = (int64_t(1) << p) + d;
+            if (m < 1) continue;
+            for (int f : {0, 1, 8, 10, 14, 20}) {
+                const int bits = symm_split_bits(m, f);
+                const int64_t nr = (m + (int64_t(1) << bits) - 1) >> bits;
+                const bool on = symm_split(m, 1, 10, 1, f);
+                if (bits < 1 || bits > kSymmSplitBits || (on && (nr < 1 || nr > kSymmSplitMax))) {
+                    std::printf("bad split m=%lld forced=%d bits=%d ranges=%lld\n", (long long)m, f, bits, (long long)nr);
+                    return 1;
+                }
+                if (symm_split(m, 2, 10, 1, f)) return 1;  // one column only
+            }
         }
     }
     std::printf("ok %ld settings, %ld bucketed\n", checked, bucketed);

@@ -164,10 +164,11 @@ def test_oom_at_every_allocation_two_pass(dev, monkeypatch):
                                                  ctypes.byref(o)), "offdiag two-pass")
 
 
-@pytest.mark.parametrize("buckets", ["0", "12"])
-def test_oom_at_every_allocation_symm(dev, buckets, monkeypatch):
+@pytest.mark.parametrize("buckets,split", [("0", "0"), ("12", "0"), ("0", "1")])
+def test_oom_at_every_allocation_symm(dev, buckets, split, monkeypatch):
     import torch
     monkeypatch.setenv("SPSYRK_SYMM_BUCKETS", buckets)
+    monkeypatch.setenv("SPSYRK_SYMM_SPLIT", split)
     lib = sp.library()
     C = sp.lower(_dev_csr(_hub_matrix(6), dev), "f64")
     c = _struct(C)
@@ -178,7 +179,7 @@ def test_oom_at_every_allocation_symm(dev, buckets, monkeypatch):
     def call(al, o):
         return lib.spsyrk_symm(ctypes.byref(c), 0, 1, ctypes.c_void_p(X.data_ptr()), 1,
                                ctypes.c_void_p(Y.data_ptr()), 1, ctypes.byref(al.struct), s)
-    _sweep(dev, call, f"symm buckets={buckets}")
+    _sweep(dev, call, f"symm buckets={buckets} split={split}")
 
 
 @pytest.mark.parametrize("semiring", ["f64", "count"])

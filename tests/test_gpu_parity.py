@@ -539,6 +539,38 @@ def test_symm_vector_buckets(dev, semiring, bits, monkeypatch):
     _check_symm(y[:, None], ref, scale, semiring, "symm buckets")
 
 
+@pytest.mark.parametrize("semiring,bits", [("f64", "10"), ("f32", "11"), ("count", "10"), ("jaccard", "12"),
+                                           ("f64", "0")])
+def test_symm_vector_split(dev, semiring, bits, monkeypatch):
+    # the product with one column with its transposed term written as records
+    # grouped by row ranges and added range by range (forced at this size:
+    # ranges of 2^10 to 2^12 rows, so 12 to 3 of them and, at 2^10, two launches
+    # of eight ranges; "0": one range of 2^18 rows), empty rows
+    import torch
+    monkeypatch.setenv("SPSYRK_SYMM_SPLIT", "1")
+    monkeypatch.setenv("SPSYRK_SYMM_BUCKETS", "0")
+    monkeypatch.setenv("SPSYRK_SYMM_SPLIT_BITS", bits)
+    rng = np.random.default_rng(51)
+    vdt = VDT[semiring]
+    xdt = np.float64 if semiring in ("f64", "count") else np.float32
+    A = _rows_csr(rng, 12000, 4000, 5)
+    A = A.with_values(rng.standard_normal(A.nnz))
+    keep = np.ones(A.nrows, dtype=bool)
+    keep[rng.choice(A.nrows, size=300, replace=False)] = False
+    D = np.zeros(A.nrows + 1, dtype=np.int64)
+    np.cumsum(np.diff(A.row_ptr) * keep, out=D[1:])
+    sel = np.repeat(keep, np.diff(A.row_ptr))
+    A = CSR(A.nrows, A.ncols, D, A.col_idx[sel], A.values[sel])
+    Ah = A.with_values(A.values.astype(vdt) if vdt is not None else None)
+    C = sp.lower(upload(A, semiring, dev), semiring)
+    L = oracle.lower(Ah, semiring)
+    print(f"[symm split {semiring} {bits}] m={A.nrows} nnz_L={L.nnz}", flush=True)
+    x = rng.standard_normal(A.nrows).astype(xdt)
+    y = sp.symm(C, torch.from_numpy(x).to(dev), semiring).cpu().numpy()
+    ref, scale = _symm_ref(L, x.astype(np.float64)[:, None])
+    _check_symm(y[:, None], ref, scale, semiring, "symm split")
+
+
 def test_symm_rejects_upper_entries(dev):
     import torch
     P = csr_from_dense(np.array([[1.0, 2.0], [0.0, 3.0]]))
