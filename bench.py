@@ -31,7 +31,8 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak, GB/s
 METRIC = "useful GFLOP/s + output nnz/s for tril(A*A^T); % of HBM roofline, 1 GPU"
 V_IN = {"f64": 8, "f32": 4, "count": 0, "jaccard": 0}       # bytes per value of A
 V_OUT = {"f64": 8, "f32": 4, "count": 4, "jaccard": 4}      # bytes per value of C
-V_CX = {"f64": 8, "f32": 4, "count": 0, "jaccard": 4}       # bytes per value in the column index
+V_CX = {"f64": 8, "f32": 4, "count": 0, "jaccard": 0}       # bytes per value in the column index
+# (Jaccard keys carry the partner's row length; no value array)
 
 
 def parse():

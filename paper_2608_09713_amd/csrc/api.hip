@@ -277,7 +277,10 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
 
     cx.gptr = runs_given ? nullptr : ar.get_t<uint32_t>(cx.ngroups + 1);
     cx.key = ar.get_t<uint32_t>(N > 0 ? N : 1);
-    cx.val = vb_out ? ar.get(size_t(N > 0 ? N : 1) * vb_out) : nullptr;
+    // with every partner run given, Jaccard keys carry the row lengths
+    // (the row field's spare bits) and no value array is kept
+    if (sr == kJaccard && runs_given) cx.lenbits = 32 - cx.rowbits;
+    cx.val = vb_out && cx.lenbits == 0 ? ar.get(size_t(N > 0 ? N : 1) * vb_out) : nullptr;
 
     if (N > 0) {
         // records (column, row, entry index) sorted by column; values are
@@ -480,6 +483,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     fa.val = L.v;
     fa.cx = cx;
     fa.m_right = R.m;
+    fa.rp_right = R.rp;
     fa.lower = lower;
     fa.sr = sr;
     fa.prod = prod;
@@ -982,6 +986,7 @@ void lower_execute(const LowerPlan& P, const void* vals, Arena& ar, hipStream_t 
     fa.val = vals;
     fa.cx = P.cx;
     fa.m_right = m;
+    fa.rp_right = P.rp;
     fa.lower = true;
     fa.sr = P.sr;
     fa.prod = P.prod;

@@ -142,11 +142,19 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
             if (last) continue;
             q = p - cols_before;
         }
-        key[q] = ((col & gmask) << rowbits) | row;
         if (vsrc) vsrc[q] = sent[p];
         if constexpr (JAC) {
-            const uint32_t lf = lenbits > 0 ? field >> rowbits : lmax;
-            static_cast<int32_t*>(val)[q] = lf < lmax ? int32_t(lf) : int32_t(rp_b[row + 1] - rp_b[row]);
+            if (!val) {
+                key[q] = field;  // (no directory) the row and its saturated length
+            } else {
+                key[q] = ((col & gmask) << rowbits) | row;
+                const uint32_t lf = lenbits > 0 ? field >> rowbits : lmax;
+                static_cast<int32_t*>(val)[q] = lf < lmax ? int32_t(lf) : int32_t(rp_b[row + 1] - rp_b[row]);
+            }
+        } else {
+            key[q] = ((col & gmask) << rowbits) | row;
+        }
+        if constexpr (JAC) {
         } else if constexpr (VB == 8) {
             static_cast<uint64_t*>(val)[q] = static_cast<const uint64_t*>(vals_b)[sent[p]];
         } else if constexpr (VB == 4) {

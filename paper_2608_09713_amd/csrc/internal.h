@@ -58,6 +58,10 @@ struct ColIndex {
     uint32_t* key = nullptr;
     void* val = nullptr;    // double / float values of B, or int32 row lengths of B (Jaccard)
     uint32_t* gptr = nullptr;  // null when every entry's partner run is given (no lookups)
+    // > 0 (Jaccard with every partner run given): each key also carries its
+    // row's length above the row bits, saturated at 2^lenbits - 1 (the full
+    // length then comes from the row pointers), and val is null
+    int lenbits = 0;
 };
 
 // ---- scan.hip
@@ -94,7 +98,7 @@ size_t radix_csr_tmp_bytes(int64_t n, int nbits);
 struct LocalPack {
     uint2* run = nullptr;
     uint32_t* key = nullptr;
-    void* val = nullptr;
+    void* val = nullptr;         // null for Jaccard: the keys carry the row lengths (the row field)
     const void* vals_b = nullptr;  // values of B by entry index (vbytes 4 or 8)
     const int64_t* rp_b = nullptr; // row pointers of B (Jaccard lengths)
     int vbytes = 0;
@@ -167,6 +171,7 @@ struct FusedArgs {
     int64_t m_right = 0;
     bool lower = true;
     int sr = kF64;
+    const int64_t* rp_right = nullptr;         // row pointers of the right operand (Jaccard lengths)
     const unsigned long long* prod = nullptr;  // off-diagonal products per row
     const uint2* run = nullptr;                // partner run {first, end} of every entry
     const int64_t* heavy_nnz = nullptr;        // output lengths of heavy rows

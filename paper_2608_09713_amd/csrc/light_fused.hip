@@ -171,11 +171,13 @@ struct Chunk {
     int64_t r0 = 0;
     int lane;
     uint32_t rowmask;
+    uint32_t lenmax;  // saturated length in a key (Jaccard keys carrying lengths)
     int jbits_right;
 
     __device__ Chunk(const FusedArgs& a_, WaveLds<Item>& L_) : a(a_), L(L_) {
         lane = lane_id();
         rowmask = a.cx.rowbits >= 32 ? 0xffffffffu : ((1u << a.cx.rowbits) - 1u);
+        lenmax = a.cx.lenbits > 0 ? ((a.cx.lenbits >= 32 ? 0xffffffffu : (1u << a.cx.lenbits) - 1u)) : 0u;
         jbits_right = bit_width_u64(a.m_right > 1 ? uint64_t(a.m_right - 1) : 0);
     }
 
@@ -314,7 +316,7 @@ struct Chunk {
                 const uint32_t pos = L.ent_start[x] + uint32_t(t - L.ent_poff[x]);
                 pj[v] = key[pos];
                 if constexpr (SR == kJaccard) {
-                    pv[v] = static_cast<const int32_t*>(a.cx.val)[pos];
+                    if (!a.cx.lenbits) pv[v] = static_cast<const int32_t*>(a.cx.val)[pos];
                 } else if constexpr (kVal) {
                     pv[v] = double(static_cast<const In*>(a.val)[ebase + x]) *
                             double(static_cast<const In*>(a.cx.val)[pos]);
@@ -328,6 +330,13 @@ struct Chunk {
             const int t = lane + v * kWave;
             if (t < P) {
                 const uint32_t j = pj[v] & rowmask;
+                if constexpr (SR == kJaccard) {
+                    if (a.cx.lenbits) {
+                        // the partner's length from its key; saturated: from the row pointers
+                        const uint32_t lf = pj[v] >> a.cx.rowbits;
+                        pv[v] = lf < lenmax ? int32_t(lf) : int32_t(a.rp_right[j + 1] - a.rp_right[j]);
+                    }
+                }
                 const int r = int(pb[v]);
                 pj[v] = j;
                 const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);

@@ -542,13 +542,18 @@ __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t fie
     if (pk.vsrc) pk.vsrc[pos] = ent;
     const uint32_t rowmask = pk.rowbits >= 32 ? 0xffffffffu : ((1u << pk.rowbits) - 1u);
     const uint32_t row = field & rowmask;
-    pk.key[pos] = row;
     if constexpr (JAC) {
-        const uint32_t lmax = pk.lenbits > 0 ? (1u << pk.lenbits) - 1u : 0u;
-        const uint32_t lf = pk.lenbits > 0 ? field >> pk.rowbits : lmax;
-        static_cast<int32_t*>(pk.val)[pos] = lf < lmax ? int32_t(lf) : int32_t(pk.rp_b[row + 1] - pk.rp_b[row]);
-    } else if constexpr (VB != 0) {
-        static_cast<typename ValT<VB>::T*>(pk.val)[pos] = v;
+        if (!pk.val) {
+            pk.key[pos] = field;  // the row and its saturated length
+        } else {
+            pk.key[pos] = row;
+            const uint32_t lmax = pk.lenbits > 0 ? (1u << pk.lenbits) - 1u : 0u;
+            const uint32_t lf = pk.lenbits > 0 ? field >> pk.rowbits : lmax;
+            static_cast<int32_t*>(pk.val)[pos] = lf < lmax ? int32_t(lf) : int32_t(pk.rp_b[row + 1] - pk.rp_b[row]);
+        }
+    } else {
+        pk.key[pos] = row;
+        if constexpr (VB != 0) static_cast<typename ValT<VB>::T*>(pk.val)[pos] = v;
     }
     if (pk.run && pos > cstart) pk.run[ent] = make_uint2(uint32_t(cstart), uint32_t(pos));
 }
