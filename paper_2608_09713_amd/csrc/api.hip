@@ -443,6 +443,13 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     const int64_t light_cap = int64_t(h.light_cap);
     HeavyArgs ha;
     int64_t* heavy_nnz = nullptr;
+    if (nheavy > 1) {
+        // the rows with the most products first, so that none starts last
+        void* otmp = ar.get(heavy_order_tmp_bytes(nheavy));
+        heavy_order(heavy_rows, nheavy, prod, otmp, s);
+        check_launch();
+        ar.release(otmp);
+    }
     if (nheavy > 0) {
         heavy_nnz = ar.get_t<int64_t>(m);
         ha.m = m;

@@ -220,6 +220,12 @@ size_t compact_tmp_bytes(int64_t staged);
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
                   const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
                   hipStream_t s);
+// Reorders the heavy-row list rows[0..n) by decreasing magnitude of their
+// product counts (powers of two; stable inside one), so that the rows with
+// the most work are taken first from the heavy kernels' queue.
+// tmp: heavy_order_tmp_bytes(n)
+size_t heavy_order_tmp_bytes(int64_t n);
+void heavy_order(int32_t* rows, int64_t n, const unsigned long long* prod, void* tmp, hipStream_t s);
 // Over the rows listed in rows[0..n): adds the entries of A (rp) to out[0]
 // and the output entries (c_rp) to out[1] (zeroed beforehand).
 void heavy_sums(const int32_t* rows, int64_t n, const int64_t* rp, const int64_t* c_rp, unsigned long long* out,

@@ -352,6 +352,33 @@ void heavy_sums(const int32_t* rows, int64_t n, const int64_t* rp, const int64_t
     heavy_sums_kernel<<<unsigned(grid), kBlock, 0, s>>>(rows, n, rp, c_rp, out);
 }
 
+namespace {
+// sort key of a heavy row: rows with more products first (63 - bits of the count)
+__global__ __launch_bounds__(kBlock) void heavy_order_keys(const int32_t* __restrict__ rows, int64_t n,
+                                                           const unsigned long long* __restrict__ prod,
+                                                           uint32_t* __restrict__ key) {
+    const int64_t q = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (q < n) key[q] = uint32_t(63 - bit_width_u64(prod[rows[q]]));
+}
+}  // namespace
+
+size_t heavy_order_tmp_bytes(int64_t n) {
+    return 3 * ((size_t(n) * sizeof(uint32_t) + 255) & ~size_t(255)) + radix_tmp_bytes(n);
+}
+
+void heavy_order(int32_t* rows, int64_t n, const unsigned long long* prod, void* tmp, hipStream_t s) {
+    if (n <= 1) return;
+    const size_t a = (size_t(n) * sizeof(uint32_t) + 255) & ~size_t(255);
+    uint32_t* ka = static_cast<uint32_t*>(tmp);
+    uint32_t* kb = reinterpret_cast<uint32_t*>(static_cast<char*>(tmp) + a);
+    uint32_t* rb = reinterpret_cast<uint32_t*>(static_cast<char*>(tmp) + 2 * a);
+    void* rtmp = static_cast<char*>(tmp) + 3 * a;
+    heavy_order_keys<<<unsigned((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(rows, n, prod, ka);
+    uint32_t* ra = reinterpret_cast<uint32_t*>(rows);
+    if (radix_sort(ka, kb, ra, rb, nullptr, nullptr, 0, n, 6, rtmp, s))
+        (void)hipMemcpyAsync(rows, rb, size_t(n) * sizeof(uint32_t), hipMemcpyDeviceToDevice, s);
+}
+
 void tile_first_rows(const int64_t* rp, int64_t m, int64_t T, int64_t* trow, hipStream_t s) {
     if (m <= 0) return;
     tile_rows<<<unsigned((m + kBlock - 1) / kBlock), kBlock, 0, s>>>(rp, m, T, trow);
