@@ -739,9 +739,10 @@ struct Slab {
 };
 
 // Column slabs of at most cap strict-lower entries (a single column may hold
-// more: it is a slab of its own), chosen from bucket histograms; a bucket
-// over the cap is split by a finer histogram of its own columns.
-std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, const int64_t* trow, Arena& ar, hipStream_t s) {
+// more: it is a slab of its own) and at most wcap columns (wcap a multiple of
+// the buckets' width), chosen from bucket histograms; a bucket over the cap
+// is split by a finer histogram of its own columns.
+std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, int64_t wcap, Arena& ar, hipStream_t s) {
     unsigned long long* hist = ar.get_t<unsigned long long>(kMirrorBins);
     std::vector<unsigned long long> h(kMirrorBins);
     std::vector<Slab> pieces;  // buckets (or single columns) in column order
@@ -750,7 +751,7 @@ std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, const int64_t* t
         int cb = 0;
         while (((w + (int64_t(1) << cb) - 1) >> cb) > kMirrorBins) ++cb;
         const int nb = int((w + (int64_t(1) << cb) - 1) >> cb);
-        mirror_coarse_hist(ma, lo, cb, nb, trow, hist, s);
+        mirror_coarse_hist(ma, lo, cb, nb, hist, s);
         check_launch();
         HIPCHK(hipMemcpyAsync(h.data(), hist, size_t(nb) * sizeof(unsigned long long), hipMemcpyDeviceToHost, s));
         HIPCHK(hipStreamSynchronize(s));
@@ -769,7 +770,7 @@ std::vector<Slab> plan_slabs(const MirrorArgs& ma, int64_t cap, const int64_t* t
     Slab cur{0, 0, 0, 0};
     int64_t before = 0;
     for (const Slab& p : pieces) {
-        if (cur.c1 > cur.c0 && cur.nrec + p.nrec > cap) {
+        if (cur.c1 > cur.c0 && (cur.nrec + p.nrec > cap || p.c1 - cur.c0 > wcap)) {
             out.push_back(cur);
             cur = {p.c0, p.c0, 0, before};
         }
@@ -805,6 +806,20 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     // and starts of the slab's rows, and every record placed after the lower
     // part of its row.  The lower rows are copied once all starts are known.
     const int64_t cap = mirror_slab_cap();
+    // Slabs of at most 2^16 columns sort in two 8-bit passes instead of
+    // three: worth it when the records are many per row (each slab costs a
+    // walk over every row's pointers).
+    // (SPSYRK_MIRROR_NARROW=b, 1 <= b <= 16, read at every call: always
+    // narrow, 2^b columns; 0: never)
+    int64_t nwidth = kMirrorNarrow;
+    const int64_t nslab16 = (m + kMirrorNarrow - 1) / kMirrorNarrow;
+    bool narrow = nslab16 > 1 && L.nnz / 64 >= m * nslab16;
+    if (const char* e = std::getenv("SPSYRK_MIRROR_NARROW")) {
+        const int b = std::atoi(e);
+        narrow = b >= 1 && b <= 16;
+        if (narrow) nwidth = int64_t(1) << b;
+    }
+    const int64_t wcap = narrow ? nwidth : std::max<int64_t>(m, 1);
     // row of every tile start of the walks over C_L's entries
     int64_t* trow = ar.get_t<int64_t>(int64_t(mirror_tile_bytes(L.nnz) / sizeof(int64_t)));
     mirror_tile_rows(L.rp, m, trow, s);
@@ -814,7 +829,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
     std::vector<Slab> slabs;
     {
         Phase ph(SPSYRK_PHASE_MIRROR_COUNT, s);
-        if (L.nnz <= cap) {
+        if (L.nnz <= cap && !narrow) {
             // one slab; its record count is the strict-lower count
             HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
             mirror_slab_counts(ma, 0, m, row_cnt, row_lo, s);
@@ -823,7 +838,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
             const Ctl h = read_ctl(ctl, s);
             slabs.push_back({0, m, h.total, 0});
         } else {
-            slabs = plan_slabs(ma, cap, trow, ar, s);
+            slabs = plan_slabs(ma, cap, wcap, ar, s);
         }
     }
     int64_t nstrict = 0, rec_max = 0, w_max = 0;
@@ -852,7 +867,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
         const Slab& sl = slabs[k];
         if (sl.c1 <= sl.c0) continue;
         Phase ph(SPSYRK_PHASE_MIRROR_TRANSPOSE, s);
-        if (k > 0 || L.nnz > cap) {
+        if (k > 0 || L.nnz > cap || narrow) {
             HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
             mirror_slab_counts(ma, sl.c0, sl.c1, row_cnt, row_lo, s);
             scan_i64(row_cnt, row_cnt, m + 1, &ctl->total, stmp, s);

@@ -61,8 +61,12 @@ __device__ inline uint32_t scan_hb(uint32_t v, uint32_t* wt, uint32_t* total) {
     return off + inc - v;
 }
 
+// Three workgroups of the numeric pass share a compute unit by their LDS;
+// that takes six wavefronts per SIMD, i.e. at most 80 VGPRs (with 88, only two
+// workgroups fit and the pass takes about 40% longer).
 template <int SR, bool NUM, bool LOWER>
-__global__ __launch_bounds__(kHB, NUM ? 4 : 8) void heavy_kernel(HeavyArgs a, int* queue) {
+__global__ __launch_bounds__(kHB) __attribute__((amdgpu_waves_per_eu(NUM ? 6 : 8)))
+void heavy_kernel(HeavyArgs a, int* queue) {
     using Tr = SrTraits<SR>;
     using In = typename Tr::In;
     using Acc = typename Tr::Acc;

@@ -308,8 +308,10 @@ struct MirrorArgs {
 // strict-lower entries with clo <= col < clo + nb * 2^cb per bucket of 2^cb
 // columns (nb <= kMirrorBins), added into hist (zeroed here)
 constexpr int kMirrorBins = 4096;
-void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, const int64_t* trow,
-                        unsigned long long* hist, hipStream_t s);
+// columns of a narrow transpose slab (its keys sort in two 8-bit passes)
+constexpr int64_t kMirrorNarrow = int64_t(1) << 16;
+void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsigned long long* hist,
+                        hipStream_t s);
 // row of every tile start of the mirror's walks over positions [0, rp[m])
 // (trow: mirror_tile_bytes(rp[m]))
 size_t mirror_tile_bytes(int64_t positions);

@@ -185,51 +185,61 @@ __global__ __launch_bounds__(kBlock) void slab_place(const int64_t* __restrict__
 }
 
 // Strict-lower entries with clo <= col < clo + nb * 2^cb per bucket of 2^cb
-// columns (nb <= kMirrorBins), for choosing column slabs: LDS counters per
-// workgroup over a grid-stride walk of tiles, then one global add per
-// non-empty bucket.
+// columns (nb <= kMirrorBins), for choosing column slabs.  Every entry of the
+// lower part is counted by its column, from coalesced loads, and the diagonal
+// entry of every row is taken off again (the strict lower part is the lower
+// part without its diagonal).  Consecutive lanes that fall in one bucket form
+// a run that its first lane adds at once, so a row's dense stretch costs one
+// LDS add, not one per lane.  LDS counters per workgroup, then one global add
+// per non-empty bucket.
+__device__ inline void add_bucket_runs(int32_t* cnt, int b, int sign) {
+    const int lane = lane_id();
+    const int pb = __shfl_up(b, 1, kWave);
+    const uint64_t starts = __ballot(lane == 0 || pb != b);
+    if (b >= 0 && (lane == 0 || pb != b)) {
+        const uint64_t after = lane == kWave - 1 ? 0 : (starts >> (lane + 1));
+        const int len = after ? __ffsll((long long)after) : kWave - lane;
+        atomicAdd(&cnt[b], sign * len);
+    }
+}
+
+constexpr int kHistU = 4;  // 64-entry stretches per wavefront in flight
+
 __global__ __launch_bounds__(kBlock) void coarse_hist(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
                                                       int64_t m, int64_t nnz, int64_t clo, int cb, int nb,
-                                                      const int64_t* __restrict__ trow,
                                                       unsigned long long* __restrict__ hist) {
-    __shared__ uint32_t cnt[kMirrorBins];
-    __shared__ int64_t win[kWin + 1];
-    __shared__ int64_t bounds[2];
+    __shared__ int32_t cnt[kMirrorBins];
     for (int x = threadIdx.x; x < nb; x += kBlock) cnt[x] = 0;
     __syncthreads();
-    for (int64_t e0 = int64_t(blockIdx.x) * kTileC; e0 < nnz; e0 += int64_t(gridDim.x) * kTileC) {
-        const int64_t e1 = min(nnz, e0 + kTileC);
-        RowFinder f = make_finder(rp, m, e0, e1, win, bounds, trow, e0 / kTileC, nnz);
-        const int64_t ea = e0 + int64_t(threadIdx.x) * kPerC;
-        const int64_t eb = min(e1, ea + kPerC);
-        if (ea < eb) {
-            int64_t r = f.row_of(ea);
-            int64_t rend = rp[r + 1];
-            // columns ascend inside a row: count runs of one bucket, add once per run
-            int64_t run_b = -1;
-            uint32_t run_n = 0;
-            for (int64_t e = ea; e < eb; ++e) {
-                while (e >= rend) {
-                    ++r;
-                    rend = rp[r + 1];
-                }
-                const int64_t c = int64_t(ci[e]);
-                const int64_t b = (c - clo) >> cb;
-                if (c < r && c >= clo && b < nb) {
-                    if (b != run_b) {
-                        if (run_n) atomicAdd(&cnt[run_b], run_n);
-                        run_b = b;
-                        run_n = 0;
-                    }
-                    ++run_n;
-                }
-            }
-            if (run_n) atomicAdd(&cnt[run_b], run_n);
+    const int lane = lane_id();
+    const int64_t span = int64_t(nb) << cb;
+    auto bucket = [&](int64_t c) -> int { return (c >= clo && c - clo < span) ? int((c - clo) >> cb) : -1; };
+    const int64_t waves = int64_t(gridDim.x) * (kBlock / kWave);
+    const int64_t wid = int64_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave;
+    // every entry, by column
+    for (int64_t base = wid * (kWave * kHistU); base < nnz; base += waves * (kWave * kHistU)) {
+        int32_t c[kHistU];
+#pragma unroll
+        for (int u = 0; u < kHistU; ++u) {
+            const int64_t e = base + u * kWave + lane;
+            c[u] = e < nnz ? ci[e] : -1;
         }
-        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kHistU; ++u) add_bucket_runs(cnt, c[u] >= 0 ? bucket(c[u]) : -1, 1);
     }
+    // less the diagonal entries
+    for (int64_t r0 = wid * kWave; r0 < m; r0 += waves * kWave) {
+        const int64_t r = r0 + lane;
+        int b = -1;
+        if (r < m) {
+            const int64_t a = rp[r], z = rp[r + 1];
+            if (z > a && int64_t(ci[z - 1]) == r) b = bucket(r);
+        }
+        add_bucket_runs(cnt, b, -1);
+    }
+    __syncthreads();
     for (int x = threadIdx.x; x < nb; x += kBlock)
-        if (cnt[x]) atomicAdd(&hist[x], (unsigned long long)cnt[x]);
+        if (cnt[x]) atomicAdd(&hist[x], (unsigned long long)(long long)cnt[x]);
 }
 
 // column runs of a sorted slab: first[k] / end[k] = first / one-past-last
@@ -284,13 +294,13 @@ void mirror_copy_lower(const MirrorArgs& a, int64_t ebeg, int64_t eend, const in
         copy_lower<0><<<nb, kBlock, 0, s>>>(a.rp, a.ci, a.val, a.m, ebeg, eend, trow, f_rp, f_ci, f_val);
 }
 
-void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, const int64_t* trow,
-                        unsigned long long* hist, hipStream_t s) {
+void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsigned long long* hist,
+                        hipStream_t s) {
     (void)hipMemsetAsync(hist, 0, size_t(nb) * sizeof(unsigned long long), s);
-    if (a.nnz <= 0) return;
+    if (a.nnz <= 0 || a.m <= 0) return;
     int64_t grid = (a.nnz + kTileC - 1) / kTileC;
     if (grid > 2048) grid = 2048;
-    coarse_hist<<<unsigned(grid), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, clo, cb, nb, trow, hist);
+    coarse_hist<<<unsigned(grid), kBlock, 0, s>>>(a.rp, a.ci, a.m, a.nnz, clo, cb, nb, hist);
 }
 
 void mirror_slab_columns(const MirrorArgs& a, int64_t c0, int64_t c1, const uint32_t* skey, int64_t nrec,

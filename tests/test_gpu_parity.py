@@ -629,6 +629,25 @@ def test_mirror_column_slabs(dev, cap, monkeypatch):
     np.testing.assert_array_equal(M.to_host()[1], ref.col_idx)
 
 
+@pytest.mark.parametrize("bits,cap", [(4, 1 << 31), (8, 1 << 31), (10, 3000)])
+def test_mirror_narrow_slabs(dev, bits, cap, monkeypatch):
+    # slabs of at most 2^bits columns (keys of at most 16 bits, two sort
+    # passes), with and without the record cap; the slab plan's histogram
+    # counts every entry by column and takes the diagonal off again
+    monkeypatch.setenv("SPSYRK_MIRROR_NARROW", str(bits))
+    monkeypatch.setenv("SPSYRK_MIRROR_SLAB", str(cap))
+    rng = np.random.default_rng(bits)
+    m = 5000
+    rp, ci, v = _random_lower(rng, m, 20, 7)
+    print(f"[mirror narrow] bits={bits} cap={cap} m={m} nnz={len(ci)}", flush=True)
+    ref = oracle.mirror(m, rp, ci, v)
+    M = sp.mirror(_raw(dev, rp, ci, m, v), "f64")
+    compare_full(M, ref, "f64", f"mirror narrow {bits}")
+    M = sp.mirror(_raw(dev, rp, ci, m, v.astype(np.float32)), "f32")
+    np.testing.assert_array_equal(M.to_host()[0], ref.row_ptr)
+    np.testing.assert_array_equal(M.to_host()[1], ref.col_idx)
+
+
 def test_mirror_structure_only(dev):
     import torch
     rng = np.random.default_rng(5)
@@ -656,7 +675,7 @@ def _raw(dev, rp, ci, n, vals=None):
     import torch
     return sp.DeviceCSR(len(rp) - 1, n, torch.tensor(rp, dtype=torch.int64, device=dev),
                         torch.tensor(ci, dtype=torch.int32, device=dev),
-                        None if vals is None else torch.tensor(vals, dtype=torch.float64, device=dev), rp[-1])
+                        None if vals is None else torch.tensor(vals, device=dev), rp[-1])
 
 
 def test_rejects_non_canonical_on_device(dev):

@@ -1,0 +1,67 @@
+"""Register and occupancy budgets of the hot kernels, read from the compiler's
+resource report for gfx950 (no GPU needed).
+
+The heavy-row numeric pass keeps three workgroups of 512 threads on a compute
+unit (its LDS allows three), which takes six wavefronts per SIMD, so at most
+80 VGPRs; at 88 only two workgroups fit and the pass runs about 40% longer.
+The symbolic pass keeps eight wavefronts per SIMD (64 VGPRs).  The light-row
+kernel keeps three wavefronts per SIMD for the plus-times semirings, at the
+price of a spill of a few words per lane (at two wavefronts per SIMD it needs
+175 VGPRs and no spill, and measures slower); the count and Jaccard kernels
+fit without one.  No other kernel here may spill.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2608_09713_amd import build
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+
+
+def _report(src):
+    flags = [f for f in build.FLAGS if f not in ("-shared",)]
+    cmd = [HIPCC, *flags, "--cuda-device-only", "-c", "-Rpass-analysis=kernel-resource-usage",
+           os.path.join(build.CSRC, src), "-o", os.devnull]
+    out = subprocess.run(cmd, capture_output=True, text=True, check=True).stderr
+    kernels = {}
+    name = None
+    for line in out.splitlines():
+        m = re.search(r"remark:\s+Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+            kernels[name] = {}
+            continue
+        m = re.search(r"remark:\s+(VGPRs|ScratchSize \[bytes/lane\]|Occupancy \[waves/SIMD\]): (\d+)", line)
+        if m and name:
+            kernels[name][m.group(1).split()[0]] = int(m.group(2))
+    return kernels
+
+
+pytestmark = pytest.mark.skipif(shutil.which(HIPCC) is None and not os.path.exists(HIPCC),
+                                reason="hipcc not available")
+
+
+def test_heavy_kernel_budgets():
+    ks = {k: v for k, v in _report("heavy.hip").items() if "heavy_kernel" in k}
+    assert len(ks) == 16  # four semirings x symbolic/numeric x lower/off-diagonal
+    for name, r in ks.items():
+        numeric = re.search(r"heavy_kernelILi\dELb1E", name) is not None
+        assert r["ScratchSize"] == 0, name
+        if numeric:
+            assert r["VGPRs"] <= 80 and r["Occupancy"] >= 6, (name, r)
+        else:
+            assert r["VGPRs"] <= 64 and r["Occupancy"] >= 8, (name, r)
+
+
+def test_light_kernel_budgets():
+    ks = {k: v for k, v in _report("light_fused.hip").items() if "fused_kernel" in k}
+    assert len(ks) == 8
+    for name, r in ks.items():
+        if re.search(r"fused_kernelILi[01]E", name):  # plus-times in f64 and f32
+            assert r["Occupancy"] >= 3 and r["ScratchSize"] <= 40, (name, r)
+        else:
+            assert r["Occupancy"] >= 3 and r["ScratchSize"] == 0, (name, r)
