@@ -880,9 +880,24 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
         const uint32_t* skey = ka;
         const uint32_t* srow = ra;
         const void* sval = va;
-        if (sl.nrec > 0) {
+        const int nbits = bit_width_u64(sl.c1 - sl.c0 > 1 ? uint64_t(sl.c1 - sl.c0 - 1) : 0);
+        // keys of at most 16 bits: the sort reads the records straight from
+        // C_L and its last pass puts them into the full rows; wider keys go
+        // through extracted records, passes and a placement
+        const bool fused = nbits <= 16;
+        if (sl.nrec > 0 && fused) {
+            SlabIo io;
+            io.ci = L.ci;
+            io.val = vb ? L.v : nullptr;
+            io.row_lo = row_lo;
+            io.c0 = sl.c0;
+            io.rp = L.rp;
+            io.before = sl.before;
+            io.f_ci = f_ci;
+            io.f_val = f_val;
+            skey = slab_sort_place(io, vb, sl.nrec, nbits, row_cnt, m, ka, kb, ra, va, rtmp, s);
+        } else if (sl.nrec > 0) {
             mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, strow, ka, ra, va, s);
-            const int nbits = bit_width_u64(sl.c1 - sl.c0 > 1 ? uint64_t(sl.c1 - sl.c0 - 1) : 0);
             if (radix_sort(ka, kb, ra, rb, va, vbb, vb, sl.nrec, nbits, rtmp, s)) {
                 skey = kb;
                 srow = rb;
@@ -891,7 +906,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
         }
         // row_cnt is free again: full lengths of the slab's rows
         mirror_slab_columns(ma, sl.c0, sl.c1, skey, sl.nrec, first, endc, row_cnt, sl.before, f_rp, stmp, s);
-        mirror_slab_place(ma, sl.c0, sl.nrec, skey, srow, sval, first, f_rp, f_ci, f_val, s);
+        if (!fused) mirror_slab_place(ma, sl.c0, sl.nrec, skey, srow, sval, first, f_rp, f_ci, f_val, s);
         check_launch();
     }
     {

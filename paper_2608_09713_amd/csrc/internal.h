@@ -296,6 +296,28 @@ size_t symm_tmp_bytes(int64_t m, int64_t k, int64_t nnz, int mode);
 void symm_product(const DevCsr& C, int sr, const void* x, int64_t ldx, int64_t k, void* y, int64_t ldy, void* tmp,
                   int mode, hipStream_t s);
 
+// ---- the mirror's slab sort (radix.hip)
+// The mirror slab behind a fused sort: record p of row r (rows from the
+// record pointers rec_rp) is entry row_lo[r] + (p - rec_rp[r]) of C_L, with
+// key = column - c0; the record at sorted position q goes to the full rows at
+// before + q + rp[c0 + key + 1] (its column's lower part, then the column's
+// strict entries in row order).
+struct SlabIo {
+    const int32_t* ci = nullptr;      // C_L's columns
+    const void* val = nullptr;        // C_L's values or null
+    const int64_t* row_lo = nullptr;  // first entry of every row in the slab
+    int64_t c0 = 0;                   // the slab's first column
+    const int64_t* rp = nullptr;      // C_L's row pointers
+    int64_t before = 0;               // strict entries of the columns before c0
+    int32_t* f_ci = nullptr;          // full rows
+    void* f_val = nullptr;
+};
+// Sort of a slab of nrec records with keys of nbits <= 16 bits (one or two
+// passes) into the full rows; returns the buffer with the sorted keys (key_a
+// or key_b).  tmp: radix_tmp_bytes(nrec).
+uint32_t* slab_sort_place(const SlabIo& io, int vbytes, int64_t nrec, int nbits, const int64_t* rec_rp, int64_t m,
+                          uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, void* val_a, void* tmp, hipStream_t s);
+
 // ---- mirror.hip
 struct MirrorArgs {
     int64_t m = 0;

@@ -10,6 +10,7 @@
 // per-wave LDS counters, the tile is reordered through LDS, then written out
 // so that consecutive threads store consecutive addresses of a digit's run.
 #include <cstdlib>
+#include <type_traits>
 
 #include "common.h"
 #include "internal.h"
@@ -88,11 +89,80 @@ __device__ inline int64_t last_leq_i64(const int64_t* a, int64_t lo, int64_t hi,
     return lo;
 }
 
-// FIRST: the records come straight from a CSR matrix: key = column, row from
-// the row pointers (rp, m), value = the entry's index (VB must be 4).  With
-// lenbits > 0 the row field also carries the row's length, saturated at
-// 2^lenbits - 1, above its low rowbits bits.
-template <int VB, bool FIRST>
+// Where a pass takes its records from (SRC) and puts them (OUT).
+//  kSrcArrays: key, row and value arrays.
+//  kSrcCsr: straight from a CSR matrix: key = column, row from the row
+//    pointers (rp, m), value = the entry's index (VB must be 4).  With
+//    lenbits > 0 the row field also carries the row's length, saturated at
+//    2^lenbits - 1, above its low rowbits bits.
+//  kSrcSlab: a mirror slab's strict-lower entries, record p of row r (rows
+//    from the record pointers rp = rec_rp) being entry sl.row_lo[r] +
+//    (p - rec_rp[r]) of C_L: key = column - sl.c0, row = r, value = the
+//    entry's value.
+//  kOutArrays: key, row and value arrays in the pass's order.
+//  kOutPlace (last pass of a mirror slab): keys to key_out; the row and
+//    value of the record at sorted position q to the full rows, at
+//    sl.before + q + sl.rp[sl.c0 + key + 1] (its column's lower part, then
+//    the strict entries of the column in row order).
+constexpr int kSrcArrays = 0, kSrcCsr = 1, kSrcSlab = 2;
+constexpr int kOutArrays = 0, kOutPlace = 1;
+
+// Digit counts of the first pass over a mirror slab (kSrcSlab): every key
+// read through its record's row (an LDS window of the record pointers rp, or
+// a search when the tile spans too many rows).
+__global__ __launch_bounds__(kBlock) void radix_hist_slab(int64_t n, uint32_t mask, uint32_t* __restrict__ hist,
+                                                          int64_t ntiles, const int64_t* __restrict__ rp, int64_t m,
+                                                          const int64_t* __restrict__ trow, SlabIo sl) {
+    __shared__ uint32_t cnt[kWavesPerBlock][kDigits];
+    __shared__ int64_t rwin[kRowWin + 1];
+    __shared__ int64_t rb[2];
+    const int w = threadIdx.x / kWave;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) cnt[q][threadIdx.x] = 0;
+    const int64_t tile = blockIdx.x;
+    const int64_t base = tile * kRTile;
+    if (threadIdx.x == 0) {
+        rb[0] = trow[tile];
+        rb[1] = base + kRTile < n ? trow[tile + 1] : last_leq_i64(rp, trow[tile], m, n - 1);
+    }
+    __syncthreads();
+    const int64_t rlo = rb[0], rhi = rb[1];
+    const bool staged = rhi - rlo + 2 <= kRowWin + 1;
+    if (staged)
+        for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) rwin[k] = rp[rlo + k];
+    __syncthreads();
+#pragma unroll 4
+    for (int k = 0; k < kRItems; ++k) {
+        const int64_t idx = base + int64_t(k) * kBlock + threadIdx.x;
+        if (idx < n) {
+            int64_t r, rs;
+            if (staged) {
+                int lo = 0, hi = int(rhi - rlo);
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (rwin[mid] <= idx)
+                        lo = mid;
+                    else
+                        hi = mid - 1;
+                }
+                r = rlo + lo;
+                rs = rwin[lo];
+            } else {
+                r = last_leq_i64(rp, rlo, rhi, idx);
+                rs = rp[r];
+            }
+            const uint32_t key = uint32_t(int64_t(sl.ci[sl.row_lo[r] + (idx - rs)]) - sl.c0);
+            atomicAdd(&cnt[w][key & mask], 1u);
+        }
+    }
+    __syncthreads();
+    uint32_t t = 0;
+#pragma unroll
+    for (int q = 0; q < kWavesPerBlock; ++q) t += cnt[q][threadIdx.x];
+    hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = t;
+}
+
+template <int VB, int SRC, int OUT = kOutArrays>
 __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restrict__ key_in,
                                                         const uint32_t* __restrict__ row_in,
                                                         const typename ValT<VB>::T* __restrict__ val_in,
@@ -100,8 +170,10 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
                                                         typename ValT<VB>::T* __restrict__ val_out, int64_t n, int shift,
                                                         uint32_t mask, const uint32_t* __restrict__ offs,
                                                         int64_t ntiles, const int64_t* __restrict__ rp, int64_t m,
-                                                        const int64_t* __restrict__ trow, int rowbits, int lenbits) {
+                                                        const int64_t* __restrict__ trow, int rowbits, int lenbits,
+                                                        SlabIo sl) {
     using V = typename ValT<VB>::T;
+    constexpr bool FIRST = SRC != kSrcArrays;  // records derived from a row structure
     // consecutive tiles on one XCD (workgroups go round-robin over the XCDs),
     // so the partial lines where their digit runs meet merge in one L2
     const int64_t per = (ntiles + kXcds - 1) / kXcds;
@@ -115,6 +187,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     // the tile is reordered through one buffer, a field at a time
     __shared__ V ex[kRTile];
     __shared__ uint8_t dig[kRTile];
+    __shared__ uint16_t kslot[OUT == kOutPlace ? kRTile : 1];  // key of every slot (keys below 2^16)
 
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -179,11 +252,29 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     // are exchanged (fewer registers, more workgroups per compute unit)
     uint32_t kr[kRItems], rr[FIRST ? kRItems : 1], loc[kRItems];
     const uint64_t lt = lanemask_lt();
+    // record idx of a slab (row r) is entry row_lo[r] + idx - rec_rp[r]
+    auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t {
+        const int64_t rs = rstaged ? rwin[r - rlo] : rp[r];
+        return sl.row_lo[r] + (idx - rs);
+    };
     // all of the segment's keys in flight at once, then the ranking
+    if constexpr (SRC == kSrcSlab) {
 #pragma unroll
-    for (int k = 0; k < kRItems; ++k) {
-        const int64_t idx = segbase + int64_t(k) * kWave + lane;
-        kr[k] = idx < n ? key_in[idx] : 0u;
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t idx = segbase + int64_t(k) * kWave + lane;
+            int64_t r = 0;
+            if (idx < n)
+                r = rstaged ? rlo + int64_t(reinterpret_cast<const uint32_t*>(ex)[idx - base])
+                            : last_leq_i64(rp, rlo, rhi, idx);
+            rr[k] = uint32_t(r);
+            kr[k] = idx < n ? uint32_t(int64_t(sl.ci[slab_entry(idx, r)]) - sl.c0) : 0u;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t idx = segbase + int64_t(k) * kWave + lane;
+            kr[k] = idx < n ? key_in[idx] : 0u;
+        }
     }
 #pragma unroll
     for (int k = 0; k < kRItems; ++k) {
@@ -203,7 +294,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         const uint32_t rank = __popcll(peers & lt);
         loc[k] = cur + rank;
         if (valid && rank == 0) wcnt[w][d] = cur + uint32_t(__popcll(peers));
-        if constexpr (FIRST) {
+        if constexpr (SRC == kSrcCsr) {
             uint32_t field = 0;
             if (valid) {
                 int64_t r, len;
@@ -253,6 +344,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             loc[k] += wcnt[w][d];
             ex[loc[k]] = V(kr[k]);
             dig[loc[k]] = uint8_t(d);
+            if constexpr (OUT == kOutPlace) kslot[loc[k]] = uint16_t(kr[k]);
         }
     }
     __syncthreads();
@@ -275,14 +367,26 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = V(rv[k]);
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < tile_n; i += kBlock) row_out[gofs[dig[i]] + i] = uint32_t(ex[i]);
+    // full-row position of the record in slot i (kOutPlace)
+    auto place = [&](int i) -> int64_t {
+        const int64_t q = gofs[dig[i]] + i;
+        return sl.before + q + sl.rp[sl.c0 + int64_t(kslot[i]) + 1];
+    };
+    for (int i = threadIdx.x; i < tile_n; i += kBlock) {
+        if constexpr (OUT == kOutPlace)
+            sl.f_ci[place(i)] = int32_t(ex[i]);
+        else
+            row_out[gofs[dig[i]] + i] = uint32_t(ex[i]);
+    }
     if constexpr (VB != 0) {
         V vv[kRItems];
 #pragma unroll
         for (int k = 0; k < kRItems; ++k) {
             const int64_t idx = segbase + int64_t(k) * kWave + lane;
-            if constexpr (FIRST)
+            if constexpr (SRC == kSrcCsr)
                 vv[k] = V(idx);
+            else if constexpr (SRC == kSrcSlab)
+                vv[k] = idx < n ? static_cast<const V*>(sl.val)[slab_entry(idx, int64_t(rr[k]))] : V(0);
             else
                 vv[k] = idx < n ? val_in[idx] : V(0);
         }
@@ -291,7 +395,12 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         for (int k = 0; k < kRItems; ++k)
             if (segbase + int64_t(k) * kWave + lane < n) ex[loc[k]] = vv[k];
         __syncthreads();
-        for (int i = threadIdx.x; i < tile_n; i += kBlock) val_out[gofs[dig[i]] + i] = ex[i];
+        for (int i = threadIdx.x; i < tile_n; i += kBlock) {
+            if constexpr (OUT == kOutPlace)
+                static_cast<V*>(sl.f_val)[place(i)] = ex[i];
+            else
+                val_out[gofs[dig[i]] + i] = ex[i];
+        }
     }
 }
 
@@ -692,17 +801,21 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
                   (unsigned long long)(pk.drop_last ? S - int64_t(distinct) : S));
 }
 
-template <int VB, bool FIRST = false>
+template <int VB, int SRC = kSrcArrays, int OUT = kOutArrays>
 void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
               int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s, const int64_t* rp = nullptr,
-              int64_t m = 0, const int64_t* trow = nullptr, int rowbits = 0, int lenbits = 0) {
+              int64_t m = 0, const int64_t* trow = nullptr, int rowbits = 0, int lenbits = 0,
+              const SlabIo& sl = SlabIo()) {
     using V = typename ValT<VB>::T;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
-    radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
+    if constexpr (SRC == kSrcSlab)
+        radix_hist_slab<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(n, mask, hist, ntiles, rp, m, trow, sl);
+    else
+        radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
     scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
-    radix_scatter<VB, FIRST><<<dim3(unsigned((ntiles + kXcds - 1) / kXcds * kXcds)), dim3(kBlock), 0, s>>>(
+    radix_scatter<VB, SRC, OUT><<<dim3(unsigned((ntiles + kXcds - 1) / kXcds * kXcds)), dim3(kBlock), 0, s>>>(
         ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, trow, rowbits,
-        lenbits);
+        lenbits, sl);
 }
 
 // Digit widths of the passes for an nbits-bit key: as few passes as 8-bit
@@ -769,7 +882,7 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     {
         PhaseTimer passes_timer(SPSYRK_PHASE_COLINDEX_PASSES, s);
         tile_first_rows(rp, m, kRTile, trow, s);
-        run_pass<4, true>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
+        run_pass<4, kSrcCsr>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
                           (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
         int shift = L + width[0];
         for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
@@ -843,6 +956,45 @@ int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_
         cur ^= 1;
     }
     return cur;
+}
+
+// A mirror slab sorted by (column, row) in one or two passes (keys of at
+// most 16 bits): the first pass reads its records straight from C_L, the last
+// puts rows and values into the full rows; the sorted keys end in the key
+// buffer returned (for the column runs).
+uint32_t* slab_sort_place(const SlabIo& io, int vbytes, int64_t nrec, int nbits, const int64_t* rec_rp, int64_t m,
+                          uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, void* val_a, void* tmp, hipStream_t s) {
+    if (nrec <= 0) return key_a;
+    const int64_t ntiles = (nrec + kRTile - 1) / kRTile;
+    uint32_t* hist = static_cast<uint32_t*>(tmp);
+    const size_t hist_bytes = (size_t(ntiles) * kDigits * sizeof(uint32_t) + 255) & ~size_t(255);
+    const size_t table_bytes = (size_t(ntiles + 1) * sizeof(int64_t) + 255) & ~size_t(255);
+    int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + hist_bytes);
+    void* scan_tmp = static_cast<char*>(tmp) + hist_bytes + table_bytes;
+    tile_first_rows(rec_rp, m, kRTile, trow, s);
+    int width[8];
+    const int passes = digit_plan(nbits, width);
+    const uint32_t m0 = (1u << width[0]) - 1u;
+    auto go = [&](auto vb) {
+        constexpr int VB = decltype(vb)::value;
+        if (passes == 1) {
+            run_pass<VB, kSrcSlab, kOutPlace>(nullptr, nullptr, nullptr, key_b, nullptr, nullptr, nrec, 0, m0, hist,
+                                              scan_tmp, s, rec_rp, m, trow, 0, 0, io);
+        } else {
+            run_pass<VB, kSrcSlab>(nullptr, nullptr, nullptr, key_a, row_a, val_a, nrec, 0, m0, hist, scan_tmp, s,
+                                   rec_rp, m, trow, 0, 0, io);
+            run_pass<VB, kSrcArrays, kOutPlace>(key_a, row_a, val_a, key_b, nullptr, nullptr, nrec, width[0],
+                                                (1u << width[1]) - 1u, hist, scan_tmp, s, nullptr, 0, nullptr, 0, 0,
+                                                io);
+        }
+    };
+    if (vbytes == 8)
+        go(std::integral_constant<int, 8>());
+    else if (vbytes == 4)
+        go(std::integral_constant<int, 4>());
+    else
+        go(std::integral_constant<int, 0>());
+    return key_b;
 }
 
 }  // namespace spsyrk

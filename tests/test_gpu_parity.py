@@ -629,16 +629,19 @@ def test_mirror_column_slabs(dev, cap, monkeypatch):
     np.testing.assert_array_equal(M.to_host()[1], ref.col_idx)
 
 
-@pytest.mark.parametrize("bits,cap", [(4, 1 << 31), (8, 1 << 31), (10, 3000)])
-def test_mirror_narrow_slabs(dev, bits, cap, monkeypatch):
-    # slabs of at most 2^bits columns (keys of at most 16 bits, two sort
-    # passes), with and without the record cap; the slab plan's histogram
-    # counts every entry by column and takes the diagonal off again
+@pytest.mark.parametrize("bits,cap,m", [(4, 1 << 31, 5000), (8, 1 << 31, 5000), (10, 3000, 5000),
+                                        (0, 1 << 31, 70000)])
+def test_mirror_narrow_slabs(dev, bits, cap, m, monkeypatch):
+    # slabs of at most 2^bits columns (keys of at most 16 bits: one or two
+    # sort passes reading C_L directly and placing into the full rows), with
+    # and without the record cap; the slab plan's histogram counts every
+    # entry by column and takes the diagonal off again.  bits 0: one slab of
+    # 70000 columns, 17-bit keys, sorted over extracted records and placed
+    # by a pass of its own
     monkeypatch.setenv("SPSYRK_MIRROR_NARROW", str(bits))
     monkeypatch.setenv("SPSYRK_MIRROR_SLAB", str(cap))
     rng = np.random.default_rng(bits)
-    m = 5000
-    rp, ci, v = _random_lower(rng, m, 20, 7)
+    rp, ci, v = _random_lower(rng, m, 20 if m < 10000 else 4, 7)
     print(f"[mirror narrow] bits={bits} cap={cap} m={m} nnz={len(ci)}", flush=True)
     ref = oracle.mirror(m, rp, ci, v)
     M = sp.mirror(_raw(dev, rp, ci, m, v), "f64")
