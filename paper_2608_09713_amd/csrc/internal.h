@@ -313,10 +313,12 @@ struct SlabIo {
     void* f_val = nullptr;
 };
 // Sort of a slab of nrec records with keys of nbits <= 16 bits (one or two
-// passes) into the full rows; returns the buffer with the sorted keys (key_a
-// or key_b).  tmp: radix_tmp_bytes(nrec).
+// passes) into the full rows, the first pass reading C_L through the slab's
+// rows or (extracted) the records already in key_a, row_a, val_a; returns
+// the buffer with the sorted keys.  tmp: radix_tmp_bytes(nrec).
 uint32_t* slab_sort_place(const SlabIo& io, int vbytes, int64_t nrec, int nbits, const int64_t* rec_rp, int64_t m,
-                          uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, void* val_a, void* tmp, hipStream_t s);
+                          bool extracted, uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b,
+                          void* val_a, void* val_b, void* tmp, hipStream_t s);
 
 // ---- mirror.hip
 struct MirrorArgs {

@@ -107,14 +107,54 @@ __device__ inline int64_t last_leq_i64(const int64_t* a, int64_t lo, int64_t hi,
 constexpr int kSrcArrays = 0, kSrcCsr = 1, kSrcSlab = 2;
 constexpr int kOutArrays = 0, kOutPlace = 1;
 
+// rowof[i] = the row of record base + i of a tile of a record structure with
+// row pointers rp (rows [rlo, rhi] span the tile, rlo holding its first
+// record): every row that starts inside the tile marks its first record,
+// then a running maximum over the tile.  The rows are walked one by one, not
+// staged, so any number of empty rows may lie between (each row pointer is
+// read by about one tile).  Called by all threads; wt: kWavesPerBlock words.
+__device__ inline void tile_rows_mark(const int64_t* __restrict__ rp, int64_t rlo, int64_t rhi, int64_t base,
+                                      uint32_t* rowof, uint32_t* wt) {
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    for (int i = threadIdx.x; i < kRTile; i += kBlock) rowof[i] = uint32_t(rlo);
+    __syncthreads();
+    for (int64_t k = rlo + 1 + threadIdx.x; k <= rhi; k += kBlock) {
+        const int64_t a = rp[k];
+        if (a - base < kRTile && rp[k + 1] > a) rowof[a - base] = uint32_t(k);
+    }
+    __syncthreads();
+    uint32_t run_max = 0;
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k) run_max = max(run_max, rowof[threadIdx.x * kRItems + k]);
+    uint32_t inc = run_max;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t u = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc = max(inc, u);
+    }
+    if (lane == kWave - 1) wt[w] = inc;
+    __syncthreads();
+    uint32_t before = 0;
+    for (int q = 0; q < w; ++q) before = max(before, wt[q]);
+    const uint32_t prev = __shfl_up(inc, 1, kWave);
+    if (lane > 0) before = max(before, prev);
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k) {
+        before = max(before, rowof[threadIdx.x * kRItems + k]);
+        rowof[threadIdx.x * kRItems + k] = before;
+    }
+    __syncthreads();
+}
+
 // Digit counts of the first pass over a mirror slab (kSrcSlab): every key
-// read through its record's row (an LDS window of the record pointers rp, or
-// a search when the tile spans too many rows).
+// read through its record's row.
 __global__ __launch_bounds__(kBlock) void radix_hist_slab(int64_t n, uint32_t mask, uint32_t* __restrict__ hist,
                                                           int64_t ntiles, const int64_t* __restrict__ rp, int64_t m,
                                                           const int64_t* __restrict__ trow, SlabIo sl) {
     __shared__ uint32_t cnt[kWavesPerBlock][kDigits];
-    __shared__ int64_t rwin[kRowWin + 1];
+    __shared__ uint32_t rowof[kRTile];
+    __shared__ uint32_t wt[kWavesPerBlock];
     __shared__ int64_t rb[2];
     const int w = threadIdx.x / kWave;
 #pragma unroll
@@ -126,35 +166,20 @@ __global__ __launch_bounds__(kBlock) void radix_hist_slab(int64_t n, uint32_t ma
         rb[1] = base + kRTile < n ? trow[tile + 1] : last_leq_i64(rp, trow[tile], m, n - 1);
     }
     __syncthreads();
-    const int64_t rlo = rb[0], rhi = rb[1];
-    const bool staged = rhi - rlo + 2 <= kRowWin + 1;
-    if (staged)
-        for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) rwin[k] = rp[rlo + k];
-    __syncthreads();
-#pragma unroll 4
+    tile_rows_mark(rp, rb[0], rb[1], base, rowof, wt);
+    uint32_t key[kRItems];
+#pragma unroll
     for (int k = 0; k < kRItems; ++k) {
         const int64_t idx = base + int64_t(k) * kBlock + threadIdx.x;
+        key[k] = 0;
         if (idx < n) {
-            int64_t r, rs;
-            if (staged) {
-                int lo = 0, hi = int(rhi - rlo);
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (rwin[mid] <= idx)
-                        lo = mid;
-                    else
-                        hi = mid - 1;
-                }
-                r = rlo + lo;
-                rs = rwin[lo];
-            } else {
-                r = last_leq_i64(rp, rlo, rhi, idx);
-                rs = rp[r];
-            }
-            const uint32_t key = uint32_t(int64_t(sl.ci[sl.row_lo[r] + (idx - rs)]) - sl.c0);
-            atomicAdd(&cnt[w][key & mask], 1u);
+            const int64_t r = rowof[idx - base];
+            key[k] = uint32_t(int64_t(sl.ci[sl.row_lo[r] + (idx - rp[r])]) - sl.c0);
         }
     }
+#pragma unroll
+    for (int k = 0; k < kRItems; ++k)
+        if (base + int64_t(k) * kBlock + threadIdx.x < n) atomicAdd(&cnt[w][key[k] & mask], 1u);
     __syncthreads();
     uint32_t t = 0;
 #pragma unroll
@@ -179,7 +204,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     const int64_t per = (ntiles + kXcds - 1) / kXcds;
     const int64_t tile = int64_t(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
     if (tile >= ntiles) return;
-    __shared__ int64_t rwin[FIRST ? kRowWin + 1 : 1];
+    __shared__ int64_t rwin[SRC == kSrcCsr ? kRowWin + 1 : 1];
     __shared__ int64_t rbounds[2];
     __shared__ uint32_t wcnt[kWavesPerBlock][kDigits];
     __shared__ int64_t gofs[kDigits];  // global position of the tile's digit run minus its tile start
@@ -210,7 +235,8 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
         __syncthreads();
         rlo = rbounds[0];
         rhi = rbounds[1];
-        rstaged = rhi - rlo + 2 <= kRowWin + 1;
+        rstaged = SRC == kSrcCsr && rhi - rlo + 2 <= kRowWin + 1;
+        if constexpr (SRC == kSrcSlab) tile_rows_mark(rp, rlo, rhi, base, reinterpret_cast<uint32_t*>(ex), wt);
         if (rstaged) {
             for (int64_t k = threadIdx.x; k < rhi - rlo + 2; k += kBlock) rwin[k] = rp[rlo + k];
             // window row of every tile position (in the exchange buffer, free
@@ -253,19 +279,13 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     uint32_t kr[kRItems], rr[FIRST ? kRItems : 1], loc[kRItems];
     const uint64_t lt = lanemask_lt();
     // record idx of a slab (row r) is entry row_lo[r] + idx - rec_rp[r]
-    auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t {
-        const int64_t rs = rstaged ? rwin[r - rlo] : rp[r];
-        return sl.row_lo[r] + (idx - rs);
-    };
+    auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t { return sl.row_lo[r] + (idx - rp[r]); };
     // all of the segment's keys in flight at once, then the ranking
     if constexpr (SRC == kSrcSlab) {
 #pragma unroll
         for (int k = 0; k < kRItems; ++k) {
             const int64_t idx = segbase + int64_t(k) * kWave + lane;
-            int64_t r = 0;
-            if (idx < n)
-                r = rstaged ? rlo + int64_t(reinterpret_cast<const uint32_t*>(ex)[idx - base])
-                            : last_leq_i64(rp, rlo, rhi, idx);
+            const int64_t r = idx < n ? int64_t(reinterpret_cast<const uint32_t*>(ex)[idx - base]) : 0;
             rr[k] = uint32_t(r);
             kr[k] = idx < n ? uint32_t(int64_t(sl.ci[slab_entry(idx, r)]) - sl.c0) : 0u;
         }
@@ -959,11 +979,13 @@ int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_
 }
 
 // A mirror slab sorted by (column, row) in one or two passes (keys of at
-// most 16 bits): the first pass reads its records straight from C_L, the last
-// puts rows and values into the full rows; the sorted keys end in the key
-// buffer returned (for the column runs).
+// most 16 bits), the last pass putting rows and values into the full rows;
+// the first pass reads its records straight from C_L, or, with extracted,
+// from the record arrays key_a, row_a, val_a.  Returns the buffer with the
+// sorted keys (for the column runs).
 uint32_t* slab_sort_place(const SlabIo& io, int vbytes, int64_t nrec, int nbits, const int64_t* rec_rp, int64_t m,
-                          uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, void* val_a, void* tmp, hipStream_t s) {
+                          bool extracted, uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b,
+                          void* val_a, void* val_b, void* tmp, hipStream_t s) {
     if (nrec <= 0) return key_a;
     const int64_t ntiles = (nrec + kRTile - 1) / kRTile;
     uint32_t* hist = static_cast<uint32_t*>(tmp);
@@ -971,13 +993,25 @@ uint32_t* slab_sort_place(const SlabIo& io, int vbytes, int64_t nrec, int nbits,
     const size_t table_bytes = (size_t(ntiles + 1) * sizeof(int64_t) + 255) & ~size_t(255);
     int64_t* trow = reinterpret_cast<int64_t*>(static_cast<char*>(tmp) + hist_bytes);
     void* scan_tmp = static_cast<char*>(tmp) + hist_bytes + table_bytes;
-    tile_first_rows(rec_rp, m, kRTile, trow, s);
+    if (!extracted) tile_first_rows(rec_rp, m, kRTile, trow, s);
     int width[8];
     const int passes = digit_plan(nbits, width);
     const uint32_t m0 = (1u << width[0]) - 1u;
+    uint32_t* out = key_b;
     auto go = [&](auto vb) {
         constexpr int VB = decltype(vb)::value;
-        if (passes == 1) {
+        if (extracted) {
+            if (passes == 1) {
+                run_pass<VB, kSrcArrays, kOutPlace>(key_a, row_a, val_a, key_b, nullptr, nullptr, nrec, 0, m0, hist,
+                                                    scan_tmp, s, nullptr, 0, nullptr, 0, 0, io);
+            } else {
+                run_pass<VB>(key_a, row_a, val_a, key_b, row_b, val_b, nrec, 0, m0, hist, scan_tmp, s);
+                run_pass<VB, kSrcArrays, kOutPlace>(key_b, row_b, val_b, key_a, nullptr, nullptr, nrec, width[0],
+                                                    (1u << width[1]) - 1u, hist, scan_tmp, s, nullptr, 0, nullptr, 0,
+                                                    0, io);
+                out = key_a;
+            }
+        } else if (passes == 1) {
             run_pass<VB, kSrcSlab, kOutPlace>(nullptr, nullptr, nullptr, key_b, nullptr, nullptr, nrec, 0, m0, hist,
                                               scan_tmp, s, rec_rp, m, trow, 0, 0, io);
         } else {
@@ -994,7 +1028,7 @@ uint32_t* slab_sort_place(const SlabIo& io, int vbytes, int64_t nrec, int nbits,
         go(std::integral_constant<int, 4>());
     else
         go(std::integral_constant<int, 0>());
-    return key_b;
+    return out;
 }
 
 }  // namespace spsyrk

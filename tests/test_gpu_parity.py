@@ -631,15 +631,18 @@ def test_mirror_column_slabs(dev, cap, monkeypatch):
 
 @pytest.mark.parametrize("bits,cap,m", [(4, 1 << 31, 5000), (8, 1 << 31, 5000), (10, 3000, 5000),
                                         (0, 1 << 31, 70000)])
-def test_mirror_narrow_slabs(dev, bits, cap, m, monkeypatch):
+@pytest.mark.parametrize("direct", ["0", "1"])
+def test_mirror_narrow_slabs(dev, bits, cap, m, direct, monkeypatch):
     # slabs of at most 2^bits columns (keys of at most 16 bits: one or two
-    # sort passes reading C_L directly and placing into the full rows), with
+    # sort passes, the first over extracted records or reading C_L through
+    # the slab's rows (direct), the last placing into the full rows), with
     # and without the record cap; the slab plan's histogram counts every
     # entry by column and takes the diagonal off again.  bits 0: one slab of
     # 70000 columns, 17-bit keys, sorted over extracted records and placed
     # by a pass of its own
     monkeypatch.setenv("SPSYRK_MIRROR_NARROW", str(bits))
     monkeypatch.setenv("SPSYRK_MIRROR_SLAB", str(cap))
+    monkeypatch.setenv("SPSYRK_SLAB_DIRECT", direct)
     rng = np.random.default_rng(bits)
     rp, ci, v = _random_lower(rng, m, 20 if m < 10000 else 4, 7)
     print(f"[mirror narrow] bits={bits} cap={cap} m={m} nnz={len(ci)}", flush=True)
