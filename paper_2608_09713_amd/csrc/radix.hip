@@ -35,6 +35,11 @@ struct ValT<8> {
 
 __global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
                                                      uint32_t mask, uint32_t* __restrict__ hist, int64_t ntiles) {
+    // consecutive tiles on one XCD, so that one L2 gathers their counts'
+    // 4-byte writes (hist is digit-major: tile t of digit d at d * ntiles + t)
+    const int64_t per = (ntiles + kXcds - 1) / kXcds;
+    const int64_t tile = int64_t(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+    if (tile >= ntiles) return;
     // one sub-histogram per wavefront keeps the LDS atomics of different
     // wavefronts apart
     __shared__ uint32_t cnt[kWavesPerBlock][kDigits];
@@ -42,7 +47,7 @@ __global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict_
 #pragma unroll
     for (int q = 0; q < kWavesPerBlock; ++q) cnt[q][threadIdx.x] = 0;
     __syncthreads();
-    const int64_t base = int64_t(blockIdx.x) * kRTile;
+    const int64_t base = tile * kRTile;
     if (base + kRTile <= n && (reinterpret_cast<uintptr_t>(keys) & 15) == 0) {
         // whole tile, 16-byte loads (the tile starts at a multiple of 16 bytes)
         uint4 kv[kRItems / 4];
@@ -73,7 +78,7 @@ __global__ __launch_bounds__(kBlock) void radix_hist(const uint32_t* __restrict_
     uint32_t t = 0;
 #pragma unroll
     for (int q = 0; q < kWavesPerBlock; ++q) t += cnt[q][threadIdx.x];
-    hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = t;
+    hist[int64_t(threadIdx.x) * ntiles + tile] = t;
 }
 
 constexpr int kRowWin = 1024;
@@ -156,10 +161,12 @@ __global__ __launch_bounds__(kBlock) void radix_hist_slab(int64_t n, uint32_t ma
     __shared__ uint32_t rowof[kRTile];
     __shared__ uint32_t wt[kWavesPerBlock];
     __shared__ int64_t rb[2];
+    const int64_t per = (ntiles + kXcds - 1) / kXcds;  // (tiles placed as in radix_hist)
+    const int64_t tile = int64_t(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+    if (tile >= ntiles) return;
     const int w = threadIdx.x / kWave;
 #pragma unroll
     for (int q = 0; q < kWavesPerBlock; ++q) cnt[q][threadIdx.x] = 0;
-    const int64_t tile = blockIdx.x;
     const int64_t base = tile * kRTile;
     if (threadIdx.x == 0) {
         rb[0] = trow[tile];
@@ -184,7 +191,7 @@ __global__ __launch_bounds__(kBlock) void radix_hist_slab(int64_t n, uint32_t ma
     uint32_t t = 0;
 #pragma unroll
     for (int q = 0; q < kWavesPerBlock; ++q) t += cnt[q][threadIdx.x];
-    hist[int64_t(threadIdx.x) * ntiles + blockIdx.x] = t;
+    hist[int64_t(threadIdx.x) * ntiles + tile] = t;
 }
 
 template <int VB, int SRC, int OUT = kOutArrays>
@@ -281,13 +288,18 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     // record idx of a slab (row r) is entry row_lo[r] + idx - rec_rp[r]
     auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t { return sl.row_lo[r] + (idx - rp[r]); };
     // all of the segment's keys in flight at once, then the ranking
+    // (a slab's values are loaded with their keys, so that each record's
+    // entry is found once)
+    V vpre[SRC == kSrcSlab && VB != 0 ? kRItems : 1];
     if constexpr (SRC == kSrcSlab) {
 #pragma unroll
         for (int k = 0; k < kRItems; ++k) {
             const int64_t idx = segbase + int64_t(k) * kWave + lane;
             const int64_t r = idx < n ? int64_t(reinterpret_cast<const uint32_t*>(ex)[idx - base]) : 0;
             rr[k] = uint32_t(r);
-            kr[k] = idx < n ? uint32_t(int64_t(sl.ci[slab_entry(idx, r)]) - sl.c0) : 0u;
+            const int64_t e = slab_entry(idx, r);
+            kr[k] = idx < n ? uint32_t(int64_t(sl.ci[e]) - sl.c0) : 0u;
+            if constexpr (VB != 0) vpre[k] = idx < n ? static_cast<const V*>(sl.val)[e] : V(0);
         }
     } else {
 #pragma unroll
@@ -406,7 +418,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             if constexpr (SRC == kSrcCsr)
                 vv[k] = V(idx);
             else if constexpr (SRC == kSrcSlab)
-                vv[k] = idx < n ? static_cast<const V*>(sl.val)[slab_entry(idx, int64_t(rr[k]))] : V(0);
+                vv[k] = vpre[k];
             else
                 vv[k] = idx < n ? val_in[idx] : V(0);
         }
@@ -828,10 +840,11 @@ void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* 
               const SlabIo& sl = SlabIo()) {
     using V = typename ValT<VB>::T;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
+    const unsigned grid = unsigned((ntiles + kXcds - 1) / kXcds * kXcds);
     if constexpr (SRC == kSrcSlab)
-        radix_hist_slab<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(n, mask, hist, ntiles, rp, m, trow, sl);
+        radix_hist_slab<<<dim3(grid), dim3(kBlock), 0, s>>>(n, mask, hist, ntiles, rp, m, trow, sl);
     else
-        radix_hist<<<dim3(unsigned(ntiles)), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
+        radix_hist<<<dim3(grid), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
     scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
     radix_scatter<VB, SRC, OUT><<<dim3(unsigned((ntiles + kXcds - 1) / kXcds * kXcds)), dim3(kBlock), 0, s>>>(
         ki, ri, static_cast<const V*>(vi), ko, ro, static_cast<V*>(vo), n, shift, mask, hist, ntiles, rp, m, trow, rowbits,
