@@ -55,10 +55,10 @@ __device__ inline T wave_reduce_max(T v) {
     return v;
 }
 
-// Exclusive scan of a block of kBlock values, one per thread.  `warp_tot`
-// is LDS scratch of kWavesPerBlock entries.  Returns the exclusive prefix of
-// this thread and writes the block total to *total (all threads).
-template <typename T>
+// Exclusive scan of a block of NT values, one per thread.  `warp_tot` is LDS
+// scratch of NT / kWave entries.  Returns the exclusive prefix of this thread
+// and writes the block total to *total (all threads).
+template <typename T, int NT = kBlock>
 __device__ inline T block_exclusive_scan(T v, T* warp_tot, T* total) {
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
@@ -67,7 +67,7 @@ __device__ inline T block_exclusive_scan(T v, T* warp_tot, T* total) {
     __syncthreads();
     T off = 0, tot = 0;
 #pragma unroll
-    for (int i = 0; i < kWavesPerBlock; ++i) {
+    for (int i = 0; i < NT / kWave; ++i) {
         T t = warp_tot[i];
         if (i < w) off += t;
         tot += t;
@@ -105,16 +105,17 @@ __device__ inline uint32_t block_exclusive_max(uint32_t v, uint32_t* wt, uint32_
 }
 
 // Exclusive scan in place of an LDS array of length n (any n) by the whole
-// block; returns the total.  `warp_tot` is LDS scratch of kWavesPerBlock.
-template <typename T>
+// block of NT threads; returns the total.  `warp_tot` is LDS scratch of
+// NT / kWave entries.
+template <typename T, int NT = kBlock>
 __device__ inline T block_exclusive_scan_array(T* a, int n, T* warp_tot) {
-    const int per = (n + kBlock - 1) / kBlock;
+    const int per = (n + NT - 1) / NT;
     const int lo = min(n, int(threadIdx.x) * per);
     const int hi = min(n, lo + per);
     T s = 0;
     for (int i = lo; i < hi; ++i) s += a[i];
     T tot;
-    T off = block_exclusive_scan(s, warp_tot, &tot);
+    T off = block_exclusive_scan<T, NT>(s, warp_tot, &tot);
     for (int i = lo; i < hi; ++i) {
         T x = a[i];
         a[i] = off;

@@ -271,6 +271,13 @@ __global__ __launch_bounds__(kBlock) void bucket_sum(const int64_t* __restrict__
 // adds the sums to its rows of the workspace.
 
 constexpr int kSplitRows = 1 << 14;  // rows per range at most (the LDS accumulator)
+// threads of a record-writing workgroup: its LDS (about 72 KiB: the tile's
+// records sorted by range) lets two share a compute unit, so the workgroup
+// is large enough for four wavefronts per SIMD to hide the gathers of X
+#ifndef SPSYRK_SPLIT_THREADS
+#define SPSYRK_SPLIT_THREADS 512
+#endif
+constexpr int kSplitThreads = SPSYRK_SPLIT_THREADS;
 
 // Entries [blk * kSub * kTileS, +kSub * kTileS) of workgroup blk: its entries
 // per range of their column, cnt[range * nblk + blk] (every entry, the
@@ -294,26 +301,26 @@ __global__ __launch_bounds__(kBlock) void split_count(const int32_t* __restrict_
 // contiguous run per range at the range's cursor of this workgroup (boff:
 // exclusive scan of split_count's counts).
 template <typename V, typename XT>
-__global__ __launch_bounds__(kBlock) void split_records(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
+__global__ __launch_bounds__(kSplitThreads) void split_records(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
                                                         const int32_t* __restrict__ ci, const V* __restrict__ cv,
                                                         const int64_t* __restrict__ trow, const XT* __restrict__ x,
                                                         int64_t ldx, double* __restrict__ w,
                                                         const int64_t* __restrict__ boff, int bits, int nr,
                                                         int64_t nblk, uint16_t* __restrict__ rj,
                                                         double* __restrict__ rv) {
-    constexpr int kPerG = kTileS / kBlock;  // 16 entries per thread
-    constexpr int kBatch = 8;
+    constexpr int kPerG = kTileS / kSplitThreads;  // entries per thread
+    constexpr int kBatch = kPerG < 8 ? kPerG : 8;
     static_assert(kPerG % kBatch == 0, "whole batches");
     __shared__ int64_t cur[kSymmSplitMax];   // next record of each range for this workgroup
     __shared__ uint32_t th[kSymmSplitMax];   // the tile's records per range, then their LDS start
     __shared__ uint32_t tc[kSymmSplitMax];   // placement cursors inside the tile
-    __shared__ uint32_t wt[kWavesPerBlock];
+    __shared__ uint32_t wt[kSplitThreads / kWave];
     __shared__ uint16_t sj[kTileS];
     __shared__ uint16_t sb[kTileS];
     __shared__ double sv[kTileS];
     __shared__ int64_t win[kWinS + 1];
     __shared__ int64_t bounds[2];
-    for (int b = threadIdx.x; b < nr; b += kBlock) {
+    for (int b = threadIdx.x; b < nr; b += kSplitThreads) {
         cur[b] = boff[int64_t(b) * nblk + blockIdx.x];
         th[b] = 0;
         tc[b] = 0;
@@ -335,7 +342,7 @@ __global__ __launch_bounds__(kBlock) void split_records(const int64_t* __restric
         const int64_t rlo = bounds[0], rhi = bounds[1];
         const bool staged = rhi - rlo + 1 <= kWinS;
         if (staged)
-            for (int64_t t = threadIdx.x; t <= rhi - rlo + 1 && rlo + t <= m; t += kBlock) win[t] = rp[rlo + t];
+            for (int64_t t = threadIdx.x; t <= rhi - rlo + 1 && rlo + t <= m; t += kSplitThreads) win[t] = rp[rlo + t];
         __syncthreads();
         const int64_t a = e0 + int64_t(threadIdx.x) * kPerG;
         const int64_t b = min(e1, a + kPerG);
@@ -391,7 +398,7 @@ __global__ __launch_bounds__(kBlock) void split_records(const int64_t* __restric
         for (int u = 0; u < kPerG; ++u)
             if (rb[u] != 0xffffffffu) atomicAdd(&th[rb[u] >> 16], 1u);
         __syncthreads();
-        block_exclusive_scan_array(th, nr, wt);  // th: start of each range's run in LDS
+        block_exclusive_scan_array<uint32_t, kSplitThreads>(th, nr, wt);  // th: start of each range's run in LDS
         __syncthreads();
 #pragma unroll
         for (int u = 0; u < kPerG; ++u) {
@@ -404,14 +411,14 @@ __global__ __launch_bounds__(kBlock) void split_records(const int64_t* __restric
         }
         __syncthreads();
         const int tn = int(e1 - e0);
-        for (int q = threadIdx.x; q < tn; q += kBlock) {
+        for (int q = threadIdx.x; q < tn; q += kSplitThreads) {
             const uint32_t g = sb[q];
             const int64_t dst = cur[g] + int64_t(q - int(th[g]));
             rj[dst] = sj[q];
             rv[dst] = sv[q];
         }
         __syncthreads();
-        for (int g = threadIdx.x; g < nr; g += kBlock) {
+        for (int g = threadIdx.x; g < nr; g += kSplitThreads) {
             cur[g] += tc[g];
             th[g] = 0;
             tc[g] = 0;
@@ -584,7 +591,7 @@ void launch_split(const DevCsr& C, const XT* x, int64_t ldx, double* w, const in
     double* rv = reinterpret_cast<double*>(tmp + L.rv);
     split_count<<<unsigned(L.nblk), kBlock, 0, s>>>(C.ci, C.nnz, L.bits, L.nr, L.nblk, boff);
     scan_i64(boff, boff, int64_t(L.nr) * L.nblk, nullptr, tmp + L.stmp, s);
-    split_records<V, XT><<<unsigned(L.nblk), kBlock, 0, s>>>(C.rp, C.m, C.nnz, C.ci, static_cast<const V*>(C.v), trow,
+    split_records<V, XT><<<unsigned(L.nblk), kSplitThreads, 0, s>>>(C.rp, C.m, C.nnz, C.ci, static_cast<const V*>(C.v), trow,
                                                              x, ldx, w, boff, L.bits, L.nr, L.nblk, rj, rv);
     split_apply<<<unsigned(L.nr), kBlock, 0, s>>>(boff, L.nr, L.nblk, C.nnz, L.bits, C.m, rj, rv, w);
 }
