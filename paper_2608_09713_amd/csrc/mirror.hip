@@ -243,14 +243,40 @@ __global__ __launch_bounds__(kBlock) void coarse_hist(const int64_t* __restrict_
 }
 
 // column runs of a sorted slab: first[k] / end[k] = first / one-past-last
-// record of slab column k (both zero for a column without records)
+// record of slab column k (both zero for a column without records).  Four
+// records per thread (one 16-byte load), the neighbouring threads' keys by
+// shuffles, a load at each wavefront's edges.
+constexpr uint32_t kNoKey = 0xffffffffu;  // (slab keys are below 2^31)
 __global__ __launch_bounds__(kBlock) void slab_col_runs(const uint32_t* __restrict__ skey, int64_t nrec,
                                                         uint32_t* __restrict__ first, uint32_t* __restrict__ end) {
-    const int64_t s = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-    if (s >= nrec) return;
-    const uint32_t k = skey[s];
-    if (s == 0 || skey[s - 1] != k) first[k] = uint32_t(s);
-    if (s == nrec - 1 || skey[s + 1] != k) end[k] = uint32_t(s + 1);
+    const int64_t t = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    const int64_t s0 = 4 * t;
+    const int lane = lane_id();
+    uint32_t k[4];
+    if (s0 + 4 <= nrec && (reinterpret_cast<uintptr_t>(skey) & 15) == 0) {
+        const uint4 v = reinterpret_cast<const uint4*>(skey)[t];
+        k[0] = v.x;
+        k[1] = v.y;
+        k[2] = v.z;
+        k[3] = v.w;
+    } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) k[u] = s0 + u < nrec ? skey[s0 + u] : kNoKey;
+    }
+    uint32_t prev = __shfl_up(k[3], 1, kWave);
+    uint32_t next = __shfl_down(k[0], 1, kWave);
+    if (lane == 0) prev = (s0 > 0 && s0 <= nrec) ? skey[s0 - 1] : kNoKey;
+    if (lane == kWave - 1) next = s0 + 4 < nrec ? skey[s0 + 4] : kNoKey;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int64_t sx = s0 + u;
+        if (sx < nrec) {
+            const uint32_t kp = u == 0 ? prev : k[u - 1];
+            const uint32_t kn = u == 3 ? next : k[u + 1];
+            if (sx == 0 || kp != k[u]) first[k[u]] = uint32_t(sx);
+            if (sx == nrec - 1 || kn != k[u]) end[k[u]] = uint32_t(sx + 1);
+        }
+    }
 }
 
 // full row lengths of the slab's columns (lower length + strict-lower
@@ -309,7 +335,7 @@ void mirror_slab_columns(const MirrorArgs& a, int64_t c0, int64_t c1, const uint
     const int64_t w = c1 - c0;
     (void)hipMemsetAsync(first, 0, size_t(w) * sizeof(uint32_t), s);
     (void)hipMemsetAsync(end, 0, size_t(w) * sizeof(uint32_t), s);
-    if (nrec > 0) slab_col_runs<<<blocks_for(nrec, kBlock), kBlock, 0, s>>>(skey, nrec, first, end);
+    if (nrec > 0) slab_col_runs<<<blocks_for((nrec + 3) / 4, kBlock), kBlock, 0, s>>>(skey, nrec, first, end);
     slab_full_len<<<blocks_for(w + 1, kBlock), kBlock, 0, s>>>(a.rp, c0, w, first, end, fl);
     scan_i64(fl, f_rp + c0, w + 1, nullptr, scan_tmp, s);
     add_carry<<<blocks_for(w + 1, kBlock), kBlock, 0, s>>>(f_rp + c0, w + 1, a.rp + c0, strict_before);
