@@ -889,7 +889,7 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
             SlabIo io;
             io.ci = L.ci;
             io.val = vb ? L.v : nullptr;
-            io.row_lo = row_lo;
+            io.row_off = row_lo;
             io.c0 = sl.c0;
             io.rp = L.rp;
             io.before = sl.before;
@@ -900,7 +900,10 @@ void mirror(const DevCsr& L, int sr, Arena& ar, hipStream_t s, spsyrk_csr_out* C
             // R-MAT's transpose)
             const char* de = std::getenv("SPSYRK_SLAB_DIRECT");
             const bool direct = !(de && de[0] == '0');
-            if (!direct) mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, strow, ka, ra, va, s);
+            if (direct)
+                mirror_slab_offsets(row_lo, row_cnt, m, s);
+            else
+                mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, strow, ka, ra, va, s);
             skey = slab_sort_place(io, vb, sl.nrec, nbits, row_cnt, m, !direct, ka, kb, ra, rb, va, vbb, rtmp, s);
         } else if (sl.nrec > 0) {
             mirror_slab_extract(ma, sl.c0, sl.nrec, row_cnt, row_lo, strow, ka, ra, va, s);

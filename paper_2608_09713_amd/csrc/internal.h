@@ -298,14 +298,14 @@ void symm_product(const DevCsr& C, int sr, const void* x, int64_t ldx, int64_t k
 
 // ---- the mirror's slab sort (radix.hip)
 // The mirror slab behind a fused sort: record p of row r (rows from the
-// record pointers rec_rp) is entry row_lo[r] + (p - rec_rp[r]) of C_L, with
+// record pointers rec_rp) is entry p + row_off[r] of C_L, with
 // key = column - c0; the record at sorted position q goes to the full rows at
 // before + q + rp[c0 + key + 1] (its column's lower part, then the column's
 // strict entries in row order).
 struct SlabIo {
     const int32_t* ci = nullptr;      // C_L's columns
     const void* val = nullptr;        // C_L's values or null
-    const int64_t* row_lo = nullptr;  // first entry of every row in the slab
+    const int64_t* row_off = nullptr; // per row: its first entry in the slab less its first record
     int64_t c0 = 0;                   // the slab's first column
     const int64_t* rp = nullptr;      // C_L's row pointers
     int64_t before = 0;               // strict entries of the columns before c0
@@ -341,6 +341,8 @@ void mirror_coarse_hist(const MirrorArgs& a, int64_t clo, int cb, int nb, unsign
 size_t mirror_tile_bytes(int64_t positions);
 void mirror_tile_rows(const int64_t* rp, int64_t m, int64_t* trow, hipStream_t s);
 // per-row counts and first entries of the strict lower part with col in [c0, c1)
+// row_lo[r] -= rec_rp[r] for every row (the entry of record p of row r is then p + row_lo[r])
+void mirror_slab_offsets(int64_t* row_lo, const int64_t* rec_rp, int64_t m, hipStream_t s);
 void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,
                         hipStream_t s);
 // records (col - c0, row, value) of the slab, in row-major order at positions

@@ -141,6 +141,12 @@ __global__ __launch_bounds__(kBlock) void slab_counts(const int64_t* __restrict_
     lo_out[r] = lo;
 }
 
+__global__ __launch_bounds__(kBlock) void slab_offsets(int64_t* __restrict__ row_lo, const int64_t* __restrict__ rec_rp,
+                                                       int64_t m) {
+    const int64_t r = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+    if (r < m) row_lo[r] -= rec_rp[r];
+}
+
 // Records [0, nrec) of a slab in row-major order: record p of row r (rows
 // found in an LDS window of rec_rp) is entry row_lo[r] + (p - rec_rp[r]), so
 // the slab reads only its own entries.
@@ -339,6 +345,10 @@ void mirror_slab_columns(const MirrorArgs& a, int64_t c0, int64_t c1, const uint
     slab_full_len<<<blocks_for(w + 1, kBlock), kBlock, 0, s>>>(a.rp, c0, w, first, end, fl);
     scan_i64(fl, f_rp + c0, w + 1, nullptr, scan_tmp, s);
     add_carry<<<blocks_for(w + 1, kBlock), kBlock, 0, s>>>(f_rp + c0, w + 1, a.rp + c0, strict_before);
+}
+
+void mirror_slab_offsets(int64_t* row_lo, const int64_t* rec_rp, int64_t m, hipStream_t s) {
+    if (m > 0) slab_offsets<<<blocks_for(m, kBlock), kBlock, 0, s>>>(row_lo, rec_rp, m);
 }
 
 void mirror_slab_counts(const MirrorArgs& a, int64_t c0, int64_t c1, int64_t* row_cnt, int64_t* row_lo,

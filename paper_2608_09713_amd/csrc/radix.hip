@@ -101,8 +101,8 @@ __device__ inline int64_t last_leq_i64(const int64_t* a, int64_t lo, int64_t hi,
 //    lenbits > 0 the row field also carries the row's length, saturated at
 //    2^lenbits - 1, above its low rowbits bits.
 //  kSrcSlab: a mirror slab's strict-lower entries, record p of row r (rows
-//    from the record pointers rp = rec_rp) being entry sl.row_lo[r] +
-//    (p - rec_rp[r]) of C_L: key = column - sl.c0, row = r, value = the
+//    from the record pointers rp = rec_rp) being entry p + sl.row_off[r] of
+//    C_L: key = column - sl.c0, row = r, value = the
 //    entry's value.
 //  kOutArrays: key, row and value arrays in the pass's order.
 //  kOutPlace (last pass of a mirror slab): keys to key_out; the row and
@@ -181,7 +181,7 @@ __global__ __launch_bounds__(kBlock) void radix_hist_slab(int64_t n, uint32_t ma
         key[k] = 0;
         if (idx < n) {
             const int64_t r = rowof[idx - base];
-            key[k] = uint32_t(int64_t(sl.ci[sl.row_lo[r] + (idx - rp[r])]) - sl.c0);
+            key[k] = uint32_t(int64_t(sl.ci[idx + sl.row_off[r]]) - sl.c0);
         }
     }
 #pragma unroll
@@ -285,8 +285,8 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     // are exchanged (fewer registers, more workgroups per compute unit)
     uint32_t kr[kRItems], rr[FIRST ? kRItems : 1], loc[kRItems];
     const uint64_t lt = lanemask_lt();
-    // record idx of a slab (row r) is entry row_lo[r] + idx - rec_rp[r]
-    auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t { return sl.row_lo[r] + (idx - rp[r]); };
+    // record idx of a slab (row r) is entry idx + row_off[r]
+    auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t { return idx + sl.row_off[r]; };
     // all of the segment's keys in flight at once, then the ranking
     // (a slab's values are loaded with their keys, so that each record's
     // entry is found once)
