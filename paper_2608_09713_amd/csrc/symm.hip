@@ -273,11 +273,10 @@ __global__ __launch_bounds__(kBlock) void bucket_sum(const int64_t* __restrict__
 constexpr int kSplitRows = 1 << 14;  // rows per range at most (the LDS accumulator)
 // threads of a record-writing workgroup: its LDS (about 72 KiB: the tile's
 // records sorted by range) lets two share a compute unit, so the workgroup
-// is large enough for four wavefronts per SIMD to hide the gathers of X
-#ifndef SPSYRK_SPLIT_THREADS
-#define SPSYRK_SPLIT_THREADS 512
-#endif
-constexpr int kSplitThreads = SPSYRK_SPLIT_THREADS;
+// is large enough for four wavefronts per SIMD to hide the gathers of X (256
+// threads measure 10% slower, 1024 25% slower; tiles of 2048 entries with
+// three workgroups per compute unit 15% slower: shorter runs per range)
+constexpr int kSplitThreads = 512;
 
 // Entries [blk * kSub * kTileS, +kSub * kTileS) of workgroup blk: its entries
 // per range of their column, cnt[range * nblk + blk] (every entry, the
