@@ -30,16 +30,18 @@ constexpr int kHeavyGroups = 1024;       // workgroups of a heavy-row launch
 constexpr int kGrp = 8;                  // lanes per short stretch of a walk
 
 // Output columns per window and ranks per value tile: the symbolic pass
-// holds a 32 KiB bitmap; the numeric pass an 8 KiB bitmap, the words' ranks
-// and a 32 KiB value tile, about 52 KiB with the activity lists, so that three
-// workgroups share a compute unit (with 16 KiB bitmaps only two fit, and rows
-// wait longer on their walks' latency).
+// holds a 32 KiB bitmap; the numeric pass a 16 KiB bitmap, the rank of every
+// 128 columns' first column (4 KiB) and a 28 KiB value tile, about 52 KiB
+// with the activity lists, so that three workgroups share a compute unit
+// (windows of 2^17 columns measure 2% faster than 2^16 with a rank per word;
+// with twice the LDS only two workgroups fit, and rows wait longer on their
+// walks' latency).
 template <int SR, bool NUM>
 struct HeavyCfg {
     using Acc = typename SrTraits<SR>::Acc;
-    static constexpr int kWin = NUM ? (1 << 16) : (1 << 18);
+    static constexpr int kWin = NUM ? (1 << 17) : (1 << 18);
     static constexpr int kWords = kWin / 32;
-    static constexpr int kAcc = 32768 / int(sizeof(Acc));
+    static constexpr int kAcc = 28672 / int(sizeof(Acc));
 };
 
 // exclusive scan over the kHB threads of a workgroup; *total gets the sum
@@ -76,8 +78,8 @@ void heavy_kernel(HeavyArgs a, int* queue) {
     constexpr int kWords = HeavyCfg<SR, NUM>::kWords;
     constexpr bool kVal = (SR == kF64 || SR == kF32);
 
-    __shared__ uint32_t bits[kWords];
-    __shared__ uint32_t prefw[NUM ? kWords : 1];  // rank of each word's first column in the window
+    __shared__ __align__(16) uint32_t bits[kWords];
+    __shared__ uint32_t prefw[NUM ? kWords / 4 : 1];  // rank of the first column of each 4 words in the window
     __shared__ Acc acc[NUM ? kAcc : 1];
     __shared__ int32_t act_short[kChunkE];
     __shared__ int32_t act_long[kChunkE];
@@ -97,7 +99,13 @@ void heavy_kernel(HeavyArgs a, int* queue) {
     auto rank_of = [&](int64_t B0, uint32_t j) -> uint32_t {
         if constexpr (!NUM) return 0u;  // (ranks exist in the numeric pass only)
         const uint32_t x = uint32_t(int64_t(j) - B0);
-        return prefw[x >> 5] + uint32_t(__popc(bits[x >> 5] & ((1u << (x & 31)) - 1u)));
+        const uint4 q = reinterpret_cast<const uint4*>(bits)[x >> 7];
+        const uint32_t wd[4] = {q.x, q.y, q.z, q.w};
+        const uint32_t k = (x >> 5) & 3u, mk = (1u << (x & 31)) - 1u;
+        uint32_t r = prefw[x >> 7];
+#pragma unroll
+        for (uint32_t i = 0; i < 4; ++i) r += i < k ? uint32_t(__popc(wd[i])) : (i == k ? uint32_t(__popc(wd[i] & mk)) : 0u);
+        return r;
     };
 
     // Walk the partner runs of entries [c0, c1) from their cursors through
@@ -280,7 +288,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
                 __syncthreads();
             } else {
                 for (int x = wlo; x < whi; ++x) {
-                    prefw[x] = off;
+                    if ((x & 3) == 0) prefw[x >> 2] = off;
                     uint32_t b = bits[x];
                     // the window's column indices, in order
                     while (b) {

@@ -138,6 +138,42 @@ def test_long_rows_use_heavy_rows(dev, semiring):
     assert sp.stats()["heavy_rows"] >= 2
 
 
+def _hub_csr(rng, m, n, per_row, hub_rows, dtype=np.float64):
+    # per_row random columns in [2, n) per row; columns 0 and 1 are hubs held
+    # by hub_rows random rows each, so these rows meet thousands of partners
+    # spread over the whole row range
+    c = rng.integers(2, n, size=(m, per_row + 2))
+    c[:, :2] = -1
+    for k in range(2):
+        c[rng.choice(m, size=hub_rows, replace=False), k] = k
+    c.sort(axis=1)
+    keep = c >= 0
+    keep[:, 1:] &= c[:, 1:] != c[:, :-1]
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(keep.sum(axis=1))
+    ci = c[keep].astype(np.int32)
+    return CSR(m, n, rp, ci, (rng.random(len(ci)) + 0.5).astype(dtype))
+
+
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+def test_heavy_rows_across_windows(dev, semiring):
+    # heavy rows whose partners spread over 300000 rows: the numeric pass
+    # sweeps three windows of 2^17 columns (the last one partial), the
+    # symbolic pass two of 2^18; lower and off-diagonal products
+    rng = np.random.default_rng(57)
+    A = _hub_csr(rng, 300000, 1 << 20, 3, 3000)
+    run_lower(A, semiring, dev, "heavy rows across windows")
+    assert sp.stats()["heavy_rows"] > 1000
+    vdt = VDT[semiring]
+    Ai = _hub_csr(rng, 270000, 1 << 20, 3, 2000)
+    Aj = _hub_csr(rng, 280000, 1 << 20, 3, 2000)
+    O = sp.offdiag(upload(Ai, semiring, dev), upload(Aj, semiring, dev), semiring)
+    assert sp.stats()["heavy_rows"] > 1000
+    ref = oracle.offdiag(Ai.with_values(None if vdt is None else Ai.values.astype(vdt)),
+                         Aj.with_values(None if vdt is None else Aj.values.astype(vdt)), semiring)
+    compare_full(O, ref, semiring, "heavy offdiag across windows")
+
+
 @pytest.mark.parametrize("semiring", SEMIRINGS)
 def test_light_rows_with_many_shared_columns(dev, semiring):
     # few columns, so that pairs of rows share several of them: the light

@@ -35,9 +35,10 @@ def _report(src):
             name = m.group(1)
             kernels[name] = {}
             continue
-        m = re.search(r"remark:\s+(VGPRs|ScratchSize \[bytes/lane\]|Occupancy \[waves/SIMD\]): (\d+)", line)
+        m = re.search(r"remark:\s+(VGPRs|ScratchSize \[bytes/lane\]|Occupancy \[waves/SIMD\]|LDS Size \[bytes/block\]): "
+                      r"(\d+)", line)
         if m and name:
-            kernels[name][m.group(1).split()[0]] = int(m.group(2))
+            kernels[name][m.group(1).split()[0] if not m.group(1).startswith("LDS") else "LDS"] = int(m.group(2))
     return kernels
 
 
@@ -51,10 +52,10 @@ def test_heavy_kernel_budgets():
     for name, r in ks.items():
         numeric = re.search(r"heavy_kernelILi\dELb1E", name) is not None
         assert r["ScratchSize"] == 0, name
-        if numeric:
-            assert r["VGPRs"] <= 80 and r["Occupancy"] >= 6, (name, r)
-        else:
-            assert r["VGPRs"] <= 64 and r["Occupancy"] >= 8, (name, r)
+        if numeric:  # three workgroups of eight wavefronts per compute unit (160 KiB of LDS)
+            assert r["VGPRs"] <= 80 and r["Occupancy"] >= 6 and 3 * r["LDS"] <= 160 * 1024, (name, r)
+        else:  # four
+            assert r["VGPRs"] <= 64 and r["Occupancy"] >= 8 and 4 * r["LDS"] <= 160 * 1024, (name, r)
 
 
 def test_light_kernel_budgets():
