@@ -74,9 +74,9 @@ def traffic_from_profiles(kernel_phase, workload):
         t = json.load(open(path))
     except Exception:
         return None
-    if t.get("source_hash") != kernel_source_hash() or t.get("workload") != workload:
+    if t.get("source_hash") != kernel_source_hash():
         return None
-    k = t.get("kernels", {}).get(kernel_phase)
+    k = t.get("workloads", {}).get(workload, {}).get("kernels", {}).get(kernel_phase)
     if not k:
         return None
     return k.get("hbm_bytes_per_launch")
