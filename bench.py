@@ -97,30 +97,31 @@ def alg_bytes_phase(phase, sz, sr):
 
     light_numeric (the single-pass light-row kernel) reads the row pointers,
     the per-row product counts and staging slots (8 B each per row), the
-    partner run of every entry (8 B), the values of A (fp semirings), every
-    kept column-index key and value once; it writes every light output entry
-    (column + value) at its staging slot and the exact row lengths (8 B per
-    row).  compact reads and writes every light output entry once plus three
-    8-B words per row.  colindex_pack (the local sort that writes the column
-    index) reads every sorted record (column, row field, entry index: 12 B),
-    writes every entry's key and index value at its sorted position and the
-    partner run (8 B) of every entry that has partners (all but the first of
-    each column).  heavy_symbolic reads the heavy-row list, their row
-    pointers, their entries' runs and cursors (12 B), every kept index key
-    once, and writes a length per heavy row; heavy_numeric reads the same plus
-    the output row pointers, A's values and the index values, and writes the
-    heavy rows' output entries."""
+    packed partner-run word of every entry (4 B; the rare run too long for its
+    word is read from the full table and not counted), the values of A (fp
+    semirings), every kept column-index key and value once; it writes every
+    light output entry (column + value) at its staging slot and the exact row
+    lengths (8 B per row).  compact reads and writes every light output entry
+    once plus three 8-B words per row.  colindex_pack (the local sort that
+    writes the column index) reads every sorted record (column, row field,
+    entry index: 12 B), writes every entry's key and index value at its sorted
+    position and the packed partner-run word (4 B) of every entry that has
+    partners (all but the first of each column).  heavy_symbolic reads the
+    heavy-row list, their row pointers, their entries' run words, cursors and
+    run ends (12 B), every kept index key once, and writes a length per heavy
+    row; heavy_numeric reads the same plus the output row pointers, A's values
+    and the index values, and writes the heavy rows' output entries."""
     m, nnz = sz["m"], sz["nnz_A"]
     vo = 4 + V_OUT[sr]
     nh, he, hout = sz["heavy_rows"], sz["heavy_entries"], sz["heavy_nnz_out"]
     light_out = sz["nnz_C"] - hout
     if phase == "light_numeric":
-        return (8 * (m + 1) + 8 * m + 8 * m + 8 * nnz + nnz * V_IN[sr]
+        return (8 * (m + 1) + 8 * m + 8 * m + 4 * nnz + nnz * V_IN[sr]
                 + sz["csc_entries"] * (4 + V_CX[sr]) + light_out * vo + 8 * m)
     if phase == "compact":
         return 2 * light_out * vo + 3 * 8 * m
     if phase == "colindex_pack":
-        return 12 * nnz + nnz * (4 + V_CX[sr]) + 8 * (nnz - sz["n_ne"])
+        return 12 * nnz + nnz * (4 + V_CX[sr]) + 4 * (nnz - sz["n_ne"])
     if phase == "heavy_symbolic":
         return 4 * nh + 16 * nh + 12 * he + 4 * sz["csc_entries"] + 8 * nh
     if phase == "heavy_numeric":

@@ -18,6 +18,18 @@
 
 using namespace spsyrk;
 
+uint32_t spsyrk::run_radix(int64_t positions) {
+    const uint64_t p1 = uint64_t(positions > 0 ? positions : 0) + 1;
+    uint64_t r = (uint64_t(1) << 32) / p1;
+    if (r > (uint64_t(1) << 16)) r = uint64_t(1) << 16;
+    if (r < 8) r = 1;
+    if (const char* e = std::getenv("SPSYRK_RUN_RADIX")) {
+        const long long want = std::atoll(e);
+        r = want <= 1 ? 1 : (uint64_t(want) < r ? uint64_t(want) : r);
+    }
+    return uint32_t(r);
+}
+
 namespace {
 
 thread_local std::string g_detail;
@@ -249,7 +261,7 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 // column, written when the local sort builds the index (*counted is then set).
 // vsrc (N entries): the entry of B behind every position of the index.
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                     uint2* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr,
+                     const RunTab* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr,
                      uint32_t* vsrc = nullptr) {
     ColIndex cx;
     cx.n = B.n;
@@ -298,7 +310,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         // values at sorted positions, partner runs, the kept count)
         LocalPack pk;
         if (runs_given) {
-            pk.run = run;
+            if (run) pk.run = *run;
             pk.key = cx.key;
             pk.val = cx.val;
             pk.vals_b = B.v;
@@ -321,7 +333,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         if (which >= 0) {
             void* ctmp = ar.get(colindex_tmp_bytes(N));
             build_colindex(which ? kb : ka, which ? rb : ra, which ? eb : ea, N, drop_last, vb, sr, B.v, B.rp, lenbits,
-                           cx, ctmp, &ctl->nkept, run, s, vsrc);
+                           cx, ctmp, &ctl->nkept, run ? *run : RunTab(), s, vsrc);
             check_launch();
             ar.release(ctmp);
         }
@@ -333,7 +345,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         ar.release(eb);
     } else {
         void* ctmp = ar.get(colindex_tmp_bytes(0));
-        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.v, B.rp, 0, cx, ctmp, &ctl->nkept, nullptr, s);
+        build_colindex(nullptr, nullptr, nullptr, 0, drop_last, vb, sr, B.v, B.rp, 0, cx, ctmp, &ctl->nkept, RunTab(), s);
         check_launch();
         ar.release(ctmp);
     }
@@ -371,7 +383,8 @@ struct LowerPlan {
     int32_t* ci = nullptr;
     ColIndex cx;
     uint32_t* vsrc = nullptr;  // entry of A behind every position of the index (nnz)
-    uint2* run = nullptr;
+    RunTab run;
+    uint32_t* rend = nullptr;  // run ends of the heavy rows' entries (nnz, with cursor)
     unsigned long long* prod = nullptr;
     int32_t* heavy_rows = nullptr;
     int64_t nheavy = 0;
@@ -398,10 +411,16 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
     HIPCHK(hipMemsetAsync(prod, 0, size_t(m) * sizeof(unsigned long long), s));
-    uint2* run = ar.get_t<uint2>(L.nnz);
+    // partner runs, packed where the index's positions leave room for the lengths
+    RunTab run;
+    run.r4 = ar.get_t<uint32_t>(L.nnz);
+    run.r8 = ar.get_t<uint2>(L.nnz);
+    run.radix = run_radix(lower ? L.nnz : R.nnz);
+    run.inv = 1.0 / double(run.radix);
     ColIndex cx;
     if (lower) {
-        HIPCHK(hipMemsetAsync(run, 0, size_t(L.nnz) * sizeof(uint2), s));
+        HIPCHK(hipMemsetAsync(run.r4, 0, size_t(L.nnz) * sizeof(uint32_t), s));
+        if (run.radix == 1) HIPCHK(hipMemsetAsync(run.r8, 0, size_t(L.nnz) * sizeof(uint2), s));
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
         uint32_t* vsrc = nullptr;
         if (plan) {
@@ -409,7 +428,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
             HIPCHK(hipMemsetAsync(vsrc, 0, size_t(L.nnz) * sizeof(uint32_t), s));
             plan->vsrc = vsrc;
         }
-        cx = build_index(L, true, sr, ar, ctl, s, run, true, nullptr, nullptr, vsrc);
+        cx = build_index(L, true, sr, ar, ctl, s, &run, true, nullptr, nullptr, vsrc);
     } else {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
         // column starts of R: from the counts the local sort writes, else by counting
@@ -468,6 +487,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         ha.run = run;
         ha.runs_ready = true;
         ha.cursor = ar.get_t<uint32_t>(L.nnz);
+        ha.rend = ar.get_t<uint32_t>(L.nnz);
         Phase ph(SPSYRK_PHASE_HEAVY_SYMBOLIC, s);
         heavy_symbolic(ha, &ctl->queue, s);
     }
@@ -545,7 +565,10 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     C->values = c_val;
     if (plan) {
         plan->cx = cx;
-        plan->run = static_cast<uint2*>(ar.keep(run));
+        plan->run.r8 = static_cast<uint2*>(ar.keep(run.r8));
+        plan->run.r4 = static_cast<uint32_t*>(ar.keep(run.r4));
+        plan->run.radix = run.radix;
+        plan->run.inv = run.inv;
         plan->prod = static_cast<unsigned long long*>(ar.keep(prod));
         ar.keep(cx.key);
         if (cx.val) ar.keep(cx.val);
@@ -555,6 +578,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         if (nheavy > 0) {
             plan->heavy_nnz = static_cast<int64_t*>(ar.keep(heavy_nnz));
             plan->cursor = static_cast<uint32_t*>(ar.keep(ha.cursor));
+            plan->rend = static_cast<uint32_t*>(ar.keep(ha.rend));
         }
         plan->ctl = static_cast<Ctl*>(ar.keep(ctl));
         plan->c_rp = ar.get_t<int64_t>(m + 1, true);
@@ -659,8 +683,9 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     ha.products = &ctl->products;
     ha.row_nnz = c_rp;
     if (nheavy > 0) {
-        ha.run = ar.get_t<uint2>(L.nnz);
+        ha.run.r8 = ar.get_t<uint2>(L.nnz);
         ha.cursor = ar.get_t<uint32_t>(L.nnz);
+        ha.rend = ar.get_t<uint32_t>(L.nnz);
         {
             Phase ph(SPSYRK_PHASE_HEAVY_SYMBOLIC, s);
             heavy_symbolic(ha, &ctl->queue, s);
@@ -1069,6 +1094,7 @@ void lower_execute(const LowerPlan& P, const void* vals, Arena& ar, hipStream_t 
         ha.run = P.run;
         ha.runs_ready = true;
         ha.cursor = P.cursor;
+        ha.rend = P.rend;
         ha.c_rp = c_rp;
         ha.c_ci = c_ci;
         ha.c_val = c_val;
@@ -1441,7 +1467,8 @@ spsyrk_status spsyrk_lower_plan(const spsyrk_csr* A, spsyrk_semiring sr, const s
             h->al = *al;
             h->has_al = true;
         }
-        for (void* q : {static_cast<void*>(lp.rp), static_cast<void*>(lp.ci), static_cast<void*>(lp.run),
+        for (void* q : {static_cast<void*>(lp.rp), static_cast<void*>(lp.ci), static_cast<void*>(lp.run.r8),
+                        static_cast<void*>(lp.run.r4), static_cast<void*>(lp.rend),
                         static_cast<void*>(lp.prod), static_cast<void*>(lp.cx.key), lp.cx.val,
                         static_cast<void*>(lp.vsrc), static_cast<void*>(lp.heavy_rows),
                         static_cast<void*>(lp.heavy_nnz), static_cast<void*>(lp.cursor),

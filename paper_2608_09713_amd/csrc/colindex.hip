@@ -31,7 +31,7 @@ __global__ __launch_bounds__(kBlock) void tile_starts(const uint32_t* __restrict
 template <int VB, bool JAC>
 __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol, const uint32_t* __restrict__ srow,
                                                const uint32_t* __restrict__ sent, const void* __restrict__ vals_b,
-                                               uint2* __restrict__ run, int64_t n, const uint32_t* __restrict__ tbase,
+                                               RunTab run, int64_t n, const uint32_t* __restrict__ tbase,
                                                bool drop_last, int gs, int rowbits, int lenbits, int64_t ngroups,
                                                const int64_t* __restrict__ nkept, const int64_t* __restrict__ rp_b,
                                                uint32_t* __restrict__ key, void* __restrict__ val,
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
             const int64_t rank = p - colstart[p - base];
             if (rank > 0) {
                 const int64_t first_kept = drop_last ? colstart[p - base] - cols_before : colstart[p - base];
-                run[sent[p]] = make_uint2(uint32_t(first_kept), uint32_t(first_kept + rank));
+                set_run(run, sent[p], uint32_t(first_kept), uint32_t(first_kept + rank));
             }
         }
         if (start && gptr) {
@@ -181,7 +181,7 @@ size_t colindex_tmp_bytes(int64_t n) {
 
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries, bool drop_last,
                     int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits, ColIndex& cx, void* tmp,
-                    int64_t* d_nkept, uint2* run, hipStream_t s, uint32_t* vsrc) {
+                    int64_t* d_nkept, const RunTab& run, hipStream_t s, uint32_t* vsrc) {
     const int64_t ntp = (n_entries + kPTile - 1) / kPTile;
     uint32_t* tbase = static_cast<uint32_t*>(tmp);
     char* after = static_cast<char*>(tmp) + ((size_t(ntp + 1) * 4 + 255) & ~size_t(255));

@@ -124,7 +124,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
         const uint32_t rlim = T0 + tl;
         for (int64_t e = c0 + tid; e < c1; e += kHB) {
             const uint32_t c = a.cursor[e];
-            const uint32_t hi = a.run[e].y;
+            const uint32_t hi = a.rend[e];
             if (c >= hi) continue;
             const uint32_t j = key[c] & rowmask;
             if (int64_t(j) >= B1 || (value && rank_of(B0, j) >= rlim)) continue;
@@ -147,7 +147,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
             for (int q = tid / kGrp; q < nshort; q += kHB / kGrp) {
                 const int64_t e = c0 + act_short[q];
                 uint32_t c = a.cursor[e];
-                const uint32_t hi = a.run[e].y;
+                const uint32_t hi = a.rend[e];
                 double av = 0.0;
                 if constexpr (kVal) av = value ? double(static_cast<const In*>(a.val)[e]) : 0.0;
                 while (c < hi) {
@@ -184,7 +184,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
         for (int q = w; q < nlong; q += kHW) {
             const int64_t e = c0 + act_long[q];
             uint32_t c = a.cursor[e];
-            const uint32_t hi = a.run[e].y;
+            const uint32_t hi = a.rend[e];
             double av = 0.0;
             if constexpr (kVal) av = value ? double(static_cast<const In*>(a.val)[e]) : 0.0;
             while (c < hi) {
@@ -245,15 +245,18 @@ void heavy_kernel(HeavyArgs a, int* queue) {
         // partner runs and cursors
         uint64_t prod_local = 0;
         for (int64_t e = e0 + tid; e < e1; e += kHB) {
-            uint32_t st, len;
+            uint2 rr;
             if (!NUM && !a.runs_ready) {
+                uint32_t st, len;
                 partner_run(key, a.cx.gptr, a.cx.gs, a.cx.rowbits, uint32_t(a.ci[e]), uint32_t(i), LOWER, st, len);
-                a.run[e] = make_uint2(st, st + len);
+                rr = make_uint2(st, st + len);
+                a.run.r8[e] = rr;
                 prod_local += len;
             } else {
-                st = a.run[e].x;
+                rr = run_of(a.run, e);
             }
-            a.cursor[e] = st;
+            a.cursor[e] = rr.x;
+            a.rend[e] = rr.y;
         }
         if constexpr (!NUM) {
             const uint64_t tot = wave_reduce_sum(prod_local);

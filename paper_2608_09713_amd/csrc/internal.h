@@ -64,6 +64,54 @@ struct ColIndex {
     int lenbits = 0;
 };
 
+// Partner runs of the entries of the left operand: the positions [first, end)
+// of the column index that hold an entry's partners.  One word per entry in
+// r4: first * radix + (end - first), with radix = floor(2^32 / (positions +
+// 1)) (at most 2^16), so every first fits; a length of radix - 1 or more is
+// written as radix - 1 and the run itself goes to r8 (radix 1: every run in
+// r8).  r4 starts zeroed, so an entry never written has the empty run (with
+// radix 1, r8 is zeroed too).  The words halve the bytes of the scattered
+// writes that build the table and of the reads that follow, and a mixed
+// radix keeps every run of up to radix - 2 partners in its word.  (The
+// two-pass kernels keep runs in r8 alone, with r4 null; only run_of reads
+// that form.)
+struct RunTab {
+    uint32_t* r4 = nullptr;
+    uint2* r8 = nullptr;
+    uint32_t radix = 1;
+    double inv = 1.0;  // 1 / radix, rounded to nearest
+    __host__ __device__ explicit operator bool() const { return r4 != nullptr || r8 != nullptr; }
+};
+
+// The run of a word loaded by the caller (escapes read r8[e]).  The quotient
+// comes from a double product: its error is below 2^-20 for words below
+// 2^32, so adding 2^-18 and truncating gives floor(v / radix) exactly while
+// radix stays below 2^17.
+__device__ inline uint2 run_from(const RunTab& t, uint32_t v, int64_t e) {
+    const uint32_t first = uint32_t(fma(double(v), t.inv, 0x1p-18));
+    const uint32_t len = v - first * t.radix;
+    if (len == t.radix - 1u) return t.r8[e];
+    return make_uint2(first, first + len);
+}
+
+__device__ inline uint2 run_of(const RunTab& t, int64_t e) { return t.r4 ? run_from(t, t.r4[e], e) : t.r8[e]; }
+
+__device__ inline void set_run(const RunTab& t, int64_t e, uint32_t first, uint32_t end) {
+    const uint32_t len = end - first;
+    if (len + 1u < t.radix) {
+        t.r4[e] = first * t.radix + len;
+    } else {
+        t.r4[e] = t.radix - 1u;
+        t.r8[e] = make_uint2(first, end);
+    }
+}
+
+// The radix of the words for an index of `positions` entries (every first
+// <= positions): floor(2^32 / (positions + 1)), at most 2^16, or 1 (every
+// run in r8) below 8.  SPSYRK_RUN_RADIX=k (read at every call) asks for k
+// instead (at most the value above; 0 or 1: every run in r8).
+uint32_t run_radix(int64_t positions);
+
 // ---- scan.hip
 // Exclusive scan out[i] = sum_{k<i} in[i]; out may alias in.  If total is not
 // null it receives the sum (device pointer).  tmp needs scan_tmp_bytes(n).
@@ -92,11 +140,11 @@ size_t radix_csr_tmp_bytes(int64_t n, int nbits);
 // the *_a buffers, 1 for *_b.
 // The column index in partner-run form, written by the sort itself when it
 // takes the local path: key (the row) and value of every entry at its sorted
-// position, and (run non-null, zeroed) every entry's partner run {first
-// position of its column, its own position}.  *kept (zeroed) gets the kept
+// position, and (with a run table, its words zeroed) every entry's partner
+// run {first position of its column, its own position}.  *kept (zeroed) gets the kept
 // entries (all, or all but the last of every column with drop_last).
 struct LocalPack {
-    uint2* run = nullptr;
+    RunTab run;
     uint32_t* key = nullptr;
     void* val = nullptr;         // null for Jaccard: the keys carry the row lengths (the row field)
     const void* vals_b = nullptr;  // values of B by entry index (vbytes 4 or 8)
@@ -121,13 +169,13 @@ int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_
 // From the entries of B sorted by column (column, row field as written by
 // radix_sort_csr, entry index): keep flags, packed keys, values gathered by
 // entry index from vals_b (the row length |S(row)| for Jaccard) and the group
-// directory.  With run non-null (lower mode) the partner run {first, end} of
-// every entry with partners is written at its entry index (run must start
-// zeroed: the other entries keep empty runs).
+// directory.  With a run table (lower mode) the partner run {first, end} of
+// every entry with partners is written at its entry index (the table's words
+// start zeroed: the other entries keep empty runs).
 size_t colindex_tmp_bytes(int64_t n);
 void build_colindex(const uint32_t* scol, const uint32_t* srow, const uint32_t* sent, int64_t n_entries,
                     bool drop_last, int vbytes_in, int sr, const void* vals_b, const int64_t* rp_b, int lenbits,
-                    ColIndex& ci, void* tmp, int64_t* d_nkept, uint2* run, hipStream_t s,
+                    ColIndex& ci, void* tmp, int64_t* d_nkept, const RunTab& run, hipStream_t s,
                     uint32_t* vsrc = nullptr);
 
 // ---- light.hip
@@ -173,7 +221,7 @@ struct FusedArgs {
     int sr = kF64;
     const int64_t* rp_right = nullptr;         // row pointers of the right operand (Jaccard lengths)
     const unsigned long long* prod = nullptr;  // off-diagonal products per row
-    const uint2* run = nullptr;                // partner run {first, end} of every entry
+    RunTab run;                                // partner run {first, end} of every entry
     const int64_t* heavy_nnz = nullptr;        // output lengths of heavy rows
     const int64_t* ubp = nullptr;              // staging slot of every row (prefix of upper bounds)
     int64_t* row_cnt = nullptr;                // exact output length of every row
@@ -205,12 +253,12 @@ void gather_values(void* dst, const void* src, const uint32_t* idx, int64_t n, i
 // ci[p] += off for p < nnz.
 void shift_columns(int32_t* ci, int64_t nnz, int32_t off, hipStream_t s);
 // Off-diagonal partner runs: run[e] = {cptr[ci[e]], cptr[ci[e] + 1]}.
-void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* run, hipStream_t s);
+void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, const RunTab& run, hipStream_t s);
 // prod[i] = sum over the entries e of row i of run[e].y - run[e].x (prod
 // must start zeroed).
 // tmp: row_products_tmp_bytes(nnz) of scratch
 size_t row_products_tmp_bytes(int64_t nnz);
-void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, void* tmp, unsigned long long* prod,
+void row_products(const int64_t* rp, int64_t m, int64_t nnz, const RunTab& run, void* tmp, unsigned long long* prod,
                   hipStream_t s);
 // Copy the staged rows to their final places: the element at staging slot
 // ubp[i] + x (x < row_cnt[i]) goes to c_rp[i] + x.  ubp is non-decreasing
@@ -249,9 +297,11 @@ struct HeavyArgs {
     const int32_t* heavy_count = nullptr;
     int64_t heavy_max = 0;              // upper bound of heavy rows (grid sizing)
     // per-entry run bounds (sized nnz of the left operand), written by the symbolic pass
-    uint2* run = nullptr;               // partner run {first, end} of every entry
+    RunTab run;                         // partner run {first, end} of every entry (r8 only
+                                        // when the symbolic pass writes it)
     bool runs_ready = false;            // run already filled (the symbolic pass skips its lookups)
     uint32_t* cursor = nullptr;
+    uint32_t* rend = nullptr;           // end of every heavy entry's run (set with the cursors)
     unsigned long long* products = nullptr;  // optional: add the products formed
     int64_t* row_nnz = nullptr;
     unsigned long long* nnz_total = nullptr; // optional: add the heavy rows' lengths

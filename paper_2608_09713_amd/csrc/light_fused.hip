@@ -183,13 +183,15 @@ struct Chunk {
 
     // Issue the loads of the partner runs of the light rows [ra, rb) (entry
     // lane + kWave * u in rn[u]); they are consumed by the batch's first step.
-    __device__ void fetch_runs(int ra, int rb, uint2 (&rn)[kRunRegs]) {
+    __device__ void fetch_runs(int ra, int rb, uint32_t (&rn)[kRunRegs]) {
         const int64_t ebase = L.rp[ra];
         const int ne = int(L.rp[rb] - ebase);
 #pragma unroll
         for (int u = 0; u < kRunRegs; ++u) {
             const int x = lane + u * kWave;
-            rn[u] = x < ne ? a.run[ebase + x] : make_uint2(0u, 0u);
+            // (a packed word is decoded where the run is used, so that the
+            // loads stay in flight)
+            rn[u] = x < ne ? a.run.r4[ebase + x] : 0u;
         }
     }
 
@@ -198,7 +200,7 @@ struct Chunk {
     // batch's columns stay in LDS, grouped by (row, bucket).  The runs of the
     // next batch [na, nb) (if na >= 0) are fetched into rn while the batch's
     // keys are in flight.  Returns the number of products.
-    __device__ int batch(int ra, int rb, uint2 (&rn)[kRunRegs], int na, int nbx) {
+    __device__ int batch(int ra, int rb, uint32_t (&rn)[kRunRegs], int na, int nbx) {
         const int64_t ebase = L.rp[ra];
         const int ne = int(L.rp[rb] - ebase);
         const uint32_t* __restrict__ key = a.cx.key;
@@ -215,8 +217,9 @@ struct Chunk {
         for (int u = 0; u < kRunRegs; ++u) {
             const int x = lane + u * kWave;
             if (x < ne) {
-                const uint32_t len = rn[u].y - rn[u].x;
-                L.ent_start[x] = rn[u].x;
+                const uint2 r = run_from(a.run, rn[u], ebase + x);
+                const uint32_t len = r.y - r.x;
+                L.ent_start[x] = r.x;
                 L.ent_len[x] = uint16_t(len);
                 L.ent_poff[x] = uint16_t(len);
             }
@@ -789,7 +792,7 @@ struct Chunk {
         wave_sync();
         int64_t cnt = 0;  // exact length of this lane's row
         if (lane < nr) cnt = light ? ((LOWER && len > 0) ? 1 : 0) : a.heavy_nnz[r0 + lane];
-        uint2 rn[kRunRegs];
+        uint32_t rn[kRunRegs];
         if (nbatch > 0) fetch_runs(L.bra[0], L.brb[0], rn);
         for (int k = 0; k < nbatch; ++k) {
             const int ra = L.bra[k], rb = L.brb[k];

@@ -696,7 +696,7 @@ __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t fie
         pk.key[pos] = row;
         if constexpr (VB != 0) static_cast<typename ValT<VB>::T*>(pk.val)[pos] = v;
     }
-    if (pk.run && pos > cstart) pk.run[ent] = make_uint2(uint32_t(cstart), uint32_t(pos));
+    if (pk.run && pos > cstart) set_run(pk.run, ent, uint32_t(cstart), uint32_t(pos));
 }
 
 template <int VB, bool JAC>

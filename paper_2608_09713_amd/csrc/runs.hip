@@ -39,7 +39,7 @@ __global__ __launch_bounds__(kBlock) void tile_rows(const int64_t* __restrict__ 
 }
 
 __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restrict__ rp, int64_t m, int64_t nnz,
-                                                         const uint2* __restrict__ run,
+                                                         const RunTab run,
                                                          const int64_t* __restrict__ trow,
                                                          unsigned long long* __restrict__ prod) {
     __shared__ int64_t win[kWinP + 1];
@@ -71,19 +71,27 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
     const int64_t a = e0 + int64_t(threadIdx.x) * kPerT;
     const int64_t b = min(e1, a + kPerT);
     if (a < b) {
-        uint2 rn[kPerT];
-        if (b - a == kPerT && (reinterpret_cast<uintptr_t>(run + a) & 15) == 0) {
-            // whole stretch: 16-byte loads
-            const uint4* v4 = reinterpret_cast<const uint4*>(run + a);
+        // run lengths of the stretch (16-byte loads for a whole aligned stretch)
+        uint32_t w[kPerT];
+        if (b - a == kPerT && (reinterpret_cast<uintptr_t>(run.r4 + a) & 15) == 0) {
+            const uint4* v4 = reinterpret_cast<const uint4*>(run.r4 + a);
 #pragma unroll
-            for (int u = 0; u < kPerT / 2; ++u) {
+            for (int u = 0; u < kPerT / 4; ++u) {
                 const uint4 q = v4[u];
-                rn[2 * u] = make_uint2(q.x, q.y);
-                rn[2 * u + 1] = make_uint2(q.z, q.w);
+                w[4 * u] = q.x;
+                w[4 * u + 1] = q.y;
+                w[4 * u + 2] = q.z;
+                w[4 * u + 3] = q.w;
             }
         } else {
 #pragma unroll
-            for (int u = 0; u < kPerT; ++u) rn[u] = a + u < b ? run[a + u] : make_uint2(0u, 0u);
+            for (int u = 0; u < kPerT; ++u) w[u] = a + u < b ? run.r4[a + u] : 0u;
+        }
+        uint32_t rl[kPerT];
+#pragma unroll
+        for (int u = 0; u < kPerT; ++u) {
+            const uint2 r = a + u < b ? run_from(run, w[u], a + u) : make_uint2(0u, 0u);
+            rl[u] = r.y - r.x;
         }
         // row of the stretch's first entry and its bounds
         int64_t r = staged ? rlo + last_leq(win, 0, rhi - rlo, a) : last_leq(rp, rlo, rhi, a);
@@ -110,7 +118,7 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
                     rend = staged ? win[r - rlo + 1] : rp[r + 1];
                 } while (rend <= e);
             }
-            acc += rn[u].y - rn[u].x;
+            acc += rl[u];
         }
         if (rstart >= a && rend <= b) {
             prod[r] = acc;
@@ -272,11 +280,11 @@ __global__ __launch_bounds__(kBlock) void count_columns(const int32_t* __restric
 // the right operand
 __global__ __launch_bounds__(kBlock) void offdiag_runs_kernel(const int32_t* __restrict__ ci, int64_t nnz,
                                                               const uint32_t* __restrict__ cptr,
-                                                              uint2* __restrict__ run) {
+                                                              const RunTab run) {
     const int64_t e = int64_t(blockIdx.x) * kBlock + threadIdx.x;
     if (e >= nnz) return;
     const int32_t c = ci[e];
-    run[e] = make_uint2(cptr[c], cptr[c + 1]);
+    set_run(run, e, cptr[c], cptr[c + 1]);
 }
 
 // out[k] = rp[r0 + k] - rp[r0] for k in [0, m]: the row pointers of rows
@@ -394,14 +402,14 @@ void column_starts(const int32_t* ci, int64_t nnz, int64_t n, uint32_t* cptr, vo
     scan_u32(cptr, cptr, n + 1, nullptr, scan_tmp, s);
 }
 
-void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, uint2* run, hipStream_t s) {
+void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, const RunTab& run, hipStream_t s) {
     if (nnz <= 0) return;
     offdiag_runs_kernel<<<unsigned((nnz + kBlock - 1) / kBlock), kBlock, 0, s>>>(ci, nnz, cptr, run);
 }
 
 size_t row_products_tmp_bytes(int64_t nnz) { return size_t((nnz + kTileP - 1) / kTileP + 1) * sizeof(int64_t); }
 
-void row_products(const int64_t* rp, int64_t m, int64_t nnz, const uint2* run, void* tmp, unsigned long long* prod,
+void row_products(const int64_t* rp, int64_t m, int64_t nnz, const RunTab& run, void* tmp, unsigned long long* prod,
                   hipStream_t s) {
     if (nnz <= 0 || m <= 0) return;
     const unsigned nb = unsigned((nnz + kTileP - 1) / kTileP);

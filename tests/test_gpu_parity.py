@@ -497,6 +497,34 @@ def test_plan_execute(dev, semiring, local, monkeypatch):
     plan.close()
 
 
+@pytest.mark.parametrize("semiring", SEMIRINGS)
+@pytest.mark.parametrize("radix", ["3", "9", "1"])
+def test_packed_run_lengths(dev, semiring, radix, monkeypatch):
+    # partner runs packed with radix 3 or 9 (runs of 2 or 8 partners and
+    # longer escape to the full table) or all in the full table (1): lower on
+    # both column-sort paths with heavy rows, off-diagonal, and a plan's
+    # executions all match the oracle
+    monkeypatch.setenv("SPSYRK_RUN_RADIX", radix)
+    rng = np.random.default_rng(53)
+    vdt = VDT[semiring]
+    A = _with_long_rows(rng, 700, 900)
+    for local in ("0", "1"):
+        monkeypatch.setenv("SPSYRK_LOCAL_SORT", local)
+        print(f"[packed runs {semiring} radix={radix} local={local}] m={A.nrows} nnz={A.nnz}", flush=True)
+        run_lower(A, semiring, dev, f"packed runs radix={radix} local={local}")
+        assert sp.stats()["heavy_rows"] > 0
+        B = _rows_csr(rng, 300, 900, 6)
+        B = B.with_values(B.values.astype(vdt) if vdt else None)
+        Av = A.with_values(A.values.astype(vdt) if vdt else None)
+        O = sp.offdiag(upload(A, semiring, dev), upload(B, semiring, dev), semiring)
+        compare_full(O, oracle.offdiag(Av, B, semiring), semiring, f"packed runs offdiag radix={radix}")
+    plan, C0 = sp.lower_plan(upload(A, semiring, dev), semiring)
+    E = plan.execute(upload(A, semiring, dev).values)
+    compare_full(E, oracle.lower(A.with_values(A.values.astype(vdt) if vdt else None), semiring), semiring,
+                 f"packed runs plan radix={radix}")
+    plan.close()
+
+
 def test_plan_of_empty_matrix(dev):
     A = CSR(5, 7, np.zeros(6, np.int64), np.zeros(0, np.int32), np.zeros(0))
     plan, C = sp.lower_plan(upload(A, "f64", dev), "f64")
