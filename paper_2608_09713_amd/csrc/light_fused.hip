@@ -36,7 +36,6 @@ constexpr int kFR = kFusedRows;      // rows per chunk (upper limit)
 constexpr int kFB = kFP + kFR;       // buckets per batch
 constexpr int kWavesF = 2;           // wavefronts per workgroup
 constexpr int kDealtBelow = 16;      // chunks per launched wavefront below which chunks are dealt out
-constexpr int kMaxBatches = kFR;
 constexpr int kRunRegs = kFE / kWave;  // partner runs per lane held in registers
 constexpr int kSmall = 8;              // buckets up to this size are merged in registers
 constexpr int kTBits = 9;              // product index bits in s_t (row above them)
@@ -81,10 +80,6 @@ struct WaveLds {
     uint16_t rnb[kFR + 1];    // buckets of the row in the current batch
     uint16_t rbb[kFR + 1];    // first bucket of the row in the current batch
     uint64_t rscale[kFR];     // bucket of column j: (j * rscale) >> 32 spreads [0, range) evenly
-    uint8_t rlight[kFR];
-    uint32_t rpp[kFR + 1];    // products of the chunk's light rows before each row
-    uint8_t rnext[kFR];       // end of a batch opened at each light row
-    uint8_t bra[kMaxBatches + 1], brb[kMaxBatches + 1];  // batches [bra, brb) of the chunk
     uint32_t ent_start[kFE];
     uint16_t ent_len[kFE];
     alignas(4) uint8_t ent_row[kFE];
@@ -745,47 +740,34 @@ struct Chunk {
         wave_sync();
         int64_t len = 0;
         bool light = false;
+        const int64_t rpn = __shfl_down(rpv, 1, kWave);  // row pointer after this lane's row
         if (lane < nr) {
-            len = L.rp[lane + 1] - rpv;
+            len = rpn - rpv;
             light = pr <= uint64_t(kFP) && len <= kFE;
-            L.rlight[lane] = light ? 1 : 0;
             L.rprod[lane] = light ? uint16_t(pr) : 0;
             // light rows are written at their upper-bound slots (products + diagonal)
             L.rcnt[lane] = ubv;
         }
-        wave_sync();
-        // batches of consecutive light rows, found in parallel: every light
-        // row knows where a batch opened at it must end (at the next heavy
-        // row, or where its entries or products would overflow the LDS
-        // budget); the batch starts are then chained (same in every lane)
+        // batches of consecutive light rows, cut greedily: a batch opened at
+        // row ra takes the following light rows while its entries and products
+        // fit the LDS budget; every lane tests its own row against the prefix
+        // sums at ra, and the batch ends at the first row that fails.  Lane k
+        // keeps batch k's rows (ra | rb << 8).
         const uint64_t lightmask = __ballot(lane < nr && light);
-        {
-            const uint32_t pinc = wave_inclusive_scan((lane < nr && light) ? uint32_t(pr) : 0u);
-            if (lane < nr) L.rpp[lane + 1] = pinc;
-            if (lane == 0) L.rpp[0] = 0;
-        }
-        wave_sync();
-        if (lane < nr && light) {
-            const uint64_t later = ~lightmask & ((uint64_t(1) << nr) - 1) & (~uint64_t(0) << (lane + 1));
-            int lo = lane + 1, hi = later ? __ffsll((unsigned long long)later) - 1 : nr;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (L.rp[mid] - L.rp[lane] <= kFE && L.rpp[mid] - L.rpp[lane] <= uint32_t(kFP))
-                    lo = mid;
-                else
-                    hi = mid - 1;
-            }
-            L.rnext[lane] = uint8_t(lo);
-        }
-        wave_sync();
+        const uint32_t mypr = (lane < nr && light) ? uint32_t(pr) : 0u;
+        const uint32_t pinc = wave_inclusive_scan(mypr);
+        const uint32_t pexc = pinc - mypr;
         int nbatch = 0;
+        uint32_t mybatch = 0;
         for (uint64_t rest = lightmask; rest;) {
             const int ra = __ffsll((unsigned long long)rest) - 1;
-            const int rb = L.rnext[ra];
-            if (lane == 0) {
-                L.bra[nbatch] = uint8_t(ra);
-                L.brb[nbatch] = uint8_t(rb);
-            }
+            const int64_t ea = int64_t(uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(rpv)), ra))) |
+                                       (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(uint64_t(rpv) >> 32)), ra))) << 32));
+            const uint32_t pa = uint32_t(__builtin_amdgcn_readlane(int(pexc), ra));
+            const bool ok = lane >= ra && lane < nr && light && rpn - ea <= kFE && pinc - pa <= uint32_t(kFP);
+            const uint64_t okm = __ballot(ok) >> ra;
+            const int rb = ra + __ffsll((unsigned long long)~okm) - 1;
+            if (lane == nbatch) mybatch = uint32_t(ra) | (uint32_t(rb) << 8);
             ++nbatch;
             rest = lightmask & (~uint64_t(0) << rb);
         }
@@ -793,11 +775,14 @@ struct Chunk {
         int64_t cnt = 0;  // exact length of this lane's row
         if (lane < nr) cnt = light ? ((LOWER && len > 0) ? 1 : 0) : a.heavy_nnz[r0 + lane];
         uint32_t rn[kRunRegs];
-        if (nbatch > 0) fetch_runs(L.bra[0], L.brb[0], rn);
+        uint32_t bk = nbatch > 0 ? uint32_t(__builtin_amdgcn_readlane(int(mybatch), 0)) : 0u;
+        if (nbatch > 0) fetch_runs(int(bk & 0xffu), int(bk >> 8), rn);
         for (int k = 0; k < nbatch; ++k) {
-            const int ra = L.bra[k], rb = L.brb[k];
+            const int ra = int(bk & 0xffu), rb = int(bk >> 8);
             const bool more = k + 1 < nbatch;
-            const int P = batch(ra, rb, rn, more ? int(L.bra[k + 1]) : -1, more ? int(L.brb[k + 1]) : 0);
+            const uint32_t bn = more ? uint32_t(__builtin_amdgcn_readlane(int(mybatch), k + 1)) : 0u;
+            const int P = batch(ra, rb, rn, more ? int(bn & 0xffu) : -1, more ? int(bn >> 8) : 0);
+            bk = bn;
             if (lane >= ra && lane < rb)
                 cnt += int64_t(L.ucnt[L.rbb[lane] + L.rnb[lane]] - L.ucnt[L.rbb[lane]]);
             write(ra, rb, P);
