@@ -100,9 +100,11 @@ def alg_bytes_phase(phase, sz, sr):
     packed partner-run word of every entry (4 B; the rare run too long for its
     word is read from the full table and not counted), the values of A (fp
     semirings), every kept column-index key and value once; it writes every
-    light output entry (column + value) at its staging slot and the exact row
-    lengths (8 B per row).  compact reads and writes every light output entry
-    once plus three 8-B words per row.  colindex_pack (the local sort that
+    light output entry at its staging slot (column + value, or one packed 4-B
+    word for counts and Jaccard values when the stats say so) and the exact
+    row lengths (8 B per row).  compact reads every staged entry and writes it
+    as column + value once, plus three 8-B words per row (and, unpacking
+    Jaccard words, the row pointers of A).  colindex_pack (the local sort that
     writes the column index) reads every sorted record (column, row field,
     entry index: 12 B), writes every entry's key and index value at its sorted
     position and the packed partner-run word (4 B) of every entry that has
@@ -115,11 +117,13 @@ def alg_bytes_phase(phase, sz, sr):
     vo = 4 + V_OUT[sr]
     nh, he, hout = sz["heavy_rows"], sz["heavy_entries"], sz["heavy_nnz_out"]
     light_out = sz["nnz_C"] - hout
+    packed = bool(sz.get("packed_staging"))
+    staged = 4 if packed else vo
     if phase == "light_numeric":
         return (8 * (m + 1) + 8 * m + 8 * m + 4 * nnz + nnz * V_IN[sr]
-                + sz["csc_entries"] * (4 + V_CX[sr]) + light_out * vo + 8 * m)
+                + sz["csc_entries"] * (4 + V_CX[sr]) + light_out * staged + 8 * m)
     if phase == "compact":
-        return 2 * light_out * vo + 3 * 8 * m
+        return light_out * (staged + vo) + 3 * 8 * m + (8 * (m + 1) if packed and sr == "jaccard" else 0)
     if phase == "colindex_pack":
         return 12 * nnz + nnz * (4 + V_CX[sr]) + 4 * (nnz - sz["n_ne"])
     if phase == "heavy_symbolic":
@@ -368,7 +372,7 @@ def main():
     sz = {"m": A.nrows, "nnz_A": A.nnz, "nnz_C": C.nnz, "csc_entries": st["csc_entries"],
           "ngroups": (A.ncols + (1 << st["group_shift"]) - 1) >> st["group_shift"], "n_ne": n_ne,
           "heavy_rows": st["heavy_rows"], "heavy_entries": st["heavy_entries"],
-          "heavy_nnz_out": st["heavy_nnz_out"]}
+          "heavy_nnz_out": st["heavy_nnz_out"], "packed_staging": st["packed_staging"]}
     flops = 2 * F_L
     value = flops / t_step / 1e9
     mirror_nnz = M.nnz if M is not None else None

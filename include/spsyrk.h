@@ -326,6 +326,9 @@ typedef struct spsyrk_stats {
     int64_t heavy_nnz_out;    /* result entries of heavy rows */
     int32_t group_shift;      /* log2 of columns per directory group */
     int32_t row_bits;         /* bits of the row id inside a packed column key */
+    int32_t packed_staging;   /* 1 if the light rows' counts or Jaccard values were staged as one
+                                 packed 4-byte word per output (column and value) */
+    int32_t reserved;         /* 0 */
 } spsyrk_stats;
 
 spsyrk_status spsyrk_last_stats(spsyrk_stats* out);

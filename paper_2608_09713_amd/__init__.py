@@ -60,7 +60,8 @@ class _Allocator(ctypes.Structure):
 class Stats(ctypes.Structure):
     _fields_ = [("nnz_out", ctypes.c_int64), ("csc_entries", ctypes.c_int64), ("heavy_rows", ctypes.c_int64),
                 ("light_rows", ctypes.c_int64), ("products", ctypes.c_int64), ("heavy_entries", ctypes.c_int64),
-                ("heavy_nnz_out", ctypes.c_int64), ("group_shift", ctypes.c_int32), ("row_bits", ctypes.c_int32)]
+                ("heavy_nnz_out", ctypes.c_int64), ("group_shift", ctypes.c_int32), ("row_bits", ctypes.c_int32),
+                ("packed_staging", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

@@ -43,6 +43,13 @@ bool two_pass() {
     return e && e[0] == '1';
 }
 
+// packed staging of count and Jaccard outputs where it fits (SPSYRK_PACK_STAGING=0
+// turns it off; read at every call)
+bool pack_staging() {
+    const char* e = std::getenv("SPSYRK_PACK_STAGING");
+    return !(e && e[0] == '0');
+}
+
 constexpr int64_t kLimit = int64_t(1) << 31;
 
 void set_detail(const char* fmt, ...) {
@@ -167,7 +174,8 @@ struct Ctl {
     unsigned long long light_cap;
     unsigned long long heavy_sums[2];  // entries of A and output entries of the heavy rows
     unsigned long long chunk_counter;
-    int64_t pad[2];
+    unsigned long long maxlen;  // largest row length of the left operand
+    int64_t pad[1];
 };
 
 struct HostCtl {
@@ -453,7 +461,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
         row_products(L.rp, m, L.nnz, run, ptmp, prod, s);
-        classify_rows(L.rp, prod, m, lower, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s);
+        classify_rows(L.rp, prod, m, lower, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s,
+                      &ctl->maxlen);
     }
     check_launch();
     Ctl h = read_ctl(ctl, s);
@@ -498,8 +507,22 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         Phase ph(SPSYRK_PHASE_SCAN, s);
         scan_i64(ub, ubp, m + 1, &ctl->total2, stmp, s);
     }
+    // counts and Jaccard values of the light rows staged as one word per
+    // output (column and packed value) where the words fit: the counts are
+    // at most the light rows' lengths, the partners' lengths at most the
+    // largest row's
+    uint32_t pack_rr = 0, pack_r2 = 0;
+    if (lower && (sr == kCount || sr == kJaccard) && pack_staging()) {
+        const uint64_t lmax = h.maxlen;
+        const uint64_t r1 = (lmax < uint64_t(kFusedEntries) ? lmax : uint64_t(kFusedEntries)) + 1, r2 = lmax + 1;
+        const uint64_t rr = sr == kJaccard ? r1 * r2 : r1;
+        if (rr < (uint64_t(1) << 17) && uint64_t(m) * rr <= (uint64_t(1) << 32)) {
+            pack_rr = uint32_t(rr);
+            pack_r2 = sr == kJaccard ? uint32_t(r2) : 0u;
+        }
+    }
     int32_t* s_ci = ar.get_t<int32_t>(light_cap > 0 ? light_cap : 1);
-    void* s_val = ar.get(size_t(light_cap > 0 ? light_cap : 1) * vbo);
+    void* s_val = ar.get(size_t(pack_rr || light_cap <= 0 ? 1 : light_cap) * vbo);
     int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
     HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
 
@@ -525,6 +548,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     fa.chunk_counter = &ctl->chunk_counter;
     fa.c_ci = s_ci;
     fa.c_val = s_val;
+    fa.pack_rr = pack_rr;
+    fa.pack_r2 = pack_r2;
     {
         Phase ph(SPSYRK_PHASE_LIGHT_NUMERIC, s);
         light_fused(fa, s);
@@ -544,7 +569,8 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     {
         Phase ph(SPSYRK_PHASE_COMPACT, s);
         void* ctmp = ar.get(compact_tmp_bytes(light_cap));
-        compact_rows(m, light_cap, ubp, row_cnt, c_rp, s_ci, s_val, vbo, ctmp, c_ci, c_val, s);
+        compact_rows(m, light_cap, ubp, row_cnt, c_rp, s_ci, s_val, vbo, ctmp, c_ci, c_val, s, pack_rr ? sr : 0,
+                     pack_rr, pack_r2, L.rp);
     }
     check_launch();
     if (nheavy > 0) {
@@ -597,6 +623,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     st.products = int64_t(h.products);
     st.group_shift = cx.gs;
     st.row_bits = cx.rowbits;
+    st.packed_staging = pack_rr != 0 ? 1 : 0;
     g_stats = st;
     g_stats_valid = true;
 }

@@ -230,16 +230,22 @@ struct FusedArgs {
     unsigned long long* chunk_counter = nullptr;  // zeroed: chunks handed out so far
     int32_t* c_ci = nullptr;                   // staging columns
     void* c_val = nullptr;                     // staging values
+    // > 0 (count and Jaccard): every output is staged as one word in c_ci,
+    // column * pack_rr + packed value, where the packed value is the count,
+    // or (Jaccard) the count * pack_r2 + the partner's length; the
+    // compaction unpacks it (c_val unused)
+    uint32_t pack_rr = 0, pack_r2 = 0;
 };
 // light rows: columns and values at the staging slots, exact lengths in row_cnt
 // (heavy rows: their length from heavy_nnz)
 void light_fused(const FusedArgs& a, hipStream_t s);
 // heavy rows (over the limits) into a list; light capacity sum(prod + diagonal) and
 // the sum of prod over all rows into the two counters
-// and ub[i] = products + diagonal for light rows, 0 for heavy rows
+// and ub[i] = products + diagonal for light rows, 0 for heavy rows; maxlen
+// (optional, zeroed): the largest row length
 void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m, bool lower, int32_t* heavy_rows,
                    int32_t* heavy_count, unsigned long long* light_cap, unsigned long long* prod_sum, int64_t* ub,
-                   hipStream_t s);
+                   hipStream_t s, unsigned long long* maxlen = nullptr);
 
 // ---- runs.hip
 // Dense column starts of a CSR matrix's column-sorted copy: cptr[c] =
@@ -263,11 +269,15 @@ void row_products(const int64_t* rp, int64_t m, int64_t nnz, const RunTab& run, 
 // Copy the staged rows to their final places: the element at staging slot
 // ubp[i] + x (x < row_cnt[i]) goes to c_rp[i] + x.  ubp is non-decreasing
 // with ubp[m] = staged; rows with no staging room (heavy rows) copy nothing.
+// packed (kCount or kJaccard, else 0): s_ci holds packed words (see
+// FusedArgs::pack_rr), unpacked into the column and the 4-byte value; rp_a
+// gives the rows' lengths (Jaccard).
 // tmp: compact_tmp_bytes(staged) of scratch
 size_t compact_tmp_bytes(int64_t staged);
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
                   const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
-                  hipStream_t s);
+                  hipStream_t s, int packed = 0, uint32_t pack_rr = 0, uint32_t pack_r2 = 0,
+                  const int64_t* rp_a = nullptr);
 // Reorders the heavy-row list rows[0..n) by decreasing magnitude of their
 // product counts (powers of two; stable inside one), so that the rows with
 // the most work are taken first from the heavy kernels' queue.

@@ -635,14 +635,17 @@ struct Chunk {
     }
 
     // value of a merged column: the sum (plus-times), the count, or the
-    // Jaccard bits from the count and the two row lengths
-    __device__ static Item finish(Item acc, int32_t cnt, int64_t len_i) {
+    // Jaccard bits from the count and the two row lengths (with packed
+    // staging: the count and the partner's length, cnt * pack_r2 + |S(j)|,
+    // for the compaction to finish)
+    __device__ Item finish(Item acc, int32_t cnt, int64_t len_i) const {
         if constexpr (kVal)
             return acc;
         else if constexpr (SR == kCount)
             return cnt;
         else
-            return __float_as_int(jaccard(cnt, len_i, acc));
+            return a.pack_rr ? int32_t(uint32_t(cnt) * a.pack_r2 + uint32_t(acc))
+                             : __float_as_int(jaccard(cnt, len_i, acc));
     }
 
     template <int N>
@@ -679,27 +682,30 @@ struct Chunk {
             const int64_t len = L.rp[r + 1] - L.rp[r];
             if (len > 0) {
                 const int64_t p = L.rcnt[r] + int64_t(L.ucnt[L.rbb[r] + L.rnb[r]] - L.ucnt[L.rbb[r]]);
-                a.c_ci[p] = int32_t(r0 + r);
-                Out dv;
+                Item dv;
                 if constexpr (kVal) {
                     double s = 0.0;
                     for (int64_t e = L.rp[r]; e < L.rp[r + 1]; ++e) {
                         const double v = double(static_cast<const In*>(a.val)[e]);
                         s += v * v;
                     }
-                    dv = Out(s);
-                } else if constexpr (SR == kCount) {
-                    dv = int32_t(len);
+                    dv = s;
                 } else {
-                    dv = jaccard(int32_t(len), len, len);
+                    dv = finish(Item(len), int32_t(len), len);  // |S(i) and S(i)| = |S(i)|
                 }
-                static_cast<Out*>(a.c_val)[p] = dv;
+                emit(p, uint32_t(r0 + r), dv);
             }
         }
         wave_sync();
     }
 
     __device__ void emit(int64_t p, uint32_t j, Item v) {
+        if constexpr (!kVal) {
+            if (a.pack_rr) {  // one staged word: column and packed value
+                reinterpret_cast<uint32_t*>(a.c_ci)[p] = j * a.pack_rr + uint32_t(v);
+                return;
+            }
+        }
         a.c_ci[p] = int32_t(j);
         Out ov;
         if constexpr (kVal)
@@ -868,13 +874,15 @@ __global__ __launch_bounds__(kBlock) void classify_kernel(const int64_t* __restr
                                                           const unsigned long long* __restrict__ prod, int64_t m,
                                                           bool lower, int32_t* __restrict__ heavy_rows,
                                                           int32_t* heavy_count, unsigned long long* light_cap,
-                                                          unsigned long long* prod_sum, int64_t* __restrict__ ub) {
-    __shared__ unsigned long long wt[kWavesPerBlock][2];
-    unsigned long long cap = 0, ps = 0;
+                                                          unsigned long long* prod_sum, int64_t* __restrict__ ub,
+                                                          unsigned long long* maxlen) {
+    __shared__ unsigned long long wt[kWavesPerBlock][3];
+    unsigned long long cap = 0, ps = 0, ml = 0;
     for (int64_t i = int64_t(blockIdx.x) * kBlock + threadIdx.x; i < m; i += int64_t(gridDim.x) * kBlock) {
         const int64_t len = rp[i + 1] - rp[i];
         const unsigned long long pr = prod[i];
         ps += pr;
+        ml = max(ml, (unsigned long long)len);
         int64_t u = 0;
         if (pr <= (unsigned long long)kFP && len <= kFE) {
             u = int64_t(pr) + ((lower && len > 0) ? 1 : 0);
@@ -886,19 +894,23 @@ __global__ __launch_bounds__(kBlock) void classify_kernel(const int64_t* __restr
     }
     cap = wave_reduce_sum(cap);
     ps = wave_reduce_sum(ps);
+    ml = wave_reduce_max(ml);
     if (lane_id() == 0) {
         wt[threadIdx.x / kWave][0] = cap;
         wt[threadIdx.x / kWave][1] = ps;
+        wt[threadIdx.x / kWave][2] = ml;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned long long c = 0, p = 0;
+        unsigned long long c = 0, p = 0, l = 0;
         for (int w = 0; w < kWavesPerBlock; ++w) {
             c += wt[w][0];
             p += wt[w][1];
+            l = max(l, wt[w][2]);
         }
         if (c) atomicAdd(light_cap, c);
         if (p) atomicAdd(prod_sum, p);
+        if (l && maxlen) atomicMax(maxlen, l);
     }
 }
 
@@ -906,12 +918,12 @@ __global__ __launch_bounds__(kBlock) void classify_kernel(const int64_t* __restr
 
 void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m, bool lower, int32_t* heavy_rows,
                    int32_t* heavy_count, unsigned long long* light_cap, unsigned long long* prod_sum, int64_t* ub,
-                   hipStream_t s) {
+                   hipStream_t s, unsigned long long* maxlen) {
     if (m <= 0) return;
     int64_t grid = (m + kBlock - 1) / kBlock;
     if (grid > 1024) grid = 1024;
     classify_kernel<<<unsigned(grid), kBlock, 0, s>>>(rp, prod, m, lower, heavy_rows, heavy_count, light_cap,
-                                                      prod_sum, ub);
+                                                      prod_sum, ub, maxlen);
 }
 
 void light_fused(const FusedArgs& a, hipStream_t s) {

@@ -3,6 +3,7 @@
 // partner runs of an off-diagonal block from dense column starts.
 #include "common.h"
 #include "internal.h"
+#include "lookup.h"
 
 namespace spsyrk {
 namespace {
@@ -151,16 +152,42 @@ struct SlotT<8> {
 };
 constexpr int kCWin = 512;    // rows held in LDS by a compaction workgroup
 
-template <int VB>
+// Staged words of packed count and Jaccard outputs (see FusedArgs::pack_rr):
+// the column and the value, from the count, the row's length and (Jaccard)
+// the partner's length.  The quotients come from double products (exact for
+// words below 2^32 and divisors below 2^17; see run_from).
+struct Unpack {
+    uint32_t rr = 0, r2 = 0;
+    double inv_rr = 0.0, inv_r2 = 0.0;
+};
+template <int PK>
+__device__ inline void unpack_store(const Unpack& u, uint32_t w, int64_t len_i, int64_t p, int32_t* c_ci, void* c_val) {
+    const uint32_t j = uint32_t(fma(double(w), u.inv_rr, 0x1p-18));
+    const uint32_t rem = w - j * u.rr;
+    c_ci[p] = int32_t(j);
+    if constexpr (PK == 1) {
+        static_cast<int32_t*>(c_val)[p] = int32_t(rem);
+    } else {
+        const uint32_t cnt = uint32_t(fma(double(rem), u.inv_r2, 0x1p-18));
+        const uint32_t lenj = rem - cnt * u.r2;
+        static_cast<float*>(c_val)[p] = jaccard(int32_t(cnt), len_i, int64_t(lenj));
+    }
+}
+
+// PK 0: columns and VB-byte values copied; PK 1 (counts) and 2 (Jaccard):
+// packed words unpacked (rp_a: the row pointers of A, for the row lengths)
+template <int VB, int PK = 0>
 __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t staged, const int64_t* __restrict__ ubp,
                                                          const int64_t* __restrict__ trow,
                                                          const int64_t* __restrict__ row_cnt,
                                                          const int64_t* __restrict__ c_rp,
                                                          const int32_t* __restrict__ s_ci, const void* __restrict__ s_val,
-                                                         int32_t* __restrict__ c_ci, void* __restrict__ c_val) {
+                                                         int32_t* __restrict__ c_ci, void* __restrict__ c_val,
+                                                         const int64_t* __restrict__ rp_a, Unpack un) {
     __shared__ int64_t wub[kCWin + 1];  // staging slot of the window's rows
     __shared__ int64_t wend[kCWin];     // end of each row's valid staged entries
     __shared__ int64_t wdel[kCWin];     // final position minus staging slot
+    __shared__ int32_t wlen[PK == 2 ? kCWin : 1];  // (Jaccard) the rows' lengths
     __shared__ uint16_t rowof[kCTile];  // window row of every slot of the tile
     __shared__ uint32_t wt[kWavesPerBlock];
     __shared__ int64_t bounds[2];
@@ -185,6 +212,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
             if (k == nrw) break;
             wend[k] = u + row_cnt[rlo + k];
             wdel[k] = c_rp[rlo + k] - u;
+            if constexpr (PK == 2) wlen[k] = int32_t(rp_a[rlo + k + 1] - rp_a[rlo + k]);
         }
         __syncthreads();
         // every row with staging room in the tile marks its first slot (a row
@@ -243,26 +271,36 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
                 const int x = (b * kBatch + q) * kBlock + threadIdx.x;
                 if (live[q]) {
                     const int64_t p = s0 + x + wdel[rowof[x]];
-                    c_ci[p] = cv[q];
-                    if constexpr (VB != 0) static_cast<V*>(c_val)[p] = vv[q];
+                    if constexpr (PK != 0) {
+                        unpack_store<PK>(un, uint32_t(cv[q]), PK == 2 ? int64_t(wlen[rowof[x]]) : 0, p, c_ci, c_val);
+                    } else {
+                        c_ci[p] = cv[q];
+                        if constexpr (VB != 0) static_cast<V*>(c_val)[p] = vv[q];
+                    }
                 }
             }
         }
         return;
     }
     for (int64_t sl = s0 + threadIdx.x; sl < s1; sl += kBlock) {
-        int64_t end, del;
+        int64_t end, del, len_i = 0;
         if (win_ok) {
             const int k = rowof[sl - s0];
             end = wend[k];
             del = wdel[k];
+            if constexpr (PK == 2) len_i = wlen[k];
         } else {
             const int64_t i = last_leq(ubp, rlo, rhi, sl);
             end = ubp[i] + row_cnt[i];
             del = c_rp[i] - ubp[i];
+            if constexpr (PK == 2) len_i = rp_a[i + 1] - rp_a[i];
         }
         if (sl >= end) continue;
         const int64_t p = sl + del;
+        if constexpr (PK != 0) {
+            unpack_store<PK>(un, uint32_t(s_ci[sl]), len_i, p, c_ci, c_val);
+            continue;
+        }
         c_ci[p] = s_ci[sl];
         if constexpr (VB == 8) static_cast<uint64_t*>(c_val)[p] = static_cast<const uint64_t*>(s_val)[sl];
         if constexpr (VB == 4) static_cast<uint32_t*>(c_val)[p] = static_cast<const uint32_t*>(s_val)[sl];
@@ -422,17 +460,30 @@ size_t compact_tmp_bytes(int64_t staged) { return size_t((staged + kCTile - 1) /
 
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
                   const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
-                  hipStream_t s) {
+                  hipStream_t s, int packed, uint32_t pack_rr, uint32_t pack_r2, const int64_t* rp_a) {
     if (staged <= 0 || m <= 0) return;
     const unsigned nb = unsigned((staged + kCTile - 1) / kCTile);
     int64_t* trow = static_cast<int64_t*>(tmp);
     tile_first_rows(ubp, m, kCTile, trow, s);
-    if (vbytes == 8)
-        compact_kernel<8><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
+    Unpack un;
+    if (packed) {
+        un.rr = pack_rr;
+        un.r2 = pack_r2 ? pack_r2 : 1u;
+        un.inv_rr = 1.0 / double(un.rr);
+        un.inv_r2 = 1.0 / double(un.r2);
+    }
+    if (packed == kCount)
+        compact_kernel<0, 1><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a,
+                                                   un);
+    else if (packed == kJaccard)
+        compact_kernel<0, 2><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a,
+                                                   un);
+    else if (vbytes == 8)
+        compact_kernel<8><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a, un);
     else if (vbytes == 4)
-        compact_kernel<4><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
+        compact_kernel<4><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a, un);
     else
-        compact_kernel<0><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val);
+        compact_kernel<0><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a, un);
 }
 
 }  // namespace spsyrk

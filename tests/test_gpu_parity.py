@@ -525,6 +525,27 @@ def test_packed_run_lengths(dev, semiring, radix, monkeypatch):
     plan.close()
 
 
+@pytest.mark.parametrize("semiring", ["count", "jaccard"])
+@pytest.mark.parametrize("pack", ["1", "0"])
+def test_packed_staging(dev, semiring, pack, monkeypatch):
+    # counts and Jaccard values of the light rows staged as one packed word
+    # (on where it fits) or as column and value (off); a matrix with a
+    # 300-entry row over 100000 rows is too wide for the words and takes the
+    # plain staging either way
+    monkeypatch.setenv("SPSYRK_PACK_STAGING", pack)
+    rng = np.random.default_rng(59)
+    for m, n, per in ((3000, 400, 6), (20000, 1 << 20, 12)):
+        A = _rows_csr(rng, m, n, per)
+        run_lower(A, semiring, dev, f"packed staging {pack} m={m}")
+    # row 0 replaced by 300 columns
+    A = _rows_csr(rng, 100000, 1 << 16, 3)
+    long_cols = np.sort(rng.choice(1 << 16, size=300, replace=False)).astype(np.int32)
+    ci = np.concatenate([long_cols, A.col_idx[A.row_ptr[1]:]])
+    rp = np.concatenate([[0], A.row_ptr[1:] - A.row_ptr[1] + 300]).astype(np.int64)
+    W = CSR(A.nrows, A.ncols, rp, ci, np.ones(len(ci)))
+    run_lower(W, semiring, dev, f"packed staging {pack} with a 300-entry row")
+
+
 def test_plan_of_empty_matrix(dev):
     A = CSR(5, 7, np.zeros(6, np.int64), np.zeros(0, np.int32), np.zeros(0))
     plan, C = sp.lower_plan(upload(A, "f64", dev), "f64")
