@@ -79,7 +79,7 @@ struct WaveLds {
     uint16_t rprod[kFR];      // products of light rows (0 for heavy rows)
     uint16_t rnb[kFR + 1];    // buckets of the row in the current batch
     uint16_t rbb[kFR + 1];    // first bucket of the row in the current batch
-    uint64_t rscale[kFR];     // bucket of column j: (j * rscale) >> 32 spreads [0, range) evenly
+    uint32_t rscale[kFR];     // bucket of column j: (j * rscale) >> 32 spreads [0, range) evenly
     uint32_t ent_start[kFE];
     uint16_t ent_len[kFE];
     alignas(4) uint8_t ent_row[kFE];
@@ -251,13 +251,14 @@ struct Chunk {
             nb = uint32_t(want);
             L.rnb[r] = uint16_t(nb);
             // floor(nb 2^32 / range) rounded down by one more: bucket < nb for
-            // every j < range (the quotient's error is far below one)
+            // every j < range (the quotient's error is far below one); nb <=
+            // range, so the scale fits 32 bits
             uint64_t sc = 0;
             if (range > 0) {
                 sc = uint64_t(ldexp(double(nb), 32) / double(range));
                 sc = sc > 0 ? sc - 1 : 0;
             }
-            L.rscale[r] = sc;
+            L.rscale[r] = uint32_t(sc);
         }
         const uint32_t inc = wave_inclusive_scan(nb);
         if (lane < nrb) L.rbb[ra + lane] = uint16_t(inc - nb);
@@ -337,7 +338,7 @@ struct Chunk {
                 }
                 const int r = int(pb[v]);
                 pj[v] = j;
-                const uint32_t b = L.rbb[r] + uint32_t((uint64_t(j) * L.rscale[r]) >> 32);
+                const uint32_t b = L.rbb[r] + __umulhi(j, L.rscale[r]);
                 pb[v] = b | (uint32_t(r) << 16);
                 add16(L.hist, b);
             }
@@ -401,15 +402,16 @@ struct Chunk {
             const uint32_t lo = b ? L.hist[b - 1] : 0u;
             L.ucnt[b] = merge_two(lo);
         }
+        const bool cols32 = !kVal && a.m_right <= (int64_t(1) << 29);
         for (uint32_t q = lane; q < n4; q += kWave) {
             const uint32_t b = list4[q];
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            L.ucnt[b] = merge_small<kSmall / 2>(lo, hi - lo);
+            L.ucnt[b] = cols32 ? merge_small_cols<kSmall / 2>(lo, hi - lo) : merge_small<kSmall / 2>(lo, hi - lo);
         }
         for (uint32_t q = lane; q < n8; q += kWave) {
             const uint32_t b = list8[q];
             const uint32_t lo = b ? L.hist[b - 1] : 0u, hi = L.hist[b];
-            L.ucnt[b] = merge_small<kSmall>(lo, hi - lo);
+            L.ucnt[b] = cols32 ? merge_small_cols<kSmall>(lo, hi - lo) : merge_small<kSmall>(lo, hi - lo);
         }
         wave_sync();
         // larger buckets, one at a time by the whole wavefront: leaders (first
@@ -606,6 +608,55 @@ struct Chunk {
                     gj = j;
                     gs = uint32_t(ku & 15u);
                     acc = v[u < N ? u : 0];
+                    cnt = 1;
+                }
+            }
+        }
+        return d;
+    }
+
+    // The same for counts and Jaccard values, whose terms need no order: the
+    // keys are (column, slot) in 32 bits (columns below 2^29), sorted with
+    // min/max pairs, and only the columns are loaded.  Any product of a
+    // column may take its tag: the output is the same.
+    template <int N>
+    __device__ uint32_t merge_small_cols(uint32_t lo, uint32_t sz) {
+        static_assert(N <= 8, "slots in three bits");
+        uint32_t k[N];
+#pragma unroll
+        for (int u = 0; u < N; ++u) k[u] = uint32_t(u) < sz ? ((L.s_j[lo + u] << 3) | uint32_t(u)) : 0xffffffffu;
+        auto cs = [&](int x, int y) {
+            const uint32_t a = min(k[x], k[y]), b = max(k[x], k[y]);
+            k[x] = a;
+            k[y] = b;
+        };
+        if constexpr (N == 4) {
+            cs(0, 1); cs(2, 3); cs(0, 2); cs(1, 3); cs(1, 2);
+        } else {
+            static_assert(N == 8, "networks for 4 and 8 products");
+            cs(0, 1); cs(2, 3); cs(4, 5); cs(6, 7);
+            cs(0, 2); cs(1, 3); cs(4, 6); cs(5, 7);
+            cs(1, 2); cs(5, 6); cs(0, 4); cs(3, 7);
+            cs(1, 5); cs(2, 6);
+            cs(1, 4); cs(3, 6);
+            cs(2, 4); cs(3, 5);
+            cs(3, 4);
+        }
+        uint32_t d = 0, gj = k[0] >> 3, gs = k[0] & 7u, cnt = 1;
+#pragma unroll
+        for (int u = 1; u <= N; ++u) {
+            const bool in = uint32_t(u) < sz;
+            const uint32_t ku = k[u < N ? u : 0];
+            const uint32_t j = in ? ku >> 3 : 0u;
+            if (in && j == gj) {
+                ++cnt;
+                L.s_rank[lo + (ku & 7u)] = uint16_t(kNoOut);
+            } else if (uint32_t(u) <= sz) {
+                L.s_rank[lo + gs] = uint16_t((cnt << kKBits) | d);
+                ++d;
+                if (in) {
+                    gj = j;
+                    gs = ku & 7u;
                     cnt = 1;
                 }
             }
