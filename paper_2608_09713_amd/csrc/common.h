@@ -25,6 +25,13 @@ __host__ __device__ inline int bit_width_u64(uint64_t x) { return x ? 64 - __bui
 
 __device__ inline int lane_id() { return __lane_id(); }
 
+// 16 bytes read once: a streamed load that does not displace cached lines
+__device__ inline uint4 nt_load4(const void* p) {
+    typedef unsigned int v4 __attribute__((ext_vector_type(4)));
+    const v4 v = __builtin_nontemporal_load(reinterpret_cast<const v4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ inline uint64_t lanemask_lt() { return (uint64_t(1) << lane_id()) - 1; }
 
 // inclusive scan across a wavefront (64 lanes)

@@ -282,7 +282,9 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     // keys and tile positions stay in registers; the first pass also keeps
     // its row fields (computed from the LDS window, which the exchange
     // buffer overwrites), other passes load rows and values only when they
-    // are exchanged (fewer registers, more workgroups per compute unit)
+    // are exchanged (fewer registers, more workgroups per compute unit).
+    // The input arrays are read once, with streaming loads, so that they do
+    // not push the tile's partly written output lines out of L2.
     uint32_t kr[kRItems], rr[FIRST ? kRItems : 1], loc[kRItems];
     const uint64_t lt = lanemask_lt();
     // record idx of a slab (row r) is entry idx + row_off[r]
@@ -305,7 +307,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 #pragma unroll
         for (int k = 0; k < kRItems; ++k) {
             const int64_t idx = segbase + int64_t(k) * kWave + lane;
-            kr[k] = idx < n ? key_in[idx] : 0u;
+            kr[k] = idx < n ? __builtin_nontemporal_load(key_in + idx) : 0u;
         }
     }
 #pragma unroll
@@ -392,7 +394,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 #pragma unroll
         for (int k = 0; k < kRItems; ++k) {
             const int64_t idx = segbase + int64_t(k) * kWave + lane;
-            rv[k] = idx < n ? row_in[idx] : 0u;
+            rv[k] = idx < n ? __builtin_nontemporal_load(row_in + idx) : 0u;
         }
 #pragma unroll
         for (int k = 0; k < kRItems; ++k)
@@ -420,7 +422,7 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             else if constexpr (SRC == kSrcSlab)
                 vv[k] = vpre[k];
             else
-                vv[k] = idx < n ? val_in[idx] : V(0);
+                vv[k] = idx < n ? __builtin_nontemporal_load(val_in + idx) : V(0);
         }
         __syncthreads();
 #pragma unroll

@@ -78,7 +78,7 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
             const uint4* v4 = reinterpret_cast<const uint4*>(run.r4 + a);
 #pragma unroll
             for (int u = 0; u < kPerT / 4; ++u) {
-                const uint4 q = v4[u];
+                const uint4 q = nt_load4(v4 + u);
                 w[4 * u] = q.x;
                 w[4 * u + 1] = q.y;
                 w[4 * u + 2] = q.z;
