@@ -489,6 +489,56 @@ __global__ __launch_bounds__(kBlock) void group_bounds(const uint32_t* __restric
     }
 }
 
+// Group starts from the passes' scanned histograms, without reading the
+// sorted keys, when the high bits take one or two passes.  With one pass
+// (digit d of w1 bits) group d starts where the pass put the digit's first
+// record.  With two (d1 of w1 bits, then d2), the groups are (d2, d1) in that
+// order, and the records of (d2, d1) come from the second pass's input tiles
+// in order: those before the tile t1 holding the first record of d1 (all of
+// smaller d1), then those of t1 before that record.  So group (d2, d1) starts
+// at the second pass's position of t1's first d2 record, plus the d2 records
+// of t1 before d1 begins.  gstart gets 2^h + 1 entries (the last is n): group
+// g occupies [gstart[g], gstart[g + 1]).
+
+// first1[d] = position of the first record of digit d after the first pass
+// (hist: the first pass's scanned histogram, digit-major)
+__global__ __launch_bounds__(kBlock) void digit_starts(const uint32_t* __restrict__ hist, int64_t ntiles, int ndig,
+                                                       uint32_t* __restrict__ first1, int64_t n) {
+    const int d = threadIdx.x;
+    if (d < ndig) first1[d] = hist[int64_t(d) * ntiles];
+    if (d == 0) first1[ndig] = uint32_t(n);
+}
+
+// one workgroup per d1: the d2 counts of tile t1 before first1[d1] (keys:
+// the first pass's output), then the starts of groups (d2, d1) for every d2
+// (hist: the second pass's scanned histogram)
+__global__ __launch_bounds__(kBlock) void group_starts(const uint32_t* __restrict__ key, int64_t n, int L, int w1,
+                                                       int w2, const uint32_t* __restrict__ first1,
+                                                       const uint32_t* __restrict__ hist, int64_t ntiles,
+                                                       uint32_t* __restrict__ gstart) {
+    __shared__ uint32_t cnt[kDigits];
+    const uint32_t d1 = blockIdx.x;
+    const int nd2 = 1 << w2;
+    cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t f = first1[d1];
+    const int64_t t1 = f / kRTile;
+    const uint32_t m2 = uint32_t(nd2 - 1);
+    if (t1 < ntiles)
+        for (int64_t p = t1 * kRTile + threadIdx.x; p < f; p += kBlock) atomicAdd(&cnt[(key[p] >> (L + w1)) & m2], 1u);
+    __syncthreads();
+    const int d2 = threadIdx.x;
+    if (d2 < nd2) {
+        uint32_t st;
+        if (t1 < ntiles)
+            st = hist[int64_t(d2) * ntiles + t1] + cnt[d2];
+        else  // d1 empty at the end: every group (d2, d1) starts where d2's records end
+            st = d2 + 1 < nd2 ? hist[int64_t(d2 + 1) * ntiles] : uint32_t(n);
+        gstart[(uint32_t(d2) << w1) | d1] = st;
+    }
+    if (d1 == 0 && threadIdx.x == 0) gstart[uint32_t(1) << (w1 + w2)] = uint32_t(n);
+}
+
 // one stable pass of the LDS sort: (dig, idx) of S <= kLCap records by bits
 // [sh, sh + w) of dig, from the *_in arrays to the *_out arrays
 __device__ inline void lds_pass(const uint16_t* dig_in, const uint16_t* idx_in, uint16_t* dig_out, uint16_t* idx_out,
@@ -623,6 +673,7 @@ __global__ __launch_bounds__(kBlock) void local_sort(uint32_t* __restrict__ kx, 
     if (g0 == kNoGroup) return;
     const int64_t b0 = g0;
     const int64_t S = int64_t(gend[blockIdx.x]) - b0;
+    if (S <= 0) return;  // (an empty group, when the starts come from the histograms)
     const uint32_t lmask = (1u << L) - 1u;
     if (S <= kLCap) {
         for (int i = threadIdx.x; i < S; i += kBlock) {
@@ -717,6 +768,7 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__
     if (g0 == kNoGroup) return;
     const int64_t b0 = g0;
     const int64_t S = int64_t(gend[blockIdx.x]) - b0;
+    if (S <= 0) return;  // (an empty group, when the starts come from the histograms)
     const uint32_t lmask = (1u << L) - 1u;
     uint32_t distinct = 0;
     if (S <= kLCap) {
@@ -887,7 +939,9 @@ int local_bits(int64_t n, int nbits) {
 size_t radix_csr_tmp_bytes(int64_t n, int nbits) {
     const int L = local_bits(n, nbits);
     const size_t groups = L ? (size_t(1) << (nbits - L)) : 0;
-    return radix_tmp_bytes(n) + 2 * ((groups * sizeof(uint32_t) + 255) & ~size_t(255));
+    // group starts (groups + 1) and ends, then the first pass's digit starts
+    return radix_tmp_bytes(n) + 2 * (((groups + 1) * sizeof(uint32_t) + 255) & ~size_t(255)) +
+           ((size_t(kDigits + 1) * sizeof(uint32_t) + 255) & ~size_t(255));
 }
 
 size_t radix_tmp_bytes(int64_t n) {
@@ -913,12 +967,28 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     const int passes = digit_plan(nbits - L, width);
     // first pass straight from the CSR arrays (into the b buffers), at least
     // one pass; the row of every tile's first entry comes from a table
+    // with the local sort: the groups' starts (and ends), and the first
+    // pass's digit starts
+    const size_t groups = L ? size_t(1) << (nbits - L) : 0;
+    uint32_t* gstart = nullptr;
+    uint32_t* gend = nullptr;
+    uint32_t* first1 = nullptr;
+    if (L) {
+        const size_t gbytes = ((groups + 1) * sizeof(uint32_t) + 255) & ~size_t(255);
+        gstart = reinterpret_cast<uint32_t*>(static_cast<char*>(tmp) + radix_tmp_bytes(n));
+        gend = gstart + gbytes / sizeof(uint32_t);
+        first1 = gend + gbytes / sizeof(uint32_t);
+    }
+    // group starts from the histograms when the high bits take one or two passes
+    const bool from_hist = L && passes <= 2;
     int cur = 1;
     {
         PhaseTimer passes_timer(SPSYRK_PHASE_COLINDEX_PASSES, s);
         tile_first_rows(rp, m, kRTile, trow, s);
         run_pass<4, kSrcCsr>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
                           (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
+        if (from_hist)
+            digit_starts<<<1, kBlock, 0, s>>>(hist, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n);
         int shift = L + width[0];
         for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
             const uint32_t mask = (1u << width[ps]) - 1u;
@@ -931,18 +1001,21 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
             run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
             cur ^= 1;
         }
+        if (from_hist && passes == 2)
+            group_starts<<<1u << width[0], kBlock, 0, s>>>(key_b, n, L, width[0], width[1], first1, hist, ntiles,
+                                                           gstart);
     }
     if (L == 0) return cur;
     // groups of equal high bits, each sorted by the low L bits into the other buffers
-    const size_t groups = size_t(1) << (nbits - L);
-    const size_t base_bytes = radix_tmp_bytes(n);
-    uint32_t* gstart = reinterpret_cast<uint32_t*>(static_cast<char*>(tmp) + base_bytes);
-    uint32_t* gend = gstart + (((groups * sizeof(uint32_t) + 255) & ~size_t(255)) / sizeof(uint32_t));
-    fill_u32(gstart, int64_t(groups), kNoGroup, s);
     uint32_t* kx = cur ? key_b : key_a;
     uint32_t* rx = cur ? row_b : row_a;
     uint32_t* ex = cur ? ent_b : ent_a;
-    group_bounds<<<unsigned((n + 8 * kBlock - 1) / (8 * kBlock)), kBlock, 0, s>>>(kx, n, L, gstart, gend);
+    if (from_hist) {
+        gend = gstart + 1;  // group g ends where group g + 1 starts
+    } else {
+        fill_u32(gstart, int64_t(groups), kNoGroup, s);
+        group_bounds<<<unsigned((n + 8 * kBlock - 1) / (8 * kBlock)), kBlock, 0, s>>>(kx, n, L, gstart, gend);
+    }
     uint32_t* ky = cur ? key_a : key_b;
     uint32_t* ry = cur ? row_a : row_b;
     uint32_t* ey = cur ? ent_a : ent_b;

@@ -260,6 +260,33 @@ def test_local_sort_path(dev, semiring, monkeypatch):
         compare_full(O, ref, semiring, f"local sort offdiag n={n}")
 
 
+@pytest.mark.parametrize("semiring", ["f64", "jaccard"])
+def test_local_sort_sparse_groups(dev, semiring, monkeypatch):
+    # 22-bit column ids sorted by two high passes (5 + 5 bits) and the local
+    # pass, with the group starts taken from the passes' histograms: the ids
+    # crowd into the lowest 2^20 and the top 2^12 columns, so most groups and
+    # the top digits of both passes are empty
+    monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
+    rng = np.random.default_rng(61)
+    m, n = 20000, 1 << 22
+    c = np.where(rng.random((m, 10)) < 0.9, rng.integers(0, 1 << 20, size=(m, 10)),
+                 rng.integers(n - 4096, n, size=(m, 10)))
+    c.sort(axis=1)
+    keep = np.ones_like(c, dtype=bool)
+    keep[:, 1:] = c[:, 1:] != c[:, :-1]
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(keep.sum(axis=1))
+    ci = c[keep].astype(np.int32)
+    A = CSR(m, n, rp, ci, rng.random(len(ci)) + 0.5)
+    run_lower(A, semiring, dev, "local sort, sparse groups")
+    B = _rows_csr(rng, 3000, n, 5)
+    vdt = VDT[semiring]
+    O = sp.offdiag(upload(B, semiring, dev), upload(A, semiring, dev), semiring)
+    ref = oracle.offdiag(B.with_values(None if vdt is None else B.values.astype(vdt)),
+                         A.with_values(None if vdt is None else A.values.astype(vdt)), semiring)
+    compare_full(O, ref, semiring, "local sort, sparse groups, offdiag")
+
+
 WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
              ("offdiag_f64", 5)]
 
