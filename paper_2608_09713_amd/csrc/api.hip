@@ -248,9 +248,10 @@ DevCsr dev(const spsyrk_csr* A) {
     return d;
 }
 
-void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name) {
+void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name,
+              const FirstHist* fh = nullptr) {
     void* vtmp = ar.get(validate_tmp_bytes(A.nnz));
-    validate_csr(A, upper_forbidden, &ctl->err, vtmp, s);
+    validate_csr(A, upper_forbidden, &ctl->err, vtmp, s, fh);
     check_launch();
     Ctl h = read_ctl(ctl, s);
     ar.release(vtmp);
@@ -270,7 +271,7 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 // vsrc (N entries): the entry of B behind every position of the index.
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
                      const RunTab* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr,
-                     uint32_t* vsrc = nullptr) {
+                     uint32_t* vsrc = nullptr, uint32_t* hist1 = nullptr) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -334,7 +335,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
             HIPCHK(hipMemsetAsync(&ctl->nkept, 0, sizeof(int64_t), s));
         }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
-                                         s, runs_given ? &pk : nullptr);
+                                         s, runs_given ? &pk : nullptr, hist1);
         check_launch();
         ar.release(tmp);
         if (counted) *counted = which < 0 && ccount;
@@ -413,8 +414,10 @@ struct LowerPlan {
 // the partner run of an entry of L in column k is the whole column k of R,
 // read from dense column starts.
 
+// hist1 (optional): the first radix pass's digit counts of the sorted operand
+// (R), counted by its validation
 void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                spsyrk_csr_out* C, LowerPlan* plan = nullptr) {
+                spsyrk_csr_out* C, LowerPlan* plan = nullptr, uint32_t* hist1 = nullptr) {
     const int64_t m = L.m;
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
@@ -436,14 +439,16 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
             HIPCHK(hipMemsetAsync(vsrc, 0, size_t(L.nnz) * sizeof(uint32_t), s));
             plan->vsrc = vsrc;
         }
-        cx = build_index(L, true, sr, ar, ctl, s, &run, true, nullptr, nullptr, vsrc);
+        cx = build_index(L, true, sr, ar, ctl, s, &run, true, nullptr, nullptr, vsrc, hist1);
+        if (hist1) ar.release(hist1);
     } else {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
         // column starts of R: from the counts the local sort writes, else by counting
         uint32_t* cptr = ar.get_t<uint32_t>(R.n + 1);
         HIPCHK(hipMemsetAsync(cptr, 0, size_t(R.n + 1) * sizeof(uint32_t), s));
         bool counted = false;
-        cx = build_index(R, false, sr, ar, ctl, s, nullptr, false, cptr, &counted);
+        cx = build_index(R, false, sr, ar, ctl, s, nullptr, false, cptr, &counted, nullptr, hist1);
+        if (hist1) ar.release(hist1);
         void* ctmp = ar.get(scan_tmp_bytes(R.n + 1));
         if (counted)
             scan_u32(cptr, cptr, R.n + 1, nullptr, ctmp, s);
@@ -633,10 +638,20 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
           LowerPlan* plan = nullptr) {
     Ctl* ctl = ar.get_t<Ctl>(1);
     zero_ctl(ctl, s);
+    // on the single-pass path the validation of the operand whose columns
+    // are sorted (R, which is L in lower mode) also counts the first radix
+    // pass's digits
+    const bool fused = (plan || !two_pass()) && (lower || R.n <= kDenseColumns);
+    FirstHist fh;
+    if (fused && R.nnz > 0 && L.m > 0 && L.nnz > 0) {
+        radix_first_digit(R.nnz, bit_width_u64(R.n > 1 ? uint64_t(R.n - 1) : 0), &fh.shift, &fh.mask);
+        fh.ntiles = (R.nnz + kRadixTile - 1) / kRadixTile;
+        fh.hist = ar.get_t<uint32_t>(size_t(fh.ntiles) * 256);
+    }
     {
         Phase ph(SPSYRK_PHASE_VALIDATE, s);
-        validate(L, false, ar, ctl, s, lower ? "A" : "Ai");
-        if (!lower) validate(R, false, ar, ctl, s, "Aj");
+        validate(L, false, ar, ctl, s, lower ? "A" : "Ai", lower && fh.hist ? &fh : nullptr);
+        if (!lower) validate(R, false, ar, ctl, s, "Aj", fh.hist ? &fh : nullptr);
     }
 
     const int64_t m = L.m;
@@ -659,8 +674,8 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
 
     // single pass over the light rows; off the diagonal when the right
     // operand's column starts fit a dense array (else the two-pass path)
-    if ((plan || !two_pass()) && (lower || R.n <= kDenseColumns)) {
-        syrk_fused(L, R, lower, sr, ar, ctl, s, C, plan);
+    if (fused) {
+        syrk_fused(L, R, lower, sr, ar, ctl, s, C, plan, fh.hist);
         return;
     }
     int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);

@@ -120,10 +120,22 @@ void scan_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total, voi
 void scan_i64(const int64_t* in, int64_t* out, int64_t n, int64_t* total, void* tmp, hipStream_t s);
 
 // ---- validate.hip
+// Records per tile of the radix passes.  The validation of a matrix whose
+// columns are sorted next counts the first pass's digits over the same tiles
+// (hist: digit-major, ntiles x 256 words; digit (col >> shift) & mask), so
+// that the pass does not read the column ids once more for them.
+constexpr int kRadixTile = 3072;
+struct FirstHist {
+    uint32_t* hist = nullptr;
+    int shift = 0;
+    uint32_t mask = 0;
+    int64_t ntiles = 0;
+};
 // ORs ErrBits into *err.  upper_forbidden: also flag entries with col > row.
 // tmp: validate_tmp_bytes(nnz) of scratch.
 size_t validate_tmp_bytes(int64_t nnz);
-void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, void* tmp, hipStream_t s);
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, void* tmp, hipStream_t s,
+                  const FirstHist* fh = nullptr);
 void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 
 // ---- radix.hip
@@ -159,9 +171,14 @@ struct LocalPack {
 };
 // pk non-null: write the column index as above when the local path is taken
 // and return -1 (no sorted copy); otherwise as described.
+// hist1 (optional): the first pass's digit histogram, already counted (by
+// the validation; it is scanned in place)
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
-                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk = nullptr);
+                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk = nullptr, uint32_t* hist1 = nullptr);
+// The digit of radix_sort_csr's first pass over n entries with nbits-bit
+// columns: (col >> shift) & mask.
+void radix_first_digit(int64_t n, int nbits, int* shift, uint32_t* mask);
 int radix_sort(uint32_t* key_a, uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, void* val_a,
                void* val_b, int vbytes, int64_t n, int nbits, void* tmp, hipStream_t s);
 

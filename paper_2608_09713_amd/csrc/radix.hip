@@ -22,6 +22,7 @@ constexpr int kRBits = 8;
 constexpr int kDigits = 1 << kRBits;
 constexpr int kRItems = 12;
 constexpr int kRTile = kBlock * kRItems;  // records per tile
+static_assert(kRTile == kRadixTile, "the validation counts the first pass's digits over the same tiles");
 constexpr int kSeg = kWave * kRItems;     // records per wave
 
 template <int VB>
@@ -891,13 +892,13 @@ template <int VB, int SRC = kSrcArrays, int OUT = kOutArrays>
 void run_pass(const uint32_t* ki, const uint32_t* ri, const void* vi, uint32_t* ko, uint32_t* ro, void* vo, int64_t n,
               int shift, uint32_t mask, uint32_t* hist, void* scan_tmp, hipStream_t s, const int64_t* rp = nullptr,
               int64_t m = 0, const int64_t* trow = nullptr, int rowbits = 0, int lenbits = 0,
-              const SlabIo& sl = SlabIo()) {
+              const SlabIo& sl = SlabIo(), bool counted = false) {
     using V = typename ValT<VB>::T;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     const unsigned grid = unsigned((ntiles + kXcds - 1) / kXcds * kXcds);
     if constexpr (SRC == kSrcSlab)
         radix_hist_slab<<<dim3(grid), dim3(kBlock), 0, s>>>(n, mask, hist, ntiles, rp, m, trow, sl);
-    else
+    else if (!counted)
         radix_hist<<<dim3(grid), dim3(kBlock), 0, s>>>(ki, n, shift, mask, hist, ntiles);
     scan_u32(hist, hist, ntiles * kDigits, nullptr, scan_tmp, s);
     radix_scatter<VB, SRC, OUT><<<dim3(unsigned((ntiles + kXcds - 1) / kXcds * kXcds)), dim3(kBlock), 0, s>>>(
@@ -936,6 +937,14 @@ int local_bits(int64_t n, int nbits) {
     return L >= 1 ? L : 0;
 }
 
+void radix_first_digit(int64_t n, int nbits, int* shift, uint32_t* mask) {
+    const int L = local_bits(n, nbits);
+    int width[8];
+    digit_plan(nbits - L, width);
+    *shift = L;
+    *mask = (1u << width[0]) - 1u;
+}
+
 size_t radix_csr_tmp_bytes(int64_t n, int nbits) {
     const int L = local_bits(n, nbits);
     const size_t groups = L ? (size_t(1) << (nbits - L)) : 0;
@@ -953,7 +962,7 @@ size_t radix_tmp_bytes(int64_t n) {
 
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
-                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk) {
+                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk, uint32_t* hist1) {
     if (n <= 0) return 0;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     uint32_t* hist = static_cast<uint32_t*>(tmp);
@@ -985,10 +994,12 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     {
         PhaseTimer passes_timer(SPSYRK_PHASE_COLINDEX_PASSES, s);
         tile_first_rows(rp, m, kRTile, trow, s);
+        uint32_t* h1 = hist1 ? hist1 : hist;
         run_pass<4, kSrcCsr>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
-                          (1u << width[0]) - 1u, hist, scan_tmp, s, rp, m, trow, rowbits, lenbits);
+                             (1u << width[0]) - 1u, h1, scan_tmp, s, rp, m, trow, rowbits, lenbits, SlabIo(),
+                             hist1 != nullptr);
         if (from_hist)
-            digit_starts<<<1, kBlock, 0, s>>>(hist, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n);
+            digit_starts<<<1, kBlock, 0, s>>>(h1, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n);
         int shift = L + width[0];
         for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
             const uint32_t mask = (1u << width[ps]) - 1u;

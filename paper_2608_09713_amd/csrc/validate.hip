@@ -1,8 +1,9 @@
 // Canonical-CSR checks.
 //
 // One kernel checks both arrays: workgroup b checks the row pointers of rows
-// [b*kTileR, (b+1)*kTileR) and the column ids of entries [b*kTileE,
-// (b+1)*kTileE).  Every thread walks a contiguous stretch of entries row by
+// [b*kTileR, (b+1)*kTileR) and the column ids of entry tile t(b) (tiles of
+// kTileE, the radix passes' tiles, dealt to the XCDs in consecutive runs as
+// the passes deal them), whose digits it can count for the first radix pass.  Every thread walks a contiguous stretch of entries row by
 // row, starting from the row of its first entry (searched in an LDS window of
 // the row pointers).  The rows of the workgroup's first entry and of its end
 // come from a table written by the rows themselves; a row with out-of-range
@@ -16,7 +17,7 @@ namespace spsyrk {
 namespace {
 
 constexpr int kTileR = 4096;  // row pointers per workgroup
-constexpr int kTileE = 4096;  // entries per workgroup
+constexpr int kTileE = kRadixTile;  // entries per workgroup
 constexpr int kWinV = 2048;   // rows held in LDS
 constexpr int kPerE = kTileE / kBlock;
 
@@ -49,12 +50,22 @@ __global__ __launch_bounds__(kBlock) void entry_tile_rows(const int64_t* __restr
 
 __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ rp, const int32_t* __restrict__ ci,
                                                     int64_t m, int64_t n, int64_t nnz, bool upper_forbidden,
-                                                    const int64_t* __restrict__ trow, uint32_t* err) {
+                                                    const int64_t* __restrict__ trow, uint32_t* err, FirstHist fh) {
     __shared__ int64_t win[kWinV + 1];
     __shared__ int64_t bounds[2];
     __shared__ uint32_t bad_s;
+    __shared__ uint32_t cnt[kWavesPerBlock][256];  // (digit counts, with fh.hist)
     if (threadIdx.x == 0) bad_s = 0;
+    if (fh.hist)
+        for (int q = 0; q < kWavesPerBlock; ++q) cnt[q][threadIdx.x] = 0;
     __syncthreads();  // (a workgroup with no entries meets no other barrier before its atomics)
+    // the entry tile: consecutive tiles on one XCD (workgroups go round-robin
+    // over the XCDs), as the radix passes place them
+    const int64_t ntiles_e = (nnz + kTileE - 1) / kTileE;
+    const int64_t per = (ntiles_e + kXcds - 1) / kXcds;
+    // (workgroups past the placed tiles, there for the row pointers only, take none)
+    const int64_t etile = int64_t(blockIdx.x) < per * kXcds ? int64_t(blockIdx.x % kXcds) * per + blockIdx.x / kXcds
+                                                              : ntiles_e;
     uint32_t bad = 0;
     // row pointers: rp[0] == 0, non-decreasing, inside [0, nnz], rp[m] == nnz
     for (int64_t i = int64_t(blockIdx.x) * kTileR + threadIdx.x;
@@ -63,14 +74,14 @@ __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ 
         if (a < 0 || a > nnz || (i == 0 && a != 0) || (i == m && a != nnz)) bad |= kErrRowPtr;
         if (i < m && rp[i + 1] < a) bad |= kErrRowPtr;
     }
-    const int64_t e0 = int64_t(blockIdx.x) * kTileE;
+    const int64_t e0 = etile * kTileE;
     const int64_t e1 = min(nnz, e0 + kTileE);
-    if (e0 < e1) {
+    if (etile < ntiles_e) {
         if (threadIdx.x == 0) {
             // row of e0, and a row at or past the row of e1 - 1 (the row of e1)
-            int64_t lo = trow[blockIdx.x];
+            int64_t lo = trow[etile];
             if (lo < 0 || lo >= m) lo = find_row(rp, 0, m, e0);
-            int64_t hi = e1 < nnz ? trow[blockIdx.x + 1] : -1;
+            int64_t hi = e1 < nnz ? trow[etile + 1] : -1;
             if (hi < lo || hi >= m) hi = find_row(rp, 0, m, e1 - 1);
             bounds[0] = lo;
             bounds[1] = hi;
@@ -125,6 +136,18 @@ __global__ __launch_bounds__(kBlock) void check_csr(const int64_t* __restrict__ 
                 prev = c;
                 first = false;
             }
+            if (fh.hist) {
+#pragma unroll
+                for (int u = 0; u < kPerE; ++u)
+                    if (ea + u < eb) atomicAdd(&cnt[threadIdx.x / kWave][(uint32_t(cc[u]) >> fh.shift) & fh.mask], 1u);
+            }
+        }
+        if (fh.hist) {
+            __syncthreads();
+            uint32_t t = 0;
+#pragma unroll
+            for (int q = 0; q < kWavesPerBlock; ++q) t += cnt[q][threadIdx.x];
+            fh.hist[int64_t(threadIdx.x) * fh.ntiles + etile] = t;
         }
     }
     if (bad) atomicOr(&bad_s, bad);
@@ -149,17 +172,20 @@ void fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
 
 size_t validate_tmp_bytes(int64_t nnz) { return size_t((nnz + kTileE - 1) / kTileE + 1) * sizeof(int64_t); }
 
-void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, void* tmp, hipStream_t s) {
+void validate_csr(const DevCsr& A, bool upper_forbidden, uint32_t* err, void* tmp, hipStream_t s,
+                  const FirstHist* fh) {
     const int64_t rb = (A.m + 1 + kTileR - 1) / kTileR;
     const int64_t eb = (A.nnz + kTileE - 1) / kTileE;
-    const int64_t nb = rb > eb ? rb : eb;
+    const int64_t ebx = (eb + kXcds - 1) / kXcds * kXcds;  // every entry tile placed (see check_csr)
+    const int64_t nb = rb > ebx ? rb : ebx;
+    const FirstHist h = fh && eb > 0 ? *fh : FirstHist();
     int64_t* trow = static_cast<int64_t*>(tmp);
     if (eb > 0) {
         fill_u32(reinterpret_cast<uint32_t*>(trow), 2 * eb, 0xffffffffu, s);
         if (A.m > 0)
             entry_tile_rows<<<unsigned((A.m + kBlock - 1) / kBlock), kBlock, 0, s>>>(A.rp, A.m, A.nnz, eb, trow);
     }
-    check_csr<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.ci, A.m, A.n, A.nnz, upper_forbidden, trow, err);
+    check_csr<<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(A.rp, A.ci, A.m, A.n, A.nnz, upper_forbidden, trow, err, h);
 }
 
 }  // namespace spsyrk
