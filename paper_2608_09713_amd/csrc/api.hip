@@ -331,8 +331,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
             pk.drop_last = drop_last;
             pk.kept = &ctl->nkept;
             pk.ccount = ccount;
-            pk.vsrc = vsrc;
-            HIPCHK(hipMemsetAsync(&ctl->nkept, 0, sizeof(int64_t), s));
+            pk.vsrc = vsrc;  // (ctl->nkept is zero: ctl is zeroed at the call's start)
         }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
                                          s, runs_given ? &pk : nullptr, hist1);
@@ -461,7 +460,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     }
     int32_t* heavy_rows = ar.get_t<int32_t>(m);
     int64_t* ub = ar.get_t<int64_t>(m + 1);
-    HIPCHK(hipMemsetAsync(ub + m, 0, sizeof(int64_t), s));
+    // (classify_rows sets ub[m] = 0, and the light kernel row_cnt[m] = 0)
     void* ptmp = ar.get(row_products_tmp_bytes(L.nnz));
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
@@ -529,7 +528,6 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     int32_t* s_ci = ar.get_t<int32_t>(light_cap > 0 ? light_cap : 1);
     void* s_val = ar.get(size_t(pack_rr || light_cap <= 0 ? 1 : light_cap) * vbo);
     int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
-    HIPCHK(hipMemsetAsync(row_cnt + m, 0, sizeof(int64_t), s));
 
     FusedArgs fa;
     fa.m = m;
@@ -549,8 +547,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     const int64_t nlight = m - nheavy;
     fa.rows_per_chunk = rows_per_chunk(nlight > 0 ? double(light_cap) / double(nlight) : 1.0);
     fa.nchunks = (m + fa.rows_per_chunk - 1) / fa.rows_per_chunk;
-    HIPCHK(hipMemsetAsync(&ctl->chunk_counter, 0, sizeof(ctl->chunk_counter), s));
-    fa.chunk_counter = &ctl->chunk_counter;
+    fa.chunk_counter = &ctl->chunk_counter;  // (zero: ctl is zeroed at the call's start)
     fa.c_ci = s_ci;
     fa.c_val = s_val;
     fa.pack_rr = pack_rr;

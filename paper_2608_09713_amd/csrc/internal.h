@@ -254,11 +254,12 @@ struct FusedArgs {
     uint32_t pack_rr = 0, pack_r2 = 0;
 };
 // light rows: columns and values at the staging slots, exact lengths in row_cnt
-// (heavy rows: their length from heavy_nnz)
+// (heavy rows: their length from heavy_nnz; row_cnt[m] = 0)
 void light_fused(const FusedArgs& a, hipStream_t s);
 // heavy rows (over the limits) into a list; light capacity sum(prod + diagonal) and
 // the sum of prod over all rows into the two counters
-// and ub[i] = products + diagonal for light rows, 0 for heavy rows; maxlen
+// and ub[i] = products + diagonal for light rows, 0 for heavy rows (and ub[m]
+// = 0); maxlen
 // (optional, zeroed): the largest row length
 void classify_rows(const int64_t* rp, const unsigned long long* prod, int64_t m, bool lower, int32_t* heavy_rows,
                    int32_t* heavy_count, unsigned long long* light_cap, unsigned long long* prod_sum, int64_t* ub,

@@ -865,6 +865,7 @@ void fused_kernel(FusedArgs a) {
     // seen), at least one, so the runs shrink towards the end.  The next
     // chunk is taken and its head loaded while the current chunk runs.
     const int lane = lane_id();
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.row_cnt[a.m] = 0;  // (the scan's last input)
     const int64_t nwaves = int64_t(gridDim.x) * kWavesF;
     const bool dealt = a.nchunks < kDealtBelow * nwaves;
     int64_t seen = 0, rend = 0;
@@ -943,6 +944,7 @@ __global__ __launch_bounds__(kBlock) void classify_kernel(const int64_t* __restr
         }
         ub[i] = u;
     }
+    if (blockIdx.x == 0 && threadIdx.x == 0) ub[m] = 0;  // (the scan's last input)
     cap = wave_reduce_sum(cap);
     ps = wave_reduce_sum(ps);
     ml = wave_reduce_max(ml);

@@ -65,9 +65,12 @@ struct SrTraits<kJaccard> {
     static constexpr bool kHasItem = true;
 };
 
-// J = c / (|a| + |b| - c), one correctly rounded float division
+// J = c / (|a| + |b| - c), one correctly rounded float division.  Row
+// lengths are below 2^31, so the denominator fits 32 unsigned bits, whose
+// conversion rounds as the 64-bit one would.
 __device__ inline float jaccard(int32_t c, int64_t len_a, int64_t len_b) {
-    return __fdiv_rn(float(c), float(len_a + len_b - c));
+    const uint32_t d = uint32_t(len_a) + uint32_t(len_b) - uint32_t(c);
+    return __fdiv_rn(float(c), float(d));
 }
 
 }  // namespace spsyrk
