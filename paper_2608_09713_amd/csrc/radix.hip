@@ -224,12 +224,24 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
+    const int64_t base = tile * kRTile;
+    const int64_t segbase = base + int64_t(w) * kSeg;
+    // the keys (the column ids in the first pass) are read once, with
+    // streaming loads so that they do not push the tile's partly written
+    // output lines out of L2, and first, so that they arrive while the tile
+    // is set up (a slab's keys are read through its rows, further below)
+    uint32_t kr[kRItems];
+    if constexpr (SRC != kSrcSlab) {
+#pragma unroll
+        for (int k = 0; k < kRItems; ++k) {
+            const int64_t idx = segbase + int64_t(k) * kWave + lane;
+            kr[k] = idx < n ? __builtin_nontemporal_load(key_in + idx) : 0u;
+        }
+    }
 #pragma unroll
     for (int q = 0; q < kWavesPerBlock; ++q) wcnt[q][threadIdx.x] = 0;
     __syncthreads();
 
-    const int64_t base = tile * kRTile;
-    const int64_t segbase = base + int64_t(w) * kSeg;
     int64_t rlo = 0, rhi = 0;
     bool rstaged = false;
     if constexpr (FIRST) {
@@ -283,10 +295,9 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     // keys and tile positions stay in registers; the first pass also keeps
     // its row fields (computed from the LDS window, which the exchange
     // buffer overwrites), other passes load rows and values only when they
-    // are exchanged (fewer registers, more workgroups per compute unit).
-    // The input arrays are read once, with streaming loads, so that they do
-    // not push the tile's partly written output lines out of L2.
-    uint32_t kr[kRItems], rr[FIRST ? kRItems : 1], loc[kRItems];
+    // are exchanged (fewer registers, more workgroups per compute unit), also
+    // with streaming loads
+    uint32_t rr[FIRST ? kRItems : 1], loc[kRItems];
     const uint64_t lt = lanemask_lt();
     // record idx of a slab (row r) is entry idx + row_off[r]
     auto slab_entry = [&](int64_t idx, int64_t r) -> int64_t { return idx + sl.row_off[r]; };
@@ -303,12 +314,6 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
             const int64_t e = slab_entry(idx, r);
             kr[k] = idx < n ? uint32_t(int64_t(sl.ci[e]) - sl.c0) : 0u;
             if constexpr (VB != 0) vpre[k] = idx < n ? static_cast<const V*>(sl.val)[e] : V(0);
-        }
-    } else {
-#pragma unroll
-        for (int k = 0; k < kRItems; ++k) {
-            const int64_t idx = segbase + int64_t(k) * kWave + lane;
-            kr[k] = idx < n ? __builtin_nontemporal_load(key_in + idx) : 0u;
         }
     }
 #pragma unroll

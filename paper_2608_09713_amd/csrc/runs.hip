@@ -49,6 +49,25 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
     __shared__ int64_t bounds[2];
     const int64_t e0 = int64_t(blockIdx.x) * kTileP;
     const int64_t e1 = min(nnz, e0 + kTileP);
+    const int64_t a = e0 + int64_t(threadIdx.x) * kPerT;
+    const int64_t b = min(e1, a + kPerT);
+    // the stretch's run words, loaded first so that they arrive while the
+    // tile's rows are set up (16-byte loads for a whole aligned stretch)
+    uint32_t w[kPerT];
+    if (b - a == kPerT && (reinterpret_cast<uintptr_t>(run.r4 + a) & 15) == 0) {
+        const uint4* v4 = reinterpret_cast<const uint4*>(run.r4 + a);
+#pragma unroll
+        for (int u = 0; u < kPerT / 4; ++u) {
+            const uint4 q = nt_load4(v4 + u);
+            w[4 * u] = q.x;
+            w[4 * u + 1] = q.y;
+            w[4 * u + 2] = q.z;
+            w[4 * u + 3] = q.w;
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < kPerT; ++u) w[u] = a + u < b ? run.r4[a + u] : 0u;
+    }
     if (threadIdx.x == 0) {
         // rows of the tile's first entry and (at most one row past the tile)
         // of its end, from the tile table; the last tile searches for its end
@@ -69,25 +88,7 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
             }
         }
     __syncthreads();
-    const int64_t a = e0 + int64_t(threadIdx.x) * kPerT;
-    const int64_t b = min(e1, a + kPerT);
     if (a < b) {
-        // run lengths of the stretch (16-byte loads for a whole aligned stretch)
-        uint32_t w[kPerT];
-        if (b - a == kPerT && (reinterpret_cast<uintptr_t>(run.r4 + a) & 15) == 0) {
-            const uint4* v4 = reinterpret_cast<const uint4*>(run.r4 + a);
-#pragma unroll
-            for (int u = 0; u < kPerT / 4; ++u) {
-                const uint4 q = nt_load4(v4 + u);
-                w[4 * u] = q.x;
-                w[4 * u + 1] = q.y;
-                w[4 * u + 2] = q.z;
-                w[4 * u + 3] = q.w;
-            }
-        } else {
-#pragma unroll
-            for (int u = 0; u < kPerT; ++u) w[u] = a + u < b ? run.r4[a + u] : 0u;
-        }
         uint32_t rl[kPerT];
 #pragma unroll
         for (int u = 0; u < kPerT; ++u) {
@@ -193,6 +194,14 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     __shared__ int64_t bounds[2];
     const int64_t s0 = int64_t(blockIdx.x) * kCTile;
     const int64_t s1 = min(staged, s0 + kCTile);
+    // a whole tile's staged columns (or packed words) are loaded first, so
+    // that they arrive while the tile's rows are set up
+    constexpr int kPerC = kCTile / kBlock;
+    const bool whole = s1 - s0 == kCTile;
+    int32_t pre[kPerC];
+    if (whole)
+#pragma unroll
+        for (int i = 0; i < kPerC; ++i) pre[i] = s_ci[s0 + i * kBlock + threadIdx.x];
     if (threadIdx.x == 0) {
         // rows of the tile's first slot and (at most one row past the tile)
         // of its end, from the tile table; the last tile searches for its end
@@ -246,7 +255,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
         }
     }
     __syncthreads();
-    if (win_ok && s1 - s0 == kCTile) {
+    if (win_ok && whole) {
         // a whole tile: the slots of a thread in batches of kBatch, every
         // batch's loads in flight together before its stores
         using V = typename SlotT<VB>::T;
@@ -261,8 +270,8 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
             for (int q = 0; q < kBatch; ++q) {
                 const int x = (b * kBatch + q) * kBlock + threadIdx.x;
                 live[q] = s0 + x < wend[rowof[x]];
+                cv[q] = pre[b * kBatch + q];
                 if (live[q]) {
-                    cv[q] = s_ci[s0 + x];
                     if constexpr (VB != 0) vv[q] = static_cast<const V*>(s_val)[s0 + x];
                 }
             }
