@@ -248,13 +248,15 @@ DevCsr dev(const spsyrk_csr* A) {
     return d;
 }
 
+// keep_rows (optional, validate_tmp_bytes(nnz)): the validation's table of
+// tile rows is left there for later kernels (tiles of kRadixTile entries)
 void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name,
-              const FirstHist* fh = nullptr) {
-    void* vtmp = ar.get(validate_tmp_bytes(A.nnz));
+              const FirstHist* fh = nullptr, void* keep_rows = nullptr) {
+    void* vtmp = keep_rows ? keep_rows : ar.get(validate_tmp_bytes(A.nnz));
     validate_csr(A, upper_forbidden, &ctl->err, vtmp, s, fh);
     check_launch();
     Ctl h = read_ctl(ctl, s);
-    ar.release(vtmp);
+    if (!keep_rows) ar.release(vtmp);
     if (h.err) {
         set_detail("%s is not canonical CSR (flags 0x%x:%s%s%s%s)", name, h.err, (h.err & kErrRowPtr) ? " row_ptr" : "",
                    (h.err & kErrColRange) ? " column-range" : "", (h.err & kErrColOrder) ? " column-order" : "",
@@ -271,7 +273,7 @@ void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStr
 // vsrc (N entries): the entry of B behind every position of the index.
 ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
                      const RunTab* run = nullptr, bool need_dir = true, uint32_t* ccount = nullptr, bool* counted = nullptr,
-                     uint32_t* vsrc = nullptr, uint32_t* hist1 = nullptr) {
+                     uint32_t* vsrc = nullptr, uint32_t* hist1 = nullptr, const int64_t* trow1 = nullptr) {
     ColIndex cx;
     cx.n = B.n;
     cx.m = B.m;
@@ -334,7 +336,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
             pk.vsrc = vsrc;  // (ctl->nkept is zero: ctl is zeroed at the call's start)
         }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
-                                         s, runs_given ? &pk : nullptr, hist1);
+                                         s, runs_given ? &pk : nullptr, hist1, trow1);
         check_launch();
         ar.release(tmp);
         if (counted) *counted = which < 0 && ccount;
@@ -414,9 +416,11 @@ struct LowerPlan {
 // read from dense column starts.
 
 // hist1 (optional): the first radix pass's digit counts of the sorted operand
-// (R), counted by its validation
+// (R), counted by its validation; vrows (optional, lower mode): the
+// validation's table of tile rows of A
 void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                spsyrk_csr_out* C, LowerPlan* plan = nullptr, uint32_t* hist1 = nullptr) {
+                spsyrk_csr_out* C, LowerPlan* plan = nullptr, uint32_t* hist1 = nullptr,
+                const int64_t* vrows = nullptr) {
     const int64_t m = L.m;
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
@@ -438,7 +442,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
             HIPCHK(hipMemsetAsync(vsrc, 0, size_t(L.nnz) * sizeof(uint32_t), s));
             plan->vsrc = vsrc;
         }
-        cx = build_index(L, true, sr, ar, ctl, s, &run, true, nullptr, nullptr, vsrc, hist1);
+        cx = build_index(L, true, sr, ar, ctl, s, &run, true, nullptr, nullptr, vsrc, hist1, vrows);
         if (hist1) ar.release(hist1);
     } else {
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
@@ -464,7 +468,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     void* ptmp = ar.get(row_products_tmp_bytes(L.nnz));
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
-        row_products(L.rp, m, L.nnz, run, ptmp, prod, s);
+        row_products(L.rp, m, L.nnz, run, ptmp, prod, s, vrows);
         classify_rows(L.rp, prod, m, lower, heavy_rows, &ctl->heavy_count, &ctl->light_cap, &ctl->products, ub, s,
                       &ctl->maxlen);
     }
@@ -645,9 +649,12 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
         fh.ntiles = (R.nnz + kRadixTile - 1) / kRadixTile;
         fh.hist = ar.get_t<uint32_t>(size_t(fh.ntiles) * 256);
     }
+    // in lower mode the validation's table of tile rows of A serves the
+    // first radix pass and the row products too
+    void* vrows = fused && lower && L.nnz > 0 ? ar.get(validate_tmp_bytes(L.nnz)) : nullptr;
     {
         Phase ph(SPSYRK_PHASE_VALIDATE, s);
-        validate(L, false, ar, ctl, s, lower ? "A" : "Ai", lower && fh.hist ? &fh : nullptr);
+        validate(L, false, ar, ctl, s, lower ? "A" : "Ai", lower && fh.hist ? &fh : nullptr, vrows);
         if (!lower) validate(R, false, ar, ctl, s, "Aj", fh.hist ? &fh : nullptr);
     }
 
@@ -672,7 +679,7 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     // single pass over the light rows; off the diagonal when the right
     // operand's column starts fit a dense array (else the two-pass path)
     if (fused) {
-        syrk_fused(L, R, lower, sr, ar, ctl, s, C, plan, fh.hist);
+        syrk_fused(L, R, lower, sr, ar, ctl, s, C, plan, fh.hist, static_cast<const int64_t*>(vrows));
         return;
     }
     int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);

@@ -173,9 +173,12 @@ struct LocalPack {
 // and return -1 (no sorted copy); otherwise as described.
 // hist1 (optional): the first pass's digit histogram, already counted (by
 // the validation; it is scanned in place)
+// trow1 (optional): the row of every tile start (tiles of kRadixTile
+// entries; -1 where left out), as the validation writes it
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
-                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk = nullptr, uint32_t* hist1 = nullptr);
+                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk = nullptr, uint32_t* hist1 = nullptr,
+                   const int64_t* trow1 = nullptr);
 // The digit of radix_sort_csr's first pass over n entries with nbits-bit
 // columns: (col >> shift) & mask.
 void radix_first_digit(int64_t n, int nbits, int* shift, uint32_t* mask);
@@ -282,8 +285,10 @@ void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, const Ru
 // must start zeroed).
 // tmp: row_products_tmp_bytes(nnz) of scratch
 size_t row_products_tmp_bytes(int64_t nnz);
+// trow1 (optional): the row of every tile start of kRadixTile entries (-1
+// where left out), as the validation writes it
 void row_products(const int64_t* rp, int64_t m, int64_t nnz, const RunTab& run, void* tmp, unsigned long long* prod,
-                  hipStream_t s);
+                  hipStream_t s, const int64_t* trow1 = nullptr);
 // Copy the staged rows to their final places: the element at staging slot
 // ubp[i] + x (x < row_cnt[i]) goes to c_rp[i] + x.  ubp is non-decreasing
 // with ubp[m] = staged; rows with no staging room (heavy rows) copy nothing.

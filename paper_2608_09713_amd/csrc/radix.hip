@@ -247,10 +247,15 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
     if constexpr (FIRST) {
         if (threadIdx.x == 0) {
             // rows of the tile's first entry and (at most one row past the
-            // tile) of its end, from the tile table; the last tile searches
-            const int64_t lo = trow[tile];
+            // tile) of its end, from the tile table; the last tile searches,
+            // and so does a tile the table leaves out (-1: a table written
+            // by the validation skips the tiles deep inside very long rows)
+            int64_t lo = trow[tile];
+            if (lo < 0) lo = last_leq_i64(rp, 0, m, base);
+            int64_t hi = base + kRTile < n ? trow[tile + 1] : -1;
+            if (hi < 0) hi = last_leq_i64(rp, lo, m, base + kRTile < n ? base + kRTile : n - 1);
             rbounds[0] = lo;
-            rbounds[1] = base + kRTile < n ? trow[tile + 1] : last_leq_i64(rp, lo, m, n - 1);
+            rbounds[1] = hi;
         }
         __syncthreads();
         rlo = rbounds[0];
@@ -967,7 +972,8 @@ size_t radix_tmp_bytes(int64_t n) {
 
 int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int rowbits, int lenbits, uint32_t* key_a,
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
-                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk, uint32_t* hist1) {
+                   int nbits, void* tmp, hipStream_t s, const LocalPack* pk, uint32_t* hist1,
+                   const int64_t* trow1) {
     if (n <= 0) return 0;
     const int64_t ntiles = (n + kRTile - 1) / kRTile;
     uint32_t* hist = static_cast<uint32_t*>(tmp);
@@ -998,11 +1004,11 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     int cur = 1;
     {
         PhaseTimer passes_timer(SPSYRK_PHASE_COLINDEX_PASSES, s);
-        tile_first_rows(rp, m, kRTile, trow, s);
+        if (!trow1) tile_first_rows(rp, m, kRTile, trow, s);
         uint32_t* h1 = hist1 ? hist1 : hist;
         run_pass<4, kSrcCsr>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
-                             (1u << width[0]) - 1u, h1, scan_tmp, s, rp, m, trow, rowbits, lenbits, SlabIo(),
-                             hist1 != nullptr);
+                             (1u << width[0]) - 1u, h1, scan_tmp, s, rp, m, trow1 ? trow1 : trow, rowbits, lenbits,
+                             SlabIo(), hist1 != nullptr);
         if (from_hist)
             digit_starts<<<1, kBlock, 0, s>>>(h1, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n);
         int shift = L + width[0];

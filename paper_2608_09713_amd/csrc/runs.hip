@@ -25,8 +25,9 @@ __device__ inline int64_t last_leq(const int64_t* a, int64_t lo, int64_t hi, int
 // lengths row by row.  A row that lies inside the stretch is stored at once;
 // the partial sums of rows cut by a stretch's ends meet in LDS, and a row cut
 // by the tile's ends is added atomically (prod starts at zero).
-constexpr int kPerT = 8;
+constexpr int kPerT = 12;
 constexpr int kTileP = kBlock * kPerT;
+static_assert(kTileP == kRadixTile, "the row products take the validation's tile table");
 constexpr int kWinP = 1024;
 
 // trow[t] = the row holding position t * T, for every tile start t * T <
@@ -70,10 +71,14 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
     }
     if (threadIdx.x == 0) {
         // rows of the tile's first entry and (at most one row past the tile)
-        // of its end, from the tile table; the last tile searches for its end
-        const int64_t lo = trow[blockIdx.x];
+        // of its end, from the tile table; the last tile searches for its
+        // end, and so does a tile the table leaves out (-1)
+        int64_t lo = trow[blockIdx.x];
+        if (lo < 0) lo = last_leq(rp, 0, m, e0);
+        int64_t hi = e1 < nnz ? trow[blockIdx.x + 1] : -1;
+        if (hi < 0) hi = last_leq(rp, lo, m, e1 < nnz ? e1 : e1 - 1);
         bounds[0] = lo;
-        bounds[1] = e1 < nnz ? trow[blockIdx.x + 1] : last_leq(rp, lo, m, e1 - 1);
+        bounds[1] = hi;
     }
     __syncthreads();
     const int64_t rlo = bounds[0], rhi = bounds[1];
@@ -457,11 +462,14 @@ void offdiag_runs(const int32_t* ci, int64_t nnz, const uint32_t* cptr, const Ru
 size_t row_products_tmp_bytes(int64_t nnz) { return size_t((nnz + kTileP - 1) / kTileP + 1) * sizeof(int64_t); }
 
 void row_products(const int64_t* rp, int64_t m, int64_t nnz, const RunTab& run, void* tmp, unsigned long long* prod,
-                  hipStream_t s) {
+                  hipStream_t s, const int64_t* trow1) {
     if (nnz <= 0 || m <= 0) return;
     const unsigned nb = unsigned((nnz + kTileP - 1) / kTileP);
     int64_t* trow = static_cast<int64_t*>(tmp);
-    tile_first_rows(rp, m, kTileP, trow, s);
+    if (trow1)
+        trow = const_cast<int64_t*>(trow1);
+    else
+        tile_first_rows(rp, m, kTileP, trow, s);
     rowprod_kernel<<<nb, kBlock, 0, s>>>(rp, m, nnz, run, trow, prod);
 }
 

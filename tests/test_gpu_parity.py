@@ -287,6 +287,22 @@ def test_local_sort_sparse_groups(dev, semiring, monkeypatch):
     compare_full(O, ref, semiring, "local sort, sparse groups, offdiag")
 
 
+@pytest.mark.parametrize("semiring", ["f64", "count"])
+def test_row_longer_than_the_tile_table(dev, semiring):
+    # a row of 250000 entries spans 82 tiles of 3072 entries; the
+    # validation's table of tile rows (which the column sort and the row
+    # products reuse) leaves the tiles deep inside it out, and those tiles
+    # find their rows by search
+    rng = np.random.default_rng(63)
+    n = 1 << 20
+    long_cols = np.sort(rng.choice(n, size=250000, replace=False)).astype(np.int32)
+    B = _rows_csr(rng, 3000, n, 5)
+    ci = np.concatenate([B.col_idx[: B.row_ptr[1500]], long_cols, B.col_idx[B.row_ptr[1500]:]])
+    rp = np.concatenate([B.row_ptr[:1501], B.row_ptr[1500:] + 250000]).astype(np.int64)
+    A = CSR(3001, n, rp, ci, rng.random(len(ci)) + 0.5)
+    run_lower(A, semiring, dev, "a row longer than 64 tiles")
+
+
 WORKLOADS = [("tiny_uniform_f64", 0), ("kmer_i32", 5), ("rmat20_f32", 7), ("jaccard_large", 7),
              ("offdiag_f64", 5)]
 
