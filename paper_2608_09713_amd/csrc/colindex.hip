@@ -142,23 +142,23 @@ __global__ __launch_bounds__(kBlock) void pack(const uint32_t* __restrict__ scol
             if (last) continue;
             q = p - cols_before;
         }
-        if (vsrc) vsrc[q] = sent[p];
+        if (vsrc) nt_store(sent[p], vsrc + q);
         if constexpr (JAC) {
             if (!val) {
-                key[q] = field;  // (no directory) the row and its saturated length
+                nt_store(field, key + q);  // (no directory) the row and its saturated length
             } else {
-                key[q] = ((col & gmask) << rowbits) | row;
+                nt_store(((col & gmask) << rowbits) | row, key + q);
                 const uint32_t lf = lenbits > 0 ? field >> rowbits : lmax;
-                static_cast<int32_t*>(val)[q] = lf < lmax ? int32_t(lf) : int32_t(rp_b[row + 1] - rp_b[row]);
+                nt_store(lf < lmax ? int32_t(lf) : int32_t(rp_b[row + 1] - rp_b[row]), static_cast<int32_t*>(val) + q);
             }
         } else {
-            key[q] = ((col & gmask) << rowbits) | row;
+            nt_store(((col & gmask) << rowbits) | row, key + q);
         }
         if constexpr (JAC) {
         } else if constexpr (VB == 8) {
-            static_cast<uint64_t*>(val)[q] = static_cast<const uint64_t*>(vals_b)[sent[p]];
+            nt_store(static_cast<const uint64_t*>(vals_b)[sent[p]], static_cast<uint64_t*>(val) + q);
         } else if constexpr (VB == 4) {
-            static_cast<uint32_t*>(val)[q] = static_cast<const uint32_t*>(vals_b)[sent[p]];
+            nt_store(static_cast<const uint32_t*>(vals_b)[sent[p]], static_cast<uint32_t*>(val) + q);
         }
     }
 }

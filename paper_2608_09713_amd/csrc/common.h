@@ -32,6 +32,13 @@ __device__ inline uint4 nt_load4(const void* p) {
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// a write not read again by this kernel: a streamed store, which leaves the
+// caches to the kernel's scattered writes (those merge there into fuller lines)
+template <typename T>
+__device__ inline void nt_store(T v, T* p) {
+    __builtin_nontemporal_store(v, p);
+}
+
 __device__ inline uint64_t lanemask_lt() { return (uint64_t(1) << lane_id()) - 1; }
 
 // inclusive scan across a wavefront (64 lanes)

@@ -9,6 +9,7 @@
 // its contiguous kSeg-record segment with ballot-based digit matching and
 // per-wave LDS counters, the tile is reordered through LDS, then written out
 // so that consecutive threads store consecutive addresses of a digit's run.
+#include <algorithm>
 #include <cstdlib>
 #include <type_traits>
 
@@ -460,14 +461,17 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 
 constexpr int kLBits = 12;       // low bits sorted locally
 constexpr int kLCap = 4096;      // records of a group sorted in LDS
+constexpr int kLCapS = 2048;     // the same in the packed sort's first launch (half the LDS and registers)
 constexpr int kLDig = 6;         // bits per local digit
 constexpr uint32_t kNoGroup = 0xffffffffu;
 
 // first and end position of every group of equal high bits (groups that do
-// not occur keep kNoGroup)
+// not occur keep kNoGroup); big, if given, is emptied as in digit_starts
 // (eight keys per thread, read with 16-byte loads when the keys are aligned)
 __global__ __launch_bounds__(kBlock) void group_bounds(const uint32_t* __restrict__ key, int64_t n, int L,
-                                                       uint32_t* __restrict__ gstart, uint32_t* __restrict__ gend) {
+                                                       uint32_t* __restrict__ gstart, uint32_t* __restrict__ gend,
+                                                       uint32_t* __restrict__ big) {
+    if (big && blockIdx.x == 0 && threadIdx.x == 0) big[0] = 0;
     const int64_t p0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * 8;
     if (p0 >= n) return;
     uint32_t k[9];  // key p0 - 1 (or none), then keys p0 .. p0 + 7
@@ -513,11 +517,16 @@ __global__ __launch_bounds__(kBlock) void group_bounds(const uint32_t* __restric
 
 // first1[d] = position of the first record of digit d after the first pass
 // (hist: the first pass's scanned histogram, digit-major)
+// (big, if given: the packed sort's list of large groups, emptied here)
 __global__ __launch_bounds__(kBlock) void digit_starts(const uint32_t* __restrict__ hist, int64_t ntiles, int ndig,
-                                                       uint32_t* __restrict__ first1, int64_t n) {
+                                                       uint32_t* __restrict__ first1, int64_t n,
+                                                       uint32_t* __restrict__ big) {
     const int d = threadIdx.x;
     if (d < ndig) first1[d] = hist[int64_t(d) * ntiles];
-    if (d == 0) first1[ndig] = uint32_t(n);
+    if (d == 0) {
+        first1[ndig] = uint32_t(n);
+        if (big) big[0] = 0;
+    }
 }
 
 // one workgroup per d1: the d2 counts of tile t1 before first1[d1] (keys:
@@ -552,9 +561,10 @@ __global__ __launch_bounds__(kBlock) void group_starts(const uint32_t* __restric
 
 // one stable pass of the LDS sort: (dig, idx) of S <= kLCap records by bits
 // [sh, sh + w) of dig, from the *_in arrays to the *_out arrays
+template <int CAP>
 __device__ inline void lds_pass(const uint16_t* dig_in, const uint16_t* idx_in, uint16_t* dig_out, uint16_t* idx_out,
                                 int S, int sh, int w, uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
-    constexpr int kCh = kLCap / kWavesPerBlock / kWave;  // chunks of a wave's segment
+    constexpr int kCh = CAP / kWavesPerBlock / kWave;  // chunks of a wave's segment
     const int wv = threadIdx.x / kWave;
     const int lane = lane_id();
     const uint32_t m = (1u << w) - 1u;
@@ -694,7 +704,7 @@ __global__ __launch_bounds__(kBlock) void local_sort(uint32_t* __restrict__ kx, 
         __syncthreads();
         int cur = 0;
         for (int sh = 0; sh < L; sh += kLDig) {
-            lds_pass(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], int(S), sh, min(kLDig, L - sh), wcnt, wt);
+            lds_pass<kLCap>(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], int(S), sh, min(kLDig, L - sh), wcnt, wt);
             cur ^= 1;
         }
         for (int j = threadIdx.x; j < S; j += kBlock) {
@@ -744,158 +754,215 @@ template <int VB, bool JAC>
 __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t field, uint32_t ent, int64_t cstart,
                                   typename ValT<VB>::T v, bool last, uint32_t col) {
     if (pk.ccount && last) pk.ccount[col] = uint32_t(pos - cstart + 1);
-    if (pk.vsrc) pk.vsrc[pos] = ent;
+    if (pk.vsrc) nt_store(ent, pk.vsrc + pos);
     const uint32_t rowmask = pk.rowbits >= 32 ? 0xffffffffu : ((1u << pk.rowbits) - 1u);
     const uint32_t row = field & rowmask;
     if constexpr (JAC) {
         if (!pk.val) {
-            pk.key[pos] = field;  // the row and its saturated length
+            nt_store(field, pk.key + pos);  // the row and its saturated length
         } else {
-            pk.key[pos] = row;
+            nt_store(row, pk.key + pos);
             const uint32_t lmax = pk.lenbits > 0 ? (1u << pk.lenbits) - 1u : 0u;
             const uint32_t lf = pk.lenbits > 0 ? field >> pk.rowbits : lmax;
-            static_cast<int32_t*>(pk.val)[pos] = lf < lmax ? int32_t(lf) : int32_t(pk.rp_b[row + 1] - pk.rp_b[row]);
+            nt_store(lf < lmax ? int32_t(lf) : int32_t(pk.rp_b[row + 1] - pk.rp_b[row]),
+                     static_cast<int32_t*>(pk.val) + pos);
         }
     } else {
-        pk.key[pos] = row;
-        if constexpr (VB != 0) static_cast<typename ValT<VB>::T*>(pk.val)[pos] = v;
+        nt_store(row, pk.key + pos);
+        if constexpr (VB != 0) nt_store(v, static_cast<typename ValT<VB>::T*>(pk.val) + pos);
     }
     if (pk.run && pos > cstart) set_run(pk.run, ent, uint32_t(cstart), uint32_t(pos));
 }
 
+// The LDS path of local_sort_pack: the group of S <= CAP records at b0.
+// Returns the number of distinct columns (the same in every thread).
+template <int VB, bool JAC, int CAP>
+__device__ inline uint32_t pack_group_lds(const uint32_t* __restrict__ kx, const uint32_t* __restrict__ rx,
+                                          const uint32_t* __restrict__ ex, int64_t b0, int S, int L,
+                                          const LocalPack& pk, uint16_t (*dg)[CAP], uint16_t (*ix)[CAP],
+                                          uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
+    static_assert(CAP % kBlock == 0 && CAP <= 65536, "whole rounds of the workgroup; 16-bit indices");
+    constexpr int kPer = CAP / kBlock;
+    const uint32_t lmask = (1u << L) - 1u;
+    // every global access of the group is issued as one batch per thread
+    // (kPer records, unrolled), so a workgroup waits on memory a few times
+    // rather than once per record stride
+    {
+        uint32_t kv[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = threadIdx.x + k * kBlock;
+            kv[k] = i < S ? kx[b0 + i] : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = threadIdx.x + k * kBlock;
+            if (i < S) {
+                dg[0][i] = uint16_t(kv[k] & lmask);
+                ix[0][i] = uint16_t(i);
+            }
+        }
+    }
+    __syncthreads();
+    int cur = 0;
+    for (int sh = 0; sh < L; sh += kLDig) {
+        lds_pass<CAP>(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], S, sh, min(kLDig, L - sh), wcnt, wt);
+        cur ^= 1;
+    }
+    // row fields and entry indices in sorted order (in flight during the scan below)
+    uint32_t rv[kPer], ev[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int j = threadIdx.x + k * kBlock;
+        if (j < S) {
+            const int64_t src = b0 + ix[cur][j];
+            rv[k] = rx[src];
+            ev[k] = ex[src];
+        }
+    }
+    // first position of every entry's column: the positions where the low
+    // bits change, then a max-scan (kPer consecutive positions per thread)
+    uint16_t* cs = dg[cur ^ 1];
+    uint32_t distinct;
+    {
+        const int j0 = threadIdx.x * kPer;
+        uint32_t run[kPer];
+        uint32_t mx = 0, nst = 0;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int j = j0 + k;
+            if (j < S && (j == 0 || dg[cur][j - 1] != dg[cur][j])) {
+                mx = uint32_t(j);
+                ++nst;
+            }
+            run[k] = mx;
+        }
+        uint32_t all;
+        const uint32_t before = block_exclusive_max(mx, wt, &all);
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int j = j0 + k;
+            if (j < S) cs[j] = uint16_t(max(run[k], before));
+        }
+        (void)block_exclusive_scan(nst, wt, &distinct);
+    }
+    __syncthreads();
+    typename ValT<VB>::T vv[kPer];
+#pragma unroll
+    for (int k = 0; k < kPer; ++k)
+        if (threadIdx.x + k * kBlock < S) vv[k] = entry_value<VB>(pk, ev[k]);
+    const uint32_t hi = kx[b0] & ~lmask;  // the group's high column bits
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int j = threadIdx.x + k * kBlock;
+        if (j < S) {
+            const uint32_t lo = dg[cur][j];
+            const bool last = j == S - 1 || dg[cur][j + 1] != lo;
+            emit_entry<VB, JAC>(pk, b0 + j, rv[k], ev[k], b0 + cs[j], vv[k], last, hi | lo);
+        }
+    }
+    return distinct;
+}
+
+// The same for a group of any size, by passes over global memory (x -> y ->
+// x ..., ending in y), then the output a tile at a time.
 template <int VB, bool JAC>
-__global__ __launch_bounds__(kBlock) void local_sort_pack(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
-                                                          uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
-                                                          uint32_t* __restrict__ ry, uint32_t* __restrict__ ey,
+__device__ inline uint32_t pack_group_global(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
+                                             uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
+                                             uint32_t* __restrict__ ry, uint32_t* __restrict__ ey, int64_t b0,
+                                             int64_t S, int L, const LocalPack& pk, uint32_t* base,
+                                             uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
+    int npass = 0;
+    for (int sh = 0; sh < L; sh += kLDig) {
+        const bool to_y = (npass & 1) == 0;
+        group_pass(to_y ? kx : ky, to_y ? rx : ry, to_y ? ex : ey, to_y ? ky : kx, to_y ? ry : rx, to_y ? ey : ex, b0,
+                   S, sh, min(kLDig, L - sh), base, wcnt, wt);
+        ++npass;
+    }
+    const uint32_t* ks = (npass & 1) ? ky : kx;
+    const uint32_t* rs = (npass & 1) ? ry : rx;
+    const uint32_t* es = (npass & 1) ? ey : ex;
+    // the column start carried over from tile to tile
+    uint32_t carry = 0, distinct = 0;
+    for (int64_t t0 = 0; t0 < S; t0 += kBlock) {
+        const int64_t j = t0 + threadIdx.x;
+        const bool st = j < S && (j == 0 || ks[b0 + j - 1] != ks[b0 + j]);
+        const uint32_t v = st ? uint32_t(j) : 0u;
+        uint32_t all;
+        const uint32_t cstart = max(max(block_exclusive_max(v, wt, &all), v), carry);
+        uint32_t tot;
+        (void)block_exclusive_scan(st ? 1u : 0u, wt, &tot);
+        distinct += tot;
+        if (j < S) {
+            const uint32_t col = ks[b0 + j];
+            const bool last = j == S - 1 || ks[b0 + j + 1] != col;
+            emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart, entry_value<VB>(pk, es[b0 + j]), last,
+                                col);
+        }
+        carry = max(carry, all);
+    }
+    return distinct;
+}
+
+__device__ inline void add_kept(const LocalPack& pk, int64_t S, uint32_t distinct) {
+    if (threadIdx.x == 0 && pk.kept)
+        atomicAdd(reinterpret_cast<unsigned long long*>(pk.kept),
+                  (unsigned long long)(pk.drop_last ? S - int64_t(distinct) : S));
+}
+
+// Group v = blockIdx.x, of S <= kLCapS records: sorted in LDS and written
+// as the column index.  A larger group is appended to the list big (big[0]
+// its length, zero on entry; then the group numbers) for
+// local_sort_pack_big.  The small capacity halves the LDS and the registers
+// of a workgroup, which doubles the workgroups a compute unit holds.
+template <int VB, bool JAC>
+__global__ __launch_bounds__(kBlock) void local_sort_pack(const uint32_t* __restrict__ kx,
+                                                          const uint32_t* __restrict__ rx,
+                                                          const uint32_t* __restrict__ ex,
                                                           const uint32_t* __restrict__ gstart,
-                                                          const uint32_t* __restrict__ gend, int L, LocalPack pk) {
-    __shared__ uint16_t dg[2][kLCap];
-    __shared__ uint16_t ix[2][kLCap];
+                                                          const uint32_t* __restrict__ gend, int L, LocalPack pk,
+                                                          uint32_t* __restrict__ big) {
+    __shared__ uint16_t dg[2][kLCapS];
+    __shared__ uint16_t ix[2][kLCapS];
     __shared__ uint32_t wcnt[kWavesPerBlock][1 << kLDig];
-    __shared__ uint32_t base[1 << kLDig];
     __shared__ uint32_t wt[kWavesPerBlock];
-    constexpr int kPer = kLCap / kBlock;
     const uint32_t g0 = gstart[blockIdx.x];
     if (g0 == kNoGroup) return;
     const int64_t b0 = g0;
     const int64_t S = int64_t(gend[blockIdx.x]) - b0;
     if (S <= 0) return;  // (an empty group, when the starts come from the histograms)
-    const uint32_t lmask = (1u << L) - 1u;
-    uint32_t distinct = 0;
-    if (S <= kLCap) {
-        // every global access of the group is issued as one batch per thread
-        // (kPer records, unrolled), so a workgroup waits on memory a few
-        // times rather than once per record stride
-        {
-            uint32_t kv[kPer];
-#pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                const int i = threadIdx.x + k * kBlock;
-                kv[k] = i < S ? kx[b0 + i] : 0u;
-            }
-#pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                const int i = threadIdx.x + k * kBlock;
-                if (i < S) {
-                    dg[0][i] = uint16_t(kv[k] & lmask);
-                    ix[0][i] = uint16_t(i);
-                }
-            }
-        }
-        __syncthreads();
-        int cur = 0;
-        for (int sh = 0; sh < L; sh += kLDig) {
-            lds_pass(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], int(S), sh, min(kLDig, L - sh), wcnt, wt);
-            cur ^= 1;
-        }
-        // row fields and entry indices in sorted order (in flight during the scan below)
-        uint32_t rv[kPer], ev[kPer];
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int j = threadIdx.x + k * kBlock;
-            if (j < S) {
-                const int64_t src = b0 + ix[cur][j];
-                rv[k] = rx[src];
-                ev[k] = ex[src];
-            }
-        }
-        // first position of every entry's column: the positions where the low
-        // bits change, then a max-scan (kPer consecutive positions per thread)
-        uint16_t* cs = dg[cur ^ 1];
-        {
-            const int j0 = threadIdx.x * kPer;
-            uint32_t run[kPer];
-            uint32_t mx = 0, nst = 0;
-#pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                const int j = j0 + k;
-                if (j < S && (j == 0 || dg[cur][j - 1] != dg[cur][j])) {
-                    mx = uint32_t(j);
-                    ++nst;
-                }
-                run[k] = mx;
-            }
-            uint32_t all;
-            const uint32_t before = block_exclusive_max(mx, wt, &all);
-#pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                const int j = j0 + k;
-                if (j < S) cs[j] = uint16_t(max(run[k], before));
-            }
-            uint32_t tot;
-            (void)block_exclusive_scan(nst, wt, &tot);
-            distinct = tot;
-        }
-        __syncthreads();
-        typename ValT<VB>::T vv[kPer];
-#pragma unroll
-        for (int k = 0; k < kPer; ++k)
-            if (threadIdx.x + k * kBlock < S) vv[k] = entry_value<VB>(pk, ev[k]);
-        const uint32_t hi = kx[b0] & ~lmask;  // the group's high column bits
-#pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int j = threadIdx.x + k * kBlock;
-            if (j < S) {
-                const uint32_t lo = dg[cur][j];
-                const bool last = j == S - 1 || dg[cur][j + 1] != lo;
-                emit_entry<VB, JAC>(pk, b0 + j, rv[k], ev[k], b0 + cs[j], vv[k], last, hi | lo);
-            }
-        }
-    } else {
-        // a large group: passes over global memory, x -> y -> x ..., ending in y
-        int npass = 0;
-        for (int sh = 0; sh < L; sh += kLDig) {
-            const bool to_y = (npass & 1) == 0;
-            group_pass(to_y ? kx : ky, to_y ? rx : ry, to_y ? ex : ey, to_y ? ky : kx, to_y ? ry : rx,
-                       to_y ? ey : ex, b0, S, sh, min(kLDig, L - sh), base, wcnt, wt);
-            ++npass;
-        }
-        const uint32_t* ks = (npass & 1) ? ky : kx;
-        const uint32_t* rs = (npass & 1) ? ry : rx;
-        const uint32_t* es = (npass & 1) ? ey : ex;
-        // the same output, a tile at a time, the column start carried over
-        uint32_t carry = 0;
-        for (int64_t t0 = 0; t0 < S; t0 += kBlock) {
-            const int64_t j = t0 + threadIdx.x;
-            const bool st = j < S && (j == 0 || ks[b0 + j - 1] != ks[b0 + j]);
-            const uint32_t v = st ? uint32_t(j) : 0u;
-            uint32_t all;
-            const uint32_t cstart = max(max(block_exclusive_max(v, wt, &all), v), carry);
-            uint32_t tot;
-            (void)block_exclusive_scan(st ? 1u : 0u, wt, &tot);
-            distinct += tot;
-            if (j < S) {
-                const uint32_t col = ks[b0 + j];
-                const bool last = j == S - 1 || ks[b0 + j + 1] != col;
-                emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart, entry_value<VB>(pk, es[b0 + j]),
-                                    last, col);
-            }
-            carry = max(carry, all);
-        }
+    if (S > kLCapS) {
+        if (threadIdx.x == 0) big[1 + atomicAdd(big, 1u)] = blockIdx.x;
+        return;
     }
-    if (threadIdx.x == 0 && pk.kept)
-        atomicAdd(reinterpret_cast<unsigned long long*>(pk.kept),
-                  (unsigned long long)(pk.drop_last ? S - int64_t(distinct) : S));
+    add_kept(pk, S, pack_group_lds<VB, JAC, kLCapS>(kx, rx, ex, b0, int(S), L, pk, dg, ix, wcnt, wt));
+}
+
+// The groups local_sort_pack listed, shared out over the grid: in LDS up to
+// kLCap records, over global memory (x and y in turn) beyond.
+template <int VB, bool JAC>
+__global__ __launch_bounds__(kBlock) void local_sort_pack_big(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
+                                                              uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
+                                                              uint32_t* __restrict__ ry, uint32_t* __restrict__ ey,
+                                                              const uint32_t* __restrict__ gstart,
+                                                              const uint32_t* __restrict__ gend, int L,
+                                                              LocalPack pk, const uint32_t* __restrict__ big) {
+    __shared__ uint16_t dg[2][kLCap];
+    __shared__ uint16_t ix[2][kLCap];
+    __shared__ uint32_t wcnt[kWavesPerBlock][1 << kLDig];
+    __shared__ uint32_t base[1 << kLDig];
+    __shared__ uint32_t wt[kWavesPerBlock];
+    const uint32_t nbig = big[0];
+    for (uint32_t q = blockIdx.x; q < nbig; q += gridDim.x) {
+        const uint32_t g = big[1 + q];
+        const int64_t b0 = gstart[g];
+        const int64_t S = int64_t(gend[g]) - b0;
+        const uint32_t distinct =
+            S <= kLCap ? pack_group_lds<VB, JAC, kLCap>(kx, rx, ex, b0, int(S), L, pk, dg, ix, wcnt, wt)
+                       : pack_group_global<VB, JAC>(kx, rx, ex, ky, ry, ey, b0, S, L, pk, base, wcnt, wt);
+        add_kept(pk, S, distinct);
+        __syncthreads();  // (the shared arrays serve the next group)
+    }
 }
 
 template <int VB, int SRC = kSrcArrays, int OUT = kOutArrays>
@@ -958,8 +1025,9 @@ void radix_first_digit(int64_t n, int nbits, int* shift, uint32_t* mask) {
 size_t radix_csr_tmp_bytes(int64_t n, int nbits) {
     const int L = local_bits(n, nbits);
     const size_t groups = L ? (size_t(1) << (nbits - L)) : 0;
-    // group starts (groups + 1) and ends, then the first pass's digit starts
-    return radix_tmp_bytes(n) + 2 * (((groups + 1) * sizeof(uint32_t) + 255) & ~size_t(255)) +
+    // group starts (groups + 1), ends and the list of large groups (length,
+    // then up to groups entries), then the first pass's digit starts
+    return radix_tmp_bytes(n) + 3 * (((groups + 1) * sizeof(uint32_t) + 255) & ~size_t(255)) +
            ((size_t(kDigits + 1) * sizeof(uint32_t) + 255) & ~size_t(255));
 }
 
@@ -993,11 +1061,13 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     uint32_t* gstart = nullptr;
     uint32_t* gend = nullptr;
     uint32_t* first1 = nullptr;
+    uint32_t* big = nullptr;
     if (L) {
         const size_t gbytes = ((groups + 1) * sizeof(uint32_t) + 255) & ~size_t(255);
         gstart = reinterpret_cast<uint32_t*>(static_cast<char*>(tmp) + radix_tmp_bytes(n));
         gend = gstart + gbytes / sizeof(uint32_t);
-        first1 = gend + gbytes / sizeof(uint32_t);
+        big = gend + gbytes / sizeof(uint32_t);
+        first1 = big + gbytes / sizeof(uint32_t);
     }
     // group starts from the histograms when the high bits take one or two passes
     const bool from_hist = L && passes <= 2;
@@ -1010,7 +1080,7 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
                              (1u << width[0]) - 1u, h1, scan_tmp, s, rp, m, trow1 ? trow1 : trow, rowbits, lenbits,
                              SlabIo(), hist1 != nullptr);
         if (from_hist)
-            digit_starts<<<1, kBlock, 0, s>>>(h1, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n);
+            digit_starts<<<1, kBlock, 0, s>>>(h1, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n, big);
         int shift = L + width[0];
         for (int ps = 1; ps < passes; shift += width[ps], ++ps) {
             const uint32_t mask = (1u << width[ps]) - 1u;
@@ -1036,22 +1106,30 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
         gend = gstart + 1;  // group g ends where group g + 1 starts
     } else {
         fill_u32(gstart, int64_t(groups), kNoGroup, s);
-        group_bounds<<<unsigned((n + 8 * kBlock - 1) / (8 * kBlock)), kBlock, 0, s>>>(kx, n, L, gstart, gend);
+        group_bounds<<<unsigned((n + 8 * kBlock - 1) / (8 * kBlock)), kBlock, 0, s>>>(kx, n, L, gstart, gend, big);
     }
     uint32_t* ky = cur ? key_a : key_b;
     uint32_t* ry = cur ? row_a : row_b;
     uint32_t* ey = cur ? ent_a : ent_b;
     if (pk) {
         const unsigned g = unsigned(groups);
+        // the large groups (listed by the first launch) on a grid of at most
+        // four workgroups per compute unit
+        const unsigned gb = unsigned(std::min<size_t>(groups, 1024));
         PhaseTimer pack_timer(SPSYRK_PHASE_COLINDEX_PACK, s);
-        if (pk->jac)
-            local_sort_pack<0, true><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
-        else if (pk->vbytes == 8)
-            local_sort_pack<8, false><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
-        else if (pk->vbytes == 4)
-            local_sort_pack<4, false><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
-        else
-            local_sort_pack<0, false><<<g, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk);
+        if (pk->jac) {
+            local_sort_pack<0, true><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<0, true><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+        } else if (pk->vbytes == 8) {
+            local_sort_pack<8, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<8, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+        } else if (pk->vbytes == 4) {
+            local_sort_pack<4, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<4, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+        } else {
+            local_sort_pack<0, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<0, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+        }
         return -1;
     }
     local_sort<<<unsigned(groups), kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L);

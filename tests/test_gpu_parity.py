@@ -287,6 +287,32 @@ def test_local_sort_sparse_groups(dev, semiring, monkeypatch):
     compare_full(O, ref, semiring, "local sort, sparse groups, offdiag")
 
 
+@pytest.mark.parametrize("semiring", ["f64", "jaccard"])
+def test_local_sort_large_groups(dev, semiring, monkeypatch):
+    # groups past the first launch's LDS capacity (2048 records): 2^22
+    # columns and about 6.3 M entries give 4096 groups of 1024 columns
+    # (high bits max(22 - 12, bit width of 6.3 M / 2048) = 12); the entries
+    # fill only the even groups, so each of those 2048 holds about 3100
+    # records (more than the 1024 workgroups of the second launch, which
+    # sorts them in LDS), and groups 2 and 6 take about 63000 each (sorted
+    # over global memory)
+    monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
+    rng = np.random.default_rng(65)
+    m, per, n = 630000, 10, 1 << 22
+    g = 2 * rng.integers(0, 2048, size=(m, per))
+    g = np.where(rng.random((m, per)) < 0.02, rng.choice([2, 6], size=(m, per)), g)
+    c = np.sort(g * 1024 + rng.integers(0, 1024, size=(m, per)), axis=1)
+    keep = np.ones_like(c, dtype=bool)
+    keep[:, 1:] = c[:, 1:] != c[:, :-1]
+    rp = np.zeros(m + 1, dtype=np.int64)
+    rp[1:] = np.cumsum(keep.sum(axis=1))
+    ci = c[keep].astype(np.int32)
+    A = CSR(m, n, rp, ci, rng.random(len(ci)) + 0.5)
+    counts = np.bincount(ci >> 10, minlength=4096)
+    assert counts[1::2].sum() == 0 and (counts[0::2] > 2048).all() and counts[2] > 4096 and counts[6] > 4096
+    run_lower(A, semiring, dev, "local sort, groups past the LDS capacity")
+
+
 @pytest.mark.parametrize("semiring", ["f64", "count"])
 def test_row_longer_than_the_tile_table(dev, semiring):
     # a row of 250000 entries spans 82 tiles of 3072 entries; the
