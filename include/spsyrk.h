@@ -50,10 +50,10 @@
  *     spsyrk_lower, spsyrk_lower_plan: 3 -- the validation word of A, the
  *       row classes (heavy rows, staging size), the output size;
  *       spsyrk_lower_plan waits once more for the plan's copies;
- *     spsyrk_offdiag: 4 -- one validation word per operand, the row classes,
- *       the output size (A_j with 2^28 columns or more: validation words,
- *       the index size, the output size); spsyrk_offdiag_half: one more,
- *       for the split row;
+ *     spsyrk_offdiag: 3 -- the validation words of both operands (one
+ *       read), the row classes, the output size (A_j with 2^28 columns or
+ *       more: validation words, the index size, the output size);
+ *       spsyrk_offdiag_half: one more, for the split row;
  *     spsyrk_mirror: 3 -- the validation word, the strict-lower count and
  *       the end of the call (when nnz(C_L) exceeds 2^31 the strict lower
  *       part is transposed in column slabs: one column histogram per
@@ -127,8 +127,12 @@ typedef struct spsyrk_csr {
 } spsyrk_csr;
 
 /* Output CSR (device arrays allocated by the call through the allocator).
- * col_idx and values hold exactly nnz entries (one allocated entry when nnz
- * is 0, so that the pointers are never null on success). */
+ * col_idx and values hold nnz entries (one allocated entry when nnz is 0, so
+ * that the pointers are never null on success).  Their allocations can be
+ * larger: when spsyrk_lower, spsyrk_lower_plan or spsyrk_offdiag have no
+ * heavy rows they are sized by the rows' staging bound (product counts, plus
+ * the diagonal in lower mode, at most 16 GiB of columns and values), which
+ * exceeds nnz by the number of products that merged. */
 typedef struct spsyrk_csr_out {
     int64_t nrows;
     int64_t ncols;

@@ -82,21 +82,25 @@ class Arena {
     bool touched() const { return touched_; }
     ~Arena() { release_all(); }
 
+    // Allocate count blocks of the given size ahead of the gets that will
+    // take them (any later get of that size takes one), so that those gets
+    // cost the host nothing at a point where the device waits on it.
+    void reserve(size_t bytes, int count = 1) {
+        bytes = round(bytes);
+        for (int i = 0; i < count; ++i) reserved_.push_back({raw(bytes), bytes});
+    }
+
     void* get(size_t bytes, bool output = false) {
         touched_ = true;
-        if (bytes == 0) bytes = 256;
-        bytes = (bytes + 255) & ~size_t(255);
-        void* p = nullptr;
-        if (al_ && al_->alloc) {
-            p = al_->alloc(al_->ctx, bytes);
-        } else {
-            hipError_t e = hipMallocAsync(&p, bytes, s_);
-            if (e != hipSuccess) p = nullptr;
-        }
-        if (!p) {
-            set_detail("allocation of %zu bytes failed", bytes);
-            throw Fail{SPSYRK_ERR_OOM};
-        }
+        bytes = round(bytes);
+        for (auto& r : reserved_)
+            if (r.p && r.bytes == bytes) {
+                void* p = r.p;
+                r.p = nullptr;
+                (output ? outputs_ : work_).push_back(p);
+                return p;
+            }
+        void* p = raw(bytes);
         (output ? outputs_ : work_).push_back(p);
         return p;
     }
@@ -134,11 +138,33 @@ class Arena {
             if (p) free_one(p);
         for (void* p : outputs_)
             if (p) free_one(p);
+        for (auto& r : reserved_)
+            if (r.p) free_one(r.p);
         work_.clear();
         outputs_.clear();
+        reserved_.clear();
     }
 
    private:
+    struct Reserved {
+        void* p;
+        size_t bytes;
+    };
+    static size_t round(size_t bytes) { return bytes == 0 ? 256 : (bytes + 255) & ~size_t(255); }
+    void* raw(size_t bytes) {
+        void* p = nullptr;
+        if (al_ && al_->alloc) {
+            p = al_->alloc(al_->ctx, bytes);
+        } else {
+            hipError_t e = hipMallocAsync(&p, bytes, s_);
+            if (e != hipSuccess) p = nullptr;
+        }
+        if (!p) {
+            set_detail("allocation of %zu bytes failed", bytes);
+            throw Fail{SPSYRK_ERR_OOM};
+        }
+        return p;
+    }
     void free_one(void* p) {
         if (al_ && al_->free)
             al_->free(al_->ctx, p);
@@ -148,6 +174,7 @@ class Arena {
     const spsyrk_allocator* al_;
     hipStream_t s_;
     std::vector<void*> work_, outputs_;
+    std::vector<Reserved> reserved_;
     bool touched_ = false;
 };
 
@@ -170,7 +197,7 @@ struct Ctl {
     int64_t nkept;
     int64_t total2;
     int32_t queue;
-    int32_t pad0;
+    uint32_t err2;  // validation flags of the second operand (off the diagonal)
     unsigned long long light_cap;
     unsigned long long heavy_sums[2];  // entries of A and output entries of the heavy rows
     unsigned long long chunk_counter;
@@ -180,23 +207,45 @@ struct Ctl {
 
 struct HostCtl {
     Ctl* h = nullptr;
+    hipEvent_t ev = nullptr;  // recorded after the copy into h
     HostCtl() {
         if (hipHostMalloc(reinterpret_cast<void**>(&h), sizeof(Ctl), hipHostMallocDefault) != hipSuccess) h = nullptr;
+        if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) ev = nullptr;
     }
     ~HostCtl() {
         if (h) (void)hipHostFree(h);
+        if (ev) (void)hipEventDestroy(ev);
     }
 };
 
-Ctl read_ctl(const Ctl* d, hipStream_t s) {
+HostCtl& host_ctl() {
     thread_local HostCtl pin;
-    if (!pin.h) {
+    if (!pin.h || !pin.ev) {
         set_detail("pinned host buffer unavailable");
         throw Fail{SPSYRK_ERR_HIP};
     }
+    return pin;
+}
+
+// Enqueue the copy of the control block to the host; ctl_wait returns it
+// once the copy is done, while the work enqueued after the copy may still
+// run.  (One copy in flight per thread: every ctl_fetch is followed by its
+// ctl_wait before the next.)
+void ctl_fetch(const Ctl* d, hipStream_t s) {
+    HostCtl& pin = host_ctl();
     HIPCHK(hipMemcpyAsync(pin.h, d, sizeof(Ctl), hipMemcpyDeviceToHost, s));
-    HIPCHK(hipStreamSynchronize(s));
+    HIPCHK(hipEventRecord(pin.ev, s));
+}
+
+Ctl ctl_wait() {
+    HostCtl& pin = host_ctl();
+    HIPCHK(hipEventSynchronize(pin.ev));
     return *pin.h;
+}
+
+Ctl read_ctl(const Ctl* d, hipStream_t s) {
+    ctl_fetch(d, s);
+    return ctl_wait();
 }
 
 void check_launch() {
@@ -248,21 +297,31 @@ DevCsr dev(const spsyrk_csr* A) {
     return d;
 }
 
+// Enqueue the validation of A, its flags into *err (zeroed beforehand);
+// check_valid takes them from a later read of the control block.
 // keep_rows (optional, validate_tmp_bytes(nnz)): the validation's table of
 // tile rows is left there for later kernels (tiles of kRadixTile entries)
-void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name,
-              const FirstHist* fh = nullptr, void* keep_rows = nullptr) {
+void validate_enqueue(const DevCsr& A, bool upper_forbidden, Arena& ar, uint32_t* err, hipStream_t s,
+                      const FirstHist* fh = nullptr, void* keep_rows = nullptr) {
     void* vtmp = keep_rows ? keep_rows : ar.get(validate_tmp_bytes(A.nnz));
-    validate_csr(A, upper_forbidden, &ctl->err, vtmp, s, fh);
+    validate_csr(A, upper_forbidden, err, vtmp, s, fh);
     check_launch();
-    Ctl h = read_ctl(ctl, s);
-    if (!keep_rows) ar.release(vtmp);
-    if (h.err) {
-        set_detail("%s is not canonical CSR (flags 0x%x:%s%s%s%s)", name, h.err, (h.err & kErrRowPtr) ? " row_ptr" : "",
-                   (h.err & kErrColRange) ? " column-range" : "", (h.err & kErrColOrder) ? " column-order" : "",
-                   (h.err & kErrUpper) ? " above-diagonal" : "");
+    if (!keep_rows) ar.release(vtmp);  // (stream-ordered: later work may reuse it)
+}
+
+void check_valid(uint32_t err, const char* name) {
+    if (err) {
+        set_detail("%s is not canonical CSR (flags 0x%x:%s%s%s%s)", name, err, (err & kErrRowPtr) ? " row_ptr" : "",
+                   (err & kErrColRange) ? " column-range" : "", (err & kErrColOrder) ? " column-order" : "",
+                   (err & kErrUpper) ? " above-diagonal" : "");
         throw Fail{SPSYRK_ERR_NOT_CANONICAL};
     }
+}
+
+void validate(const DevCsr& A, bool upper_forbidden, Arena& ar, Ctl* ctl, hipStream_t s, const char* name,
+              const FirstHist* fh = nullptr, void* keep_rows = nullptr) {
+    validate_enqueue(A, upper_forbidden, ar, &ctl->err, s, fh, keep_rows);
+    check_valid(read_ctl(ctl, s).err, name);
 }
 
 // Build the column index of B (sorted by column, packed keys, directory).
@@ -407,6 +466,24 @@ struct LowerPlan {
     int64_t nchunks = 0;
 };
 
+// The buffers build_index takes for the column index of B in lower mode
+// (every partner run given), allocated ahead with Arena::reserve: the keys,
+// two buffers each of sorted keys, rows and entries, the values (none for
+// Jaccard, whose keys carry the lengths) and the sort's workspace.
+void reserve_index(const DevCsr& B, int sr, Arena& ar) {
+    const int64_t N = B.nnz;
+    if (N <= 0) return;
+    const int nbits = bit_width_u64(B.n > 1 ? uint64_t(B.n - 1) : 0);
+    ar.reserve(size_t(N) * sizeof(uint32_t), 7);
+    const int vb = csc_value_bytes(sr);
+    if (vb && sr != kJaccard) ar.reserve(size_t(N) * size_t(vb));
+    ar.reserve(radix_csr_tmp_bytes(N, nbits));
+}
+
+// Largest output allocated at the staging slots' size before its exact size
+// is known (columns and values).
+constexpr size_t kEarlyOutputBytes = size_t(16) << 30;
+
 // C_L = tril(A A^T) (lower, R = L) or L R^T: column index with the partner
 // run of every entry, per-row product counts, row classes, exact lengths of
 // the heavy rows, the light rows computed once into upper-bound staging slots
@@ -415,12 +492,14 @@ struct LowerPlan {
 // the partner run of an entry of L in column k is the whole column k of R,
 // read from dense column starts.
 
+// checked: waits for the operands' validation flags and throws on a bad
+// operand; called before the first kernel that reads their indices.
 // hist1 (optional): the first radix pass's digit counts of the sorted operand
 // (R), counted by its validation; vrows (optional, lower mode): the
 // validation's table of tile rows of A
 void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, Ctl* ctl, hipStream_t s,
-                spsyrk_csr_out* C, LowerPlan* plan = nullptr, uint32_t* hist1 = nullptr,
-                const int64_t* vrows = nullptr) {
+                spsyrk_csr_out* C, const std::function<void()>& checked, LowerPlan* plan = nullptr,
+                uint32_t* hist1 = nullptr, const int64_t* vrows = nullptr) {
     const int64_t m = L.m;
     const int vbo = out_value_bytes(sr);
     unsigned long long* prod = ar.get_t<unsigned long long>(m);
@@ -431,20 +510,27 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     run.r8 = ar.get_t<uint2>(L.nnz);
     run.radix = run_radix(lower ? L.nnz : R.nnz);
     run.inv = 1.0 / double(run.radix);
+    int32_t* heavy_rows = ar.get_t<int32_t>(m);
+    int64_t* ub = ar.get_t<int64_t>(m + 1);
+    // (classify_rows sets ub[m] = 0, and the light kernel row_cnt[m] = 0)
+    void* ptmp = ar.get(row_products_tmp_bytes(L.nnz));
     ColIndex cx;
     if (lower) {
         HIPCHK(hipMemsetAsync(run.r4, 0, size_t(L.nnz) * sizeof(uint32_t), s));
         if (run.radix == 1) HIPCHK(hipMemsetAsync(run.r8, 0, size_t(L.nnz) * sizeof(uint2), s));
-        Phase ph(SPSYRK_PHASE_COLINDEX, s);
         uint32_t* vsrc = nullptr;
         if (plan) {
             vsrc = ar.get_t<uint32_t>(L.nnz);
             HIPCHK(hipMemsetAsync(vsrc, 0, size_t(L.nnz) * sizeof(uint32_t), s));
             plan->vsrc = vsrc;
         }
+        reserve_index(L, sr, ar);
+        checked();
+        Phase ph(SPSYRK_PHASE_COLINDEX, s);
         cx = build_index(L, true, sr, ar, ctl, s, &run, true, nullptr, nullptr, vsrc, hist1, vrows);
         if (hist1) ar.release(hist1);
     } else {
+        checked();
         Phase ph(SPSYRK_PHASE_COLINDEX, s);
         // column starts of R: from the counts the local sort writes, else by counting
         uint32_t* cptr = ar.get_t<uint32_t>(R.n + 1);
@@ -462,10 +548,6 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         ar.release(ctmp);
         ar.release(cptr);
     }
-    int32_t* heavy_rows = ar.get_t<int32_t>(m);
-    int64_t* ub = ar.get_t<int64_t>(m + 1);
-    // (classify_rows sets ub[m] = 0, and the light kernel row_cnt[m] = 0)
-    void* ptmp = ar.get(row_products_tmp_bytes(L.nnz));
     {
         Phase ph(SPSYRK_PHASE_RUNS, s);
         row_products(L.rp, m, L.nnz, run, ptmp, prod, s, vrows);
@@ -473,7 +555,18 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
                       &ctl->maxlen);
     }
     check_launch();
-    Ctl h = read_ctl(ctl, s);
+    // the row classes go to the host; the scan of the staging slots needs
+    // none of them and runs meanwhile
+    ctl_fetch(ctl, s);
+    int64_t* ubp = ub;
+    void* stmp = ar.get(scan_tmp_bytes(m + 1));
+    {
+        Phase ph(SPSYRK_PHASE_SCAN, s);
+        scan_i64(ub, ubp, m + 1, &ctl->total2, stmp, s);
+    }
+    int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
+    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
+    Ctl h = ctl_wait();
     ar.release(ptmp);
     const int64_t nheavy = h.heavy_count;
     const int64_t light_cap = int64_t(h.light_cap);
@@ -509,12 +602,6 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         heavy_symbolic(ha, &ctl->queue, s);
     }
     check_launch();
-    int64_t* ubp = ub;
-    void* stmp = ar.get(scan_tmp_bytes(m + 1));
-    {
-        Phase ph(SPSYRK_PHASE_SCAN, s);
-        scan_i64(ub, ubp, m + 1, &ctl->total2, stmp, s);
-    }
     // counts and Jaccard values of the light rows staged as one word per
     // output (column and packed value) where the words fit: the counts are
     // at most the light rows' lengths, the partners' lengths at most the
@@ -531,7 +618,6 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     }
     int32_t* s_ci = ar.get_t<int32_t>(light_cap > 0 ? light_cap : 1);
     void* s_val = ar.get(size_t(pack_rr || light_cap <= 0 ? 1 : light_cap) * vbo);
-    int64_t* row_cnt = ar.get_t<int64_t>(m + 1);
 
     FusedArgs fa;
     fa.m = m;
@@ -561,24 +647,43 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
         light_fused(fa, s);
     }
     check_launch();
-    int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
     {
         Phase ph(SPSYRK_PHASE_SCAN, s);
         scan_i64(row_cnt, c_rp, m + 1, &ctl->total, stmp, s);
     }
     heavy_sums(heavy_rows, nheavy, L.rp, c_rp, ctl->heavy_sums, s);  // (counters for the statistics)
     check_launch();
-    h = read_ctl(ctl, s);
-    const int64_t total = h.total;
-    int32_t* c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
-    void* c_val = ar.get(size_t(total > 0 ? total : 1) * vbo, true);
-    {
-        Phase ph(SPSYRK_PHASE_COMPACT, s);
+    // With every row light the staging slots bound the output: it is then
+    // allocated at that size and compacted before the host reads its exact
+    // size, so that the device does not wait for the host (up to a bound on
+    // the extra memory; the slots exceed the output by the merged products).
+    const bool early = nheavy == 0 && size_t(light_cap) * size_t(4 + vbo) <= kEarlyOutputBytes;
+    int64_t total = 0;
+    int32_t* c_ci = nullptr;
+    void* c_val = nullptr;
+    auto compact = [&]() {
         void* ctmp = ar.get(compact_tmp_bytes(light_cap));
+        Phase ph(SPSYRK_PHASE_COMPACT, s);
         compact_rows(m, light_cap, ubp, row_cnt, c_rp, s_ci, s_val, vbo, ctmp, c_ci, c_val, s, pack_rr ? sr : 0,
                      pack_rr, pack_r2, L.rp);
+    };
+    if (early) {
+        const int64_t cap = light_cap > 0 ? light_cap : 1;
+        c_ci = ar.get_t<int32_t>(cap, true);
+        c_val = ar.get(size_t(cap) * vbo, true);
+        ctl_fetch(ctl, s);
+        compact();
+        check_launch();
+        h = ctl_wait();
+        total = h.total;
+    } else {
+        h = read_ctl(ctl, s);
+        total = h.total;
+        c_ci = ar.get_t<int32_t>(total > 0 ? total : 1, true);
+        c_val = ar.get(size_t(total > 0 ? total : 1) * vbo, true);
+        compact();
+        check_launch();
     }
-    check_launch();
     if (nheavy > 0) {
         ha.c_rp = c_rp;
         ha.c_ci = c_ci;
@@ -654,13 +759,24 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     void* vrows = fused && lower && L.nnz > 0 ? ar.get(validate_tmp_bytes(L.nnz)) : nullptr;
     {
         Phase ph(SPSYRK_PHASE_VALIDATE, s);
-        validate(L, false, ar, ctl, s, lower ? "A" : "Ai", lower && fh.hist ? &fh : nullptr, vrows);
-        if (!lower) validate(R, false, ar, ctl, s, "Aj", fh.hist ? &fh : nullptr);
+        validate_enqueue(L, false, ar, &ctl->err, s, lower && fh.hist ? &fh : nullptr, vrows);
+        if (!lower) validate_enqueue(R, false, ar, &ctl->err2, s, fh.hist ? &fh : nullptr);
     }
+    // The flags are read with one copy and checked before any kernel reads
+    // the matrices' indices; the single-pass path first enqueues the
+    // allocations and clears that depend on the sizes alone, so that the
+    // host prepares them while the validation runs.
+    ctl_fetch(ctl, s);
+    const std::function<void()> checked = [&]() {
+        const Ctl h = ctl_wait();
+        check_valid(h.err, lower ? "A" : "Ai");
+        if (!lower) check_valid(h.err2, "Aj");
+    };
 
     const int64_t m = L.m;
     spsyrk_stats st{};
     if (m == 0 || L.nnz == 0 || R.nnz == 0) {
+        checked();
         int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
         HIPCHK(hipMemsetAsync(c_rp, 0, size_t(m + 1) * sizeof(int64_t), s));
         C->nrows = m;
@@ -679,9 +795,10 @@ void syrk(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar, hipSt
     // single pass over the light rows; off the diagonal when the right
     // operand's column starts fit a dense array (else the two-pass path)
     if (fused) {
-        syrk_fused(L, R, lower, sr, ar, ctl, s, C, plan, fh.hist, static_cast<const int64_t*>(vrows));
+        syrk_fused(L, R, lower, sr, ar, ctl, s, C, checked, plan, fh.hist, static_cast<const int64_t*>(vrows));
         return;
     }
+    checked();
     int64_t* c_rp = ar.get_t<int64_t>(m + 1, true);
     ColIndex cx;
     {
