@@ -345,7 +345,8 @@ spsyrk_status spsyrk_last_stats(spsyrk_stats* out);
  * each.  spsyrk_timing_end waits for the recorded
  * events, returns the summed milliseconds and the number of timed launches
  * per phase, releases the events and stops recording.  Recording adds no
- * synchronisation to the calls themselves.
+ * synchronisation to the calls themselves, but every recorded event leaves
+ * the device idle for a few microseconds between the kernels around it.
  */
 typedef enum spsyrk_phase {
     SPSYRK_PHASE_VALIDATE = 0,       /* canonical-CSR checks of the inputs */
@@ -373,6 +374,9 @@ typedef struct spsyrk_phase_times {
 } spsyrk_phase_times;
 
 spsyrk_status spsyrk_timing_begin(void);
+/* As spsyrk_timing_begin, for the phases whose bits are set in mask (bit p:
+ * phase p) only; the other phases record nothing. */
+spsyrk_status spsyrk_timing_begin_phases(uint32_t mask);
 spsyrk_status spsyrk_timing_end(spsyrk_phase_times* out);
 
 /* ABI version the library was built with (SPSYRK_ABI_VERSION). */

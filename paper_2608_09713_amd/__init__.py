@@ -119,6 +119,8 @@ def library():
             lib.spsyrk_last_stats.restype = ctypes.c_int
             lib.spsyrk_abi_version.restype = ctypes.c_int
             lib.spsyrk_timing_begin.restype = ctypes.c_int
+            lib.spsyrk_timing_begin_phases.argtypes = [ctypes.c_uint32]
+            lib.spsyrk_timing_begin_phases.restype = ctypes.c_int
             lib.spsyrk_timing_end.argtypes = [ctypes.POINTER(_PhaseTimes)]
             lib.spsyrk_timing_end.restype = ctypes.c_int
             _lib = lib
@@ -130,7 +132,7 @@ EXPORTS = ("spsyrk_lower", "spsyrk_lower_plan", "spsyrk_lower_execute", "spsyrk_
            "spsyrk_symm", "spsyrk_symm_noalloc",
            "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
-           "spsyrk_timing_end")
+           "spsyrk_timing_begin_phases", "spsyrk_timing_end")
 
 PHASES = ("validate", "colindex", "light_symbolic", "heavy_symbolic", "scan", "light_numeric", "heavy_numeric",
           "mirror_count", "mirror_copy", "mirror_transpose", "runs", "compact", "colindex_passes", "colindex_pack")
@@ -437,9 +439,16 @@ def stats() -> dict:
     return s.as_dict()
 
 
-def timing_begin() -> None:
-    """Start recording HIP events around every phase of the calls on this thread."""
-    library().spsyrk_timing_begin()
+def timing_begin(phases=None) -> None:
+    """Start recording HIP events around every phase of the calls on this
+    thread, or around the named phases only."""
+    if phases is None:
+        library().spsyrk_timing_begin()
+    else:
+        mask = 0
+        for name in phases:
+            mask |= 1 << PHASES.index(name)
+        library().spsyrk_timing_begin_phases(mask)
 
 
 def timing_end() -> dict:

@@ -184,7 +184,24 @@ struct PhaseMark {
     hipEvent_t a, b;
 };
 thread_local bool g_timing = false;
+thread_local uint32_t g_phase_mask = 0;  // bit p: phase p is timed
 thread_local std::vector<PhaseMark> g_marks;
+// events of finished marks, reused so that a timed call creates none
+thread_local std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t pooled_event() {
+    if (!g_event_pool.empty()) {
+        hipEvent_t e = g_event_pool.back();
+        g_event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+}
+
+void pool_event(hipEvent_t e) {
+    if (e) g_event_pool.push_back(e);
+}
 
 using Phase = PhaseTimer;
 
@@ -239,7 +256,12 @@ void ctl_fetch(const Ctl* d, hipStream_t s) {
 
 Ctl ctl_wait() {
     HostCtl& pin = host_ctl();
-    HIPCHK(hipEventSynchronize(pin.ev));
+    // polled rather than blocked on: the waits are short, and a blocked
+    // thread resumes some microseconds after the event, with the device idle
+    hipError_t e;
+    while ((e = hipEventQuery(pin.ev)) == hipErrorNotReady) {
+    }
+    HIPCHK(e);
     return *pin.h;
 }
 
@@ -1344,15 +1366,12 @@ size_t symm_noalloc_bytes(int64_t m, int64_t k, int64_t nnz) {
 }  // namespace
 
 spsyrk::PhaseTimer::PhaseTimer(int phase, hipStream_t s) : s_(s), phase_(phase) {
-    if (!g_timing) return;
-    if (hipEventCreate(&a_) != hipSuccess) return;
-    if (hipEventCreate(&b_) != hipSuccess) {
-        (void)hipEventDestroy(a_);
-        return;
-    }
-    if (hipEventRecord(a_, s_) != hipSuccess) {
-        (void)hipEventDestroy(a_);
-        (void)hipEventDestroy(b_);
+    if (!g_timing || phase < 0 || phase >= 32 || !((g_phase_mask >> phase) & 1u)) return;
+    a_ = pooled_event();
+    b_ = pooled_event();
+    if (!a_ || !b_ || hipEventRecord(a_, s_) != hipSuccess) {
+        pool_event(a_);
+        pool_event(b_);
         return;
     }
     on_ = true;
@@ -1363,8 +1382,8 @@ spsyrk::PhaseTimer::~PhaseTimer() {
     if (hipEventRecord(b_, s_) == hipSuccess) {
         g_marks.push_back(PhaseMark{phase_, a_, b_});
     } else {
-        (void)hipEventDestroy(a_);
-        (void)hipEventDestroy(b_);
+        pool_event(a_);
+        pool_event(b_);
     }
 }
 
@@ -1727,12 +1746,21 @@ spsyrk_status spsyrk_last_stats(spsyrk_stats* out) {
 
 int spsyrk_abi_version(void) { return SPSYRK_ABI_VERSION; }
 
-spsyrk_status spsyrk_timing_begin(void) {
+spsyrk_status spsyrk_timing_begin(void) { return spsyrk_timing_begin_phases(0xffffffffu); }
+
+spsyrk_status spsyrk_timing_begin_phases(uint32_t mask) {
     for (auto& mk : g_marks) {
-        (void)hipEventDestroy(mk.a);
-        (void)hipEventDestroy(mk.b);
+        pool_event(mk.a);
+        pool_event(mk.b);
     }
     g_marks.clear();
+    // enough events for a few calls' phases, created now rather than inside them
+    while (g_event_pool.size() < 64) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) break;
+        g_event_pool.push_back(e);
+    }
+    g_phase_mask = mask;
     g_timing = true;
     return SPSYRK_OK;
 }
@@ -1750,8 +1778,8 @@ spsyrk_status spsyrk_timing_end(spsyrk_phase_times* out) {
             out->ms[mk.phase] += ms;
             out->launches[mk.phase] += 1;
         }
-        (void)hipEventDestroy(mk.a);
-        (void)hipEventDestroy(mk.b);
+        pool_event(mk.a);
+        pool_event(mk.b);
     }
     g_marks.clear();
     return st;

@@ -823,6 +823,28 @@ def test_mirror_structure_only(dev):
     del torch
 
 
+def test_phase_timing(dev):
+    # every phase timed, then only the light numeric phase: the selection
+    # records that phase alone, once per call, and the product is unchanged
+    A = W.make("kmer_i32", 1, 6)["A"]
+    Ad = upload(A, "count", dev)
+    sp.timing_begin()
+    X = sp.lower(Ad, "count").to_host()
+    ph = sp.timing_end()
+    assert {"validate", "colindex", "runs", "light_numeric", "compact"} <= set(ph)
+    sp.timing_begin(["light_numeric"])
+    Y = sp.lower(Ad, "count").to_host()
+    Y2 = sp.lower(Ad, "count").to_host()
+    ph = sp.timing_end()
+    assert set(ph) == {"light_numeric"} and ph["light_numeric"][1] == 2 and ph["light_numeric"][0] > 0
+    sp.timing_begin([])
+    sp.lower(Ad, "count")
+    assert sp.timing_end() == {}
+    for a, b, c in zip(X, Y, Y2):
+        np.testing.assert_array_equal(a, b)
+        np.testing.assert_array_equal(a, c)
+
+
 def test_deterministic(dev):
     A = W.make("kmer_i32", 1, 6)["A"]
     X = sp.lower(upload(A, "count", dev), "count").to_host()
