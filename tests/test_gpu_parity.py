@@ -874,3 +874,17 @@ def test_rejects_non_canonical_on_device(dev):
     with pytest.raises(sp.SpsyrkError) as ei:   # entry above the diagonal
         sp.mirror(_raw(dev, [0, 2, 3], [0, 1, 0], 2, np.ones(3)), "f64")
     assert ei.value.status == 2
+    # off the diagonal both operands' flags are read at once; the message
+    # names the operand that failed (the left one first)
+    good = _raw(dev, [0, 2, 3], [1, 2, 3], 4, np.ones(3))
+    for rp, ci, n in bad:
+        for left in (True, False):
+            B = _raw(dev, rp, ci, n, np.ones(len(ci)))
+            with pytest.raises(sp.SpsyrkError) as ei:
+                sp.offdiag(B, good, "f64") if left else sp.offdiag(good, B, "f64")
+            assert ei.value.status == 2 and ("Ai" if left else "Aj") in ei.value.detail
+    with pytest.raises(sp.SpsyrkError) as ei:
+        sp.offdiag(_raw(dev, [0, 2, 3], [1, 0, 2], 4, np.ones(3)), _raw(dev, [0, 2, 3], [1, 7, 2], 4, np.ones(3)),
+                   "f64")
+    assert ei.value.status == 2 and "Ai" in ei.value.detail
+    np.testing.assert_array_equal(sp.offdiag(good, good, "f64").to_host()[0], [0, 1, 2])
