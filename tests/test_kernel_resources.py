@@ -66,3 +66,19 @@ def test_light_kernel_budgets():
             assert r["Occupancy"] >= 3 and r["ScratchSize"] <= 40, (name, r)
         else:
             assert r["Occupancy"] >= 3 and r["ScratchSize"] == 0, (name, r)
+
+
+def test_local_sort_budgets():
+    # the packed column sort's first launch holds groups of up to 2048
+    # records: at most 18 KiB of LDS and 72 VGPRs, so that seven workgroups
+    # of four wavefronts share a compute unit (the second launch, for the
+    # rare larger groups, keeps the 4096-record LDS arrays); no spills
+    ks = _report("radix.hip")
+    small = {k: v for k, v in ks.items() if "local_sort_packILi" in k}
+    big = {k: v for k, v in ks.items() if "local_sort_pack_bigILi" in k}
+    assert len(small) == 4 and len(big) == 4  # f64, f32, count and Jaccard records
+    for name, r in small.items():
+        assert r["ScratchSize"] == 0 and r["VGPRs"] <= 72 and r["LDS"] <= 18 * 1024, (name, r)
+        assert r["Occupancy"] >= 7 and 7 * r["LDS"] <= 160 * 1024, (name, r)
+    for name, r in big.items():
+        assert r["ScratchSize"] == 0 and r["LDS"] <= 36 * 1024, (name, r)
