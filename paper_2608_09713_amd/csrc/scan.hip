@@ -1,5 +1,6 @@
 // Device-wide exclusive prefix sums (three launches: tile reduce, scan of
-// tile sums in one workgroup, tile scan with carry-in).
+// tile sums in one workgroup, tile scan with carry-in; one launch for arrays
+// of at most four tiles).
 #include "common.h"
 #include "internal.h"
 
@@ -59,12 +60,12 @@ __global__ __launch_bounds__(kBlock) void scan_sums(T* __restrict__ sums, int64_
     if (threadIdx.x == 0 && total) *total = carry;
 }
 
+// Exclusive scan of the tile at base (kTile values of in, zero past n) into
+// out, starting from carry; returns the tile's sum.  The tile is read whole
+// into LDS before any of it is written, so in may equal out.
 template <typename T>
-__global__ __launch_bounds__(kBlock) void tile_scan(const T* __restrict__ in, T* __restrict__ out, int64_t n,
-                                                    const T* __restrict__ sums) {
-    __shared__ T wt[kWavesPerBlock];
-    __shared__ T buf[kTile];
-    const int64_t base = int64_t(blockIdx.x) * kTile;
+__device__ inline T scan_tile(const T* __restrict__ in, T* __restrict__ out, int64_t n, int64_t base, T carry,
+                              T* buf, T* wt) {
     // coalesced loads into LDS, then a blocked arrangement: thread t holds
     // kItems consecutive elements
 #pragma unroll
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(kBlock) void tile_scan(const T* __restrict__ in, T*
         s += v[k];
     }
     T tot;
-    T off = block_exclusive_scan(s, wt, &tot) + sums[blockIdx.x];
+    T off = block_exclusive_scan(s, wt, &tot) + carry;
 #pragma unroll
     for (int k = 0; k < kItems; ++k) {
         buf[threadIdx.x * kItems + k] = off;
@@ -93,6 +94,29 @@ __global__ __launch_bounds__(kBlock) void tile_scan(const T* __restrict__ in, T*
         const int64_t i = base + int64_t(k) * kBlock + threadIdx.x;
         if (i < n) out[i] = buf[k * kBlock + threadIdx.x];
     }
+    __syncthreads();  // (buf is reused by the next tile)
+    return tot;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void tile_scan(const T* __restrict__ in, T* __restrict__ out, int64_t n,
+                                                    const T* __restrict__ sums) {
+    __shared__ T wt[kWavesPerBlock];
+    __shared__ T buf[kTile];
+    (void)scan_tile(in, out, n, int64_t(blockIdx.x) * kTile, sums[blockIdx.x], buf, wt);
+}
+
+// up to kOneBlockTiles tiles scanned by one workgroup, tile after tile with
+// the carry (one launch instead of three for short arrays); total -> *total
+constexpr int64_t kOneBlockTiles = 4;
+template <typename T>
+__global__ __launch_bounds__(kBlock) void scan_one_block(const T* __restrict__ in, T* __restrict__ out, int64_t n,
+                                                         T* __restrict__ total) {
+    __shared__ T wt[kWavesPerBlock];
+    __shared__ T buf[kTile];
+    T carry = 0;
+    for (int64_t base = 0; base < n; base += kTile) carry += scan_tile(in, out, n, base, carry, buf, wt);
+    if (total && threadIdx.x == 0) *total = carry;
 }
 
 template <typename T>
@@ -101,6 +125,10 @@ void scan_impl(const T* in, T* out, int64_t n, T* total, void* tmp, hipStream_t 
     T* sums = static_cast<T*>(tmp);
     if (nb == 0) {
         if (total) (void)hipMemsetAsync(total, 0, sizeof(T), s);
+        return;
+    }
+    if (nb <= kOneBlockTiles) {
+        scan_one_block<T><<<1, kBlock, 0, s>>>(in, out, n, total);
         return;
     }
     tile_reduce<T><<<dim3(unsigned(nb)), dim3(kBlock), 0, s>>>(in, n, sums);
