@@ -452,12 +452,18 @@ spsyrk_status finish(spsyrk_status st) {
 
 // Rows per wavefront chunk of the light-row kernel (SPSYRK_ROWS_PER_CHUNK
 // overrides it for tuning); a chunk splits into as many LDS batches as needed.
-int rows_per_chunk(double) {
+// A matrix of fewer rows than the device's wavefronts hold in chunks of
+// kFusedRows takes shorter chunks (down to 8 rows), so that more wavefronts
+// share it: tiny_uniform_f64 (4096 rows) 28 -> 17 us.
+int rows_per_chunk(int64_t m) {
     if (const char* e = std::getenv("SPSYRK_ROWS_PER_CHUNK")) {
         const int v = std::atoi(e);
         if (v >= 1 && v <= kFusedRows) return v;
     }
-    return kFusedRows;
+    constexpr int64_t kWaves = 3072;  // wavefronts of the light kernel resident on the device
+    int r = kFusedRows;
+    while (r > 8 && m < int64_t(r) * kWaves) r /= 2;
+    return r;
 }
 
 constexpr int64_t kDenseColumns = int64_t(1) << 28;  // dense column starts: at most 1 GiB
@@ -657,7 +663,7 @@ void syrk_fused(const DevCsr& L, const DevCsr& R, bool lower, int sr, Arena& ar,
     fa.ubp = ubp;
     fa.row_cnt = row_cnt;
     const int64_t nlight = m - nheavy;
-    fa.rows_per_chunk = rows_per_chunk(nlight > 0 ? double(light_cap) / double(nlight) : 1.0);
+    fa.rows_per_chunk = rows_per_chunk(m);
     fa.nchunks = (m + fa.rows_per_chunk - 1) / fa.rows_per_chunk;
     fa.chunk_counter = &ctl->chunk_counter;  // (zero: ctl is zeroed at the call's start)
     fa.c_ci = s_ci;

@@ -615,6 +615,25 @@ def test_packed_staging(dev, semiring, pack, monkeypatch):
     run_lower(W, semiring, dev, f"packed staging {pack} with a 300-entry row")
 
 
+@pytest.mark.parametrize("semiring", ["f64", "jaccard"])
+@pytest.mark.parametrize("rows", ["32", "8", "1"])
+def test_rows_per_chunk(dev, semiring, rows, monkeypatch):
+    # the light kernel's chunks of 32 rows (large matrices), 8 (small ones)
+    # and 1, forced on a matrix with heavy rows: lower and off-diagonal
+    # products match the oracle
+    monkeypatch.setenv("SPSYRK_ROWS_PER_CHUNK", rows)
+    rng = np.random.default_rng(67)
+    vdt = VDT[semiring]
+    A = _with_long_rows(rng, 1500, 1200)
+    run_lower(A, semiring, dev, f"{rows} rows per chunk")
+    assert sp.stats()["heavy_rows"] > 0
+    B = _rows_csr(rng, 700, 1200, 5)
+    O = sp.offdiag(upload(A, semiring, dev), upload(B, semiring, dev), semiring)
+    compare_full(O, oracle.offdiag(A.with_values(A.values.astype(vdt) if vdt else None),
+                                   B.with_values(B.values.astype(vdt) if vdt else None), semiring), semiring,
+                 f"{rows} rows per chunk offdiag")
+
+
 def test_plan_of_empty_matrix(dev):
     A = CSR(5, 7, np.zeros(6, np.int64), np.zeros(0, np.int32), np.zeros(0))
     plan, C = sp.lower_plan(upload(A, "f64", dev), "f64")
