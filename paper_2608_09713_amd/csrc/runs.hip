@@ -148,6 +148,7 @@ __global__ __launch_bounds__(kBlock) void rowprod_kernel(const int64_t* __restri
 }
 
 constexpr int kCTile = 4096;  // staging slots per compaction workgroup
+constexpr int kCTileSmall = 512;  // the same for few slots (compact_tile)
 template <int VB>
 struct SlotT {  // a staged value of VB bytes (a placeholder for VB 0)
     using T = uint32_t;
@@ -182,7 +183,7 @@ __device__ inline void unpack_store(const Unpack& u, uint32_t w, int64_t len_i, 
 
 // PK 0: columns and VB-byte values copied; PK 1 (counts) and 2 (Jaccard):
 // packed words unpacked (rp_a: the row pointers of A, for the row lengths)
-template <int VB, int PK = 0>
+template <int VB, int PK, int CT>
 __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t staged, const int64_t* __restrict__ ubp,
                                                          const int64_t* __restrict__ trow,
                                                          const int64_t* __restrict__ row_cnt,
@@ -194,15 +195,15 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     __shared__ int64_t wend[kCWin];     // end of each row's valid staged entries
     __shared__ int64_t wdel[kCWin];     // final position minus staging slot
     __shared__ int32_t wlen[PK == 2 ? kCWin : 1];  // (Jaccard) the rows' lengths
-    __shared__ uint16_t rowof[kCTile];  // window row of every slot of the tile
+    __shared__ uint16_t rowof[CT];  // window row of every slot of the tile
     __shared__ uint32_t wt[kWavesPerBlock];
     __shared__ int64_t bounds[2];
-    const int64_t s0 = int64_t(blockIdx.x) * kCTile;
-    const int64_t s1 = min(staged, s0 + kCTile);
+    const int64_t s0 = int64_t(blockIdx.x) * CT;
+    const int64_t s1 = min(staged, s0 + CT);
     // a whole tile's staged columns (or packed words) are loaded first, so
     // that they arrive while the tile's rows are set up
-    constexpr int kPerC = kCTile / kBlock;
-    const bool whole = s1 - s0 == kCTile;
+    constexpr int kPerC = CT / kBlock;
+    const bool whole = s1 - s0 == CT;
     int32_t pre[kPerC];
     if (whole)
 #pragma unroll
@@ -219,7 +220,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
     const int64_t nrw = rhi - rlo + 1;
     const bool win_ok = nrw <= kCWin;
     if (win_ok) {
-        for (int x = threadIdx.x; x < kCTile; x += kBlock) rowof[x] = 0;
+        for (int x = threadIdx.x; x < CT; x += kBlock) rowof[x] = 0;
         for (int64_t k = threadIdx.x; k <= nrw; k += kBlock) {
             const int64_t u = ubp[rlo + k];
             wub[k] = u;
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
         for (int64_t k = 1 + threadIdx.x; k < nrw; k += kBlock)
             if (wub[k] < wub[k + 1] && wub[k] < s1) rowof[wub[k] - s0] = uint16_t(k);
         __syncthreads();
-        constexpr int kPer = kCTile / kBlock;
+        constexpr int kPer = CT / kBlock;
         const int lane = lane_id();
         const int w = threadIdx.x / kWave;
         uint32_t run_max = 0;
@@ -264,10 +265,10 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
         // a whole tile: the slots of a thread in batches of kBatch, every
         // batch's loads in flight together before its stores
         using V = typename SlotT<VB>::T;
-        constexpr int kBatch = 8;
-        static_assert(kCTile % (kBlock * kBatch) == 0, "whole batches per tile");
+        constexpr int kBatch = CT / kBlock < 8 ? CT / kBlock : 8;
+        static_assert(CT % (kBlock * kBatch) == 0, "whole batches per tile");
 #pragma unroll
-        for (int b = 0; b < kCTile / (kBlock * kBatch); ++b) {
+        for (int b = 0; b < CT / (kBlock * kBatch); ++b) {
             int32_t cv[kBatch];
             V vv[kBatch];
             bool live[kBatch];
@@ -473,15 +474,44 @@ void row_products(const int64_t* rp, int64_t m, int64_t nnz, const RunTab& run, 
     rowprod_kernel<<<nb, kBlock, 0, s>>>(rp, m, nnz, run, trow, prod);
 }
 
-size_t compact_tmp_bytes(int64_t staged) { return size_t((staged + kCTile - 1) / kCTile + 1) * sizeof(int64_t); }
+// Staging slots per compaction workgroup: kCTile, or for fewer slots than
+// 256 such tiles (fewer workgroups than compute units) tiles of kCTileSmall,
+// so that more workgroups share the work.
+static int compact_tile(int64_t staged) { return staged < int64_t(256) * kCTile ? kCTileSmall : kCTile; }
+
+size_t compact_tmp_bytes(int64_t staged) {
+    const int ct = compact_tile(staged);
+    return size_t((staged + ct - 1) / ct + 1) * sizeof(int64_t);
+}
+
+template <int CT>
+static void launch_compact(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
+                    const int32_t* s_ci, const void* s_val, int vbytes, int64_t* trow, int32_t* c_ci, void* c_val,
+                    hipStream_t s, int packed, const Unpack& un, const int64_t* rp_a) {
+    const unsigned nb = unsigned((staged + CT - 1) / CT);
+    tile_first_rows(ubp, m, CT, trow, s);
+    if (packed == kCount)
+        compact_kernel<0, 1, CT><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val,
+                                                       rp_a, un);
+    else if (packed == kJaccard)
+        compact_kernel<0, 2, CT><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val,
+                                                       rp_a, un);
+    else if (vbytes == 8)
+        compact_kernel<8, 0, CT><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val,
+                                                       rp_a, un);
+    else if (vbytes == 4)
+        compact_kernel<4, 0, CT><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val,
+                                                       rp_a, un);
+    else
+        compact_kernel<0, 0, CT><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val,
+                                                       rp_a, un);
+}
 
 void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* row_cnt, const int64_t* c_rp,
                   const int32_t* s_ci, const void* s_val, int vbytes, void* tmp, int32_t* c_ci, void* c_val,
                   hipStream_t s, int packed, uint32_t pack_rr, uint32_t pack_r2, const int64_t* rp_a) {
     if (staged <= 0 || m <= 0) return;
-    const unsigned nb = unsigned((staged + kCTile - 1) / kCTile);
     int64_t* trow = static_cast<int64_t*>(tmp);
-    tile_first_rows(ubp, m, kCTile, trow, s);
     Unpack un;
     if (packed) {
         un.rr = pack_rr;
@@ -489,18 +519,12 @@ void compact_rows(int64_t m, int64_t staged, const int64_t* ubp, const int64_t* 
         un.inv_rr = 1.0 / double(un.rr);
         un.inv_r2 = 1.0 / double(un.r2);
     }
-    if (packed == kCount)
-        compact_kernel<0, 1><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a,
-                                                   un);
-    else if (packed == kJaccard)
-        compact_kernel<0, 2><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a,
-                                                   un);
-    else if (vbytes == 8)
-        compact_kernel<8><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a, un);
-    else if (vbytes == 4)
-        compact_kernel<4><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a, un);
+    if (compact_tile(staged) == kCTile)
+        launch_compact<kCTile>(m, staged, ubp, row_cnt, c_rp, s_ci, s_val, vbytes, trow, c_ci, c_val, s, packed, un,
+                               rp_a);
     else
-        compact_kernel<0><<<nb, kBlock, 0, s>>>(m, staged, ubp, trow, row_cnt, c_rp, s_ci, s_val, c_ci, c_val, rp_a, un);
+        launch_compact<kCTileSmall>(m, staged, ubp, row_cnt, c_rp, s_ci, s_val, vbytes, trow, c_ci, c_val, s, packed,
+                                    un, rp_a);
 }
 
 }  // namespace spsyrk
