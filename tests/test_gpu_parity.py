@@ -313,6 +313,39 @@ def test_local_sort_large_groups(dev, semiring, monkeypatch):
     run_lower(A, semiring, dev, "local sort, groups past the LDS capacity")
 
 
+@pytest.mark.parametrize("semiring", ["f64", "count", "jaccard"])
+def test_local_sort_group_size_limits(dev, semiring, monkeypatch):
+    # 2^15 columns and under 16384 entries give 8 groups of 4096 columns
+    # (high bits max(15 - 12, bit width of nnz / 2048) = 3), filled with
+    # exactly 2048, 2049, 4096, 4097, 1, 0, 0 and 7 records: the limits of
+    # the first launch's LDS (2048), of the second's (4096), and tiny groups
+    monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
+    rng = np.random.default_rng(71)
+    sizes = [2048, 2049, 4096, 4097, 1, 0, 0, 7]
+    cols = np.concatenate([g * 4096 + rng.integers(0, 4096, size=k) for g, k in enumerate(sizes)])
+    rng.shuffle(cols)
+    per = 6
+    rows = [cols[i:i + per].copy() for i in range(0, len(cols), per)]
+    for r in rows:  # distinct columns within a row, each redrawn inside its own group
+        while len(np.unique(r)) < len(r):
+            _, first = np.unique(r, return_index=True)
+            dup = np.setdiff1d(np.arange(len(r)), first)
+            r[dup] = (r[dup] // 4096) * 4096 + rng.integers(0, 4096, size=len(dup))
+        r.sort()
+    rp = np.zeros(len(rows) + 1, dtype=np.int64)
+    rp[1:] = np.cumsum([len(r) for r in rows])
+    ci = np.concatenate(rows).astype(np.int32)
+    assert list(np.bincount(ci >> 12, minlength=8)) == sizes
+    A = CSR(len(rows), 1 << 15, rp, ci, rng.random(len(ci)) + 0.5)
+    run_lower(A, semiring, dev, "local sort, groups at the LDS limits")
+    B = _rows_csr(rng, 500, 1 << 15, 5)
+    vdt = VDT[semiring]
+    O = sp.offdiag(upload(B, semiring, dev), upload(A, semiring, dev), semiring)
+    compare_full(O, oracle.offdiag(B.with_values(None if vdt is None else B.values.astype(vdt)),
+                                   A.with_values(None if vdt is None else A.values.astype(vdt)), semiring),
+                 semiring, "local sort, groups at the LDS limits, offdiag")
+
+
 @pytest.mark.parametrize("semiring", ["f64", "count"])
 def test_row_longer_than_the_tile_table(dev, semiring):
     # a row of 250000 entries spans 82 tiles of 3072 entries; the
