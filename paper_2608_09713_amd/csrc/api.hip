@@ -393,8 +393,15 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
         uint32_t* kb = ar.get_t<uint32_t>(N);
         uint32_t* ra = ar.get_t<uint32_t>(N);
         uint32_t* rb = ar.get_t<uint32_t>(N);
-        uint32_t* ea = ar.get_t<uint32_t>(N);
-        uint32_t* eb = ar.get_t<uint32_t>(N);
+        // with no run table and no entry map the local sort needs the entries'
+        // values only, so the passes carry them instead of the entry indices
+        const int carried = runs_given && !run && !vsrc && (vb == 4 || vb == 8) && B.v &&
+                                    local_bits(N, nbits_n) > 0
+                                ? vb
+                                : 0;
+        const size_t eb_bytes = size_t(N) * size_t(carried ? carried : int(sizeof(uint32_t)));
+        uint32_t* ea = static_cast<uint32_t*>(ar.get(eb_bytes));
+        uint32_t* eb = static_cast<uint32_t*>(ar.get(eb_bytes));
         void* tmp = ar.get(radix_csr_tmp_bytes(N, nbits_n));
         // Jaccard keeps the row lengths in the row field's spare bits
         const int lenbits = sr == kJaccard ? 32 - cx.rowbits : 0;
@@ -415,6 +422,7 @@ ColIndex build_index(const DevCsr& B, bool drop_last, int sr, Arena& ar, Ctl* ct
             pk.kept = &ctl->nkept;
             pk.ccount = ccount;
             pk.vsrc = vsrc;  // (ctl->nkept is zero: ctl is zeroed at the call's start)
+            pk.carried = carried;
         }
         const int which = radix_sort_csr(B.ci, B.rp, B.m, cx.rowbits, lenbits, ka, kb, ra, rb, ea, eb, N, nbits_n, tmp,
                                          s, runs_given ? &pk : nullptr, hist1, trow1);

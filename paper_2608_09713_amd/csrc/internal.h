@@ -168,6 +168,11 @@ struct LocalPack {
     int64_t* kept = nullptr;
     uint32_t* ccount = nullptr;  // non-null (zeroed, one per column): entries of every column
     uint32_t* vsrc = nullptr;    // non-null: the entry index of every written position
+    // 4 or 8 (with vals_b, and no run table and no vsrc): the record passes
+    // carry each entry's value in place of its index (the third record
+    // buffers then hold values of that size), so the local sort reads values
+    // in sorted order instead of gathering them by entry index
+    int carried = 0;
 };
 // pk non-null: write the column index as above when the local path is taken
 // and return -1 (no sorted copy); otherwise as described.
@@ -179,6 +184,9 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
                    uint32_t* key_b, uint32_t* row_a, uint32_t* row_b, uint32_t* ent_a, uint32_t* ent_b, int64_t n,
                    int nbits, void* tmp, hipStream_t s, const LocalPack* pk = nullptr, uint32_t* hist1 = nullptr,
                    const int64_t* trow1 = nullptr);
+// Low column bits sorted inside groups by radix_sort_csr for n entries with
+// nbits-bit columns (0: passes over every bit, no local sort).
+int local_bits(int64_t n, int nbits);
 // The digit of radix_sort_csr's first pass over n entries with nbits-bit
 // columns: (col >> shift) & mask.
 void radix_first_digit(int64_t n, int nbits, int* shift, uint32_t* mask);

@@ -99,7 +99,8 @@ __device__ inline int64_t last_leq_i64(const int64_t* a, int64_t lo, int64_t hi,
 // Where a pass takes its records from (SRC) and puts them (OUT).
 //  kSrcArrays: key, row and value arrays.
 //  kSrcCsr: straight from a CSR matrix: key = column, row from the row
-//    pointers (rp, m), value = the entry's index (VB must be 4).  With
+//    pointers (rp, m), value = the entry's index (VB 4), or with val_in the
+//    entry's value (VB 4 or 8, read from val_in in entry order).  With
 //    lenbits > 0 the row field also carries the row's length, saturated at
 //    2^lenbits - 1, above its low rowbits bits.
 //  kSrcSlab: a mirror slab's strict-lower entries, record p of row r (rows
@@ -429,8 +430,8 @@ __global__ __launch_bounds__(kBlock) void radix_scatter(const uint32_t* __restri
 #pragma unroll
         for (int k = 0; k < kRItems; ++k) {
             const int64_t idx = segbase + int64_t(k) * kWave + lane;
-            if constexpr (SRC == kSrcCsr)
-                vv[k] = V(idx);
+            if constexpr (SRC == kSrcCsr)  // the entry index, or with val_in the entry's value
+                vv[k] = val_in ? (idx < n ? __builtin_nontemporal_load(val_in + idx) : V(0)) : V(idx);
             else if constexpr (SRC == kSrcSlab)
                 vv[k] = vpre[k];
             else
@@ -622,8 +623,9 @@ __device__ inline void lds_pass(const uint16_t* dig_in, const uint16_t* idx_in, 
 // one stable pass of the global-memory sort of a large group [b0, b0 + S):
 // by bits [sh, sh + w) of the key, from the *i arrays to the *o arrays, in
 // tiles of kBlock records in order
-__device__ inline void group_pass(const uint32_t* ki, const uint32_t* ri, const uint32_t* ei, uint32_t* ko, uint32_t* ro,
-                                  uint32_t* eo, int64_t b0, int64_t S, int sh, int w, uint32_t* base,
+template <typename E>
+__device__ inline void group_pass(const uint32_t* ki, const uint32_t* ri, const E* ei, uint32_t* ko, uint32_t* ro,
+                                  E* eo, int64_t b0, int64_t S, int sh, int w, uint32_t* base,
                                   uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
     const int wv = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -774,11 +776,16 @@ __device__ inline void emit_entry(const LocalPack& pk, int64_t pos, uint32_t fie
     if (pk.run && pos > cstart) set_run(pk.run, ent, uint32_t(cstart), uint32_t(pos));
 }
 
+// The third field of the records: the entry index, or with CARRY the
+// entry's value itself (VB bytes, carried through the passes).
+template <int VB, bool CARRY>
+using EntT = typename std::conditional<CARRY, typename ValT<VB>::T, uint32_t>::type;
+
 // The LDS path of local_sort_pack: the group of S <= CAP records at b0.
 // Returns the number of distinct columns (the same in every thread).
-template <int VB, bool JAC, int CAP>
+template <int VB, bool JAC, int CAP, bool CARRY>
 __device__ inline uint32_t pack_group_lds(const uint32_t* __restrict__ kx, const uint32_t* __restrict__ rx,
-                                          const uint32_t* __restrict__ ex, int64_t b0, int S, int L,
+                                          const EntT<VB, CARRY>* __restrict__ ex, int64_t b0, int S, int L,
                                           const LocalPack& pk, uint16_t (*dg)[CAP], uint16_t (*ix)[CAP],
                                           uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
     static_assert(CAP % kBlock == 0 && CAP <= 65536, "whole rounds of the workgroup; 16-bit indices");
@@ -809,8 +816,10 @@ __device__ inline uint32_t pack_group_lds(const uint32_t* __restrict__ kx, const
         lds_pass<CAP>(dg[cur], ix[cur], dg[cur ^ 1], ix[cur ^ 1], S, sh, min(kLDig, L - sh), wcnt, wt);
         cur ^= 1;
     }
-    // row fields and entry indices in sorted order (in flight during the scan below)
-    uint32_t rv[kPer], ev[kPer];
+    // row fields and entry indices (or values) in sorted order (in flight
+    // during the scan below)
+    uint32_t rv[kPer];
+    EntT<VB, CARRY> ev[kPer];
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
         const int j = threadIdx.x + k * kBlock;
@@ -850,7 +859,12 @@ __device__ inline uint32_t pack_group_lds(const uint32_t* __restrict__ kx, const
     typename ValT<VB>::T vv[kPer];
 #pragma unroll
     for (int k = 0; k < kPer; ++k)
-        if (threadIdx.x + k * kBlock < S) vv[k] = entry_value<VB>(pk, ev[k]);
+        if (threadIdx.x + k * kBlock < S) {
+            if constexpr (CARRY)
+                vv[k] = ev[k];
+            else
+                vv[k] = entry_value<VB>(pk, ev[k]);
+        }
     const uint32_t hi = kx[b0] & ~lmask;  // the group's high column bits
 #pragma unroll
     for (int k = 0; k < kPer; ++k) {
@@ -858,7 +872,8 @@ __device__ inline uint32_t pack_group_lds(const uint32_t* __restrict__ kx, const
         if (j < S) {
             const uint32_t lo = dg[cur][j];
             const bool last = j == S - 1 || dg[cur][j + 1] != lo;
-            emit_entry<VB, JAC>(pk, b0 + j, rv[k], ev[k], b0 + cs[j], vv[k], last, hi | lo);
+            const uint32_t ent = CARRY ? 0u : uint32_t(ev[k]);  // (with CARRY no entry index is written)
+            emit_entry<VB, JAC>(pk, b0 + j, rv[k], ent, b0 + cs[j], vv[k], last, hi | lo);
         }
     }
     return distinct;
@@ -866,10 +881,10 @@ __device__ inline uint32_t pack_group_lds(const uint32_t* __restrict__ kx, const
 
 // The same for a group of any size, by passes over global memory (x -> y ->
 // x ..., ending in y), then the output a tile at a time.
-template <int VB, bool JAC>
+template <int VB, bool JAC, bool CARRY>
 __device__ inline uint32_t pack_group_global(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
-                                             uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
-                                             uint32_t* __restrict__ ry, uint32_t* __restrict__ ey, int64_t b0,
+                                             EntT<VB, CARRY>* __restrict__ ex, uint32_t* __restrict__ ky,
+                                             uint32_t* __restrict__ ry, EntT<VB, CARRY>* __restrict__ ey, int64_t b0,
                                              int64_t S, int L, const LocalPack& pk, uint32_t* base,
                                              uint32_t (*wcnt)[1 << kLDig], uint32_t* wt) {
     int npass = 0;
@@ -881,7 +896,7 @@ __device__ inline uint32_t pack_group_global(uint32_t* __restrict__ kx, uint32_t
     }
     const uint32_t* ks = (npass & 1) ? ky : kx;
     const uint32_t* rs = (npass & 1) ? ry : rx;
-    const uint32_t* es = (npass & 1) ? ey : ex;
+    const EntT<VB, CARRY>* es = (npass & 1) ? ey : ex;
     // the column start carried over from tile to tile
     uint32_t carry = 0, distinct = 0;
     for (int64_t t0 = 0; t0 < S; t0 += kBlock) {
@@ -896,8 +911,15 @@ __device__ inline uint32_t pack_group_global(uint32_t* __restrict__ kx, uint32_t
         if (j < S) {
             const uint32_t col = ks[b0 + j];
             const bool last = j == S - 1 || ks[b0 + j + 1] != col;
-            emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], es[b0 + j], b0 + cstart, entry_value<VB>(pk, es[b0 + j]), last,
-                                col);
+            typename ValT<VB>::T v;
+            uint32_t ent = 0;
+            if constexpr (CARRY) {
+                v = es[b0 + j];
+            } else {
+                ent = es[b0 + j];
+                v = entry_value<VB>(pk, ent);
+            }
+            emit_entry<VB, JAC>(pk, b0 + j, rs[b0 + j], ent, b0 + cstart, v, last, col);
         }
         carry = max(carry, all);
     }
@@ -915,10 +937,10 @@ __device__ inline void add_kept(const LocalPack& pk, int64_t S, uint32_t distinc
 // its length, zero on entry; then the group numbers) for
 // local_sort_pack_big.  The small capacity halves the LDS and the registers
 // of a workgroup, which doubles the workgroups a compute unit holds.
-template <int VB, bool JAC>
+template <int VB, bool JAC, bool CARRY>
 __global__ __launch_bounds__(kBlock) void local_sort_pack(const uint32_t* __restrict__ kx,
                                                           const uint32_t* __restrict__ rx,
-                                                          const uint32_t* __restrict__ ex,
+                                                          const EntT<VB, CARRY>* __restrict__ ex,
                                                           const uint32_t* __restrict__ gstart,
                                                           const uint32_t* __restrict__ gend, int L, LocalPack pk,
                                                           uint32_t* __restrict__ big) {
@@ -935,15 +957,16 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack(const uint32_t* __rest
         if (threadIdx.x == 0) big[1 + atomicAdd(big, 1u)] = blockIdx.x;
         return;
     }
-    add_kept(pk, S, pack_group_lds<VB, JAC, kLCapS>(kx, rx, ex, b0, int(S), L, pk, dg, ix, wcnt, wt));
+    add_kept(pk, S, pack_group_lds<VB, JAC, kLCapS, CARRY>(kx, rx, ex, b0, int(S), L, pk, dg, ix, wcnt, wt));
 }
 
 // The groups local_sort_pack listed, shared out over the grid: in LDS up to
 // kLCap records, over global memory (x and y in turn) beyond.
-template <int VB, bool JAC>
+template <int VB, bool JAC, bool CARRY>
 __global__ __launch_bounds__(kBlock) void local_sort_pack_big(uint32_t* __restrict__ kx, uint32_t* __restrict__ rx,
-                                                              uint32_t* __restrict__ ex, uint32_t* __restrict__ ky,
-                                                              uint32_t* __restrict__ ry, uint32_t* __restrict__ ey,
+                                                              EntT<VB, CARRY>* __restrict__ ex,
+                                                              uint32_t* __restrict__ ky, uint32_t* __restrict__ ry,
+                                                              EntT<VB, CARRY>* __restrict__ ey,
                                                               const uint32_t* __restrict__ gstart,
                                                               const uint32_t* __restrict__ gend, int L,
                                                               LocalPack pk, const uint32_t* __restrict__ big) {
@@ -958,8 +981,8 @@ __global__ __launch_bounds__(kBlock) void local_sort_pack_big(uint32_t* __restri
         const int64_t b0 = gstart[g];
         const int64_t S = int64_t(gend[g]) - b0;
         const uint32_t distinct =
-            S <= kLCap ? pack_group_lds<VB, JAC, kLCap>(kx, rx, ex, b0, int(S), L, pk, dg, ix, wcnt, wt)
-                       : pack_group_global<VB, JAC>(kx, rx, ex, ky, ry, ey, b0, S, L, pk, base, wcnt, wt);
+            S <= kLCap ? pack_group_lds<VB, JAC, kLCap, CARRY>(kx, rx, ex, b0, int(S), L, pk, dg, ix, wcnt, wt)
+                       : pack_group_global<VB, JAC, CARRY>(kx, rx, ex, ky, ry, ey, b0, S, L, pk, base, wcnt, wt);
         add_kept(pk, S, distinct);
         __syncthreads();  // (the shared arrays serve the next group)
     }
@@ -1053,6 +1076,8 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
     const int L = local_bits(n, nbits);
     int width[8];
     const int passes = digit_plan(nbits - L, width);
+    // bytes of the values carried in place of the entry indices (local sort only)
+    const int cv = pk && L ? pk->carried : 0;
     // first pass straight from the CSR arrays (into the b buffers), at least
     // one pass; the row of every tile's first entry comes from a table
     // with the local sort: the groups' starts (and ends), and the first
@@ -1076,9 +1101,15 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
         PhaseTimer passes_timer(SPSYRK_PHASE_COLINDEX_PASSES, s);
         if (!trow1) tile_first_rows(rp, m, kRTile, trow, s);
         uint32_t* h1 = hist1 ? hist1 : hist;
-        run_pass<4, kSrcCsr>(reinterpret_cast<const uint32_t*>(col_idx), nullptr, nullptr, key_b, row_b, ent_b, n, L,
-                             (1u << width[0]) - 1u, h1, scan_tmp, s, rp, m, trow1 ? trow1 : trow, rowbits, lenbits,
-                             SlabIo(), hist1 != nullptr);
+        const uint32_t* ck = reinterpret_cast<const uint32_t*>(col_idx);
+        const int64_t* tr = trow1 ? trow1 : trow;
+        if (cv == 8)
+            run_pass<8, kSrcCsr>(ck, nullptr, pk->vals_b, key_b, row_b, ent_b, n, L, (1u << width[0]) - 1u, h1,
+                                 scan_tmp, s, rp, m, tr, rowbits, lenbits, SlabIo(), hist1 != nullptr);
+        else
+            run_pass<4, kSrcCsr>(ck, nullptr, cv == 4 ? pk->vals_b : nullptr, key_b, row_b, ent_b, n, L,
+                                 (1u << width[0]) - 1u, h1, scan_tmp, s, rp, m, tr, rowbits, lenbits, SlabIo(),
+                                 hist1 != nullptr);
         if (from_hist)
             digit_starts<<<1, kBlock, 0, s>>>(h1, ntiles, 1 << width[0], passes == 1 ? gstart : first1, n, big);
         int shift = L + width[0];
@@ -1090,7 +1121,10 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
             uint32_t* ro = cur ? row_a : row_b;
             uint32_t* vi = cur ? ent_b : ent_a;
             uint32_t* vo = cur ? ent_a : ent_b;
-            run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+            if (cv == 8)
+                run_pass<8>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
+            else
+                run_pass<4>(ki, ri, vi, ko, ro, vo, n, shift, mask, hist, scan_tmp, s);
             cur ^= 1;
         }
         if (from_hist && passes == 2)
@@ -1118,17 +1152,32 @@ int radix_sort_csr(const int32_t* col_idx, const int64_t* rp, int64_t m, int row
         const unsigned gb = unsigned(std::min<size_t>(groups, 1024));
         PhaseTimer pack_timer(SPSYRK_PHASE_COLINDEX_PACK, s);
         if (pk->jac) {
-            local_sort_pack<0, true><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
-            local_sort_pack_big<0, true><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+            local_sort_pack<0, true, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<0, true, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk,
+                                                                      big);
+        } else if (cv == 8) {
+            using V = ValT<8>::T;
+            V* vx = reinterpret_cast<V*>(ex);
+            V* vy = reinterpret_cast<V*>(ey);
+            local_sort_pack<8, false, true><<<g, kBlock, 0, s>>>(kx, rx, vx, gstart, gend, L, *pk, big);
+            local_sort_pack_big<8, false, true><<<gb, kBlock, 0, s>>>(kx, rx, vx, ky, ry, vy, gstart, gend, L, *pk,
+                                                                      big);
+        } else if (cv == 4) {
+            local_sort_pack<4, false, true><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<4, false, true><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk,
+                                                                      big);
         } else if (pk->vbytes == 8) {
-            local_sort_pack<8, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
-            local_sort_pack_big<8, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+            local_sort_pack<8, false, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<8, false, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk,
+                                                                       big);
         } else if (pk->vbytes == 4) {
-            local_sort_pack<4, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
-            local_sort_pack_big<4, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+            local_sort_pack<4, false, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<4, false, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk,
+                                                                       big);
         } else {
-            local_sort_pack<0, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
-            local_sort_pack_big<0, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk, big);
+            local_sort_pack<0, false, false><<<g, kBlock, 0, s>>>(kx, rx, ex, gstart, gend, L, *pk, big);
+            local_sort_pack_big<0, false, false><<<gb, kBlock, 0, s>>>(kx, rx, ex, ky, ry, ey, gstart, gend, L, *pk,
+                                                                       big);
         }
         return -1;
     }

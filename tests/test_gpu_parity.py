@@ -313,12 +313,13 @@ def test_local_sort_large_groups(dev, semiring, monkeypatch):
     run_lower(A, semiring, dev, "local sort, groups past the LDS capacity")
 
 
-@pytest.mark.parametrize("semiring", ["f64", "count", "jaccard"])
+@pytest.mark.parametrize("semiring", SEMIRINGS)
 def test_local_sort_group_size_limits(dev, semiring, monkeypatch):
     # 2^15 columns and under 16384 entries give 8 groups of 4096 columns
     # (high bits max(15 - 12, bit width of nnz / 2048) = 3), filled with
     # exactly 2048, 2049, 4096, 4097, 1, 0, 0 and 7 records: the limits of
-    # the first launch's LDS (2048), of the second's (4096), and tiny groups
+    # the first launch's LDS (2048), of the second's (4096), and tiny groups;
+    # off the diagonal the plus-times records carry their values
     monkeypatch.setenv("SPSYRK_LOCAL_SORT", "1")
     rng = np.random.default_rng(71)
     sizes = [2048, 2049, 4096, 4097, 1, 0, 0, 7]
