@@ -42,6 +42,16 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
+def build_sanitized(out_path: str) -> str:
+    """Compile the same source with AddressSanitizer and UndefinedBehaviorSanitizer
+    into ``out_path`` (host code only; the tests load it in a child process
+    with the ASan runtime preloaded and pass it as ``lib=`` to every entry point)."""
+    subprocess.check_call(["g++", "-O1", "-g", "-std=c++17", "-shared", "-fPIC", "-pthread",
+                           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                           "-fno-omit-frame-pointer", "-o", out_path, _SRC])
+    return out_path
+
+
 def _declare(lib):
     i64, i32p, i64p, vp = ctypes.c_int64, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int64), ctypes.c_void_p
     lib.oracle_syrk.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64p, i32p, vp,

@@ -344,6 +344,7 @@ void oracle_result_copy(const void* h, int64_t* row_ptr, int32_t* col, void* val
     const Result* R = static_cast<const Result*>(h);
     const size_t nnz = R->col.size();
     if (row_ptr) std::memcpy(row_ptr, R->row_ptr.data(), R->row_ptr.size() * sizeof(int64_t));
+    if (nnz == 0) return;  // an empty vector's data() may be null, and memcpy takes no null
     if (col) std::memcpy(col, R->col.data(), nnz * sizeof(int32_t));
     if (sum_abs) std::memcpy(sum_abs, R->sum_abs.data(), nnz * sizeof(double));
     if (count) std::memcpy(count, R->count.data(), nnz * sizeof(uint32_t));
