@@ -319,6 +319,21 @@ const char* spsyrk_status_string(spsyrk_status s);
 /* Detail of the last error on the calling thread ("" if none). */
 const char* spsyrk_last_error_detail(void);
 
+/* Invariant checks of the kernels (a debugging aid, not a passage of the paper).
+ * A build compiled with -DSPSYRK_DEBUG=1 (libspsyrk_debug.so) checks, inside its
+ * kernels, that every output slot written lies in its row's range of C and that
+ * the heavy rows' numeric pass fills exactly the columns its symbolic pass
+ * counted; a broken check sets a bit in a device word and the kernel goes on.
+ * spsyrk_debug_build returns 1 for that build, 0 for the ordinary one.
+ * spsyrk_debug_flags waits for the whole device (hipDeviceSynchronize), then
+ * writes the OR of the raised bits to *flags and clears them: 1 compaction
+ * destination outside C, 2 heavy output slot outside its row, 4 heavy column
+ * count differs from the symbolic count, 2^31 a word could not be read.  The
+ * ordinary build always writes 0.  SPSYRK_ERR_INVALID_ARG if flags is NULL,
+ * SPSYRK_ERR_HIP if the wait fails. */
+int spsyrk_debug_build(void);
+spsyrk_status spsyrk_debug_flags(uint32_t* flags);
+
 /* Counters from the last successful call on the calling thread. */
 typedef struct spsyrk_stats {
     int64_t nnz_out;          /* entries in the result */

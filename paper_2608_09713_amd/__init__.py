@@ -22,6 +22,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libspsyrk.so")
+# SPSYRK_DEBUG=1 in the environment loads the build with the kernels' invariant
+# checks (debug_flags() reads what they found); it must be set before the first call
+DEBUG_LIB_PATH = os.path.join(_HERE, "libspsyrk_debug.so")
 
 SEMIRINGS = {"f64": 0, "f32": 1, "count": 2, "jaccard": 3}
 # dtype of A's values each semiring reads, and of the output values
@@ -76,10 +79,15 @@ def library():
     global _lib
     with _lib_lock:
         if _lib is None:
-            if not os.path.exists(LIB_PATH):
-                raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2608_09713_amd.build` "
+            # torch's HIP runtime comes up first: a process that loaded this
+            # library before torch touched the device saw no device in it
+            import torch
+            torch.cuda.is_available()
+            path = DEBUG_LIB_PATH if os.environ.get("SPSYRK_DEBUG") == "1" else LIB_PATH
+            if not os.path.exists(path):
+                raise ImportError(f"{path} is missing: run `python -m paper_2608_09713_amd.build` "
                                   "(or __graft_entry__.build()) first")
-            lib = ctypes.CDLL(LIB_PATH)
+            lib = ctypes.CDLL(path)
             for name in ("spsyrk_lower", "spsyrk_offdiag", "spsyrk_offdiag_half", "spsyrk_mirror"):
                 getattr(lib, name).restype = ctypes.c_int
             lib.spsyrk_lower.argtypes = [ctypes.POINTER(_Csr), ctypes.c_int, ctypes.POINTER(_Allocator),
@@ -123,6 +131,10 @@ def library():
             lib.spsyrk_timing_begin_phases.restype = ctypes.c_int
             lib.spsyrk_timing_end.argtypes = [ctypes.POINTER(_PhaseTimes)]
             lib.spsyrk_timing_end.restype = ctypes.c_int
+            lib.spsyrk_debug_build.argtypes = []
+            lib.spsyrk_debug_build.restype = ctypes.c_int
+            lib.spsyrk_debug_flags.argtypes = [ctypes.POINTER(ctypes.c_uint32)]
+            lib.spsyrk_debug_flags.restype = ctypes.c_int
             _lib = lib
     return _lib
 
@@ -132,7 +144,23 @@ EXPORTS = ("spsyrk_lower", "spsyrk_lower_plan", "spsyrk_lower_execute", "spsyrk_
            "spsyrk_symm", "spsyrk_symm_noalloc",
            "spsyrk_status_string",
            "spsyrk_last_error_detail", "spsyrk_last_stats", "spsyrk_abi_version", "spsyrk_timing_begin",
-           "spsyrk_timing_begin_phases", "spsyrk_timing_end")
+           "spsyrk_timing_begin_phases", "spsyrk_timing_end", "spsyrk_debug_build", "spsyrk_debug_flags")
+
+
+def debug_build() -> bool:
+    """Whether the loaded library has the kernels' invariant checks compiled in."""
+    return bool(library().spsyrk_debug_build())
+
+
+def debug_flags() -> int:
+    """Waits for the device, then returns and clears the OR of the check bits
+    that the debug build's kernels raised (0 in the ordinary build)."""
+    lib = library()
+    f = ctypes.c_uint32(0)
+    rc = lib.spsyrk_debug_flags(ctypes.byref(f))
+    if rc != 0:
+        raise SpsyrkError(rc, lib.spsyrk_last_error_detail().decode())
+    return int(f.value)
 
 PHASES = ("validate", "colindex", "light_symbolic", "heavy_symbolic", "scan", "light_numeric", "heavy_numeric",
           "mirror_count", "mirror_copy", "mirror_transpose", "runs", "compact", "colindex_passes", "colindex_pack")

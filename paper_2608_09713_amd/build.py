@@ -13,6 +13,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libspsyrk.so")
+# the same sources with the kernels' invariant checks compiled in (SPSYRK_DEBUG)
+DEBUG_LIB = os.path.join(PKG, "libspsyrk_debug.so")
 ARCH = os.environ.get("SPSYRK_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [
@@ -28,15 +30,17 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, debug: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    flags = FLAGS + (["-DSPSYRK_DEBUG=1"] if debug else [])
+    target = DEBUG_LIB if debug else LIB
     objs = []
-    tmpdir = os.path.join(PKG, "_build")
+    tmpdir = os.path.join(PKG, "_build", "debug") if debug else os.path.join(PKG, "_build")
     os.makedirs(tmpdir, exist_ok=True)
     procs = []
     for src in sources():
         obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
-        cmd = [hipcc, *[f for f in FLAGS if f != "-shared"], "-c", src, "-o", obj]
+        cmd = [hipcc, *[f for f in flags if f != "-shared"], "-c", src, "-o", obj]
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
         objs.append(obj)
     failed = []
@@ -51,10 +55,10 @@ def build(verbose: bool = False) -> str:
         for src, text in failed:
             sys.stderr.write(f"--- {src}\n{text}\n")
         raise RuntimeError("hipcc failed for " + ", ".join(os.path.basename(s) for s, _ in failed))
-    tmp = LIB + f".tmp{os.getpid()}"
-    subprocess.check_call([hipcc, *FLAGS, *objs, "-o", tmp])
-    os.replace(tmp, LIB)
-    return LIB
+    tmp = target + f".tmp{os.getpid()}"
+    subprocess.check_call([hipcc, *flags, *objs, "-o", tmp])
+    os.replace(tmp, target)
+    return target
 
 
 if __name__ == "__main__":

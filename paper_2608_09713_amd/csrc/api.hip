@@ -1410,6 +1410,17 @@ struct spsyrk_plan_s {
     std::vector<void*> bufs;  // device buffers owned by the plan
 };
 
+namespace spsyrk {
+namespace dbg {
+// the debug build's per-unit readers, filled by static initialisers at load
+std::vector<Reader>& readers() {
+    static std::vector<Reader> v;
+    return v;
+}
+void add_reader(Reader r) { readers().push_back(r); }
+}  // namespace dbg
+}  // namespace spsyrk
+
 extern "C" {
 
 spsyrk_status spsyrk_lower(const spsyrk_csr* A, spsyrk_semiring sr, const spsyrk_allocator* al, void* hip_stream,
@@ -1747,6 +1758,31 @@ const char* spsyrk_status_string(spsyrk_status s) {
 }
 
 const char* spsyrk_last_error_detail(void) { return g_detail.c_str(); }
+
+int spsyrk_debug_build(void) {
+#if defined(SPSYRK_DEBUG) && SPSYRK_DEBUG
+    return 1;
+#else
+    return 0;
+#endif
+}
+
+spsyrk_status spsyrk_debug_flags(uint32_t* flags) {
+    if (!flags) {
+        set_detail("spsyrk_debug_flags: flags is NULL");
+        return SPSYRK_ERR_INVALID_ARG;
+    }
+    *flags = 0;
+    const hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        set_detail("hipDeviceSynchronize: %s", hipGetErrorString(e));
+        return SPSYRK_ERR_HIP;
+    }
+    uint32_t f = 0;
+    for (spsyrk::dbg::Reader r : spsyrk::dbg::readers()) f |= r();
+    *flags = f;
+    return SPSYRK_OK;
+}
 
 spsyrk_status spsyrk_last_stats(spsyrk_stats* out) {
     if (!out) return SPSYRK_ERR_INVALID_ARG;

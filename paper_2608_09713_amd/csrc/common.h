@@ -20,6 +20,43 @@ enum ErrBits : uint32_t {
     kErrUpper = 8u,         // entry above the diagonal (mirror input)
 };
 
+// Debug checks, compiled only with -DSPSYRK_DEBUG=1.  A kernel that finds one
+// of its invariants broken ORs the check's bit into a device word of its
+// translation unit and goes on (no trap, so a broken check cannot take the
+// device down); spsyrk_debug_flags() collects and clears every unit's word.
+enum DbgBits : uint32_t {
+    kDbgCompactOut = 1u,     // compaction: destination outside [0, nnz(C))
+    kDbgHeavyOut = 2u,       // heavy rows: an output slot outside the row's range of C
+    kDbgHeavyCount = 4u,     // heavy rows: the numeric pass found more columns than the symbolic pass
+    kDbgReadFailed = 1u << 31,  // the host could not read a unit's word
+};
+namespace dbg {
+using Reader = uint32_t (*)();
+void add_reader(Reader r);  // registers a unit's reader (api.hip)
+#if defined(SPSYRK_DEBUG) && SPSYRK_DEBUG
+static __device__ unsigned word;
+static uint32_t read_and_clear() {
+    void* p = nullptr;
+    uint32_t v = 0, z = 0;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(word)) != hipSuccess) return kDbgReadFailed;
+    if (hipMemcpy(&v, p, sizeof v, hipMemcpyDeviceToHost) != hipSuccess) return kDbgReadFailed;
+    if (hipMemcpy(p, &z, sizeof z, hipMemcpyHostToDevice) != hipSuccess) return kDbgReadFailed;
+    return v;
+}
+[[maybe_unused]] static const bool registered = (add_reader(&read_and_clear), true);
+#endif
+}  // namespace dbg
+#if defined(SPSYRK_DEBUG) && SPSYRK_DEBUG
+#define SPSYRK_CHECK(cond, bit) \
+    do {                        \
+        if (!(cond)) atomicOr(&::spsyrk::dbg::word, uint32_t(bit)); \
+    } while (0)
+#else
+#define SPSYRK_CHECK(cond, bit) \
+    do {                        \
+    } while (0)
+#endif
+
 // number of bits needed to write x (0 -> 0)
 __host__ __device__ inline int bit_width_u64(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
 

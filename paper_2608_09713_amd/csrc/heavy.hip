@@ -297,6 +297,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
                     while (b) {
                         const int t = __ffs(b) - 1;
                         b &= b - 1;
+                        SPSYRK_CHECK(outp + off < a.c_rp[i + 1], kDbgHeavyOut);
                         a.c_ci[outp + off] = int32_t(B0 + 32 * x + t);
                         ++off;
                     }
@@ -315,6 +316,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
                         walk(c0, min(e1, c0 + int64_t(kChunkE)), B0, B1, true, T0, tl, true);
                     for (uint32_t x = tid; x < tl; x += kHB) {
                         const int64_t p = outp + T0 + x;
+                        SPSYRK_CHECK(p < a.c_rp[i + 1], kDbgHeavyOut);
                         Out ov;
                         if constexpr (kVal) {
                             ov = Out(acc[x]);
@@ -330,6 +332,9 @@ void heavy_kernel(HeavyArgs a, int* queue) {
                 }
                 outp += Nw;
             }
+        }
+        if constexpr (NUM) {
+            if (tid == 0) SPSYRK_CHECK(outp + (LOWER ? 1 : 0) == a.c_rp[i + 1], kDbgHeavyCount);
         }
         // diagonal (lower triangle only; a heavy row is never empty)
         if constexpr (!NUM) {
@@ -359,6 +364,7 @@ void heavy_kernel(HeavyArgs a, int* queue) {
                 dv = jaccard(int32_t(E), E, E);
             }
             if (tid == 0) {
+                SPSYRK_CHECK(outp < a.c_rp[i + 1], kDbgHeavyOut);
                 a.c_ci[outp] = i;
                 static_cast<Out*>(a.c_val)[outp] = dv;
             }

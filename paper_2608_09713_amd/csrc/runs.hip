@@ -286,6 +286,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
                 const int x = (b * kBatch + q) * kBlock + threadIdx.x;
                 if (live[q]) {
                     const int64_t p = s0 + x + wdel[rowof[x]];
+                    SPSYRK_CHECK(p >= 0 && p < c_rp[m], kDbgCompactOut);
                     if constexpr (PK != 0) {
                         unpack_store<PK>(un, uint32_t(cv[q]), PK == 2 ? int64_t(wlen[rowof[x]]) : 0, p, c_ci, c_val);
                     } else {
@@ -312,6 +313,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(int64_t m, int64_t stag
         }
         if (sl >= end) continue;
         const int64_t p = sl + del;
+        SPSYRK_CHECK(p >= 0 && p < c_rp[m], kDbgCompactOut);
         if constexpr (PK != 0) {
             unpack_store<PK>(un, uint32_t(s_ci[sl]), len_i, p, c_ci, c_val);
             continue;

@@ -128,3 +128,18 @@ def test_binding_refuses_to_run_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(sp, "_lib", None)
     with pytest.raises(ImportError):
         sp.library()
+
+
+def test_debug_build_exports_and_reports_itself(lib):
+    """The build with the kernels' invariant checks exports the same symbols and
+    says so; the ordinary build says it has none and reports no bits."""
+    if not os.path.exists(sp.DEBUG_LIB_PATH):
+        from paper_2608_09713_amd import build
+        build.build(debug=True)
+    out = subprocess.check_output(["nm", "-D", "--defined-only", sp.DEBUG_LIB_PATH]).decode()
+    exported = set(re.findall(r"\bT (spsyrk_\w+)", out))
+    assert not [f for f in declared_functions() if f not in exported]
+    dbg = ctypes.CDLL(sp.DEBUG_LIB_PATH)
+    assert dbg.spsyrk_debug_build() == 1
+    assert lib.spsyrk_debug_build() == 0
+    assert lib.spsyrk_debug_flags(None) == 1  # SPSYRK_ERR_INVALID_ARG, before any device call
